@@ -1,0 +1,399 @@
+"""Plain fp64 CPU oracle of the Pruned CTC head and loss (forward and backward).
+
+TEST INFRASTRUCTURE ONLY: used by tests/, the build entry point's smoke check
+and the benchmark's CPU-baseline leg; never by the product path.
+
+What it computes, with the passage each step follows:
+
+* Union subset and relabelling (Sec. 3.2 "Reformulation"; Algorithm 1, union and
+  relabel steps; App. B.1 "Forward computation"): the selected classes are blank
+  followed by the sorted distinct target labels of the whole batch; each target
+  is relabelled by its index in that list.
+* Full-vocabulary normaliser lambda_m = log sum_v exp Z_{m,v} with Z = H W^T
+  (Eq. "lognorm"), accumulated over vocabulary chunks as Algorithm 1's online
+  log-sum-exp does.
+* Standard CTC over the extended label sequence (Sec. 3.1, Eq. "ctc"):
+  alignments are the length-T label strings that collapse to y (merge repeats,
+  then drop blanks).  The recursion over the 2U+1 extended states is the
+  textbook one of Graves et al. (2006), in log space.
+* Finite-beam pruning (Sec. 3.3, App. B.3 "Alignment pruning"): every trellis
+  arc is scored by the best alignment through it; arcs scoring below the best
+  alignment minus beta are dropped, and the loss sums over the alignments whose
+  arcs are all kept (Eq. "pruned-ctc").
+* Loss aggregation (App. B.1 "Loss aggregation"): an utterance is structurally
+  alignable iff T_n >= U_n + r_n (r_n = adjacent identical label pairs);
+  excluded or nonfinite utterances contribute zero loss and zero gradient.
+* Gradient dL/dZ_{m,v} = p_v(m) - gamma_v(m) (Eq. "grad-full"; for a pruned
+  lattice held fixed, gamma is the occupancy over retained alignments, Sec. 3.3),
+  and the head gradients dX = dZ W, dW = dZ^T X (App. A, end of Step 3).
+
+Everything is float64.  Inputs are taken exactly as the device sees them (bf16
+values are exact in float32, and float32 is exact in float64).
+"""
+from __future__ import annotations
+
+import math
+from typing import Dict, List, Optional, Sequence
+
+import numpy as np
+
+# Status codes shared in meaning (not in code) with the C ABI.
+PCTC_OK = 0
+PCTC_EINVAL = -1
+PCTC_ELABEL = -2
+PCTC_ELENGTH = -3
+
+STATUS_OK = 0
+STATUS_NOT_ALIGNABLE = 1
+STATUS_NONFINITE = 2
+
+# Slack (nats) added to the beam threshold so that the best alignment is never lost
+# to rounding when beta is 0 (reading of App. B.3; the paper states no tie rule).
+KEEP_SLACK = 1e-3
+
+
+class OracleError(ValueError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(msg)
+        self.code = code
+
+
+def beam_enabled(beam: float) -> bool:
+    """A finite, non-negative beam prunes; +inf or a negative value keeps all alignments."""
+    return bool(np.isfinite(beam) and beam >= 0.0)
+
+
+def validate(N: int, input_lengths, target_lengths, targets, D: int, V: int, blank: int,
+             beam: float) -> None:
+    """Argument checks in the order the C ABI applies them."""
+    if N < 0 or D <= 0 or V <= 1 or not (0 <= blank < V) or math.isnan(beam):
+        raise OracleError(PCTC_EINVAL, "bad sizes, blank or beam")
+    T = np.asarray(input_lengths)
+    U = np.asarray(target_lengths)
+    if T.shape[0] != N or U.shape[0] != N:
+        raise OracleError(PCTC_EINVAL, "length arrays do not have N entries")
+    if (T <= 0).any() or (U < 0).any():
+        raise OracleError(PCTC_ELENGTH, "T_n must be >= 1 and U_n >= 0")
+    y = np.asarray(targets)
+    if y.shape[0] != int(U.sum()):
+        raise OracleError(PCTC_EINVAL, "targets length differs from sum of target lengths")
+    if y.size and ((y < 0).any() or (y >= V).any() or (y == blank).any()):
+        raise OracleError(PCTC_ELABEL, "label out of range or equal to blank")
+
+
+# ---------------------------------------------------------------------------------------
+# Union subset, remap, relabelled targets (Sec. 3.2; Algorithm 1; App. B.1)
+# ---------------------------------------------------------------------------------------
+
+def union_remap(targets, target_lengths, blank: int, V: int) -> Dict[str, np.ndarray]:
+    """U = [blank] + sorted(distinct labels); remap[v] = index of v in U or -1; y_rel = remap[y]."""
+    distinct = sorted(set(int(v) for v in np.asarray(targets).tolist()))
+    u_ids = [int(blank)] + distinct
+    remap = np.full(V, -1, dtype=np.int64)
+    for j, v in enumerate(u_ids):
+        remap[v] = j
+    y = np.asarray(targets, dtype=np.int64)
+    y_rel = remap[y] if y.size else np.zeros(0, np.int64)
+    return {"u_ids": np.array(u_ids, np.int64), "remap": remap, "y_rel": y_rel,
+            "K": len(u_ids)}
+
+
+# ---------------------------------------------------------------------------------------
+# Normaliser and selected log-probabilities (Eq. lognorm; Algorithm 1)
+# ---------------------------------------------------------------------------------------
+
+def log_normalizer(H, W, chunk: int = 4096) -> np.ndarray:
+    """lambda_m = log sum_v exp(Z_{m,v}), Z = H W^T, combined online over vocabulary chunks."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    M = H.shape[0]
+    run_max = np.full(M, -np.inf)
+    run_sum = np.zeros(M)
+    for v0 in range(0, W.shape[0], chunk):
+        Z = H @ W[v0:v0 + chunk].T
+        cmax = Z.max(axis=1)
+        new_max = np.maximum(run_max, cmax)
+        safe = np.where(np.isfinite(new_max), new_max, 0.0)
+        with np.errstate(invalid="ignore"):
+            run_sum = run_sum * np.exp(run_max - safe) + np.exp(Z - safe[:, None]).sum(axis=1)
+        run_max = new_max
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(np.isfinite(run_max), run_max + np.log(run_sum), run_max)
+
+
+def selected_logprobs(H, W, u_ids, lam) -> np.ndarray:
+    """S = X W_U^T - lambda 1^T: the log-probabilities of the selected classes (Algorithm 1)."""
+    H = np.asarray(H, np.float64)
+    Wu = np.asarray(W, np.float64)[np.asarray(u_ids)]
+    return H @ Wu.T - np.asarray(lam, np.float64)[:, None]
+
+
+# ---------------------------------------------------------------------------------------
+# CTC over the extended label sequence, optionally beam-pruned (Sec. 3.1, 3.3; App. B.3)
+# ---------------------------------------------------------------------------------------
+
+def extended_labels(y: Sequence[int], blank_col: int):
+    """l' = (blank, y_1, blank, ..., y_U, blank) and, per state, whether the skip arc
+    s-2 -> s exists (l'_s is a label different from l'_{s-2})."""
+    y = [int(v) for v in y]
+    ext = [blank_col]
+    for v in y:
+        ext += [v, blank_col]
+    S = len(ext)
+    skip_ok = np.zeros(S, bool)
+    for s in range(2, S):
+        skip_ok[s] = (ext[s] != blank_col) and (ext[s] != ext[s - 2])
+    return np.array(ext, np.int64), skip_ok
+
+
+def _combine(op: str, *xs: np.ndarray) -> np.ndarray:
+    """Elementwise max (Viterbi) or log-sum-exp (total probability) with -inf handled."""
+    m = xs[0]
+    for x in xs[1:]:
+        m = np.maximum(m, x)
+    if op == "max":
+        return m
+    fin = np.isfinite(m)
+    safe = np.where(fin, m, 0.0)
+    acc = np.zeros_like(m)
+    for x in xs:
+        with np.errstate(invalid="ignore"):
+            acc = acc + np.exp(x - safe)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        return np.where(fin, safe + np.log(acc), m)
+
+
+def _shift_right(a: np.ndarray, k: int) -> np.ndarray:
+    out = np.full_like(a, -np.inf)
+    if k < a.shape[-1]:
+        out[..., k:] = a[..., :a.shape[-1] - k]
+    return out
+
+
+def _shift_left(a: np.ndarray, k: int, fill) -> np.ndarray:
+    out = np.full_like(a, fill)
+    if k < a.shape[-1]:
+        out[..., :a.shape[-1] - k] = a[..., k:]
+    return out
+
+
+def _recursions(E: np.ndarray, skip_ok: np.ndarray, keep: Dict[str, np.ndarray], op: str):
+    """Forward and backward recursions over the trellis with per-arc keep flags.
+
+    E[t, s] is the log-probability of extended state s at frame t (0-based t).
+    alpha[t, s]: combined score of partial alignments ending in s at t, including E[t, s].
+    beta[t, s]: combined score of continuations from (t, s) to the end, excluding E[t, s].
+    Arcs: start -> (0, s); (t-1, s) -> (t, s) "stay"; (t-1, s-1) -> (t, s) "step";
+    (t-1, s-2) -> (t, s) "skip" (only where skip_ok); (T-1, s) -> end "final".
+    """
+    T, S = E.shape
+    NEG = -np.inf
+    alpha = np.full((T, S), NEG)
+    beta = np.full((T, S), NEG)
+    alpha[0] = np.where(keep["start"], E[0], NEG)
+    for t in range(1, T):
+        a = alpha[t - 1]
+        stay = np.where(keep["stay"][t], a, NEG)
+        step = np.where(keep["step"][t], _shift_right(a, 1), NEG)
+        skip = np.where(keep["skip"][t] & skip_ok, _shift_right(a, 2), NEG)
+        alpha[t] = E[t] + _combine(op, stay, step, skip)
+    beta[T - 1] = np.where(keep["final"], 0.0, NEG)
+    for t in range(T - 2, -1, -1):
+        nxt = E[t + 1] + beta[t + 1]
+        stay = np.where(keep["stay"][t + 1], nxt, NEG)
+        step = np.where(_shift_left(keep["step"][t + 1], 1, False), _shift_left(nxt, 1, NEG), NEG)
+        skip_arc = _shift_left(keep["skip"][t + 1] & skip_ok, 2, False)
+        skip = np.where(skip_arc, _shift_left(nxt, 2, NEG), NEG)
+        beta[t] = _combine(op, stay, step, skip)
+    final_scores = np.where(keep["final"], alpha[T - 1], NEG)
+    total = _combine(op, *[final_scores[s:s + 1] for s in range(S)])[0]
+    return alpha, beta, total
+
+
+def _all_arcs(T: int, S: int) -> Dict[str, np.ndarray]:
+    start = np.zeros(S, bool)
+    start[0] = True
+    if S > 1:
+        start[1] = True
+    final = np.zeros(S, bool)
+    final[S - 1] = True
+    if S > 1:
+        final[S - 2] = True
+    stay = np.ones((T, S), bool)
+    step = np.ones((T, S), bool)
+    step[:, 0] = False
+    skip = np.ones((T, S), bool)
+    skip[:, :2] = False
+    return {"start": start, "final": final, "stay": stay, "step": step, "skip": skip}
+
+
+def ctc_utterance(logp: np.ndarray, y: Sequence[int], blank_col: int, beam: float = math.inf,
+                  slack: float = KEEP_SLACK) -> Dict[str, object]:
+    """CTC (or beam-pruned CTC) for one utterance.
+
+    logp: [T, C] log-probabilities over some column space; y: labels in that space;
+    blank_col: the blank's column.  Returns log P (log of the retained alignment sum),
+    per-state occupancies gamma [T, 2U+1], the extended labels, the arc keep flags and,
+    when pruning, the signed margin of every arc's decision.
+    """
+    logp = np.asarray(logp, np.float64)
+    T = logp.shape[0]
+    ext, skip_ok = extended_labels(y, blank_col)
+    S = ext.size
+    U = len(y)
+    r = sum(1 for i in range(1, U) if y[i] == y[i - 1])
+    out: Dict[str, object] = {"ext": ext, "skip_ok": skip_ok, "alignable": T >= U + r}
+    E = logp[:, ext]
+    keep = _all_arcs(T, S)
+    margins = None
+    if beam_enabled(beam):
+        va, vb, vbest = _recursions(E, skip_ok, keep, "max")
+        thr = vbest - beam - slack
+        margins = {}
+        with np.errstate(invalid="ignore"):
+            margins["start"] = np.where(keep["start"], E[0] + vb[0] - thr, -np.inf)
+            margins["final"] = np.where(keep["final"], va[T - 1] - thr, -np.inf)
+            through_in = E[1:] + vb[1:]
+            margins["stay"] = np.full((T, S), -np.inf)
+            margins["step"] = np.full((T, S), -np.inf)
+            margins["skip"] = np.full((T, S), -np.inf)
+            if T > 1:
+                margins["stay"][1:] = va[:-1] + through_in - thr
+                margins["step"][1:] = _shift_right(va[:-1], 1) + through_in - thr
+                margins["skip"][1:] = np.where(skip_ok, _shift_right(va[:-1], 2) + through_in - thr,
+                                               -np.inf)
+        keep = {k: keep[k] & (margins[k] >= 0.0) for k in keep}
+        out["viterbi_best"] = vbest
+    alpha, beta, logP = _recursions(E, skip_ok, keep, "lse")
+    with np.errstate(invalid="ignore", over="ignore"):
+        gamma = np.exp(alpha + beta - logP) if np.isfinite(logP) else np.zeros((T, S))
+    out.update({"logP": logP, "alpha": alpha, "beta": beta, "gamma": gamma, "keep": keep,
+                "margins": margins})
+    return out
+
+
+def _offsets(lengths) -> np.ndarray:
+    lengths = np.asarray(lengths, np.int64)
+    off = np.zeros(lengths.size + 1, np.int64)
+    off[1:] = np.cumsum(lengths)
+    return off
+
+
+def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: float = math.inf,
+                    slack: float = KEEP_SLACK) -> Dict[str, object]:
+    """The alignment stage alone: given per-frame scores S [M, K] over the selected classes
+    (blank = column 0) and relabelled targets, return per-utterance losses, statuses, the
+    occupancy-derived G = dL/dS (G[m, j] = -gamma over the states labelled j; zero for
+    excluded utterances, Algorithm 1 output) and its row sums g."""
+    S = np.asarray(S, np.float64)
+    M, K = S.shape
+    toff = _offsets(input_lengths)
+    yoff = _offsets(target_lengths)
+    N = len(input_lengths)
+    loss_n = np.zeros(N)
+    status = np.zeros(N, np.int64)
+    G = np.zeros((M, K))
+    per_utt: List[Dict[str, object]] = []
+    for n in range(N):
+        rows = slice(int(toff[n]), int(toff[n + 1]))
+        y = [int(v) for v in np.asarray(y_rel)[yoff[n]:yoff[n + 1]]]
+        res = ctc_utterance(S[rows], y, 0, beam, slack)
+        per_utt.append(res)
+        if not res["alignable"]:
+            status[n] = STATUS_NOT_ALIGNABLE
+            continue
+        if not np.isfinite(res["logP"]):
+            status[n] = STATUS_NONFINITE
+            continue
+        loss_n[n] = -res["logP"]
+        gam = res["gamma"]
+        ext = res["ext"]
+        for s in range(ext.size):
+            G[rows, ext[s]] -= gam[:, s]
+    g = G.sum(axis=1)
+    return {"loss_n": loss_n, "status": status, "G": G, "g": g, "per_utt": per_utt,
+            "loss": float(loss_n.sum())}
+
+
+# ---------------------------------------------------------------------------------------
+# Whole path: loss and head gradients by the full-vocabulary definition
+# ---------------------------------------------------------------------------------------
+
+def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: float = math.inf,
+            chunk: int = 4096, want_grads: bool = True, slack: float = KEEP_SLACK) -> Dict[str, object]:
+    """Loss and gradients of (beam-pruned) CTC on log-softmax(H W^T) over the full vocabulary.
+
+    Returns loss (sum of finite per-utterance losses over alignable utterances), loss_n,
+    status, dH [M, D], dW [V, D] and the stages u_ids, remap, y_rel, lam, S, G, g.
+    """
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    M, D = H.shape
+    V = W.shape[0]
+    targets = np.asarray(targets, np.int64)
+    N = len(input_lengths)
+    validate(N, input_lengths, target_lengths, targets, D, V, blank, beam)
+    if int(np.sum(input_lengths)) != M:
+        raise OracleError(PCTC_EINVAL, "H rows differ from the sum of input lengths")
+    un = union_remap(targets, target_lengths, blank, V)
+    lam = log_normalizer(H, W, chunk)
+    Ssel = selected_logprobs(H, W, un["u_ids"], lam)
+    toff = _offsets(input_lengths)
+    yoff = _offsets(target_lengths)
+    loss_n = np.zeros(N)
+    status = np.zeros(N, np.int64)
+    included = np.zeros(M, bool)
+    gamma_cols: List[np.ndarray] = []   # per utterance: the full-vocabulary ids of its states
+    gamma_vals: List[np.ndarray] = []
+    per_utt = []
+    for n in range(N):
+        rows = slice(int(toff[n]), int(toff[n + 1]))
+        y = [int(v) for v in targets[yoff[n]:yoff[n + 1]]]
+        # log p_v(m) on the columns this utterance's alignments can use (Eq. lognorm)
+        cols = np.array([blank] + sorted(set(y)), np.int64)
+        logp_cols = H[rows] @ W[cols].T - lam[rows, None]
+        col_of = {int(v): i for i, v in enumerate(cols)}
+        res = ctc_utterance(logp_cols, [col_of[v] for v in y], 0, beam, slack)
+        res["cols"] = cols
+        per_utt.append(res)
+        if not res["alignable"]:
+            status[n] = STATUS_NOT_ALIGNABLE
+        elif not np.isfinite(res["logP"]):
+            status[n] = STATUS_NONFINITE
+        else:
+            loss_n[n] = -res["logP"]
+            included[rows] = True
+    # G over the selected classes (the alignment stage's output) and its row sums
+    G = np.zeros((M, un["K"]))
+    for n in range(N):
+        if status[n] != STATUS_OK:
+            continue
+        rows = slice(int(toff[n]), int(toff[n + 1]))
+        res = per_utt[n]
+        ext_ids = res["cols"][res["ext"]]
+        for s in range(ext_ids.size):
+            G[rows, un["remap"][ext_ids[s]]] -= res["gamma"][:, s]
+    out = {"loss": float(loss_n.sum()), "loss_n": loss_n, "status": status,
+           "u_ids": un["u_ids"], "remap": un["remap"], "y_rel": un["y_rel"], "K": un["K"],
+           "lam": lam, "S": Ssel, "G": G, "g": G.sum(axis=1), "per_utt": per_utt,
+           "included": included}
+    if not want_grads:
+        return out
+    # dZ = p - gamma (Eq. grad-full), dense over V, one chunk at a time; zero on excluded frames.
+    dH = np.zeros((M, D))
+    dW = np.zeros((V, D))
+    inc = included
+    for v0 in range(0, V, chunk):
+        v1 = min(V, v0 + chunk)
+        Z = H[inc] @ W[v0:v1].T
+        dZ = np.exp(Z - lam[inc, None])
+        # subtract the occupancies gamma_v(m) for v in this chunk
+        Ginc = G[inc]
+        for j, v in enumerate(un["u_ids"]):
+            if v0 <= v < v1:
+                dZ[:, v - v0] += Ginc[:, j]
+        dH[inc] += dZ @ W[v0:v1]
+        dW[v0:v1] = dZ.T @ H[inc]
+    out["dH"] = dH
+    out["dW"] = dW
+    return out

@@ -1,0 +1,400 @@
+"""Pins for the CPU oracle: each check ties it to something other than itself.
+
+* brute-force enumeration of alignments (collapse map of Sec. 3.1);
+* closed forms (uniform logits, empty target, unique alignment);
+* PyTorch's CPU CTC loss in float64, a library routine for the unpruned case;
+* central finite differences of the loss for dH and dW (App. A, Step 3);
+* Proposition 1: CTC on the grouped logits R (Eq. "grouped") equals full CTC;
+* invariants: occupancies sum to one per frame (App. A, Step 3), dZ rows sum to
+  zero, L_beta >= L and |gamma_beta - gamma| <= delta (App. B.3).
+"""
+import math
+
+import numpy as np
+import pytest
+
+import oracle
+from oracle import prunedctc_oracle as O
+from tests import brute
+
+
+def _logsoftmax(z):
+    z = np.asarray(z, np.float64)
+    m = z.max(axis=-1, keepdims=True)
+    return z - (m + np.log(np.exp(z - m).sum(axis=-1, keepdims=True)))
+
+
+# ---------------------------------------------------------------------------------------
+# union / remap
+# ---------------------------------------------------------------------------------------
+
+def test_union_remap_by_hand():
+    # targets of two utterances: [7, 3, 7] and [2, 9]; blank = 5
+    u = oracle.union_remap(np.array([7, 3, 7, 2, 9]), np.array([3, 2]), blank=5, V=10)
+    assert u["u_ids"].tolist() == [5, 2, 3, 7, 9]
+    assert u["K"] == 5
+    assert u["remap"].tolist() == [-1, -1, 1, 2, -1, 0, -1, 3, -1, 4]
+    assert u["y_rel"].tolist() == [3, 2, 3, 1, 4]
+
+
+def test_union_remap_empty_targets():
+    u = oracle.union_remap(np.zeros(0, np.int64), np.array([0, 0]), blank=0, V=4)
+    assert u["u_ids"].tolist() == [0] and u["K"] == 1
+    assert u["remap"].tolist() == [0, -1, -1, -1]
+
+
+# ---------------------------------------------------------------------------------------
+# normaliser
+# ---------------------------------------------------------------------------------------
+
+def test_lambda_closed_form_zero_head():
+    H = np.random.default_rng(1).standard_normal((5, 3))
+    W = np.zeros((17, 3))
+    np.testing.assert_allclose(oracle.log_normalizer(H, W, chunk=4), np.log(17.0), rtol=0, atol=1e-14)
+
+
+def test_lambda_shift_invariance_and_mpmath():
+    import mpmath
+    rng = np.random.default_rng(2)
+    H = rng.standard_normal((4, 6))
+    W = rng.standard_normal((23, 6)) * 3
+    lam = oracle.log_normalizer(H, W, chunk=5)
+    # adding a constant feature shifts every logit by c -> lambda shifts by c
+    c = 7.25
+    H2 = np.concatenate([H, np.ones((4, 1))], axis=1)
+    W2 = np.concatenate([W, np.full((23, 1), c)], axis=1)
+    np.testing.assert_allclose(oracle.log_normalizer(H2, W2, chunk=3), lam + c, rtol=0, atol=1e-12)
+    mpmath.mp.dps = 40
+    Z = H @ W.T
+    for m in range(4):
+        ref = mpmath.log(mpmath.fsum(mpmath.exp(mpmath.mpf(float(z))) for z in Z[m]))
+        assert abs(float(ref) - lam[m]) < 1e-12
+
+
+# ---------------------------------------------------------------------------------------
+# unpruned CTC against enumeration and closed forms
+# ---------------------------------------------------------------------------------------
+
+CASES = [
+    # (T, C, y, blank)
+    (1, 3, [], 0), (1, 3, [2], 0), (3, 3, [1, 2], 0), (4, 3, [1, 1], 0),
+    (5, 4, [1, 2, 1], 0), (6, 3, [2, 2], 0), (5, 4, [3, 1], 2), (6, 4, [0, 0, 1], 3),
+    (4, 3, [1, 1], 0), (3, 3, [1, 1], 0), (2, 3, [1, 1], 0), (6, 4, [], 1), (7, 3, [1, 2, 2], 0),
+]
+
+
+@pytest.mark.parametrize("T,C,y,blank", CASES)
+def test_ctc_matches_enumeration(T, C, y, blank):
+    rng = np.random.default_rng(T * 100 + C * 10 + len(y))
+    logp = _logsoftmax(rng.standard_normal((T, C)) * 2.0)
+    ref = brute.brute_ctc(logp, y, blank)
+    res = oracle.ctc_utterance(logp, y, blank)
+    r = sum(1 for i in range(1, len(y)) if y[i] == y[i - 1])
+    assert res["alignable"] == (T >= len(y) + r) == (ref["n_align"] > 0)
+    if ref["n_align"] == 0:
+        assert res["logP"] == -math.inf
+        return
+    assert abs(res["logP"] - ref["logP"]) < 1e-12
+    gam = np.zeros((T, C))
+    for s, c in enumerate(res["ext"]):
+        gam[:, c] += res["gamma"][:, s]
+    np.testing.assert_allclose(gam, ref["gamma"], rtol=0, atol=1e-12)
+    np.testing.assert_allclose(gam.sum(axis=1), 1.0, rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("T,U,r", [(30, 8, 0), (30, 8, 3), (25, 1, 0), (11, 6, 5), (40, 0, 0), (9, 5, 4)])
+def test_uniform_logits_closed_form(T, U, r):
+    # With W = 0 every class has p = 1/V, and the count of alignments of U labels with r
+    # adjacent repeats into T frames is C(T+U-r, 2U) (2U+1 segments, U+r of them non-empty).
+    V = 11
+    y = []
+    for i in range(U):
+        y.append(1 if i == 0 else (y[-1] if i <= r else (y[-1] % (V - 1)) + 1))
+    assert sum(1 for i in range(1, U) if y[i] == y[i - 1]) == r
+    H = np.ones((T, 2))
+    W = np.zeros((V, 2))
+    out = oracle.fwd_bwd(H, W, np.array(y), np.array([T]), np.array([U]), blank=0, want_grads=False)
+    expect = T * math.log(V) - math.log(math.comb(T + U - r, 2 * U))
+    assert abs(out["loss"] - expect) < 1e-9 * max(1.0, expect)
+
+
+def test_empty_target_closed_form():
+    rng = np.random.default_rng(3)
+    H = rng.standard_normal((9, 4))
+    W = rng.standard_normal((13, 4))
+    blank = 6
+    out = oracle.fwd_bwd(H, W, np.zeros(0, np.int64), np.array([9]), np.array([0]), blank=blank)
+    logp = _logsoftmax(H @ W.T)
+    assert abs(out["loss"] - (-logp[:, blank].sum())) < 1e-11
+    # single alignment: gamma is one-hot on blank, so dZ = p - e_blank
+    p = np.exp(logp)
+    dZ = p.copy()
+    dZ[:, blank] -= 1.0
+    np.testing.assert_allclose(out["dH"], dZ @ W, atol=1e-12)
+    np.testing.assert_allclose(out["dW"], dZ.T @ H, atol=1e-12)
+
+
+def test_unique_alignment_closed_form():
+    # T = U + r: exactly one alignment, labels with a blank between the repeats
+    y = [4, 4, 2, 7, 7]
+    path = [4, 0, 4, 2, 7, 0, 7]
+    rng = np.random.default_rng(4)
+    H = rng.standard_normal((7, 5))
+    W = rng.standard_normal((9, 5))
+    out = oracle.fwd_bwd(H, W, np.array(y), np.array([7]), np.array([5]), blank=0)
+    logp = _logsoftmax(H @ W.T)
+    assert abs(out["loss"] + sum(logp[t, c] for t, c in enumerate(path))) < 1e-11
+    dZ = np.exp(logp)
+    for t, c in enumerate(path):
+        dZ[t, c] -= 1.0
+    np.testing.assert_allclose(out["dH"], dZ @ W, atol=1e-12)
+
+
+# ---------------------------------------------------------------------------------------
+# library cross-check: PyTorch CPU CTC in float64
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,blank", [(0, 0), (1, 0), (2, 13), (3, 49)])
+def test_against_torch_ctc_loss(seed, blank):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(seed)
+    N, V, D = 4, 50, 8
+    T = rng.integers(5, 30, size=N)
+    U = np.minimum(rng.integers(0, 9, size=N), T // 2)
+    ys = []
+    for u in U:
+        y = rng.integers(0, V - 1, size=u)
+        y = np.where(y >= blank, y + 1, y)
+        if u > 2:
+            y[2] = y[1]  # one adjacent repeat
+        ys.append(y)
+    targets = np.concatenate(ys)
+    H = rng.standard_normal((int(T.sum()), D))
+    W = rng.standard_normal((V, D))
+    out = oracle.fwd_bwd(H, W, targets, T, U, blank=blank)
+    # torch: padded (T, N, C) log-probs, gradient via autograd through log_softmax
+    Ht = torch.tensor(H, dtype=torch.float64, requires_grad=True)
+    Wt = torch.tensor(W, dtype=torch.float64, requires_grad=True)
+    logp = torch.log_softmax(Ht @ Wt.T, dim=1)
+    Tm = int(T.max())
+    pad = torch.zeros((Tm, N, V), dtype=torch.float64)
+    off = np.concatenate([[0], np.cumsum(T)])
+    rows = []
+    for n in range(N):
+        rows.append(torch.nn.functional.pad(logp[off[n]:off[n + 1]], (0, 0, 0, Tm - int(T[n]))))
+    pad = torch.stack(rows, dim=1)
+    loss = torch.nn.functional.ctc_loss(pad, torch.tensor(targets), torch.tensor(T), torch.tensor(U),
+                                        blank=blank, reduction="sum", zero_infinity=True)
+    loss.backward()
+    assert abs(float(loss.detach()) - out["loss"]) < 1e-9 * max(1.0, abs(out["loss"]))
+    np.testing.assert_allclose(out["dH"], Ht.grad.numpy(), rtol=0, atol=1e-9)
+    np.testing.assert_allclose(out["dW"], Wt.grad.numpy(), rtol=0, atol=1e-9)
+
+
+# ---------------------------------------------------------------------------------------
+# finite differences of the loss (head gradients, App. A)
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("beam", [math.inf, 3.0])
+def test_finite_differences(beam):
+    rng = np.random.default_rng(5)
+    T = np.array([4, 3])
+    U = np.array([2, 1])
+    targets = np.array([1, 3, 2])
+    H = rng.standard_normal((7, 3))
+    W = rng.standard_normal((5, 3))
+    out = oracle.fwd_bwd(H, W, targets, T, U, blank=0, beam=beam)
+
+    def loss(Hx, Wx):
+        return oracle.fwd_bwd(Hx, Wx, targets, T, U, blank=0, beam=beam, want_grads=False)["loss"]
+
+    h = 1e-6
+    for (i, j) in [(0, 0), (3, 2), (6, 1), (4, 0)]:
+        Hp, Hm = H.copy(), H.copy()
+        Hp[i, j] += h
+        Hm[i, j] -= h
+        fd = (loss(Hp, W) - loss(Hm, W)) / (2 * h)
+        assert abs(fd - out["dH"][i, j]) < 1e-6
+    for (i, j) in [(0, 0), (1, 2), (3, 1), (4, 2), (2, 0)]:
+        Wp, Wm = W.copy(), W.copy()
+        Wp[i, j] += h
+        Wm[i, j] -= h
+        fd = (loss(H, Wp) - loss(H, Wm)) / (2 * h)
+        assert abs(fd - out["dW"][i, j]) < 1e-6
+
+
+# ---------------------------------------------------------------------------------------
+# Proposition 1: the grouped formulation (Eq. grouped) gives the same loss and gradient
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_proposition1_grouped_equals_full(seed):
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(10 + seed)
+    N, V, D = 3, 40, 6
+    T = np.array([12, 9, 15])
+    U = np.array([3, 4, 5])
+    targets = rng.integers(1, 12, size=int(U.sum()))
+    H = rng.standard_normal((int(T.sum()), D))
+    W = rng.standard_normal((V, D))
+    full = oracle.fwd_bwd(H, W, targets, T, U, blank=0)
+    u = oracle.union_remap(targets, U, 0, V)
+    # grouped logits via torch autograd: R = [Z_U, LSE over the complement]
+    Ht = torch.tensor(H, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    Z = Ht @ Wt.T
+    comp = [v for v in range(V) if u["remap"][v] < 0]
+    R = torch.cat([Z[:, torch.tensor(u["u_ids"])], torch.logsumexp(Z[:, comp], dim=1, keepdim=True)], 1)
+    logp_R = torch.log_softmax(R, dim=1)
+    off = np.concatenate([[0], np.cumsum(T)])
+    yoff = np.concatenate([[0], np.cumsum(U)])
+    total = 0.0
+    for n in range(N):
+        y_rel = u["y_rel"][yoff[n]:yoff[n + 1]].tolist()
+        res = oracle.ctc_utterance(logp_R[off[n]:off[n + 1]].detach().numpy(), y_rel, 0)
+        total += -res["logP"]
+    assert abs(total - full["loss"]) < 1e-10 * abs(full["loss"])
+    # gradient of the grouped loss through torch's CTC on R
+    Tm = int(T.max())
+    pad = torch.stack([torch.nn.functional.pad(logp_R[off[n]:off[n + 1]], (0, 0, 0, Tm - int(T[n])))
+                       for n in range(N)], 1)
+    l = torch.nn.functional.ctc_loss(pad, torch.tensor(u["y_rel"]), torch.tensor(T), torch.tensor(U),
+                                     blank=0, reduction="sum")
+    l.backward()
+    np.testing.assert_allclose(Ht.grad.numpy(), full["dH"], atol=1e-10)
+    np.testing.assert_allclose(Wt.grad.numpy(), full["dW"], atol=1e-10)
+
+
+# ---------------------------------------------------------------------------------------
+# invariants on a mid-size case
+# ---------------------------------------------------------------------------------------
+
+def test_invariants_midsize():
+    from paper_2609_33645_amd import workloads
+    wl = workloads.random_small(7, N=5, T_range=(10, 60), D=16, V=300, dtype="f32", p_repeat=0.2)
+    out = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank,
+                         chunk=37)
+    inc = out["included"]
+    # occupancies sum to one on included frames: g = -1
+    np.testing.assert_allclose(out["g"][inc], -1.0, atol=1e-12)
+    assert (out["G"] <= 1e-15).all()
+    # dZ rows sum to zero: append a zero feature to H and an all-ones column to W;
+    # the logits are unchanged and dH[:, -1] = sum_v dZ[m, v]
+    ones = np.ones((wl.V, 1))
+    H0 = np.concatenate([wl.H, np.zeros((wl.M, 1))], 1)
+    out3 = oracle.fwd_bwd(H0, np.concatenate([wl.W, ones], 1), wl.targets, wl.input_lengths,
+                          wl.target_lengths, wl.blank, chunk=64)
+    np.testing.assert_allclose(out3["dH"][:, -1], 0.0, atol=1e-11)
+    # chunk width does not change anything beyond rounding
+    out4 = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank,
+                          chunk=4096)
+    assert abs(out4["loss"] - out["loss"]) < 1e-10 * abs(out["loss"])
+    np.testing.assert_allclose(out4["dW"], out["dW"], atol=1e-12)
+
+
+def test_excluded_and_nonfinite_utterances():
+    rng = np.random.default_rng(8)
+    V, D = 20, 4
+    T = np.array([3, 6, 5])
+    U = np.array([2, 2, 2])
+    targets = np.array([4, 4, 1, 2, 3, 5])   # utt 0: "4 4" needs 3 frames -> alignable; make it 2
+    T[0] = 2                                  # now T < U + r -> excluded
+    H = rng.standard_normal((int(T.sum()), D))
+    W = rng.standard_normal((V, D))
+    H[2 + 6 + 1, 0] = np.nan                  # NaN in utterance 2
+    out = oracle.fwd_bwd(H, W, targets, T, U, blank=0)
+    assert out["status"].tolist() == [oracle.STATUS_NOT_ALIGNABLE, oracle.STATUS_OK,
+                                      oracle.STATUS_NONFINITE]
+    assert out["loss_n"][0] == 0 and out["loss_n"][2] == 0
+    assert np.isfinite(out["dW"]).all()
+    assert (out["dH"][:2] == 0).all() and (out["dH"][8:] == 0).all()
+    # utterance 1 alone gives the same dW
+    alone = oracle.fwd_bwd(H[2:8], W, targets[2:4], T[1:2], U[1:2], blank=0)
+    np.testing.assert_allclose(out["dW"], alone["dW"], atol=1e-13)
+    assert abs(out["loss"] - alone["loss"]) < 1e-12
+
+
+@pytest.mark.parametrize("bad,code", [
+    (dict(targets=np.array([0, 1])), oracle.PCTC_ELABEL),
+    (dict(targets=np.array([1, 20])), oracle.PCTC_ELABEL),
+    (dict(T=np.array([0, 3])), oracle.PCTC_ELENGTH),
+    (dict(U=np.array([-1, 3])), oracle.PCTC_ELENGTH),
+    (dict(blank=20), oracle.PCTC_EINVAL),
+    (dict(beam=float("nan")), oracle.PCTC_EINVAL),
+])
+def test_validation_codes(bad, code):
+    args = dict(targets=np.array([1, 2]), T=np.array([2, 3]), U=np.array([1, 1]), blank=0, beam=math.inf)
+    args.update(bad)
+    H = np.zeros((max(1, int(np.sum(np.maximum(args["T"], 0)))), 2))
+    with pytest.raises(oracle.OracleError) as e:
+        oracle.fwd_bwd(H, np.zeros((20, 2)), args["targets"], args["T"], args["U"], args["blank"],
+                       args["beam"])
+    assert e.value.code == code
+
+
+# ---------------------------------------------------------------------------------------
+# beam pruning (Sec. 3.3, App. B.3)
+# ---------------------------------------------------------------------------------------
+
+BEAM_CASES = [(6, 4, [1, 2, 1], 0), (6, 3, [1, 1], 0), (7, 3, [2, 1], 0), (5, 4, [3], 1), (6, 3, [], 0)]
+
+
+@pytest.mark.parametrize("T,C,y,blank", BEAM_CASES)
+@pytest.mark.parametrize("beam", [0.0, 0.7, 2.0, 5.0, 40.0])
+def test_beam_matches_enumeration(T, C, y, blank, beam):
+    rng = np.random.default_rng(T * 7 + C + len(y) * 3)
+    logp = _logsoftmax(rng.standard_normal((T, C)) * 2.5)
+    ref = brute.brute_ctc(logp, y, blank, beam=beam, slack=O.KEEP_SLACK)
+    res = oracle.ctc_utterance(logp, y, blank, beam=beam)
+    assert abs(res["logP"] - ref["logP"]) < 1e-12
+    gam = np.zeros((T, C))
+    for s, c in enumerate(res["ext"]):
+        gam[:, c] += res["gamma"][:, s]
+    np.testing.assert_allclose(gam, ref["gamma"], atol=1e-12)
+    # no arc decision sits on the threshold in these cases
+    for k, m in res["margins"].items():
+        fm = np.asarray(m)[np.isfinite(m)]
+        assert (np.abs(fm) > 1e-9).all(), k
+
+
+def test_beam_properties():
+    from paper_2609_33645_amd import workloads
+    wl = workloads.random_small(11, N=4, T_range=(20, 50), D=16, V=200, dtype="f32", p_repeat=0.1,
+                                w_std=1.0)
+    full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0)
+    big = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0, beam=1e6)
+    assert abs(big["loss"] - full["loss"]) < 1e-9 * abs(full["loss"])
+    np.testing.assert_allclose(big["dW"], full["dW"], atol=1e-12)
+    for beam in [0.0, 1.0, 4.0, 10.0]:
+        pr = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0, beam=beam)
+        for n in range(wl.N):
+            if full["status"][n] != 0:
+                continue
+            delta_n = pr["loss_n"][n] - full["loss_n"][n]
+            assert delta_n >= -1e-9                       # L_beta >= L
+            dmass = -math.expm1(-max(delta_n, 0.0))
+            rows = slice(int(np.sum(wl.input_lengths[:n])), int(np.sum(wl.input_lengths[:n + 1])))
+            diff = np.abs(pr["G"][rows] - full["G"][rows])
+            assert diff.max() <= dmass + 1e-9              # |gamma_beta - gamma| <= delta
+            assert diff.sum(axis=1).max() <= 2 * dmass + 1e-9
+
+
+def test_beam_zero_keeps_only_best_path():
+    rng = np.random.default_rng(12)
+    logp = _logsoftmax(rng.standard_normal((8, 5)) * 3)
+    y = [2, 4, 4]
+    res = oracle.ctc_utterance(logp, y, 0, beam=0.0)
+    ref = brute.brute_ctc(logp, y, 0)
+    assert abs(res["logP"] - max(ref["scores"])) < 1e-12
+    gam = res["gamma"]
+    assert set(np.round(gam, 12).ravel().tolist()) <= {0.0, 1.0}
+
+
+def test_scores_stage_matches_full_path():
+    """The alignment stage on the oracle's own S reproduces the full-vocabulary result."""
+    from paper_2609_33645_amd import workloads
+    wl = workloads.random_small(13, N=3, T_range=(8, 30), D=8, V=120, dtype="f32", p_repeat=0.2)
+    full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0, beam=3.0)
+    st = oracle.ctc_from_scores(full["S"], full["y_rel"], wl.input_lengths, wl.target_lengths, beam=3.0)
+    np.testing.assert_allclose(st["loss_n"], full["loss_n"], atol=1e-10)
+    np.testing.assert_allclose(st["G"], full["G"], atol=1e-12)
