@@ -1,0 +1,173 @@
+"""Benchmark: frames/s of the fused vocabulary head + Pruned CTC forward and backward.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload zipformer_m] [--beam 16]
+
+One step = one pruned_ctc_fwd_bwd call over one synthetic batch (union/relabel, online
+full-vocabulary log-sum-exp, selected log-probabilities, beam-pruned lattice, chunked
+recomputed backward producing dH and dW), inputs resident in device memory.  Prints one
+JSON line.  Kernel durations come from HIP events the library records on its stream
+around every launch during the timed region.  The CPU baseline is the fp64 oracle on a
+bounded sample of the same workload (whole utterances, full vocabulary).
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
+PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix/vector peak
+PEAK_HBM_GBS = 8000.0
+
+GEMM_KERNELS = ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm", "gather_s")
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="zipformer_m")
+    ap.add_argument("--beam", type=float, default=None, help="alignment beam (default: 16 for zipformer_m)")
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--chunk", type=int, default=0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-utts", type=int, default=16, help="utterances in the CPU-baseline sample")
+    ap.add_argument("--frozen-head", action="store_true", help="skip dW (frozen LLM head)")
+    return ap.parse_args()
+
+
+def make_workload(name: str, seed: int, beam):
+    from paper_2609_33645_amd import workloads
+    fn = workloads.NAMED[name]
+    if beam is None:
+        beam = {"zipformer_m": 16.0, "qwen3_0p6b": 32.0, "qwen3_8b": 32.0, "qwen3_32b": 16.0}.get(name, math.inf)
+    if name == "tiny_f32":
+        wl = fn(seed)
+        wl.beam = beam
+        return wl
+    return fn(seed, beam=beam)
+
+
+def cpu_baseline(wl, n_utts: int):
+    """Time the oracle on the first n_utts whole utterances of the workload."""
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    n = min(n_utts, wl.N)
+    T = wl.input_lengths[:n]
+    U = wl.target_lengths[:n]
+    M = int(T.sum())
+    Y = int(U.sum())
+    t0 = time.perf_counter()
+    oracle.fwd_bwd(wl.H[:M], wl.W, wl.targets[:Y], T, U, wl.blank, wl.beam)
+    dt = time.perf_counter() - t0
+    return {"value": M / dt, "unit": "frames/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n} utterances ({M} frames) of the same batch, full V={wl.V}, D={wl.D}, "
+                      f"fp64 NumPy/BLAS, {dt:.1f} s"}
+
+
+def main():
+    a = parse()
+    if a.gpus != 1:
+        print(f"bench.py measures one GPU only (this build runs the whole path on a single MI355X); "
+              f"--gpus {a.gpus} is not supported", file=sys.stderr)
+        return 2
+    import torch
+    from paper_2609_33645_amd import prunedctc
+
+    wl = make_workload(a.workload, a.seed, a.beam)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    H = torch.from_numpy(wl.H).to(dev).to(tdt)
+    W = torch.from_numpy(wl.W).to(dev).to(tdt)
+    y = torch.from_numpy(wl.targets).to(dev)
+    T, U = wl.input_lengths, wl.target_lengths
+    K = len(set(wl.targets.tolist())) + 1
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, T, U, wl.blank, wl.beam, chunk=a.chunk, want_dW=not a.frozen_head)
+    torch.cuda.synchronize()
+    peak_mb = (torch.cuda.max_memory_allocated() - base_alloc) / 2**20
+    ws_mb = out["workspace_bytes"] / 2**20
+    ws = prunedctc._workspace(out["workspace_bytes"], dev)
+    del out
+    outs = {}
+
+    def step():
+        outs["o"] = prunedctc.pruned_ctc_fwd_bwd(H, W, y, T, U, wl.blank, wl.beam, chunk=a.chunk,
+                                                 want_dW=not a.frozen_head, workspace=ws)
+
+    for _ in range(a.warmup):
+        step()
+    torch.cuda.synchronize()
+    prunedctc.prof_reset()
+    prunedctc.prof_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(a.steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prunedctc.prof_enable(False)
+    prof = prunedctc.prof_read()
+    ms_step = dt * 1e3 / a.steps
+    M, D, V = wl.M, wl.D, wl.V
+    fps = M * a.steps / dt
+
+    # algorithmic work per step (bf16/fp32 matrix products)
+    gemm_flops = {"lse_partial": 2.0 * M * V * D, "recompute_dz": 2.0 * M * V * D, "dh_gemm": 2.0 * M * V * D,
+                  "dw_gemm": 0.0 if a.frozen_head else 2.0 * M * V * D, "gather_s": 2.0 * M * K * D}
+    kernel_ms = {k: v["total_ms"] / a.steps for k, v in prof.items()}
+    launches = {k: v["launches"] / a.steps for k, v in prof.items()}
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    dom = max((k for k in GEMM_KERNELS if k in kernel_ms), key=lambda k: kernel_ms[k])
+    dom_avg_ms = kernel_ms[dom] / launches[dom]
+    dom_flops_per_launch = gemm_flops[dom] / launches[dom]
+    achieved = dom_flops_per_launch / (dom_avg_ms * 1e-3) / 1e12
+    gemm_ms = sum(kernel_ms.get(k, 0.0) for k in GEMM_KERNELS)
+    gemm_total = sum(gemm_flops[k] for k in gemm_flops if k != "gather_s")
+    line = {
+        "metric": "frames/sec fused head+Pruned-CTC fwd+bwd at V=180K; % bf16 MFMA peak; peak MB",
+        "value": round(fps, 1),
+        "unit": "frames/s",
+        "n_gpus": 1,
+        "steps": a.steps,
+        "warmup": a.warmup,
+        "ms_per_step": round(ms_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": wl.dtype,
+        "data": "synthetic (seeded; shapes of the paper's workloads, no corpus data)",
+        "config": {"workload": wl.name, "N": wl.N, "M": M, "D": D, "V": V, "K": K, "beam": wl.beam,
+                   "chunk": a.chunk or 16384, "seed": a.seed, "dW": not a.frozen_head},
+        "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": None},
+        "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),
+        "mfma_frac_step": round(gemm_total / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "peak_mb": round(peak_mb, 1),
+        "workspace_mb": round(ws_mb, 1),
+        "kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(kernel_ms.items(), key=lambda kv: -kv[1])},
+    }
+    if not a.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, a.cpu_utts)
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

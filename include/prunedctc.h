@@ -1,0 +1,184 @@
+/*
+ * prunedctc.h -- C ABI of the Pruned CTC head-and-loss library for MI355X (gfx950).
+ *
+ * The library evaluates the loss of "Pruned CTC for Memory-Efficient Large-Vocabulary
+ * ASR Training" and its gradients with respect to the head input and head weight:
+ *
+ *   Z = H W^T (logits, never stored), lambda_m = log sum_v exp Z[m, v]      (Eq. lognorm)
+ *   L_beta = -sum over alignable utterances of log sum over retained alignments of
+ *            prod_t p_{pi_t}(frame)                                          (Eq. pruned-ctc)
+ *   dL/dZ[m, v] = scatter_U(G)[m, v] - g_m p_v(m)                              (Eq. vjp)
+ *   dH = dZ W,   dW = dZ^T H                                          (App. A, Step 3)
+ *
+ * following Algorithm 1 ("Pruned CTC"): union of target labels plus blank, online
+ * full-vocabulary log-sum-exp over vocabulary chunks, selected-class log-probabilities
+ * S, beam-pruned alignment lattice, and a chunk-by-chunk recomputed backward pass.
+ *
+ * Conventions (Sec. 3.1): a batch holds N utterances; utterance n has T_n >= 1 frames
+ * and a blank-free target of U_n >= 0 labels.  The M = sum T_n frames are stacked
+ * row-wise, utterance after utterance, without padding.  Class ids are 0-based.
+ *
+ * Memory: every buffer argument is a HIP device pointer owned by the caller, except the
+ * two length arrays, which are host pointers.  The library allocates no device memory in
+ * these calls; all scratch comes from the caller's workspace.  The loss is the sum of
+ * per-utterance losses (unit weights); gradients are of that sum.
+ *
+ * Excluded utterances are not errors: an utterance whose target cannot be aligned to
+ * its frames (T_n < U_n + r_n, r_n = number of adjacent equal label pairs; App. B.1
+ * "Loss aggregation") or whose loss is not finite contributes zero loss, zero dH rows
+ * and nothing to dW, and is reported in utt_status.
+ *
+ * Threading: calls on different streams may run concurrently if they use different
+ * workspaces and outputs.  The optional kernel-timing facility (pctc_prof_*) keeps
+ * process-wide state and is meant for single-threaded benchmarking.
+ */
+#ifndef PRUNEDCTC_H
+#define PRUNEDCTC_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Storage type of H and W.  Arithmetic: bf16 inputs are multiplied on bf16 matrix cores
+ * with fp32 accumulation; f32 inputs on fp32 matrix cores. */
+typedef enum { PCTC_F32 = 0, PCTC_BF16 = 1 } pctc_dtype;
+
+typedef enum {
+  PCTC_OK = 0,
+  PCTC_EINVAL = -1,     /* bad sizes, pointers, blank, beam, chunk or dtype */
+  PCTC_ELABEL = -2,     /* a target label is outside [0, V) or equals blank */
+  PCTC_ELENGTH = -3,    /* some T_n < 1 or U_n < 0 */
+  PCTC_EWORKSPACE = -4, /* workspace_bytes smaller than pctc_workspace_size() */
+  PCTC_EHIP = -5,       /* a HIP runtime call failed; see pctc_last_error() */
+  PCTC_ETOOLONG = -6    /* a target longer than PCTC_MAX_TARGET labels */
+} pctc_status;
+
+/* Per-utterance status codes written to utt_status. */
+enum { PCTC_UTT_OK = 0, PCTC_UTT_NOT_ALIGNABLE = 1, PCTC_UTT_NONFINITE = 2 };
+
+/* Limits of this implementation. */
+#define PCTC_MAX_TARGET 1023    /* U_n (2U_n+1 lattice states per frame held in one wavefront) */
+#define PCTC_MAX_VOCAB 524288   /* V (membership bitmap of the union kept in on-chip memory) */
+
+/* Bytes of workspace pruned_ctc_fwd_bwd needs for this batch.  Depends on N, the frame
+ * and target lengths, D, the chunk width and (through the union bitmap, the vocabulary
+ * chunk and the remap table) linearly on V only in a V-sized int32 table; the dominant
+ * terms scale with M*K (selected log-probabilities and their gradient), the lattice
+ * size sum_n T_n (2U_n+1), and M*chunk (one recomputed bf16 gradient chunk).
+ * chunk: vocabulary columns recomputed per backward step; 0 selects the default (16384).
+ * Returns 0 if the arguments are invalid. */
+size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
+                           const int32_t* target_lengths, int32_t D, int32_t V, float beam,
+                           int32_t chunk);
+
+/* Forward and backward pass of Pruned CTC (Algorithm 1).
+ *
+ * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8.
+ * W        [V, D] row-major, dtype (the head weight; no bias).
+ * targets  device int32 [sum target_lengths]: concatenated blank-free labels.
+ * input_lengths, target_lengths: HOST int32 [N].
+ * blank    the blank class id, 0 <= blank < V.  It becomes column 0 of the union.
+ * beam     alignment beam in natural-log units (Sec. 3.3, App. B.3).  A finite value
+ *          >= 0 prunes every lattice arc whose best complete alignment scores more than
+ *          beam (+1e-3 slack) below the best alignment; +INF or a negative value keeps
+ *          all alignments (unpruned reduced CTC).  NaN is PCTC_EINVAL.
+ * chunk    vocabulary columns per backward recompute step (0 = default 16384; otherwise
+ *          a positive multiple of 256).
+ * loss     device double [1]: sum over utterances of the finite per-utterance losses.
+ * loss_per_utt  device double [N] or NULL.
+ * utt_status    device int32 [N] or NULL (PCTC_UTT_* codes).
+ * dH       device float [M, D] or NULL (not computed).
+ * dW       device float [V, D] or NULL (frozen head: not computed).
+ * workspace/workspace_bytes: device scratch of at least pctc_workspace_size() bytes,
+ *          256-byte aligned.  Contents on entry are ignored.
+ * stream   hipStream_t to run on (NULL = the default stream).
+ *
+ * The call is asynchronous except for one stream synchronisation at the end, which
+ * reads back the device-side label check.  Host-checkable errors return before any
+ * work is queued.  On any error the outputs are unspecified.
+ */
+int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const void* W, int32_t V,
+                           const int32_t* targets, const int32_t* input_lengths,
+                           const int32_t* target_lengths, int32_t N, int32_t blank, float beam,
+                           int32_t chunk, double* loss, double* loss_per_utt, int32_t* utt_status,
+                           float* dH, float* dW, void* workspace, size_t workspace_bytes,
+                           void* stream);
+
+/* Human-readable text of a status code, and the text of the last HIP error seen by the
+ * calling thread. */
+const char* pctc_status_string(int32_t status);
+const char* pctc_last_error(void);
+
+/* ----------------------------------------------------------------------------------
+ * Stage entry points.  Each runs one stage of Algorithm 1 on caller buffers, so that a
+ * stage can be checked on its own.  All run asynchronously on `stream` unless stated.
+ * ---------------------------------------------------------------------------------- */
+
+/* Union subset and relabelling (Sec. 3.2 "Reformulation"; Algorithm 1).  The selected
+ * classes are blank followed by the distinct target labels in increasing id order.
+ * remap    device int32 [V]: index of class v in the union, or -1.
+ * u_ids    device int32 [1 + sum target_lengths]: the union; entries past K unspecified.
+ * y_rel    device int32 [sum target_lengths]: targets relabelled by their union index.
+ * K        device int32 [1]: the union size.
+ * err      device int32 [1]: set non-zero if a label is out of range or equals blank.
+ * Synchronous (reads err back); returns PCTC_ELABEL on a bad label. */
+int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t blank, int32_t V,
+                         int32_t* remap, int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err,
+                         void* stream);
+
+/* Normaliser and selected-class log-probabilities (Eq. lognorm; Algorithm 1):
+ * lam[m] = log sum_v exp (H W^T)[m, v] in double; S[m, j] = float(Z[m, u_ids[j]] - lam[m])
+ * with the subtraction in double and one rounding to float, for j < K (K read from the
+ * device scalar), S row pitch ldS >= K_max.  K_max bounds K (1 + total targets).
+ * partials: device scratch of pctc_lse_scratch_bytes(M) bytes. */
+size_t pctc_lse_scratch_bytes(int32_t M);
+int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
+                        int32_t V, const int32_t* u_ids, const int32_t* K, int32_t K_max,
+                        double* lam, float* S, int32_t ldS, void* partials, void* stream);
+
+/* Alignment stage (Sec. 3.3; Algorithm 1 lattice, total scores and gradient): from the
+ * selected log-probabilities S [M, ldS] (column 0 = blank) and the relabelled targets,
+ * per-utterance losses, statuses, G = dL/dS [M, ldS] (-occupancy summed over the states
+ * of each class; zero on excluded utterances and unused columns) and g[m] = sum_j G[m, j].
+ * keep_mask (optional, device uint8 [sum_n T_n (2U_n+1)], utterance-major, frame-major):
+ * bit0 self arc kept, bit1 arc from s-1 kept, bit2 arc from s-2 kept (bit0 at t = 0:
+ * start arc), bit3 final arc kept (last frame only).  NULL when not wanted.
+ * dp_scratch: device scratch of pctc_dp_scratch_bytes() bytes. */
+size_t pctc_dp_scratch_bytes(int32_t N, const int32_t* input_lengths, const int32_t* target_lengths,
+                             float beam);
+int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y_rel,
+                    const int32_t* input_lengths, const int32_t* target_lengths, int32_t N,
+                    float beam, double* loss_per_utt, int32_t* utt_status, float* G, float* g,
+                    uint8_t* keep_mask, void* dp_scratch, void* stream);
+
+/* Recomputed backward (Eq. vjp; Algorithm 1 backward loop): for each vocabulary chunk,
+ * dZ = scatter_U(G) - g p with p = exp(H W^T - lam) recomputed, then dH = sum dZ W and
+ * dW = dZ^T H (rows of frames with g[m] == 0 contribute nothing).  remap: device
+ * int32 [V] from pctc_union_remap.  dH and/or dW may be NULL.
+ * bwd_scratch: device scratch of pctc_bwd_scratch_bytes() bytes. */
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
+int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
+                      int32_t V, const double* lam, const float* G, int32_t ldG, const float* g,
+                      const int32_t* remap, int32_t chunk, float* dH, float* dW, void* bwd_scratch,
+                      void* stream);
+
+/* ----------------------------------------------------------------------------------
+ * Kernel timing for benchmarks.  When enabled, every kernel the library launches is
+ * bracketed by HIP events on its stream; times are accumulated per kernel name at the
+ * end of each pruned_ctc_fwd_bwd call (which synchronises anyway).
+ * ---------------------------------------------------------------------------------- */
+void pctc_prof_enable(int32_t on);
+void pctc_prof_reset(void);
+int32_t pctc_prof_count(void);
+/* Name, total milliseconds and launch count of the i-th kernel kind; returns 0 if i is
+ * out of range. */
+int32_t pctc_prof_get(int32_t i, const char** name, double* total_ms, int64_t* launches);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PRUNEDCTC_H */

@@ -18,5 +18,6 @@ from .prunedctc_oracle import (  # noqa: F401
     extended_labels,
     ctc_utterance,
     ctc_from_scores,
+    head_backward,
     fwd_bwd,
 )

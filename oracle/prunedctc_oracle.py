@@ -315,6 +315,35 @@ def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: f
             "loss": float(loss_n.sum())}
 
 
+def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096) -> Dict[str, np.ndarray]:
+    """The recomputed backward stage alone (Eq. vjp; Algorithm 1 backward loop):
+    dZ[m, v] = scatter_U(G)[m, v] - g_m p_v(m) with p_v(m) = exp(Z[m, v] - lambda_m),
+    formed one vocabulary chunk at a time, then dH = dZ W and dW = dZ^T H.  A frame with
+    g_m = 0 belongs to an excluded utterance and contributes nothing to either product."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    lam = np.asarray(lam, np.float64)
+    G = np.asarray(G, np.float64)
+    g = np.asarray(g, np.float64)
+    M, D = H.shape
+    V = W.shape[0]
+    inc = g != 0
+    dH = np.zeros((M, D))
+    dW = np.zeros((V, D))
+    col = {int(v): j for j, v in enumerate(np.asarray(u_ids).tolist())}
+    for v0 in range(0, V, chunk):
+        v1 = min(V, v0 + chunk)
+        Z = H[inc] @ W[v0:v1].T
+        dZ = -g[inc, None] * np.exp(Z - lam[inc, None])
+        for v in range(v0, v1):
+            j = col.get(v)
+            if j is not None:
+                dZ[:, v - v0] += G[inc, j]
+        dH[inc] += dZ @ W[v0:v1]
+        dW[v0:v1] = dZ.T @ H[inc]
+    return {"dH": dH, "dW": dW}
+
+
 # ---------------------------------------------------------------------------------------
 # Whole path: loss and head gradients by the full-vocabulary definition
 # ---------------------------------------------------------------------------------------

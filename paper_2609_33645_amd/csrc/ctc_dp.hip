@@ -1,0 +1,590 @@
+// Alignment lattice of Pruned CTC (Sec. 3.1 CTC; Sec. 3.3 and App. B.3 beam pruning;
+// Algorithm 1 lattice, total scores, zeroing of nonfinite losses and dL/dS).
+//
+// The lattice of utterance n is the extended label sequence l' = (blank, y1, blank, ...,
+// yU, blank) of S' = 2U+1 states per frame; it is implicit (states are indices).  Arcs:
+// start -> (0, s) for s < 2; (t-1, s) -> (t, s); (t-1, s-1) -> (t, s); (t-1, s-2) -> (t, s)
+// when l'_s is a label different from l'_{s-2}; (T-1, s) -> end for s >= S'-2.
+//
+// Kernels:
+//   dp_prep      per utterance: alignability T >= U + r (App. B.1), duplicate-label links,
+//                frame -> utterance map.
+//   dp_pass      one wavefront per (utterance, direction); lane l holds states
+//                [lQ, lQ+Q).  Viterbi (max-plus, float) or total score (log-sum-exp,
+//                accumulated in double), renormalised every frame by the wave maximum
+//                with the running offsets kept in double.
+//   dp_mask      beam rule: keep an arc iff the best complete alignment through it scores
+//                at least (best alignment) - beam - slack.
+//   dp_occupancy gamma_t(s) = alpha_t(s) beta_t(s) / P, summed per selected class into
+//                G = dL/dS = -gamma (Algorithm 1 output), and g = row sums of G.
+//   loss_reduce  sum of finite per-utterance losses (Algorithm 1, zero nonfinite).
+#include <type_traits>
+
+#include "pctc_internal.h"
+
+namespace pctc {
+
+constexpr float kNeg = -1.0e30f;  // "impossible" score; absorbs finite additions
+
+DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
+  DpPlan p{};
+  p.N = N;
+  p.pruned = (beam == beam) && beam >= 0.f && beam < INFINITY;
+  int64_t M = 0, Y = 0, L = 0;
+  int Smax = 1;
+  for (int n = 0; n < N; ++n) {
+    M += T[n];
+    Y += U[n];
+    L += static_cast<int64_t>(T[n]) * (2 * U[n] + 1);
+    Smax = U[n] * 2 + 1 > Smax ? U[n] * 2 + 1 : Smax;
+  }
+  p.M = static_cast<int>(M);
+  p.Y = static_cast<int>(Y);
+  p.Smax = Smax;
+  p.lattice = L;
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o += align_up(bytes > 0 ? bytes : 1, 256);
+    return at;
+  };
+  p.off_toff = take((N + 1) * sizeof(int32_t));
+  p.off_yoff = take((N + 1) * sizeof(int32_t));
+  p.off_soff = take((N + 1) * sizeof(int64_t));
+  p.off_frame_utt = take(M * sizeof(int32_t));
+  p.off_dup_next = take(Y * sizeof(int32_t));
+  p.off_dup_first = take(Y * sizeof(int32_t));
+  p.off_logp = take(N * sizeof(double));
+  p.off_tab_fa = take(L * sizeof(float));
+  p.off_tab_fb = take(L * sizeof(float));
+  p.off_sc_fa = take(M * sizeof(double));
+  p.off_sc_fb = take(M * sizeof(double));
+  if (p.pruned) {
+    p.off_tab_va = take(L * sizeof(float));
+    p.off_tab_vb = take(L * sizeof(float));
+    p.off_sc_va = take(M * sizeof(double));
+    p.off_sc_vb = take(M * sizeof(double));
+    p.off_vbest = take(N * sizeof(double));
+    p.off_mask = take(L * sizeof(uint8_t));
+  }
+  p.total = o;
+  return p;
+}
+
+// ---------------------------------------------------------------------------------------
+
+__global__ void dp_prep_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ yoff,
+                               const int32_t* __restrict__ y_rel, int ncols, int32_t* __restrict__ status,
+                               int32_t* __restrict__ dup_next, int32_t* __restrict__ dup_first,
+                               int32_t* __restrict__ frame_utt, double* __restrict__ loss_n) {
+  const int n = blockIdx.x;
+  const int t0 = toff[n], T = toff[n + 1] - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  const int* y = y_rel + y0;
+  __shared__ int reps, badlab;
+  if (threadIdx.x == 0) {
+    reps = 0;
+    badlab = 0;
+  }
+  __syncthreads();
+  int myreps = 0;
+  for (int i = threadIdx.x; i < U; i += blockDim.x) {
+    if (y[i] < 1 || y[i] >= ncols) badlab = 1;  // not a label column of S
+    if (i > 0 && y[i] == y[i - 1]) ++myreps;
+    int nx = -1;
+    for (int j = i + 1; j < U; ++j)
+      if (y[j] == y[i]) {
+        nx = j;
+        break;
+      }
+    int first = 1;
+    for (int j = 0; j < i; ++j)
+      if (y[j] == y[i]) {
+        first = 0;
+        break;
+      }
+    dup_next[y0 + i] = nx;
+    dup_first[y0 + i] = first;
+  }
+  if (myreps) atomicAdd(&reps, myreps);
+  for (int t = threadIdx.x; t < T; t += blockDim.x) frame_utt[t0 + t] = n;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    // 3: a relabelled target is not a label column; the lattice is not evaluated
+    status[n] = badlab ? 3 : ((T >= U + reps) ? 0 : 1);
+    loss_n[n] = 0.0;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+
+__device__ __forceinline__ float lane_up(float x, int lane) {  // value of lane-1 (kNeg at lane 0)
+  float v = __shfl_up(x, 1, 64);
+  return lane == 0 ? kNeg : v;
+}
+__device__ __forceinline__ float lane_down(float x, int lane) {  // value of lane+1 (kNeg at lane 63)
+  float v = __shfl_down(x, 1, 64);
+  return lane == 63 ? kNeg : v;
+}
+__device__ __forceinline__ double lane_up(double x, int lane) {
+  double v = __shfl_up(x, 1, 64);
+  return lane == 0 ? static_cast<double>(kNeg) : v;
+}
+__device__ __forceinline__ double lane_down(double x, int lane) {
+  double v = __shfl_down(x, 1, 64);
+  return lane == 63 ? static_cast<double>(kNeg) : v;
+}
+__device__ __forceinline__ int lane_up_i(int x, int lane) {
+  int v = __shfl_up(x, 1, 64);
+  return lane == 0 ? 0 : v;
+}
+__device__ __forceinline__ int lane_down_i(int x, int lane) {
+  int v = __shfl_down(x, 1, 64);
+  return lane == 63 ? 0 : v;
+}
+
+// Max (Viterbi) or log-sum-exp (natural log) of three scores.  The log-sum-exp keeps
+// the scores in Acc (double for the total-score pass) and evaluates exp/log in float on
+// differences from the maximum, where float is accurate.
+template <bool VIT, typename Acc>
+__device__ __forceinline__ Acc comb3(Acc a, Acc b, Acc c) {
+  const Acc m = fmax(fmax(a, b), c);
+  if constexpr (VIT) {
+    return m;
+  } else {
+    const float s = fast_exp2(static_cast<float>(a - m) * kLog2e) + fast_exp2(static_cast<float>(b - m) * kLog2e) +
+                    fast_exp2(static_cast<float>(c - m) * kLog2e);
+    return m + static_cast<Acc>(fast_log2(s) * kLn2);
+  }
+}
+
+// One wavefront per (utterance, direction), natural-log units.  VIT: Viterbi (max-plus)
+// accumulated in float; otherwise the total score (log-sum-exp) accumulated in double,
+// so the per-frame additions do not round at the magnitude of the emission scores.
+// Tables hold scores minus a per-frame offset (rounded to float once); the offsets are
+// kept per frame in double.
+template <int Q, bool VIT>
+__global__ void __launch_bounds__(64)
+dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
+               const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
+               int32_t* __restrict__ status, const uint8_t* __restrict__ mask, float* __restrict__ tab_f,
+               float* __restrict__ tab_b, double* __restrict__ sc_f, double* __restrict__ sc_b,
+               double* __restrict__ total_out, double* __restrict__ loss_n) {
+  const int n = blockIdx.x;
+  const int dir = blockIdx.y;
+  const int lane = threadIdx.x;
+  if (status[n] != 0) return;
+  const int t0 = toff[n], T = toff[n + 1] - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  const int Sp = 2 * U + 1;
+  const int64_t base = soff[n];
+  using Acc = typename std::conditional<VIT, float, double>::type;
+  const int* y = y_rel + y0;
+
+  int col[Q];
+  bool valid[Q], skip_in[Q], skip_out[Q], fin[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int s = lane * Q + q;
+    valid[q] = s < Sp;
+    col[q] = (valid[q] && (s & 1)) ? y[(s - 1) >> 1] : 0;
+    // arc s-2 -> s exists
+    skip_in[q] = valid[q] && (s & 1) && s >= 3 && y[(s - 1) >> 1] != y[(s - 3) >> 1];
+    // arc s -> s+2 exists
+    const int s2 = s + 2;
+    skip_out[q] = (s2 < Sp) && (s2 & 1) && y[(s2 - 1) >> 1] != y[(s2 - 3) >> 1];
+    fin[q] = valid[q] && s >= Sp - 2;
+  }
+
+  if (dir == 0) {
+    // ---------------- forward ----------------
+    Acc a[Q];
+    {
+      const float* row = S + static_cast<int64_t>(t0) * ldS;
+      uint8_t mk[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) mk[q] = (mask && valid[q]) ? mask[base + lane * Q + q] : 0xff;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int s = lane * Q + q;
+        a[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? static_cast<Acc>(row[col[q]]) : static_cast<Acc>(kNeg);
+      }
+    }
+    double off = 0.0;
+    for (int t = 0; t < T; ++t) {
+      if (t > 0) {
+        const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
+        Acc e[Q];
+        uint8_t mk[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          e[q] = valid[q] ? static_cast<Acc>(row[col[q]]) : Acc(0);
+          mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q] : 0x07;
+        }
+        const Acc up1 = lane_up(a[Q - 1], lane);
+        const Acc up2 = (Q >= 2) ? lane_up(a[Q >= 2 ? Q - 2 : 0], lane) : lane_up(up1, lane);
+        Acc na[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const Acc neg = kNeg;
+          const Acc p0 = a[q];
+          const Acc p1 = (q >= 1) ? a[q >= 1 ? q - 1 : 0] : up1;
+          const Acc p2 = (q >= 2) ? a[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
+          const Acc c0 = (mk[q] & 1) ? p0 : neg;
+          const Acc c1 = (mk[q] & 2) ? p1 : neg;
+          const Acc c2 = (skip_in[q] && (mk[q] & 4)) ? p2 : neg;
+          na[q] = valid[q] ? e[q] + comb3<VIT, Acc>(c0, c1, c2) : neg;
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q) a[q] = na[q];
+      }
+      // renormalise by the wave maximum (found in float; subtracted exactly)
+      float mx = kNeg;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) mx = fmaxf(mx, static_cast<float>(a[q]));
+      mx = wave_max(mx);
+      if (mx <= kNeg * 0.5f || mx != mx) mx = 0.f;  // all impossible (or NaN): keep as is
+#pragma unroll
+      for (int q = 0; q < Q; ++q) a[q] = (a[q] <= Acc(kNeg * 0.5f)) ? Acc(kNeg) : a[q] - Acc(mx);
+      off += static_cast<double>(mx);
+      float* trow = tab_f + base + static_cast<int64_t>(t) * Sp;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (valid[q]) trow[lane * Q + q] = static_cast<float>(a[q]);
+      if (lane == 0) sc_f[t0 + t] = off;
+    }
+    // total over final states (with final-arc flags)
+    float fm = kNeg;
+    uint8_t fk[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      fk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(T - 1) * Sp + lane * Q + q] : 0xff;
+      if (fin[q] && (fk[q] & 8)) fm = fmaxf(fm, static_cast<float>(a[q]));
+    }
+    fm = wave_max(fm);
+    double total;
+    if (VIT) {
+      total = off + static_cast<double>(fm);
+    } else {
+      float s = 0.f;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (fin[q] && (fk[q] & 8)) s += fast_exp2(static_cast<float>(a[q] - Acc(fm)) * kLog2e);
+      s = wave_sum(s);
+      total = off + static_cast<double>(fm) + static_cast<double>(fast_log2(s) * kLn2);
+      if (fm <= kNeg * 0.5f) total = -INFINITY;
+    }
+    if (lane == 0) {
+      total_out[n] = total;
+      if (!VIT) {
+        const double L = -total;
+        const bool finite = (L == L) && L < INFINITY && L > -INFINITY;
+        loss_n[n] = finite ? L : 0.0;
+        if (!finite) status[n] = 2;
+      }
+    }
+  } else {
+    // ---------------- backward ----------------
+    Acc b[Q];
+    {
+      uint8_t mk[Q];
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(T - 1) * Sp + lane * Q + q] : 0xff;
+        b[q] = (fin[q] && (mk[q] & 8)) ? Acc(0) : Acc(kNeg);
+      }
+    }
+    double off = 0.0;
+    for (int t = T - 1; t >= 0; --t) {
+      if (t < T - 1) {
+        const float* row = S + static_cast<int64_t>(t0 + t + 1) * ldS;
+        Acc nb[Q];
+        int mk[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          nb[q] = valid[q] ? static_cast<Acc>(row[col[q]]) + b[q] : Acc(kNeg);
+          mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(t + 1) * Sp + lane * Q + q] : 0x07;
+          if (!valid[q]) mk[q] = 0;
+        }
+        const Acc dn0 = lane_down(nb[0], lane);
+        const Acc dn1 = (Q >= 2) ? lane_down(nb[Q >= 2 ? 1 : 0], lane) : lane_down(dn0, lane);
+        const int mdn0 = lane_down_i(mk[0], lane);
+        const int mdn1 = (Q >= 2) ? lane_down_i(mk[Q >= 2 ? 1 : 0], lane) : lane_down_i(mdn0, lane);
+        Acc nbb[Q];
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+          const Acc neg = kNeg;
+          const Acc s0 = nb[q];
+          const Acc s1 = (q + 1 < Q) ? nb[q + 1 < Q ? q + 1 : 0] : dn0;
+          const Acc s2 = (q + 2 < Q) ? nb[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? dn0 : dn1);
+          const int m0 = mk[q];
+          const int m1 = (q + 1 < Q) ? mk[q + 1 < Q ? q + 1 : 0] : mdn0;
+          const int m2 = (q + 2 < Q) ? mk[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? mdn0 : mdn1);
+          const Acc c0 = (m0 & 1) ? s0 : neg;
+          const Acc c1 = (m1 & 2) ? s1 : neg;
+          const Acc c2 = (skip_out[q] && (m2 & 4)) ? s2 : neg;
+          nbb[q] = valid[q] ? comb3<VIT, Acc>(c0, c1, c2) : neg;
+        }
+#pragma unroll
+        for (int q = 0; q < Q; ++q) b[q] = nbb[q];
+      }
+      float mx = kNeg;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) mx = fmaxf(mx, static_cast<float>(b[q]));
+      mx = wave_max(mx);
+      if (mx <= kNeg * 0.5f || mx != mx) mx = 0.f;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) b[q] = (b[q] <= Acc(kNeg * 0.5f)) ? Acc(kNeg) : b[q] - Acc(mx);
+      off += static_cast<double>(mx);
+      float* trow = tab_b + base + static_cast<int64_t>(t) * Sp;
+#pragma unroll
+      for (int q = 0; q < Q; ++q)
+        if (valid[q]) trow[lane * Q + q] = static_cast<float>(b[q]);
+      if (lane == 0) sc_b[t0 + t] = off;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+
+// One workgroup per frame.  Margin of each arc into (t, s):
+//   alpha^(t-1, s') + E_t(s) + beta^(t, s) - (best - beam - slack) >= 0 keeps it.
+__global__ void dp_mask_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
+                               const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff,
+                               const int32_t* __restrict__ y_rel, const int32_t* __restrict__ frame_utt,
+                               const int32_t* __restrict__ status, const float* __restrict__ va,
+                               const float* __restrict__ vb, const double* __restrict__ sva,
+                               const double* __restrict__ svb, const double* __restrict__ vbest, float beam,
+                               float slack, uint8_t* __restrict__ mask) {
+  const int m = blockIdx.x;
+  const int n = frame_utt[m];
+  if (status[n] != 0) return;
+  const int t0 = toff[n], T = toff[n + 1] - t0;
+  const int t = m - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  const int Sp = 2 * U + 1;
+  const int64_t base = soff[n];
+  const int* y = y_rel + y0;
+  const double thr = vbest[n] - static_cast<double>(beam) - static_cast<double>(slack);
+  const float* row = S + static_cast<int64_t>(m) * ldS;
+  // frame offsets: alpha^ at t-1 and beta^ at t
+  const float off_arc = (t > 0) ? static_cast<float>(sva[m - 1] + svb[m] - thr) : 0.f;
+  const float off_start = static_cast<float>(svb[m] - thr);
+  const float off_final = static_cast<float>(sva[m] - thr);
+  for (int s = threadIdx.x; s < Sp; s += blockDim.x) {
+    const int c = (s & 1) ? y[(s - 1) >> 1] : 0;
+    const float e = row[c];
+    const float bt = vb[base + static_cast<int64_t>(t) * Sp + s];
+    uint8_t bits = 0;
+    if (t == 0) {
+      if (s < 2 && e + bt + off_start >= 0.f) bits |= 1;
+    } else {
+      const float* ap = va + base + static_cast<int64_t>(t - 1) * Sp;
+      const float through = e + bt + off_arc;
+      if (ap[s] + through >= 0.f) bits |= 1;
+      if (s >= 1 && ap[s - 1] + through >= 0.f) bits |= 2;
+      const bool skip = (s & 1) && s >= 3 && y[(s - 1) >> 1] != y[(s - 3) >> 1];
+      if (skip && ap[s - 2] + through >= 0.f) bits |= 4;
+    }
+    if (t == T - 1 && s >= Sp - 2) {
+      const float at = va[base + static_cast<int64_t>(t) * Sp + s];
+      if (at + off_final >= 0.f) bits |= 8;
+    }
+    mask[base + static_cast<int64_t>(t) * Sp + s] = bits;
+  }
+}
+
+// ---------------------------------------------------------------------------------------
+
+constexpr int kOccThreads = 256;
+
+__global__ void __launch_bounds__(kOccThreads)
+dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ yoff,
+                    const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
+                    const int32_t* __restrict__ frame_utt, const int32_t* __restrict__ status,
+                    const int32_t* __restrict__ dup_next, const int32_t* __restrict__ dup_first,
+                    const float* __restrict__ fa, const float* __restrict__ fb, const double* __restrict__ sfa,
+                    const double* __restrict__ sfb, const double* __restrict__ logp, float* __restrict__ G,
+                    int ldG, float* __restrict__ g) {
+  extern __shared__ float gam[];  // [Smax]
+  __shared__ float red[kOccThreads];
+  const int m = blockIdx.x;
+  const int n = frame_utt[m];
+  if (status[n] != 0) return;  // G row stays zero, g stays zero
+  const int t0 = toff[n];
+  const int t = m - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  const int Sp = 2 * U + 1;
+  const int64_t rowb = soff[n] + static_cast<int64_t>(t) * Sp;
+  const float off = static_cast<float>(sfa[m] + sfb[m] - logp[n]);
+  for (int s = threadIdx.x; s < Sp; s += kOccThreads) {
+    const float x = fa[rowb + s] + fb[rowb + s] + off;
+    gam[s] = fast_exp2(x * kLog2e);
+  }
+  __syncthreads();
+  // blank column: sum over even states (fixed-order per thread, then tree)
+  float bsum = 0.f;
+  for (int s = 2 * threadIdx.x; s < Sp; s += 2 * kOccThreads) bsum += gam[s];
+  // label columns: the first occurrence of each label sums its states in target order
+  float lsum = 0.f;
+  for (int i = threadIdx.x; i < U; i += kOccThreads) {
+    if (!dup_first[y0 + i]) continue;
+    float acc = gam[2 * i + 1];
+    int j = dup_next[y0 + i];
+    while (j >= 0) {
+      acc += gam[2 * j + 1];
+      j = dup_next[y0 + j];
+    }
+    G[static_cast<int64_t>(m) * ldG + y_rel[y0 + i]] = -acc;
+    lsum += acc;
+  }
+  red[threadIdx.x] = bsum;
+  __syncthreads();
+  for (int o = kOccThreads / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  const float blank_total = red[0];
+  __syncthreads();
+  red[threadIdx.x] = lsum;
+  __syncthreads();
+  for (int o = kOccThreads / 2; o > 0; o >>= 1) {
+    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
+    __syncthreads();
+  }
+  if (threadIdx.x == 0) {
+    G[static_cast<int64_t>(m) * ldG + 0] = -blank_total;
+    g[m] = -(blank_total + red[0]);
+  }
+}
+
+__global__ void loss_reduce_kernel(int N, const double* __restrict__ loss_n, const int32_t* __restrict__ status,
+                                   double* __restrict__ loss) {
+  if (threadIdx.x != 0 || blockIdx.x != 0) return;
+  double s = 0.0;
+  for (int n = 0; n < N; ++n)
+    if (status[n] == 0) s += loss_n[n];
+  *loss = s;
+}
+
+hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, double* loss,
+                              hipStream_t stream) {
+  Prof pr("loss_reduce", stream);
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(64), 0, stream, N, loss_n, status, loss);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+
+template <bool VIT>
+static hipError_t launch_pass(int Q, dim3 grid, hipStream_t stream, const float* S, int ldS, const int32_t* toff,
+                              const int32_t* yoff, const int64_t* soff, const int32_t* y_rel, int32_t* status,
+                              const uint8_t* mask, float* tf, float* tb, double* sf, double* sb, double* total,
+                              double* loss_n) {
+#define PCTC_PASS(QQ)                                                                                       \
+  case QQ:                                                                                                  \
+    hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT>), grid, dim3(64), 0, stream, S, ldS, toff, yoff, soff, y_rel, \
+                       status, mask, tf, tb, sf, sb, total, loss_n);                                        \
+    break;
+  switch (Q) {
+    PCTC_PASS(1)
+    PCTC_PASS(2)
+    PCTC_PASS(3)
+    PCTC_PASS(4)
+    PCTC_PASS(6)
+    PCTC_PASS(8)
+    PCTC_PASS(10)
+    PCTC_PASS(13)
+    PCTC_PASS(16)
+    PCTC_PASS(20)
+    PCTC_PASS(24)
+    PCTC_PASS(32)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef PCTC_PASS
+  return hipGetLastError();
+}
+
+static int pick_q(int Smax) {
+  static const int qs[] = {1, 2, 3, 4, 6, 8, 10, 13, 16, 20, 24, 32};
+  const int need = (Smax + 63) / 64;
+  for (int q : qs)
+    if (q >= need) return q;
+  return -1;
+}
+
+hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
+                         const int32_t* y_rel, float beam, double* loss_n, int32_t* status, float* G, float* g,
+                         uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream, void*) {
+  const int N = plan.N;
+  char* sc = static_cast<char*>(scratch);
+  int32_t* toff = reinterpret_cast<int32_t*>(sc + plan.off_toff);
+  int32_t* yoff = reinterpret_cast<int32_t*>(sc + plan.off_yoff);
+  int64_t* soff = reinterpret_cast<int64_t*>(sc + plan.off_soff);
+  int32_t* frame_utt = reinterpret_cast<int32_t*>(sc + plan.off_frame_utt);
+  int32_t* dnext = reinterpret_cast<int32_t*>(sc + plan.off_dup_next);
+  int32_t* dfirst = reinterpret_cast<int32_t*>(sc + plan.off_dup_first);
+  double* logp = reinterpret_cast<double*>(sc + plan.off_logp);
+  float* tfa = reinterpret_cast<float*>(sc + plan.off_tab_fa);
+  float* tfb = reinterpret_cast<float*>(sc + plan.off_tab_fb);
+  double* sfa = reinterpret_cast<double*>(sc + plan.off_sc_fa);
+  double* sfb = reinterpret_cast<double*>(sc + plan.off_sc_fb);
+  hipError_t e;
+  // G and g start at zero: excluded utterances and unused columns stay zero.
+  if (plan.M > 0) {
+    e = hipMemsetAsync(G, 0, static_cast<size_t>(plan.M) * ldS * sizeof(float), stream);
+    if (e != hipSuccess) return e;
+    e = hipMemsetAsync(g, 0, static_cast<size_t>(plan.M) * sizeof(float), stream);
+    if (e != hipSuccess) return e;
+  }
+  if (N == 0) return hipSuccess;
+  {
+    Prof pr("dp_prep", stream);
+    hipLaunchKernelGGL(dp_prep_kernel, dim3(N), dim3(256), 0, stream, toff, yoff, y_rel, K_max, status, dnext,
+                       dfirst, frame_utt, loss_n);
+  }
+  const int Q = pick_q(plan.Smax);
+  if (Q < 0) return hipErrorInvalidValue;
+  uint8_t* mask = nullptr;
+  if (plan.pruned) {
+    float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
+    float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);
+    double* sva = reinterpret_cast<double*>(sc + plan.off_sc_va);
+    double* svb = reinterpret_cast<double*>(sc + plan.off_sc_vb);
+    double* vbest = reinterpret_cast<double*>(sc + plan.off_vbest);
+    mask = reinterpret_cast<uint8_t*>(sc + plan.off_mask);
+    {
+      Prof pr("dp_viterbi", stream);
+      e = launch_pass<true>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva,
+                            svb, vbest, loss_n);
+      if (e != hipSuccess) return e;
+    }
+    if (plan.M > 0) {
+      Prof pr("dp_mask", stream);
+      hipLaunchKernelGGL(dp_mask_kernel, dim3(plan.M), dim3(256), 0, stream, S, ldS, toff, yoff, soff, y_rel,
+                         frame_utt, status, tva, tvb, sva, svb, vbest, beam, kKeepSlack, mask);
+    }
+  }
+  {
+    Prof pr("dp_alpha_beta", stream);
+    e = launch_pass<false>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, mask, tfa, tfb, sfa, sfb,
+                           logp, loss_n);
+    if (e != hipSuccess) return e;
+  }
+  if (plan.M > 0) {
+    Prof pr("dp_occupancy", stream);
+    hipLaunchKernelGGL(dp_occupancy_kernel, dim3(plan.M), dim3(kOccThreads), plan.Smax * sizeof(float), stream,
+                       toff, yoff, soff, y_rel, frame_utt, status, dnext, dfirst, tfa, tfb, sfa, sfb, logp, G, ldS,
+                       g);
+  }
+  if (keep_mask_out && mask && plan.lattice > 0) {
+    e = hipMemcpyAsync(keep_mask_out, mask, plan.lattice, hipMemcpyDeviceToDevice, stream);
+    if (e != hipSuccess) return e;
+  }
+  (void)T;
+  (void)U;
+  return hipGetLastError();
+}
+
+}  // namespace pctc

@@ -1,0 +1,538 @@
+// Vocabulary-head products of Pruned CTC on matrix cores (gfx950).
+//
+//  * lse_partial: logits tile Z^T = W_tile H_tile^T with a fused online log-sum-exp
+//    epilogue over the vocabulary (Eq. lognorm; Algorithm 1 "online log-sum-exp over
+//    vocabulary chunks").  The M x V logits are never written; each workgroup keeps a
+//    running (max, sum) per frame over its vocabulary partition.
+//  * lse_finalize: combines the partitions per frame in double.
+//  * gather_s: S = Z[:, U] - lambda for the selected classes, subtraction in double and
+//    one rounding to float (Algorithm 1; App. B.1 "Forward computation").
+//  * recompute_dz: one vocabulary chunk of dZ = scatter_U(G) - g p, p = exp(Z - lambda),
+//    with Z recomputed (Eq. vjp; Algorithm 1 backward loop); stored in the input dtype.
+//  * dh_gemm / dw_gemm: dH += dZ W_c and dW_c = dZ^T H (App. A, Step 3).
+//
+// Every product C[i][j] = sum_k A[i][k] B[j][k] goes through tile_gemm (pctc_device.h).
+#include "pctc_internal.h"
+
+namespace pctc {
+
+// Frames (columns) per forward tile, vocabulary rows per forward tile.
+constexpr int kFwdBR = 256;
+constexpr int kFwdBC = 128;
+constexpr int kBwdB = 128;
+
+template <typename T>
+struct Cfg;
+template <>
+struct Cfg<uint16_t> {
+  static constexpr int BK = 64;
+};
+template <>
+struct Cfg<float> {
+  static constexpr int BK = 32;
+};
+
+// blockIdx -> logical work id such that consecutive logical ids land on the same XCD
+// (the dispatcher places workgroup b on XCD b % 8).
+__device__ __forceinline__ int xcd_swizzle(int bid, int nblocks) {
+  const int full = (nblocks / 8) * 8;
+  if (bid >= full) return bid;
+  return (bid % 8) * (full / 8) + bid / 8;
+}
+
+// ---------------------------------------------------------------------------------------
+// Forward: online log-sum-exp partials
+// ---------------------------------------------------------------------------------------
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, int V, int P, int vper,
+                   float2* __restrict__ partials) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  const int work = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int mt = work % nMt;
+  const int p = work / nMt;
+  const int m0 = mt * kFwdBC;
+  const int vbeg = p * vper;
+  const int vend = min(V, vbeg + vper);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  Operand<T> A{W, D, V, D, nullptr, nullptr};
+  Operand<T> B{H, D, M, D, nullptr, nullptr};
+  float run_max[FC], run_sum[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    run_max[j] = -INFINITY;
+    run_sum[j] = 0.f;
+  }
+  f32x16 acc[FR][FC];
+  for (int v0 = vbeg; v0 < vend; v0 += kFwdBR) {
+    tile_gemm<T, kFwdBR, kFwdBC, BK, Lay::KMajor, Lay::KMajor>(A, B, v0, m0, 0, D, lds, acc);
+    // rows past the partition end take no part in the sums
+    if (v0 + kFwdBR > vend) {
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const bool ok = v0 + acc_row<kFwdBR>(wave, lane, i, r) < vend;
+#pragma unroll
+          for (int j = 0; j < FC; ++j) acc[i][j][r] = ok ? acc[i][j][r] : -INFINITY;
+        }
+    }
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      float tmax = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[i][j][r]);
+      tmax = fmaxf(tmax, swap_halves(tmax));
+      const float nmax = fmaxf(run_max[j], tmax);
+      const float ms = nmax * kLog2e;
+      float s = 0.f;
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(acc[i][j][r], kLog2e, -ms));
+      s += swap_halves(s);
+      const float scale = (run_max[j] == -INFINITY) ? 0.f : fast_exp2((run_max[j] - nmax) * kLog2e);
+      run_sum[j] = fmaf(run_sum[j], scale, s);
+      run_max[j] = nmax;
+    }
+  }
+  // Combine the two wavefronts that share frames (row halves), then write the partial.
+  __syncthreads();
+  float2* xch = reinterpret_cast<float2*>(lds);  // [2 col halves][FC*32]
+  const int rowhalf = wave >> 1, colhalf = wave & 1;
+  if (rowhalf == 1 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) xch[colhalf * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
+  }
+  __syncthreads();
+  if (rowhalf == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const float2 o = xch[colhalf * (FC * 32) + j * 32 + lane];
+      const float nmax = fmaxf(run_max[j], o.x);
+      float s = 0.f;
+      if (run_max[j] != -INFINITY) s += run_sum[j] * fast_exp2((run_max[j] - nmax) * kLog2e);
+      if (o.x != -INFINITY) s += o.y * fast_exp2((o.x - nmax) * kLog2e);
+      if (nmax != nmax) s = nmax;  // NaN logits propagate
+      const int m = m0 + acc_col<kFwdBC>(wave, lane, j);
+      if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(nmax, s);
+    }
+  }
+}
+
+__global__ void lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
+                                    float2* __restrict__ lam2) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  double mx = -INFINITY;
+  bool nan = false;
+  for (int p = 0; p < P; ++p) {
+    const float2 q = partials[static_cast<int64_t>(p) * M + m];
+    if (q.x != q.x || q.y != q.y) nan = true;
+    mx = fmax(mx, static_cast<double>(q.x));
+  }
+  double s = 0.0;
+  for (int p = 0; p < P; ++p) {
+    const float2 q = partials[static_cast<int64_t>(p) * M + m];
+    if (q.x != -INFINITY) s += static_cast<double>(q.y) * exp(static_cast<double>(q.x) - mx);
+  }
+  double l = mx + log(s);
+  if (nan) l = __longlong_as_double(0x7ff8000000000000LL);
+  lam[m] = l;
+  const double l2 = l * kLog2eD;
+  const float hi = static_cast<float>(l2);
+  lam2[m] = make_float2(hi, static_cast<float>(l2 - static_cast<double>(hi)));
+}
+
+__global__ void lam2_kernel(const double* __restrict__ lam, int M, float2* __restrict__ lam2) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  const double l2 = lam[m] * kLog2eD;
+  const float hi = static_cast<float>(l2);
+  lam2[m] = make_float2(hi, static_cast<float>(l2 - static_cast<double>(hi)));
+}
+
+int lse_partitions(int M, int V) {
+  // Enough workgroups to fill 256 compute units a few times over; the partition count
+  // (not V) sets the size of the partial buffer.
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  int P = (2048 + nMt - 1) / nMt;
+  const int vtiles = (V + kFwdBR - 1) / kFwdBR;
+  if (P > vtiles) P = vtiles;
+  if (P > 256) P = 256;
+  if (P < 1) P = 1;
+  return P;
+}
+
+size_t lse_partial_bytes(int M) { return align_up(static_cast<size_t>(256) * M * sizeof(float2), 256); }
+
+hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  Prof pr("lam2", stream);
+  hipLaunchKernelGGL(lam2_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, lam, M, lam2);
+  return hipGetLastError();
+}
+
+hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int V, float2* partials,
+                      double* lam, float2* lam2, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  const int P = lse_partitions(M, V);
+  const int vtiles = (V + kFwdBR - 1) / kFwdBR;
+  const int vper = ((vtiles + P - 1) / P) * kFwdBR;
+  const int Peff = (V + vper - 1) / vper;
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  {
+    Prof pr("lse_partial", stream);
+    if (dtype == 1)
+      hipLaunchKernelGGL(lse_partial_kernel<uint16_t>, dim3(nMt * Peff), dim3(256), 0, stream,
+                         static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, Peff, vper,
+                         partials);
+    else
+      hipLaunchKernelGGL(lse_partial_kernel<float>, dim3(nMt * Peff), dim3(256), 0, stream,
+                         static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, Peff, vper,
+                         partials);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  Prof pr("lse_finalize", stream);
+  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Peff, lam,
+                     lam2);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Selected-class log-probabilities S
+// ---------------------------------------------------------------------------------------
+
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+gather_s_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const int32_t* __restrict__ u_ids,
+                const int32_t* __restrict__ Kdev, int K_max, const double* __restrict__ lam, float* __restrict__ S,
+                int ldS) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  const int mt = blockIdx.x % nMt;
+  const int jt = blockIdx.x / nMt;
+  const int K = *Kdev;
+  const int j0 = jt * kFwdBR;
+  if (j0 >= K) return;
+  const int m0 = mt * kFwdBC;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  Operand<T> A{W, D, K_max, D, u_ids, Kdev};
+  Operand<T> B{H, D, M, D, nullptr, nullptr};
+  f32x16 acc[FR][FC];
+  tile_gemm<T, kFwdBR, kFwdBC, BK, Lay::Gathered, Lay::KMajor>(A, B, j0, m0, 0, D, lds, acc);
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const int m = m0 + acc_col<kFwdBC>(wave, lane, j);
+    if (m >= M) continue;
+    const double l = lam[m];
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int jj = j0 + acc_row<kFwdBR>(wave, lane, i, r);
+        if (jj < K) S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(static_cast<double>(acc[i][j][r]) - l);
+      }
+  }
+}
+
+hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const int32_t* u_ids,
+                           const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+                           hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  const int nJt = (K_max + kFwdBR - 1) / kFwdBR;
+  Prof pr("gather_s", stream);
+  if (dtype == 1)
+    hipLaunchKernelGGL(gather_s_kernel<uint16_t>, dim3(nMt * nJt), dim3(256), 0, stream,
+                       static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), u_ids, K, K_max, lam,
+                       S, ldS);
+  else
+    hipLaunchKernelGGL(gather_s_kernel<float>, dim3(nMt * nJt), dim3(256), 0, stream, static_cast<const float*>(H),
+                       M, D, static_cast<const float*>(W), u_ids, K, K_max, lam, S, ldS);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Backward
+// ---------------------------------------------------------------------------------------
+
+template <typename T>
+__device__ __forceinline__ T to_elem(float x);
+template <>
+__device__ __forceinline__ uint16_t to_elem<uint16_t>(float x) {
+  return f32_to_bf16(x);
+}
+template <>
+__device__ __forceinline__ float to_elem<float>(float x) {
+  return x;
+}
+
+// dZ chunk [M][chunk] (row pitch `chunk`): columns v_local in [0, cw) hold
+// scatter_U(G) - g p for vocabulary id c0 + v_local; columns in [cw, tile end) hold 0.
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+recompute_dz_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, int c0, int cw,
+                    const float2* __restrict__ lam2, const float* __restrict__ G, int ldG, const float* __restrict__ g,
+                    const int32_t* __restrict__ remap, T* __restrict__ dZ, int chunk) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  __shared__ int sel[kFwdBR];
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  const int work = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int mt = work % nMt;
+  const int vt = work / nMt;
+  const int m0 = mt * kFwdBC;
+  const int vl0 = vt * kFwdBR;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  {
+    const int vl = vl0 + tid;
+    sel[tid] = (vl < cw) ? remap[c0 + vl] : -1;
+  }
+  const int any_sel = __syncthreads_or(sel[tid] >= 0);
+  Operand<T> A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr, nullptr};
+  Operand<T> B{H, D, M, D, nullptr, nullptr};
+  f32x16 acc[FR][FC];
+  tile_gemm<T, kFwdBR, kFwdBC, BK, Lay::KMajor, Lay::KMajor>(A, B, vl0, m0, 0, D, lds, acc);
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const int m = m0 + acc_col<kFwdBC>(wave, lane, j);
+    if (m >= M) continue;
+    const float gm = g[m];
+    const float2 l2 = lam2[m];
+    const bool inc = (gm != 0.f);
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int rl0 = acc_row<kFwdBR>(wave, lane, i, 4 * q);  // 4 consecutive rows
+        T out[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int rl = rl0 + e;
+          const int vl = vl0 + rl;
+          float val = 0.f;
+          if (inc && vl < cw) {
+            const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -l2.x) - l2.y;
+            val = -gm * fast_exp2(t);
+            if (any_sel) {
+              const int jj = sel[rl];
+              if (jj >= 0) val += G[static_cast<int64_t>(m) * ldG + jj];
+            }
+          }
+          out[e] = to_elem<T>(val);
+        }
+        T* dst = dZ + static_cast<int64_t>(m) * chunk + vl0 + rl0;
+        if constexpr (sizeof(T) == 2) {
+          u32x2 w = {static_cast<uint32_t>(out[0]) | (static_cast<uint32_t>(out[1]) << 16),
+                     static_cast<uint32_t>(out[2]) | (static_cast<uint32_t>(out[3]) << 16)};
+          *reinterpret_cast<u32x2*>(dst) = w;
+        } else {
+          *reinterpret_cast<float4*>(dst) = make_float4(out[0], out[1], out[2], out[3]);
+        }
+      }
+  }
+}
+
+// part[s][M][D] += dZ[:, slice s] . W[c0 + slice s, :]
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+dh_gemm_kernel(const T* __restrict__ dZ, int M, int chunk, const T* __restrict__ W, int D, int c0, int cw,
+               int slice, float* __restrict__ part) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kBwdB, kBwdB, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  const int nMt = (M + kBwdB - 1) / kBwdB;
+  const int nDt = (D + kBwdB - 1) / kBwdB;
+  const int work = blockIdx.x;
+  const int mt = work % nMt;
+  const int dt = (work / nMt) % nDt;
+  const int s = work / (nMt * nDt);
+  const int m0 = mt * kBwdB, d0 = dt * kBwdB;
+  const int kb = s * slice;
+  const int ke = min(cw, kb + slice);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  Operand<T> A{dZ, chunk, M, cw, nullptr, nullptr};
+  Operand<T> B{W + static_cast<int64_t>(c0) * D, D, D, cw, nullptr, nullptr};
+  f32x16 acc[FR][FC];
+  tile_gemm<T, kBwdB, kBwdB, BK, Lay::KMajor, Lay::RowMajorT>(A, B, m0, d0, kb, ke, lds, acc);
+  if (kb >= ke) return;
+  float* dst = part + static_cast<int64_t>(s) * M * D;
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int d = d0 + acc_col<kBwdB>(wave, lane, j);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + acc_row<kBwdB>(wave, lane, i, r);
+        if (m < M) dst[static_cast<int64_t>(m) * D + d] += acc[i][j][r];
+      }
+    }
+}
+
+// dW[c0 + v][:] = sum_m dZ[m][v] Ht[:, m]   (Ht: head input transposed, excluded frames zero)
+template <typename T>
+__global__ void __launch_bounds__(256, 2)
+dw_gemm_kernel(const T* __restrict__ dZ, int M, int chunk, const T* __restrict__ Ht, int Mp, int D, int c0, int cw,
+               float* __restrict__ dW) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kBwdB, kBwdB, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  const int nVt = (cw + kBwdB - 1) / kBwdB;
+  const int work = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int vt = work % nVt;
+  const int dt = work / nVt;
+  const int v0 = vt * kBwdB, d0 = dt * kBwdB;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  Operand<T> A{dZ, chunk, cw, M, nullptr, nullptr};
+  Operand<T> B{Ht, Mp, D, M, nullptr, nullptr};
+  f32x16 acc[FR][FC];
+  tile_gemm<T, kBwdB, kBwdB, BK, Lay::RowMajorT, Lay::KMajor>(A, B, v0, d0, 0, M, lds, acc);
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int d = d0 + acc_col<kBwdB>(wave, lane, j);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + acc_row<kBwdB>(wave, lane, i, r);
+        if (v < cw) dW[static_cast<int64_t>(c0 + v) * D + d] = acc[i][j][r];
+      }
+    }
+}
+
+// Ht[d][m] = H[m][d] for frames with g[m] != 0, else 0; m in [M, Mp) zero.
+template <typename T>
+__global__ void ht_build_kernel(const T* __restrict__ H, int M, int D, const float* __restrict__ g, T* __restrict__ Ht,
+                                int Mp) {
+  __shared__ T tile[64][65];
+  const int m0 = blockIdx.x * 64, d0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;  // 256 threads: 64 x 4
+  for (int r = ty; r < 64; r += 4) {
+    const int m = m0 + r, d = d0 + tx;
+    T v = T(0);
+    if (m < M && d < D && g[m] != 0.f) v = H[static_cast<int64_t>(m) * D + d];
+    tile[r][tx] = v;
+  }
+  __syncthreads();
+  for (int r = ty; r < 64; r += 4) {
+    const int d = d0 + r, m = m0 + tx;
+    if (d < D && m < Mp) Ht[static_cast<int64_t>(d) * Mp + m] = tile[tx][r];
+  }
+}
+
+__global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ dH) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  float s = 0.f;
+  for (int k = 0; k < splits; ++k) s += part[k * n + i];
+  dH[i] = s;
+}
+
+BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
+  BwdPlan p{};
+  p.chunk = (chunk > 0) ? chunk : kDefaultChunk;
+  const size_t es = (dtype == 1) ? 2 : 4;
+  const int tiles = ((M + kBwdB - 1) / kBwdB) * ((D + kBwdB - 1) / kBwdB);
+  int splits = (1024 + tiles - 1) / tiles;
+  const int maxs = p.chunk / 256;
+  if (splits > maxs) splits = maxs;
+  if (splits > 8) splits = 8;
+  if (splits < 1) splits = 1;
+  p.splits = splits;
+  p.Mp = ((M + 63) / 64) * 64;
+  p.dz_bytes = align_up(static_cast<size_t>(M) * p.chunk * es, 256);
+  p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);
+  p.part_bytes = align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
+  p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
+  p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes;
+  return p;
+}
+
+template <typename T>
+static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const float2* lam2, const float* G,
+                             int ldG, const float* g, const int32_t* remap, float* dH, float* dW, char* scratch,
+                             const BwdPlan& plan, hipStream_t stream) {
+  T* dZ = reinterpret_cast<T*>(scratch);
+  T* Ht = reinterpret_cast<T*>(scratch + plan.dz_bytes);
+  float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
+  const int chunk = plan.chunk;
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  if (dW) {
+    Prof pr("ht_build", stream);
+    hipLaunchKernelGGL(ht_build_kernel<T>, dim3(plan.Mp / 64, (D + 63) / 64), dim3(256), 0, stream, H, M, D, g,
+                       Ht, plan.Mp);
+  }
+  int slice = ((chunk / plan.splits + 63) / 64) * 64;
+  if (dH) {
+    hipError_t e = hipMemsetAsync(part, 0, static_cast<size_t>(plan.splits) * M * D * sizeof(float), stream);
+    if (e != hipSuccess) return e;
+  }
+  for (int c0 = 0; c0 < V; c0 += chunk) {
+    const int cw = min(chunk, V - c0);
+    const int nVt = (cw + kFwdBR - 1) / kFwdBR;
+    {
+      Prof pr("recompute_dz", stream);
+      hipLaunchKernelGGL(recompute_dz_kernel<T>, dim3(nMt * nVt), dim3(256), 0, stream, H, M, D, W, c0, cw, lam2,
+                         G, ldG, g, remap, dZ, chunk);
+    }
+    if (dH) {
+      const int tiles = ((M + kBwdB - 1) / kBwdB) * ((D + kBwdB - 1) / kBwdB);
+      const int ns = (cw + slice - 1) / slice;
+      Prof pr("dh_gemm", stream);
+      hipLaunchKernelGGL(dh_gemm_kernel<T>, dim3(tiles * ns), dim3(256), 0, stream, dZ, M, chunk, W, D, c0, cw,
+                         slice, part);
+    }
+    if (dW) {
+      const int grid = ((cw + kBwdB - 1) / kBwdB) * ((D + kBwdB - 1) / kBwdB);
+      Prof pr("dw_gemm", stream);
+      hipLaunchKernelGGL(dw_gemm_kernel<T>, dim3(grid), dim3(256), 0, stream, dZ, M, chunk, Ht, plan.Mp, D, c0, cw,
+                         dW);
+    }
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (dH) {
+    const int64_t n = static_cast<int64_t>(M) * D;
+    Prof pr("dh_reduce", stream);
+    hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
+                       plan.splits, n, dH);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
+                           const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
+                           void* scratch, const BwdPlan& plan, hipStream_t stream) {
+  if (M <= 0) {
+    if (dW) return hipMemsetAsync(dW, 0, static_cast<size_t>(V) * D * sizeof(float), stream);
+    return hipSuccess;
+  }
+  char* sc = static_cast<char*>(scratch);
+  if (dtype == 1)
+    return head_bwd_t<uint16_t>(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, lam2, G,
+                                ldG, g, remap, dH, dW, sc, plan, stream);
+  return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, lam2, G, ldG, g,
+                           remap, dH, dW, sc, plan, stream);
+}
+
+}  // namespace pctc

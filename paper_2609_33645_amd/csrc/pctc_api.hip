@@ -1,0 +1,396 @@
+// C ABI of the Pruned CTC library: argument checks, workspace layout, stage ordering
+// (Algorithm 1 of "Pruned CTC for Memory-Efficient Large-Vocabulary ASR Training").
+#include <math.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <map>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "../../include/prunedctc.h"
+#include "pctc_internal.h"
+
+namespace pctc {
+
+// ---------------------------------------------------------------------------------------
+// Kernel timing
+// ---------------------------------------------------------------------------------------
+namespace {
+struct ProfRec {
+  const char* name;
+  hipEvent_t start, stop;
+};
+struct ProfState {
+  std::mutex mu;
+  bool enabled = false;
+  std::vector<hipEvent_t> pool;
+  std::vector<ProfRec> pending;
+  std::vector<std::string> names;
+  std::map<std::string, std::pair<double, int64_t>> totals;
+};
+ProfState& prof_state() {
+  static ProfState* s = new ProfState();  // never destroyed: events may outlive static teardown
+  return *s;
+}
+hipEvent_t take_event(ProfState& s) {
+  if (!s.pool.empty()) {
+    hipEvent_t e = s.pool.back();
+    s.pool.pop_back();
+    return e;
+  }
+  hipEvent_t e = nullptr;
+  if (hipEventCreate(&e) != hipSuccess) return nullptr;
+  return e;
+}
+thread_local char g_last_error[512] = "";
+}  // namespace
+
+Prof::Prof(const char* name, hipStream_t st) : slot(-1), stream(st) {
+  ProfState& s = prof_state();
+  if (!s.enabled) return;
+  std::lock_guard<std::mutex> lk(s.mu);
+  ProfRec r{name, take_event(s), take_event(s)};
+  if (!r.start || !r.stop) return;
+  hipEventRecord(r.start, stream);
+  slot = static_cast<int>(s.pending.size());
+  s.pending.push_back(r);
+}
+
+Prof::~Prof() {
+  if (slot < 0) return;
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  hipEventRecord(s.pending[slot].stop, stream);
+}
+
+void prof_flush() {
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  for (auto& r : s.pending) {
+    float ms = 0.f;
+    if (hipEventSynchronize(r.stop) == hipSuccess && hipEventElapsedTime(&ms, r.start, r.stop) == hipSuccess) {
+      auto it = s.totals.find(r.name);
+      if (it == s.totals.end()) {
+        s.names.push_back(r.name);
+        s.totals[r.name] = {static_cast<double>(ms), 1};
+      } else {
+        it->second.first += ms;
+        it->second.second += 1;
+      }
+    }
+    s.pool.push_back(r.start);
+    s.pool.push_back(r.stop);
+  }
+  s.pending.clear();
+}
+
+static void set_error(const char* what, hipError_t e) {
+  snprintf(g_last_error, sizeof(g_last_error), "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------------------
+// Workspace layout
+// ---------------------------------------------------------------------------------------
+struct Layout {
+  int N, M, Y, K_max, ldS;
+  bool pruned;
+  DpPlan dp;
+  BwdPlan bwd;
+  size_t o_remap, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_dp, o_bwd,
+      total;
+};
+
+static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
+                          float beam, int32_t chunk) {
+  if (dtype != PCTC_F32 && dtype != PCTC_BF16) return PCTC_EINVAL;
+  if (N < 0 || D <= 0 || (D % 8) != 0 || V <= 1 || V > PCTC_MAX_VOCAB) return PCTC_EINVAL;
+  if (beam != beam) return PCTC_EINVAL;
+  if (chunk < 0 || (chunk > 0 && (chunk % 256) != 0)) return PCTC_EINVAL;
+  if (N > 0 && (!T || !U)) return PCTC_EINVAL;
+  int64_t M = 0, Y = 0;
+  for (int n = 0; n < N; ++n) {
+    if (T[n] < 1 || U[n] < 0) return PCTC_ELENGTH;
+  }
+  for (int n = 0; n < N; ++n) {
+    if (U[n] > PCTC_MAX_TARGET) return PCTC_ETOOLONG;
+    M += T[n];
+    Y += U[n];
+  }
+  if (M > (1LL << 30) || Y > (1LL << 28)) return PCTC_EINVAL;
+  return PCTC_OK;
+}
+
+static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
+                          float beam, int32_t chunk) {
+  Layout L{};
+  L.N = N;
+  L.dp = plan_dp(N, T, U, beam);
+  L.M = L.dp.M;
+  L.Y = L.dp.Y;
+  L.pruned = L.dp.pruned;
+  L.K_max = (1 + L.Y < V) ? 1 + L.Y : V;
+  L.ldS = static_cast<int>(align_up(static_cast<size_t>(L.K_max), 4));
+  L.bwd = plan_bwd(dtype == PCTC_BF16 ? 1 : 0, L.M, D, chunk);
+  size_t o = 0;
+  auto take = [&](size_t bytes) {
+    size_t at = o;
+    o += align_up(bytes > 0 ? bytes : 1, 256);
+    return at;
+  };
+  L.o_remap = take(static_cast<size_t>(V) * 4);
+  L.o_uids = take(static_cast<size_t>(1 + L.Y) * 4);
+  L.o_yrel = take(static_cast<size_t>(L.Y) * 4);
+  L.o_small = take(64);
+  L.o_status = take(static_cast<size_t>(N) * 4);
+  L.o_lossn = take(static_cast<size_t>(N) * 8);
+  L.o_part = take(lse_partial_bytes(L.M));
+  L.o_lam = take(static_cast<size_t>(L.M) * 8);
+  L.o_lam2 = take(static_cast<size_t>(L.M) * 8);
+  L.o_S = take(static_cast<size_t>(L.M) * L.ldS * 4);
+  L.o_G = take(static_cast<size_t>(L.M) * L.ldS * 4);
+  L.o_g = take(static_cast<size_t>(L.M) * 4);
+  L.o_dp = take(L.dp.total);
+  L.o_bwd = take(L.bwd.total);
+  L.total = o;
+  return L;
+}
+
+// Host offsets of the utterances: frames, targets, lattice cells.
+static void host_offsets(int N, const int32_t* T, const int32_t* U, std::vector<int32_t>& toff,
+                         std::vector<int32_t>& yoff, std::vector<int64_t>& soff) {
+  toff.assign(N + 1, 0);
+  yoff.assign(N + 1, 0);
+  soff.assign(N + 1, 0);
+  for (int n = 0; n < N; ++n) {
+    toff[n + 1] = toff[n] + T[n];
+    yoff[n + 1] = yoff[n] + U[n];
+    soff[n + 1] = soff[n] + static_cast<int64_t>(T[n]) * (2 * U[n] + 1);
+  }
+}
+
+static hipError_t upload_offsets(const DpPlan& dp, char* dpbase, const std::vector<int32_t>& toff,
+                                 const std::vector<int32_t>& yoff, const std::vector<int64_t>& soff,
+                                 hipStream_t stream) {
+  hipError_t e;
+  e = hipMemcpyAsync(dpbase + dp.off_toff, toff.data(), toff.size() * 4, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return e;
+  e = hipMemcpyAsync(dpbase + dp.off_yoff, yoff.data(), yoff.size() * 4, hipMemcpyHostToDevice, stream);
+  if (e != hipSuccess) return e;
+  return hipMemcpyAsync(dpbase + dp.off_soff, soff.data(), soff.size() * 8, hipMemcpyHostToDevice, stream);
+}
+
+}  // namespace pctc
+
+using namespace pctc;
+
+extern "C" {
+
+size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_lengths, const int32_t* target_lengths,
+                           int32_t D, int32_t V, float beam, int32_t chunk) {
+  if (check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk) != PCTC_OK) return 0;
+  return make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk).total;
+}
+
+const char* pctc_status_string(int32_t status) {
+  switch (status) {
+    case PCTC_OK: return "ok";
+    case PCTC_EINVAL: return "invalid argument";
+    case PCTC_ELABEL: return "target label out of range or equal to blank";
+    case PCTC_ELENGTH: return "frame count < 1 or target length < 0";
+    case PCTC_EWORKSPACE: return "workspace too small";
+    case PCTC_EHIP: return "HIP runtime error";
+    case PCTC_ETOOLONG: return "target longer than the supported maximum";
+    default: return "unknown status";
+  }
+}
+
+const char* pctc_last_error(void) { return g_last_error; }
+
+#define PCTC_HIP(call)                         \
+  do {                                         \
+    hipError_t _e = (call);                    \
+    if (_e != hipSuccess) {                    \
+      set_error(#call, _e);                    \
+      return PCTC_EHIP;                        \
+    }                                          \
+  } while (0)
+
+int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const void* W, int32_t V,
+                           const int32_t* targets, const int32_t* input_lengths, const int32_t* target_lengths,
+                           int32_t N, int32_t blank, float beam, int32_t chunk, double* loss, double* loss_per_utt,
+                           int32_t* utt_status, float* dH, float* dW, void* workspace, size_t workspace_bytes,
+                           void* stream_ptr) {
+  int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (st != PCTC_OK) return st;
+  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
+  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (L.M > 0 && !H) return PCTC_EINVAL;
+  if (L.Y > 0 && !targets) return PCTC_EINVAL;
+  if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  const int dt = (dtype == PCTC_BF16) ? 1 : 0;
+  char* ws = static_cast<char*>(workspace);
+  int32_t* remap = reinterpret_cast<int32_t*>(ws + L.o_remap);
+  int32_t* u_ids = reinterpret_cast<int32_t*>(ws + L.o_uids);
+  int32_t* y_rel = reinterpret_cast<int32_t*>(ws + L.o_yrel);
+  int32_t* Kdev = reinterpret_cast<int32_t*>(ws + L.o_small);
+  int32_t* err = Kdev + 1;
+  int32_t* status = reinterpret_cast<int32_t*>(ws + L.o_status);
+  double* loss_n = reinterpret_cast<double*>(ws + L.o_lossn);
+  float2* partials = reinterpret_cast<float2*>(ws + L.o_part);
+  double* lam = reinterpret_cast<double*>(ws + L.o_lam);
+  float2* lam2 = reinterpret_cast<float2*>(ws + L.o_lam2);
+  float* S = reinterpret_cast<float*>(ws + L.o_S);
+  float* G = reinterpret_cast<float*>(ws + L.o_G);
+  float* g = reinterpret_cast<float*>(ws + L.o_g);
+  char* dps = ws + L.o_dp;
+  char* bws = ws + L.o_bwd;
+
+  std::vector<int32_t> toff, yoff;
+  std::vector<int64_t> soff;
+  host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
+  PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
+  // Algorithm 1: union and relabel
+  PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
+  // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
+  PCTC_HIP(launch_lse(dt, H, L.M, D, W, V, partials, lam, lam2, stream));
+  PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
+  // lattice, total scores, zeroing of nonfinite losses, G = dL/dS
+  PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, loss_n, status, G, g, nullptr,
+                         dps, L.K_max, stream, nullptr));
+  PCTC_HIP(launch_loss_reduce(N, loss_n, status, loss, stream));
+  if (loss_per_utt && N > 0)
+    PCTC_HIP(hipMemcpyAsync(loss_per_utt, loss_n, N * sizeof(double), hipMemcpyDeviceToDevice, stream));
+  if (utt_status && N > 0)
+    PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
+  // backward: chunk by chunk recomputation
+  if (dH || dW)
+    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, V, lam2, G, L.ldS, g, remap, dH, dW, bws, L.bwd, stream));
+  int32_t herr = 0;
+  PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  if (herr) return PCTC_ELABEL;
+  return PCTC_OK;
+}
+
+int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t blank, int32_t V, int32_t* remap,
+                         int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err, void* stream_ptr) {
+  if (V <= 1 || V > PCTC_MAX_VOCAB || blank < 0 || blank >= V || total_targets < 0) return PCTC_EINVAL;
+  if (!remap || !u_ids || !K || !err || (total_targets > 0 && (!targets || !y_rel))) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  PCTC_HIP(launch_union_remap(targets, total_targets, blank, V, remap, u_ids, y_rel, K, err, stream));
+  int32_t herr = 0;
+  PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return herr ? PCTC_ELABEL : PCTC_OK;
+}
+
+size_t pctc_lse_scratch_bytes(int32_t M) {
+  return M < 0 ? 0 : lse_partial_bytes(M) + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(float2), 256);
+}
+
+int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
+                        const int32_t* u_ids, const int32_t* K, int32_t K_max, double* lam, float* S, int32_t ldS,
+                        void* partials, void* stream_ptr) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || V <= 1 || K_max < 1 ||
+      ldS < K_max || !W || !lam || !partials || (M > 0 && !H))
+    return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  const int dt = (dtype == PCTC_BF16) ? 1 : 0;
+  // scratch = [partials][lam2]
+  float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(partials) + lse_partial_bytes(M));
+  PCTC_HIP(launch_lse(dt, H, M, D, W, V, static_cast<float2*>(partials), lam, lam2, stream));
+  if (S && u_ids && K) PCTC_HIP(launch_gather_s(dt, H, M, D, W, u_ids, K, K_max, lam, S, ldS, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
+size_t pctc_dp_scratch_bytes(int32_t N, const int32_t* input_lengths, const int32_t* target_lengths, float beam) {
+  if (N < 0 || (N > 0 && (!input_lengths || !target_lengths))) return 0;
+  for (int n = 0; n < N; ++n)
+    if (input_lengths[n] < 1 || target_lengths[n] < 0 || target_lengths[n] > PCTC_MAX_TARGET) return 0;
+  return plan_dp(N, input_lengths, target_lengths, beam).total;
+}
+
+int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y_rel, const int32_t* input_lengths,
+                    const int32_t* target_lengths, int32_t N, float beam, double* loss_per_utt, int32_t* utt_status,
+                    float* G, float* g, uint8_t* keep_mask, void* dp_scratch, void* stream_ptr) {
+  if (N < 0 || beam != beam || ldS < K_max || K_max < 1) return PCTC_EINVAL;
+  if (N > 0 && (!input_lengths || !target_lengths || !loss_per_utt || !utt_status || !dp_scratch)) return PCTC_EINVAL;
+  for (int n = 0; n < N; ++n) {
+    if (input_lengths[n] < 1 || target_lengths[n] < 0) return PCTC_ELENGTH;
+    if (target_lengths[n] > PCTC_MAX_TARGET) return PCTC_ETOOLONG;
+  }
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  const DpPlan dp = plan_dp(N, input_lengths, target_lengths, beam);
+  if (dp.M > 0 && (!S || !G || !g)) return PCTC_EINVAL;
+  std::vector<int32_t> toff, yoff;
+  std::vector<int64_t> soff;
+  host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
+  char* dps = static_cast<char*>(dp_scratch);
+  PCTC_HIP(upload_offsets(dp, dps, toff, yoff, soff, stream));
+  PCTC_HIP(launch_ctc_dp(dp, input_lengths, target_lengths, S, ldS, y_rel, beam, loss_per_utt, utt_status, G, g,
+                         keep_mask, dps, K_max, stream, nullptr));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || chunk < 0 || (chunk > 0 && chunk % 256))
+    return 0;
+  return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, chunk).total;
+}
+
+int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
+                      const double* lam, const float* G, int32_t ldG, const float* g, const int32_t* remap,
+                      int32_t chunk, float* dH, float* dW, void* bwd_scratch, void* stream_ptr) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || V <= 1 || chunk < 0 ||
+      (chunk > 0 && chunk % 256) || !W || !bwd_scratch)
+    return PCTC_EINVAL;
+  if (M > 0 && (!H || !lam || !G || !g || !remap || ldG < 1)) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  const int dt = (dtype == PCTC_BF16) ? 1 : 0;
+  const BwdPlan plan = plan_bwd(dt, M, D, chunk);
+  float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(bwd_scratch) + plan.dz_bytes + plan.ht_bytes +
+                                           plan.part_bytes);
+  PCTC_HIP(launch_lam2(lam, M, lam2, stream));
+  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, V, lam2, G, ldG, g, remap, dH, dW, bwd_scratch, plan, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
+void pctc_prof_enable(int32_t on) { prof_state().enabled = (on != 0); }
+
+void pctc_prof_reset(void) {
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  s.totals.clear();
+  s.names.clear();
+}
+
+int32_t pctc_prof_count(void) {
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  return static_cast<int32_t>(s.names.size());
+}
+
+int32_t pctc_prof_get(int32_t i, const char** name, double* total_ms, int64_t* launches) {
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  if (i < 0 || i >= static_cast<int32_t>(s.names.size())) return 0;
+  const auto& t = s.totals[s.names[i]];
+  if (name) *name = s.names[i].c_str();
+  if (total_ms) *total_ms = t.first;
+  if (launches) *launches = t.second;
+  return 1;
+}
+
+}  // extern "C"

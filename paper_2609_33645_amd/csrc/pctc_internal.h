@@ -1,0 +1,72 @@
+// Host-side declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "pctc_device.h"
+
+namespace pctc {
+
+// Kernel timing: records a start event on construction and a stop event on destruction
+// when timing is enabled (pctc_prof_enable); resolved at pctc_prof_flush().
+struct Prof {
+  Prof(const char* name, hipStream_t stream);
+  ~Prof();
+  int slot;
+  hipStream_t stream;
+};
+void prof_flush();
+
+constexpr int kDefaultChunk = 16384;
+constexpr float kKeepSlack = 1e-3f;  // nats added to the beam threshold (tie/rounding rule)
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+// ---- union / relabel -------------------------------------------------------------------
+hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t blank, int32_t V,
+                              int32_t* remap, int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err,
+                              hipStream_t stream);
+
+// ---- normaliser and selected log-probabilities ------------------------------------------
+int lse_partitions(int M, int V);
+size_t lse_partial_bytes(int M);
+hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int V, float2* partials,
+                      double* lam, float2* lam2, hipStream_t stream);
+hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const int32_t* u_ids,
+                           const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+                           hipStream_t stream);
+
+// ---- backward ---------------------------------------------------------------------------
+struct BwdPlan {
+  int chunk;       // vocabulary columns per step
+  int splits;      // k-slices of the dH product per chunk
+  int Mp;          // padded frame count (pitch of the transposed head input)
+  size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, total;
+};
+BwdPlan plan_bwd(int dtype, int M, int D, int chunk);
+hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
+                           const float* G, int ldG, const float* g, const int32_t* remap, float* dH,
+                           float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream);
+hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
+
+// ---- alignment lattice ------------------------------------------------------------------
+struct DpPlan {
+  int N, M, Y, Smax;
+  bool pruned;
+  int64_t lattice;  // sum_n T_n (2U_n+1)
+  size_t off_toff, off_yoff, off_soff, off_frame_utt, off_dup_next, off_dup_first, off_logp,
+      off_tab_fa, off_tab_fb, off_tab_va, off_tab_vb, off_sc_fa, off_sc_fb, off_sc_va, off_sc_vb,
+      off_vbest, off_mask, total;
+};
+DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam);
+// Uploads the host offsets into the scratch (async) and runs the whole lattice stage.
+hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
+                         const int32_t* y_rel, float beam, double* loss_n, int32_t* status, float* G,
+                         float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
+                         void* host_staging);
+hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, double* loss,
+                              hipStream_t stream);
+
+}  // namespace pctc

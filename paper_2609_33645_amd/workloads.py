@@ -201,11 +201,14 @@ def random_small(seed: int, *, N: int, T_range=(1, 40), D: int = 32, V: int = 20
                       w_std=w_std)
 
 
-def random_scores(seed: int, M: int, K: int, scale: float = 3.0) -> np.ndarray:
+def random_scores(seed: int, M: int, K: int, scale: float = 3.0, integer: bool = False) -> np.ndarray:
     """Seeded per-frame class scores [M, K] (float32) for stand-alone tests of the
     alignment recursion: non-positive values -Exp(scale), with every 7th row shifted
-    by a seeded offset so that rows do not share a common level."""
+    by a seeded offset so that rows do not share a common level.  integer=True rounds
+    every score to an integer (sums of scores are then exact in float32)."""
     rng = np.random.default_rng(seed)
     s = -rng.exponential(scale, size=(M, K))
     s[::7] -= rng.uniform(0.0, 20.0, size=(s[::7].shape[0], 1))
+    if integer:
+        s = np.round(s)
     return s.astype(np.float32)

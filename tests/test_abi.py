@@ -1,0 +1,58 @@
+"""The C-ABI library loads and exports every function include/prunedctc.h declares
+(no compute calls: runs without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "prunedctc.h")
+LIB = os.path.join(ROOT, "paper_2609_33645_amd", "libprunedctc.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"^\s*(?:const\s+)?[A-Za-z_][\w\s\*]*?\b([a-z_][a-z0-9_]*)\s*\(", text, flags=re.M)
+    return sorted(set(n for n in names if n.startswith(("pctc_", "pruned_ctc"))))
+
+
+def test_header_declares_entry_points():
+    names = declared_functions()
+    for must in ["pruned_ctc_fwd_bwd", "pctc_workspace_size", "pctc_union_remap", "pctc_lse_select", "pctc_ctc_dp",
+                 "pctc_head_bwd", "pctc_status_string", "pctc_prof_enable"]:
+        assert must in names
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_library_exports_every_declared_symbol():
+    import torch  # noqa: F401  (binds the library to torch's HIP runtime)
+    lib = ctypes.CDLL(LIB)
+    missing = [n for n in declared_functions() if not hasattr(lib, n)]
+    assert not missing, missing
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_host_side_validation_without_gpu():
+    """Argument checks and workspace sizing are host code: they run without a device."""
+    import numpy as np
+    import torch  # noqa: F401
+    lib = ctypes.CDLL(LIB)
+    lib.pctc_workspace_size.restype = ctypes.c_size_t
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.pctc_workspace_size.argtypes = [ctypes.c_int32, ctypes.c_int32, i32p, i32p, ctypes.c_int32, ctypes.c_int32,
+                                        ctypes.c_float, ctypes.c_int32]
+    T = np.array([300, 200], np.int32)
+    U = np.array([50, 40], np.int32)
+    p = lambda a: a.ctypes.data_as(i32p)  # noqa: E731
+    ws = [lib.pctc_workspace_size(1, 2, p(T), p(U), 512, V, 16.0, 0) for V in (10_000, 100_000, 180_000)]
+    assert all(w > 0 for w in ws)
+    # only the V-entry remap table grows with V (4 bytes per class, 256-byte aligned)
+    assert ws[2] - ws[0] <= 4 * (180_000 - 10_000) + 256
+    assert lib.pctc_workspace_size(1, 2, p(T), p(U), 500, 1000, 16.0, 0) == 0      # D % 8 != 0
+    assert lib.pctc_workspace_size(1, 2, p(T), p(U), 512, 1000, float("nan"), 0) == 0
+    U2 = np.array([50, 2000], np.int32)
+    assert lib.pctc_workspace_size(1, 2, p(T), p(U2), 512, 1000, 16.0, 0) == 0   # target too long
+    lib.pctc_status_string.restype = ctypes.c_char_p
+    assert lib.pctc_status_string(-2).decode().startswith("target label")

@@ -398,3 +398,20 @@ def test_scores_stage_matches_full_path():
     st = oracle.ctc_from_scores(full["S"], full["y_rel"], wl.input_lengths, wl.target_lengths, beam=3.0)
     np.testing.assert_allclose(st["loss_n"], full["loss_n"], atol=1e-10)
     np.testing.assert_allclose(st["G"], full["G"], atol=1e-12)
+
+
+def test_head_backward_stage_matches_full_path():
+    """Eq. vjp with the alignment stage's G and g reproduces the full-vocabulary gradient
+    (Algorithm 1 backward equals Eq. grad-full when G = -gamma, App. B.1)."""
+    from paper_2609_33645_amd import workloads
+    wl = workloads.random_small(14, N=4, T_range=(5, 30), D=12, V=150, dtype="f32", p_repeat=0.2)
+    wl.input_lengths[1] = 1
+    wl.target_lengths[1] = 3          # excluded utterance
+    wl.H = wl.H[:int(wl.input_lengths.sum())]
+    U = wl.target_lengths
+    wl.targets = np.resize(wl.targets, int(U.sum())) % 140 + 1
+    full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, U, 0, beam=4.0, chunk=32)
+    st = oracle.head_backward(wl.H, wl.W, full["lam"], full["G"], full["g"], full["u_ids"], chunk=50)
+    np.testing.assert_allclose(st["dH"], full["dH"], atol=1e-12)
+    np.testing.assert_allclose(st["dW"], full["dW"], atol=1e-12)
+    assert full["status"][1] == oracle.STATUS_NOT_ALIGNABLE
