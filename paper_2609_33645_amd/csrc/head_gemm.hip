@@ -189,21 +189,20 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int
   const int vper = ((vtiles + P - 1) / P) * kFwdBR;
   const int Peff = (V + vper - 1) / vper;
   const int nMt = (M + kFwdBC - 1) / kFwdBC;
-  {
+  int Pfin = Peff;
+  if (dtype == 1) {
+    hipError_t e1 = launch_lse_partial_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V,
+                                            partials, &Pfin, stream);
+    if (e1 != hipSuccess) return e1;
+  } else {
     Prof pr("lse_partial", stream);
-    if (dtype == 1)
-      hipLaunchKernelGGL(lse_partial_kernel<uint16_t>, dim3(nMt * Peff), dim3(256), 0, stream,
-                         static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, Peff, vper,
-                         partials);
-    else
-      hipLaunchKernelGGL(lse_partial_kernel<float>, dim3(nMt * Peff), dim3(256), 0, stream,
-                         static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, Peff, vper,
-                         partials);
+    hipLaunchKernelGGL(lse_partial_kernel<float>, dim3(nMt * Peff), dim3(256), 0, stream,
+                       static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, Peff, vper, partials);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   Prof pr("lse_finalize", stream);
-  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Peff, lam,
+  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Pfin, lam,
                      lam2);
   return hipGetLastError();
 }
@@ -252,16 +251,14 @@ hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W
                            const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream) {
   if (M <= 0) return hipSuccess;
+  if (dtype == 1)
+    return launch_gather_s_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), u_ids, K, K_max,
+                                lam, S, ldS, stream);
   const int nMt = (M + kFwdBC - 1) / kFwdBC;
   const int nJt = (K_max + kFwdBR - 1) / kFwdBR;
   Prof pr("gather_s", stream);
-  if (dtype == 1)
-    hipLaunchKernelGGL(gather_s_kernel<uint16_t>, dim3(nMt * nJt), dim3(256), 0, stream,
-                       static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), u_ids, K, K_max, lam,
-                       S, ldS);
-  else
-    hipLaunchKernelGGL(gather_s_kernel<float>, dim3(nMt * nJt), dim3(256), 0, stream, static_cast<const float*>(H),
-                       M, D, static_cast<const float*>(W), u_ids, K, K_max, lam, S, ldS);
+  hipLaunchKernelGGL(gather_s_kernel<float>, dim3(nMt * nJt), dim3(256), 0, stream, static_cast<const float*>(H), M, D,
+                     static_cast<const float*>(W), u_ids, K, K_max, lam, S, ldS);
   return hipGetLastError();
 }
 
@@ -450,10 +447,23 @@ __global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int
 
 BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
   BwdPlan p{};
-  p.chunk = (chunk > 0) ? chunk : kDefaultChunk;
+  if (chunk > 0) {
+    p.chunk = chunk;
+  } else {
+    // default: the recomputed gradient chunk (M x chunk in the input dtype) takes about
+    // 256 MiB, in whole multiples of 4096 columns, between 4096 and 65536 columns
+    const size_t es0 = (dtype == 1) ? 2 : 4;
+    size_t c = (static_cast<size_t>(256) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
+    c = (c / 4096) * 4096;
+    if (c < 4096) c = 4096;
+    if (c > 65536) c = 65536;
+    p.chunk = static_cast<int>(c);
+  }
   const size_t es = (dtype == 1) ? 2 : 4;
-  const int tiles = ((M + kBwdB - 1) / kBwdB) * ((D + kBwdB - 1) / kBwdB);
-  int splits = (1024 + tiles - 1) / tiles;
+  const int tr = (dtype == 1) ? 256 : kBwdB;  // dH tile rows of the kernel used
+  const int tc = (dtype == 1) ? 128 : kBwdB;
+  const int tiles = ((M + tr - 1) / tr) * ((D + tc - 1) / tc);
+  int splits = (512 + tiles - 1) / tiles;
   const int maxs = p.chunk / 256;
   if (splits > maxs) splits = maxs;
   if (splits > 8) splits = 8;
@@ -461,7 +471,7 @@ BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
   p.splits = splits;
   p.Mp = ((M + 63) / 64) * 64;
   p.dz_bytes = align_up(static_cast<size_t>(M) * p.chunk * es, 256);
-  p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);
+  p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);  // >= M x D (bf16 masked copy of H)
   p.part_bytes = align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
   p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
   p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes;
@@ -520,6 +530,38 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const 
   return hipGetLastError();
 }
 
+static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, const float2* lam2,
+                                const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
+                                char* scratch, const BwdPlan& plan, hipStream_t stream) {
+  uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
+  uint16_t* Hs = reinterpret_cast<uint16_t*>(scratch + plan.dz_bytes);
+  float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
+  const int chunk = plan.chunk;
+  hipError_t e;
+  if (dW) {
+    e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
+    if (e != hipSuccess) return e;
+  }
+  const int slice = ((chunk / plan.splits + 63) / 64) * 64;
+  if (dH) {
+    e = hipMemsetAsync(part, 0, static_cast<size_t>(plan.splits) * M * D * sizeof(float), stream);
+    if (e != hipSuccess) return e;
+  }
+  for (int c0 = 0; c0 < V; c0 += chunk) {
+    const int cw = min(chunk, V - c0);
+    e = launch_bwd_chunk_bf16(H, Hs, M, D, W, c0, cw, lam2, G, ldG, g, remap, dZ, chunk, part, slice, dH != nullptr,
+                              dW != nullptr, dW, stream);
+    if (e != hipSuccess) return e;
+  }
+  if (dH) {
+    const int64_t n = static_cast<int64_t>(M) * D;
+    Prof pr("dh_reduce", stream);
+    hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
+                       plan.splits, n, dH);
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
                            const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
                            void* scratch, const BwdPlan& plan, hipStream_t stream) {
@@ -529,8 +571,8 @@ hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W
   }
   char* sc = static_cast<char*>(scratch);
   if (dtype == 1)
-    return head_bwd_t<uint16_t>(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, lam2, G,
-                                ldG, g, remap, dH, dW, sc, plan, stream);
+    return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, lam2, G, ldG, g,
+                         remap, dH, dW, sc, plan, stream);
   return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, lam2, G, ldG, g,
                            remap, dH, dW, sc, plan, stream);
 }

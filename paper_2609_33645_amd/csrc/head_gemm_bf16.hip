@@ -1,0 +1,436 @@
+// bf16 vocabulary-head products of Pruned CTC on the direct-to-LDS matrix-core engine
+// (gemm_bf16.h).  Same computations as the generic kernels in head_gemm.hip:
+//  * lse_partial: Z^T tile = W H^T with the online log-sum-exp epilogue (Eq. lognorm;
+//    Algorithm 1 online log-sum-exp over vocabulary chunks);
+//  * gather_s:    S = Z[:, U] - lambda, subtraction in double, one rounding to float
+//    (Algorithm 1; App. B.1 "Forward computation");
+//  * recompute_dz: dZ = scatter_U(G) - g p for one vocabulary chunk (Eq. vjp);
+//  * dh_gemm: dH partial += dZ W_c;  dw_gemm: dW_c = dZ^T H  (App. A, Step 3).
+// Layouts in LDS follow global memory: W and H rows and dZ rows are K-contiguous for the
+// forward/recompute/dH-left operands; W (for dH) and dZ, H (for dW) are consumed
+// transposed through the LDS transpose read.
+#include "gemm_bf16.h"
+#include "pctc_internal.h"
+
+namespace pctc {
+
+using bf::GOp;
+using bf::LL;
+
+namespace {
+
+constexpr int kFR = 256;  // vocabulary rows per forward/recompute tile
+constexpr int kFC = 128;  // frames per forward/recompute tile
+constexpr int kFK = 32;   // k per stage
+constexpr int kNS = 3;    // LDS stages
+constexpr int kBR = 256;  // backward tile rows (dH: frames, dW: vocabulary)
+constexpr int kBC = 128;  // backward tile columns (D)
+
+using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, kNS>;
+using GDh = bf::Gemm<kBR, kBC, kFK, LL::KC, LL::MC, kNS>;
+using GDw = bf::Gemm<kBR, kBC, kFK, LL::MC, LL::MC, kNS>;
+
+#define PCTC_STAGES(G)                                                   \
+  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st2_[G::kStageBytes]; \
+  char* const st[3] = {st0_, st1_, st2_};
+
+__device__ __forceinline__ int xcd_swz(int bid, int nblocks) {
+  const int full = (nblocks / 8) * 8;
+  if (bid >= full) return bid;
+  return (bid % 8) * (full / 8) + bid / 8;
+}
+
+// Tile order for an nA x nB grid of output tiles: consecutive work ids walk 8 x 8 groups
+// (a fastest), so the workgroups resident on one XCD at a time share a few rows of A
+// tiles and B tiles in that XCD's L2.  Grid = groupsA * groupsB * 64; ids past the
+// edge return false.
+constexpr int kGrp = 8;
+__host__ __device__ __forceinline__ int grouped_grid(int nA, int nB) {
+  return ((nA + kGrp - 1) / kGrp) * ((nB + kGrp - 1) / kGrp) * kGrp * kGrp;
+}
+__device__ __forceinline__ bool grouped_tile(int work, int nA, int nB, int& a, int& b) {
+  const int gA = (nA + kGrp - 1) / kGrp;
+  const int blk = work / (kGrp * kGrp), in = work % (kGrp * kGrp);
+  a = (blk % gA) * kGrp + in % kGrp;
+  b = (blk / gA) * kGrp + in / kGrp;
+  return a < nA && b < nB;
+}
+
+// Online log-sum-exp update of the running (max, sum) of this lane's frames with one
+// tile; rows at or past vend are skipped when MASK.
+template <bool MASK, int FR, int FC>
+__device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], float (&run_max)[FC], float (&run_sum)[FC],
+                                                int v0, int vend, int wave, int lane) {
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    float tmax = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float x = acc[i][j][r];
+        if (MASK) {
+          if (v0 + GFwd::row_of(wave, lane, i, r) < vend) tmax = fmaxf(tmax, x);
+        } else {
+          tmax = fmaxf(tmax, x);
+        }
+      }
+    tmax = fmaxf(tmax, swap_halves(tmax));
+    const float nmax = fmaxf(run_max[j], tmax);
+    const float ms = nmax * kLog2e;
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float e = fast_exp2(fmaf(acc[i][j][r], kLog2e, -ms));
+        if (MASK) {
+          if (v0 + GFwd::row_of(wave, lane, i, r) < vend) s += e;
+        } else {
+          s += e;
+        }
+      }
+    s += swap_halves(s);
+    const float scale = (run_max[j] == -INFINITY) ? 0.f : fast_exp2((run_max[j] - nmax) * kLog2e);
+    run_sum[j] = fmaf(run_sum[j], scale, s);
+    run_max[j] = nmax;
+  }
+}
+
+}  // namespace
+
+__global__ void __launch_bounds__(256, 2)
+lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int V, int P,
+                 int vper, float2* __restrict__ partials) {
+  using G = GFwd;
+  constexpr int FR = G::FR, FC = G::FC;
+  PCTC_STAGES(G)
+  const int nMt = (M + kFC - 1) / kFC;
+  int mt, p;
+  if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) return;
+  const int m0 = mt * kFC;
+  const int vbeg = p * vper;
+  const int vend = min(V, vbeg + vper);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const GOp A{W, D, vend, D, nullptr};
+  const GOp B{H, D, M, D, nullptr};
+  float run_max[FC], run_sum[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    run_max[j] = -INFINITY;
+    run_sum[j] = 0.f;
+  }
+  f32x16 acc[FR][FC];
+  for (int v0 = vbeg; v0 < vend; v0 += kFR) {
+    G::run(A, B, v0, m0, 0, D, st, acc);
+    if (v0 + kFR <= vend)
+      lse_tile_update<false, FR, FC>(acc, run_max, run_sum, v0, vend, wave, lane);
+    else
+      lse_tile_update<true, FR, FC>(acc, run_max, run_sum, v0, vend, wave, lane);
+  }
+  __syncthreads();
+  float2* xch = reinterpret_cast<float2*>(st0_);
+  const int rowhalf = wave >> 1, colhalf = wave & 1;
+  if (rowhalf == 1 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) xch[colhalf * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
+  }
+  __syncthreads();
+  if (rowhalf == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const float2 o = xch[colhalf * (FC * 32) + j * 32 + lane];
+      const float nmax = fmaxf(run_max[j], o.x);
+      float s = 0.f;
+      if (run_max[j] != -INFINITY) s += run_sum[j] * fast_exp2((run_max[j] - nmax) * kLog2e);
+      if (o.x != -INFINITY) s += o.y * fast_exp2((o.x - nmax) * kLog2e);
+      if (nmax != nmax) s = nmax;
+      const int m = m0 + GFwd::col_of(wave, lane, j);
+      if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(nmax, s);
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256, 2)
+gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
+              const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev, const double* __restrict__ lam,
+              float* __restrict__ S, int ldS) {
+  using G = GFwd;
+  constexpr int FR = G::FR, FC = G::FC;
+  PCTC_STAGES(G)
+  const int nMt = (M + kFC - 1) / kFC;
+  const int mt = blockIdx.x % nMt;
+  const int jt = blockIdx.x / nMt;
+  const int K = *Kdev;
+  const int j0 = jt * kFR;
+  if (j0 >= K) return;
+  const int m0 = mt * kFC;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const GOp A{W, D, K, D, u_ids};
+  const GOp B{H, D, M, D, nullptr};
+  f32x16 acc[FR][FC];
+  G::run(A, B, j0, m0, 0, D, st, acc);
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const int m = m0 + GFwd::col_of(wave, lane, j);
+    if (m >= M) continue;
+    const double l = lam[m];
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int jj = j0 + GFwd::row_of(wave, lane, i, r);
+        if (jj < K) S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(static_cast<double>(acc[i][j][r]) - l);
+      }
+  }
+}
+
+// dZ chunk [M][chunk] (row pitch `chunk`): columns [0, cw) hold scatter_U(G) - g p for
+// vocabulary ids c0.., columns [cw, tile end) hold 0.  Each 256 x 128 tile is staged through
+// LDS so that every frame row is stored as contiguous 16-byte vectors.
+template <bool FULL>
+__device__ __forceinline__ void dz_values_(const f32x16 (&acc)[GFwd::FR][GFwd::FC], int j, int i, int q, float gm,
+                                          float2 l2, bool inc, int vl0, int cw, int any_sel, const int* sel,
+                                          const float* Grow, int wave, int lane, uint32_t (&o)[2]) {
+  const int rl0 = GFwd::row_of(wave, lane, i, 4 * q);
+  float val[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int rl = rl0 + e;
+    float v = 0.f;
+    if (inc && (FULL || vl0 + rl < cw)) {
+      const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -l2.x) - l2.y;
+      v = -gm * fast_exp2(t);
+      if (any_sel) {
+        const int jj = sel[rl];
+        if (jj >= 0) v += Grow[jj];
+      }
+    }
+    val[e] = v;
+  }
+  o[0] = static_cast<uint32_t>(f32_to_bf16(val[0])) | (static_cast<uint32_t>(f32_to_bf16(val[1])) << 16);
+  o[1] = static_cast<uint32_t>(f32_to_bf16(val[2])) | (static_cast<uint32_t>(f32_to_bf16(val[3])) << 16);
+}
+
+__global__ void __launch_bounds__(256, 2)
+recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
+                  const float2* __restrict__ lam2, const float* __restrict__ G, int ldG, const float* __restrict__ g,
+                  const int32_t* __restrict__ remap, uint16_t* __restrict__ dZ, int chunk) {
+  using GG = GFwd;
+  constexpr int FR = GG::FR, FC = GG::FC;
+  constexpr int kPitch = kFR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
+  static_assert(32 * kPitch <= GG::kStageBytes, "staging fits one stage");
+  PCTC_STAGES(GG)
+  __shared__ int sel[kFR];
+  const int nMt = (M + kFC - 1) / kFC;
+  const int nVt = (cw + kFR - 1) / kFR;
+  int mt, vt;
+  if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, nVt, mt, vt)) return;
+  const int m0 = mt * kFC;
+  const int vl0 = vt * kFR;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  {
+    const int vl = vl0 + tid;
+    sel[tid] = (vl < cw) ? remap[c0 + vl] : -1;
+  }
+  const int any_sel = __syncthreads_or(sel[tid] >= 0);
+  const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
+  const GOp B{H, D, M, D, nullptr};
+  f32x16 acc[FR][FC];
+  GG::run(A, B, vl0, m0, 0, D, st, acc);
+  const bool full = vl0 + kFR <= cw;
+  const int ch = wave & 1;          // column half: frames [64 ch, 64 ch + 64) of the tile
+  char* stage = ch ? st1_ : st0_;   // 32 frames x 256 vocabulary columns per pass
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    __syncthreads();  // previous pass's readers (and the product's last reads) are done
+    const int mloc = 64 * ch + 32 * j + (lane & 31);
+    const int m = m0 + mloc;
+    const bool mok = m < M;
+    const float gm = mok ? g[m] : 0.f;
+    const float2 l2 = mok ? lam2[m] : make_float2(0.f, 0.f);
+    const bool inc = mok && (gm != 0.f);
+    const float* Grow = G + static_cast<int64_t>(mok ? m : 0) * ldG;
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        uint32_t o[2];
+        if (full)
+          dz_values_<true>(acc, j, i, q, gm, l2, inc, vl0, cw, any_sel, sel, Grow, wave, lane, o);
+        else
+          dz_values_<false>(acc, j, i, q, gm, l2, inc, vl0, cw, any_sel, sel, Grow, wave, lane, o);
+        const int rl0 = GFwd::row_of(wave, lane, i, 4 * q);
+        *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) = u32x2{o[0], o[1]};
+      }
+    __syncthreads();
+    // 2 stages x 32 frames x 32 vectors of 16 bytes
+#pragma unroll
+    for (int k = 0; k < 8; ++k) {
+      const int idx = tid + 256 * k;
+      const int half = idx >> 10;             // which stage (column half)
+      const int row = (idx >> 5) & 31;        // frame within the pass
+      const int vec = idx & 31;               // 16-byte vector within the 256-column row
+      const int mm = m0 + 64 * half + 32 * j + row;
+      const char* src = (half ? st1_ : st0_) + row * kPitch + vec * 16;
+      const u32x4 v = *reinterpret_cast<const u32x4*>(src);
+      if (mm < M) *reinterpret_cast<u32x4*>(dZ + static_cast<int64_t>(mm) * chunk + vl0 + vec * 8) = v;
+    }
+  }
+}
+
+__global__ void __launch_bounds__(256, 2)
+dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
+             int slice, float* __restrict__ part) {
+  using G = GDh;
+  constexpr int FR = G::FR, FC = G::FC;
+  PCTC_STAGES(G)
+  const int nMt = (M + kBR - 1) / kBR;
+  const int nDt = (D + kBC - 1) / kBC;
+  // d-tiles fastest: the workgroups that read the same dZ rows run together on one XCD
+  const int work = xcd_swz(blockIdx.x, gridDim.x);
+  const int dt = work % nDt;
+  const int mt = (work / nDt) % nMt;
+  const int s = work / (nMt * nDt);
+  const int m0 = mt * kBR, d0 = dt * kBC;
+  const int kb = s * slice;
+  const int ke = min(cw, kb + slice);
+  if (kb >= ke) return;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // A: dZ rows (frames), k = vocabulary column; B: W_c viewed as rows d, k = vocabulary row
+  const GOp A{dZ, chunk, M, cw, nullptr};
+  const GOp B{W + static_cast<int64_t>(c0) * D, D, D, cw, nullptr};
+  f32x16 acc[FR][FC];
+  G::run(A, B, m0, d0, kb, ke, st, acc);
+  float* dst = part + static_cast<int64_t>(s) * M * D;
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int d = d0 + G::col_of(wave, lane, j);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + G::row_of(wave, lane, i, r);
+        if (m < M) dst[static_cast<int64_t>(m) * D + d] += acc[i][j][r];
+      }
+    }
+}
+
+__global__ void __launch_bounds__(256, 2)
+dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ Hs, int D, int c0, int cw,
+             float* __restrict__ dW) {
+  using G = GDw;
+  constexpr int FR = G::FR, FC = G::FC;
+  PCTC_STAGES(G)
+  const int nDt = (D + kBC - 1) / kBC;
+  const int work = xcd_swz(blockIdx.x, gridDim.x);
+  const int dt = work % nDt;
+  const int vt = work / nDt;
+  const int v0 = vt * kBR, d0 = dt * kBC;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  // A: dZ viewed as rows v (columns of dZ), k = frame; B: Hs viewed as rows d, k = frame
+  const GOp A{dZ, chunk, cw, M, nullptr};
+  const GOp B{Hs, D, D, M, nullptr};
+  f32x16 acc[FR][FC];
+  G::run(A, B, v0, d0, 0, M, st, acc);
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int d = d0 + G::col_of(wave, lane, j);
+      if (d >= D) continue;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int v = v0 + G::row_of(wave, lane, i, r);
+        if (v < cw) dW[static_cast<int64_t>(c0 + v) * D + d] = acc[i][j][r];
+      }
+    }
+}
+
+// Hs = H with the rows of excluded frames (g[m] == 0) set to zero.
+__global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, const float* __restrict__ g,
+                              uint16_t* __restrict__ Hs) {
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 8;
+  if (i >= n) return;
+  const int m = static_cast<int>(i / D);
+  u32x4 v = *reinterpret_cast<const u32x4*>(H + i);
+  if (g[m] == 0.f) v = u32x4{0u, 0u, 0u, 0u};
+  *reinterpret_cast<u32x4*>(Hs + i) = v;
+}
+
+// ---------------------------------------------------------------------------------------
+// launchers (bf16 path)
+// ---------------------------------------------------------------------------------------
+
+int lse_partitions_bf16(int M, int V) {
+  const int nMt = (M + kFC - 1) / kFC;
+  int P = (2048 + nMt - 1) / nMt;
+  const int vtiles = (V + kFR - 1) / kFR;
+  if (P > vtiles) P = vtiles;
+  if (P > 256) P = 256;
+  if (P < 1) P = 1;
+  return P;
+}
+
+hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
+                                   int* P_out, hipStream_t stream) {
+  const int P = lse_partitions_bf16(M, V);
+  const int vtiles = (V + kFR - 1) / kFR;
+  const int vper = ((vtiles + P - 1) / P) * kFR;
+  const int Peff = (V + vper - 1) / vper;
+  const int nMt = (M + kFC - 1) / kFC;
+  *P_out = Peff;
+  Prof pr("lse_partial", stream);
+  hipLaunchKernelGGL(lse_partial_bf16, dim3(grouped_grid(nMt, Peff)), dim3(256), 0, stream, H, M, D, W, V, Peff, vper,
+                     partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const int32_t* u_ids,
+                                const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+                                hipStream_t stream) {
+  const int nMt = (M + kFC - 1) / kFC;
+  const int nJt = (K_max + kFR - 1) / kFR;
+  Prof pr("gather_s", stream);
+  hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(256), 0, stream, H, M, D, W, u_ids, K, lam, S, ldS);
+  return hipGetLastError();
+}
+
+hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
+                                 int cw, const float2* lam2, const float* G, int ldG, const float* g,
+                                 const int32_t* remap, uint16_t* dZ, int chunk, float* part, int slice, bool want_dH,
+                                 bool want_dW, float* dW, hipStream_t stream) {
+  const int nMt = (M + kFC - 1) / kFC;
+  const int nVt = (cw + kFR - 1) / kFR;
+  {
+    Prof pr("recompute_dz", stream);
+    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(256), 0, stream, H, M, D, W, c0, cw, lam2,
+                       G, ldG, g, remap, dZ, chunk);
+  }
+  if (want_dH) {
+    const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    const int ns = (cw + slice - 1) / slice;
+    Prof pr("dh_gemm", stream);
+    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles * ns), dim3(256), 0, stream, dZ, M, chunk, W, D, c0, cw, slice, part);
+  }
+  if (want_dW) {
+    const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    Prof pr("dw_gemm", stream);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(256), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream) {
+  const int64_t n = static_cast<int64_t>(M) * D;
+  const int64_t threads = (n + 7) / 8;
+  Prof pr("hs_build", stream);
+  hipLaunchKernelGGL(hs_build_bf16, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream, H, n,
+                     D, g, Hs);
+  return hipGetLastError();
+}
+
+}  // namespace pctc

@@ -51,6 +51,17 @@ hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W
                            float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream);
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
 
+// ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
+hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
+                                   int* P_out, hipStream_t stream);
+hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const int32_t* u_ids,
+                                const int32_t* K, int K_max, const double* lam, float* S, int ldS, hipStream_t stream);
+hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
+                                 int cw, const float2* lam2, const float* G, int ldG, const float* g,
+                                 const int32_t* remap, uint16_t* dZ, int chunk, float* part, int slice, bool want_dH,
+                                 bool want_dW, float* dW, hipStream_t stream);
+hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
+
 // ---- alignment lattice ------------------------------------------------------------------
 struct DpPlan {
   int N, M, Y, Smax;
