@@ -118,29 +118,47 @@ __global__ void dp_prep_kernel(const int32_t* __restrict__ toff, const int32_t* 
 
 // ---------------------------------------------------------------------------------------
 
-__device__ __forceinline__ float lane_up(float x, int lane) {  // value of lane-1 (kNeg at lane 0)
-  float v = __shfl_up(x, 1, 64);
-  return lane == 0 ? kNeg : v;
+// Cross-lane moves with DPP (VALU, no LDS round trip).
+// wave_shr:1 -> lane l receives lane l-1 (lane 0 keeps `old`); wave_shl:1 -> lane l
+// receives lane l+1 (lane 63 keeps `old`).
+__device__ __forceinline__ int dpp_up_i(int x, int old) { return __builtin_amdgcn_update_dpp(old, x, 0x138, 0xf, 0xf, false); }
+__device__ __forceinline__ int dpp_dn_i(int x, int old) { return __builtin_amdgcn_update_dpp(old, x, 0x130, 0xf, 0xf, false); }
+__device__ __forceinline__ float lane_up(float x) { return __int_as_float(dpp_up_i(__float_as_int(x), __float_as_int(kNeg))); }
+__device__ __forceinline__ float lane_down(float x) { return __int_as_float(dpp_dn_i(__float_as_int(x), __float_as_int(kNeg))); }
+__device__ __forceinline__ double lane_up(double x) {
+  const long long b = __double_as_longlong(x);
+  const long long nb = __double_as_longlong(static_cast<double>(kNeg));
+  const int lo = dpp_up_i(static_cast<int>(b), static_cast<int>(nb));
+  const int hi = dpp_up_i(static_cast<int>(b >> 32), static_cast<int>(nb >> 32));
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
 }
-__device__ __forceinline__ float lane_down(float x, int lane) {  // value of lane+1 (kNeg at lane 63)
-  float v = __shfl_down(x, 1, 64);
-  return lane == 63 ? kNeg : v;
+__device__ __forceinline__ double lane_down(double x) {
+  const long long b = __double_as_longlong(x);
+  const long long nb = __double_as_longlong(static_cast<double>(kNeg));
+  const int lo = dpp_dn_i(static_cast<int>(b), static_cast<int>(nb));
+  const int hi = dpp_dn_i(static_cast<int>(b >> 32), static_cast<int>(nb >> 32));
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
 }
-__device__ __forceinline__ double lane_up(double x, int lane) {
-  double v = __shfl_up(x, 1, 64);
-  return lane == 0 ? static_cast<double>(kNeg) : v;
+__device__ __forceinline__ int lane_up_i(int x) { return dpp_up_i(x, 0); }
+__device__ __forceinline__ int lane_down_i(int x) { return dpp_dn_i(x, 0); }
+
+// Maximum over the wavefront: DPP reductions within each row of 16 lanes, then the four
+// row results read as scalars.
+template <int CTRL>
+__device__ __forceinline__ float dpp_max_step(float v) {
+  return fmaxf(v, __int_as_float(__builtin_amdgcn_update_dpp(__float_as_int(v), __float_as_int(v), CTRL, 0xf, 0xf,
+                                                               false)));
 }
-__device__ __forceinline__ double lane_down(double x, int lane) {
-  double v = __shfl_down(x, 1, 64);
-  return lane == 63 ? static_cast<double>(kNeg) : v;
-}
-__device__ __forceinline__ int lane_up_i(int x, int lane) {
-  int v = __shfl_up(x, 1, 64);
-  return lane == 0 ? 0 : v;
-}
-__device__ __forceinline__ int lane_down_i(int x, int lane) {
-  int v = __shfl_down(x, 1, 64);
-  return lane == 63 ? 0 : v;
+__device__ __forceinline__ float wave_max_dpp(float x) {
+  x = dpp_max_step<0xB1>(x);   // quad_perm [1,0,3,2]
+  x = dpp_max_step<0x4E>(x);   // quad_perm [2,3,0,1]
+  x = dpp_max_step<0x141>(x);  // row_half_mirror
+  x = dpp_max_step<0x140>(x);  // row_mirror
+  const float a = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 0));
+  const float b = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 16));
+  const float c = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 32));
+  const float d = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(x), 48));
+  return fmaxf(fmaxf(a, b), fmaxf(c, d));
 }
 
 // Max (Viterbi) or log-sum-exp (natural log) of three scores.  The log-sum-exp keeps
@@ -158,11 +176,18 @@ __device__ __forceinline__ Acc comb3(Acc a, Acc b, Acc c) {
   }
 }
 
+// Frames of emissions (and arc flags) loaded ahead of the recursion.
+template <int Q>
+constexpr int prefetch_depth() {
+  return Q <= 3 ? 8 : (Q <= 4 ? 6 : (Q <= 6 ? 4 : (Q <= 8 ? 3 : 2)));
+}
+
 // One wavefront per (utterance, direction), natural-log units.  VIT: Viterbi (max-plus)
 // accumulated in float; otherwise the total score (log-sum-exp) accumulated in double,
 // so the per-frame additions do not round at the magnitude of the emission scores.
 // Tables hold scores minus a per-frame offset (rounded to float once); the offsets are
-// kept per frame in double.
+// kept per frame in double.  Emissions and arc flags for the next PF frames are held in
+// a register ring so that the gathers are issued well before they are needed.
 template <int Q, bool VIT>
 __global__ void __launch_bounds__(64)
 dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
@@ -170,6 +195,8 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
                int32_t* __restrict__ status, const uint8_t* __restrict__ mask, float* __restrict__ tab_f,
                float* __restrict__ tab_b, double* __restrict__ sc_f, double* __restrict__ sc_b,
                double* __restrict__ total_out, double* __restrict__ loss_n) {
+  using Acc = typename std::conditional<VIT, float, double>::type;
+  constexpr int PF = prefetch_depth<Q>();
   const int n = blockIdx.x;
   const int dir = blockIdx.y;
   const int lane = threadIdx.x;
@@ -178,8 +205,8 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
   const int y0 = yoff[n], U = yoff[n + 1] - y0;
   const int Sp = 2 * U + 1;
   const int64_t base = soff[n];
-  using Acc = typename std::conditional<VIT, float, double>::type;
   const int* y = y_rel + y0;
+  const Acc neg = kNeg;
 
   int col[Q];
   bool valid[Q], skip_in[Q], skip_out[Q], fin[Q];
@@ -188,80 +215,100 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     const int s = lane * Q + q;
     valid[q] = s < Sp;
     col[q] = (valid[q] && (s & 1)) ? y[(s - 1) >> 1] : 0;
-    // arc s-2 -> s exists
     skip_in[q] = valid[q] && (s & 1) && s >= 3 && y[(s - 1) >> 1] != y[(s - 3) >> 1];
-    // arc s -> s+2 exists
     const int s2 = s + 2;
     skip_out[q] = (s2 < Sp) && (s2 & 1) && y[(s2 - 1) >> 1] != y[(s2 - 3) >> 1];
     fin[q] = valid[q] && s >= Sp - 2;
   }
+  // one frame of emissions and arc flags for this lane's states
+  auto fetch = [&](int t, float (&e)[Q], int (&mk)[Q]) {
+    const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
+    const uint8_t* mrow = mask ? mask + base + static_cast<int64_t>(t) * Sp + lane * Q : nullptr;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      e[q] = valid[q] ? row[col[q]] : 0.f;
+      mk[q] = valid[q] ? (mrow ? static_cast<int>(mrow[q]) : 0x0f) : 0;
+    }
+  };
+  auto renorm_store = [&](Acc (&v)[Q], double& off, float* tab, double* sc, int t) {
+    float mx = kNeg;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) mx = fmaxf(mx, static_cast<float>(v[q]));
+    mx = wave_max_dpp(mx);
+    if (mx <= kNeg * 0.5f || mx != mx) mx = 0.f;  // all impossible (or NaN): keep as is
+#pragma unroll
+    for (int q = 0; q < Q; ++q) v[q] = (v[q] <= Acc(kNeg * 0.5f)) ? Acc(kNeg) : v[q] - Acc(mx);
+    off += static_cast<double>(mx);
+    float* trow = tab + base + static_cast<int64_t>(t) * Sp + lane * Q;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (valid[q]) trow[q] = static_cast<float>(v[q]);
+    if (lane == 0) sc[t0 + t] = off;
+  };
 
+  float ring_e[PF][Q];
+  int ring_m[PF][Q];
   if (dir == 0) {
     // ---------------- forward ----------------
     Acc a[Q];
     {
-      const float* row = S + static_cast<int64_t>(t0) * ldS;
-      uint8_t mk[Q];
-#pragma unroll
-      for (int q = 0; q < Q; ++q) mk[q] = (mask && valid[q]) ? mask[base + lane * Q + q] : 0xff;
+      float e[Q];
+      int mk[Q];
+      fetch(0, e, mk);
 #pragma unroll
       for (int q = 0; q < Q; ++q) {
         const int s = lane * Q + q;
-        a[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? static_cast<Acc>(row[col[q]]) : static_cast<Acc>(kNeg);
+        a[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? static_cast<Acc>(e[q]) : neg;
       }
     }
+#pragma unroll
+    for (int k = 0; k < PF; ++k)
+      if (1 + k < T) fetch(1 + k, ring_e[k], ring_m[k]);
     double off = 0.0;
-    for (int t = 0; t < T; ++t) {
-      if (t > 0) {
-        const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
-        Acc e[Q];
-        uint8_t mk[Q];
+    renorm_store(a, off, tab_f, sc_f, 0);
+    for (int tb = 1; tb < T; tb += PF) {
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          e[q] = valid[q] ? static_cast<Acc>(row[col[q]]) : Acc(0);
-          mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q] : 0x07;
+      for (int k = 0; k < PF; ++k) {
+        const int t = tb + k;
+        if (t < T) {
+          float e[Q];
+          int mk[Q];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            e[q] = ring_e[k][q];
+            mk[q] = ring_m[k][q];
+          }
+          if (t + PF < T) fetch(t + PF, ring_e[k], ring_m[k]);
+          const Acc up1 = lane_up(a[Q - 1]);
+          const Acc up2 = (Q >= 2) ? lane_up(a[Q >= 2 ? Q - 2 : 0]) : lane_up(up1);
+          Acc na[Q];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            const Acc p0 = a[q];
+            const Acc p1 = (q >= 1) ? a[q >= 1 ? q - 1 : 0] : up1;
+            const Acc p2 = (q >= 2) ? a[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
+            const Acc c0 = (mk[q] & 1) ? p0 : neg;
+            const Acc c1 = (mk[q] & 2) ? p1 : neg;
+            const Acc c2 = (skip_in[q] && (mk[q] & 4)) ? p2 : neg;
+            na[q] = valid[q] ? static_cast<Acc>(e[q]) + comb3<VIT, Acc>(c0, c1, c2) : neg;
+          }
+#pragma unroll
+          for (int q = 0; q < Q; ++q) a[q] = na[q];
+          renorm_store(a, off, tab_f, sc_f, t);
         }
-        const Acc up1 = lane_up(a[Q - 1], lane);
-        const Acc up2 = (Q >= 2) ? lane_up(a[Q >= 2 ? Q - 2 : 0], lane) : lane_up(up1, lane);
-        Acc na[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const Acc neg = kNeg;
-          const Acc p0 = a[q];
-          const Acc p1 = (q >= 1) ? a[q >= 1 ? q - 1 : 0] : up1;
-          const Acc p2 = (q >= 2) ? a[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
-          const Acc c0 = (mk[q] & 1) ? p0 : neg;
-          const Acc c1 = (mk[q] & 2) ? p1 : neg;
-          const Acc c2 = (skip_in[q] && (mk[q] & 4)) ? p2 : neg;
-          na[q] = valid[q] ? e[q] + comb3<VIT, Acc>(c0, c1, c2) : neg;
-        }
-#pragma unroll
-        for (int q = 0; q < Q; ++q) a[q] = na[q];
       }
-      // renormalise by the wave maximum (found in float; subtracted exactly)
-      float mx = kNeg;
-#pragma unroll
-      for (int q = 0; q < Q; ++q) mx = fmaxf(mx, static_cast<float>(a[q]));
-      mx = wave_max(mx);
-      if (mx <= kNeg * 0.5f || mx != mx) mx = 0.f;  // all impossible (or NaN): keep as is
-#pragma unroll
-      for (int q = 0; q < Q; ++q) a[q] = (a[q] <= Acc(kNeg * 0.5f)) ? Acc(kNeg) : a[q] - Acc(mx);
-      off += static_cast<double>(mx);
-      float* trow = tab_f + base + static_cast<int64_t>(t) * Sp;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-        if (valid[q]) trow[lane * Q + q] = static_cast<float>(a[q]);
-      if (lane == 0) sc_f[t0 + t] = off;
     }
     // total over final states (with final-arc flags)
-    float fm = kNeg;
-    uint8_t fk[Q];
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      fk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(T - 1) * Sp + lane * Q + q] : 0xff;
-      if (fin[q] && (fk[q] & 8)) fm = fmaxf(fm, static_cast<float>(a[q]));
+    int fk[Q];
+    {
+      float e[Q];
+      fetch(T - 1, e, fk);
     }
-    fm = wave_max(fm);
+    float fm = kNeg;
+#pragma unroll
+    for (int q = 0; q < Q; ++q)
+      if (fin[q] && (fk[q] & 8)) fm = fmaxf(fm, static_cast<float>(a[q]));
+    fm = wave_max_dpp(fm);
     double total;
     if (VIT) {
       total = off + static_cast<double>(fm);
@@ -287,60 +334,57 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     // ---------------- backward ----------------
     Acc b[Q];
     {
-      uint8_t mk[Q];
+      float e[Q];
+      int mk[Q];
+      fetch(T - 1, e, mk);
 #pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(T - 1) * Sp + lane * Q + q] : 0xff;
-        b[q] = (fin[q] && (mk[q] & 8)) ? Acc(0) : Acc(kNeg);
-      }
+      for (int q = 0; q < Q; ++q) b[q] = (fin[q] && (mk[q] & 8)) ? Acc(0) : neg;
     }
+    // ring slot k holds frame (T-1) - k - ... : frames T-1, T-2, ... are consumed as t+1
+#pragma unroll
+    for (int k = 0; k < PF; ++k)
+      if (T - 1 - k >= 1) fetch(T - 1 - k, ring_e[k], ring_m[k]);
     double off = 0.0;
-    for (int t = T - 1; t >= 0; --t) {
-      if (t < T - 1) {
-        const float* row = S + static_cast<int64_t>(t0 + t + 1) * ldS;
-        Acc nb[Q];
-        int mk[Q];
+    renorm_store(b, off, tab_b, sc_b, T - 1);
+    for (int tb = T - 2; tb >= 0; tb -= PF) {
 #pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          nb[q] = valid[q] ? static_cast<Acc>(row[col[q]]) + b[q] : Acc(kNeg);
-          mk[q] = (mask && valid[q]) ? mask[base + static_cast<int64_t>(t + 1) * Sp + lane * Q + q] : 0x07;
-          if (!valid[q]) mk[q] = 0;
+      for (int k = 0; k < PF; ++k) {
+        const int t = tb - k;  // uses emissions and arcs of frame t + 1
+        if (t >= 0) {
+          float e[Q];
+          int mk[Q];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            e[q] = ring_e[k][q];
+            mk[q] = ring_m[k][q];
+          }
+          if (t + 1 - PF >= 1) fetch(t + 1 - PF, ring_e[k], ring_m[k]);
+          Acc nb[Q];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) nb[q] = valid[q] ? static_cast<Acc>(e[q]) + b[q] : neg;
+          const Acc dn0 = lane_down(nb[0]);
+          const Acc dn1 = (Q >= 2) ? lane_down(nb[Q >= 2 ? 1 : 0]) : lane_down(dn0);
+          const int mdn0 = lane_down_i(mk[0]);
+          const int mdn1 = (Q >= 2) ? lane_down_i(mk[Q >= 2 ? 1 : 0]) : lane_down_i(mdn0);
+          Acc nbb[Q];
+#pragma unroll
+          for (int q = 0; q < Q; ++q) {
+            const Acc s0 = nb[q];
+            const Acc s1 = (q + 1 < Q) ? nb[q + 1 < Q ? q + 1 : 0] : dn0;
+            const Acc s2 = (q + 2 < Q) ? nb[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? dn0 : dn1);
+            const int m0 = mk[q];
+            const int m1 = (q + 1 < Q) ? mk[q + 1 < Q ? q + 1 : 0] : mdn0;
+            const int m2 = (q + 2 < Q) ? mk[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? mdn0 : mdn1);
+            const Acc c0 = (m0 & 1) ? s0 : neg;
+            const Acc c1 = (m1 & 2) ? s1 : neg;
+            const Acc c2 = (skip_out[q] && (m2 & 4)) ? s2 : neg;
+            nbb[q] = valid[q] ? comb3<VIT, Acc>(c0, c1, c2) : neg;
+          }
+#pragma unroll
+          for (int q = 0; q < Q; ++q) b[q] = nbb[q];
+          renorm_store(b, off, tab_b, sc_b, t);
         }
-        const Acc dn0 = lane_down(nb[0], lane);
-        const Acc dn1 = (Q >= 2) ? lane_down(nb[Q >= 2 ? 1 : 0], lane) : lane_down(dn0, lane);
-        const int mdn0 = lane_down_i(mk[0], lane);
-        const int mdn1 = (Q >= 2) ? lane_down_i(mk[Q >= 2 ? 1 : 0], lane) : lane_down_i(mdn0, lane);
-        Acc nbb[Q];
-#pragma unroll
-        for (int q = 0; q < Q; ++q) {
-          const Acc neg = kNeg;
-          const Acc s0 = nb[q];
-          const Acc s1 = (q + 1 < Q) ? nb[q + 1 < Q ? q + 1 : 0] : dn0;
-          const Acc s2 = (q + 2 < Q) ? nb[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? dn0 : dn1);
-          const int m0 = mk[q];
-          const int m1 = (q + 1 < Q) ? mk[q + 1 < Q ? q + 1 : 0] : mdn0;
-          const int m2 = (q + 2 < Q) ? mk[q + 2 < Q ? q + 2 : 0] : (q + 1 < Q ? mdn0 : mdn1);
-          const Acc c0 = (m0 & 1) ? s0 : neg;
-          const Acc c1 = (m1 & 2) ? s1 : neg;
-          const Acc c2 = (skip_out[q] && (m2 & 4)) ? s2 : neg;
-          nbb[q] = valid[q] ? comb3<VIT, Acc>(c0, c1, c2) : neg;
-        }
-#pragma unroll
-        for (int q = 0; q < Q; ++q) b[q] = nbb[q];
       }
-      float mx = kNeg;
-#pragma unroll
-      for (int q = 0; q < Q; ++q) mx = fmaxf(mx, static_cast<float>(b[q]));
-      mx = wave_max(mx);
-      if (mx <= kNeg * 0.5f || mx != mx) mx = 0.f;
-#pragma unroll
-      for (int q = 0; q < Q; ++q) b[q] = (b[q] <= Acc(kNeg * 0.5f)) ? Acc(kNeg) : b[q] - Acc(mx);
-      off += static_cast<double>(mx);
-      float* trow = tab_b + base + static_cast<int64_t>(t) * Sp;
-#pragma unroll
-      for (int q = 0; q < Q; ++q)
-        if (valid[q]) trow[lane * Q + q] = static_cast<float>(b[q]);
-      if (lane == 0) sc_b[t0 + t] = off;
     }
   }
 }
