@@ -105,6 +105,27 @@ struct TileCopy {
     }
   }
 
+  // Same as init for a tile whose first row is row0 (no row gather).
+  __device__ __forceinline__ void retarget(const GOp& op, int row0, int w, int lane) {
+#pragma unroll
+    for (int i = 0; i < kPerWave; ++i) {
+      const int c = w + NW * i;
+      if constexpr (L == LL::KC) {
+        using G = KC<BK>;
+        const int r = c * G::kRowsPerCopy + lane / G::kSlots;
+        const int row = row0 + r;
+        ok[i] = row < op.rows;
+        src[i] = op.base + static_cast<int64_t>(row) * op.pitch + lim[i];
+      } else {
+        using G = MC<NR>;
+        const int lc = (lane % G::kSlots) ^ G::swz(lim[i]);
+        const int row = row0 + lc * 8;
+        ok[i] = row < op.rows;
+        src[i] = op.base + static_cast<int64_t>(lim[i]) * op.pitch + row;
+      }
+    }
+  }
+
   __device__ __forceinline__ void issue(const GOp& op, int k0, char* lds, int w) const {
 #pragma unroll
     for (int i = 0; i < kPerWave; ++i) {
@@ -219,6 +240,60 @@ struct Gemm {
       cb.issue(B, kbeg + nt * BK, st[SN] + kABytes, wave);
     }
     compute(st[S], wave, lane, acc);
+  }
+
+  // A sequence of ntiles output tiles sharing the B rows (col0) and the k range [0, K):
+  // tile i uses A rows from row0 + i * BR.  The copy pipeline runs straight through the
+  // tile boundaries; epi(i, acc) is called after tile i's last product (while the copy of
+  // the next tile's first k-tile is in flight) and must not touch the LDS stages.
+  template <class Epi>
+  __device__ static __forceinline__ void run_tiles(const GOp& A, const GOp& B, int row0, int col0, int ntiles, int K,
+                                                   char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi) {
+    static_assert(NS == 2, "flattened sequence uses two stages");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int nk = (K + BK - 1) / BK;
+    const int nsteps = ntiles * nk;
+    CA ca;
+    CB cb;
+    ca.init(A, row0, wave, lane);
+    cb.init(B, col0, wave, lane);
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int j = 0; j < FC; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    __builtin_amdgcn_s_barrier();
+    if (nsteps <= 0) return;
+    ca.issue(A, 0, st[0], wave);
+    cb.issue(B, 0, st[0] + kABytes, wave);
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    auto half = [&](int sidx, char* cur, char* nxt) {
+      const int tile = sidx / nk, kt = sidx - tile * nk;
+      if (sidx + 1 < nsteps) {
+        const int kn = (kt + 1 == nk) ? 0 : kt + 1;
+        if (kn == 0) ca.retarget(A, row0 + (tile + 1) * BR, wave, lane);
+        ca.issue(A, kn * BK, nxt, wave);
+        cb.issue(B, kn * BK, nxt + kABytes, wave);
+      }
+      compute(cur, wave, lane, acc);
+      if (kt == nk - 1) {
+        epi(tile, acc);
+#pragma unroll
+        for (int i = 0; i < FR; ++i)
+#pragma unroll
+          for (int j = 0; j < FC; ++j)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+      }
+      wait_vmcnt<0>();
+      __builtin_amdgcn_s_barrier();
+    };
+    for (int sidx = 0; sidx < nsteps; sidx += 2) {
+      half(sidx, st[0], st[1]);
+      if (sidx + 1 < nsteps) half(sidx + 1, st[1], st[0]);
+    }
   }
 
   // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here).

@@ -451,19 +451,25 @@ BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
     p.chunk = chunk;
   } else {
     // default: the recomputed gradient chunk (M x chunk in the input dtype) takes about
-    // 256 MiB, in whole multiples of 4096 columns, between 4096 and 65536 columns
+    // 256 MiB.  For bf16 the chunk is a multiple of q columns, where q makes the dW
+    // launch (256 x 256 tiles) a whole number of 256-workgroup waves.
     const size_t es0 = (dtype == 1) ? 2 : 4;
     size_t c = (static_cast<size_t>(256) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
-    c = (c / 4096) * 4096;
-    if (c < 4096) c = 4096;
-    if (c > 65536) c = 65536;
+    size_t q = 4096;
+    if (dtype == 1) {
+      const int ndt = (D + 255) / 256;
+      q = static_cast<size_t>(256) * ((256 + ndt - 1) / ndt);
+    }
+    c = (c / q) * q;
+    if (c < q) c = q;
+    if (c > 65536) c = (65536 / q) * q > 0 ? (65536 / q) * q : q;
     p.chunk = static_cast<int>(c);
   }
   const size_t es = (dtype == 1) ? 2 : 4;
   const int tr = (dtype == 1) ? 256 : kBwdB;  // dH tile rows of the kernel used
-  const int tc = (dtype == 1) ? 128 : kBwdB;
+  const int tc = (dtype == 1) ? 256 : kBwdB;
   const int tiles = ((M + tr - 1) / tr) * ((D + tc - 1) / tc);
-  int splits = (512 + tiles - 1) / tiles;
+  int splits = 256 / tiles;  // one wave of 256 workgroups
   const int maxs = p.chunk / 256;
   if (splits > maxs) splits = maxs;
   if (splits > 8) splits = 8;

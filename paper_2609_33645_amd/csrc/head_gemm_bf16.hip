@@ -22,13 +22,21 @@ namespace {
 constexpr int kFR = 256;  // vocabulary rows per forward/recompute tile
 constexpr int kFC = 128;  // frames per forward/recompute tile
 constexpr int kFK = 32;   // k per stage
-constexpr int kNS = 3;    // LDS stages
 constexpr int kBR = 256;  // backward tile rows (dH: frames, dW: vocabulary)
-constexpr int kBC = 128;  // backward tile columns (D)
+constexpr int kBC = 256;  // backward tile columns (D)
+constexpr int kBK = 64;
 
-using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, kNS>;
-using GDh = bf::Gemm<kBR, kBC, kFK, LL::KC, LL::MC, kNS>;
-using GDw = bf::Gemm<kBR, kBC, kFK, LL::MC, LL::MC, kNS>;
+// 4 wavefronts (2 x 2), two workgroups per CU so that one's epilogue overlaps the
+// other's products
+using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
+// 8 wavefronts (2 x 4), two stages of 256 x 64 + 256 x 64
+using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 2, 2, 4>;
+using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 2, 2, 4>;
+
+#define PCTC_STAGES2(G)                                                  \
+  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
+  char* const st[2] = {st0_, st1_};
 
 #define PCTC_STAGES(G)                                                   \
   __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
@@ -131,23 +139,24 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
       lse_tile_update<true, FR, FC>(acc, run_max, run_sum, v0, vend, wave, lane);
   }
   __syncthreads();
+  // the two wavefronts of each frame column (row halves) combine their partial sums
   float2* xch = reinterpret_cast<float2*>(st0_);
-  const int rowhalf = wave >> 1, colhalf = wave & 1;
+  const int rowhalf = wave / 2, colq = wave % 2;
   if (rowhalf == 1 && lane < 32) {
 #pragma unroll
-    for (int j = 0; j < FC; ++j) xch[colhalf * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
+    for (int j = 0; j < FC; ++j) xch[colq * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
   }
   __syncthreads();
   if (rowhalf == 0 && lane < 32) {
 #pragma unroll
     for (int j = 0; j < FC; ++j) {
-      const float2 o = xch[colhalf * (FC * 32) + j * 32 + lane];
+      const float2 o = xch[colq * (FC * 32) + j * 32 + lane];
       const float nmax = fmaxf(run_max[j], o.x);
       float s = 0.f;
       if (run_max[j] != -INFINITY) s += run_sum[j] * fast_exp2((run_max[j] - nmax) * kLog2e);
       if (o.x != -INFINITY) s += o.y * fast_exp2((o.x - nmax) * kLog2e);
       if (nmax != nmax) s = nmax;
-      const int m = m0 + GFwd::col_of(wave, lane, j);
+      const int m = m0 + G::col_of(wave, lane, j);
       if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(nmax, s);
     }
   }
@@ -241,8 +250,8 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   f32x16 acc[FR][FC];
   GG::run(A, B, vl0, m0, 0, D, st, acc);
   const bool full = vl0 + kFR <= cw;
-  const int ch = wave & 1;          // column half: frames [64 ch, 64 ch + 64) of the tile
-  char* stage = ch ? st1_ : st0_;   // 32 frames x 256 vocabulary columns per pass
+  const int ch = wave & 1;            // column half: frames [64 ch, 64 ch + 64) of the tile
+  char* stage = ch ? st1_ : st0_;     // 32 frames x 256 vocabulary columns per pass
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     __syncthreads();  // previous pass's readers (and the product's last reads) are done
@@ -270,9 +279,9 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
       const int idx = tid + 256 * k;
-      const int half = idx >> 10;             // which stage (column half)
-      const int row = (idx >> 5) & 31;        // frame within the pass
-      const int vec = idx & 31;               // 16-byte vector within the 256-column row
+      const int half = idx >> 10;
+      const int row = (idx >> 5) & 31;
+      const int vec = idx & 31;
       const int mm = m0 + 64 * half + 32 * j + row;
       const char* src = (half ? st1_ : st0_) + row * kPitch + vec * 16;
       const u32x4 v = *reinterpret_cast<const u32x4*>(src);
@@ -281,12 +290,12 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   }
 }
 
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(512, 1)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
              int slice, float* __restrict__ part) {
   using G = GDh;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES(G)
+  PCTC_STAGES2(G)
   const int nMt = (M + kBR - 1) / kBR;
   const int nDt = (D + kBC - 1) / kBC;
   // d-tiles fastest: the workgroups that read the same dZ rows run together on one XCD
@@ -319,12 +328,12 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
     }
 }
 
-__global__ void __launch_bounds__(256, 2)
+__global__ void __launch_bounds__(512, 1)
 dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ Hs, int D, int c0, int cw,
              float* __restrict__ dW) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES(G)
+  PCTC_STAGES2(G)
   const int nDt = (D + kBC - 1) / kBC;
   const int work = xcd_swz(blockIdx.x, gridDim.x);
   const int dt = work % nDt;
@@ -367,7 +376,7 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
 
 int lse_partitions_bf16(int M, int V) {
   const int nMt = (M + kFC - 1) / kFC;
-  int P = (2048 + nMt - 1) / nMt;
+  int P = (2048 + nMt - 1) / nMt;  // a few waves of two workgroups per CU
   const int vtiles = (V + kFR - 1) / kFR;
   if (P > vtiles) P = vtiles;
   if (P > 256) P = 256;
@@ -384,8 +393,8 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
   const int nMt = (M + kFC - 1) / kFC;
   *P_out = Peff;
   Prof pr("lse_partial", stream);
-  hipLaunchKernelGGL(lse_partial_bf16, dim3(grouped_grid(nMt, Peff)), dim3(256), 0, stream, H, M, D, W, V, Peff, vper,
-                     partials);
+  hipLaunchKernelGGL(lse_partial_bf16, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M, D, W, V,
+                     Peff, vper, partials);
   return hipGetLastError();
 }
 
@@ -395,7 +404,8 @@ hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t*
   const int nMt = (M + kFC - 1) / kFC;
   const int nJt = (K_max + kFR - 1) / kFR;
   Prof pr("gather_s", stream);
-  hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(256), 0, stream, H, M, D, W, u_ids, K, lam, S, ldS);
+  hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(GFwd::kThreads), 0, stream, H, M, D, W, u_ids, K, lam, S,
+                     ldS);
   return hipGetLastError();
 }
 
@@ -407,19 +417,20 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, i
   const int nVt = (cw + kFR - 1) / kFR;
   {
     Prof pr("recompute_dz", stream);
-    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(256), 0, stream, H, M, D, W, c0, cw, lam2,
-                       G, ldG, g, remap, dZ, chunk);
+    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, H, M, D, W, c0,
+                       cw, lam2, G, ldG, g, remap, dZ, chunk);
   }
   if (want_dH) {
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
-    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles * ns), dim3(256), 0, stream, dZ, M, chunk, W, D, c0, cw, slice, part);
+    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D, c0, cw, slice,
+                       part);
   }
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("dw_gemm", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(256), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW);
   }
   return hipGetLastError();
 }
