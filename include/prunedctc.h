@@ -160,6 +160,10 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
  * int32 [V] from pctc_union_remap.  dH and/or dW may be NULL.
  * bwd_scratch: device scratch of pctc_bwd_scratch_bytes() bytes. */
 size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
+/* Vocabulary columns per backward step that a call with this chunk argument uses (0 picks
+ * the default: about 256 MiB of recomputed gradient, rounded to whole launch waves).
+ * Returns 0 for invalid arguments. */
+int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
                       int32_t V, const double* lam, const float* G, int32_t ldG, const float* g,
                       const int32_t* remap, int32_t chunk, float* dH, float* dW, void* bwd_scratch,

@@ -19,5 +19,6 @@ from .prunedctc_oracle import (  # noqa: F401
     ctc_utterance,
     ctc_from_scores,
     head_backward,
+    head_backward_rows,
     fwd_bwd,
 )

@@ -344,6 +344,41 @@ def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096) -> Dict[str, np.nda
     return {"dH": dH, "dW": dW}
 
 
+def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 4096) -> Dict[str, np.ndarray]:
+    """Selected outputs of the recomputed backward (Eq. vjp), each over its full contraction:
+    dH[m] = sum_v dZ[m, v] W[v] for the given frames (every class v) and
+    dW[v] = sum_m dZ[m, v] H[m] for the given classes (every frame m), with
+    dZ[m, v] = scatter_U(G)[m, v] - g_m exp(Z[m, v] - lambda_m) as in head_backward."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    lam = np.asarray(lam, np.float64)
+    G = np.asarray(G, np.float64)
+    g = np.asarray(g, np.float64)
+    frames = np.asarray(frames, np.int64)
+    classes = np.asarray(classes, np.int64)
+    V = W.shape[0]
+    col = {int(v): j for j, v in enumerate(np.asarray(u_ids).tolist())}
+
+    def dz(rows: np.ndarray, vs: np.ndarray) -> np.ndarray:
+        Z = H[rows] @ W[vs].T
+        with np.errstate(invalid="ignore", over="ignore"):
+            out = -g[rows, None] * np.exp(Z - lam[rows, None])
+        for i, v in enumerate(vs.tolist()):
+            j = col.get(int(v))
+            if j is not None:
+                out[:, i] += G[rows, j]
+        out[g[rows] == 0] = 0.0
+        return out
+
+    dH = np.zeros((frames.size, H.shape[1]))
+    for v0 in range(0, V, chunk):
+        vs = np.arange(v0, min(V, v0 + chunk))
+        dH += dz(frames, vs) @ W[vs]
+    inc = np.nonzero(g != 0)[0]
+    dW = dz(inc, classes).T @ H[inc]
+    return {"dH": dH, "dW": dW}
+
+
 # ---------------------------------------------------------------------------------------
 # Whole path: loss and head gradients by the full-vocabulary definition
 # ---------------------------------------------------------------------------------------

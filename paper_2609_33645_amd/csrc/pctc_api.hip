@@ -348,6 +348,12 @@ size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ch
   return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, chunk).total;
 }
 
+int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || chunk < 0 || (chunk > 0 && chunk % 256))
+    return 0;
+  return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, chunk).chunk;
+}
+
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
                       const double* lam, const float* G, int32_t ldG, const float* g, const int32_t* remap,
                       int32_t chunk, float* dH, float* dW, void* bwd_scratch, void* stream_ptr) {

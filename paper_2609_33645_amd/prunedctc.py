@@ -67,6 +67,8 @@ def lib() -> ctypes.CDLL:
     L.pctc_ctc_dp.restype = c_i32
     L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_scratch_bytes.restype = c_sz
+    L.pctc_bwd_chunk.argtypes = [c_i32, c_i32, c_i32, c_i32]
+    L.pctc_bwd_chunk.restype = c_i32
     L.pctc_head_bwd.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p,
                                 c_p, c_p]
     L.pctc_head_bwd.restype = c_i32
@@ -127,13 +129,28 @@ def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, be
     return int(lib().pctc_workspace_size(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk))
 
 
+def bwd_chunk(dtype: int, M: int, D: int, chunk: int = 0) -> int:
+    """Vocabulary columns per backward step used for this problem (0 chunk = the default)."""
+    return int(lib().pctc_bwd_chunk(int(dtype), int(M), int(D), int(chunk)))
+
+
+def _grad_buffer(t: Optional[torch.Tensor], shape, dev) -> torch.Tensor:
+    if t is None:
+        return torch.empty(shape, dtype=torch.float32, device=dev)
+    if t.dtype != torch.float32 or tuple(t.shape) != tuple(shape) or not t.is_contiguous() or t.device != dev:
+        raise PrunedCTCError(-1, f"gradient buffer must be contiguous float32 {tuple(shape)} on {dev}")
+    return t
+
+
 def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, input_lengths: Sequence[int],
                        target_lengths: Sequence[int], blank: int = 0, beam: float = math.inf, chunk: int = 0,
                        want_dH: bool = True, want_dW: bool = True, workspace: Optional[torch.Tensor] = None,
-                       stream=None) -> Dict[str, torch.Tensor]:
+                       stream=None, dH_out: Optional[torch.Tensor] = None,
+                       dW_out: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
     """Loss and head gradients of Pruned CTC.  H [M, D] and W [V, D] are device tensors of
     the same dtype (bfloat16 or float32); targets is a device int32 tensor; the length
-    arrays are host sequences.  Returns loss (float64 [1]), loss_per_utt, status, dH, dW."""
+    arrays are host sequences.  Returns loss (float64 [1]), loss_per_utt, status, dH, dW.
+    dH_out / dW_out: optional preallocated float32 [M, D] / [V, D] gradient buffers."""
     L = lib()
     dt = _dtype_code(H)
     if W.dtype != H.dtype:
@@ -163,8 +180,8 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
     loss = torch.zeros(1, dtype=torch.float64, device=dev)
     loss_n = torch.zeros(max(N, 1), dtype=torch.float64, device=dev)
     status = torch.zeros(max(N, 1), dtype=torch.int32, device=dev)
-    dH = torch.empty((M, D), dtype=torch.float32, device=dev) if want_dH else None
-    dW = torch.empty((V, D), dtype=torch.float32, device=dev) if want_dW else None
+    dH = _grad_buffer(dH_out, (M, D), dev) if want_dH else None
+    dW = _grad_buffer(dW_out, (V, D), dev) if want_dW else None
     code = L.pruned_ctc_fwd_bwd(dt, _ptr(H), D, _ptr(W), V, _ptr(targets), _i32p(T), _i32p(U), N, int(blank),
                                 float(beam), int(chunk), _ptr(loss), _ptr(loss_n), _ptr(status), _ptr(dH), _ptr(dW),
                                 ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()), _stream(stream))

@@ -59,10 +59,17 @@ class Workload:
 def round_to_bf16(x: np.ndarray) -> np.ndarray:
     """Round float32 values to the nearest bfloat16 (ties to even); return float32."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16) << 16
-    out = r.astype(np.uint32).view(np.float32).copy()
+    out = np.empty_like(x)
+    src = x.reshape(-1).view(np.uint32)
+    dst = out.reshape(-1).view(np.uint32)
+    step = 1 << 22
+    for i in range(0, src.size, step):
+        u = src[i:i + step]
+        # finite values and infinities cannot overflow 32 bits here (|u| <= 0xFF800000)
+        r = u + np.uint32(0x7FFF)
+        r += (u >> np.uint32(16)) & np.uint32(1)
+        r &= np.uint32(0xFFFF0000)
+        dst[i:i + step] = r
     nan = np.isnan(x)
     if nan.any():
         out[nan] = np.float32("nan")

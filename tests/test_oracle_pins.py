@@ -415,3 +415,34 @@ def test_head_backward_stage_matches_full_path():
     np.testing.assert_allclose(st["dH"], full["dH"], atol=1e-12)
     np.testing.assert_allclose(st["dW"], full["dW"], atol=1e-12)
     assert full["status"][1] == oracle.STATUS_NOT_ALIGNABLE
+
+
+def test_head_backward_rows_is_gradient_of_surrogate():
+    """The sampled backward rows are the gradient of f(H, W) = sum G * Z_U - sum_m g_m lambda_m
+    (its derivative w.r.t. Z is scatter_U(G) - g p, Eq. vjp), taken by torch autograd in float64;
+    frames with g = 0 are left out of f, and NaN in such a frame must not reach dW."""
+    import torch
+    rng = np.random.default_rng(21)
+    M, D, V, K = 40, 9, 300, 12
+    H = rng.standard_normal((M, D))
+    W = rng.standard_normal((V, D)) / 3
+    u_ids = np.concatenate([[7], np.sort(rng.choice(np.setdiff1d(np.arange(V), [7]), K - 1, replace=False))])
+    G = -rng.random((M, K))
+    G[5:9] = 0.0                       # an excluded utterance's frames
+    g = G.sum(axis=1)
+    H[6] = np.nan
+    lam = oracle.log_normalizer(H, W, chunk=64)
+    frames = np.array([0, 3, 6, 17, M - 1])
+    classes = np.array([0, 7, int(u_ids[3]), 150, V - 1])
+    got = oracle.head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk=77)
+    inc = g != 0
+    Ht = torch.tensor(H[inc], dtype=torch.float64, requires_grad=True)
+    Wt = torch.tensor(W, dtype=torch.float64, requires_grad=True)
+    Z = Ht @ Wt.T
+    f = (torch.tensor(G[inc]) * Z[:, torch.tensor(u_ids)]).sum() - (torch.tensor(g[inc]) * torch.logsumexp(Z, 1)).sum()
+    f.backward()
+    dH = np.zeros((M, D))
+    dH[inc] = Ht.grad.numpy()
+    np.testing.assert_allclose(got["dH"], dH[frames], atol=1e-11)
+    np.testing.assert_allclose(got["dW"], Wt.grad.numpy()[classes], atol=1e-11)
+    assert np.all(got["dH"][2] == 0.0) and np.all(np.isfinite(got["dW"]))
