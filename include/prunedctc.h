@@ -158,8 +158,9 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
  * dZ = scatter_U(G) - g p with p = exp(H W^T - lam) recomputed, then dH = sum dZ W and
  * dW = dZ^T H (rows of frames with g[m] == 0 contribute nothing).  remap: device
  * int32 [V] from pctc_union_remap.  dH and/or dW may be NULL.
- * bwd_scratch: device scratch of pctc_bwd_scratch_bytes() bytes. */
-size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
+ * bwd_scratch: device scratch of pctc_bwd_scratch_bytes() bytes (ldG: the row pitch of G,
+ * at least the union size K). */
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ldG, int32_t chunk);
 /* Vocabulary columns per backward step that a call with this chunk argument uses (0 picks
  * the default: about 256 MiB of recomputed gradient, rounded to whole launch waves).
  * Returns 0 for invalid arguments. */

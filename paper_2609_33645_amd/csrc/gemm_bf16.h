@@ -12,8 +12,13 @@
 //       yields the 8-element k-run of column n that the matrix core expects.
 // 16-byte slots within an LDS row are XOR-swizzled by a function of the row so that the
 // fragment reads of neighbouring rows fall in different banks.
-// NS LDS stages form a ring; the copy of k-tile t+NS-1 runs while tile t is consumed.
-// Out-of-range rows or k read from a 16-byte zero page, so ragged tiles need no masking.
+// NS LDS stages form a ring: while k-tile t is consumed, the copies of tiles t+1..t+NS-1
+// are in flight, and the copy of t+NS is issued as soon as every wave has read tile t.
+// Fragments are double-buffered in registers across k-steps, and every k-step issues its
+// matrix products interleaved one by one with the next step's LDS reads (and copies), so
+// the matrix pipe is fed while the reads are in flight.
+// Out-of-range rows or k read from a 16-byte zero page, so ragged tiles need no masking;
+// the k loop runs a multiple of NS tiles (the extra tiles are zeros).
 #pragma once
 
 #include "pctc_device.h"
@@ -126,11 +131,12 @@ struct TileCopy {
     }
   }
 
-  __device__ __forceinline__ void issue(const GOp& op, int k0, char* lds, int w) const {
+  // Copies k-tile [k0, k0 + BK); k at or past klim reads zeros.
+  __device__ __forceinline__ void issue(const GOp& op, int k0, int klim, char* lds, int w) const {
 #pragma unroll
     for (int i = 0; i < kPerWave; ++i) {
       const int c = w + NW * i;
-      const bool valid = ok[i] && (k0 + lim[i] < op.kmax);
+      const bool valid = ok[i] && (k0 + lim[i] < klim);
       const int64_t koff = (L == LL::KC) ? static_cast<int64_t>(k0) : static_cast<int64_t>(k0) * op.pitch;
       const void* g = valid ? static_cast<const void*>(src[i] + koff) : static_cast<const void*>(kZeroPage);
       lds_copy16(g, (lds_void*)(lds + c * 1024));
@@ -165,13 +171,8 @@ __device__ __forceinline__ bf16x8 frag(const char* lds, int rr_base, int kk, int
   }
 }
 
-// NS-stage ring with one barrier per k-tile.  Iteration t: wait until this wave's copies
-// of tile t have landed (later tiles may still be in flight), barrier (tile t visible to
-// every wave; every wave is done reading tile t-1's stage), issue the copy of tile
-// t+NS-1 into that freed stage, then consume tile t.  The k loop is unrolled by NS so
-// that each stage is a distinct LDS object: the compiler can see that reading one stage
-// does not depend on copies in flight into the others.
-// Waves form a WR x WC grid; each owns (BR/WR) x (BC/WC) = FR x FC blocks of 32x32.
+// Tile engine.  Waves form a WR x WC grid; each owns (BR/WR) x (BC/WC) = FR x FC blocks of
+// 32x32.  BK must be a multiple of 32 (an even number of 16-deep k-steps per tile).
 template <int BR, int BC, int BK, LL LA, LL LB, int NS, int WR = 2, int WC = 2>
 struct Gemm {
   static constexpr int kNS = NS;
@@ -179,14 +180,23 @@ struct Gemm {
   static constexpr int NW = WR * WC;
   static constexpr int kThreads = 64 * NW;
   static constexpr int FR = BR / WR / 32, FC = BC / WC / 32;
+  static constexpr int KK = BK / 16;
   static constexpr int kABytes = BR * BK * 2;
   static constexpr int kBBytes = BC * BK * 2;
   static constexpr int kStageBytes = kABytes + kBBytes;
   using CA = TileCopy<LA, BR, BK, NW>;
   using CB = TileCopy<LB, BC, BK, NW>;
-  static constexpr int kCopiesPerWave = CA::kPerWave + CB::kPerWave;
+  static constexpr int CPW = CA::kPerWave + CB::kPerWave;  // copies per wave per k-tile
   static_assert(NS >= 2 && NS <= 4, "stages");
-  static_assert(kCopiesPerWave * (NS - 1) < 64, "vmcnt range");
+  static_assert(KK % 2 == 0, "BK must be a multiple of 32");
+  static_assert(CPW * NS < 64, "vmcnt range");
+  // LDS reads per fragment set (the transpose read takes two per fragment)
+  static constexpr int ND = FR * (LA == LL::MC ? 2 : 1) + FC * (LB == LL::MC ? 2 : 1);
+  static constexpr int NM = FR * FC;
+
+  struct Frags {
+    bf16x8 a[FR], b[FC];
+  };
 
   // Row (within the tile) of accumulator register r of block i, and column of block j.
   __device__ static __forceinline__ int row_of(int wave, int lane, int i, int r) {
@@ -196,299 +206,179 @@ struct Gemm {
     return (wave % WC) * (BC / WC) + 32 * j + (lane & 31);
   }
 
-  __device__ static __forceinline__ void compute(const char* stage, int wave, int lane, f32x16 (&acc)[FR][FC]) {
-    const char* la = stage;
-    const char* lb = stage + kABytes;
-    const int wr0 = (wave / WC) * (BR / WR);
-    const int wc0 = (wave % WC) * (BC / WC);
-#pragma unroll
-    for (int kk = 0; kk < BK; kk += 16) {
-      bf16x8 a[FR], b[FC];
-#pragma unroll
-      for (int i = 0; i < FR; ++i) a[i] = frag<LA, BR, BK>(la, wr0 + 32 * i, kk, lane);
-#pragma unroll
-      for (int j = 0; j < FC; ++j) b[j] = frag<LB, BC, BK>(lb, wc0 + 32 * j, kk, lane);
-#pragma unroll
-      for (int i = 0; i < FR; ++i)
-#pragma unroll
-        for (int j = 0; j < FC; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
-    }
-  }
-
-  template <int S>
-  __device__ static __forceinline__ void step(const GOp& A, const GOp& B, const CA& ca, const CB& cb, int kbeg, int kt,
-                                              int nk, char* const (&st)[NS], int wave, int lane,
-                                              f32x16 (&acc)[FR][FC]) {
-    // copies issued after tile kt so far: tiles kt+1 .. min(kt+NS-2, nk-1)
-    const int after = min(NS - 2, nk - 1 - kt);
-    if constexpr (NS >= 4) {
-      if (after >= 2) wait_vmcnt<2 * kCopiesPerWave>();
-      else if (after == 1) wait_vmcnt<kCopiesPerWave>();
-      else wait_vmcnt<0>();
-    } else if constexpr (NS == 3) {
-      if (after >= 1) wait_vmcnt<kCopiesPerWave>();
-      else wait_vmcnt<0>();
-    } else {
-      wait_vmcnt<0>();
-    }
-    __builtin_amdgcn_s_barrier();
-    const int nt = kt + NS - 1;
-    if (nt < nk) {
-      constexpr int SN = (S + NS - 1) % NS;
-      ca.issue(A, kbeg + nt * BK, st[SN], wave);
-      cb.issue(B, kbeg + nt * BK, st[SN] + kABytes, wave);
-    }
-    compute(st[S], wave, lane, acc);
-  }
-
-  // A sequence of ntiles output tiles sharing the B rows (col0) and the k range [0, K):
-  // tile i uses A rows from row0 + i * BR.  The copy pipeline runs straight through the
-  // tile boundaries; epi(i, acc) is called after tile i's last product (while the copy of
-  // the next tile's first k-tile is in flight) and must not touch the LDS stages.
-  template <class Epi>
-  __device__ static __forceinline__ void run_tiles(const GOp& A, const GOp& B, int row0, int col0, int ntiles, int K,
-                                                   char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi) {
-    static_assert(NS == 2, "flattened sequence uses two stages");
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int nk = (K + BK - 1) / BK;
-    const int nsteps = ntiles * nk;
-    CA ca;
-    CB cb;
-    ca.init(A, row0, wave, lane);
-    cb.init(B, col0, wave, lane);
+  __device__ static __forceinline__ void zero(f32x16 (&acc)[FR][FC]) {
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int j = 0; j < FC; ++j)
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    __builtin_amdgcn_s_barrier();
-    if (nsteps <= 0) return;
-    ca.issue(A, 0, st[0], wave);
-    cb.issue(B, 0, st[0] + kABytes, wave);
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_barrier();
-    auto half = [&](int sidx, char* cur, char* nxt) {
-      const int tile = sidx / nk, kt = sidx - tile * nk;
-      if (sidx + 1 < nsteps) {
-        const int kn = (kt + 1 == nk) ? 0 : kt + 1;
-        if (kn == 0) ca.retarget(A, row0 + (tile + 1) * BR, wave, lane);
-        ca.issue(A, kn * BK, nxt, wave);
-        cb.issue(B, kn * BK, nxt + kABytes, wave);
+  }
+
+  __device__ static __forceinline__ void load(const char* stage, int kk, int wave, int lane, Frags& f) {
+    const int wr0 = (wave / WC) * (BR / WR), wc0 = (wave % WC) * (BC / WC);
+#pragma unroll
+    for (int i = 0; i < FR; ++i) f.a[i] = frag<LA, BR, BK>(stage, wr0 + 32 * i, kk * 16, lane);
+#pragma unroll
+    for (int j = 0; j < FC; ++j) f.b[j] = frag<LB, BC, BK>(stage + kABytes, wc0 + 32 * j, kk * 16, lane);
+  }
+
+  __device__ static __forceinline__ void mma(const Frags& f, f32x16 (&acc)[FR][FC]) {
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int j = 0; j < FC; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+  }
+
+  // Instruction order of one k-step: each matrix product is followed by its share of the
+  // ND reads of the next step and, in a tile's last step, of the NV copies.
+  template <int NV>
+  __device__ static __forceinline__ void interleave() {
+#pragma unroll
+    for (int q = 0; q < NM; ++q) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix product
+      if (q < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
+      const int d = (q + 1) * ND / NM - q * ND / NM;
+      if (d == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS reads
+      else if (d == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
+      else if (d == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+      else if (d >= 4) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  // One k-tile held in stage S; the fragments of its first k-step are in f0.  In the last
+  // k-step: wait for this wave's copies of the next tile, barrier (the next tile is
+  // visible and every wave is done reading stage S), then `issue` refills stage S and
+  // the next tile's first fragments are read into f0 (stage S+1).
+  template <int S, class Issue>
+  __device__ static __forceinline__ void ktile(char* const (&st)[NS], int wave, int lane, f32x16 (&acc)[FR][FC],
+                                               Frags& f0, Frags& f1, Issue&& issue) {
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+      Frags& cur = (kk & 1) ? f1 : f0;
+      Frags& nxt = (kk & 1) ? f0 : f1;
+      if (kk + 1 < KK) {
+        load(st[S], kk + 1, wave, lane, nxt);
+        mma(cur, acc);
+        interleave<0>();
+      } else {
+        wait_vmcnt<(NS - 2) * CPW>();
+        __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of stage S are done
+        __builtin_amdgcn_s_barrier();
+        issue(st[S]);
+        load(st[(S + 1) % NS], 0, wave, lane, nxt);
+        mma(cur, acc);
+        interleave<CPW>();
       }
-      compute(cur, wave, lane, acc);
-      if (kt == nk - 1) {
-        epi(tile, acc);
-#pragma unroll
-        for (int i = 0; i < FR; ++i)
-#pragma unroll
-          for (int j = 0; j < FC; ++j)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-      }
-      wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-    };
-    for (int sidx = 0; sidx < nsteps; sidx += 2) {
-      half(sidx, st[0], st[1]);
-      if (sidx + 1 < nsteps) half(sidx + 1, st[1], st[0]);
     }
   }
 
-  // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here).
-  // All kThreads threads must call; contains barriers.  st[s]: kStageBytes each.
+  // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here).  All
+  // kThreads threads must call; contains barriers.  st[s]: kStageBytes each.  On return
+  // every copy has landed and every wave is past its last LDS read.
   __device__ static __forceinline__ void run(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
                                              char* const (&st)[NS], f32x16 (&acc)[FR][FC]) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-#pragma unroll
-    for (int i = 0; i < FR; ++i)
-#pragma unroll
-      for (int j = 0; j < FC; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+    zero(acc);
     const int nk = (kend - kbeg + BK - 1) / BK;
+    if (nk <= 0) return;
+    const int klimA = min(A.kmax, kend), klimB = min(B.kmax, kend);
     CA ca;
     CB cb;
     ca.init(A, row0, wave, lane);
     cb.init(B, col0, wave, lane);
     __builtin_amdgcn_s_barrier();  // previous users of the stages are done
 #pragma unroll
-    for (int s = 0; s < NS - 1; ++s) {
-      if (s < nk) {
-        ca.issue(A, kbeg + s * BK, st[s], wave);
-        cb.issue(B, kbeg + s * BK, st[s] + kABytes, wave);
-      }
+    for (int s = 0; s < NS; ++s) {
+      ca.issue(A, kbeg + s * BK, klimA, st[s], wave);
+      cb.issue(B, kbeg + s * BK, klimB, st[s] + kABytes, wave);
     }
-    for (int kt = 0; kt < nk; kt += NS) {
-      step<0>(A, B, ca, cb, kbeg, kt, nk, st, wave, lane, acc);
-      if (kt + 1 < nk) step<1>(A, B, ca, cb, kbeg, kt + 1, nk, st, wave, lane, acc);
-      if constexpr (NS >= 3)
-        if (kt + 2 < nk) step<2 % NS>(A, B, ca, cb, kbeg, kt + 2, nk, st, wave, lane, acc);
-      if constexpr (NS >= 4)
-        if (kt + 3 < nk) step<3 % NS>(A, B, ca, cb, kbeg, kt + 3, nk, st, wave, lane, acc);
-    }
-  }
-};
-
-// ---------------------------------------------------------------------------------------
-// Variant with one operand loaded straight into registers.
-//
-// The LDS copy path has limited throughput, so one operand (the "direct" one, which must
-// be K-contiguous in global memory) bypasses LDS: each lane loads its own 16-byte MFMA
-// fragments with ordinary vector loads, one k-tile ahead into a register double buffer.
-// The other operand goes through a two-stage LDS ring as above.  Within a k-tile of BK,
-// lane half h owns k in [h BK/2, (h+1) BK/2) and step s uses the s-th 8-run of it, so a
-// lane's direct loads for one k-tile are contiguous.
-// ---------------------------------------------------------------------------------------
-
-__device__ __forceinline__ int kidx_of(int BKh, int s, int lane) { return BKh * (lane >> 5) + 8 * s; }
-
-template <LL L, int NR, int BK>
-__device__ __forceinline__ bf16x8 frag_k(const char* lds, int rr_base, int kidx, int lane) {
-  if constexpr (L == LL::KC) {
-    using G = KC<BK>;
-    const int r = rr_base + (lane & 31);
-    const int c = kidx >> 3;
-    const int off = r * G::kRowBytes + ((c ^ G::swz(r)) << 4);
-    return *reinterpret_cast<const bf16x8*>(lds + off);
-  } else {
-    using G = MC<NR>;
-    const int g2 = (lane >> 4) & 1, j = lane & 15;
-    const int n = rr_base + 16 * g2 + 4 * (j & 3);
-    const int c = n >> 3, half = (n >> 2) & 1;
-    s16x4 v[2];
-#pragma unroll
-    for (int rd = 0; rd < 2; ++rd) {
-      const int kr = kidx + 4 * rd + (j >> 2);
-      const int off = kr * G::kRowBytes + ((c ^ G::swz(kr)) << 4) + (half << 3);
-      v[rd] = __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(lds + off));
-    }
-    bf16x8 out;
-    __builtin_memcpy(&out, v, 16);
-    return out;
-  }
-}
-
-// Fragments of NB 32-row blocks of a K-contiguous operand for one k-tile, loaded by this lane.
-template <int NB, int BK>
-struct Direct {
-  static constexpr int KS = BK / 16;
-  const uint16_t* src[NB];
-  bool ok[NB];
-  __device__ __forceinline__ void init(const GOp& op, int rowbase, int lane) {
-#pragma unroll
-    for (int b = 0; b < NB; ++b) {
-      const int row = rowbase + 32 * b + (lane & 31);
-      ok[b] = row < op.rows;
-      int64_t grow = row;
-      if (op.rowidx) grow = ok[b] ? op.rowidx[row] : 0;
-      src[b] = op.base + grow * op.pitch + (BK / 2) * (lane >> 5);
-    }
-  }
-  __device__ __forceinline__ void load(const GOp& op, int k0, int lane, bf16x8 (&f)[NB][KS]) const {
-    const int kb = k0 + (BK / 2) * (lane >> 5);
-#pragma unroll
-    for (int b = 0; b < NB; ++b)
-#pragma unroll
-      for (int s = 0; s < KS; ++s) {
-        const bool valid = ok[b] && (kb + 8 * s < op.kmax);
-        const bf16x8* p = valid ? reinterpret_cast<const bf16x8*>(src[b] + k0 + 8 * s)
-                                : reinterpret_cast<const bf16x8*>(kZeroPage);
-        f[b][s] = *p;
-      }
-  }
-};
-
-// DIRECT = 1: A direct, B through LDS.  DIRECT = 2: B direct, A through LDS.
-template <int BR, int BC, int BK, LL LL_LDS, int DIRECT, int WR = 2, int WC = 2>
-struct GemmD {
-  static constexpr int NW = WR * WC;
-  static constexpr int kThreads = 64 * NW;
-  static constexpr int kBR = BR, kBC = BC;
-  static constexpr int FR = BR / WR / 32, FC = BC / WC / 32;
-  static constexpr int KS = BK / 16;
-  static constexpr int kLdsRows = (DIRECT == 1) ? BC : BR;
-  static constexpr int kStageBytes = kLdsRows * BK * 2;
-  static constexpr int ND = (DIRECT == 1) ? FR : FC;  // direct blocks per wave
-  static constexpr int NL = (DIRECT == 1) ? FC : FR;  // LDS blocks per wave
-  using CL = TileCopy<LL_LDS, kLdsRows, BK, NW>;
-  using DR = Direct<ND, BK>;
-
-  __device__ static __forceinline__ int row_of(int wave, int lane, int i, int r) {
-    return (wave / WC) * (BR / WR) + 32 * i + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-  }
-  __device__ static __forceinline__ int col_of(int wave, int lane, int j) {
-    return (wave % WC) * (BC / WC) + 32 * j + (lane & 31);
-  }
-
-  __device__ static __forceinline__ void compute(const char* stage, const bf16x8 (&d)[ND][KS], int wave, int lane,
-                                                 f32x16 (&acc)[FR][FC]) {
-    const int wr0 = (wave / WC) * (BR / WR);
-    const int wc0 = (wave % WC) * (BC / WC);
-#pragma unroll
-    for (int s = 0; s < KS; ++s) {
-      const int kidx = kidx_of(BK / 2, s, lane);
-      bf16x8 l[NL];
-#pragma unroll
-      for (int t = 0; t < NL; ++t)
-        l[t] = frag_k<LL_LDS, kLdsRows, BK>(stage, (DIRECT == 1 ? wc0 : wr0) + 32 * t, kidx, lane);
-#pragma unroll
-      for (int i = 0; i < FR; ++i)
-#pragma unroll
-        for (int j = 0; j < FC; ++j) {
-          if constexpr (DIRECT == 1)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(d[i][s], l[j], acc[i][j], 0, 0, 0);
-          else
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(l[i], d[j][s], acc[i][j], 0, 0, 0);
-        }
-    }
-  }
-
-  // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here).
-  // A and B as in Gemm; the direct operand must be KC.  All kThreads threads must call.
-  __device__ static __forceinline__ void run(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
-                                             char* st0, char* st1, f32x16 (&acc)[FR][FC]) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-#pragma unroll
-    for (int i = 0; i < FR; ++i)
-#pragma unroll
-      for (int j = 0; j < FC; ++j)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-    const GOp& OL = (DIRECT == 1) ? B : A;
-    const GOp& OD = (DIRECT == 1) ? A : B;
-    const int lbase = (DIRECT == 1) ? col0 : row0;
-    const int dbase = (DIRECT == 1) ? row0 + (wave / WC) * (BR / WR) : col0 + (wave % WC) * (BC / WC);
-    const int nk = (kend - kbeg + BK - 1) / BK;
-    CL cl;
-    DR dr;
-    cl.init(OL, lbase, wave, lane);
-    dr.init(OD, dbase, lane);
-    bf16x8 d0[ND][KS], d1[ND][KS];
-    __builtin_amdgcn_s_barrier();  // previous users of st0/st1 are done
-    if (nk <= 0) return;
-    cl.issue(OL, kbeg, st0, wave);
-    dr.load(OD, kbeg, lane, d0);
-    wait_vmcnt<0>();
+    wait_vmcnt<(NS - 1) * CPW>();
     __builtin_amdgcn_s_barrier();
-    const int npairs = nk >> 1;
-    for (int p = 0; p < npairs; ++p) {
-      const int kt = 2 * p;
-      cl.issue(OL, kbeg + (kt + 1) * BK, st1, wave);
-      dr.load(OD, kbeg + (kt + 1) * BK, lane, d1);
-      compute(st0, d0, wave, lane, acc);
-      wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
-      if (kt + 2 < nk) {
-        cl.issue(OL, kbeg + (kt + 2) * BK, st0, wave);
-        dr.load(OD, kbeg + (kt + 2) * BK, lane, d0);
-      }
-      compute(st1, d1, wave, lane, acc);
-      wait_vmcnt<0>();
-      __builtin_amdgcn_s_barrier();
+    Frags f0, f1;
+    load(st[0], 0, wave, lane, f0);
+    const int nkp = (nk + NS - 1) / NS * NS;
+    int knext = kbeg + NS * BK;  // k of the next tile to copy
+    auto issue = [&](char* stage) {
+      ca.issue(A, knext, klimA, stage, wave);
+      cb.issue(B, knext, klimB, stage + kABytes, wave);
+      knext += BK;
+    };
+    for (int t = 0; t < nkp; t += NS) {
+      ktile<0>(st, wave, lane, acc, f0, f1, issue);
+      ktile<1 % NS>(st, wave, lane, acc, f0, f1, issue);
+      if constexpr (NS >= 3) ktile<2 % NS>(st, wave, lane, acc, f0, f1, issue);
+      if constexpr (NS >= 4) ktile<3 % NS>(st, wave, lane, acc, f0, f1, issue);
     }
-    if (nk & 1) compute(st0, d0, wave, lane, acc);
+    wait_vmcnt<0>();                      // the copies past the end (zeros) have landed
+    __builtin_amdgcn_s_waitcnt(0xC07F);   // and this wave's last (unused) fragment reads
+    __builtin_amdgcn_s_barrier();         // before anyone reuses the stages
+  }
+
+  // A sequence of ntiles output tiles over k in [0, K): tile i uses A rows from
+  // row0 + i * BR and the same B rows (col0).  One copy pipeline runs through the tile
+  // boundaries; epi(i, acc) is called after tile i's last product, while the next tile's
+  // copies are in flight, and must not touch the LDS stages.  No row gather on A.
+  template <class Epi>
+  __device__ static __forceinline__ void run_seq(const GOp& A, const GOp& B, int row0, int col0, int ntiles, int K,
+                                                 char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi) {
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    zero(acc);
+    const int nk = (K + BK - 1) / BK;
+    if (nk <= 0 || ntiles <= 0) return;
+    const int klimA = min(A.kmax, K), klimB = min(B.kmax, K);
+    CA ca;
+    CB cb;
+    ca.init(A, row0, wave, lane);
+    cb.init(B, col0, wave, lane);
+    int ctile = 0, ck = 0;  // copy stream position
+    auto issue = [&](char* stage) {
+      if (ck == nk) {
+        ck = 0;
+        ++ctile;
+        ca.retarget(A, row0 + ctile * BR, wave, lane);
+      }
+      const bool live = ctile < ntiles;
+      ca.issue(A, ck * BK, live ? klimA : 0, stage, wave);
+      cb.issue(B, ck * BK, live ? klimB : 0, stage + kABytes, wave);
+      ++ck;
+    };
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) issue(st[s]);
+    wait_vmcnt<(NS - 1) * CPW>();
+    __builtin_amdgcn_s_barrier();
+    Frags f0, f1;
+    load(st[0], 0, wave, lane, f0);
+    const int total = ntiles * nk;
+    const int totalp = (total + NS - 1) / NS * NS;
+    int tile = 0, kt = 0;  // compute stream position
+    auto after = [&]() {
+      if (++kt == nk) {
+        if (tile < ntiles) epi(tile, acc);
+        zero(acc);
+        kt = 0;
+        ++tile;
+      }
+    };
+    for (int g = 0; g < totalp; g += NS) {
+      ktile<0>(st, wave, lane, acc, f0, f1, issue);
+      after();
+      ktile<1 % NS>(st, wave, lane, acc, f0, f1, issue);
+      after();
+      if constexpr (NS >= 3) {
+        ktile<2 % NS>(st, wave, lane, acc, f0, f1, issue);
+        after();
+      }
+      if constexpr (NS >= 4) {
+        ktile<3 % NS>(st, wave, lane, acc, f0, f1, issue);
+        after();
+      }
+    }
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
   }
 };
 

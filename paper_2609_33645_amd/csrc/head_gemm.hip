@@ -128,23 +128,44 @@ lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ 
   }
 }
 
-__global__ void lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
-                                    float2* __restrict__ lam2) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= M) return;
-  double mx = -INFINITY;
-  bool nan = false;
-  for (int p = 0; p < P; ++p) {
-    const float2 q = partials[static_cast<int64_t>(p) * M + m];
-    if (q.x != q.x || q.y != q.y) nan = true;
-    mx = fmax(mx, static_cast<double>(q.x));
-  }
+// lambda_m from the per-partition (max, sum) pairs: 64 frames per block, the partitions
+// split over 4 thread phases; the maximum is exact, the rescaled sum is accumulated in
+// double (each term's exponent taken in float on the exact difference to the maximum).
+__global__ void __launch_bounds__(256)
+lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
+                    float2* __restrict__ lam2) {
+  __shared__ float smax[4][64];
+  __shared__ double ssum[4][64];
+  __shared__ int snan[4][64];
+  const int t = threadIdx.x & 63, ph = threadIdx.x >> 6;
+  const int m = blockIdx.x * 64 + t;
+  float mx = -INFINITY;
+  int nan = 0;
+  if (m < M)
+    for (int p = ph; p < P; p += 4) {
+      const float2 q = partials[static_cast<int64_t>(p) * M + m];
+      nan |= (q.x != q.x) | (q.y != q.y);
+      mx = fmaxf(mx, q.x);
+    }
+  smax[ph][t] = mx;
+  snan[ph][t] = nan;
+  __syncthreads();
+  mx = fmaxf(fmaxf(smax[0][t], smax[1][t]), fmaxf(smax[2][t], smax[3][t]));
+  nan = snan[0][t] | snan[1][t] | snan[2][t] | snan[3][t];
   double s = 0.0;
-  for (int p = 0; p < P; ++p) {
-    const float2 q = partials[static_cast<int64_t>(p) * M + m];
-    if (q.x != -INFINITY) s += static_cast<double>(q.y) * exp(static_cast<double>(q.x) - mx);
-  }
-  double l = mx + log(s);
+  if (m < M && mx != -INFINITY)
+    for (int p = ph; p < P; p += 4) {
+      const float2 q = partials[static_cast<int64_t>(p) * M + m];
+      if (q.x != -INFINITY)
+        s += static_cast<double>(q.y) *
+             static_cast<double>(fast_exp2(static_cast<float>(static_cast<double>(q.x) - mx) * kLog2e));
+    }
+  ssum[ph][t] = s;
+  __syncthreads();
+  if (ph != 0 || m >= M) return;
+  s = (ssum[0][t] + ssum[1][t]) + (ssum[2][t] + ssum[3][t]);
+  double l = static_cast<double>(mx) + log(s);
+  if (mx == -INFINITY) l = -INFINITY;
   if (nan) l = __longlong_as_double(0x7ff8000000000000LL);
   lam[m] = l;
   const double l2 = l * kLog2eD;
@@ -202,8 +223,7 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   Prof pr("lse_finalize", stream);
-  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Pfin, lam,
-                     lam2);
+  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 63) / 64), dim3(256), 0, stream, partials, M, Pfin, lam, lam2);
   return hipGetLastError();
 }
 
@@ -537,8 +557,9 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const 
 }
 
 static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, const float2* lam2,
-                                const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
-                                char* scratch, const BwdPlan& plan, hipStream_t stream) {
+                                const float* G, int ldG, const float* g, const int32_t* remap, const float* S,
+                                int ldS, float* dH, float* dW, char* scratch, const BwdPlan& plan,
+                                hipStream_t stream) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
   uint16_t* Hs = reinterpret_cast<uint16_t*>(scratch + plan.dz_bytes);
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
@@ -555,8 +576,8 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   }
   for (int c0 = 0; c0 < V; c0 += chunk) {
     const int cw = min(chunk, V - c0);
-    e = launch_bwd_chunk_bf16(H, Hs, M, D, W, c0, cw, lam2, G, ldG, g, remap, dZ, chunk, part, slice, dH != nullptr,
-                              dW != nullptr, dW, stream);
+    e = launch_bwd_chunk_bf16(H, Hs, M, D, W, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+                              dH != nullptr, dW != nullptr, dW, stream);
     if (e != hipSuccess) return e;
   }
   if (dH) {
@@ -569,8 +590,8 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
 }
 
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
-                           const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
-                           void* scratch, const BwdPlan& plan, hipStream_t stream) {
+                           const float* G, int ldG, const float* g, const int32_t* remap, const float* S, int ldS,
+                           float* dH, float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream) {
   if (M <= 0) {
     if (dW) return hipMemsetAsync(dW, 0, static_cast<size_t>(V) * D * sizeof(float), stream);
     return hipSuccess;
@@ -578,7 +599,7 @@ hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W
   char* sc = static_cast<char*>(scratch);
   if (dtype == 1)
     return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, lam2, G, ldG, g,
-                         remap, dH, dW, sc, plan, stream);
+                         remap, S, ldS, dH, dW, sc, plan, stream);
   return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, lam2, G, ldG, g,
                            remap, dH, dW, sc, plan, stream);
 }

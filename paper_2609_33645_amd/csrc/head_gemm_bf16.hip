@@ -24,19 +24,26 @@ constexpr int kFC = 128;  // frames per forward/recompute tile
 constexpr int kFK = 32;   // k per stage
 constexpr int kBR = 256;  // backward tile rows (dH: frames, dW: vocabulary)
 constexpr int kBC = 256;  // backward tile columns (D)
-constexpr int kBK = 64;
+constexpr int kBK = 32;
 
 // 4 wavefronts (2 x 2), two workgroups per CU so that one's epilogue overlaps the
 // other's products
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
-// 8 wavefronts (2 x 4), two stages of 256 x 64 + 256 x 64
-using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 2, 2, 4>;
-using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 2, 2, 4>;
+// 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
+using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4>;
+using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4>;
 
 #define PCTC_STAGES2(G)                                                  \
   __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
   __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
   char* const st[2] = {st0_, st1_};
+
+#define PCTC_STAGES4(G)                                                  \
+  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st2_[G::kStageBytes]; \
+  __shared__ __attribute__((aligned(1024))) char st3_[G::kStageBytes]; \
+  char* const st[4] = {st0_, st1_, st2_, st3_};
 
 #define PCTC_STAGES(G)                                                   \
   __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
@@ -131,13 +138,14 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
     run_sum[j] = 0.f;
   }
   f32x16 acc[FR][FC];
-  for (int v0 = vbeg; v0 < vend; v0 += kFR) {
-    G::run(A, B, v0, m0, 0, D, st, acc);
+  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
+  G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, [&](int i, const f32x16 (&a)[FR][FC]) {
+    const int v0 = vbeg + i * kFR;
     if (v0 + kFR <= vend)
-      lse_tile_update<false, FR, FC>(acc, run_max, run_sum, v0, vend, wave, lane);
+      lse_tile_update<false, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
     else
-      lse_tile_update<true, FR, FC>(acc, run_max, run_sum, v0, vend, wave, lane);
-  }
+      lse_tile_update<true, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+  });
   __syncthreads();
   // the two wavefronts of each frame column (row halves) combine their partial sums
   float2* xch = reinterpret_cast<float2*>(st0_);
@@ -196,43 +204,23 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
   }
 }
 
-// dZ chunk [M][chunk] (row pitch `chunk`): columns [0, cw) hold scatter_U(G) - g p for
-// vocabulary ids c0.., columns [cw, tile end) hold 0.  Each 256 x 128 tile is staged through
-// LDS so that every frame row is stored as contiguous 16-byte vectors.
-template <bool FULL>
-__device__ __forceinline__ void dz_values_(const f32x16 (&acc)[GFwd::FR][GFwd::FC], int j, int i, int q, float gm,
-                                          float2 l2, bool inc, int vl0, int cw, int any_sel, const int* sel,
-                                          const float* Grow, int wave, int lane, uint32_t (&o)[2]) {
-  const int rl0 = GFwd::row_of(wave, lane, i, 4 * q);
-  float val[4];
-#pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int rl = rl0 + e;
-    float v = 0.f;
-    if (inc && (FULL || vl0 + rl < cw)) {
-      const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -l2.x) - l2.y;
-      v = -gm * fast_exp2(t);
-      if (any_sel) {
-        const int jj = sel[rl];
-        if (jj >= 0) v += Grow[jj];
-      }
-    }
-    val[e] = v;
-  }
-  o[0] = static_cast<uint32_t>(f32_to_bf16(val[0])) | (static_cast<uint32_t>(f32_to_bf16(val[1])) << 16);
-  o[1] = static_cast<uint32_t>(f32_to_bf16(val[2])) | (static_cast<uint32_t>(f32_to_bf16(val[3])) << 16);
-}
-
+// dZ chunk [M][chunk] (row pitch `chunk`): dZ[m][v] = scatter_U(G)[m][v] - g_m p_v(m) for
+// the chunk's 256-column tiles (Eq. vjp; zero on excluded frames).  The dense part -g p
+// comes from the recomputed logits; the few union columns of a tile are then rewritten
+// in the staging buffer as G[m][j] - g_m exp(S[m][j]) from the forward's selected
+// log-probabilities.  Columns past cw within the last tile hold finite values that no
+// consumer reads (their W rows read as zero).  Each 256 x 128 tile is staged through LDS
+// so that every frame row is stored as contiguous 16-byte vectors.
 __global__ void __launch_bounds__(256, 2)
 recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
-                  const float2* __restrict__ lam2, const float* __restrict__ G, int ldG, const float* __restrict__ g,
-                  const int32_t* __restrict__ remap, uint16_t* __restrict__ dZ, int chunk) {
+                  const float2* __restrict__ lam2, const float* __restrict__ g, const int32_t* __restrict__ remap,
+                  const float* __restrict__ S, int ldS, const float* __restrict__ G, int ldG,
+                  uint16_t* __restrict__ dZ, int chunk) {
   using GG = GFwd;
   constexpr int FR = GG::FR, FC = GG::FC;
   constexpr int kPitch = kFR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
   static_assert(32 * kPitch <= GG::kStageBytes, "staging fits one stage");
   PCTC_STAGES(GG)
-  __shared__ int sel[kFR];
   const int nMt = (M + kFC - 1) / kFC;
   const int nVt = (cw + kFR - 1) / kFR;
   int mt, vt;
@@ -240,41 +228,72 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   const int m0 = mt * kFC;
   const int vl0 = vt * kFR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  {
-    const int vl = vl0 + tid;
-    sel[tid] = (vl < cw) ? remap[c0 + vl] : -1;
+  // union columns of this tile: (tile column, union index) pairs
+  __shared__ int ulist[kFR];
+  __shared__ int nu;
+  if (tid == 0) nu = 0;
+  const int vl = vl0 + tid;
+  const int jsel = (vl < cw) ? remap[c0 + vl] : -1;
+  const int any_sel = __syncthreads_or(jsel >= 0);
+  if (any_sel) {
+    if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
+    __syncthreads();
   }
-  const int any_sel = __syncthreads_or(sel[tid] >= 0);
+  // this lane's frames: -g_m (0 when excluded) and the hi/lo parts of lambda_m log2(e)
+  float ng[FC], lx[FC], ly[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const int m = m0 + GG::col_of(wave, lane, j);
+    const bool mok = m < M;
+    const float gm = mok ? g[m] : 0.f;
+    const float2 l2 = mok ? lam2[m] : make_float2(0.f, 0.f);
+    ng[j] = -gm;
+    lx[j] = l2.x;
+    ly[j] = l2.y;
+  }
   const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
   const GOp B{H, D, M, D, nullptr};
   f32x16 acc[FR][FC];
   GG::run(A, B, vl0, m0, 0, D, st, acc);
-  const bool full = vl0 + kFR <= cw;
+  const int nunion = any_sel ? nu : 0;
   const int ch = wave & 1;            // column half: frames [64 ch, 64 ch + 64) of the tile
   char* stage = ch ? st1_ : st0_;     // 32 frames x 256 vocabulary columns per pass
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
-    __syncthreads();  // previous pass's readers (and the product's last reads) are done
-    const int mloc = 64 * ch + 32 * j + (lane & 31);
-    const int m = m0 + mloc;
-    const bool mok = m < M;
-    const float gm = mok ? g[m] : 0.f;
-    const float2 l2 = mok ? lam2[m] : make_float2(0.f, 0.f);
-    const bool inc = mok && (gm != 0.f);
-    const float* Grow = G + static_cast<int64_t>(mok ? m : 0) * ldG;
+    if (j > 0) __syncthreads();  // the previous pass's readers are done
+    const bool inc = ng[j] != 0.f;
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        uint32_t o[2];
-        if (full)
-          dz_values_<true>(acc, j, i, q, gm, l2, inc, vl0, cw, any_sel, sel, Grow, wave, lane, o);
-        else
-          dz_values_<false>(acc, j, i, q, gm, l2, inc, vl0, cw, any_sel, sel, Grow, wave, lane, o);
-        const int rl0 = GFwd::row_of(wave, lane, i, 4 * q);
-        *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) = u32x2{o[0], o[1]};
+        float v[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -lx[j]) - ly[j];
+          v[e] = inc ? ng[j] * fast_exp2(t) : 0.f;
+        }
+        const int rl0 = GG::row_of(wave, lane, i, 4 * q);
+        *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) =
+            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       }
     __syncthreads();
+    if (nunion > 0) {
+      // the union columns of the 2 x 32 staged frames
+      for (int idx = tid; idx < nunion * 64; idx += 256) {
+        const int e = ulist[idx >> 6];
+        const int col = e & 255, ju = e >> 8;
+        const int half = (idx >> 5) & 1, row = idx & 31;
+        const int m = m0 + 64 * half + 32 * j + row;
+        float val = 0.f;
+        if (m < M) {
+          const float gm = g[m];
+          if (gm != 0.f)
+            val = G[static_cast<int64_t>(m) * ldG + ju] - gm * fast_exp2(S[static_cast<int64_t>(m) * ldS + ju] * kLog2e);
+        }
+        *reinterpret_cast<uint16_t*>((half ? st1_ : st0_) + row * kPitch + col * 2) = f32_to_bf16(val);
+      }
+      __syncthreads();
+    }
     // 2 stages x 32 frames x 32 vectors of 16 bytes
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -295,7 +314,7 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
              int slice, float* __restrict__ part) {
   using G = GDh;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES2(G)
+  PCTC_STAGES4(G)
   const int nMt = (M + kBR - 1) / kBR;
   const int nDt = (D + kBC - 1) / kBC;
   // d-tiles fastest: the workgroups that read the same dZ rows run together on one XCD
@@ -333,7 +352,7 @@ dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
              float* __restrict__ dW) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES2(G)
+  PCTC_STAGES4(G)
   const int nDt = (D + kBC - 1) / kBC;
   const int work = xcd_swz(blockIdx.x, gridDim.x);
   const int dt = work % nDt;
@@ -375,8 +394,8 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
 // ---------------------------------------------------------------------------------------
 
 int lse_partitions_bf16(int M, int V) {
-  const int nMt = (M + kFC - 1) / kFC;
-  int P = (2048 + nMt - 1) / nMt;  // a few waves of two workgroups per CU
+  (void)M;
+  int P = 256;  // runs of a few vocabulary tiles per workgroup
   const int vtiles = (V + kFR - 1) / kFR;
   if (P > vtiles) P = vtiles;
   if (P > 256) P = 256;
@@ -411,14 +430,14 @@ hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t*
 
 hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
-                                 const int32_t* remap, uint16_t* dZ, int chunk, float* part, int slice, bool want_dH,
-                                 bool want_dW, float* dW, hipStream_t stream) {
+                                 const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
+                                 int slice, bool want_dH, bool want_dW, float* dW, hipStream_t stream) {
   const int nMt = (M + kFC - 1) / kFC;
-  const int nVt = (cw + kFR - 1) / kFR;
   {
+    const int nVt = (cw + kFR - 1) / kFR;
     Prof pr("recompute_dz", stream);
-    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, H, M, D, W, c0,
-                       cw, lam2, G, ldG, g, remap, dZ, chunk);
+    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, H, M, D, W,
+                       c0, cw, lam2, g, remap, S, ldS, G, ldG, dZ, chunk);
   }
   if (want_dH) {
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);

@@ -268,7 +268,7 @@ int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const voi
     PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
   // backward: chunk by chunk recomputation
   if (dH || dW)
-    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, V, lam2, G, L.ldS, g, remap, dH, dW, bws, L.bwd, stream));
+    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, bws, L.bwd, stream));
   int32_t herr = 0;
   PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
@@ -342,10 +342,26 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
   return PCTC_OK;
 }
 
-size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || chunk < 0 || (chunk > 0 && chunk % 256))
+// Stage entry scratch: the backward plan, then u_ids [ldG], K, and S [M][ldG].
+struct BwdStageLayout {
+  BwdPlan plan;
+  size_t o_uids, o_K, o_S, total;
+};
+static BwdStageLayout bwd_stage_layout(int dt, int M, int D, int ldG, int chunk) {
+  BwdStageLayout b;
+  b.plan = plan_bwd(dt, M, D, chunk);
+  b.o_uids = b.plan.total;
+  b.o_K = b.o_uids + align_up(static_cast<size_t>(ldG) * 4, 256);
+  b.o_S = b.o_K + 256;
+  b.total = b.o_S + align_up(static_cast<size_t>(M) * ldG * 4, 256);
+  return b;
+}
+
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ldG, int32_t chunk) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || ldG < 1 || chunk < 0 ||
+      (chunk > 0 && chunk % 256))
     return 0;
-  return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, chunk).total;
+  return bwd_stage_layout(dtype == PCTC_BF16 ? 1 : 0, M, D, ldG, chunk).total;
 }
 
 int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk) {
@@ -358,16 +374,25 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
                       const double* lam, const float* G, int32_t ldG, const float* g, const int32_t* remap,
                       int32_t chunk, float* dH, float* dW, void* bwd_scratch, void* stream_ptr) {
   if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || V <= 1 || chunk < 0 ||
-      (chunk > 0 && chunk % 256) || !W || !bwd_scratch)
+      (chunk > 0 && chunk % 256) || !W || !bwd_scratch || ldG < 1)
     return PCTC_EINVAL;
-  if (M > 0 && (!H || !lam || !G || !g || !remap || ldG < 1)) return PCTC_EINVAL;
+  if (M > 0 && (!H || !lam || !G || !g || !remap)) return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
-  const BwdPlan plan = plan_bwd(dt, M, D, chunk);
-  float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(bwd_scratch) + plan.dz_bytes + plan.ht_bytes +
-                                           plan.part_bytes);
+  const BwdStageLayout b = bwd_stage_layout(dt, M, D, ldG, chunk);
+  const BwdPlan& plan = b.plan;
+  char* sc = static_cast<char*>(bwd_scratch);
+  float2* lam2 = reinterpret_cast<float2*>(sc + plan.dz_bytes + plan.ht_bytes + plan.part_bytes);
+  int32_t* u_ids = reinterpret_cast<int32_t*>(sc + b.o_uids);
+  int32_t* Kdev = reinterpret_cast<int32_t*>(sc + b.o_K);
+  float* S = reinterpret_cast<float*>(sc + b.o_S);
   PCTC_HIP(launch_lam2(lam, M, lam2, stream));
-  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, V, lam2, G, ldG, g, remap, dH, dW, bwd_scratch, plan, stream));
+  if (dt == 1 && M > 0) {
+    // the union and its selected log-probabilities, as the forward would have left them
+    PCTC_HIP(launch_remap_invert(remap, V, u_ids, Kdev, stream));
+    PCTC_HIP(launch_gather_s(dt, H, M, D, W, u_ids, Kdev, ldG, lam, S, ldG, stream));
+  }
+  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, V, lam2, G, ldG, g, remap, S, ldG, dH, dW, bwd_scratch, plan, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
   prof_flush();
   return PCTC_OK;

@@ -28,6 +28,14 @@ __device__ __forceinline__ uint16_t f32_to_bf16(float f) {
   return static_cast<uint16_t>(u >> 16);
 }
 
+// Two floats rounded to bfloat16 (nearest even) and packed, the first in the low half.
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) float f2_;
+  typedef __attribute__((ext_vector_type(2))) __bf16 b2_;
+  const b2_ b = __builtin_convertvector(f2_{lo, hi}, b2_);
+  return __builtin_bit_cast(uint32_t, b);
+}
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 __device__ __forceinline__ float fast_log2(float x) { return __builtin_amdgcn_logf(x); }
 

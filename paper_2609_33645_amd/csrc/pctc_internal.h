@@ -25,6 +25,8 @@ constexpr float kKeepSlack = 1e-3f;  // nats added to the beam threshold (tie/ro
 inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 
 // ---- union / relabel -------------------------------------------------------------------
+// u_ids[remap[v]] = v for remap[v] >= 0 and K = 1 + max remap (K zeroed here).
+hipError_t launch_remap_invert(const int32_t* remap, int32_t V, int32_t* u_ids, int32_t* K, hipStream_t stream);
 hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t blank, int32_t V,
                               int32_t* remap, int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err,
                               hipStream_t stream);
@@ -46,9 +48,11 @@ struct BwdPlan {
   size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int chunk);
+// S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
+// of each recomputed chunk from them).
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
-                           const float* G, int ldG, const float* g, const int32_t* remap, float* dH,
-                           float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream);
+                           const float* G, int ldG, const float* g, const int32_t* remap, const float* S, int ldS,
+                           float* dH, float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream);
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
 
 // ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
@@ -58,8 +62,8 @@ hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t*
                                 const int32_t* K, int K_max, const double* lam, float* S, int ldS, hipStream_t stream);
 hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
-                                 const int32_t* remap, uint16_t* dZ, int chunk, float* part, int slice, bool want_dH,
-                                 bool want_dW, float* dW, hipStream_t stream);
+                                 const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
+                                 int slice, bool want_dH, bool want_dW, float* dW, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
 
 // ---- alignment lattice ------------------------------------------------------------------

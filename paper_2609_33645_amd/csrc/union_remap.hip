@@ -97,4 +97,24 @@ hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t bla
   return hipGetLastError();
 }
 
+// Inverse of a remap table: u_ids[remap[v]] = v and K = 1 + max remap.
+__global__ void remap_invert_kernel(const int32_t* __restrict__ remap, int32_t V, int32_t* __restrict__ u_ids,
+                                    int32_t* __restrict__ K) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= V) return;
+  const int r = remap[v];
+  if (r >= 0) {
+    u_ids[r] = v;
+    atomicMax(K, r + 1);
+  }
+}
+
+hipError_t launch_remap_invert(const int32_t* remap, int32_t V, int32_t* u_ids, int32_t* K, hipStream_t stream) {
+  hipError_t e = hipMemsetAsync(K, 0, sizeof(int32_t), stream);
+  if (e != hipSuccess) return e;
+  Prof p("remap_invert", stream);
+  hipLaunchKernelGGL(remap_invert_kernel, dim3((V + 255) / 256), dim3(256), 0, stream, remap, V, u_ids, K);
+  return hipGetLastError();
+}
+
 }  // namespace pctc

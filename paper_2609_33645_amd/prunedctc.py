@@ -65,7 +65,7 @@ def lib() -> ctypes.CDLL:
     L.pctc_dp_scratch_bytes.restype = c_sz
     L.pctc_ctc_dp.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, c_f, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_ctc_dp.restype = c_i32
-    L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32]
+    L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_scratch_bytes.restype = c_sz
     L.pctc_bwd_chunk.argtypes = [c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_chunk.restype = c_i32
@@ -284,7 +284,7 @@ def head_bwd(H: torch.Tensor, W: torch.Tensor, lam: torch.Tensor, G: torch.Tenso
     ldG = int(G.shape[1])
     dH = torch.empty((M, D), dtype=torch.float32, device=dev) if want_dH else None
     dW = torch.empty((V, D), dtype=torch.float32, device=dev) if want_dW else None
-    scratch = _workspace(int(L.pctc_bwd_scratch_bytes(dt, M, D, int(chunk))), dev)
+    scratch = _workspace(int(L.pctc_bwd_scratch_bytes(dt, M, D, ldG, int(chunk))), dev)
     code = L.pctc_head_bwd(dt, _ptr(H), M, D, _ptr(W), V, _ptr(lam.to(torch.float64).contiguous()), _ptr(G), ldG,
                            _ptr(g.to(torch.float32).contiguous()), _ptr(remap.to(torch.int32).contiguous()),
                            int(chunk), _ptr(dH), _ptr(dW), ctypes.c_void_p(scratch.data_ptr()), _stream(stream))
