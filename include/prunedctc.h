@@ -176,6 +176,10 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
  * end of each pruned_ctc_fwd_bwd call (which synchronises anyway).
  * ---------------------------------------------------------------------------------- */
 void pctc_prof_enable(int32_t on);
+/* Restrict timing to the kernels of one name (as reported by pctc_prof_get); NULL or ""
+ * times every kernel again.  Each timed launch is bracketed by two events, which keeps the
+ * launches around it from overlapping, so timing fewer kinds disturbs the run less. */
+void pctc_prof_select(const char* name);
 void pctc_prof_reset(void);
 int32_t pctc_prof_count(void);
 /* Name, total milliseconds and launch count of the i-th kernel kind; returns 0 if i is

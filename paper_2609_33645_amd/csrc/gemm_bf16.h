@@ -274,13 +274,15 @@ struct Gemm {
     }
   }
 
-  // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here).  All
-  // kThreads threads must call; contains barriers.  st[s]: kStageBytes each.  On return
-  // every copy has landed and every wave is past its last LDS read.
+  // Accumulates k in [kbeg, kend) (kbeg a multiple of BK) into acc (zeroed here unless
+  // ZERO is false, when acc holds starting values).  All kThreads threads must call;
+  // contains barriers.  st[s]: kStageBytes each.  On return every copy has landed and
+  // every wave is past its last LDS read.
+  template <bool ZERO = true>
   __device__ static __forceinline__ void run(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
                                              char* const (&st)[NS], f32x16 (&acc)[FR][FC]) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    zero(acc);
+    if constexpr (ZERO) zero(acc);
     const int nk = (kend - kbeg + BK - 1) / BK;
     if (nk <= 0) return;
     const int klimA = min(A.kmax, kend), klimB = min(B.kmax, kend);

@@ -471,18 +471,21 @@ BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
     p.chunk = chunk;
   } else {
     // default: the recomputed gradient chunk (M x chunk in the input dtype) takes about
-    // 256 MiB.  For bf16 the chunk is a multiple of q columns, where q makes the dW
-    // launch (256 x 256 tiles) a whole number of 256-workgroup waves.
+    // 512 MiB.  For bf16 the chunk is the nearest multiple of q columns when that is at
+    // least q, where q makes the dW launch (256 x 256 tiles) a whole number of
+    // 256-workgroup waves; otherwise a multiple of 256.
     const size_t es0 = (dtype == 1) ? 2 : 4;
-    size_t c = (static_cast<size_t>(256) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
+    size_t c = (static_cast<size_t>(512) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
+    if (c > 65536) c = 65536;
     size_t q = 4096;
     if (dtype == 1) {
       const int ndt = (D + 255) / 256;
       q = static_cast<size_t>(256) * ((256 + ndt - 1) / ndt);
     }
-    c = (c / q) * q;
-    if (c < q) c = q;
-    if (c > 65536) c = (65536 / q) * q > 0 ? (65536 / q) * q : q;
+    if (c >= q) c = (c + q / 2) / q * q;
+    else c = (c / 256) * 256;
+    if (c > 65536) c = 65536;
+    if (c < 256) c = 256;
     p.chunk = static_cast<int>(c);
   }
   const size_t es = (dtype == 1) ? 2 : 4;

@@ -312,6 +312,7 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
 __global__ void __launch_bounds__(512, 1)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
              int slice, float* __restrict__ part) {
+  const bool first = c0 == 0;
   using G = GDh;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES4(G)
@@ -330,9 +331,22 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
   // A: dZ rows (frames), k = vocabulary column; B: W_c viewed as rows d, k = vocabulary row
   const GOp A{dZ, chunk, M, cw, nullptr};
   const GOp B{W + static_cast<int64_t>(c0) * D, D, D, cw, nullptr};
-  f32x16 acc[FR][FC];
-  G::run(A, B, m0, d0, kb, ke, st, acc);
   float* dst = part + static_cast<int64_t>(s) * M * D;
+  // the accumulators start from this slice's partial sums of the earlier chunks (loaded
+  // before the copy pipeline starts, so their latency hides behind its first copies)
+  f32x16 acc[FR][FC];
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int d = d0 + G::col_of(wave, lane, j);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + G::row_of(wave, lane, i, r);
+        acc[i][j][r] = (first || d >= D || m >= M) ? 0.f : dst[static_cast<int64_t>(m) * D + d];
+      }
+    }
+  G::template run<false>(A, B, m0, d0, kb, ke, st, acc);
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
@@ -342,7 +356,7 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + G::row_of(wave, lane, i, r);
-        if (m < M) dst[static_cast<int64_t>(m) * D + d] += acc[i][j][r];
+        if (m < M) dst[static_cast<int64_t>(m) * D + d] = acc[i][j][r];
       }
     }
 }

@@ -25,6 +25,7 @@ struct ProfRec {
 struct ProfState {
   std::mutex mu;
   bool enabled = false;
+  std::string only;  // when non-empty, only kernels of this name are timed
   std::vector<hipEvent_t> pool;
   std::vector<ProfRec> pending;
   std::vector<std::string> names;
@@ -51,6 +52,7 @@ Prof::Prof(const char* name, hipStream_t st) : slot(-1), stream(st) {
   ProfState& s = prof_state();
   if (!s.enabled) return;
   std::lock_guard<std::mutex> lk(s.mu);
+  if (!s.only.empty() && s.only != name) return;
   ProfRec r{name, take_event(s), take_event(s)};
   if (!r.start || !r.stop) return;
   hipEventRecord(r.start, stream);
@@ -399,6 +401,12 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
 }
 
 void pctc_prof_enable(int32_t on) { prof_state().enabled = (on != 0); }
+
+void pctc_prof_select(const char* name) {
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  s.only = name ? name : "";
+}
 
 void pctc_prof_reset(void) {
   ProfState& s = prof_state();

@@ -73,6 +73,7 @@ def lib() -> ctypes.CDLL:
                                 c_p, c_p]
     L.pctc_head_bwd.restype = c_i32
     L.pctc_prof_enable.argtypes = [c_i32]
+    L.pctc_prof_select.argtypes = [ctypes.c_char_p]
     L.pctc_prof_reset.argtypes = []
     L.pctc_prof_count.argtypes = []
     L.pctc_prof_count.restype = c_i32
@@ -296,6 +297,11 @@ def head_bwd(H: torch.Tensor, W: torch.Tensor, lam: torch.Tensor, G: torch.Tenso
 
 def prof_enable(on: bool = True) -> None:
     lib().pctc_prof_enable(1 if on else 0)
+
+
+def prof_select(name: Optional[str] = None) -> None:
+    """Time only the kernels called `name` (None: all of them)."""
+    lib().pctc_prof_select(name.encode() if name else None)
 
 
 def prof_reset() -> None:
