@@ -208,13 +208,18 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
   const int* y = y_rel + y0;
   const Acc neg = kNeg;
 
+  // The blank column index is an opaque per-lane zero: with a literal 0 the compiler would
+  // turn the (uniform) blank emission load into a scalar load and wait for it on the spot,
+  // defeating the prefetch ring.
+  int zero_v;
+  asm volatile("v_mov_b32 %0, 0" : "=v"(zero_v));
   int col[Q];
   bool valid[Q], skip_in[Q], skip_out[Q], fin[Q];
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
     const int s = lane * Q + q;
     valid[q] = s < Sp;
-    col[q] = (valid[q] && (s & 1)) ? y[(s - 1) >> 1] : 0;
+    col[q] = (valid[q] && (s & 1)) ? y[(s - 1) >> 1] : zero_v;
     skip_in[q] = valid[q] && (s & 1) && s >= 3 && y[(s - 1) >> 1] != y[(s - 3) >> 1];
     const int s2 = s + 2;
     skip_out[q] = (s2 < Sp) && (s2 & 1) && y[(s2 - 1) >> 1] != y[(s2 - 3) >> 1];
@@ -226,7 +231,7 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     const uint8_t* mrow = mask ? mask + base + static_cast<int64_t>(t) * Sp + lane * Q : nullptr;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-      e[q] = valid[q] ? row[col[q]] : 0.f;
+      e[q] = row[col[q]];  // invalid states read the blank column (a valid address)
       mk[q] = valid[q] ? (mrow ? static_cast<int>(mrow[q]) : 0x0f) : 0;
     }
   };
