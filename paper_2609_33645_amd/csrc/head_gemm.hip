@@ -568,10 +568,9 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
   const int chunk = plan.chunk;
   hipError_t e;
-  if (dW) {
-    e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
-    if (e != hipSuccess) return e;
-  }
+  // Hs: H with the rows of excluded frames zeroed (read by the recompute and by dW)
+  e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
+  if (e != hipSuccess) return e;
   const int slice = ((chunk / plan.splits + 63) / 64) * 64;
   if (dH) {
     e = hipMemsetAsync(part, 0, static_cast<size_t>(plan.splits) * M * D * sizeof(float), stream);

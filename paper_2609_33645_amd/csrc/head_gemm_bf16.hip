@@ -206,13 +206,14 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
 
 // dZ chunk [M][chunk] (row pitch `chunk`): dZ[m][v] = scatter_U(G)[m][v] - g_m p_v(m) for
 // the chunk's 256-column tiles (Eq. vjp; zero on excluded frames).  The dense part -g p
-// comes from the recomputed logits; the few union columns of a tile are then rewritten
-// in the staging buffer as G[m][j] - g_m exp(S[m][j]) from the forward's selected
-// log-probabilities.  Columns past cw within the last tile hold finite values that no
-// consumer reads (their W rows read as zero).  Each 256 x 128 tile is staged through LDS
-// so that every frame row is stored as contiguous 16-byte vectors.
+// comes from the recomputed logits of Hs (H with excluded rows zeroed, so their products
+// are finite and, with g_m = 0, give zeros); the few union columns of a tile are then
+// rewritten in the staging buffer as G[m][j] - g_m exp(S[m][j]) from the forward's
+// selected log-probabilities.  Columns past cw within the last tile hold finite values
+// that no consumer reads (their W rows read as zero).  Each 256 x 128 tile is staged
+// through LDS so that every frame row is stored as contiguous 16-byte vectors.
 __global__ void __launch_bounds__(256, 2)
-recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
+recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
                   const float2* __restrict__ lam2, const float* __restrict__ g, const int32_t* __restrict__ remap,
                   const float* __restrict__ S, int ldS, const float* __restrict__ G, int ldG,
                   uint16_t* __restrict__ dZ, int chunk) {
@@ -228,31 +229,28 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   const int m0 = mt * kFC;
   const int vl0 = vt * kFR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // union columns of this tile: (tile column, union index) pairs
+  // union columns of this tile: (union index << 8) | tile column
   __shared__ int ulist[kFR];
   __shared__ int nu;
   if (tid == 0) nu = 0;
-  const int vl = vl0 + tid;
-  const int jsel = (vl < cw) ? remap[c0 + vl] : -1;
+  const int jsel = (vl0 + tid < cw) ? remap[c0 + vl0 + tid] : -1;
   const int any_sel = __syncthreads_or(jsel >= 0);
   if (any_sel) {
     if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
     __syncthreads();
   }
-  // this lane's frames: -g_m (0 when excluded) and the hi/lo parts of lambda_m log2(e)
-  float ng[FC], lx[FC], ly[FC];
+  // this lane's frames: -g_m and lambda_m log2(e) (both zero on excluded frames)
+  float ng[FC], ll[FC];
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     const int m = m0 + GG::col_of(wave, lane, j);
-    const bool mok = m < M;
-    const float gm = mok ? g[m] : 0.f;
-    const float2 l2 = mok ? lam2[m] : make_float2(0.f, 0.f);
+    const float gm = (m < M) ? g[m] : 0.f;
+    const float2 l2 = (m < M) ? lam2[m] : make_float2(0.f, 0.f);
     ng[j] = -gm;
-    lx[j] = l2.x;
-    ly[j] = l2.y;
+    ll[j] = (gm != 0.f) ? l2.x + l2.y : 0.f;
   }
   const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
-  const GOp B{H, D, M, D, nullptr};
+  const GOp B{Hs, D, M, D, nullptr};
   f32x16 acc[FR][FC];
   GG::run(A, B, vl0, m0, 0, D, st, acc);
   const int nunion = any_sel ? nu : 0;
@@ -261,17 +259,13 @@ recompute_dz_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     if (j > 0) __syncthreads();  // the previous pass's readers are done
-    const bool inc = ng[j] != 0.f;
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -lx[j]) - ly[j];
-          v[e] = inc ? ng[j] * fast_exp2(t) : 0.f;
-        }
+        for (int e = 0; e < 4; ++e) v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ll[j]));
         const int rl0 = GG::row_of(wave, lane, i, 4 * q);
         *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) =
             u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
@@ -446,11 +440,12 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, i
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool want_dH, bool want_dW, float* dW, hipStream_t stream) {
-  const int nMt = (M + kFC - 1) / kFC;
+  (void)H;
   {
+    const int nMt = (M + kFC - 1) / kFC;
     const int nVt = (cw + kFR - 1) / kFR;
     Prof pr("recompute_dz", stream);
-    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, H, M, D, W,
+    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, Hs, M, D, W,
                        c0, cw, lam2, g, remap, S, ldS, G, ldG, dZ, chunk);
   }
   if (want_dH) {
