@@ -102,15 +102,21 @@ def union_remap(targets, target_lengths, blank: int, V: int) -> Dict[str, np.nda
 # Normaliser and selected log-probabilities (Eq. lognorm; Algorithm 1)
 # ---------------------------------------------------------------------------------------
 
-def log_normalizer(H, W, chunk: int = 4096) -> np.ndarray:
-    """lambda_m = log sum_v exp(Z_{m,v}), Z = H W^T, combined online over vocabulary chunks."""
+def _bias(bias, V: int) -> np.ndarray:
+    return np.zeros(V) if bias is None else np.asarray(bias, np.float64)
+
+
+def log_normalizer(H, W, chunk: int = 4096, bias=None) -> np.ndarray:
+    """lambda_m = log sum_v exp(Z_{m,v}), Z = H W^T + 1 b^T (Sec. 2 head (W, b)), combined
+    online over vocabulary chunks."""
     H = np.asarray(H, np.float64)
     W = np.asarray(W, np.float64)
+    b = _bias(bias, W.shape[0])
     M = H.shape[0]
     run_max = np.full(M, -np.inf)
     run_sum = np.zeros(M)
     for v0 in range(0, W.shape[0], chunk):
-        Z = H @ W[v0:v0 + chunk].T
+        Z = H @ W[v0:v0 + chunk].T + b[v0:v0 + chunk]
         cmax = Z.max(axis=1)
         new_max = np.maximum(run_max, cmax)
         safe = np.where(np.isfinite(new_max), new_max, 0.0)
@@ -121,11 +127,14 @@ def log_normalizer(H, W, chunk: int = 4096) -> np.ndarray:
         return np.where(np.isfinite(run_max), run_max + np.log(run_sum), run_max)
 
 
-def selected_logprobs(H, W, u_ids, lam) -> np.ndarray:
-    """S = X W_U^T - lambda 1^T: the log-probabilities of the selected classes (Algorithm 1)."""
+def selected_logprobs(H, W, u_ids, lam, bias=None) -> np.ndarray:
+    """S = X W_U^T + 1 b_U^T - lambda 1^T: the log-probabilities of the selected classes
+    (Algorithm 1)."""
     H = np.asarray(H, np.float64)
-    Wu = np.asarray(W, np.float64)[np.asarray(u_ids)]
-    return H @ Wu.T - np.asarray(lam, np.float64)[:, None]
+    u = np.asarray(u_ids)
+    Wu = np.asarray(W, np.float64)[u]
+    bu = _bias(bias, np.asarray(W).shape[0])[u]
+    return H @ Wu.T + bu - np.asarray(lam, np.float64)[:, None]
 
 
 # ---------------------------------------------------------------------------------------
@@ -280,7 +289,7 @@ def _offsets(lengths) -> np.ndarray:
 
 
 def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: float = math.inf,
-                    slack: float = KEEP_SLACK) -> Dict[str, object]:
+                    slack: float = KEEP_SLACK, weights=None) -> Dict[str, object]:
     """The alignment stage alone: given per-frame scores S [M, K] over the selected classes
     (blank = column 0) and relabelled targets, return per-utterance losses, statuses, the
     occupancy-derived G = dL/dS (G[m, j] = -gamma over the states labelled j; zero for
@@ -308,20 +317,24 @@ def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: f
         loss_n[n] = -res["logP"]
         gam = res["gamma"]
         ext = res["ext"]
+        w = 1.0 if weights is None else float(weights[n])
         for s in range(ext.size):
-            G[rows, ext[s]] -= gam[:, s]
+            G[rows, ext[s]] -= w * gam[:, s]
     g = G.sum(axis=1)
+    wv = np.ones(N) if weights is None else np.asarray(weights, np.float64)
     return {"loss_n": loss_n, "status": status, "G": G, "g": g, "per_utt": per_utt,
-            "loss": float(loss_n.sum())}
+            "loss": float((wv * loss_n).sum())}
 
 
-def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096) -> Dict[str, np.ndarray]:
+def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096, bias=None) -> Dict[str, np.ndarray]:
     """The recomputed backward stage alone (Eq. vjp; Algorithm 1 backward loop):
     dZ[m, v] = scatter_U(G)[m, v] - g_m p_v(m) with p_v(m) = exp(Z[m, v] - lambda_m),
-    formed one vocabulary chunk at a time, then dH = dZ W and dW = dZ^T H.  A frame with
-    g_m = 0 belongs to an excluded utterance and contributes nothing to either product."""
+    formed one vocabulary chunk at a time, then dH = dZ W, dW = dZ^T H and db = dZ^T 1
+    (the gradients w.r.t. X, W and b by the chain rule, App. A).  A frame with g_m = 0
+    belongs to an excluded utterance and contributes nothing."""
     H = np.asarray(H, np.float64)
     W = np.asarray(W, np.float64)
+    b = _bias(bias, W.shape[0])
     lam = np.asarray(lam, np.float64)
     G = np.asarray(G, np.float64)
     g = np.asarray(g, np.float64)
@@ -330,10 +343,11 @@ def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096) -> Dict[str, np.nda
     inc = g != 0
     dH = np.zeros((M, D))
     dW = np.zeros((V, D))
+    db = np.zeros(V)
     col = {int(v): j for j, v in enumerate(np.asarray(u_ids).tolist())}
     for v0 in range(0, V, chunk):
         v1 = min(V, v0 + chunk)
-        Z = H[inc] @ W[v0:v1].T
+        Z = H[inc] @ W[v0:v1].T + b[v0:v1]
         dZ = -g[inc, None] * np.exp(Z - lam[inc, None])
         for v in range(v0, v1):
             j = col.get(v)
@@ -341,10 +355,11 @@ def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096) -> Dict[str, np.nda
                 dZ[:, v - v0] += G[inc, j]
         dH[inc] += dZ @ W[v0:v1]
         dW[v0:v1] = dZ.T @ H[inc]
-    return {"dH": dH, "dW": dW}
+        db[v0:v1] = dZ.sum(axis=0)
+    return {"dH": dH, "dW": dW, "db": db}
 
 
-def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 4096) -> Dict[str, np.ndarray]:
+def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 4096, bias=None) -> Dict[str, np.ndarray]:
     """Selected outputs of the recomputed backward (Eq. vjp), each over its full contraction:
     dH[m] = sum_v dZ[m, v] W[v] for the given frames (every class v) and
     dW[v] = sum_m dZ[m, v] H[m] for the given classes (every frame m), with
@@ -357,10 +372,11 @@ def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 409
     frames = np.asarray(frames, np.int64)
     classes = np.asarray(classes, np.int64)
     V = W.shape[0]
+    b = _bias(bias, V)
     col = {int(v): j for j, v in enumerate(np.asarray(u_ids).tolist())}
 
     def dz(rows: np.ndarray, vs: np.ndarray) -> np.ndarray:
-        Z = H[rows] @ W[vs].T
+        Z = H[rows] @ W[vs].T + b[vs]
         with np.errstate(invalid="ignore", over="ignore"):
             out = -g[rows, None] * np.exp(Z - lam[rows, None])
         for i, v in enumerate(vs.tolist()):
@@ -375,8 +391,8 @@ def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 409
         vs = np.arange(v0, min(V, v0 + chunk))
         dH += dz(frames, vs) @ W[vs]
     inc = np.nonzero(g != 0)[0]
-    dW = dz(inc, classes).T @ H[inc]
-    return {"dH": dH, "dW": dW}
+    dzc = dz(inc, classes)
+    return {"dH": dH, "dW": dzc.T @ H[inc], "db": dzc.sum(axis=0)}
 
 
 # ---------------------------------------------------------------------------------------
@@ -384,11 +400,15 @@ def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 409
 # ---------------------------------------------------------------------------------------
 
 def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: float = math.inf,
-            chunk: int = 4096, want_grads: bool = True, slack: float = KEEP_SLACK) -> Dict[str, object]:
-    """Loss and gradients of (beam-pruned) CTC on log-softmax(H W^T) over the full vocabulary.
+            chunk: int = 4096, want_grads: bool = True, slack: float = KEEP_SLACK, bias=None,
+            weights=None) -> Dict[str, object]:
+    """Loss and gradients of (beam-pruned) CTC on log-softmax(H W^T + 1 b^T) over the full
+    vocabulary (Sec. 2 head (W, b); Eqs. lognorm, ctc, pruned-ctc).
 
-    Returns loss (sum of finite per-utterance losses over alignable utterances), loss_n,
-    status, dH [M, D], dW [V, D] and the stages u_ids, remap, y_rel, lam, S, G, g.
+    Returns loss = sum_n w_n L_n over alignable utterances with finite loss (w_n = 1 unless
+    `weights` is given: a per-utterance loss weight, e.g. one over the target-token count),
+    the unweighted loss_n, status, dH [M, D], dW [V, D], db [V] (gradients of that weighted
+    sum) and the stages u_ids, remap, y_rel, lam, S, G, g.
     """
     H = np.asarray(H, np.float64)
     W = np.asarray(W, np.float64)
@@ -400,8 +420,10 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
     if int(np.sum(input_lengths)) != M:
         raise OracleError(PCTC_EINVAL, "H rows differ from the sum of input lengths")
     un = union_remap(targets, target_lengths, blank, V)
-    lam = log_normalizer(H, W, chunk)
-    Ssel = selected_logprobs(H, W, un["u_ids"], lam)
+    b = _bias(bias, V)
+    wv = np.ones(N) if weights is None else np.asarray(weights, np.float64)
+    lam = log_normalizer(H, W, chunk, bias=b)
+    Ssel = selected_logprobs(H, W, un["u_ids"], lam, bias=b)
     toff = _offsets(input_lengths)
     yoff = _offsets(target_lengths)
     loss_n = np.zeros(N)
@@ -415,7 +437,7 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
         y = [int(v) for v in targets[yoff[n]:yoff[n + 1]]]
         # log p_v(m) on the columns this utterance's alignments can use (Eq. lognorm)
         cols = np.array([blank] + sorted(set(y)), np.int64)
-        logp_cols = H[rows] @ W[cols].T - lam[rows, None]
+        logp_cols = H[rows] @ W[cols].T + b[cols] - lam[rows, None]
         col_of = {int(v): i for i, v in enumerate(cols)}
         res = ctc_utterance(logp_cols, [col_of[v] for v in y], 0, beam, slack)
         res["cols"] = cols
@@ -436,8 +458,8 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
         res = per_utt[n]
         ext_ids = res["cols"][res["ext"]]
         for s in range(ext_ids.size):
-            G[rows, un["remap"][ext_ids[s]]] -= res["gamma"][:, s]
-    out = {"loss": float(loss_n.sum()), "loss_n": loss_n, "status": status,
+            G[rows, un["remap"][ext_ids[s]]] -= wv[n] * res["gamma"][:, s]
+    out = {"loss": float((wv * loss_n).sum()), "loss_n": loss_n, "status": status,
            "u_ids": un["u_ids"], "remap": un["remap"], "y_rel": un["y_rel"], "K": un["K"],
            "lam": lam, "S": Ssel, "G": G, "g": G.sum(axis=1), "per_utt": per_utt,
            "included": included}
@@ -446,11 +468,13 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
     # dZ = p - gamma (Eq. grad-full), dense over V, one chunk at a time; zero on excluded frames.
     dH = np.zeros((M, D))
     dW = np.zeros((V, D))
+    db = np.zeros(V)
     inc = included
     for v0 in range(0, V, chunk):
         v1 = min(V, v0 + chunk)
-        Z = H[inc] @ W[v0:v1].T
-        dZ = np.exp(Z - lam[inc, None])
+        Z = H[inc] @ W[v0:v1].T + b[v0:v1]
+        # dZ = -g p - (-G) scattered: -g_m = w_n for a frame of included utterance n
+        dZ = -G.sum(axis=1)[inc, None] * np.exp(Z - lam[inc, None])
         # subtract the occupancies gamma_v(m) for v in this chunk
         Ginc = G[inc]
         for j, v in enumerate(un["u_ids"]):
@@ -458,6 +482,8 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
                 dZ[:, v - v0] += Ginc[:, j]
         dH[inc] += dZ @ W[v0:v1]
         dW[v0:v1] = dZ.T @ H[inc]
+        db[v0:v1] = dZ.sum(axis=0)
     out["dH"] = dH
     out["dW"] = dW
+    out["db"] = db
     return out

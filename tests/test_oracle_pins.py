@@ -446,3 +446,93 @@ def test_head_backward_rows_is_gradient_of_surrogate():
     np.testing.assert_allclose(got["dH"], dH[frames], atol=1e-11)
     np.testing.assert_allclose(got["dW"], Wt.grad.numpy()[classes], atol=1e-11)
     assert np.all(got["dH"][2] == 0.0) and np.all(np.isfinite(got["dW"]))
+
+
+# ---------------------------------------------------------------------------------------
+# head bias, blank offset and loss weights (Sec. 2 head (W, b); LLM-CTC blank offset;
+# token-count normalisation): library and finite-difference cross-checks
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,blank", [(0, 0), (1, 17)])
+def test_bias_and_weights_against_torch_ctc_loss(seed, blank):
+    """Loss sum_n w_n L_n on log_softmax(H W^T + b) and its gradients w.r.t. H, W and b,
+    against PyTorch's CPU CTC (reduction 'none', weighted by hand) and autograd in float64."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(100 + seed)
+    N, V, D = 4, 40, 6
+    T = rng.integers(6, 25, size=N)
+    U = np.minimum(rng.integers(1, 7, size=N), T // 2)
+    ys = []
+    for u in U:
+        y = rng.integers(0, V - 1, size=u)
+        ys.append(np.where(y >= blank, y + 1, y))
+    targets = np.concatenate(ys)
+    H = rng.standard_normal((int(T.sum()), D))
+    W = rng.standard_normal((V, D)) / 2
+    b = rng.standard_normal(V)
+    b[blank] += 1.5                      # a blank offset eta
+    w = rng.uniform(0.1, 2.0, size=N)
+    out = oracle.fwd_bwd(H, W, targets, T, U, blank=blank, bias=b, weights=w)
+    Ht = torch.tensor(H, dtype=torch.float64, requires_grad=True)
+    Wt = torch.tensor(W, dtype=torch.float64, requires_grad=True)
+    bt = torch.tensor(b, dtype=torch.float64, requires_grad=True)
+    logp = torch.log_softmax(Ht @ Wt.T + bt, dim=1)
+    Tm = int(T.max())
+    off = np.concatenate([[0], np.cumsum(T)])
+    pad = torch.stack([torch.nn.functional.pad(logp[off[n]:off[n + 1]], (0, 0, 0, Tm - int(T[n])))
+                       for n in range(N)], dim=1)
+    ln = torch.nn.functional.ctc_loss(pad, torch.tensor(targets), torch.tensor(T), torch.tensor(U),
+                                      blank=blank, reduction="none", zero_infinity=True)
+    loss = (ln * torch.tensor(w)).sum()
+    loss.backward()
+    np.testing.assert_allclose(out["loss_n"], ln.detach().numpy(), rtol=1e-10)
+    assert abs(float(loss.detach()) - out["loss"]) < 1e-9 * abs(out["loss"])
+    np.testing.assert_allclose(out["dH"], Ht.grad.numpy(), rtol=0, atol=1e-9)
+    np.testing.assert_allclose(out["dW"], Wt.grad.numpy(), rtol=0, atol=1e-9)
+    np.testing.assert_allclose(out["db"], bt.grad.numpy(), rtol=0, atol=1e-9)
+    # the blank offset's gradient is the blank entry of db
+    assert abs(out["db"][blank] - float(bt.grad[blank])) < 1e-9
+
+
+@pytest.mark.parametrize("beam", [math.inf, 3.0])
+def test_bias_finite_differences(beam):
+    """db (and the eta = b[blank] entry) by central differences of the weighted loss,
+    unpruned and beam-pruned."""
+    rng = np.random.default_rng(7)
+    T = np.array([5, 4, 3])
+    U = np.array([2, 1, 1])
+    targets = np.array([1, 3, 2, 4])
+    H = rng.standard_normal((12, 3))
+    W = rng.standard_normal((6, 3))
+    b = rng.standard_normal(6)
+    w = np.array([0.5, 2.0, 1.0])
+    out = oracle.fwd_bwd(H, W, targets, T, U, blank=0, beam=beam, bias=b, weights=w)
+
+    def loss(bx):
+        return oracle.fwd_bwd(H, W, targets, T, U, blank=0, beam=beam, want_grads=False, bias=bx, weights=w)["loss"]
+
+    h = 1e-6
+    for v in range(6):
+        bp, bm = b.copy(), b.copy()
+        bp[v] += h
+        bm[v] -= h
+        assert abs((loss(bp) - loss(bm)) / (2 * h) - out["db"][v]) < 1e-6
+
+
+def test_bias_rows_and_stage_agree():
+    """head_backward and head_backward_rows with a bias reproduce the full path's dH, dW, db."""
+    from paper_2609_33645_amd import workloads
+    wl = workloads.random_small(31, N=3, T_range=(6, 20), D=8, V=90, dtype="f32", p_repeat=0.2)
+    b = np.random.default_rng(3).standard_normal(90)
+    w = np.array([1.0, 0.25, 3.0])
+    full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0, beam=4.0, bias=b,
+                          weights=w, chunk=17)
+    st = oracle.head_backward(wl.H, wl.W, full["lam"], full["G"], full["g"], full["u_ids"], chunk=40, bias=b)
+    for k in ("dH", "dW", "db"):
+        np.testing.assert_allclose(st[k], full[k], atol=1e-12)
+    fr = np.array([0, 5, int(wl.M) - 1])
+    cl = np.array([0, 3, 50, 89])
+    rows = oracle.head_backward_rows(wl.H, wl.W, full["lam"], full["G"], full["g"], full["u_ids"], fr, cl, bias=b)
+    np.testing.assert_allclose(rows["dH"], full["dH"][fr], atol=1e-12)
+    np.testing.assert_allclose(rows["dW"], full["dW"][cl], atol=1e-12)
+    np.testing.assert_allclose(rows["db"], full["db"][cl], atol=1e-12)
