@@ -68,8 +68,9 @@ enum { PCTC_UTT_OK = 0, PCTC_UTT_NOT_ALIGNABLE = 1, PCTC_UTT_NONFINITE = 2 };
  * chunk and the remap table) linearly on V only in a V-sized int32 table; the dominant
  * terms scale with M*K (selected log-probabilities and their gradient), the lattice
  * size sum_n T_n (2U_n+1), and M*chunk (one recomputed bf16 gradient chunk).
- * chunk: vocabulary columns recomputed per backward step; 0 selects the default (16384).
- * Returns 0 if the arguments are invalid. */
+ * chunk: vocabulary columns recomputed per backward step; 0 selects the default (about
+ * 512 MiB of recomputed gradient, see pctc_bwd_chunk).  Returns 0 if the arguments are
+ * invalid.  The same workspace serves pruned_ctc_fwd_bwd_ex. */
 size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
                            const int32_t* target_lengths, int32_t D, int32_t V, float beam,
                            int32_t chunk);
@@ -77,7 +78,7 @@ size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_len
 /* Forward and backward pass of Pruned CTC (Algorithm 1).
  *
  * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8.
- * W        [V, D] row-major, dtype (the head weight; no bias).
+ * W        [V, D] row-major, dtype (the head weight; a bias: pruned_ctc_fwd_bwd_ex).
  * targets  device int32 [sum target_lengths]: concatenated blank-free labels.
  * input_lengths, target_lengths: HOST int32 [N].
  * blank    the blank class id, 0 <= blank < V.  It becomes column 0 of the union.
@@ -85,8 +86,8 @@ size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_len
  *          >= 0 prunes every lattice arc whose best complete alignment scores more than
  *          beam (+1e-3 slack) below the best alignment; +INF or a negative value keeps
  *          all alignments (unpruned reduced CTC).  NaN is PCTC_EINVAL.
- * chunk    vocabulary columns per backward recompute step (0 = default 16384; otherwise
- *          a positive multiple of 256).
+ * chunk    vocabulary columns per backward recompute step (0 = the default of
+ *          pctc_bwd_chunk; otherwise a positive multiple of 256).
  * loss     device double [1]: sum over utterances of the finite per-utterance losses.
  * loss_per_utt  device double [N] or NULL.
  * utt_status    device int32 [N] or NULL (PCTC_UTT_* codes).
@@ -106,6 +107,29 @@ int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const voi
                            int32_t chunk, double* loss, double* loss_per_utt, int32_t* utt_status,
                            float* dH, float* dW, void* workspace, size_t workspace_bytes,
                            void* stream);
+
+/* The same with a head bias, per-utterance loss weights and the bias gradient (Sec. 2:
+ * the head is the affine map (W, b); Algorithm 1 writes the rows of dL/dW and dL/db per
+ * vocabulary chunk; the LLM-CTC blank offset eta enters as b = b_pre + eta e_blank, so
+ * dL/deta = db[blank]; App. C normalises losses by the batch's target-token count,
+ * which is w_n = 1 / sum_n U_n).
+ *
+ * bias        device float [V] or NULL: logits are H W^T + 1 b^T.
+ * utt_weight  device float [N] or NULL (all 1): loss = sum_n w_n L_n over the included
+ *             utterances, and dH, dW, db are the gradients of that sum.  loss_per_utt
+ *             still receives the unweighted L_n.  A zero weight excludes the utterance
+ *             from the gradients.
+ * db          device float [V] or NULL: dL/db, the column sums of dL/dZ (bf16 path:
+ *             the sums of the bf16-rounded dL/dZ that the dH and dW products also use).
+ * Every other argument is as for pruned_ctc_fwd_bwd, which equals this call with three
+ * NULLs. */
+int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const void* W,
+                              const float* bias, int32_t V, const int32_t* targets,
+                              const int32_t* input_lengths, const int32_t* target_lengths,
+                              int32_t N, int32_t blank, float beam, int32_t chunk,
+                              const float* utt_weight, double* loss, double* loss_per_utt,
+                              int32_t* utt_status, float* dH, float* dW, float* db,
+                              void* workspace, size_t workspace_bytes, void* stream);
 
 /* Human-readable text of a status code, and the text of the last HIP error seen by the
  * calling thread. */

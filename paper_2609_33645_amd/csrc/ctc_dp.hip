@@ -453,8 +453,8 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
                     const int32_t* __restrict__ frame_utt, const int32_t* __restrict__ status,
                     const int32_t* __restrict__ dup_next, const int32_t* __restrict__ dup_first,
                     const float* __restrict__ fa, const float* __restrict__ fb, const double* __restrict__ sfa,
-                    const double* __restrict__ sfb, const double* __restrict__ logp, float* __restrict__ G,
-                    int ldG, float* __restrict__ g) {
+                    const double* __restrict__ sfb, const double* __restrict__ logp,
+                    const float* __restrict__ weight, float* __restrict__ G, int ldG, float* __restrict__ g) {
   extern __shared__ float gam[];  // [Smax]
   __shared__ float red[kOccThreads];
   const int m = blockIdx.x;
@@ -466,6 +466,7 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
   const int Sp = 2 * U + 1;
   const int64_t rowb = soff[n] + static_cast<int64_t>(t) * Sp;
   const float off = static_cast<float>(sfa[m] + sfb[m] - logp[n]);
+  const float w = weight ? weight[n] : 1.f;  // loss weight of the utterance: G = -w gamma
   for (int s = threadIdx.x; s < Sp; s += kOccThreads) {
     const float x = fa[rowb + s] + fb[rowb + s] + off;
     gam[s] = fast_exp2(x * kLog2e);
@@ -484,7 +485,7 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
       acc += gam[2 * j + 1];
       j = dup_next[y0 + j];
     }
-    G[static_cast<int64_t>(m) * ldG + y_rel[y0 + i]] = -acc;
+    G[static_cast<int64_t>(m) * ldG + y_rel[y0 + i]] = -w * acc;
     lsum += acc;
   }
   red[threadIdx.x] = bsum;
@@ -502,24 +503,25 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
     __syncthreads();
   }
   if (threadIdx.x == 0) {
-    G[static_cast<int64_t>(m) * ldG + 0] = -blank_total;
-    g[m] = -(blank_total + red[0]);
+    G[static_cast<int64_t>(m) * ldG + 0] = -w * blank_total;
+    g[m] = -w * (blank_total + red[0]);
   }
 }
 
+// loss = sum over included utterances of w_n L_n (w_n = 1 without weights)
 __global__ void loss_reduce_kernel(int N, const double* __restrict__ loss_n, const int32_t* __restrict__ status,
-                                   double* __restrict__ loss) {
+                                   const float* __restrict__ weight, double* __restrict__ loss) {
   if (threadIdx.x != 0 || blockIdx.x != 0) return;
   double s = 0.0;
   for (int n = 0; n < N; ++n)
-    if (status[n] == 0) s += loss_n[n];
+    if (status[n] == 0) s += (weight ? static_cast<double>(weight[n]) : 1.0) * loss_n[n];
   *loss = s;
 }
 
-hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, double* loss,
+hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, const float* weight, double* loss,
                               hipStream_t stream) {
   Prof pr("loss_reduce", stream);
-  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(64), 0, stream, N, loss_n, status, loss);
+  hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(64), 0, stream, N, loss_n, status, weight, loss);
   return hipGetLastError();
 }
 
@@ -564,8 +566,9 @@ static int pick_q(int Smax) {
 }
 
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
-                         const int32_t* y_rel, float beam, double* loss_n, int32_t* status, float* G, float* g,
-                         uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream, void*) {
+                         const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
+                         float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
+                         void*) {
   const int N = plan.N;
   char* sc = static_cast<char*>(scratch);
   int32_t* toff = reinterpret_cast<int32_t*>(sc + plan.off_toff);
@@ -624,8 +627,8 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   if (plan.M > 0) {
     Prof pr("dp_occupancy", stream);
     hipLaunchKernelGGL(dp_occupancy_kernel, dim3(plan.M), dim3(kOccThreads), plan.Smax * sizeof(float), stream,
-                       toff, yoff, soff, y_rel, frame_utt, status, dnext, dfirst, tfa, tfb, sfa, sfb, logp, G, ldS,
-                       g);
+                       toff, yoff, soff, y_rel, frame_utt, status, dnext, dfirst, tfa, tfb, sfa, sfb, logp, weight, G,
+                       ldS, g);
   }
   if (keep_mask_out && mask && plan.lattice > 0) {
     e = hipMemcpyAsync(keep_mask_out, mask, plan.lattice, hipMemcpyDeviceToDevice, stream);

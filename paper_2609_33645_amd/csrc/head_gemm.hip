@@ -46,8 +46,8 @@ __device__ __forceinline__ int xcd_swizzle(int bid, int nblocks) {
 
 template <typename T>
 __global__ void __launch_bounds__(256)
-lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, int V, int P, int vper,
-                   float2* __restrict__ partials) {
+lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const float* __restrict__ bias,
+                   int V, int P, int vper, float2* __restrict__ partials) {
   constexpr int BK = Cfg<T>::BK;
   using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
   constexpr int FR = Shape::FR, FC = Shape::FC;
@@ -72,6 +72,17 @@ lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ 
   f32x16 acc[FR][FC];
   for (int v0 = vbeg; v0 < vend; v0 += kFwdBR) {
     tile_gemm<T, kFwdBR, kFwdBC, BK, Lay::KMajor, Lay::KMajor>(A, B, v0, m0, 0, D, lds, acc);
+    if (bias) {
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = v0 + acc_row<kFwdBR>(wave, lane, i, r);
+          const float b = (v < vend) ? bias[v] : 0.f;
+#pragma unroll
+          for (int j = 0; j < FC; ++j) acc[i][j][r] += b;
+        }
+    }
     // rows past the partition end take no part in the sums
     if (v0 + kFwdBR > vend) {
 #pragma unroll
@@ -202,8 +213,8 @@ hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t strea
   return hipGetLastError();
 }
 
-hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int V, float2* partials,
-                      double* lam, float2* lam2, hipStream_t stream) {
+hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                      float2* partials, double* lam, float2* lam2, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
   const int P = lse_partitions(M, V);
   const int vtiles = (V + kFwdBR - 1) / kFwdBR;
@@ -212,13 +223,13 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int
   const int nMt = (M + kFwdBC - 1) / kFwdBC;
   int Pfin = Peff;
   if (dtype == 1) {
-    hipError_t e1 = launch_lse_partial_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V,
-                                            partials, &Pfin, stream);
+    hipError_t e1 = launch_lse_partial_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias,
+                                            V, partials, &Pfin, stream);
     if (e1 != hipSuccess) return e1;
   } else {
     Prof pr("lse_partial", stream);
     hipLaunchKernelGGL(lse_partial_kernel<float>, dim3(nMt * Peff), dim3(256), 0, stream,
-                       static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, Peff, vper, partials);
+                       static_cast<const float*>(H), M, D, static_cast<const float*>(W), bias, V, Peff, vper, partials);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
@@ -233,9 +244,9 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int
 
 template <typename T>
 __global__ void __launch_bounds__(256, 2)
-gather_s_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const int32_t* __restrict__ u_ids,
-                const int32_t* __restrict__ Kdev, int K_max, const double* __restrict__ lam, float* __restrict__ S,
-                int ldS) {
+gather_s_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const float* __restrict__ bias,
+                const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev, int K_max,
+                const double* __restrict__ lam, float* __restrict__ S, int ldS) {
   constexpr int BK = Cfg<T>::BK;
   using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
   constexpr int FR = Shape::FR, FC = Shape::FC;
@@ -262,23 +273,27 @@ gather_s_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = j0 + acc_row<kFwdBR>(wave, lane, i, r);
-        if (jj < K) S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(static_cast<double>(acc[i][j][r]) - l);
+        if (jj < K) {
+          double z = static_cast<double>(acc[i][j][r]);
+          if (bias) z += static_cast<double>(bias[u_ids[jj]]);
+          S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(z - l);
+        }
       }
   }
 }
 
-hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const int32_t* u_ids,
-                           const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const float* bias,
+                           const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream) {
   if (M <= 0) return hipSuccess;
   if (dtype == 1)
-    return launch_gather_s_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), u_ids, K, K_max,
-                                lam, S, ldS, stream);
+    return launch_gather_s_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias, u_ids, K,
+                                K_max, lam, S, ldS, stream);
   const int nMt = (M + kFwdBC - 1) / kFwdBC;
   const int nJt = (K_max + kFwdBR - 1) / kFwdBR;
   Prof pr("gather_s", stream);
   hipLaunchKernelGGL(gather_s_kernel<float>, dim3(nMt * nJt), dim3(256), 0, stream, static_cast<const float*>(H), M, D,
-                     static_cast<const float*>(W), u_ids, K, K_max, lam, S, ldS);
+                     static_cast<const float*>(W), bias, u_ids, K, K_max, lam, S, ldS);
   return hipGetLastError();
 }
 
@@ -301,9 +316,9 @@ __device__ __forceinline__ float to_elem<float>(float x) {
 // scatter_U(G) - g p for vocabulary id c0 + v_local; columns in [cw, tile end) hold 0.
 template <typename T>
 __global__ void __launch_bounds__(256, 2)
-recompute_dz_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, int c0, int cw,
-                    const float2* __restrict__ lam2, const float* __restrict__ G, int ldG, const float* __restrict__ g,
-                    const int32_t* __restrict__ remap, T* __restrict__ dZ, int chunk) {
+recompute_dz_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const float* __restrict__ bias,
+                    int c0, int cw, const float2* __restrict__ lam2, const float* __restrict__ G, int ldG,
+                    const float* __restrict__ g, const int32_t* __restrict__ remap, T* __restrict__ dZ, int chunk) {
   constexpr int BK = Cfg<T>::BK;
   using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
   constexpr int FR = Shape::FR, FC = Shape::FC;
@@ -344,7 +359,8 @@ recompute_dz_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__
           const int vl = vl0 + rl;
           float val = 0.f;
           if (inc && vl < cw) {
-            const float t = fmaf(acc[i][j][4 * q + e], kLog2e, -l2.x) - l2.y;
+            const float z = acc[i][j][4 * q + e] + (bias ? bias[c0 + vl] : 0.f);
+            const float t = fmaf(z, kLog2e, -l2.x) - l2.y;
             val = -gm * fast_exp2(t);
             if (any_sel) {
               const int jj = sel[rl];
@@ -503,14 +519,26 @@ BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
   p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);  // >= M x D (bf16 masked copy of H)
   p.part_bytes = align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
   p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
-  p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes;
+  // bf16: per 128-frame tile column sums of dZ for db
+  p.dbpart_bytes = (dtype == 1) ? align_up(static_cast<size_t>((M + 127) / 128) * p.chunk * sizeof(float), 256) : 0;
+  p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes + p.dbpart_bytes;
   return p;
 }
 
+// db[v] = sum over frames of dZ[m][v] for the chunk's columns v < cw.
 template <typename T>
-static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const float2* lam2, const float* G,
-                             int ldG, const float* g, const int32_t* remap, float* dH, float* dW, char* scratch,
-                             const BwdPlan& plan, hipStream_t stream) {
+__global__ void dz_colsum_kernel(const T* __restrict__ dZ, int M, int chunk, int cw, float* __restrict__ db) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= cw) return;
+  float s = 0.f;
+  for (int m = 0; m < M; ++m) s += static_cast<float>(dZ[static_cast<int64_t>(m) * chunk + v]);
+  db[v] = s;
+}
+
+template <typename T>
+static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* bias, int V, const float2* lam2,
+                             const float* G, int ldG, const float* g, const int32_t* remap, float* dH, float* dW,
+                             float* db, char* scratch, const BwdPlan& plan, hipStream_t stream) {
   T* dZ = reinterpret_cast<T*>(scratch);
   T* Ht = reinterpret_cast<T*>(scratch + plan.dz_bytes);
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
@@ -531,8 +559,13 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const 
     const int nVt = (cw + kFwdBR - 1) / kFwdBR;
     {
       Prof pr("recompute_dz", stream);
-      hipLaunchKernelGGL(recompute_dz_kernel<T>, dim3(nMt * nVt), dim3(256), 0, stream, H, M, D, W, c0, cw, lam2,
-                         G, ldG, g, remap, dZ, chunk);
+      hipLaunchKernelGGL(recompute_dz_kernel<T>, dim3(nMt * nVt), dim3(256), 0, stream, H, M, D, W, bias, c0, cw,
+                         lam2, G, ldG, g, remap, dZ, chunk);
+    }
+    if (db) {
+      Prof pr("db_colsum", stream);
+      hipLaunchKernelGGL(dz_colsum_kernel<T>, dim3((cw + 255) / 256), dim3(256), 0, stream, dZ, M, chunk, cw,
+                         db + c0);
     }
     if (dH) {
       const int tiles = ((M + kBwdB - 1) / kBwdB) * ((D + kBwdB - 1) / kBwdB);
@@ -559,13 +592,14 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, int V, const 
   return hipGetLastError();
 }
 
-static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, const float2* lam2,
-                                const float* G, int ldG, const float* g, const int32_t* remap, const float* S,
-                                int ldS, float* dH, float* dW, char* scratch, const BwdPlan& plan,
-                                hipStream_t stream) {
+static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
+                                const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
+                                const float* S, int ldS, float* dH, float* dW, float* db, char* scratch,
+                                const BwdPlan& plan, hipStream_t stream) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
   uint16_t* Hs = reinterpret_cast<uint16_t*>(scratch + plan.dz_bytes);
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
+  float* dbpart = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes + plan.part_bytes + plan.lam2_bytes);
   const int chunk = plan.chunk;
   hipError_t e;
   // Hs: H with the rows of excluded frames zeroed (read by the recompute and by dW)
@@ -578,8 +612,8 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   }
   for (int c0 = 0; c0 < V; c0 += chunk) {
     const int cw = min(chunk, V - c0);
-    e = launch_bwd_chunk_bf16(H, Hs, M, D, W, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                              dH != nullptr, dW != nullptr, dW, stream);
+    e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+                              dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
     if (e != hipSuccess) return e;
   }
   if (dH) {
@@ -591,19 +625,24 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   return hipGetLastError();
 }
 
-hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
-                           const float* G, int ldG, const float* g, const int32_t* remap, const float* S, int ldS,
-                           float* dH, float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream) {
+hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                           const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
+                           const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
+                           const BwdPlan& plan, hipStream_t stream) {
   if (M <= 0) {
+    if (db) {
+      hipError_t e = hipMemsetAsync(db, 0, static_cast<size_t>(V) * sizeof(float), stream);
+      if (e != hipSuccess) return e;
+    }
     if (dW) return hipMemsetAsync(dW, 0, static_cast<size_t>(V) * D * sizeof(float), stream);
     return hipSuccess;
   }
   char* sc = static_cast<char*>(scratch);
   if (dtype == 1)
-    return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), V, lam2, G, ldG, g,
-                         remap, S, ldS, dH, dW, sc, plan, stream);
-  return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), V, lam2, G, ldG, g,
-                           remap, dH, dW, sc, plan, stream);
+    return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias, V, lam2, G, ldG,
+                         g, remap, S, ldS, dH, dW, db, sc, plan, stream);
+  return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), bias, V, lam2, G, ldG, g,
+                           remap, dH, dW, db, sc, plan, stream);
 }
 
 }  // namespace pctc

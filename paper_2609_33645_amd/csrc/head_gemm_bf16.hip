@@ -74,22 +74,31 @@ __device__ __forceinline__ bool grouped_tile(int work, int nA, int nB, int& a, i
 }
 
 // Online log-sum-exp update of the running (max, sum) of this lane's frames with one
-// tile; rows at or past vend are skipped when MASK.
-template <bool MASK, int FR, int FC>
-__device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], float (&run_max)[FC], float (&run_sum)[FC],
-                                                int v0, int vend, int wave, int lane) {
+// tile; rows at or past vend are skipped when MASK.  With BIAS, b[v] (staged in LDS, bt
+// pointing at the tile's first row) is added to every logit of row v.
+template <bool MASK, bool BIAS, int FR, int FC>
+__device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], const float* bt, float (&run_max)[FC],
+                                                float (&run_sum)[FC], int v0, int vend, int wave, int lane) {
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     float tmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float x = acc[i][j][r];
-        if (MASK) {
-          if (v0 + GFwd::row_of(wave, lane, i, r) < vend) tmax = fmaxf(tmax, x);
-        } else {
-          tmax = fmaxf(tmax, x);
+      for (int q = 0; q < 4; ++q) {
+        const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
+        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (BIAS) b4 = *reinterpret_cast<const float4*>(bt + r0);
+        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float x = acc[i][j][4 * q + e];
+          if (BIAS) x += bb[e];
+          if (MASK) {
+            if (v0 + r0 + e < vend) tmax = fmaxf(tmax, x);
+          } else {
+            tmax = fmaxf(tmax, x);
+          }
         }
       }
     tmax = fmaxf(tmax, swap_halves(tmax));
@@ -99,12 +108,21 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float e = fast_exp2(fmaf(acc[i][j][r], kLog2e, -ms));
-        if (MASK) {
-          if (v0 + GFwd::row_of(wave, lane, i, r) < vend) s += e;
-        } else {
-          s += e;
+      for (int q = 0; q < 4; ++q) {
+        const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
+        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (BIAS) b4 = *reinterpret_cast<const float4*>(bt + r0);
+        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          float x = acc[i][j][4 * q + e];
+          if (BIAS) x += bb[e];
+          const float ex = fast_exp2(fmaf(x, kLog2e, -ms));
+          if (MASK) {
+            if (v0 + r0 + e < vend) s += ex;
+          } else {
+            s += ex;
+          }
         }
       }
     s += swap_halves(s);
@@ -116,9 +134,11 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
 
 }  // namespace
 
+template <bool BIAS>
 __global__ void __launch_bounds__(256, 2)
-lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int V, int P,
-                 int vper, float2* __restrict__ partials) {
+lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, const float* __restrict__ bias,
+                 int V, int P, int vper, float2* __restrict__ partials) {
+  extern __shared__ float bsh[];  // BIAS: b over this partition's rows (vper, padded to whole tiles)
   using G = GFwd;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES(G)
@@ -129,6 +149,12 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
   const int vbeg = p * vper;
   const int vend = min(V, vbeg + vper);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
+  if (BIAS) {
+    // visible to every wave after the engine's first barrier
+    for (int r = tid; r < ntiles * kFR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
+    __syncthreads();
+  }
   const GOp A{W, D, vend, D, nullptr};
   const GOp B{H, D, M, D, nullptr};
   float run_max[FC], run_sum[FC];
@@ -138,13 +164,13 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
     run_sum[j] = 0.f;
   }
   f32x16 acc[FR][FC];
-  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
   G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, [&](int i, const f32x16 (&a)[FR][FC]) {
     const int v0 = vbeg + i * kFR;
+    const float* bt = bsh + i * kFR;
     if (v0 + kFR <= vend)
-      lse_tile_update<false, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+      lse_tile_update<false, BIAS, FR, FC>(a, bt, run_max, run_sum, v0, vend, wave, lane);
     else
-      lse_tile_update<true, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+      lse_tile_update<true, BIAS, FR, FC>(a, bt, run_max, run_sum, v0, vend, wave, lane);
   });
   __syncthreads();
   // the two wavefronts of each frame column (row halves) combine their partial sums
@@ -172,8 +198,8 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
 
 __global__ void __launch_bounds__(256, 2)
 gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
-              const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev, const double* __restrict__ lam,
-              float* __restrict__ S, int ldS) {
+              const float* __restrict__ bias, const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev,
+              const double* __restrict__ lam, float* __restrict__ S, int ldS) {
   using G = GFwd;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES(G)
@@ -199,7 +225,11 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int jj = j0 + GFwd::row_of(wave, lane, i, r);
-        if (jj < K) S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(static_cast<double>(acc[i][j][r]) - l);
+        if (jj < K) {
+          double z = static_cast<double>(acc[i][j][r]);
+          if (bias) z += static_cast<double>(bias[u_ids[jj]]);
+          S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(z - l);
+        }
       }
   }
 }
@@ -207,16 +237,20 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
 // dZ chunk [M][chunk] (row pitch `chunk`): dZ[m][v] = scatter_U(G)[m][v] - g_m p_v(m) for
 // the chunk's 256-column tiles (Eq. vjp; zero on excluded frames).  The dense part -g p
 // comes from the recomputed logits of Hs (H with excluded rows zeroed, so their products
-// are finite and, with g_m = 0, give zeros); the few union columns of a tile are then
-// rewritten in the staging buffer as G[m][j] - g_m exp(S[m][j]) from the forward's
-// selected log-probabilities.  Columns past cw within the last tile hold finite values
-// that no consumer reads (their W rows read as zero).  Each 256 x 128 tile is staged
-// through LDS so that every frame row is stored as contiguous 16-byte vectors.
+// are finite and, with g_m = 0, give zeros) plus the bias when there is one; the few union
+// columns of a tile are then rewritten in the staging buffer as G[m][j] - g_m exp(S[m][j])
+// from the forward's selected log-probabilities.  Columns past cw within the last tile
+// hold finite values that no consumer reads (their W rows read as zero).  Each 256 x 128
+// tile is staged through LDS so that every frame row is stored as contiguous 16-byte
+// vectors.  DB: the staged (rounded) values are also summed over the tile's frames, giving
+// this tile's share of db = dZ^T 1 in dbpart[frame tile][column].
+template <bool BIAS, bool DB>
 __global__ void __launch_bounds__(256, 2)
-recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
-                  const float2* __restrict__ lam2, const float* __restrict__ g, const int32_t* __restrict__ remap,
-                  const float* __restrict__ S, int ldS, const float* __restrict__ G, int ldG,
-                  uint16_t* __restrict__ dZ, int chunk) {
+recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W,
+                  const float* __restrict__ bias, int c0, int cw, const float2* __restrict__ lam2,
+                  const float* __restrict__ g, const int32_t* __restrict__ remap, const float* __restrict__ S, int ldS,
+                  const float* __restrict__ G, int ldG, uint16_t* __restrict__ dZ, int chunk,
+                  float* __restrict__ dbpart) {
   using GG = GFwd;
   constexpr int FR = GG::FR, FC = GG::FC;
   constexpr int kPitch = kFR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
@@ -229,11 +263,14 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   const int m0 = mt * kFC;
   const int vl0 = vt * kFR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // union columns of this tile: (union index << 8) | tile column
+  // union columns of this tile: (union index << 8) | tile column; b log2(e) per column
   __shared__ int ulist[kFR];
   __shared__ int nu;
+  __shared__ __attribute__((aligned(16))) float bl[BIAS ? kFR : 4];
   if (tid == 0) nu = 0;
-  const int jsel = (vl0 + tid < cw) ? remap[c0 + vl0 + tid] : -1;
+  const bool vin = vl0 + tid < cw;
+  const int jsel = vin ? remap[c0 + vl0 + tid] : -1;
+  if (BIAS) bl[tid] = vin ? bias[c0 + vl0 + tid] * kLog2e : 0.f;
   const int any_sel = __syncthreads_or(jsel >= 0);
   if (any_sel) {
     if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
@@ -256,6 +293,7 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   const int nunion = any_sel ? nu : 0;
   const int ch = wave & 1;            // column half: frames [64 ch, 64 ch + 64) of the tile
   char* stage = ch ? st1_ : st0_;     // 32 frames x 256 vocabulary columns per pass
+  float dbsum = 0.f;                  // DB: column tid of the tile, summed over the passes
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     if (j > 0) __syncthreads();  // the previous pass's readers are done
@@ -263,10 +301,14 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
+        const int rl0 = GG::row_of(wave, lane, i, 4 * q);
+        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (BIAS) b4 = *reinterpret_cast<const float4*>(bl + rl0);
+        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ll[j]));
-        const int rl0 = GG::row_of(wave, lane, i, 4 * q);
+        for (int e = 0; e < 4; ++e)
+          v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, BIAS ? bb[e] - ll[j] : -ll[j]));
         *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) =
             u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       }
@@ -288,6 +330,14 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
       }
       __syncthreads();
     }
+    if (DB) {
+      // column tid over the 64 staged frames (frames past M hold zeros)
+#pragma unroll 4
+      for (int row = 0; row < 32; ++row) {
+        dbsum += bf16_to_f32(*reinterpret_cast<const uint16_t*>(st0_ + row * kPitch + tid * 2));
+        dbsum += bf16_to_f32(*reinterpret_cast<const uint16_t*>(st1_ + row * kPitch + tid * 2));
+      }
+    }
     // 2 stages x 32 frames x 32 vectors of 16 bytes
 #pragma unroll
     for (int k = 0; k < 8; ++k) {
@@ -301,6 +351,17 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
       if (mm < M) *reinterpret_cast<u32x4*>(dZ + static_cast<int64_t>(mm) * chunk + vl0 + vec * 8) = v;
     }
   }
+  if (DB) dbpart[static_cast<int64_t>(mt) * chunk + vl0 + tid] = dbsum;
+}
+
+// db[c0 + v] = sum over frame tiles of dbpart[t][v], v < cw (fixed order).
+__global__ void db_reduce_bf16(const float* __restrict__ dbpart, int ntiles, int chunk, int cw,
+                               float* __restrict__ db) {
+  const int v = blockIdx.x * blockDim.x + threadIdx.x;
+  if (v >= cw) return;
+  float s = 0.f;
+  for (int t = 0; t < ntiles; ++t) s += dbpart[static_cast<int64_t>(t) * chunk + v];
+  db[v] = s;
 }
 
 __global__ void __launch_bounds__(512, 1)
@@ -411,8 +472,8 @@ int lse_partitions_bf16(int M, int V) {
   return P;
 }
 
-hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
-                                   int* P_out, hipStream_t stream) {
+hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
+                                   float2* partials, int* P_out, hipStream_t stream) {
   const int P = lse_partitions_bf16(M, V);
   const int vtiles = (V + kFR - 1) / kFR;
   const int vper = ((vtiles + P - 1) / P) * kFR;
@@ -420,33 +481,51 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
   const int nMt = (M + kFC - 1) / kFC;
   *P_out = Peff;
   Prof pr("lse_partial", stream);
-  hipLaunchKernelGGL(lse_partial_bf16, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M, D, W, V,
-                     Peff, vper, partials);
+  if (bias)
+    hipLaunchKernelGGL(lse_partial_bf16<true>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads),
+                       static_cast<size_t>(vper) * sizeof(float), stream, H, M, D, W, bias, V, Peff, vper, partials);
+  else
+    hipLaunchKernelGGL(lse_partial_bf16<false>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M,
+                       D, W, bias, V, Peff, vper, partials);
   return hipGetLastError();
 }
 
-hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const int32_t* u_ids,
-                                const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias,
+                                const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                                 hipStream_t stream) {
   const int nMt = (M + kFC - 1) / kFC;
   const int nJt = (K_max + kFR - 1) / kFR;
   Prof pr("gather_s", stream);
-  hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(GFwd::kThreads), 0, stream, H, M, D, W, u_ids, K, lam, S,
-                     ldS);
+  hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias, u_ids, K, lam,
+                     S, ldS);
   return hipGetLastError();
 }
 
-hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
+hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
-                                 int slice, bool want_dH, bool want_dW, float* dW, hipStream_t stream) {
-  (void)H;
+                                 int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
+                                 hipStream_t stream) {
+  const int nMt = (M + kFC - 1) / kFC;
   {
-    const int nMt = (M + kFC - 1) / kFC;
     const int nVt = (cw + kFR - 1) / kFR;
+    const dim3 grid(grouped_grid(nMt, nVt));
     Prof pr("recompute_dz", stream);
-    hipLaunchKernelGGL(recompute_dz_bf16, dim3(grouped_grid(nMt, nVt)), dim3(GFwd::kThreads), 0, stream, Hs, M, D, W,
-                       c0, cw, lam2, g, remap, S, ldS, G, ldG, dZ, chunk);
+#define PCTC_RECOMPUTE(BI, DBI)                                                                                      \
+  hipLaunchKernelGGL((recompute_dz_bf16<BI, DBI>), grid, dim3(GFwd::kThreads), 0, stream, Hs, M, D, W, bias, c0, cw, \
+                     lam2, g, remap, S, ldS, G, ldG, dZ, chunk, dbpart)
+    if (bias) {
+      if (db) PCTC_RECOMPUTE(true, true);
+      else PCTC_RECOMPUTE(true, false);
+    } else {
+      if (db) PCTC_RECOMPUTE(false, true);
+      else PCTC_RECOMPUTE(false, false);
+    }
+#undef PCTC_RECOMPUTE
+  }
+  if (db) {
+    Prof pr("db_reduce", stream);
+    hipLaunchKernelGGL(db_reduce_bf16, dim3((cw + 255) / 256), dim3(256), 0, stream, dbpart, nMt, chunk, cw, db + c0);
   }
   if (want_dH) {
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);

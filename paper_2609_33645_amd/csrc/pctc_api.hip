@@ -224,6 +224,16 @@ int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const voi
                            int32_t N, int32_t blank, float beam, int32_t chunk, double* loss, double* loss_per_utt,
                            int32_t* utt_status, float* dH, float* dW, void* workspace, size_t workspace_bytes,
                            void* stream_ptr) {
+  return pruned_ctc_fwd_bwd_ex(dtype, H, D, W, nullptr, V, targets, input_lengths, target_lengths, N, blank, beam,
+                               chunk, nullptr, loss, loss_per_utt, utt_status, dH, dW, nullptr, workspace,
+                               workspace_bytes, stream_ptr);
+}
+
+int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
+                              const int32_t* targets, const int32_t* input_lengths, const int32_t* target_lengths,
+                              int32_t N, int32_t blank, float beam, int32_t chunk, const float* utt_weight,
+                              double* loss, double* loss_per_utt, int32_t* utt_status, float* dH, float* dW,
+                              float* db, void* workspace, size_t workspace_bytes, void* stream_ptr) {
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
   if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
@@ -258,19 +268,20 @@ int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const voi
   // Algorithm 1: union and relabel
   PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
   // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
-  PCTC_HIP(launch_lse(dt, H, L.M, D, W, V, partials, lam, lam2, stream));
-  PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
+  PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
+  PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
   // lattice, total scores, zeroing of nonfinite losses, G = dL/dS
-  PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, loss_n, status, G, g, nullptr,
-                         dps, L.K_max, stream, nullptr));
-  PCTC_HIP(launch_loss_reduce(N, loss_n, status, loss, stream));
+  PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status, G, g,
+                         nullptr, dps, L.K_max, stream, nullptr));
+  PCTC_HIP(launch_loss_reduce(N, loss_n, status, utt_weight, loss, stream));
   if (loss_per_utt && N > 0)
     PCTC_HIP(hipMemcpyAsync(loss_per_utt, loss_n, N * sizeof(double), hipMemcpyDeviceToDevice, stream));
   if (utt_status && N > 0)
     PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
   // backward: chunk by chunk recomputation
-  if (dH || dW)
-    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, bws, L.bwd, stream));
+  if (dH || dW || db)
+    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
+                             stream));
   int32_t herr = 0;
   PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
@@ -306,8 +317,8 @@ int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, c
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
   // scratch = [partials][lam2]
   float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(partials) + lse_partial_bytes(M));
-  PCTC_HIP(launch_lse(dt, H, M, D, W, V, static_cast<float2*>(partials), lam, lam2, stream));
-  if (S && u_ids && K) PCTC_HIP(launch_gather_s(dt, H, M, D, W, u_ids, K, K_max, lam, S, ldS, stream));
+  PCTC_HIP(launch_lse(dt, H, M, D, W, nullptr, V, static_cast<float2*>(partials), lam, lam2, stream));
+  if (S && u_ids && K) PCTC_HIP(launch_gather_s(dt, H, M, D, W, nullptr, u_ids, K, K_max, lam, S, ldS, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
   prof_flush();
   return PCTC_OK;
@@ -337,7 +348,7 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
   char* dps = static_cast<char*>(dp_scratch);
   PCTC_HIP(upload_offsets(dp, dps, toff, yoff, soff, stream));
-  PCTC_HIP(launch_ctc_dp(dp, input_lengths, target_lengths, S, ldS, y_rel, beam, loss_per_utt, utt_status, G, g,
+  PCTC_HIP(launch_ctc_dp(dp, input_lengths, target_lengths, S, ldS, y_rel, beam, nullptr, loss_per_utt, utt_status, G, g,
                          keep_mask, dps, K_max, stream, nullptr));
   PCTC_HIP(hipStreamSynchronize(stream));
   prof_flush();
@@ -392,9 +403,10 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
   if (dt == 1 && M > 0) {
     // the union and its selected log-probabilities, as the forward would have left them
     PCTC_HIP(launch_remap_invert(remap, V, u_ids, Kdev, stream));
-    PCTC_HIP(launch_gather_s(dt, H, M, D, W, u_ids, Kdev, ldG, lam, S, ldG, stream));
+    PCTC_HIP(launch_gather_s(dt, H, M, D, W, nullptr, u_ids, Kdev, ldG, lam, S, ldG, stream));
   }
-  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, V, lam2, G, ldG, g, remap, S, ldG, dH, dW, bwd_scratch, plan, stream));
+  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, nullptr, V, lam2, G, ldG, g, remap, S, ldG, dH, dW, nullptr, bwd_scratch,
+                           plan, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
   prof_flush();
   return PCTC_OK;

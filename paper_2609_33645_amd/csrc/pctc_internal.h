@@ -34,10 +34,11 @@ hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t bla
 // ---- normaliser and selected log-probabilities ------------------------------------------
 int lse_partitions(int M, int V);
 size_t lse_partial_bytes(int M);
-hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, int V, float2* partials,
-                      double* lam, float2* lam2, hipStream_t stream);
-hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const int32_t* u_ids,
-                           const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+// bias: device float [V] or null (logits H W^T + b).
+hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                      float2* partials, double* lam, float2* lam2, hipStream_t stream);
+hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const float* bias,
+                           const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream);
 
 // ---- backward ---------------------------------------------------------------------------
@@ -45,25 +46,28 @@ struct BwdPlan {
   int chunk;       // vocabulary columns per step
   int splits;      // k-slices of the dH product per chunk
   int Mp;          // padded frame count (pitch of the transposed head input)
-  size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, total;
+  size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int chunk);
 // S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
 // of each recomputed chunk from them).
-hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, int V, const float2* lam2,
-                           const float* G, int ldG, const float* g, const int32_t* remap, const float* S, int ldS,
-                           float* dH, float* dW, void* scratch, const BwdPlan& plan, hipStream_t stream);
+hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                           const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
+                           const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
+                           const BwdPlan& plan, hipStream_t stream);
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
 
 // ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
-hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
-                                   int* P_out, hipStream_t stream);
-hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const int32_t* u_ids,
-                                const int32_t* K, int K_max, const double* lam, float* S, int ldS, hipStream_t stream);
-hipError_t launch_bwd_chunk_bf16(const uint16_t* H, const uint16_t* Hs, int M, int D, const uint16_t* W, int c0,
+hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
+                                   float2* partials, int* P_out, hipStream_t stream);
+hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias,
+                                const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
+                                hipStream_t stream);
+hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
-                                 int slice, bool want_dH, bool want_dW, float* dW, hipStream_t stream);
+                                 int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
+                                 hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
 
 // ---- alignment lattice ------------------------------------------------------------------
@@ -77,11 +81,13 @@ struct DpPlan {
 };
 DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam);
 // Uploads the host offsets into the scratch (async) and runs the whole lattice stage.
+// weight: device float [N] loss weights of the utterances, or null (all 1): G rows of
+// utterance n are -w_n gamma.
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
-                         const int32_t* y_rel, float beam, double* loss_n, int32_t* status, float* G,
-                         float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
+                         const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
+                         float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
                          void* host_staging);
-hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, double* loss,
+hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, const float* weight, double* loss,
                               hipStream_t stream);
 
 }  // namespace pctc

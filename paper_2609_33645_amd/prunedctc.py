@@ -51,6 +51,9 @@ def lib() -> ctypes.CDLL:
     L.pruned_ctc_fwd_bwd.argtypes = [c_i32, c_p, c_i32, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f, c_i32,
                                      c_p, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]
     L.pruned_ctc_fwd_bwd.restype = c_i32
+    L.pruned_ctc_fwd_bwd_ex.argtypes = [c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f, c_i32,
+                                        c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]
+    L.pruned_ctc_fwd_bwd_ex.restype = c_i32
     L.pctc_status_string.argtypes = [c_i32]
     L.pctc_status_string.restype = ctypes.c_char_p
     L.pctc_last_error.argtypes = []
@@ -147,11 +150,16 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
                        target_lengths: Sequence[int], blank: int = 0, beam: float = math.inf, chunk: int = 0,
                        want_dH: bool = True, want_dW: bool = True, workspace: Optional[torch.Tensor] = None,
                        stream=None, dH_out: Optional[torch.Tensor] = None,
-                       dW_out: Optional[torch.Tensor] = None) -> Dict[str, torch.Tensor]:
+                       dW_out: Optional[torch.Tensor] = None, bias: Optional[torch.Tensor] = None,
+                       utt_weight: Optional[torch.Tensor] = None, want_db: bool = False) -> Dict[str, torch.Tensor]:
     """Loss and head gradients of Pruned CTC.  H [M, D] and W [V, D] are device tensors of
     the same dtype (bfloat16 or float32); targets is a device int32 tensor; the length
-    arrays are host sequences.  Returns loss (float64 [1]), loss_per_utt, status, dH, dW.
-    dH_out / dW_out: optional preallocated float32 [M, D] / [V, D] gradient buffers."""
+    arrays are host sequences.  Returns loss (float64 [1]), loss_per_utt, status, dH, dW
+    and, with want_db, db.  dH_out / dW_out: optional preallocated float32 [M, D] / [V, D]
+    gradient buffers.  bias: optional float32 [V] head bias (logits H W^T + b; a blank
+    offset eta is added to bias[blank], and its gradient is db[blank]).  utt_weight:
+    optional float32 [N] loss weights (loss = sum_n w_n L_n; loss_per_utt stays
+    unweighted)."""
     L = lib()
     dt = _dtype_code(H)
     if W.dtype != H.dtype:
@@ -183,11 +191,27 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
     status = torch.zeros(max(N, 1), dtype=torch.int32, device=dev)
     dH = _grad_buffer(dH_out, (M, D), dev) if want_dH else None
     dW = _grad_buffer(dW_out, (V, D), dev) if want_dW else None
-    code = L.pruned_ctc_fwd_bwd(dt, _ptr(H), D, _ptr(W), V, _ptr(targets), _i32p(T), _i32p(U), N, int(blank),
-                                float(beam), int(chunk), _ptr(loss), _ptr(loss_n), _ptr(status), _ptr(dH), _ptr(dW),
-                                ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()), _stream(stream))
+    db = torch.empty(V, dtype=torch.float32, device=dev) if want_db else None
+    if bias is not None:
+        bias = bias.to(device=dev, dtype=torch.float32).contiguous()
+        if bias.numel() != V:
+            raise PrunedCTCError(-1, "bias must have V entries")
+    if utt_weight is not None:
+        utt_weight = utt_weight.to(device=dev, dtype=torch.float32).contiguous()
+        if utt_weight.numel() != N:
+            raise PrunedCTCError(-1, "utt_weight must have N entries")
+    if bias is None and utt_weight is None and db is None:
+        code = L.pruned_ctc_fwd_bwd(dt, _ptr(H), D, _ptr(W), V, _ptr(targets), _i32p(T), _i32p(U), N, int(blank),
+                                    float(beam), int(chunk), _ptr(loss), _ptr(loss_n), _ptr(status), _ptr(dH),
+                                    _ptr(dW), ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()),
+                                    _stream(stream))
+    else:
+        code = L.pruned_ctc_fwd_bwd_ex(dt, _ptr(H), D, _ptr(W), _ptr(bias), V, _ptr(targets), _i32p(T), _i32p(U), N,
+                                       int(blank), float(beam), int(chunk), _ptr(utt_weight), _ptr(loss), _ptr(loss_n),
+                                       _ptr(status), _ptr(dH), _ptr(dW), _ptr(db), ctypes.c_void_p(ws.data_ptr()),
+                                       ctypes.c_size_t(ws.numel()), _stream(stream))
     _check(code, "pruned_ctc_fwd_bwd")
-    return {"loss": loss, "loss_per_utt": loss_n[:N], "status": status[:N], "dH": dH, "dW": dW,
+    return {"loss": loss, "loss_per_utt": loss_n[:N], "status": status[:N], "dH": dH, "dW": dW, "db": db,
             "workspace_bytes": nbytes}
 
 

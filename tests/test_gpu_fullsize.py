@@ -177,3 +177,47 @@ def test_workspace_flat_in_vocabulary():
         del out, W, dW
     vals = np.array(list(extra.values()))
     assert vals.max() - vals.min() <= 1 << 20, extra
+
+
+@pytest.mark.timeout(900)
+def test_full_size_bias_weights_db():
+    """Zipformer-M-sized head with a bias (blank offset included), token-count loss weights
+    and db, in the benchmark's launch configuration; sampled outputs as above."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.zipformer_m(1, beam=16.0)
+    rng = np.random.default_rng(11)
+    b = (0.5 * rng.standard_normal(wl.V)).astype(np.float32)
+    b[wl.blank] += 3.0
+    w = np.full(wl.N, 1.0 / float(wl.target_lengths.sum()), np.float32)
+    say(f"full-size bias/weights zipformer_m: N={wl.N} M={wl.M} V={wl.V}")
+    H, W, y = to_dev(wl)
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
+                                       bias=torch.from_numpy(b).cuda(), utt_weight=torch.from_numpy(w).cuda(),
+                                       want_db=True)
+    torch.cuda.synchronize()
+    W64 = wl.W.astype(np.float64)
+    H64 = wl.H.astype(np.float64)
+    b64 = b.astype(np.float64)
+    un = oracle.union_remap(wl.targets, wl.target_lengths, wl.blank, wl.V)
+    lam = oracle.log_normalizer(H64, W64, bias=b64)
+    S = oracle.selected_logprobs(H64, W64, un["u_ids"], lam, bias=b64)
+    dp = oracle.ctc_from_scores(S, un["y_rel"], wl.input_lengths, wl.target_lengths, wl.beam,
+                                weights=w.astype(np.float64))
+    say("  oracle forward done")
+    np.testing.assert_array_equal(out["status"].cpu().numpy(), dp["status"])
+    assert loss_rel(float(out["loss"].item()), dp["loss"]) <= 1e-5
+    np.testing.assert_allclose(out["loss_per_utt"].cpu().numpy(), dp["loss_n"], rtol=1e-5)
+    frames, classes = _samples(wl, rng, un["u_ids"])
+    rows = oracle.head_backward_rows(H64, W64, lam, dp["G"], dp["g"], un["u_ids"], frames, classes, bias=b64)
+    dH_s = out["dH"][torch.from_numpy(frames).cuda()].cpu().numpy()
+    dW_s = out["dW"][torch.from_numpy(classes).cuda()].cpu().numpy()
+    db_s = out["db"][torch.from_numpy(classes).cuda()].cpu().numpy()
+    say(f"  cos dH={cosine(dH_s, rows['dH']):.7f} dW={cosine(dW_s, rows['dW']):.7f} db={cosine(db_s, rows['db']):.7f}")
+    assert cosine(dH_s, rows["dH"]) >= 0.99999 and cosine(dW_s, rows["dW"]) >= 0.99999
+    assert cosine(db_s, rows["db"]) >= 0.999
+    # d eta = db[blank]
+    bi = int(np.nonzero(classes == wl.blank)[0][0])
+    assert abs(db_s[bi] - rows["db"][bi]) <= 1e-3 * abs(rows["db"][bi])
+    del out, H, W, y
+    torch.cuda.empty_cache()

@@ -283,3 +283,43 @@ def test_error_codes():
                                          blank, beam)
         assert e.value.code == code, (targets, T, U, blank, beam)
     del y
+
+
+# ---------------------------------------------------------------------------------------
+# head bias, blank offset, loss weights and the bias gradient (pruned_ctc_fwd_bwd_ex)
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,dtype,beam,blank,chunk,zero_w", [
+    (0, "f32", math.inf, 0, 256, False), (1, "bf16", 16.0, 0, 0, True), (2, "bf16", math.inf, 2999, 512, False),
+    (3, "f32", 4.0, 11, 0, True), (4, "bf16", 0.0, 0, 1024, False)])
+def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w):
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(40 + seed, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
+                                blank=blank, beam=beam, w_std=0.5)
+    rng = np.random.default_rng(seed)
+    b = rng.standard_normal(wl.V).astype(np.float32)
+    b[blank] += 2.0                                  # blank offset eta
+    w = rng.uniform(0.05, 2.0, size=wl.N).astype(np.float32)
+    if zero_w:
+        w[1] = 0.0
+    say(f"e2e bias/weights seed={seed} {dtype} beam={beam} blank={blank} M={wl.M} w={np.round(w, 3).tolist()}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
+                         bias=b.astype(np.float64), weights=w.astype(np.float64))
+    H, W, y = to_dev(wl)
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam, chunk=chunk,
+                                       bias=torch.from_numpy(b).cuda(), utt_weight=torch.from_numpy(w).cuda(),
+                                       want_db=True)
+    res = {"loss": float(out["loss"].item()), "status": out["status"].cpu().numpy(), "dH": out["dH"].cpu().numpy(),
+           "dW": out["dW"].cpu().numpy()}
+    np.testing.assert_allclose(out["loss_per_utt"].cpu().numpy(), ref["loss_n"], rtol=1e-5, atol=1e-6)
+    _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
+    db = out["db"].cpu().numpy()
+    cdb = cosine(db, ref["db"])
+    say(f"  db cos={cdb:.7f} rel={rel_err(db, ref['db']):.3g}  d_eta gpu={db[blank]:.6g} oracle={ref['db'][blank]:.6g}")
+    if dtype == "f32":
+        assert rel_err(db, ref["db"]) <= 1e-4
+    else:
+        assert cdb >= 0.999
+        assert cdb >= 0.99999
+    assert abs(db[blank] - ref["db"][blank]) <= 2e-3 * max(1.0, abs(ref["db"][blank]))
