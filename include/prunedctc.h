@@ -178,6 +178,24 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
                     float beam, double* loss_per_utt, int32_t* utt_status, float* G, float* g,
                     uint8_t* keep_mask, void* dp_scratch, void* stream);
 
+/* Discarded posterior mass (App. B.3): for each beam b and utterance n,
+ *   delta[b * N + n] = 1 - (sum over the alignments that the beam retains) /
+ *                          (sum over all valid alignments),
+ * both sums of prod_t p_{pi_t}(t) on the same scores S (layout as for pctc_ctc_dp).  The
+ * retained set is the one pruned_ctc_fwd_bwd uses at that beam.  Two forward recursions run
+ * in lockstep in double precision with one shared per-frame scale; the per-frame emission
+ * factors are formed once in float and used by both, so their rounding cancels in the
+ * ratio.  Estimates carry the rounding of both sums (they are not certified bounds) and
+ * can be slightly negative.  Utterances that are not alignable get NaN.
+ * beams: HOST float [nbeams], each finite and >= 0.  delta: device double [nbeams * N].
+ * dp_scratch: pctc_discarded_mass_scratch_bytes() bytes.  Synchronises the stream. */
+size_t pctc_discarded_mass_scratch_bytes(int32_t N, const int32_t* input_lengths,
+                                         const int32_t* target_lengths);
+int32_t pctc_discarded_mass(const float* S, int32_t ldS, int32_t K_max, const int32_t* y_rel,
+                            const int32_t* input_lengths, const int32_t* target_lengths, int32_t N,
+                            const float* beams, int32_t nbeams, double* delta, void* dp_scratch,
+                            void* stream);
+
 /* Recomputed backward (Eq. vjp; Algorithm 1 backward loop): for each vocabulary chunk,
  * dZ = scatter_U(G) - g p with p = exp(H W^T - lam) recomputed, then dH = sum dZ W and
  * dW = dZ^T H (rows of frames with g[m] == 0 contribute nothing).  remap: device

@@ -18,6 +18,7 @@ from .prunedctc_oracle import (  # noqa: F401
     extended_labels,
     ctc_utterance,
     ctc_from_scores,
+    discarded_mass,
     head_backward,
     head_backward_rows,
     fwd_bwd,

@@ -326,6 +326,30 @@ def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: f
             "loss": float((wv * loss_n).sum())}
 
 
+def discarded_mass(S: np.ndarray, y_rel, input_lengths, target_lengths, beams,
+                   slack: float = KEEP_SLACK) -> np.ndarray:
+    """Discarded posterior mass (App. B.3): delta[b, n] = 1 - exp(-(L_beta,n - L_n)) for each
+    beam, the posterior mass (given the transcript) of the alignments the beam drops, from
+    the pruned and unpruned losses on the same scores (fp64), evaluated as
+    -expm1(-Delta).  NaN for utterances that are not alignable."""
+    S = np.asarray(S, np.float64)
+    toff = _offsets(input_lengths)
+    yoff = _offsets(target_lengths)
+    N = len(input_lengths)
+    beams = list(beams)
+    out = np.full((len(beams), N), np.nan)
+    for n in range(N):
+        rows = slice(int(toff[n]), int(toff[n + 1]))
+        y = [int(v) for v in np.asarray(y_rel)[yoff[n]:yoff[n + 1]]]
+        full = ctc_utterance(S[rows], y, 0, math.inf, slack)
+        if not full["alignable"] or not np.isfinite(full["logP"]):
+            continue
+        for b, beam in enumerate(beams):
+            pr = ctc_utterance(S[rows], y, 0, beam, slack)
+            out[b, n] = -math.expm1(-(full["logP"] - pr["logP"]))
+    return out
+
+
 def head_backward(H, W, lam, G, g, u_ids, chunk: int = 4096, bias=None) -> Dict[str, np.ndarray]:
     """The recomputed backward stage alone (Eq. vjp; Algorithm 1 backward loop):
     dZ[m, v] = scatter_U(G)[m, v] - g_m p_v(m) with p_v(m) = exp(Z[m, v] - lambda_m),

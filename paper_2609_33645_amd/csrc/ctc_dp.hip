@@ -55,6 +55,7 @@ DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
   p.off_dup_next = take(Y * sizeof(int32_t));
   p.off_dup_first = take(Y * sizeof(int32_t));
   p.off_logp = take(N * sizeof(double));
+  p.off_status = take(N * sizeof(int32_t));
   p.off_tab_fa = take(L * sizeof(float));
   p.off_tab_fb = take(L * sizeof(float));
   p.off_sc_fa = take(M * sizeof(double));
@@ -636,6 +637,199 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   }
   (void)T;
   (void)U;
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
+// Discarded posterior mass (App. B.3): delta_n = 1 - (sum over retained alignments) /
+// (sum over all valid alignments), both of prod_t p_{pi_t}(t) on the same scores.  One
+// wavefront per utterance runs the two forward recursions in lockstep in linear space and
+// double precision, with one shared scale per frame (the full recursion's maximum), so
+// the per-frame scaling cancels in the ratio.  The emission factor exp(S - m_t) (m_t the
+// frame's largest selected score) is formed once in float and used by both recursions.
+// Utterances that are not alignable get NaN.
+// ---------------------------------------------------------------------------------------
+
+__device__ __forceinline__ double lane_up_d(double x) { return lane_up(x); }
+
+__device__ __forceinline__ double wave_max_d(double x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x = fmax(x, __shfl_xor(x, o, 64));
+  return x;
+}
+__device__ __forceinline__ double wave_sum_d(double x) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) x += __shfl_xor(x, o, 64);
+  return x;
+}
+
+template <int Q>
+__global__ void __launch_bounds__(64)
+dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
+                    const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff,
+                    const int32_t* __restrict__ y_rel, const int32_t* __restrict__ status,
+                    const uint8_t* __restrict__ mask, double* __restrict__ delta) {
+  const int n = blockIdx.x;
+  const int lane = threadIdx.x;
+  if (status[n] != 0) {
+    if (lane == 0) delta[n] = __longlong_as_double(0x7ff8000000000000LL);
+    return;
+  }
+  const int t0 = toff[n], T = toff[n + 1] - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  const int Sp = 2 * U + 1;
+  const int64_t base = soff[n];
+  const int* y = y_rel + y0;
+  int col[Q];
+  bool valid[Q], skip_in[Q], fin[Q];
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    const int s = lane * Q + q;
+    valid[q] = s < Sp;
+    col[q] = (valid[q] && (s & 1)) ? y[(s - 1) >> 1] : 0;
+    skip_in[q] = valid[q] && (s & 1) && s >= 3 && y[(s - 1) >> 1] != y[(s - 3) >> 1];
+    fin[q] = valid[q] && s >= Sp - 2;
+  }
+  double af[Q], ap[Q];  // full and retained forward sums, scaled per frame
+  for (int t = 0; t < T; ++t) {
+    const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
+    float e[Q];
+    int mk[Q];
+    float em = -INFINITY;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      e[q] = valid[q] ? row[col[q]] : -INFINITY;
+      mk[q] = valid[q] ? static_cast<int>(mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q]) : 0;
+      em = fmaxf(em, e[q]);
+    }
+    em = wave_max(em);
+    double pe[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) pe[q] = valid[q] ? static_cast<double>(fast_exp2((e[q] - em) * kLog2e)) : 0.0;
+    double nf[Q], np[Q];
+    if (t == 0) {
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int s = lane * Q + q;
+        nf[q] = (valid[q] && s < 2) ? pe[q] : 0.0;
+        np[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? pe[q] : 0.0;
+      }
+    } else {
+      const double uf1 = lane_up_d(af[Q - 1]), up1 = lane_up_d(ap[Q - 1]);
+      const double uf2 = (Q >= 2) ? lane_up_d(af[Q >= 2 ? Q - 2 : 0]) : lane_up_d(uf1);
+      const double up2 = (Q >= 2) ? lane_up_d(ap[Q >= 2 ? Q - 2 : 0]) : lane_up_d(up1);
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const double f0 = af[q], p0 = ap[q];
+        const double f1 = (q >= 1) ? af[q >= 1 ? q - 1 : 0] : uf1;
+        const double p1 = (q >= 1) ? ap[q >= 1 ? q - 1 : 0] : up1;
+        const double f2 = (q >= 2) ? af[q >= 2 ? q - 2 : 0] : (q == 1 ? uf1 : uf2);
+        const double p2 = (q >= 2) ? ap[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
+        nf[q] = valid[q] ? pe[q] * (f0 + f1 + (skip_in[q] ? f2 : 0.0)) : 0.0;
+        np[q] = valid[q] ? pe[q] * (((mk[q] & 1) ? p0 : 0.0) + ((mk[q] & 2) ? p1 : 0.0) +
+                                    ((skip_in[q] && (mk[q] & 4)) ? p2 : 0.0))
+                         : 0.0;
+      }
+    }
+    double c = 0.0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) c = fmax(c, nf[q]);
+    c = wave_max_d(c);
+    const double inv = (c > 0.0) ? 1.0 / c : 0.0;
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      af[q] = nf[q] * inv;
+      ap[q] = np[q] * inv;
+    }
+  }
+  double sf = 0.0, sp = 0.0;
+#pragma unroll
+  for (int q = 0; q < Q; ++q) {
+    if (!fin[q]) continue;
+    const int mk = static_cast<int>(mask[base + static_cast<int64_t>(T - 1) * Sp + lane * Q + q]);
+    sf += af[q];
+    if (mk & 8) sp += ap[q];
+  }
+  sf = wave_sum_d(sf);
+  sp = wave_sum_d(sp);
+  if (lane == 0) delta[n] = (sf > 0.0) ? 1.0 - sp / sf : __longlong_as_double(0x7ff8000000000000LL);
+}
+
+static hipError_t launch_discarded(int Q, int N, hipStream_t stream, const float* S, int ldS, const int32_t* toff,
+                                   const int32_t* yoff, const int64_t* soff, const int32_t* y_rel,
+                                   const int32_t* status, const uint8_t* mask, double* delta) {
+#define PCTC_DISC(QQ)                                                                                             \
+  case QQ:                                                                                                        \
+    hipLaunchKernelGGL((dp_discarded_kernel<QQ>), dim3(N), dim3(64), 0, stream, S, ldS, toff, yoff, soff, y_rel, \
+                       status, mask, delta);                                                                      \
+    break;
+  switch (Q) {
+    PCTC_DISC(1)
+    PCTC_DISC(2)
+    PCTC_DISC(3)
+    PCTC_DISC(4)
+    PCTC_DISC(6)
+    PCTC_DISC(8)
+    PCTC_DISC(10)
+    PCTC_DISC(13)
+    PCTC_DISC(16)
+    PCTC_DISC(20)
+    PCTC_DISC(24)
+    PCTC_DISC(32)
+    default:
+      return hipErrorInvalidValue;
+  }
+#undef PCTC_DISC
+  return hipGetLastError();
+}
+
+hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, const int32_t* y_rel, const float* beams,
+                                 int nbeams, double* delta, void* scratch, int K_max, hipStream_t stream) {
+  const int N = plan.N;
+  if (N == 0 || nbeams == 0) return hipSuccess;
+  if (!plan.pruned) return hipErrorInvalidValue;
+  char* sc = static_cast<char*>(scratch);
+  int32_t* toff = reinterpret_cast<int32_t*>(sc + plan.off_toff);
+  int32_t* yoff = reinterpret_cast<int32_t*>(sc + plan.off_yoff);
+  int64_t* soff = reinterpret_cast<int64_t*>(sc + plan.off_soff);
+  int32_t* frame_utt = reinterpret_cast<int32_t*>(sc + plan.off_frame_utt);
+  int32_t* dnext = reinterpret_cast<int32_t*>(sc + plan.off_dup_next);
+  int32_t* dfirst = reinterpret_cast<int32_t*>(sc + plan.off_dup_first);
+  int32_t* status = reinterpret_cast<int32_t*>(sc + plan.off_status);
+  double* loss_n = reinterpret_cast<double*>(sc + plan.off_logp);  // scratch use only
+  float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
+  float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);
+  double* sva = reinterpret_cast<double*>(sc + plan.off_sc_va);
+  double* svb = reinterpret_cast<double*>(sc + plan.off_sc_vb);
+  double* vbest = reinterpret_cast<double*>(sc + plan.off_vbest);
+  uint8_t* mask = reinterpret_cast<uint8_t*>(sc + plan.off_mask);
+  {
+    Prof pr("dp_prep", stream);
+    hipLaunchKernelGGL(dp_prep_kernel, dim3(N), dim3(256), 0, stream, toff, yoff, y_rel, K_max, status, dnext, dfirst,
+                       frame_utt, loss_n);
+  }
+  const int Q = pick_q(plan.Smax);
+  if (Q < 0) return hipErrorInvalidValue;
+  for (int b = 0; b < nbeams; ++b) {
+    hipError_t e;
+    {
+      Prof pr("dp_viterbi", stream);
+      e = launch_pass<true>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva, svb,
+                            vbest, loss_n);
+      if (e != hipSuccess) return e;
+    }
+    if (plan.M > 0) {
+      Prof pr("dp_mask", stream);
+      hipLaunchKernelGGL(dp_mask_kernel, dim3(plan.M), dim3(256), 0, stream, S, ldS, toff, yoff, soff, y_rel, frame_utt,
+                         status, tva, tvb, sva, svb, vbest, beams[b], kKeepSlack, mask);
+    }
+    {
+      Prof pr("dp_discarded", stream);
+      e = launch_discarded(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, mask,
+                           delta + static_cast<int64_t>(b) * N);
+      if (e != hipSuccess) return e;
+    }
+  }
   return hipGetLastError();
 }
 

@@ -355,6 +355,37 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
   return PCTC_OK;
 }
 
+size_t pctc_discarded_mass_scratch_bytes(int32_t N, const int32_t* input_lengths, const int32_t* target_lengths) {
+  if (N < 0 || (N > 0 && (!input_lengths || !target_lengths))) return 0;
+  for (int n = 0; n < N; ++n)
+    if (input_lengths[n] < 1 || target_lengths[n] < 0 || target_lengths[n] > PCTC_MAX_TARGET) return 0;
+  return plan_dp(N, input_lengths, target_lengths, 1.f).total;
+}
+
+int32_t pctc_discarded_mass(const float* S, int32_t ldS, int32_t K_max, const int32_t* y_rel,
+                            const int32_t* input_lengths, const int32_t* target_lengths, int32_t N, const float* beams,
+                            int32_t nbeams, double* delta, void* dp_scratch, void* stream_ptr) {
+  if (N < 0 || nbeams < 0 || ldS < K_max || K_max < 1 || (nbeams > 0 && !beams)) return PCTC_EINVAL;
+  for (int b = 0; b < nbeams; ++b)
+    if (!(beams[b] >= 0.f) || !(beams[b] < INFINITY)) return PCTC_EINVAL;  // finite, non-negative
+  for (int n = 0; n < N; ++n) {
+    if (input_lengths[n] < 1 || target_lengths[n] < 0) return PCTC_ELENGTH;
+    if (target_lengths[n] > PCTC_MAX_TARGET) return PCTC_ETOOLONG;
+  }
+  if (N == 0 || nbeams == 0) return PCTC_OK;
+  if (!S || !delta || !dp_scratch) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  const DpPlan dp = plan_dp(N, input_lengths, target_lengths, 1.f);
+  std::vector<int32_t> toff, yoff;
+  std::vector<int64_t> soff;
+  host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
+  PCTC_HIP(upload_offsets(dp, static_cast<char*>(dp_scratch), toff, yoff, soff, stream));
+  PCTC_HIP(launch_discarded_mass(dp, S, ldS, y_rel, beams, nbeams, delta, dp_scratch, K_max, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
 // Stage entry scratch: the backward plan, then u_ids [ldG], K, and S [M][ldG].
 struct BwdStageLayout {
   BwdPlan plan;

@@ -75,7 +75,7 @@ struct DpPlan {
   int N, M, Y, Smax;
   bool pruned;
   int64_t lattice;  // sum_n T_n (2U_n+1)
-  size_t off_toff, off_yoff, off_soff, off_frame_utt, off_dup_next, off_dup_first, off_logp,
+  size_t off_toff, off_yoff, off_soff, off_frame_utt, off_dup_next, off_dup_first, off_logp, off_status,
       off_tab_fa, off_tab_fb, off_tab_va, off_tab_vb, off_sc_fa, off_sc_fb, off_sc_va, off_sc_vb,
       off_vbest, off_mask, total;
 };
@@ -87,6 +87,10 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
                          const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
                          void* host_staging);
+// delta [nbeams][N]: discarded posterior mass of each utterance at each beam (host beams).
+// Needs a plan made with a finite beam (the Viterbi tables and the arc mask).
+hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, const int32_t* y_rel, const float* beams,
+                                 int nbeams, double* delta, void* scratch, int K_max, hipStream_t stream);
 hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, const float* weight, double* loss,
                               hipStream_t stream);
 

@@ -68,6 +68,11 @@ def lib() -> ctypes.CDLL:
     L.pctc_dp_scratch_bytes.restype = c_sz
     L.pctc_ctc_dp.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, c_f, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_ctc_dp.restype = c_i32
+    L.pctc_discarded_mass_scratch_bytes.argtypes = [c_i32, i32p, i32p]
+    L.pctc_discarded_mass_scratch_bytes.restype = c_sz
+    L.pctc_discarded_mass.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, ctypes.POINTER(ctypes.c_float), c_i32,
+                                      c_p, c_p, c_p]
+    L.pctc_discarded_mass.restype = c_i32
     L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_scratch_bytes.restype = c_sz
     L.pctc_bwd_chunk.argtypes = [c_i32, c_i32, c_i32, c_i32]
@@ -293,6 +298,31 @@ def ctc_dp(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_lengths, 
     if mask is not None:
         out["mask"] = mask[:lattice]
     return out
+
+
+def discarded_mass(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_lengths, beams: Sequence[float],
+                   stream=None) -> torch.Tensor:
+    """Discarded posterior mass delta [len(beams), N] (float64) of every utterance at every
+    beam, on given selected-class scores S [M, K] (column 0 = blank)."""
+    L = lib()
+    T = _host_i32(input_lengths)
+    U = _host_i32(target_lengths)
+    N = int(T.size)
+    M, K = int(S.shape[0]), int(S.shape[1])
+    dev = S.device
+    ldS = ((K + 3) // 4) * 4
+    Sp = torch.zeros((max(M, 1), ldS), dtype=torch.float32, device=dev)
+    Sp[:M, :K] = S.to(torch.float32)
+    y_rel = y_rel.to(torch.int32).contiguous()
+    b = np.ascontiguousarray(np.asarray(beams, np.float32))
+    delta = torch.empty((max(len(b), 1), max(N, 1)), dtype=torch.float64, device=dev)
+    nbytes = int(L.pctc_discarded_mass_scratch_bytes(N, _i32p(T), _i32p(U)))
+    scratch = _workspace(nbytes, dev)
+    code = L.pctc_discarded_mass(_ptr(Sp), ldS, K, _ptr(y_rel), _i32p(T), _i32p(U), N,
+                                 b.ctypes.data_as(ctypes.POINTER(ctypes.c_float)), int(b.size), _ptr(delta),
+                                 ctypes.c_void_p(scratch.data_ptr()), _stream(stream))
+    _check(code, "pctc_discarded_mass")
+    return delta[:len(b), :N]
 
 
 def head_bwd(H: torch.Tensor, W: torch.Tensor, lam: torch.Tensor, G: torch.Tensor, g: torch.Tensor,

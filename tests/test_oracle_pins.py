@@ -536,3 +536,44 @@ def test_bias_rows_and_stage_agree():
     np.testing.assert_allclose(rows["dH"], full["dH"][fr], atol=1e-12)
     np.testing.assert_allclose(rows["dW"], full["dW"][cl], atol=1e-12)
     np.testing.assert_allclose(rows["db"], full["db"][cl], atol=1e-12)
+
+
+# ---------------------------------------------------------------------------------------
+# discarded posterior mass (App. B.3)
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,beam", [(0, 0.5), (1, 1.5), (2, 3.0), (3, 0.0)])
+def test_discarded_mass_by_enumeration(seed, beam):
+    """delta = 1 - (retained alignment sum) / (all-alignment sum), with both sums taken by
+    brute-force enumeration of alignments and the arc rule applied per enumerated arc."""
+    rng = np.random.default_rng(300 + seed)
+    T, C = 5, 3
+    y = [1, 2] if seed % 2 == 0 else [2]
+    logp = np.log(rng.dirichlet(np.ones(C), size=T))
+    aligns = brute.valid_alignments(T, C, y, 0)
+    scores = np.array([sum(logp[t, pi[t]] for t in range(T)) for pi in aligns])
+    best_through = {}
+    for pi, sc in zip(aligns, scores):
+        for a in brute.arcs_of(pi, 0):
+            best_through[a] = max(best_through.get(a, -math.inf), sc)
+    kept = {a for a, v in best_through.items() if v >= scores.max() - beam - oracle.KEEP_SLACK}
+    keep = np.array([all(a in kept for a in brute.arcs_of(pi, 0)) for pi in aligns])
+    want = 1.0 - np.exp(scores[keep]).sum() / np.exp(scores).sum()
+    got = oracle.discarded_mass(logp, np.array(y), [T], [len(y)], [beam])
+    assert abs(got[0, 0] - want) < 1e-12
+    assert -1e-15 <= got[0, 0] <= 1.0
+
+
+def test_discarded_mass_limits():
+    """delta = 0 without pruning (infinite beam), the occupancy bound of App. B.3
+    |gamma_beta - gamma| <= delta holds, and a not-alignable utterance gives NaN."""
+    from paper_2609_33645_amd import workloads
+    S = workloads.random_scores(9, 30, 6).astype(np.float64)
+    T, U = [20, 10], [4, 7]
+    y = np.array([1, 2, 3, 1, 2, 2, 2, 2, 2, 2, 2], np.int64)
+    d = oracle.discarded_mass(S, y, T, U, [math.inf, 2.0, 6.0])
+    assert d[0, 0] == 0.0 and np.isnan(d[:, 1]).all()   # 7 labels with 6 repeats need 13 frames
+    assert 0.0 <= d[2, 0] <= d[1, 0] <= 1.0
+    full = oracle.ctc_utterance(S[:20], [1, 2, 3, 1], 0)
+    pr = oracle.ctc_utterance(S[:20], [1, 2, 3, 1], 0, beam=2.0)
+    assert np.abs(pr["gamma"] - full["gamma"]).max() <= d[1, 0] + 1e-12
