@@ -650,7 +650,13 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
 // Utterances that are not alignable get NaN.
 // ---------------------------------------------------------------------------------------
 
-__device__ __forceinline__ double lane_up_d(double x) { return lane_up(x); }
+// Linear-space neighbour move: lane l receives lane l-1, lane 0 receives 0 (no state).
+__device__ __forceinline__ double lane_up_d(double x) {
+  const long long b = __double_as_longlong(x);
+  const int lo = dpp_up_i(static_cast<int>(b), 0);
+  const int hi = dpp_up_i(static_cast<int>(b >> 32), 0);
+  return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
+}
 
 __device__ __forceinline__ double wave_max_d(double x) {
 #pragma unroll

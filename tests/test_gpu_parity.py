@@ -323,3 +323,50 @@ def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w):
         assert cdb >= 0.999
         assert cdb >= 0.99999
     assert abs(db[blank] - ref["db"][blank]) <= 2e-3 * max(1.0, abs(ref["db"][blank]))
+
+
+# ---------------------------------------------------------------------------------------
+# discarded posterior mass (App. B.3)
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,N,Trange,K", [(0, 4, (20, 90), 40), (1, 3, (100, 300), 120), (2, 2, (1500, 1500), 420)])
+def test_discarded_mass(seed, N, Trange, K):
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    # integer scores and half-integer beams: every arc decision is at least 0.499 from the
+    # threshold, so both sides retain the same arcs
+    S, y_rel, T, U = _dp_case(60 + seed, N, Trange, K, U_frac=0.27 if seed == 2 else 0.3, integer=True)
+    beams = [0.5, 2.5, 6.5, 12.5, 30.5, 1.0e4]
+    say(f"discarded mass seed={seed} N={N} T={T.tolist()} U={U.tolist()} beams={beams}")
+    ref = oracle.discarded_mass(S.astype(np.float64), y_rel, T, U, beams)
+    got = prunedctc.discarded_mass(torch.from_numpy(S).cuda(), torch.from_numpy(y_rel).cuda(), T, U, beams)
+    got = got.cpu().numpy()
+    np.testing.assert_array_equal(np.isnan(got), np.isnan(ref))
+    ok = ~np.isnan(ref)
+    err = np.abs(got[ok] - ref[ok])
+    say(f"  max delta {np.nanmax(ref):.3g}; max |gpu - oracle| {err.max() if err.size else 0:.3g}")
+    assert np.all(err <= 1e-10 + 1e-5 * np.abs(ref[ok]))
+    assert np.all(got[-1][ok[-1]] == 0.0)  # a beam above every margin drops nothing
+
+
+def test_beam_sweep_tool():
+    """The sweep tool end to end on a small bf16 batch: deltas agree with the oracle's on the
+    same S (the oracle's S), decrease with the beam, and the required beam is the first beam
+    whose maximum is within the criterion."""
+    import torch
+    from paper_2609_33645_amd import beam_sweep
+    wl = workloads.random_small(77, N=4, T_range=(30, 120), D=64, V=2000, dtype="bf16", p_repeat=0.1, w_std=0.4)
+    H, W, y = to_dev(wl)
+    beams = [2.0, 8.0, 32.0, 200.0]
+    res = beam_sweep.beam_sweep(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, beams)
+    mx = [r["max_delta"] for r in res["rows"]]
+    say(f"beam sweep: {[(r['beam'], r['max_delta'], r['above']) for r in res['rows']]} required={res['required_beam']}")
+    assert all(mx[i] >= mx[i + 1] - 1e-12 for i in range(len(mx) - 1))
+    first_ok = next((r["beam"] for r in res["rows"] if r["above"] == 0), None)
+    assert res["required_beam"] == first_ok
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, math.inf,
+                         want_grads=False)
+    d_ref = oracle.discarded_mass(ref["S"], ref["y_rel"], wl.input_lengths, wl.target_lengths, beams)
+    # float scores on both sides: compare where the oracle's delta is well above rounding
+    big = d_ref > 1e-6
+    np.testing.assert_allclose(res["delta"][big], d_ref[big], rtol=2e-3)
