@@ -22,4 +22,6 @@ from .prunedctc_oracle import (  # noqa: F401
     head_backward,
     head_backward_rows,
     fwd_bwd,
+    ctc_collapse,
+    greedy_decode,
 )

@@ -511,3 +511,49 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
     out["dW"] = dW
     out["db"] = db
     return out
+
+
+# ---------------------------------------------------------------------------------------
+# Greedy (best-path) emission head for recognition: framewise argmax over the full
+# vocabulary, then the CTC collapse (merge repeated ids, drop blanks; Sec. 3.1)
+# ---------------------------------------------------------------------------------------
+
+def ctc_collapse(ids: Sequence[int], blank: int) -> List[int]:
+    """The collapse map B of Sec. 3.1: merge consecutive repeats, then remove blanks."""
+    out: List[int] = []
+    prev = None
+    for c in ids:
+        c = int(c)
+        if c != prev and c != blank:
+            out.append(c)
+        prev = c
+    return out
+
+
+def greedy_decode(H, W, input_lengths, blank: int, bias=None, chunk: int = 4096) -> Dict[str, object]:
+    """Per frame the class with the largest logit H W^T + b (the first such class on ties),
+    computed one vocabulary chunk at a time in fp64; per utterance the collapsed sequence.
+    Returns ids [M], the top two logits per frame (for tie analysis) and tokens (a list of
+    lists)."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    b = _bias(bias, W.shape[0])
+    M = H.shape[0]
+    best = np.full(M, -np.inf)
+    second = np.full(M, -np.inf)
+    ids = np.zeros(M, np.int64)
+    for v0 in range(0, W.shape[0], chunk):
+        Z = H @ W[v0:v0 + chunk].T + b[v0:v0 + chunk]
+        j = np.argmax(Z, axis=1)
+        zmax = Z[np.arange(M), j]
+        Z2 = Z.copy()
+        Z2[np.arange(M), j] = -np.inf
+        z2 = Z2.max(axis=1) if Z.shape[1] > 1 else np.full(M, -np.inf)
+        better = zmax > best
+        second = np.where(better, np.maximum(best, z2), np.maximum(second, zmax))
+        ids = np.where(better, v0 + j, ids)
+        best = np.where(better, zmax, best)
+    toff = _offsets(input_lengths)
+    tokens = [ctc_collapse(ids[toff[n]:toff[n + 1]], blank) for n in range(len(input_lengths))]
+    return {"ids": ids, "best": best, "second": second, "tokens": tokens}
+

@@ -577,3 +577,47 @@ def test_discarded_mass_limits():
     full = oracle.ctc_utterance(S[:20], [1, 2, 3, 1], 0)
     pr = oracle.ctc_utterance(S[:20], [1, 2, 3, 1], 0, beam=2.0)
     assert np.abs(pr["gamma"] - full["gamma"]).max() <= d[1, 0] + 1e-12
+
+
+# ---------------------------------------------------------------------------------------
+# greedy emission head (framewise argmax, CTC collapse)
+# ---------------------------------------------------------------------------------------
+
+def test_ctc_collapse_examples():
+    """The collapse map of Sec. 3.1 on written-out strings (blank = '-')."""
+    enc = {"-": 0, "a": 1, "b": 2, "c": 3}
+
+    def col(sx):
+        return "".join("-abc"[i] for i in oracle.ctc_collapse([enc[ch] for ch in sx], 0))
+    assert col("aa-ab-") == "aab"
+    assert col("--a--") == "a"
+    assert col("abc") == "abc"
+    assert col("aaaa") == "a"
+    assert col("a-a") == "aa"
+    assert col("----") == ""
+    assert col("") == ""
+    # every alignment of a target collapses to it (brute-force enumeration)
+    for pi in brute.valid_alignments(4, 3, [1, 1], 0):
+        assert oracle.ctc_collapse(pi, 0) == [1, 1]
+
+
+def test_greedy_decode_against_torch_argmax():
+    """Framewise argmax equals torch.argmax of the dense logits (first index on ties),
+    across chunk widths, with a bias; ties are broken toward the smaller class id."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(12)
+    H = rng.standard_normal((37, 5))
+    W = rng.standard_normal((301, 5))
+    b = rng.standard_normal(301)
+    W[200] = W[17]
+    b[200] = b[17]                           # duplicate class: exact ties between 17 and 200
+    Z = torch.tensor(H) @ torch.tensor(W).T + torch.tensor(b)
+    want = torch.argmax(Z, dim=1).numpy()
+    for chunk in (7, 64, 4096):
+        got = oracle.greedy_decode(H, W, [20, 17], blank=3, bias=b, chunk=chunk)
+        np.testing.assert_array_equal(got["ids"], want)
+        assert np.all(got["ids"] != 200)
+        srt = np.sort(Z.numpy(), axis=1)
+        np.testing.assert_allclose(got["best"], srt[:, -1], atol=1e-12)
+        np.testing.assert_allclose(got["second"], srt[:, -2], atol=1e-12)
+    assert got["tokens"][0] == oracle.ctc_collapse(want[:20], 3)
