@@ -178,6 +178,23 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
                     float beam, double* loss_per_utt, int32_t* utt_status, float* G, float* g,
                     uint8_t* keep_mask, void* dp_scratch, void* stream);
 
+/* Greedy (best-path) recognition with the same head (the inference side of the method):
+ * per frame the class with the largest logit H W^T + b over the full vocabulary (the
+ * smallest class id on exact ties), computed on the vocabulary-tiled matrix-core products
+ * without storing the logits; then per utterance the CTC collapse (Sec. 3.1): repeated ids
+ * merged, blanks removed.
+ * H, D, W, bias, V, blank: as for pruned_ctc_fwd_bwd_ex.  input_lengths: HOST int32 [N].
+ * ids: device int32 [M] or NULL: the per-frame argmax.  tokens: device int32 [M]: utterance
+ * n's sequence occupies [o_n, o_n + token_lengths[n]) with o_n = sum of the earlier
+ * input_lengths; the rest is unspecified.  token_lengths: device int32 [N].
+ * workspace: pctc_greedy_workspace_size(N, M) bytes, 256-byte aligned.
+ * NaN logits give an unspecified id for their frame.  Synchronises the stream. */
+size_t pctc_greedy_workspace_size(int32_t N, int32_t M);
+int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const void* W,
+                           const float* bias, int32_t V, const int32_t* input_lengths, int32_t N,
+                           int32_t blank, int32_t* ids, int32_t* tokens, int32_t* token_lengths,
+                           void* workspace, size_t workspace_bytes, void* stream);
+
 /* Discarded posterior mass (App. B.3): for each beam b and utterance n,
  *   delta[b * N + n] = 1 - (sum over the alignments that the beam retains) /
  *                          (sum over all valid alignments),

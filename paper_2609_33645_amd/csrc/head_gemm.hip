@@ -239,6 +239,141 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, con
 }
 
 // ---------------------------------------------------------------------------------------
+// Greedy emission head (framewise argmax over V, smallest class id on ties) and the CTC
+// collapse of each utterance's argmax sequence (Sec. 3.1: merge repeats, drop blanks)
+// ---------------------------------------------------------------------------------------
+
+__device__ __forceinline__ void amax_merge_g(float& bv, int& bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+template <typename T>
+__global__ void __launch_bounds__(256)
+amax_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ W, const float* __restrict__ bias,
+                    int V, int P, int vper, float2* __restrict__ partials) {
+  constexpr int BK = Cfg<T>::BK;
+  using Shape = TileShape<T, kFwdBR, kFwdBC, BK>;
+  constexpr int FR = Shape::FR, FC = Shape::FC;
+  __shared__ __attribute__((aligned(16))) T lds[Shape::kLdsElems];
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  const int work = xcd_swizzle(blockIdx.x, gridDim.x);
+  const int mt = work % nMt;
+  const int p = work / nMt;
+  const int m0 = mt * kFwdBC;
+  const int vbeg = p * vper;
+  const int vend = min(V, vbeg + vper);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  Operand<T> A{W, D, V, D, nullptr, nullptr};
+  Operand<T> B{H, D, M, D, nullptr, nullptr};
+  float bv[FC];
+  int bi[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    bv[j] = -INFINITY;
+    bi[j] = 0x7fffffff;
+  }
+  f32x16 acc[FR][FC];
+  for (int v0 = vbeg; v0 < vend; v0 += kFwdBR) {
+    tile_gemm<T, kFwdBR, kFwdBC, BK, Lay::KMajor, Lay::KMajor>(A, B, v0, m0, 0, D, lds, acc);
+#pragma unroll
+    for (int j = 0; j < FC; ++j)
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int v = v0 + acc_row<kFwdBR>(wave, lane, i, r);
+          if (v >= vend) continue;
+          const float x = acc[i][j][r] + (bias ? bias[v] : 0.f);
+          if (x > bv[j]) {
+            bv[j] = x;
+            bi[j] = v;
+          }
+        }
+  }
+#pragma unroll
+  for (int j = 0; j < FC; ++j) amax_merge_g(bv[j], bi[j], swap_halves(bv[j]), __shfl_xor(bi[j], 32, 64));
+  __syncthreads();
+  float2* xch = reinterpret_cast<float2*>(lds);
+  const int rowhalf = wave >> 1, colhalf = wave & 1;
+  if (rowhalf == 1 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) xch[colhalf * (FC * 32) + j * 32 + lane] = make_float2(bv[j], __int_as_float(bi[j]));
+  }
+  __syncthreads();
+  if (rowhalf == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const float2 o = xch[colhalf * (FC * 32) + j * 32 + lane];
+      amax_merge_g(bv[j], bi[j], o.x, __float_as_int(o.y));
+      const int m = m0 + acc_col<kFwdBC>(wave, lane, j);
+      if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(bv[j], __int_as_float(bi[j]));
+    }
+  }
+}
+
+// ids[m]: the best of the partitions' (value, id) pairs, in partition order.
+__global__ void amax_finalize_kernel(const float2* __restrict__ partials, int M, int P, int32_t* __restrict__ ids) {
+  const int m = blockIdx.x * blockDim.x + threadIdx.x;
+  if (m >= M) return;
+  float bv = -INFINITY;
+  int bi = 0x7fffffff;
+  for (int p = 0; p < P; ++p) {
+    const float2 q = partials[static_cast<int64_t>(p) * M + m];
+    amax_merge_g(bv, bi, q.x, __float_as_int(q.y));
+  }
+  ids[m] = (bi == 0x7fffffff) ? 0 : bi;
+}
+
+// One thread per utterance walks its frames in order (lengths are at most a few thousand).
+__global__ void ctc_collapse_kernel(const int32_t* __restrict__ ids, const int32_t* __restrict__ toff, int N,
+                                    int blank, int32_t* __restrict__ tokens, int32_t* __restrict__ lengths) {
+  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+  if (n >= N) return;
+  const int t0 = toff[n], t1 = toff[n + 1];
+  int k = 0, prev = -1;
+  for (int m = t0; m < t1; ++m) {
+    const int c = ids[m];
+    if (c != prev && c != blank) tokens[t0 + k++] = c;
+    prev = c;
+  }
+  lengths[n] = k;
+}
+
+hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                         const int32_t* toff, int N, int blank, float2* partials, int32_t* ids, int32_t* tokens,
+                         int32_t* lengths, hipStream_t stream) {
+  if (M > 0) {
+    int Pfin;
+    if (dtype == 1) {
+      hipError_t e = launch_amax_partial_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W),
+                                              bias, V, partials, &Pfin, stream);
+      if (e != hipSuccess) return e;
+    } else {
+      const int P = lse_partitions(M, V);
+      const int vtiles = (V + kFwdBR - 1) / kFwdBR;
+      const int vper = ((vtiles + P - 1) / P) * kFwdBR;
+      Pfin = (V + vper - 1) / vper;
+      const int nMt = (M + kFwdBC - 1) / kFwdBC;
+      Prof pr("amax_partial", stream);
+      hipLaunchKernelGGL(amax_partial_kernel<float>, dim3(nMt * Pfin), dim3(256), 0, stream,
+                         static_cast<const float*>(H), M, D, static_cast<const float*>(W), bias, V, Pfin, vper,
+                         partials);
+    }
+    Prof pr("amax_finalize", stream);
+    hipLaunchKernelGGL(amax_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Pfin, ids);
+  }
+  if (N > 0) {
+    Prof pr("ctc_collapse", stream);
+    hipLaunchKernelGGL(ctc_collapse_kernel, dim3((N + 63) / 64), dim3(64), 0, stream, ids, toff, N, blank, tokens,
+                       lengths);
+  }
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
 // Selected-class log-probabilities S
 // ---------------------------------------------------------------------------------------
 

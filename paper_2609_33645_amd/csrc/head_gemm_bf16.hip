@@ -196,6 +196,94 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
   }
 }
 
+// ---------------------------------------------------------------------------------------
+// Greedy emission head: framewise argmax of H W^T (+ b) over a vocabulary partition, on the
+// same pipelined tiles as the normaliser.  Within a lane the rows are visited in
+// increasing order and only a strictly larger logit replaces the best, so ties keep the
+// smallest class id; the combines below keep that rule.
+// ---------------------------------------------------------------------------------------
+__device__ __forceinline__ void amax_merge(float& bv, int& bi, float ov, int oi) {
+  if (ov > bv || (ov == bv && oi < bi)) {
+    bv = ov;
+    bi = oi;
+  }
+}
+
+template <bool BIAS>
+__global__ void __launch_bounds__(256, 2)
+amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
+                  const float* __restrict__ bias, int V, int P, int vper, float2* __restrict__ partials) {
+  extern __shared__ float bsh[];  // BIAS: b over this partition's rows
+  using G = GFwd;
+  constexpr int FR = G::FR, FC = G::FC;
+  PCTC_STAGES(G)
+  const int nMt = (M + kFC - 1) / kFC;
+  int mt, p;
+  if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) return;
+  const int m0 = mt * kFC;
+  const int vbeg = p * vper;
+  const int vend = min(V, vbeg + vper);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
+  if (BIAS) {
+    for (int r = tid; r < ntiles * kFR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
+    __syncthreads();
+  }
+  const GOp A{W, D, vend, D, nullptr};
+  const GOp B{H, D, M, D, nullptr};
+  float bv[FC];
+  int bi[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    bv[j] = -INFINITY;
+    bi[j] = 0x7fffffff;
+  }
+  f32x16 acc[FR][FC];
+  G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, [&](int it, const f32x16 (&a)[FR][FC]) {
+    const int v0 = vbeg + it * kFR;
+    const float* bt = bsh + it * kFR;
+#pragma unroll
+    for (int j = 0; j < FC; ++j)
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int rl = G::row_of(wave, lane, i, r);
+          float x = a[i][j][r];
+          if (BIAS) x += bt[rl];
+          if (v0 + rl < vend && x > bv[j]) {
+            bv[j] = x;
+            bi[j] = v0 + rl;
+          }
+        }
+  });
+  // lane halves hold the other half of each 32-row block, then the row halves of the tile
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const float ov = swap_halves(bv[j]);
+    const int oi = __shfl_xor(bi[j], 32, 64);
+    amax_merge(bv[j], bi[j], ov, oi);
+  }
+  __syncthreads();
+  float2* xch = reinterpret_cast<float2*>(st0_);
+  const int rowhalf = wave / 2, colq = wave % 2;
+  if (rowhalf == 1 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j)
+      xch[colq * (FC * 32) + j * 32 + lane] = make_float2(bv[j], __int_as_float(bi[j]));
+  }
+  __syncthreads();
+  if (rowhalf == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const float2 o = xch[colq * (FC * 32) + j * 32 + lane];
+      amax_merge(bv[j], bi[j], o.x, __float_as_int(o.y));
+      const int m = m0 + G::col_of(wave, lane, j);
+      if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(bv[j], __int_as_float(bi[j]));
+    }
+  }
+}
+
 __global__ void __launch_bounds__(256, 2)
 gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
               const float* __restrict__ bias, const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev,
@@ -486,6 +574,24 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
                        static_cast<size_t>(vper) * sizeof(float), stream, H, M, D, W, bias, V, Peff, vper, partials);
   else
     hipLaunchKernelGGL(lse_partial_bf16<false>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M,
+                       D, W, bias, V, Peff, vper, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
+                                    float2* partials, int* P_out, hipStream_t stream) {
+  const int P = lse_partitions_bf16(M, V);
+  const int vtiles = (V + kFR - 1) / kFR;
+  const int vper = ((vtiles + P - 1) / P) * kFR;
+  const int Peff = (V + vper - 1) / vper;
+  const int nMt = (M + kFC - 1) / kFC;
+  *P_out = Peff;
+  Prof pr("amax_partial", stream);
+  if (bias)
+    hipLaunchKernelGGL(amax_partial_bf16<true>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads),
+                       static_cast<size_t>(vper) * sizeof(float), stream, H, M, D, W, bias, V, Peff, vper, partials);
+  else
+    hipLaunchKernelGGL(amax_partial_bf16<false>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M,
                        D, W, bias, V, Peff, vper, partials);
   return hipGetLastError();
 }

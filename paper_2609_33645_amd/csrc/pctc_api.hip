@@ -355,6 +355,54 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
   return PCTC_OK;
 }
 
+// Greedy decode workspace: argmax partials, frame offsets, and the ids when not returned.
+static size_t greedy_layout(int32_t N, int32_t M, size_t* o_toff, size_t* o_ids) {
+  const size_t part = lse_partial_bytes(M > 0 ? M : 1);
+  *o_toff = part;
+  *o_ids = part + align_up(static_cast<size_t>(N + 1) * sizeof(int32_t), 256);
+  return *o_ids + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(int32_t), 256);
+}
+
+size_t pctc_greedy_workspace_size(int32_t N, int32_t M) {
+  if (N < 0 || M < 0) return 0;
+  size_t a, b;
+  return greedy_layout(N, M, &a, &b);
+}
+
+int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
+                           const int32_t* input_lengths, int32_t N, int32_t blank, int32_t* ids, int32_t* tokens,
+                           int32_t* token_lengths, void* workspace, size_t workspace_bytes, void* stream_ptr) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || N < 0 || D <= 0 || D % 8 || V <= 1 || V > PCTC_MAX_VOCAB ||
+      blank < 0 || blank >= V || !W)
+    return PCTC_EINVAL;
+  if (N > 0 && !input_lengths) return PCTC_EINVAL;
+  int64_t M64 = 0;
+  for (int n = 0; n < N; ++n) {
+    if (input_lengths[n] < 1) return PCTC_ELENGTH;
+    M64 += input_lengths[n];
+  }
+  if (M64 > INT32_MAX) return PCTC_EINVAL;
+  const int M = static_cast<int>(M64);
+  if (M > 0 && (!H || !tokens || !token_lengths)) return PCTC_EINVAL;
+  size_t o_toff, o_ids;
+  const size_t need = greedy_layout(N, M, &o_toff, &o_ids);
+  if (!workspace || workspace_bytes < need) return PCTC_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
+  if (N == 0) return PCTC_OK;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  char* ws = static_cast<char*>(workspace);
+  std::vector<int32_t> toff(N + 1, 0);
+  for (int n = 0; n < N; ++n) toff[n + 1] = toff[n] + input_lengths[n];
+  int32_t* dtoff = reinterpret_cast<int32_t*>(ws + o_toff);
+  PCTC_HIP(hipMemcpyAsync(dtoff, toff.data(), (N + 1) * sizeof(int32_t), hipMemcpyHostToDevice, stream));
+  int32_t* idv = ids ? ids : reinterpret_cast<int32_t*>(ws + o_ids);
+  PCTC_HIP(launch_greedy(dtype == PCTC_BF16 ? 1 : 0, H, M, D, W, bias, V, dtoff, N, blank,
+                         reinterpret_cast<float2*>(ws), idv, tokens, token_lengths, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));  // the host offsets must outlive the copy
+  prof_flush();
+  return PCTC_OK;
+}
+
 size_t pctc_discarded_mass_scratch_bytes(int32_t N, const int32_t* input_lengths, const int32_t* target_lengths) {
   if (N < 0 || (N > 0 && (!input_lengths || !target_lengths))) return 0;
   for (int n = 0; n < N; ++n)

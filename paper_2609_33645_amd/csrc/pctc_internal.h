@@ -41,6 +41,14 @@ hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W
                            const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream);
 
+// ---- greedy emission head -----------------------------------------------------------------
+// partials: lse_partial_bytes(M); ids [M]; tokens [M] (utterance n at toff[n]); lengths [N].
+hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                         const int32_t* toff, int N, int blank, float2* partials, int32_t* ids, int32_t* tokens,
+                         int32_t* lengths, hipStream_t stream);
+hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
+                                    float2* partials, int* P_out, hipStream_t stream);
+
 // ---- backward ---------------------------------------------------------------------------
 struct BwdPlan {
   int chunk;       // vocabulary columns per step

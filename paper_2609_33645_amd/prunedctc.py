@@ -68,6 +68,11 @@ def lib() -> ctypes.CDLL:
     L.pctc_dp_scratch_bytes.restype = c_sz
     L.pctc_ctc_dp.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, c_f, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_ctc_dp.restype = c_i32
+    L.pctc_greedy_workspace_size.argtypes = [c_i32, c_i32]
+    L.pctc_greedy_workspace_size.restype = c_sz
+    L.pctc_greedy_decode.argtypes = [c_i32, c_p, c_i32, c_p, c_p, c_i32, i32p, c_i32, c_i32, c_p, c_p, c_p, c_p, c_sz,
+                                     c_p]
+    L.pctc_greedy_decode.restype = c_i32
     L.pctc_discarded_mass_scratch_bytes.argtypes = [c_i32, i32p, i32p]
     L.pctc_discarded_mass_scratch_bytes.restype = c_sz
     L.pctc_discarded_mass.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, ctypes.POINTER(ctypes.c_float), c_i32,
@@ -298,6 +303,38 @@ def ctc_dp(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_lengths, 
     if mask is not None:
         out["mask"] = mask[:lattice]
     return out
+
+
+def greedy_decode(H: torch.Tensor, W: torch.Tensor, input_lengths, blank: int = 0,
+                  bias: Optional[torch.Tensor] = None, stream=None) -> Dict[str, object]:
+    """Framewise full-vocabulary argmax ids [M] and the collapsed token sequence of each
+    utterance (a list of lists), plus the raw device buffers."""
+    L = lib()
+    dt = _dtype_code(H)
+    H = H.contiguous()
+    W = W.contiguous()
+    T = _host_i32(input_lengths)
+    N = int(T.size)
+    M, D = int(H.shape[0]), int(H.shape[1])
+    V = int(W.shape[0])
+    if int(T.sum()) != M:
+        raise PrunedCTCError(-1, "sum of input lengths differs from the rows of H")
+    dev = H.device
+    if bias is not None:
+        bias = bias.to(device=dev, dtype=torch.float32).contiguous()
+    ids = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
+    tokens = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
+    lengths = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
+    ws = _workspace(int(L.pctc_greedy_workspace_size(N, M)), dev)
+    code = L.pctc_greedy_decode(dt, _ptr(H), D, _ptr(W), _ptr(bias), V, _i32p(T), N, int(blank), _ptr(ids),
+                                _ptr(tokens), _ptr(lengths), ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()),
+                                _stream(stream))
+    _check(code, "pctc_greedy_decode")
+    off = np.concatenate([[0], np.cumsum(T)]).astype(np.int64)
+    tk = tokens.cpu().numpy()
+    ln = lengths.cpu().numpy()[:N]
+    seqs = [tk[off[n]:off[n] + ln[n]].tolist() for n in range(N)]
+    return {"ids": ids[:M], "tokens": seqs, "token_lengths": lengths[:N]}
 
 
 def discarded_mass(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_lengths, beams: Sequence[float],

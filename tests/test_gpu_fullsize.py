@@ -221,3 +221,24 @@ def test_full_size_bias_weights_db():
     assert abs(db_s[bi] - rows["db"][bi]) <= 1e-3 * abs(rows["db"][bi])
     del out, H, W, y
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("name", ["zipformer_m", "qwen3_8b"])
+def test_full_size_greedy(name):
+    """Greedy emission head at full size; the oracle recomputes a sample of frames over the
+    full vocabulary."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    from tests.test_gpu_parity import _check_greedy
+    wl = workloads.NAMED[name](2)
+    say(f"full-size greedy {name}: M={wl.M} D={wl.D} V={wl.V}")
+    H, W, _ = to_dev(wl)
+    got = prunedctc.greedy_decode(H, W, wl.input_lengths, wl.blank)
+    rng = np.random.default_rng(4)
+    frames = np.sort(rng.choice(wl.M, size=64, replace=False))
+    H64, W64 = wl.H.astype(np.float64), wl.W.astype(np.float64)
+    ref = oracle.greedy_decode(H64[frames], W64, [frames.size], wl.blank)
+    _check_greedy(wl, H64, W64, np.zeros(wl.V), got, ref, frames=frames)
+    del H, W
+    torch.cuda.empty_cache()

@@ -370,3 +370,53 @@ def test_beam_sweep_tool():
     # float scores on both sides: compare where the oracle's delta is well above rounding
     big = d_ref > 1e-6
     np.testing.assert_allclose(res["delta"][big], d_ref[big], rtol=2e-3)
+
+
+# ---------------------------------------------------------------------------------------
+# greedy emission head
+# ---------------------------------------------------------------------------------------
+
+def _check_greedy(wl, H64, W64, b64, got, ref, frames=None, eps=1e-3):
+    """ids agree wherever the oracle's best logit leads the runner-up by more than eps; at
+    nearer ties the GPU's id must score within eps of the best.  Token sequences agree for
+    utterances without near ties and are always the collapse of the GPU's own ids."""
+    ids = got["ids"].cpu().numpy()
+    if frames is not None:
+        ids = ids[frames]
+    sure = (ref["best"] - ref["second"]) > eps
+    np.testing.assert_array_equal(ids[sure], ref["ids"][sure])
+    rows = np.nonzero(~sure)[0]
+    fr = rows if frames is None else frames[rows]
+    if rows.size:
+        z = np.einsum("md,md->m", H64[fr], W64[ids[rows]]) + b64[ids[rows]]
+        assert np.all(z >= ref["best"][rows] - eps)
+    say(f"  greedy: {int(sure.sum())} frames decided, {rows.size} near ties")
+    return ids, sure
+
+
+@pytest.mark.parametrize("seed,dtype,blank,with_bias", [(0, "f32", 0, False), (1, "bf16", 0, True),
+                                                        (2, "bf16", 2999, False), (3, "f32", 5, True)])
+def test_greedy_decode(seed, dtype, blank, with_bias):
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(90 + seed, N=6, T_range=(1, 150), D=128, V=3000, dtype=dtype, blank=blank, w_std=0.5)
+    H, W, _ = to_dev(wl)
+    rng = np.random.default_rng(seed)
+    b = rng.standard_normal(wl.V).astype(np.float32) if with_bias else np.zeros(wl.V, np.float32)
+    # a duplicated class row makes exact ties, broken toward the smaller id
+    Wn = wl.W.copy()
+    Wn[2500] = Wn[33]
+    b[2500] = b[33]
+    W = torch.from_numpy(Wn).cuda().to(H.dtype)
+    say(f"greedy seed={seed} {dtype} blank={blank} bias={with_bias} M={wl.M} T={wl.input_lengths.tolist()}")
+    got = prunedctc.greedy_decode(H, W, wl.input_lengths, blank, bias=torch.from_numpy(b).cuda() if with_bias else None)
+    H64, W64, b64 = wl.H.astype(np.float64), Wn.astype(np.float64), b.astype(np.float64)
+    ref = oracle.greedy_decode(H64, W64, wl.input_lengths, blank, bias=b64)
+    ids, sure = _check_greedy(wl, H64, W64, b64, got, ref)
+    assert not np.any(ids == 2500)
+    off = np.concatenate([[0], np.cumsum(wl.input_lengths)])
+    for n in range(wl.N):
+        own = oracle.ctc_collapse(ids[off[n]:off[n + 1]], blank)
+        assert got["tokens"][n] == own
+        if sure[off[n]:off[n + 1]].all():
+            assert got["tokens"][n] == ref["tokens"][n]
