@@ -21,6 +21,8 @@ from .prunedctc_oracle import (  # noqa: F401
     discarded_mass,
     head_backward,
     head_backward_rows,
+    grouped_logprobs,
+    grouped_gradient,
     fwd_bwd,
     ctc_collapse,
     greedy_decode,

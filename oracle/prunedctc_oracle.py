@@ -514,6 +514,48 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
 
 
 # ---------------------------------------------------------------------------------------
+# Grouped logits for unpruned reduced CTC through a stock CTC (Eq. grouped; Prop. 1;
+# Eq. offsupport)
+# ---------------------------------------------------------------------------------------
+
+def grouped_logprobs(H, W, u_ids, bias=None, chunk: int = 4096) -> Dict[str, np.ndarray]:
+    """log softmax of R [M, K+1]: R[:, j] = Z[:, U[j]] and R[:, K] = log sum over the
+    complement O of exp Z (the "other class"); the normaliser of R equals lambda, so the
+    first K columns are the selected log-probabilities S and the last is log P_O.  The
+    complement column is dropped when O is empty.  Also returns lambda."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    V = W.shape[0]
+    b = _bias(bias, V)
+    u = np.asarray(u_ids, np.int64)
+    lam = log_normalizer(H, W, chunk, bias=b)
+    S = selected_logprobs(H, W, u, lam, bias=b)
+    comp = np.setdiff1d(np.arange(V), u)
+    if comp.size == 0:
+        return {"logp": S, "lam": lam}
+    bo = b.copy()
+    bo[u] = -np.inf                       # the complement's log-sum-exp
+    lam_o = log_normalizer(H, W, chunk, bias=bo)
+    return {"logp": np.concatenate([S, (lam_o - lam)[:, None]], axis=1), "lam": lam}
+
+
+def grouped_gradient(logp, dlogp) -> Dict[str, np.ndarray]:
+    """From a gradient w.r.t. log softmax(R) to G = dL/dS and g (Algorithm 1's inputs to the
+    recomputed backward).  With c = dlogp[:, K] / P_O and sigma = sum_j dlogp[:, j]:
+    dL/dZ_v = dlogp_j - p_v sigma for v = U[j], and p_v (c - sigma) for v in O (Eq.
+    offsupport), i.e. scatter_U(G) - g p with G_j = dlogp_j - c p_{U[j]} and g = sigma - c."""
+    logp = np.asarray(logp, np.float64)
+    dlogp = np.asarray(dlogp, np.float64)
+    sigma = dlogp.sum(axis=1)
+    K = logp.shape[1] - 1
+    with np.errstate(divide="ignore", invalid="ignore"):
+        po = np.exp(logp[:, K])
+        c = np.where(po > 0, dlogp[:, K] / po, 0.0)
+    G = dlogp[:, :K] - c[:, None] * np.exp(logp[:, :K])
+    return {"G": G, "g": sigma - c}
+
+
+# ---------------------------------------------------------------------------------------
 # Greedy (best-path) emission head for recognition: framewise argmax over the full
 # vocabulary, then the CTC collapse (merge repeated ids, drop blanks; Sec. 3.1)
 # ---------------------------------------------------------------------------------------

@@ -621,3 +621,74 @@ def test_greedy_decode_against_torch_argmax():
         np.testing.assert_allclose(got["best"], srt[:, -1], atol=1e-12)
         np.testing.assert_allclose(got["second"], srt[:, -2], atol=1e-12)
     assert got["tokens"][0] == oracle.ctc_collapse(want[:20], 3)
+
+
+# ---------------------------------------------------------------------------------------
+# grouped-logit export for a stock CTC (Eq. grouped, Prop. 1, Eq. offsupport)
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("seed,leaf_grad", [(0, True), (1, False), (2, True)])
+def test_grouped_export_through_torch_ctc(seed, leaf_grad):
+    """The exported log softmax(R) matches torch's log_softmax of R built by autograd; torch's
+    CTC on it gives the full loss; the gradient w.r.t. the exported log-probabilities, taken
+    back through grouped_gradient and the recomputed backward, gives the autograd dH, dW and db.
+    leaf_grad: the exported tensor is a leaf (torch's CTC then returns p - gamma, its
+    convention) or the output of torch's log_softmax (true gradient -gamma)."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(50 + seed)
+    N, V, D = 3, 40, 6
+    T = np.array([12, 9, 15])
+    U = np.array([3, 4, 5])
+    targets = rng.integers(1, 12, size=int(U.sum()))
+    H = rng.standard_normal((int(T.sum()), D))
+    W = rng.standard_normal((V, D))
+    b = rng.standard_normal(V)
+    full = oracle.fwd_bwd(H, W, targets, T, U, blank=0, bias=b)
+    u = oracle.union_remap(targets, U, 0, V)
+    ex = oracle.grouped_logprobs(H, W, u["u_ids"], bias=b, chunk=13)
+    Ht = torch.tensor(H, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    Z = Ht @ Wt.T + bt
+    comp = [v for v in range(V) if u["remap"][v] < 0]
+    R = torch.cat([Z[:, torch.tensor(u["u_ids"])], torch.logsumexp(Z[:, comp], dim=1, keepdim=True)], 1)
+    np.testing.assert_allclose(ex["logp"], torch.log_softmax(R, 1).detach().numpy(), atol=1e-12)
+    np.testing.assert_allclose(ex["lam"], full["lam"], atol=1e-12)
+    off = np.concatenate([[0], np.cumsum(T)])
+    Tm = int(T.max())
+    lp = torch.tensor(ex["logp"], requires_grad=True) if leaf_grad else torch.log_softmax(R, 1)
+    if not leaf_grad:
+        lp.retain_grad()
+    pad = torch.stack([torch.nn.functional.pad(lp[off[n]:off[n + 1]], (0, 0, 0, Tm - int(T[n]))) for n in range(N)], 1)
+    loss = torch.nn.functional.ctc_loss(pad, torch.tensor(u["y_rel"]), torch.tensor(T), torch.tensor(U), blank=0,
+                                        reduction="sum")
+    assert abs(float(loss) - full["loss"]) < 1e-10 * abs(full["loss"])
+    loss.backward()
+    gg = oracle.grouped_gradient(ex["logp"], lp.grad.numpy())
+    back = oracle.head_backward(H, W, ex["lam"], gg["G"], gg["g"], u["u_ids"], bias=b)
+    np.testing.assert_allclose(back["dH"], full["dH"], atol=1e-10)
+    np.testing.assert_allclose(back["dW"], full["dW"], atol=1e-10)
+    np.testing.assert_allclose(back["db"], full["db"], atol=1e-10)
+    if not leaf_grad:
+        np.testing.assert_allclose(back["dH"], Ht.grad.numpy(), atol=1e-10)
+        np.testing.assert_allclose(back["db"], bt.grad.numpy(), atol=1e-10)
+
+
+def test_grouped_export_invariants():
+    """Rows of exp(log softmax R) sum to one; the complement column is log(1 - sum_U p);
+    a union covering the whole vocabulary leaves no complement column and G = dlogp, g = sigma."""
+    rng = np.random.default_rng(77)
+    M, V, D = 20, 9, 4
+    H = rng.standard_normal((M, D))
+    W = rng.standard_normal((V, D))
+    u_ids = np.array([0, 2, 5, 7])
+    ex = oracle.grouped_logprobs(H, W, u_ids, chunk=4)
+    np.testing.assert_allclose(np.exp(ex["logp"]).sum(1), 1.0, atol=1e-13)
+    np.testing.assert_allclose(ex["logp"][:, -1], np.log1p(-np.exp(ex["logp"][:, :-1]).sum(1)), atol=1e-12)
+    full = oracle.grouped_logprobs(H, W, np.arange(V))
+    assert full["logp"].shape == (M, V)
+    dl = rng.standard_normal((M, V))
+    gg = oracle.grouped_gradient(np.concatenate([full["logp"], np.full((M, 1), -np.inf)], 1),
+                                 np.concatenate([dl, np.zeros((M, 1))], 1))
+    np.testing.assert_allclose(gg["G"], dl, atol=0)
+    np.testing.assert_allclose(gg["g"], dl.sum(1), atol=1e-13)
