@@ -221,13 +221,47 @@ int32_t pctc_discarded_mass(const float* S, int32_t ldS, int32_t K_max, const in
  * at least the union size K). */
 size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ldG, int32_t chunk);
 /* Vocabulary columns per backward step that a call with this chunk argument uses (0 picks
- * the default: about 256 MiB of recomputed gradient, rounded to whole launch waves).
+ * the default: about 512 MiB of recomputed gradient, rounded to whole launch waves).
  * Returns 0 for invalid arguments. */
 int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
                       int32_t V, const double* lam, const float* G, int32_t ldG, const float* g,
                       const int32_t* remap, int32_t chunk, float* dH, float* dW, void* bwd_scratch,
                       void* stream);
+
+/* Grouped logits for a stock CTC (Sec. 3.2, Eq. grouped; Prop. 1; Eq. offsupport).  The
+ * selected classes u_ids (device int32 [K], distinct, in [0, V); e.g. the union of
+ * pctc_union_remap with its size read back) keep their own logits and every other class is
+ * merged into one "other" class whose logit is the log-sum-exp of the remaining logits.  The
+ * log softmax of these K + 1 grouped logits is exported; an unmodified CTC loss over K + 1
+ * classes (blank at the blank's position in u_ids, targets relabelled by their position) on
+ * it gives the full-vocabulary CTC loss exactly, and its gradient maps back to dH, dW, db.
+ *
+ * pctc_grouped_logprobs: logp device float [M, K + 1] row-major:
+ *   logp[m, j] = Z[m, u_ids[j]] - lam[m] (j < K),
+ *   logp[m, K] = log sum over the classes not in u_ids of exp Z[m, v] - lam[m]
+ *   (-inf when u_ids covers the vocabulary), Z = H W^T + bias (bias device float [V] or NULL);
+ * lam device double [M]: the full log normaliser, needed by the backward.  One pass over
+ * the vocabulary.
+ * pctc_grouped_backward: dlogp device float [M, K + 1]: dL/dlogp as a CTC implementation
+ * returns it (either the true gradient or one with a multiple of exp(logp) added per row:
+ * the result is the same).  logp and lam as the forward returned them.  dH [M, D], dW [V, D],
+ * db [V] device float, each may be NULL; they are overwritten.  chunk: as for
+ * pctc_head_bwd (0 = default).
+ * workspace: pctc_grouped_workspace_size(dtype, M, D, V, K, chunk) bytes, 256-byte aligned
+ * (the forward needs no more than the size for chunk 0).  Both calls check u_ids first and
+ * return PCTC_ELABEL for an id outside [0, V) or given twice; both synchronise the stream. */
+size_t pctc_grouped_workspace_size(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t K,
+                                   int32_t chunk);
+int32_t pctc_grouped_logprobs(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
+                              const float* bias, int32_t V, const int32_t* u_ids, int32_t K,
+                              float* logp, double* lam, void* workspace, size_t workspace_bytes,
+                              void* stream);
+int32_t pctc_grouped_backward(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
+                              const float* bias, int32_t V, const int32_t* u_ids, int32_t K,
+                              const float* logp, const double* lam, const float* dlogp,
+                              int32_t chunk, float* dH, float* dW, float* db, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /* ----------------------------------------------------------------------------------
  * Kernel timing for benchmarks.  When enabled, every kernel the library launches is

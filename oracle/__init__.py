@@ -23,6 +23,7 @@ from .prunedctc_oracle import (  # noqa: F401
     head_backward_rows,
     grouped_logprobs,
     grouped_gradient,
+    grouped_backward,
     fwd_bwd,
     ctc_collapse,
     greedy_decode,

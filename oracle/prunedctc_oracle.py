@@ -555,6 +555,48 @@ def grouped_gradient(logp, dlogp) -> Dict[str, np.ndarray]:
     return {"G": G, "g": sigma - c}
 
 
+def grouped_backward(H, W, lam, logp, dlogp, u_ids, bias=None, chunk: int = 4096) -> Dict[str, np.ndarray]:
+    """dH, dW, db from dL/d(log softmax R) (Eq. offsupport, written out): with p_v =
+    exp(Z_v - lambda), sigma the row sum of dlogp and P_O = exp(logp[:, K]),
+    dL/dZ_v = dlogp_j - sigma p_v for the selected class v = U[j] and
+    dL/dZ_v = p_v (dlogp_K / P_O - sigma) for v in the complement; then dH = dZ W,
+    dW = dZ^T H, db = dZ^T 1.  logp, dlogp: [M, K + 1], or [M, K] when U is the whole
+    vocabulary."""
+    H = np.asarray(H, np.float64)
+    W = np.asarray(W, np.float64)
+    lam = np.asarray(lam, np.float64)
+    logp = np.asarray(logp, np.float64)
+    dlogp = np.asarray(dlogp, np.float64)
+    M, D = H.shape
+    V = W.shape[0]
+    b = _bias(bias, V)
+    u = np.asarray(u_ids, np.int64)
+    K = u.size
+    sigma = dlogp.sum(axis=1)
+    c = np.zeros(M)
+    if logp.shape[1] == K + 1:
+        po = np.exp(logp[:, K])
+        nz = po > 0
+        c[nz] = dlogp[nz, K] / po[nz]
+    col = np.full(V, -1, np.int64)
+    col[u] = np.arange(K)
+    dH = np.zeros((M, D))
+    dW = np.zeros((V, D))
+    db = np.zeros(V)
+    for v0 in range(0, V, chunk):
+        v1 = min(V, v0 + chunk)
+        p = np.exp(H @ W[v0:v1].T + b[v0:v1] - lam[:, None])
+        dZ = p * (c - sigma)[:, None]
+        for v in range(v0, v1):
+            j = col[v]
+            if j >= 0:
+                dZ[:, v - v0] = dlogp[:, j] - sigma * p[:, v - v0]
+        dH += dZ @ W[v0:v1]
+        dW[v0:v1] = dZ.T @ H
+        db[v0:v1] = dZ.sum(axis=0)
+    return {"dH": dH, "dW": dW, "db": db}
+
+
 # ---------------------------------------------------------------------------------------
 # Greedy (best-path) emission head for recognition: framewise argmax over the full
 # vocabulary, then the CTC collapse (merge repeated ids, drop blanks; Sec. 3.1)

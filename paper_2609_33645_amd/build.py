@@ -21,7 +21,7 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libprunedctc.so")
 ROOT = os.path.dirname(HERE)
 
-SOURCES = ["pctc_api.hip", "union_remap.hip", "head_gemm.hip", "head_gemm_bf16.hip", "ctc_dp.hip"]
+SOURCES = ["pctc_api.hip", "union_remap.hip", "head_gemm.hip", "head_gemm_bf16.hip", "ctc_dp.hip", "grouped_head.hip"]
 
 
 def hipcc() -> str:

@@ -103,7 +103,8 @@ lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ 
         for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[i][j][r]);
       tmax = fmaxf(tmax, swap_halves(tmax));
       const float nmax = fmaxf(run_max[j], tmax);
-      const float ms = nmax * kLog2e;
+      // a column with no finite logit yet (rows masked by a -inf bias) adds nothing
+      const float ms = (nmax == -INFINITY) ? 0.f : nmax * kLog2e;
       float s = 0.f;
 #pragma unroll
       for (int i = 0; i < FR; ++i)

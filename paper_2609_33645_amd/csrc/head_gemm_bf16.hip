@@ -103,7 +103,8 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], con
       }
     tmax = fmaxf(tmax, swap_halves(tmax));
     const float nmax = fmaxf(run_max[j], tmax);
-    const float ms = nmax * kLog2e;
+    // a column with no finite logit yet (rows masked by a -inf bias) adds nothing
+    const float ms = (nmax == -INFINITY) ? 0.f : nmax * kLog2e;
     float s = 0.f;
 #pragma unroll
     for (int i = 0; i < FR; ++i)

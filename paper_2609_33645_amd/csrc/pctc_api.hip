@@ -491,6 +491,117 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
   return PCTC_OK;
 }
 
+// Grouped logits: one workspace serves both directions.
+//   [small 256 B][remap V][ forward: partials | lse_O | lam2 | zero | complement bias ]
+//                         [ backward: G M x K | g | lam2 | recomputed-backward scratch ]
+struct GroupedLayout {
+  BwdPlan plan;
+  size_t o_remap, o_part, o_lamo, o_lam2f, o_zero, o_bo, o_G, o_g, o_lam2b, o_bwd, total;
+};
+static GroupedLayout grouped_layout(int dt, int M, int D, int V, int K, int chunk) {
+  GroupedLayout L;
+  const size_t m8 = align_up(static_cast<size_t>(M > 0 ? M : 1) * 8, 256);
+  L.plan = plan_bwd(dt, M, D, chunk);
+  L.o_remap = 256;
+  L.o_part = L.o_remap + align_up(static_cast<size_t>(V) * 4, 256);
+  L.o_lamo = L.o_part + lse_partial_bytes(M);
+  L.o_lam2f = L.o_lamo + m8;
+  L.o_zero = L.o_lam2f + m8;
+  L.o_bo = L.o_zero + m8;
+  const size_t fwd_end = L.o_bo + align_up(static_cast<size_t>(V) * 4, 256);
+  L.o_G = L.o_part;
+  L.o_g = L.o_G + align_up(static_cast<size_t>(M) * K * 4, 256);
+  L.o_lam2b = L.o_g + align_up(static_cast<size_t>(M > 0 ? M : 1) * 4, 256);
+  L.o_bwd = L.o_lam2b + m8;
+  const size_t bwd_end = L.o_bwd + L.plan.total;
+  L.total = fwd_end > bwd_end ? fwd_end : bwd_end;
+  return L;
+}
+
+static bool grouped_args_ok(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t K, int32_t chunk) {
+  return (dtype == PCTC_F32 || dtype == PCTC_BF16) && M >= 0 && D > 0 && D % 8 == 0 && V > 1 && K >= 1 && K <= V &&
+         chunk >= 0 && (chunk == 0 || chunk % 256 == 0) && static_cast<int64_t>(M) * (K + 1) <= INT32_MAX;
+}
+
+// Builds remap from u_ids and reads the error flag back (synchronous).
+static int32_t grouped_index(const int32_t* u_ids, int32_t K, int32_t V, char* ws, hipStream_t stream) {
+  int32_t* small = reinterpret_cast<int32_t*>(ws);
+  int32_t* remap = reinterpret_cast<int32_t*>(ws + 256);
+  PCTC_HIP(launch_grouped_index(u_ids, K, V, remap, small, stream));
+  int32_t herr = 0;
+  PCTC_HIP(hipMemcpyAsync(&herr, small + 1, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  return herr ? PCTC_ELABEL : PCTC_OK;
+}
+
+size_t pctc_grouped_workspace_size(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t K, int32_t chunk) {
+  if (!grouped_args_ok(dtype, M, D, V, K, chunk)) return 0;
+  return grouped_layout(dtype == PCTC_BF16 ? 1 : 0, M, D, V, K, chunk).total;
+}
+
+int32_t pctc_grouped_logprobs(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, const float* bias,
+                              int32_t V, const int32_t* u_ids, int32_t K, float* logp, double* lam, void* workspace,
+                              size_t workspace_bytes, void* stream_ptr) {
+  if (!grouped_args_ok(dtype, M, D, V, K, 0) || !W || !u_ids) return PCTC_EINVAL;
+  if (M > 0 && (!H || !logp || !lam)) return PCTC_EINVAL;
+  const int dt = (dtype == PCTC_BF16) ? 1 : 0;
+  const GroupedLayout L = grouped_layout(dt, M, D, V, K, 0);
+  if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  char* ws = static_cast<char*>(workspace);
+  const int32_t st = grouped_index(u_ids, K, V, ws, stream);
+  if (st != PCTC_OK || M == 0) return st;
+  const int32_t* Kdev = reinterpret_cast<const int32_t*>(ws);
+  const int32_t* remap = reinterpret_cast<const int32_t*>(ws + L.o_remap);
+  double* lse_o = reinterpret_cast<double*>(ws + L.o_lamo);
+  double* zero = reinterpret_cast<double*>(ws + L.o_zero);
+  float* bo = reinterpret_cast<float*>(ws + L.o_bo);
+  if (K < V) {
+    // the complement's log-sum-exp: the normaliser pass with the selected rows masked out
+    PCTC_HIP(launch_grouped_comp_bias(bias, remap, V, bo, stream));
+    PCTC_HIP(launch_lse(dt, H, M, D, W, bo, V, reinterpret_cast<float2*>(ws + L.o_part), lse_o,
+                        reinterpret_cast<float2*>(ws + L.o_lam2f), stream));
+  } else {
+    PCTC_HIP(launch_fill_d(lse_o, M, -INFINITY, stream));
+  }
+  // raw selected logits into the first K columns of each exported row
+  PCTC_HIP(launch_fill_d(zero, M, 0.0, stream));
+  PCTC_HIP(launch_gather_s(dt, H, M, D, W, bias, u_ids, Kdev, K, zero, logp, K + 1, stream));
+  PCTC_HIP(launch_grouped_finalize(logp, K, M, lse_o, lam, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
+int32_t pctc_grouped_backward(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, const float* bias,
+                              int32_t V, const int32_t* u_ids, int32_t K, const float* logp, const double* lam,
+                              const float* dlogp, int32_t chunk, float* dH, float* dW, float* db, void* workspace,
+                              size_t workspace_bytes, void* stream_ptr) {
+  if (!grouped_args_ok(dtype, M, D, V, K, chunk) || !W || !u_ids) return PCTC_EINVAL;
+  if (M > 0 && (!H || !logp || !lam || !dlogp)) return PCTC_EINVAL;
+  const int dt = (dtype == PCTC_BF16) ? 1 : 0;
+  const GroupedLayout L = grouped_layout(dt, M, D, V, K, chunk);
+  if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
+  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+  char* ws = static_cast<char*>(workspace);
+  const int32_t st = grouped_index(u_ids, K, V, ws, stream);
+  if (st != PCTC_OK) return st;
+  if (!dH && !dW && !db) return PCTC_OK;
+  const int32_t* remap = reinterpret_cast<const int32_t*>(ws + L.o_remap);
+  float* G = reinterpret_cast<float*>(ws + L.o_G);
+  float* g = reinterpret_cast<float*>(ws + L.o_g);
+  float2* lam2 = reinterpret_cast<float2*>(ws + L.o_lam2b);
+  PCTC_HIP(launch_grouped_adapter(logp, dlogp, K, M, G, g, stream));
+  PCTC_HIP(launch_lam2(lam, M, lam2, stream));
+  PCTC_HIP(launch_head_bwd(dt, H, M, D, W, bias, V, lam2, G, K, g, remap, logp, K + 1, dH, dW, db, ws + L.o_bwd,
+                           L.plan, stream));
+  PCTC_HIP(hipStreamSynchronize(stream));
+  prof_flush();
+  return PCTC_OK;
+}
+
 void pctc_prof_enable(int32_t on) { prof_state().enabled = (on != 0); }
 
 void pctc_prof_select(const char* name) {

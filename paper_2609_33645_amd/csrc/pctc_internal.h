@@ -78,6 +78,17 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
 
+// ---- grouped logits for a stock CTC (grouped_head.hip) ----------------------------------
+// small: device int32 [2] = {K, error flag}; remap[v] = j for v = u_ids[j], else -1.
+hipError_t launch_grouped_index(const int32_t* u_ids, int K, int V, int32_t* remap, int32_t* small,
+                                hipStream_t stream);
+hipError_t launch_grouped_comp_bias(const float* bias, const int32_t* remap, int V, float* bo, hipStream_t stream);
+hipError_t launch_fill_d(double* x, int n, double val, hipStream_t stream);
+// logp [M][K + 1]: raw selected logits in, exported log-probabilities out; lam [M] out.
+hipError_t launch_grouped_finalize(float* logp, int K, int M, const double* lse_o, double* lam, hipStream_t stream);
+hipError_t launch_grouped_adapter(const float* logp, const float* dlogp, int K, int M, float* G, float* g,
+                                  hipStream_t stream);
+
 // ---- alignment lattice ------------------------------------------------------------------
 struct DpPlan {
   int N, M, Y, Smax;

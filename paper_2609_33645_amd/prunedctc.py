@@ -85,6 +85,13 @@ def lib() -> ctypes.CDLL:
     L.pctc_head_bwd.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p,
                                 c_p, c_p]
     L.pctc_head_bwd.restype = c_i32
+    L.pctc_grouped_workspace_size.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32, c_i32]
+    L.pctc_grouped_workspace_size.restype = c_sz
+    L.pctc_grouped_logprobs.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_i32, c_p, c_p, c_p, c_sz, c_p]
+    L.pctc_grouped_logprobs.restype = c_i32
+    L.pctc_grouped_backward.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_p, c_i32, c_p, c_i32, c_p, c_p, c_p, c_i32,
+                                        c_p, c_p, c_p, c_p, c_sz, c_p]
+    L.pctc_grouped_backward.restype = c_i32
     L.pctc_prof_enable.argtypes = [c_i32]
     L.pctc_prof_select.argtypes = [ctypes.c_char_p]
     L.pctc_prof_reset.argtypes = []
@@ -135,6 +142,12 @@ def _workspace(nbytes: int, device) -> torch.Tensor:
     ws = torch.empty(max(int(nbytes), 256) + 256, dtype=torch.uint8, device=device)
     off = (-ws.data_ptr()) % 256
     return ws[off:off + max(int(nbytes), 256)]
+
+
+def _bias_vector(bias: torch.Tensor, V: int, dev) -> torch.Tensor:
+    if bias.numel() != V:
+        raise PrunedCTCError(-1, f"bias must hold V = {V} values, got {bias.numel()}")
+    return bias.reshape(V).to(device=dev, dtype=torch.float32).contiguous()
 
 
 def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, beam: float, chunk: int = 0) -> int:
@@ -203,9 +216,7 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
     dW = _grad_buffer(dW_out, (V, D), dev) if want_dW else None
     db = torch.empty(V, dtype=torch.float32, device=dev) if want_db else None
     if bias is not None:
-        bias = bias.to(device=dev, dtype=torch.float32).contiguous()
-        if bias.numel() != V:
-            raise PrunedCTCError(-1, "bias must have V entries")
+        bias = _bias_vector(bias, V, dev)
     if utt_weight is not None:
         utt_weight = utt_weight.to(device=dev, dtype=torch.float32).contiguous()
         if utt_weight.numel() != N:
@@ -321,7 +332,7 @@ def greedy_decode(H: torch.Tensor, W: torch.Tensor, input_lengths, blank: int = 
         raise PrunedCTCError(-1, "sum of input lengths differs from the rows of H")
     dev = H.device
     if bias is not None:
-        bias = bias.to(device=dev, dtype=torch.float32).contiguous()
+        bias = _bias_vector(bias, V, dev)
     ids = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
     tokens = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
     lengths = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
@@ -382,6 +393,98 @@ def head_bwd(H: torch.Tensor, W: torch.Tensor, lam: torch.Tensor, G: torch.Tenso
                            int(chunk), _ptr(dH), _ptr(dW), ctypes.c_void_p(scratch.data_ptr()), _stream(stream))
     _check(code, "pctc_head_bwd")
     return {"dH": dH, "dW": dW}
+
+
+# ---- grouped logits for a stock CTC -------------------------------------------------------
+
+def grouped_logprobs(H: torch.Tensor, W: torch.Tensor, u_ids: torch.Tensor, bias: Optional[torch.Tensor] = None,
+                     stream=None) -> Dict[str, torch.Tensor]:
+    """log softmax of the grouped logits [M, K + 1] (float32: the K selected classes, then
+    the merged "other" class) and the full normaliser lam [M] (float64)."""
+    L = lib()
+    dt = _dtype_code(H)
+    H = H.contiguous()
+    W = W.contiguous()
+    M, D = int(H.shape[0]), int(H.shape[1])
+    V = int(W.shape[0])
+    dev = H.device
+    u_ids = u_ids.to(device=dev, dtype=torch.int32).contiguous()
+    K = int(u_ids.numel())
+    if bias is not None:
+        bias = _bias_vector(bias, V, dev)
+    logp = torch.empty((M, K + 1), dtype=torch.float32, device=dev)
+    lam = torch.empty(max(M, 1), dtype=torch.float64, device=dev)
+    nbytes = int(L.pctc_grouped_workspace_size(dt, M, D, V, K, 0))
+    if nbytes == 0:
+        raise PrunedCTCError(-1, "pctc_grouped_workspace_size: invalid arguments")
+    ws = _workspace(nbytes, dev)
+    code = L.pctc_grouped_logprobs(dt, _ptr(H), M, D, _ptr(W), _ptr(bias), V, _ptr(u_ids), K, _ptr(logp), _ptr(lam),
+                                   ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()), _stream(stream))
+    _check(code, "pctc_grouped_logprobs")
+    return {"logp": logp, "lam": lam[:M]}
+
+
+def grouped_backward(H: torch.Tensor, W: torch.Tensor, u_ids: torch.Tensor, logp: torch.Tensor, lam: torch.Tensor,
+                     dlogp: torch.Tensor, bias: Optional[torch.Tensor] = None, chunk: int = 0,
+                     want_dH: bool = True, want_dW: bool = True, want_db: bool = False,
+                     stream=None) -> Dict[str, Optional[torch.Tensor]]:
+    """dH, dW (and db) from the gradient of a loss w.r.t. the exported grouped log-probabilities."""
+    L = lib()
+    dt = _dtype_code(H)
+    H = H.contiguous()
+    W = W.contiguous()
+    M, D = int(H.shape[0]), int(H.shape[1])
+    V = int(W.shape[0])
+    dev = H.device
+    u_ids = u_ids.to(device=dev, dtype=torch.int32).contiguous()
+    K = int(u_ids.numel())
+    if tuple(logp.shape) != (M, K + 1) or tuple(dlogp.shape) != (M, K + 1):
+        raise PrunedCTCError(-1, f"logp and dlogp must be [{M}, {K + 1}]")
+    if bias is not None:
+        bias = _bias_vector(bias, V, dev)
+    logp = logp.to(torch.float32).contiguous()
+    dlogp = dlogp.to(torch.float32).contiguous()
+    lam = lam.to(torch.float64).contiguous()
+    dH = torch.empty((M, D), dtype=torch.float32, device=dev) if want_dH else None
+    dW = torch.empty((V, D), dtype=torch.float32, device=dev) if want_dW else None
+    db = torch.empty(V, dtype=torch.float32, device=dev) if want_db else None
+    nbytes = int(L.pctc_grouped_workspace_size(dt, M, D, V, K, int(chunk)))
+    if nbytes == 0:
+        raise PrunedCTCError(-1, "pctc_grouped_workspace_size: invalid arguments")
+    ws = _workspace(nbytes, dev)
+    code = L.pctc_grouped_backward(dt, _ptr(H), M, D, _ptr(W), _ptr(bias), V, _ptr(u_ids), K, _ptr(logp), _ptr(lam),
+                                   _ptr(dlogp), int(chunk), _ptr(dH), _ptr(dW), _ptr(db),
+                                   ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()), _stream(stream))
+    _check(code, "pctc_grouped_backward")
+    return {"dH": dH, "dW": dW, "db": db}
+
+
+class GroupedHead(torch.autograd.Function):
+    """Autograd wrapper: grouped log-probabilities [M, K + 1] of the head H W^T (+ b), for a
+    stock CTC loss over K + 1 classes.  The backward runs the library's recomputed backward;
+    gradients are returned in the dtypes of H, W and b."""
+
+    @staticmethod
+    def forward(ctx, H, W, bias, u_ids):
+        out = grouped_logprobs(H.detach(), W.detach(), u_ids, None if bias is None else bias.detach())
+        ctx.save_for_backward(H, W, bias, u_ids, out["logp"], out["lam"])
+        return out["logp"]
+
+    @staticmethod
+    def backward(ctx, dlogp):
+        H, W, bias, u_ids, logp, lam = ctx.saved_tensors
+        need = ctx.needs_input_grad
+        r = grouped_backward(H.detach(), W.detach(), u_ids, logp, lam, dlogp,
+                             bias=None if bias is None else bias.detach(), want_dH=need[0], want_dW=need[1],
+                             want_db=bias is not None and need[2])
+        dH = r["dH"].to(H.dtype) if r["dH"] is not None else None
+        dW = r["dW"].to(W.dtype) if r["dW"] is not None else None
+        db = r["db"].to(bias.dtype) if r["db"] is not None else None
+        return dH, dW, db, None
+
+
+def grouped_head(H: torch.Tensor, W: torch.Tensor, u_ids: torch.Tensor, bias: Optional[torch.Tensor] = None):
+    return GroupedHead.apply(H, W, bias, u_ids)
 
 
 # ---- kernel timing -----------------------------------------------------------------------

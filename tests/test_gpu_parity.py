@@ -420,3 +420,106 @@ def test_greedy_decode(seed, dtype, blank, with_bias):
         assert got["tokens"][n] == own
         if sure[off[n]:off[n + 1]].all():
             assert got["tokens"][n] == ref["tokens"][n]
+
+
+# ---------------------------------------------------------------------------------------
+# grouped logits for a stock CTC (Eq. grouped, Prop. 1, Eq. offsupport)
+# ---------------------------------------------------------------------------------------
+
+def _stock_ctc(torch, logp, y_rel, T, U, dev):
+    """torch's own CTC over K + 1 classes (blank = column 0) on [M, K + 1] log-probabilities."""
+    off = np.concatenate([[0], np.cumsum(T)])
+    Tm = int(T.max())
+    pad = torch.stack([torch.nn.functional.pad(logp[off[n]:off[n + 1]], (0, 0, 0, Tm - int(T[n])))
+                       for n in range(len(T))], 1)
+    return torch.nn.functional.ctc_loss(pad, torch.as_tensor(y_rel, dtype=torch.long, device=dev),
+                                        torch.as_tensor(T, dtype=torch.long), torch.as_tensor(U, dtype=torch.long),
+                                        blank=0, reduction="sum")
+
+
+@pytest.mark.parametrize("seed,dtype,with_bias,chunk", [(0, "f32", False, 0), (1, "bf16", True, 512),
+                                                        (2, "bf16", False, 0), (3, "f32", True, 256)])
+def test_grouped_export(seed, dtype, with_bias, chunk):
+    """Export vs the oracle element by element; then torch's CTC on the GPU over the export,
+    through the autograd wrapper, against the full-vocabulary loss and gradients (Prop. 1)."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(60 + seed, N=4, T_range=(20, 150), D=128, V=3000, dtype=dtype, p_repeat=0.15,
+                                w_std=0.5)
+    rng = np.random.default_rng(seed)
+    b = rng.standard_normal(wl.V).astype(np.float32) if with_bias else None
+    b64 = None if b is None else b.astype(np.float64)
+    u = oracle.union_remap(wl.targets, wl.target_lengths, wl.blank, wl.V)
+    say(f"grouped seed={seed} {dtype} bias={with_bias} chunk={chunk} M={wl.M} K={u['K']} "
+        f"T={wl.input_lengths.tolist()}")
+    ex = oracle.grouped_logprobs(wl.H, wl.W, u["u_ids"], bias=b64)
+    full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, bias=b64)
+    H, W, _ = to_dev(wl)
+    uid = torch.from_numpy(u["u_ids"].astype(np.int32)).cuda()
+    bt = None if b is None else torch.from_numpy(b).cuda()
+    out = prunedctc.grouped_logprobs(H, W, uid, bias=bt)
+    logp = out["logp"].cpu().numpy()
+    assert logp.shape == ex["logp"].shape
+    say(f"  logp max err {np.abs(logp - ex['logp']).max():.3g}  lam max err "
+        f"{np.abs(out['lam'].cpu().numpy() - ex['lam']).max():.3g}")
+    assert np.abs(out["lam"].cpu().numpy() - ex["lam"]).max() < 2e-5
+    assert np.abs(logp - ex["logp"]).max() < 5e-5
+    # backward from the oracle's CTC gradient on the oracle's export, at this chunk
+    lp_ref = torch.tensor(ex["logp"], requires_grad=True)
+    _stock_ctc(torch, lp_ref, u["y_rel"], wl.input_lengths, wl.target_lengths, "cpu").backward()
+    dl = lp_ref.grad.numpy()
+    r = prunedctc.grouped_backward(H, W, uid, out["logp"], out["lam"], torch.from_numpy(dl.astype(np.float32)).cuda(),
+                                   bias=bt, chunk=chunk, want_db=with_bias)
+    fp32 = dtype == "f32"
+    for name in ("dH", "dW") + (("db",) if with_bias else ()):
+        got = r[name].cpu().numpy()
+        e, c = rel_err(got, full[name]), cosine(got, full[name])
+        say(f"  {name} rel={e:.3g} cos={c:.7f}")
+        assert (e <= 1e-4) if fp32 else (c >= 0.99999)
+    # the stock CTC on the GPU through the autograd wrapper
+    Hg = H.clone().requires_grad_(True)
+    Wg = W.clone().requires_grad_(True)
+    bg = None if bt is None else bt.clone().requires_grad_(True)
+    lp = prunedctc.grouped_head(Hg, Wg, uid, bg)
+    loss = _stock_ctc(torch, lp, u["y_rel"], wl.input_lengths, wl.target_lengths, "cuda")
+    loss.backward()
+    lr = loss_rel(float(loss.item()), full["loss"])
+    say(f"  stock CTC loss gpu={float(loss.item()):.9g} oracle={full['loss']:.9g} rel={lr:.3g}")
+    assert lr <= (1e-5 if fp32 else 2e-3)
+    for name, t in (("dH", Hg), ("dW", Wg)) + ((("db", bg),) if with_bias else ()):
+        got = t.grad.float().cpu().numpy()
+        c = cosine(got, full[name])
+        say(f"  autograd {name} cos={c:.7f}")
+        assert c >= (0.99999 if fp32 else 0.999)
+
+
+def test_grouped_edges():
+    """The selected ids cover the vocabulary (no merged class: its column is -inf); ids out
+    of range or repeated are rejected."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    rng = np.random.default_rng(5)
+    V, D, M = 24, 16, 70
+    H = rng.standard_normal((M, D)).astype(np.float32)
+    W = (rng.standard_normal((V, D)) * 0.4).astype(np.float32)
+    perm = rng.permutation(V).astype(np.int32)
+    ex = oracle.grouped_logprobs(H, W, perm)
+    out = prunedctc.grouped_logprobs(torch.from_numpy(H).cuda(), torch.from_numpy(W).cuda(),
+                                     torch.from_numpy(perm).cuda())
+    logp = out["logp"].cpu().numpy()
+    assert np.isneginf(logp[:, V]).all()
+    assert np.abs(logp[:, :V] - ex["logp"]).max() < 5e-5
+    dl = rng.standard_normal((M, V + 1)).astype(np.float32)
+    dl[:, V] = 0.0
+    dl[::3, :V] -= dl[::3, :V].mean(axis=1, keepdims=True)   # rows whose sum (g) is ~0
+    dl[1::3, :V] = 0.0                                        # rows with no gradient at all
+    r = prunedctc.grouped_backward(torch.from_numpy(H).cuda(), torch.from_numpy(W).cuda(), torch.from_numpy(perm).cuda(),
+                                   out["logp"], out["lam"], torch.from_numpy(dl).cuda())
+    ref = oracle.grouped_backward(H, W, ex["lam"], ex["logp"], dl[:, :V].astype(np.float64), perm)
+    assert rel_err(r["dH"].cpu().numpy(), ref["dH"]) <= 1e-4
+    assert rel_err(r["dW"].cpu().numpy(), ref["dW"]) <= 1e-4
+    for bad in ([0, 3, 3], [0, V], [-1, 2]):
+        with pytest.raises(prunedctc.PrunedCTCError) as e:
+            prunedctc.grouped_logprobs(torch.from_numpy(H).cuda(), torch.from_numpy(W).cuda(),
+                                       torch.tensor(bad, dtype=torch.int32, device="cuda"))
+        assert e.value.code == -2

@@ -669,7 +669,11 @@ def test_grouped_export_through_torch_ctc(seed, leaf_grad):
     np.testing.assert_allclose(back["dH"], full["dH"], atol=1e-10)
     np.testing.assert_allclose(back["dW"], full["dW"], atol=1e-10)
     np.testing.assert_allclose(back["db"], full["db"], atol=1e-10)
+    direct = oracle.grouped_backward(H, W, ex["lam"], ex["logp"], lp.grad.numpy(), u["u_ids"], bias=b, chunk=11)
+    for k in ("dH", "dW", "db"):
+        np.testing.assert_allclose(direct[k], full[k], atol=1e-10)
     if not leaf_grad:
+        np.testing.assert_allclose(direct["dW"], Wt.grad.numpy(), atol=1e-10)
         np.testing.assert_allclose(back["dH"], Ht.grad.numpy(), atol=1e-10)
         np.testing.assert_allclose(back["db"], bt.grad.numpy(), atol=1e-10)
 
@@ -692,3 +696,28 @@ def test_grouped_export_invariants():
                                  np.concatenate([dl, np.zeros((M, 1))], 1))
     np.testing.assert_allclose(gg["G"], dl, atol=0)
     np.testing.assert_allclose(gg["g"], dl.sum(1), atol=1e-13)
+
+
+def test_grouped_backward_whole_vocabulary_autograd():
+    """U = the whole vocabulary (no complement column) and a linear loss sum(dl * logp) whose
+    row sums vanish (the case where g = 0 for every frame): the written-out backward matches
+    torch autograd through log_softmax of the permuted logits."""
+    torch = pytest.importorskip("torch")
+    rng = np.random.default_rng(78)
+    M, V, D = 15, 7, 5
+    H = rng.standard_normal((M, D))
+    W = rng.standard_normal((V, D))
+    b = rng.standard_normal(V)
+    perm = rng.permutation(V)
+    dl = rng.standard_normal((M, V))
+    dl -= dl.mean(axis=1, keepdims=True)
+    ex = oracle.grouped_logprobs(H, W, perm, bias=b)
+    Ht = torch.tensor(H, requires_grad=True)
+    Wt = torch.tensor(W, requires_grad=True)
+    bt = torch.tensor(b, requires_grad=True)
+    lp = torch.log_softmax((Ht @ Wt.T + bt)[:, torch.tensor(perm)], dim=1)
+    (lp * torch.tensor(dl)).sum().backward()
+    direct = oracle.grouped_backward(H, W, ex["lam"], ex["logp"], dl, perm, bias=b, chunk=3)
+    np.testing.assert_allclose(direct["dH"], Ht.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(direct["dW"], Wt.grad.numpy(), atol=1e-12)
+    np.testing.assert_allclose(direct["db"], bt.grad.numpy(), atol=1e-12)
