@@ -242,3 +242,60 @@ def test_full_size_greedy(name):
     _check_greedy(wl, H64, W64, np.zeros(wl.V), got, ref, frames=frames)
     del H, W
     torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(900)
+def test_full_size_grouped_export():
+    """The grouped export at the zipformer_m size feeding torch's own CTC on the GPU: sampled
+    exported rows against the oracle's, every row a distribution, the stock loss against the
+    oracle's full-vocabulary loss, and sampled gradient rows (Prop. 1) against the oracle's."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.NAMED["zipformer_m"](0, beam=math.inf)
+    say(f"full-size grouped export: N={wl.N} M={wl.M} D={wl.D} V={wl.V}")
+    H, W, y = to_dev(wl)
+    un = prunedctc.union_remap(y, wl.blank, wl.V)
+    K = un["K"]
+    uid = un["u_ids"][:K].contiguous()
+    Hg = H.clone().requires_grad_(True)
+    Wg = W.clone().requires_grad_(True)
+    lp = prunedctc.grouped_head(Hg, Wg, uid)
+    off = np.concatenate([[0], np.cumsum(wl.input_lengths)])
+    Tm = int(wl.input_lengths.max())
+    pad = torch.stack([torch.nn.functional.pad(lp[off[n]:off[n + 1]], (0, 0, 0, Tm - int(wl.input_lengths[n])))
+                       for n in range(wl.N)], 1)
+    loss = torch.nn.functional.ctc_loss(pad, un["y_rel"].long(), torch.as_tensor(wl.input_lengths, dtype=torch.long),
+                                        torch.as_tensor(wl.target_lengths, dtype=torch.long), blank=0,
+                                        reduction="sum")
+    loss.backward()
+    torch.cuda.synchronize()
+    logp = lp.detach().cpu().numpy()
+    say(f"  gpu path done (K={K})")
+    rowsum = np.exp(logp.astype(np.float64)).sum(axis=1)
+    assert np.abs(rowsum - 1.0).max() < 1e-5
+
+    W64 = wl.W.astype(np.float64)
+    H64 = wl.H.astype(np.float64)
+    ref_un = oracle.union_remap(wl.targets, wl.target_lengths, wl.blank, wl.V)
+    np.testing.assert_array_equal(uid.cpu().numpy(), ref_un["u_ids"])
+    rng = np.random.default_rng(11)
+    frames, classes = _samples(wl, rng, ref_un["u_ids"])
+    ex = oracle.grouped_logprobs(H64[frames], W64, ref_un["u_ids"])
+    say(f"  sampled export max err {np.abs(logp[frames] - ex['logp']).max():.3g}")
+    assert np.abs(logp[frames] - ex["logp"]).max() < 5e-5
+
+    lam = oracle.log_normalizer(H64, W64)
+    S = oracle.selected_logprobs(H64, W64, ref_un["u_ids"], lam)
+    dp = oracle.ctc_from_scores(S, ref_un["y_rel"], wl.input_lengths, wl.target_lengths, math.inf)
+    assert (dp["status"] == 0).all()
+    lr = loss_rel(float(loss.item()), dp["loss"])
+    say(f"  stock CTC loss gpu={float(loss.item()):.9g} oracle={dp['loss']:.9g} rel={lr:.3g}")
+    assert lr <= 2e-3
+    rows = oracle.head_backward_rows(H64, W64, lam, dp["G"], dp["g"], ref_un["u_ids"], frames, classes)
+    dH_s = Hg.grad.float()[torch.from_numpy(frames).cuda()].cpu().numpy()
+    dW_s = Wg.grad.float()[torch.from_numpy(classes).cuda()].cpu().numpy()
+    cH, cW = cosine(dH_s, rows["dH"]), cosine(dW_s, rows["dW"])
+    say(f"  sampled gradients cos dH={cH:.7f} dW={cW:.7f}")
+    assert cH >= 0.999 and cW >= 0.999
+    del lp, pad, loss, Hg, Wg, H, W, y
+    torch.cuda.empty_cache()
