@@ -43,6 +43,11 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-utts", type=int, default=16, help="utterances in the CPU-baseline sample")
     ap.add_argument("--frozen-head", action="store_true", help="skip dW (frozen LLM head)")
+    ap.add_argument("--path", default="fused", choices=("fused", "greedy", "grouped", "discarded"),
+                    help="fused: the training step (default); greedy: the argmax emission head; grouped: the "
+                         "grouped-logit export and its backward; discarded: the discarded-mass estimator")
+    ap.add_argument("--oracle-timing", action="store_true",
+                    help="only time the oracle (CPU) on a bounded sample of every workload, 1 thread and all cores")
     ap.add_argument("--copy-probe", action="store_true",
                     help="only run a plain 256 MiB device-to-device copy (calibrates memory counters)")
     return ap.parse_args()
@@ -124,6 +129,173 @@ def cpu_baseline(wl, n_utts: int):
                       f"fp64 NumPy/BLAS, {dt:.1f} s"}
 
 
+def aux_figures(wl, K: int, kernel_ms):
+    """HBM rates of the small kernels against 8 TB/s and the lattice stage's share of the step."""
+    T, U = wl.input_lengths, wl.target_lengths
+    Y = int(U.sum())
+    out = {}
+    if kernel_ms.get("union_remap"):
+        b = Y * 4 * 3 + wl.V * 4        # targets read twice, y_rel written, remap written
+        out["union_remap_gbs"] = round(b / (kernel_ms["union_remap"] * 1e-3) / 1e9, 2)
+    if kernel_ms.get("gather_s"):
+        es = 2 if wl.dtype == "bf16" else 4
+        b = K * wl.D * es + wl.M * wl.D * es + wl.M * K * 4
+        out["gather_s_gbs"] = round(b / (kernel_ms["gather_s"] * 1e-3) / 1e9, 2)
+    dp = [k for k in kernel_ms if k.startswith("dp_")]
+    dp_ms = sum(kernel_ms[k] for k in dp)
+    tot = sum(kernel_ms.values())
+    if dp_ms:
+        # alpha and beta passes read each frame's U_n + 1 scores; tables written once per pass
+        b = 2 * sum(int(t) * (int(u) + 1) * 4 + int(t) * (2 * int(u) + 1) * 4 for t, u in zip(T, U))
+        out["dp_ms"] = round(dp_ms, 4)
+        out["dp_share_of_kernel_time"] = round(dp_ms / tot, 4)
+        out["dp_alpha_beta_gbs"] = round(b / (kernel_ms.get("dp_alpha_beta", dp_ms) * 1e-3) / 1e9, 2)
+    return out
+
+
+def timed(step, steps: int, warmup: int, kernels):
+    """Warm up, time every kernel with events (breakdown), then time `steps` calls with events
+    only around the dominant kernel of `kernels`.  Returns (seconds, breakdown, dominant, its
+    event totals)."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    prunedctc.prof_select(None)
+    prunedctc.prof_reset()
+    prunedctc.prof_enable(True)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    prunedctc.prof_enable(False)
+    prof = prunedctc.prof_read()
+    dom = max((k for k in kernels if k in prof), key=lambda k: prof[k]["total_ms"])
+    prunedctc.prof_select(dom)
+    prunedctc.prof_reset()
+    prunedctc.prof_enable(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    prunedctc.prof_enable(False)
+    dom_prof = prunedctc.prof_read()[dom]
+    prunedctc.prof_select(None)
+    return dt, prof, dom, dom_prof
+
+
+def bench_extra(a):
+    """One JSON line for the widening rows: greedy head, grouped export (+ backward from a
+    fixed upstream gradient), discarded-mass estimator at one beam."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = make_workload(a.workload, a.seed, a.beam)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    tdt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    H = torch.from_numpy(wl.H).to(dev).to(tdt)
+    W = torch.from_numpy(wl.W).to(dev).to(tdt)
+    y = torch.from_numpy(wl.targets).to(dev)
+    T, U = wl.input_lengths, wl.target_lengths
+    M, D, V = wl.M, wl.D, wl.V
+    un = prunedctc.union_remap(y, wl.blank, V)
+    K = un["K"]
+    uid = un["u_ids"][:K].contiguous()
+    peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
+    extra = {}
+    if a.path == "greedy":
+        def step():
+            prunedctc.greedy_decode(H, W, T, wl.blank, to_host=False)
+        kernels, flops = ("amax_partial",), {"amax_partial": 2.0 * M * V * D}
+        metric = "frames/sec greedy full-vocabulary argmax head + CTC collapse at V=180K"
+    elif a.path == "grouped":
+        dl = torch.randn((M, K + 1), generator=torch.Generator().manual_seed(a.seed)).to(dev)
+        ex = prunedctc.grouped_logprobs(H, W, uid)
+
+        def step():
+            e = prunedctc.grouped_logprobs(H, W, uid)
+            prunedctc.grouped_backward(H, W, uid, e["logp"], e["lam"], dl, chunk=a.chunk)
+        kernels = ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm")
+        flops = {k: 2.0 * M * V * D for k in kernels}
+        metric = "frames/sec grouped-logit export fwd + bwd (stock-CTC interface) at V=180K"
+        del ex
+    else:
+        beam = 16.0 if not math.isfinite(wl.beam) else wl.beam
+        st = prunedctc.lse_select(H, W, uid)
+        S = st["S"].contiguous()
+        yrel = un["y_rel"]
+
+        def step():
+            prunedctc.discarded_mass(S, yrel, T, U, [beam])
+        kernels, flops = ("dp_discarded",), None
+        metric = "frames/sec discarded-mass estimator (retained and full lattice sums, fp64)"
+        extra["beam"] = beam
+    dt, prof, dom, dom_prof = timed(step, a.steps, a.warmup, kernels)
+    kernel_ms = {k: v["total_ms"] / a.steps for k, v in prof.items()}
+    dom_avg_ms = dom_prof["total_ms"] / dom_prof["launches"]
+    if flops is not None:
+        per_launch = flops[dom] / (dom_prof["launches"] / a.steps)
+        ach = per_launch / (dom_avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
+                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom)}
+    else:
+        # lattice sums: each frame reads its U_n + 1 selected scores and 2U_n + 1 arc-mask bytes
+        nbytes = float(sum(int(t) * ((int(u) + 1) * 4 + (2 * int(u) + 1)) for t, u in zip(T, U)))
+        ach = nbytes / (dom_avg_ms * 1e-3) / 1e9
+        roof = {"bound": "latency", "kernel": dom, "achieved": round(ach, 2), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(ach / PEAK_HBM_GBS, 5), "traffic": None}
+    line = {"metric": metric, "value": round(M * a.steps / dt, 1), "unit": "frames/s", "n_gpus": 1,
+            "steps": a.steps, "warmup": a.warmup, "ms_per_step": round(dt * 1e3 / a.steps, 4),
+            "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": wl.dtype,
+            "data": "synthetic (seeded; shapes of the paper's workloads, no corpus data)",
+            "config": {"workload": wl.name, "path": a.path, "N": wl.N, "M": M, "D": D, "V": V, "K": K, **extra},
+            "roofline": roof,
+            "kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(kernel_ms.items(), key=lambda kv: -kv[1])}}
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+def oracle_timing(a):
+    """The oracle on a bounded sample (first utterance, full vocabulary) of every workload, at
+    one BLAS thread and at all cores."""
+    import platform
+    from threadpoolctl import threadpool_limits
+    from paper_2609_33645_amd import workloads
+    import oracle
+    cores = len(os.sched_getaffinity(0))
+    cpu = platform.processor() or "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    cpu = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    blas = sorted({f"{p.get('internal_api')}:{p.get('version')}" for p in __import__("threadpoolctl").threadpool_info()})
+    rows = []
+    for name in ("tiny_f32", "zipformer_m", "qwen3_0p6b", "qwen3_8b", "qwen3_32b"):
+        wl = make_workload(name, a.seed, None)
+        T, U = wl.input_lengths[:1], wl.target_lengths[:1]
+        M, Y = int(T[0]), int(U[0])
+        res = {}
+        est_flops = 8.0 * M * wl.V * wl.D
+        for nt in (1, cores):
+            if nt == 1 and est_flops > 1e12:
+                res["threads_1"] = "skipped (over 1e12 fp64 flops: minutes at one thread)"
+                continue
+            with threadpool_limits(limits=nt):
+                t0 = time.perf_counter()
+                oracle.fwd_bwd(wl.H[:M], wl.W, wl.targets[:Y], T, U, wl.blank, wl.beam)
+                res[f"threads_{nt}"] = round(M / (time.perf_counter() - t0), 2)
+        rows.append({"workload": name, "frames": M, "V": wl.V, "D": wl.D, "frames_per_s": res})
+        print(json.dumps(rows[-1]), flush=True)
+    print(json.dumps({"oracle_timing": rows, "cores": cores, "cpu": cpu, "blas": blas}), flush=True)
+    return 0
+
+
 def main():
     a = parse()
     if a.copy_probe:
@@ -132,6 +304,10 @@ def main():
         print(f"bench.py measures one GPU only (this build runs the whole path on a single MI355X); "
               f"--gpus {a.gpus} is not supported", file=sys.stderr)
         return 2
+    if a.oracle_timing:
+        return oracle_timing(a)
+    if a.path != "fused":
+        return bench_extra(a)
     import torch
     from paper_2609_33645_amd import prunedctc
 
@@ -172,33 +348,9 @@ def main():
                                                  want_dW=not a.frozen_head, workspace=ws, dH_out=dH_buf,
                                                  dW_out=dW_buf)
 
-    for _ in range(a.warmup):
-        step()
-    torch.cuda.synchronize()
     # per-kernel breakdown: HIP events around every kernel the library launches (its stream);
     # not the timed region, since events between launches keep them from overlapping
-    prunedctc.prof_select(None)
-    prunedctc.prof_reset()
-    prunedctc.prof_enable(True)
-    for _ in range(a.steps):
-        step()
-    torch.cuda.synchronize()
-    prunedctc.prof_enable(False)
-    prof = prunedctc.prof_read()
-    dom = max((k for k in GEMM_KERNELS if k in prof), key=lambda k: prof[k]["total_ms"])
-    # timed region: events only around the dominant kernel's launches
-    prunedctc.prof_select(dom)
-    prunedctc.prof_reset()
-    prunedctc.prof_enable(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(a.steps):
-        step()
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    prunedctc.prof_enable(False)
-    dom_prof = prunedctc.prof_read()[dom]
-    prunedctc.prof_select(None)
+    dt, prof, dom, dom_prof = timed(step, a.steps, a.warmup, GEMM_KERNELS)
     ms_step = dt * 1e3 / a.steps
     M, D, V = wl.M, wl.D, wl.V
     fps = M * a.steps / dt
@@ -233,6 +385,8 @@ def main():
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom)},
         "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),
         "mfma_frac_step": round(gemm_total / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "mfma_frac_useful": round(6.0 * M * V * D / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "aux": aux_figures(wl, K, kernel_ms),
         "peak_mb": round(peak_mb, 1),
         "peak_mb_incl_grads": round(peak_mb_grads, 1),
         "workspace_mb": round(ws_mb, 1),

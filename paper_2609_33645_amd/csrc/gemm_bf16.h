@@ -318,15 +318,23 @@ struct Gemm {
     __builtin_amdgcn_s_barrier();         // before anyone reuses the stages
   }
 
+  struct ZeroInit {
+    __device__ __forceinline__ void operator()(int, f32x16 (&acc)[FR][FC]) const { zero(acc); }
+  };
   // A sequence of ntiles output tiles over k in [0, K): tile i uses A rows from
   // row0 + i * BR and the same B rows (col0).  One copy pipeline runs through the tile
   // boundaries; epi(i, acc) is called after tile i's last product, while the next tile's
-  // copies are in flight, and must not touch the LDS stages.  No row gather on A.
-  template <class Epi>
+  // copies are in flight, and must not touch the LDS stages.  init(i, acc) sets the
+  // accumulators before tile i's first product (zero by default; a caller can start them
+  // at a per-row offset, which then enters the sum exactly as an fp32 addend).  No row
+  // gather on A.
+  template <class Epi, class Init = ZeroInit>
   __device__ static __forceinline__ void run_seq(const GOp& A, const GOp& B, int row0, int col0, int ntiles, int K,
-                                                 char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi) {
+                                                 char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi,
+                                                 Init&& init = Init{}) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    zero(acc);
+    if (ntiles > 0) init(0, acc);
+    else zero(acc);
     const int nk = (K + BK - 1) / BK;
     if (nk <= 0 || ntiles <= 0) return;
     const int klimA = min(A.kmax, K), klimB = min(B.kmax, K);
@@ -359,7 +367,8 @@ struct Gemm {
     auto after = [&]() {
       if (++kt == nk) {
         if (tile < ntiles) epi(tile, acc);
-        zero(acc);
+        if (tile + 1 < ntiles) init(tile + 1, acc);
+        else zero(acc);
         kt = 0;
         ++tile;
       }

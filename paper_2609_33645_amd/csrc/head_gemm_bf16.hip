@@ -73,11 +73,28 @@ __device__ __forceinline__ bool grouped_tile(int work, int nA, int nB, int& a, i
   return a < nA && b < nB;
 }
 
+// Accumulators of a tile start at the bias of their row (bt: the tile's rows, in LDS).
+template <int FR, int FC>
+__device__ __forceinline__ void bias_init(f32x16 (&acc)[FR][FC], const float* bt, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float4 b4 = *reinterpret_cast<const float4*>(bt + GFwd::row_of(wave, lane, i, 4 * q));
+#pragma unroll
+      for (int j = 0; j < FC; ++j) {
+        acc[i][j][4 * q + 0] = b4.x;
+        acc[i][j][4 * q + 1] = b4.y;
+        acc[i][j][4 * q + 2] = b4.z;
+        acc[i][j][4 * q + 3] = b4.w;
+      }
+    }
+}
+
 // Online log-sum-exp update of the running (max, sum) of this lane's frames with one
-// tile; rows at or past vend are skipped when MASK.  With BIAS, b[v] (staged in LDS, bt
-// pointing at the tile's first row) is added to every logit of row v.
-template <bool MASK, bool BIAS, int FR, int FC>
-__device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], const float* bt, float (&run_max)[FC],
+// tile of logits (bias included); rows at or past vend are skipped when MASK.
+template <bool MASK, int FR, int FC>
+__device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], float (&run_max)[FC],
                                                 float (&run_sum)[FC], int v0, int vend, int wave, int lane) {
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
@@ -87,13 +104,9 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], con
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
-        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (BIAS) b4 = *reinterpret_cast<const float4*>(bt + r0);
-        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float x = acc[i][j][4 * q + e];
-          if (BIAS) x += bb[e];
+          const float x = acc[i][j][4 * q + e];
           if (MASK) {
             if (v0 + r0 + e < vend) tmax = fmaxf(tmax, x);
           } else {
@@ -111,14 +124,9 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], con
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
-        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (BIAS) b4 = *reinterpret_cast<const float4*>(bt + r0);
-        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float x = acc[i][j][4 * q + e];
-          if (BIAS) x += bb[e];
-          const float ex = fast_exp2(fmaf(x, kLog2e, -ms));
+          const float ex = fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ms));
           if (MASK) {
             if (v0 + r0 + e < vend) s += ex;
           } else {
@@ -165,14 +173,19 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
     run_sum[j] = 0.f;
   }
   f32x16 acc[FR][FC];
-  G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, [&](int i, const f32x16 (&a)[FR][FC]) {
+  auto epi = [&](int i, const f32x16 (&a)[FR][FC]) {
     const int v0 = vbeg + i * kFR;
-    const float* bt = bsh + i * kFR;
     if (v0 + kFR <= vend)
-      lse_tile_update<false, BIAS, FR, FC>(a, bt, run_max, run_sum, v0, vend, wave, lane);
+      lse_tile_update<false, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
     else
-      lse_tile_update<true, BIAS, FR, FC>(a, bt, run_max, run_sum, v0, vend, wave, lane);
-  });
+      lse_tile_update<true, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+  };
+  if (BIAS)
+    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int i, f32x16 (&a)[FR][FC]) {
+      bias_init<FR, FC>(a, bsh + i * kFR, wave, lane);
+    });
+  else
+    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
   __syncthreads();
   // the two wavefronts of each frame column (row halves) combine their partial sums
   float2* xch = reinterpret_cast<float2*>(st0_);
@@ -240,9 +253,8 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
     bi[j] = 0x7fffffff;
   }
   f32x16 acc[FR][FC];
-  G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, [&](int it, const f32x16 (&a)[FR][FC]) {
+  auto epi = [&](int it, const f32x16 (&a)[FR][FC]) {
     const int v0 = vbeg + it * kFR;
-    const float* bt = bsh + it * kFR;
 #pragma unroll
     for (int j = 0; j < FC; ++j)
 #pragma unroll
@@ -250,14 +262,18 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int rl = G::row_of(wave, lane, i, r);
-          float x = a[i][j][r];
-          if (BIAS) x += bt[rl];
-          if (v0 + rl < vend && x > bv[j]) {
-            bv[j] = x;
+          if (v0 + rl < vend && a[i][j][r] > bv[j]) {
+            bv[j] = a[i][j][r];
             bi[j] = v0 + rl;
           }
         }
-  });
+  };
+  if (BIAS)
+    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int it, f32x16 (&a)[FR][FC]) {
+      bias_init<FR, FC>(a, bsh + it * kFR, wave, lane);
+    });
+  else
+    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
   // lane halves hold the other half of each 32-row block, then the row halves of the tile
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
@@ -352,14 +368,14 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   const int m0 = mt * kFC;
   const int vl0 = vt * kFR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // union columns of this tile: (union index << 8) | tile column; b log2(e) per column
+  // union columns of this tile: (union index << 8) | tile column; b per column
   __shared__ int ulist[kFR];
   __shared__ int nu;
   __shared__ __attribute__((aligned(16))) float bl[BIAS ? kFR : 4];
   if (tid == 0) nu = 0;
   const bool vin = vl0 + tid < cw;
   const int jsel = vin ? remap[c0 + vl0 + tid] : -1;
-  if (BIAS) bl[tid] = vin ? bias[c0 + vl0 + tid] * kLog2e : 0.f;
+  if (BIAS) bl[tid] = vin ? bias[c0 + vl0 + tid] : 0.f;
   const int any_sel = __syncthreads_or(jsel >= 0);
   if (any_sel) {
     if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
@@ -378,7 +394,12 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
   const GOp B{Hs, D, M, D, nullptr};
   f32x16 acc[FR][FC];
-  GG::run(A, B, vl0, m0, 0, D, st, acc);
+  if (BIAS) {  // the logits' accumulators start at b (visible after the barrier above)
+    bias_init<FR, FC>(acc, bl, wave, lane);
+    GG::template run<false>(A, B, vl0, m0, 0, D, st, acc);
+  } else {
+    GG::run(A, B, vl0, m0, 0, D, st, acc);
+  }
   const int nunion = any_sel ? nu : 0;
   const int ch = wave & 1;            // column half: frames [64 ch, 64 ch + 64) of the tile
   char* stage = ch ? st1_ : st0_;     // 32 frames x 256 vocabulary columns per pass
@@ -391,13 +412,9 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int rl0 = GG::row_of(wave, lane, i, 4 * q);
-        float4 b4 = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (BIAS) b4 = *reinterpret_cast<const float4*>(bl + rl0);
-        const float bb[4] = {b4.x, b4.y, b4.z, b4.w};
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, BIAS ? bb[e] - ll[j] : -ll[j]));
+        for (int e = 0; e < 4; ++e) v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ll[j]));
         *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) =
             u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
       }

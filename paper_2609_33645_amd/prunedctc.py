@@ -317,9 +317,10 @@ def ctc_dp(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_lengths, 
 
 
 def greedy_decode(H: torch.Tensor, W: torch.Tensor, input_lengths, blank: int = 0,
-                  bias: Optional[torch.Tensor] = None, stream=None) -> Dict[str, object]:
+                  bias: Optional[torch.Tensor] = None, stream=None, to_host: bool = True) -> Dict[str, object]:
     """Framewise full-vocabulary argmax ids [M] and the collapsed token sequence of each
-    utterance (a list of lists), plus the raw device buffers."""
+    utterance (a list of lists, only when to_host), plus the device buffers (tokens of
+    utterance n at the offset of its first frame)."""
     L = lib()
     dt = _dtype_code(H)
     H = H.contiguous()
@@ -341,6 +342,8 @@ def greedy_decode(H: torch.Tensor, W: torch.Tensor, input_lengths, blank: int = 
                                 _ptr(tokens), _ptr(lengths), ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()),
                                 _stream(stream))
     _check(code, "pctc_greedy_decode")
+    if not to_host:
+        return {"ids": ids[:M], "tokens_dev": tokens[:M], "token_lengths": lengths[:N]}
     off = np.concatenate([[0], np.cumsum(T)]).astype(np.int64)
     tk = tokens.cpu().numpy()
     ln = lengths.cpu().numpy()[:N]
@@ -358,9 +361,12 @@ def discarded_mass(S: torch.Tensor, y_rel: torch.Tensor, input_lengths, target_l
     N = int(T.size)
     M, K = int(S.shape[0]), int(S.shape[1])
     dev = S.device
-    ldS = ((K + 3) // 4) * 4
-    Sp = torch.zeros((max(M, 1), ldS), dtype=torch.float32, device=dev)
-    Sp[:M, :K] = S.to(torch.float32)
+    if S.dtype == torch.float32 and S.is_contiguous() and K % 4 == 0 and M > 0:
+        ldS, Sp = K, S                     # already in the library's layout
+    else:
+        ldS = ((K + 3) // 4) * 4
+        Sp = torch.zeros((max(M, 1), ldS), dtype=torch.float32, device=dev)
+        Sp[:M, :K] = S.to(torch.float32)
     y_rel = y_rel.to(torch.int32).contiguous()
     b = np.ascontiguousarray(np.asarray(beams, np.float32))
     delta = torch.empty((max(len(b), 1), max(N, 1)), dtype=torch.float64, device=dev)
