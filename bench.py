@@ -55,7 +55,7 @@ def parse():
 
 KERNEL_SOURCES = ("paper_2609_33645_amd/csrc/head_gemm_bf16.hip", "paper_2609_33645_amd/csrc/gemm_bf16.h",
                   "paper_2609_33645_amd/csrc/pctc_device.h", "paper_2609_33645_amd/csrc/head_gemm.hip",
-                  "paper_2609_33645_amd/csrc/ctc_dp.hip")
+                  "paper_2609_33645_amd/csrc/ctc_dp.hip", "paper_2609_33645_amd/csrc/grouped_head.hip")
 
 
 def kernel_source_hash() -> str:
