@@ -68,7 +68,10 @@ struct MC {
   static constexpr int kSlots = R / 8;
   static constexpr int kRowBytes = R * 2;
   static constexpr int kRowsPerCopy = 64 / kSlots;
-  __device__ static __forceinline__ int swz(int kr) { return ((kr & 7) << 1) & (kSlots - 1); }
+  // A transpose read takes, per half-wavefront, 4 consecutive k-lines x 4 consecutive slots:
+  // k-line kr moves its slots by (kr mod 4) groups of 4, so the 16 reads land in 16
+  // different 16-byte bank groups.
+  __device__ static __forceinline__ int swz(int kr) { return ((kr & 3) << 2) & (kSlots - 1); }
 };
 
 // Copies one operand tile (NR rows x BK k) into LDS as kCopies 1 KB copies; wave w of
