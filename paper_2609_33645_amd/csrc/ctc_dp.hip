@@ -527,6 +527,67 @@ hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status
 }
 
 // ---------------------------------------------------------------------------------------
+// Inclusion forecast.  For an included utterance every frame's occupancies sum to one
+// (each retained alignment occupies exactly one state per frame), so g_m = -w_n there and
+// 0 on excluded utterances.  Before the lattice runs, an utterance is forecast included when
+// its targets fit its frames (T_n >= U_n + repeats), every frame has a finite normaliser,
+// and w_n != 0; the lattice's statuses are checked against the forecast afterwards.
+// ---------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+g_forecast_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ yoff, const int32_t* __restrict__ y_rel,
+                  const double* __restrict__ lam, const float* __restrict__ weight, float* __restrict__ g_pred,
+                  int32_t* __restrict__ pred) {
+  const int n = blockIdx.x;
+  const int t0 = toff[n], T = toff[n + 1] - t0;
+  const int y0 = yoff[n], U = yoff[n + 1] - y0;
+  int reps = 0, bad = 0;
+  for (int i = 1 + threadIdx.x; i < U; i += blockDim.x) reps += (y_rel[y0 + i] == y_rel[y0 + i - 1]);
+  for (int t = threadIdx.x; t < T; t += blockDim.x) {
+    const double l = lam[t0 + t];
+    bad |= !(l > -INFINITY && l < INFINITY);  // NaN fails both
+  }
+  __shared__ int sreps;
+  if (threadIdx.x == 0) sreps = 0;
+  __syncthreads();
+  if (reps) atomicAdd(&sreps, reps);
+  const int anybad = __syncthreads_or(bad);
+  const float w = weight ? weight[n] : 1.f;
+  const bool inc = !anybad && T >= U + sreps && w != 0.f;
+  for (int t = threadIdx.x; t < T; t += blockDim.x) g_pred[t0 + t] = inc ? -w : 0.f;
+  if (threadIdx.x == 0) pred[n] = inc ? 1 : 0;
+}
+
+// flag = 1 if any utterance's inclusion (status 0 and w_n != 0) differs from the forecast
+__global__ void forecast_check_kernel(int N, const int32_t* __restrict__ status, const float* __restrict__ weight,
+                                      const int32_t* __restrict__ pred, int32_t* __restrict__ flag) {
+  int bad = 0;
+  for (int n = threadIdx.x; n < N; n += blockDim.x) {
+    const float w = weight ? weight[n] : 1.f;
+    const int inc = (status[n] == 0 && w != 0.f) ? 1 : 0;
+    bad |= (inc != pred[n]);
+  }
+  bad = __syncthreads_or(bad);
+  if (threadIdx.x == 0) flag[0] = bad;
+}
+
+hipError_t launch_g_forecast(const DpPlan& plan, void* scratch, const int32_t* y_rel, const double* lam,
+                             const float* weight, float* g_pred, int32_t* pred, hipStream_t stream) {
+  if (plan.N == 0) return hipSuccess;
+  char* sc = static_cast<char*>(scratch);
+  const int32_t* toff = reinterpret_cast<const int32_t*>(sc + plan.off_toff);
+  const int32_t* yoff = reinterpret_cast<const int32_t*>(sc + plan.off_yoff);
+  hipLaunchKernelGGL(g_forecast_kernel, dim3(plan.N), dim3(256), 0, stream, toff, yoff, y_rel, lam, weight, g_pred,
+                     pred);
+  return hipGetLastError();
+}
+
+hipError_t launch_forecast_check(int N, const int32_t* status, const float* weight, const int32_t* pred,
+                                 int32_t* flag, hipStream_t stream) {
+  hipLaunchKernelGGL(forecast_check_kernel, dim3(1), dim3(256), 0, stream, N, status, weight, pred, flag);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------------------
 
 template <bool VIT>
 static hipError_t launch_pass(int Q, dim3 grid, hipStream_t stream, const float* S, int ldS, const int32_t* toff,

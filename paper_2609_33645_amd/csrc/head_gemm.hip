@@ -609,11 +609,14 @@ __global__ void ht_build_kernel(const T* __restrict__ H, int M, int D, const flo
   }
 }
 
-__global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int64_t n, float* __restrict__ dH) {
+// dH = sum of the split-K partials (+ extra, the union-column part, when given), in order.
+__global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int64_t n, const float* __restrict__ extra,
+                                 float* __restrict__ dH) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= n) return;
   float s = 0.f;
   for (int k = 0; k < splits; ++k) s += part[k * n + i];
+  if (extra) s += extra[i];
   dH[i] = s;
 }
 
@@ -723,7 +726,7 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* 
     const int64_t n = static_cast<int64_t>(M) * D;
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
-                       plan.splits, n, dH);
+                       plan.splits, n, nullptr, dH);
   }
   return hipGetLastError();
 }
@@ -731,7 +734,8 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* 
 static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                 const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                                 const float* S, int ldS, float* dH, float* dW, float* db, char* scratch,
-                                const BwdPlan& plan, hipStream_t stream) {
+                                const BwdPlan& plan, hipStream_t stream, const float* dH_extra,
+                                hipEvent_t before_reduce) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
   uint16_t* Hs = reinterpret_cast<uint16_t*>(scratch + plan.dz_bytes);
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
@@ -752,11 +756,15 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
                               dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
     if (e != hipSuccess) return e;
   }
+  if (before_reduce) {
+    e = hipStreamWaitEvent(stream, before_reduce, 0);
+    if (e != hipSuccess) return e;
+  }
   if (dH) {
     const int64_t n = static_cast<int64_t>(M) * D;
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
-                       plan.splits, n, dH);
+                       plan.splits, n, dH_extra, dH);
   }
   return hipGetLastError();
 }
@@ -764,7 +772,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                            const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                            const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
-                           const BwdPlan& plan, hipStream_t stream) {
+                           const BwdPlan& plan, hipStream_t stream, const float* dH_extra, hipEvent_t before_reduce) {
   if (M <= 0) {
     if (db) {
       hipError_t e = hipMemsetAsync(db, 0, static_cast<size_t>(V) * sizeof(float), stream);
@@ -776,7 +784,7 @@ hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W
   char* sc = static_cast<char*>(scratch);
   if (dtype == 1)
     return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias, V, lam2, G, ldG,
-                         g, remap, S, ldS, dH, dW, db, sc, plan, stream);
+                         g, remap, S, ldS, dH, dW, db, sc, plan, stream, dH_extra, before_reduce);
   return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), bias, V, lam2, G, ldG, g,
                            remap, dH, dW, db, sc, plan, stream);
 }

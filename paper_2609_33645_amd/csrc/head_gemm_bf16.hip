@@ -374,7 +374,7 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   __shared__ __attribute__((aligned(16))) float bl[BIAS ? kFR : 4];
   if (tid == 0) nu = 0;
   const bool vin = vl0 + tid < cw;
-  const int jsel = vin ? remap[c0 + vl0 + tid] : -1;
+  const int jsel = (vin && remap) ? remap[c0 + vl0 + tid] : -1;  // no remap: dense part only
   if (BIAS) bl[tid] = vin ? bias[c0 + vl0 + tid] : 0.f;
   const int any_sel = __syncthreads_or(jsel >= 0);
   if (any_sel) {
@@ -562,6 +562,149 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
   u32x4 v = *reinterpret_cast<const u32x4*>(H + i);
   if (g[m] == 0.f) v = u32x4{0u, 0u, 0u, 0u};
   *reinterpret_cast<u32x4*>(Hs + i) = v;
+}
+
+// ---------------------------------------------------------------------------------------
+// Union-column part of the backward, computed beside the dense part -g p:
+//   dH_u = G W_U,  dW_u = G^T Hs,  db_u = column sums of G
+// (scatter_U(G) of Eq. vjp taken through the two products).  G is split into bf16 hi + lo
+// halves laid side by side, Gb = [hi | lo] (K' = 2 ldK columns), so the matrix cores carry
+// G to about 16 bits: dH_u is one product against [W_U; W_U], dW_u two row blocks that are
+// summed when merged into dW.
+// ---------------------------------------------------------------------------------------
+__global__ void __launch_bounds__(256)
+union_split_bf16(const float* __restrict__ G, int ldG, int K_max, int ldK, int M, uint16_t* __restrict__ Gb) {
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
+  if (i >= static_cast<int64_t>(M) * ldK) return;
+  const int m = static_cast<int>(i / ldK), j = static_cast<int>(i % ldK);
+  const float x = (j < K_max) ? G[static_cast<int64_t>(m) * ldG + j] : 0.f;
+  const uint16_t hi = f32_to_bf16(x);
+  const uint16_t lo = f32_to_bf16(x - bf16_to_f32(hi));
+  uint16_t* row = Gb + static_cast<int64_t>(m) * (2 * ldK);
+  row[j] = hi;
+  row[ldK + j] = lo;
+}
+
+// WU2 [2 ldK][D]: rows j and ldK + j hold W[U_j] for j < K, zeros otherwise.
+__global__ void __launch_bounds__(256)
+union_rows_bf16(const uint16_t* __restrict__ W, int D, const int32_t* __restrict__ u_ids,
+                const int32_t* __restrict__ Kdev, int ldK, uint16_t* __restrict__ WU2) {
+  const int r = blockIdx.x;
+  const int j = r % ldK;
+  const bool live = j < *Kdev;
+  const uint16_t* src = live ? W + static_cast<int64_t>(u_ids[j]) * D : nullptr;
+  for (int d = threadIdx.x * 8; d < D; d += 256 * 8) {
+    const u32x4 v = live ? *reinterpret_cast<const u32x4*>(src + d) : u32x4{0u, 0u, 0u, 0u};
+    *reinterpret_cast<u32x4*>(WU2 + static_cast<int64_t>(r) * D + d) = v;
+  }
+}
+
+// dbp[z][j] = sum of G[m][j] over the frames of slice z (fp32, in frame order)
+__global__ void __launch_bounds__(256)
+union_colsum_bf16(const float* __restrict__ G, int ldG, int M, int K_max, int mper, float* __restrict__ dbp) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  const int z = blockIdx.y;
+  if (j >= K_max) return;
+  const int mb = z * mper, me = min(M, mb + mper);
+  float acc = 0.f;
+  for (int m = mb; m < me; ++m) acc += G[static_cast<int64_t>(m) * ldG + j];
+  dbp[static_cast<int64_t>(z) * K_max + j] = acc;
+}
+
+// dW[U_j, :] += dW_u2[j, :] + dW_u2[ldK + j, :];  db[U_j] += sum_z dbp[z][j]
+__global__ void __launch_bounds__(256)
+union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u_ids, int D, int ldK, int K_max,
+                 int nz, const float* __restrict__ dWu2, const float* __restrict__ dbp, float* __restrict__ dW,
+                 float* __restrict__ db) {
+  const int j = blockIdx.y;
+  if (j >= *Kdev) return;
+  const int v = u_ids[j];
+  const int d = blockIdx.x * 256 + threadIdx.x;
+  if (dW && d < D)
+    dW[static_cast<int64_t>(v) * D + d] +=
+        dWu2[static_cast<int64_t>(j) * D + d] + dWu2[static_cast<int64_t>(ldK + j) * D + d];
+  if (db && blockIdx.x == 0 && threadIdx.x == 0) {
+    float s = 0.f;
+    for (int z = 0; z < nz; ++z) s += dbp[static_cast<int64_t>(z) * K_max + j];
+    db[v] += s;
+  }
+}
+
+namespace {
+constexpr int kColSlices = 16;
+struct UnionCorrLayout {
+  int ldK;
+  size_t o_dwu, o_gb, o_wu, o_hs, o_dbp, total;
+};
+UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
+  UnionCorrLayout L;
+  L.ldK = (K_max + 7) / 8 * 8;
+  const size_t k2 = static_cast<size_t>(2) * L.ldK;
+  L.o_dwu = align_up(static_cast<size_t>(M) * D * sizeof(float), 256);                   // after dH_u
+  L.o_gb = L.o_dwu + align_up(k2 * D * sizeof(float), 256);
+  L.o_wu = L.o_gb + align_up(static_cast<size_t>(M) * k2 * sizeof(uint16_t), 256);
+  L.o_hs = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
+  L.o_dbp = L.o_hs + align_up(static_cast<size_t>(M) * D * sizeof(uint16_t), 256);
+  L.total = L.o_dbp + align_up(static_cast<size_t>(kColSlices) * K_max * sizeof(float), 256);
+  return L;
+}
+}  // namespace
+
+size_t union_corr_bytes(int M, int D, int K_max) { return union_corr_layout(M, D, K_max).total; }
+
+hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, int M, int D,
+                                  bool want_dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
+                                  hipStream_t stream) {
+  *dH_u = nullptr;
+  if (M <= 0 || K_max <= 0) return hipSuccess;
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max);
+  char* sc = static_cast<char*>(scratch);
+  const int k2 = 2 * L.ldK;
+  uint16_t* Gb = reinterpret_cast<uint16_t*>(sc + L.o_gb);
+  if (want_dH || want_dW) {
+    Prof pr("union_prep", stream);
+    const int64_t n = static_cast<int64_t>(M) * L.ldK;
+    hipLaunchKernelGGL(union_split_bf16, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, G, ldG,
+                       K_max, L.ldK, M, Gb);
+  }
+  if (want_dH) {
+    uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
+    hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, L.ldK, WU2);
+    *dH_u = reinterpret_cast<float*>(sc);
+    const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    Prof pr("union_dh", stream);
+    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles), dim3(GDh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2, k2,
+                       *dH_u);
+  }
+  if (want_dW) {
+    uint16_t* Hs2 = reinterpret_cast<uint16_t*>(sc + L.o_hs);
+    hipError_t e = launch_hs_build_bf16(H, M, D, g, Hs2, stream);
+    if (e != hipSuccess) return e;
+    const int grid = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    Prof pr("union_dw", stream);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,
+                       reinterpret_cast<float*>(sc + L.o_dwu));
+  }
+  if (want_db) {
+    const int mper = (M + kColSlices - 1) / kColSlices;
+    Prof pr("union_colsum", stream);
+    hipLaunchKernelGGL(union_colsum_bf16, dim3((K_max + 255) / 256, kColSlices), dim3(256), 0, stream, G, ldG, M,
+                       K_max, mper, reinterpret_cast<float*>(sc + L.o_dbp));
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
+                                   float* db, void* scratch, hipStream_t stream) {
+  if (M <= 0 || K_max <= 0 || (!dW && !db)) return hipSuccess;
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max);
+  char* sc = static_cast<char*>(scratch);
+  Prof pr("union_merge", stream);
+  hipLaunchKernelGGL(union_merge_bf16, dim3((D + 255) / 256, K_max), dim3(256), 0, stream, Kdev, u_ids, D, L.ldK,
+                     K_max, kColSlices, reinterpret_cast<const float*>(sc + L.o_dwu),
+                     reinterpret_cast<const float*>(sc + L.o_dbp), dW, db);
+  return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------------------

@@ -100,8 +100,8 @@ struct Layout {
   bool pruned;
   DpPlan dp;
   BwdPlan bwd;
-  size_t o_remap, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_dp, o_bwd,
-      total;
+  size_t o_remap, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_gpred, o_pred,
+      o_corr, o_dp, o_bwd, total;
 };
 
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
@@ -153,6 +153,11 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.o_S = take(static_cast<size_t>(L.M) * L.ldS * 4);
   L.o_G = take(static_cast<size_t>(L.M) * L.ldS * 4);
   L.o_g = take(static_cast<size_t>(L.M) * 4);
+  if (dtype == PCTC_BF16) {  // the overlapped schedule: forecast g and the union-column part
+    L.o_gpred = take(static_cast<size_t>(L.M) * 4);
+    L.o_pred = take(static_cast<size_t>(N) * 4);
+    L.o_corr = take(union_corr_bytes(L.M, D, L.K_max));
+  }
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
   L.total = o;
@@ -181,6 +186,28 @@ static hipError_t upload_offsets(const DpPlan& dp, char* dpbase, const std::vect
   e = hipMemcpyAsync(dpbase + dp.off_yoff, yoff.data(), yoff.size() * 4, hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return e;
   return hipMemcpyAsync(dpbase + dp.off_soff, soff.data(), soff.size() * 8, hipMemcpyHostToDevice, stream);
+}
+
+// A second stream per device for the lattice stage, which runs beside the dense part of the
+// backward.  Created once (default priority, non-blocking), kept until the process ends.
+static hipError_t side_stream(hipStream_t* out) {
+  static std::mutex mu;
+  static std::map<int, hipStream_t> streams;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = streams.find(dev);
+  if (it != streams.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  hipStream_t st = nullptr;
+  e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+  if (e != hipSuccess) return e;
+  streams[dev] = st;
+  *out = st;
+  return hipSuccess;
 }
 
 }  // namespace pctc
@@ -270,23 +297,69 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
   PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
   PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
+  const bool want_bwd = (dH || dW || db);
+  int32_t* fflag = Kdev + 2;  // forecast mismatch flag
+  const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
+  hipStream_t dps_stream = stream;
+  struct Events {
+    hipEvent_t fork = nullptr, join = nullptr;
+    ~Events() {
+      if (fork) hipEventDestroy(fork);
+      if (join) hipEventDestroy(join);
+    }
+  } ev;
+  float* g_pred = nullptr;
+  if (overlap) {
+    // Dense part -g p of the backward beside the lattice: g is forecast (-w_n on included
+    // utterances), the lattice runs on a second stream, and the union columns' part (from its
+    // G) is added once both are done.  A wrong forecast (rare: a -inf logit on a selected
+    // class) is caught and the backward is redone in the plain order.
+    g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
+    int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
+    PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, lam, utt_weight, g_pred, pred, stream));
+    PCTC_HIP(side_stream(&dps_stream));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
+    PCTC_HIP(hipEventRecord(ev.fork, stream));
+    PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
+  }
   // lattice, total scores, zeroing of nonfinite losses, G = dL/dS
   PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status, G, g,
-                         nullptr, dps, L.K_max, stream, nullptr));
-  PCTC_HIP(launch_loss_reduce(N, loss_n, status, utt_weight, loss, stream));
+                         nullptr, dps, L.K_max, dps_stream, nullptr));
+  PCTC_HIP(launch_loss_reduce(N, loss_n, status, utt_weight, loss, dps_stream));
   if (loss_per_utt && N > 0)
-    PCTC_HIP(hipMemcpyAsync(loss_per_utt, loss_n, N * sizeof(double), hipMemcpyDeviceToDevice, stream));
+    PCTC_HIP(hipMemcpyAsync(loss_per_utt, loss_n, N * sizeof(double), hipMemcpyDeviceToDevice, dps_stream));
   if (utt_status && N > 0)
-    PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, stream));
-  // backward: chunk by chunk recomputation
-  if (dH || dW || db)
+    PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, dps_stream));
+  if (overlap) {
+    PCTC_HIP(launch_forecast_check(N, status, utt_weight, reinterpret_cast<int32_t*>(ws + L.o_pred), fflag,
+                                   dps_stream));
+    // the union columns' part of the backward, from the lattice's G, still beside the dense part
+    float* dH_u = nullptr;
+    PCTC_HIP(launch_union_part_bf16(G, L.ldS, g, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
+                                    static_cast<const uint16_t*>(H), L.M, D, dH != nullptr, dW != nullptr,
+                                    db != nullptr, ws + L.o_corr, &dH_u, dps_stream));
+    PCTC_HIP(hipEventRecord(ev.join, dps_stream));
+    // dense part, chunk by chunk, on the caller's stream; its final dH reduction adds dH_u
+    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, nullptr, L.ldS, g_pred, nullptr, nullptr, L.ldS, dH, dW,
+                             db, bws, L.bwd, stream, dH_u, ev.join));
+    PCTC_HIP(hipStreamWaitEvent(stream, ev.join, 0));
+    PCTC_HIP(launch_union_merge_bf16(Kdev, L.K_max, u_ids, L.M, D, dW, db, ws + L.o_corr, stream));
+  } else if (want_bwd) {
+    // backward: chunk by chunk recomputation
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
                              stream));
-  int32_t herr = 0;
-  PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+  }
+  int32_t hflags[2] = {0, 0};  // label error, forecast mismatch
+  PCTC_HIP(hipMemcpyAsync(hflags, err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
+  if (overlap && hflags[1] && !hflags[0]) {
+    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
+                             stream));
+    PCTC_HIP(hipStreamSynchronize(stream));
+  }
   prof_flush();
-  if (herr) return PCTC_ELABEL;
+  if (hflags[0]) return PCTC_ELABEL;
   return PCTC_OK;
 }
 

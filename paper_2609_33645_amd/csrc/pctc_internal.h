@@ -58,11 +58,14 @@ struct BwdPlan {
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int chunk);
 // S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
-// of each recomputed chunk from them).
+// of each recomputed chunk from them).  remap == null (bf16 path): the dense part -g p only.
+// dH_extra (bf16 path, may be null): [M][D] added to dH by the final reduction, which
+// first waits for before_reduce when that is not null.
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                            const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                            const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
-                           const BwdPlan& plan, hipStream_t stream);
+                           const BwdPlan& plan, hipStream_t stream, const float* dH_extra = nullptr,
+                           hipEvent_t before_reduce = nullptr);
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
 
 // ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
@@ -76,6 +79,16 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
                                  hipStream_t stream);
+// Union-column part of the backward (bf16 path), into its own buffers: dH_u = G W_U [M][D],
+// dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left out;
+// then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch: union_corr_bytes().
+size_t union_corr_bytes(int M, int D, int K_max);
+hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, int M, int D,
+                                  bool want_dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
+                                  hipStream_t stream);
+hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
+                                   float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
 
 // ---- grouped logits for a stock CTC (grouped_head.hip) ----------------------------------
@@ -112,5 +125,13 @@ hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, co
                                  int nbeams, double* delta, void* scratch, int K_max, hipStream_t stream);
 hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status, const float* weight, double* loss,
                               hipStream_t stream);
+// Forecast of g before the lattice runs: g_pred[m] = -w_n on utterances whose targets fit
+// their frames and whose normalisers are finite (and w_n != 0), else 0; pred[n] = 1/0.
+// Needs the offsets uploaded into the lattice scratch.
+hipError_t launch_g_forecast(const DpPlan& plan, void* scratch, const int32_t* y_rel, const double* lam,
+                             const float* weight, float* g_pred, int32_t* pred, hipStream_t stream);
+// flag[0] = 1 when the lattice's inclusions differ from the forecast.
+hipError_t launch_forecast_check(int N, const int32_t* status, const float* weight, const int32_t* pred,
+                                 int32_t* flag, hipStream_t stream);
 
 }  // namespace pctc

@@ -523,3 +523,32 @@ def test_grouped_edges():
             prunedctc.grouped_logprobs(torch.from_numpy(H).cuda(), torch.from_numpy(W).cuda(),
                                        torch.tensor(bad, dtype=torch.int32, device="cuda"))
         assert e.value.code == -2
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_e2e_forecast_miss(dtype):
+    """A -inf bias on one target label makes its utterance's loss infinite (status 2) although
+    every normaliser is finite: the bf16 schedule's forecast of g is wrong for that utterance
+    and the backward must still match the oracle (which excludes it)."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(70, N=4, T_range=(30, 120), D=64, V=500, dtype=dtype, p_repeat=0.1, w_std=0.5)
+    b = np.zeros(wl.V, np.float32)
+    lab = int(wl.targets[wl.target_lengths[0] + 1])   # a label of utterance 1
+    b[lab] = -np.inf
+    say(f"forecast miss {dtype} label={lab} M={wl.M}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank,
+                         bias=b.astype(np.float64))
+    assert ref["status"][1] == 2
+    H, W, y = to_dev(wl)
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, math.inf,
+                                       bias=torch.from_numpy(b).cuda(), want_db=True)
+    np.testing.assert_array_equal(out["status"].cpu().numpy(), ref["status"])
+    assert loss_rel(float(out["loss"].item()), ref["loss"]) <= 1e-5
+    for name in ("dH", "dW", "db"):
+        got = out[name].cpu().numpy()
+        assert np.isfinite(got).all(), name
+        if dtype == "f32":
+            assert rel_err(got, ref[name]) <= 1e-4, name
+        else:
+            assert cosine(got, ref[name]) >= 0.99999, name
