@@ -446,21 +446,26 @@ __global__ void dp_mask_kernel(const float* __restrict__ S, int ldS, const int32
 
 // ---------------------------------------------------------------------------------------
 
-constexpr int kOccThreads = 256;
+constexpr int kOccFrames = 4;  // frames per block, one wavefront each
 
-__global__ void __launch_bounds__(kOccThreads)
+// One wavefront per frame (no block barriers: a wavefront's LDS accesses are performed in
+// program order, and the fence keeps the compiler from reordering them).
+__global__ void __launch_bounds__(64 * kOccFrames)
 dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ yoff,
                     const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
                     const int32_t* __restrict__ frame_utt, const int32_t* __restrict__ status,
                     const int32_t* __restrict__ dup_next, const int32_t* __restrict__ dup_first,
                     const float* __restrict__ fa, const float* __restrict__ fb, const double* __restrict__ sfa,
                     const double* __restrict__ sfb, const double* __restrict__ logp,
-                    const float* __restrict__ weight, float* __restrict__ G, int ldG, float* __restrict__ g) {
-  extern __shared__ float gam[];  // [Smax]
-  __shared__ float red[kOccThreads];
-  const int m = blockIdx.x;
+                    const float* __restrict__ weight, float* __restrict__ G, int ldG, float* __restrict__ g, int M,
+                    int Smax) {
+  extern __shared__ float gam_all[];  // [kOccFrames][Smax]
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int m = blockIdx.x * kOccFrames + wv;
+  if (m >= M) return;
   const int n = frame_utt[m];
   if (status[n] != 0) return;  // G row stays zero, g stays zero
+  float* gam = gam_all + wv * Smax;
   const int t0 = toff[n];
   const int t = m - t0;
   const int y0 = yoff[n], U = yoff[n + 1] - y0;
@@ -468,17 +473,18 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
   const int64_t rowb = soff[n] + static_cast<int64_t>(t) * Sp;
   const float off = static_cast<float>(sfa[m] + sfb[m] - logp[n]);
   const float w = weight ? weight[n] : 1.f;  // loss weight of the utterance: G = -w gamma
-  for (int s = threadIdx.x; s < Sp; s += kOccThreads) {
+  for (int s = lane; s < Sp; s += 64) {
     const float x = fa[rowb + s] + fb[rowb + s] + off;
     gam[s] = fast_exp2(x * kLog2e);
   }
-  __syncthreads();
-  // blank column: sum over even states (fixed-order per thread, then tree)
+  __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  // blank column: sum over even states (fixed order per lane, then across lanes)
   float bsum = 0.f;
-  for (int s = 2 * threadIdx.x; s < Sp; s += 2 * kOccThreads) bsum += gam[s];
+  for (int s = 2 * lane; s < Sp; s += 128) bsum += gam[s];
   // label columns: the first occurrence of each label sums its states in target order
   float lsum = 0.f;
-  for (int i = threadIdx.x; i < U; i += kOccThreads) {
+  for (int i = lane; i < U; i += 64) {
     if (!dup_first[y0 + i]) continue;
     float acc = gam[2 * i + 1];
     int j = dup_next[y0 + i];
@@ -489,23 +495,11 @@ dp_occupancy_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict_
     G[static_cast<int64_t>(m) * ldG + y_rel[y0 + i]] = -w * acc;
     lsum += acc;
   }
-  red[threadIdx.x] = bsum;
-  __syncthreads();
-  for (int o = kOccThreads / 2; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
-  }
-  const float blank_total = red[0];
-  __syncthreads();
-  red[threadIdx.x] = lsum;
-  __syncthreads();
-  for (int o = kOccThreads / 2; o > 0; o >>= 1) {
-    if (threadIdx.x < o) red[threadIdx.x] += red[threadIdx.x + o];
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
+  const float blank_total = wave_sum(bsum);
+  const float label_total = wave_sum(lsum);
+  if (lane == 0) {
     G[static_cast<int64_t>(m) * ldG + 0] = -w * blank_total;
-    g[m] = -w * (blank_total + red[0]);
+    g[m] = -w * (blank_total + label_total);
   }
 }
 
@@ -688,9 +682,10 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   }
   if (plan.M > 0) {
     Prof pr("dp_occupancy", stream);
-    hipLaunchKernelGGL(dp_occupancy_kernel, dim3(plan.M), dim3(kOccThreads), plan.Smax * sizeof(float), stream,
-                       toff, yoff, soff, y_rel, frame_utt, status, dnext, dfirst, tfa, tfb, sfa, sfb, logp, weight, G,
-                       ldS, g);
+    hipLaunchKernelGGL(dp_occupancy_kernel, dim3((plan.M + kOccFrames - 1) / kOccFrames), dim3(64 * kOccFrames),
+                       static_cast<size_t>(kOccFrames) * plan.Smax * sizeof(float), stream, toff, yoff, soff, y_rel,
+                       frame_utt, status, dnext, dfirst, tfa, tfb, sfa, sfb, logp, weight, G, ldS, g, plan.M,
+                       plan.Smax);
   }
   if (keep_mask_out && mask && plan.lattice > 0) {
     e = hipMemcpyAsync(keep_mask_out, mask, plan.lattice, hipMemcpyDeviceToDevice, stream);

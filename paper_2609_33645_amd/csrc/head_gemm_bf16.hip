@@ -57,19 +57,31 @@ __device__ __forceinline__ int xcd_swz(int bid, int nblocks) {
   return (bid % 8) * (full / 8) + bid / 8;
 }
 
-// Tile order for an nA x nB grid of output tiles: consecutive work ids walk 8 x 8 groups
-// (a fastest), so the workgroups resident on one XCD at a time share a few rows of A
-// tiles and B tiles in that XCD's L2.  Grid = groupsA * groupsB * 64; ids past the
-// edge return false.
-constexpr int kGrp = 8;
+// Tile order for an nA x nB grid of output tiles, A = frame tiles (few), B = vocabulary
+// tiles or partitions (many).  Consecutive work ids walk groups of ga x gb tiles (a
+// fastest) with about 64 tiles per group (what one XCD runs at a time) and ga ~ 11 frame
+// tiles; the groups walk the frame groups fastest, so the few groups that cover every frame
+// tile of a run of vocabulary rows are consecutive: that XCD fetches the rows once and the
+// frame tiles (the small operand) stay in its L2.  Grid = ceil(nA/ga) ga * ceil(nB/gb) gb;
+// ids past the edge return false.
+__host__ __device__ __forceinline__ void group_shape(int nA, int& ga, int& gb) {
+  const int groups = (nA + 10) / 11;
+  ga = (nA + groups - 1) / groups;
+  gb = 64 / ga;
+  if (gb < 1) gb = 1;
+}
 __host__ __device__ __forceinline__ int grouped_grid(int nA, int nB) {
-  return ((nA + kGrp - 1) / kGrp) * ((nB + kGrp - 1) / kGrp) * kGrp * kGrp;
+  int ga, gb;
+  group_shape(nA, ga, gb);
+  return ((nA + ga - 1) / ga) * ga * ((nB + gb - 1) / gb) * gb;
 }
 __device__ __forceinline__ bool grouped_tile(int work, int nA, int nB, int& a, int& b) {
-  const int gA = (nA + kGrp - 1) / kGrp;
-  const int blk = work / (kGrp * kGrp), in = work % (kGrp * kGrp);
-  a = (blk % gA) * kGrp + in % kGrp;
-  b = (blk / gA) * kGrp + in / kGrp;
+  int ga, gb;
+  group_shape(nA, ga, gb);
+  const int gA = (nA + ga - 1) / ga;
+  const int blk = work / (ga * gb), in = work % (ga * gb);
+  a = (blk % gA) * ga + in % ga;
+  b = (blk / gA) * gb + in / ga;
   return a < nA && b < nB;
 }
 
