@@ -189,18 +189,24 @@ constexpr int prefetch_depth() {
 // Tables hold scores minus a per-frame offset (rounded to float once); the offsets are
 // kept per frame in double.  Emissions and arc flags for the next PF frames are held in
 // a register ring so that the gathers are issued well before they are needed.
+// kPassWaves wavefronts per workgroup (independent; no barriers), so that the few
+// wavefronts of this latency-bound stage occupy few compute units.
+constexpr int kPassWaves = 4;
+
 template <int Q, bool VIT>
-__global__ void __launch_bounds__(64)
+__global__ void __launch_bounds__(64 * kPassWaves)
 dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
                const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
                int32_t* __restrict__ status, const uint8_t* __restrict__ mask, float* __restrict__ tab_f,
                float* __restrict__ tab_b, double* __restrict__ sc_f, double* __restrict__ sc_b,
-               double* __restrict__ total_out, double* __restrict__ loss_n) {
+               double* __restrict__ total_out, double* __restrict__ loss_n, int N) {
   using Acc = typename std::conditional<VIT, float, double>::type;
   constexpr int PF = prefetch_depth<Q>();
-  const int n = blockIdx.x;
-  const int dir = blockIdx.y;
-  const int lane = threadIdx.x;
+  const int unit = blockIdx.x * kPassWaves + (threadIdx.x >> 6);  // (utterance, direction)
+  if (unit >= 2 * N) return;
+  const int n = unit >> 1;
+  const int dir = unit & 1;
+  const int lane = threadIdx.x & 63;
   if (status[n] != 0) return;
   const int t0 = toff[n], T = toff[n + 1] - t0;
   const int y0 = yoff[n], U = yoff[n + 1] - y0;
@@ -584,15 +590,16 @@ hipError_t launch_forecast_check(int N, const int32_t* status, const float* weig
 // ---------------------------------------------------------------------------------------
 
 template <bool VIT>
-static hipError_t launch_pass(int Q, dim3 grid, hipStream_t stream, const float* S, int ldS, const int32_t* toff,
+static hipError_t launch_pass(int Q, int N, hipStream_t stream, const float* S, int ldS, const int32_t* toff,
                               const int32_t* yoff, const int64_t* soff, const int32_t* y_rel, int32_t* status,
                               const uint8_t* mask, float* tf, float* tb, double* sf, double* sb, double* total,
                               double* loss_n) {
 #define PCTC_PASS(QQ)                                                                                       \
   case QQ:                                                                                                  \
-    hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT>), grid, dim3(64), 0, stream, S, ldS, toff, yoff, soff, y_rel, \
-                       status, mask, tf, tb, sf, sb, total, loss_n);                                        \
+    hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT>), grid, dim3(64 * kPassWaves), 0, stream, S, ldS, toff, yoff, \
+                       soff, y_rel, status, mask, tf, tb, sf, sb, total, loss_n, N);                        \
     break;
+  const dim3 grid((2 * N + kPassWaves - 1) / kPassWaves);
   switch (Q) {
     PCTC_PASS(1)
     PCTC_PASS(2)
@@ -664,7 +671,7 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
     mask = reinterpret_cast<uint8_t*>(sc + plan.off_mask);
     {
       Prof pr("dp_viterbi", stream);
-      e = launch_pass<true>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva,
+      e = launch_pass<true>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva,
                             svb, vbest, loss_n);
       if (e != hipSuccess) return e;
     }
@@ -676,7 +683,7 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   }
   {
     Prof pr("dp_alpha_beta", stream);
-    e = launch_pass<false>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, mask, tfa, tfb, sfa, sfb,
+    e = launch_pass<false>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, mask, tfa, tfb, sfa, sfb,
                            logp, loss_n);
     if (e != hipSuccess) return e;
   }
@@ -876,7 +883,7 @@ hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, co
     hipError_t e;
     {
       Prof pr("dp_viterbi", stream);
-      e = launch_pass<true>(Q, dim3(N, 2), stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva, svb,
+      e = launch_pass<true>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva, svb,
                             vbest, loss_n);
       if (e != hipSuccess) return e;
     }

@@ -534,23 +534,31 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
     }
 }
 
+// dW[c0 + v][:] = sum over frames of dZ[m][v] Hs[m][:].  With nz > 1 the frames are split
+// into nz slices of mslice frames and slice z writes its partial sums at dW + z * zstride.
 __global__ void __launch_bounds__(512, 1)
 dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ Hs, int D, int c0, int cw,
-             float* __restrict__ dW) {
+             float* __restrict__ dW, int nz, int mslice, int64_t zstride) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES4(G)
   const int nDt = (D + kBC - 1) / kBC;
+  const int nVt = (cw + kBR - 1) / kBR;
   const int work = xcd_swz(blockIdx.x, gridDim.x);
   const int dt = work % nDt;
-  const int vt = work / nDt;
+  const int vt = (work / nDt) % nVt;
+  const int z = work / (nDt * nVt);
   const int v0 = vt * kBR, d0 = dt * kBC;
+  const int mb = z * mslice;
+  const int mlen = min(M - mb, mslice);
+  if (z >= nz || mlen <= 0) return;
+  dW += static_cast<int64_t>(z) * zstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // A: dZ viewed as rows v (columns of dZ), k = frame; B: Hs viewed as rows d, k = frame
-  const GOp A{dZ, chunk, cw, M, nullptr};
-  const GOp B{Hs, D, D, M, nullptr};
+  const GOp A{dZ + static_cast<int64_t>(mb) * chunk, chunk, cw, mlen, nullptr};
+  const GOp B{Hs + static_cast<int64_t>(mb) * D, D, D, mlen, nullptr};
   f32x16 acc[FR][FC];
-  G::run(A, B, v0, d0, 0, M, st, acc);
+  G::run(A, B, v0, d0, 0, mlen, st, acc);
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
@@ -623,18 +631,24 @@ union_colsum_bf16(const float* __restrict__ G, int ldG, int M, int K_max, int mp
   dbp[static_cast<int64_t>(z) * K_max + j] = acc;
 }
 
-// dW[U_j, :] += dW_u2[j, :] + dW_u2[ldK + j, :];  db[U_j] += sum_z dbp[z][j]
+// dW[U_j, :] += sum over the frame slices of dW_u2[j, :] + dW_u2[ldK + j, :];
+// db[U_j] += sum_z dbp[z][j]
 __global__ void __launch_bounds__(256)
 union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u_ids, int D, int ldK, int K_max,
-                 int nz, const float* __restrict__ dWu2, const float* __restrict__ dbp, float* __restrict__ dW,
+                 int nz, int nzw, const float* __restrict__ dWu2, const float* __restrict__ dbp, float* __restrict__ dW,
                  float* __restrict__ db) {
   const int j = blockIdx.y;
   if (j >= *Kdev) return;
   const int v = u_ids[j];
   const int d = blockIdx.x * 256 + threadIdx.x;
-  if (dW && d < D)
-    dW[static_cast<int64_t>(v) * D + d] +=
-        dWu2[static_cast<int64_t>(j) * D + d] + dWu2[static_cast<int64_t>(ldK + j) * D + d];
+  if (dW && d < D) {
+    float s = 0.f;
+    for (int z = 0; z < nzw; ++z) {
+      const float* p = dWu2 + static_cast<int64_t>(z) * 2 * ldK * D;
+      s += p[static_cast<int64_t>(j) * D + d] + p[static_cast<int64_t>(ldK + j) * D + d];
+    }
+    dW[static_cast<int64_t>(v) * D + d] += s;
+  }
   if (db && blockIdx.x == 0 && threadIdx.x == 0) {
     float s = 0.f;
     for (int z = 0; z < nz; ++z) s += dbp[static_cast<int64_t>(z) * K_max + j];
@@ -645,15 +659,22 @@ union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u
 namespace {
 constexpr int kColSlices = 16;
 struct UnionCorrLayout {
-  int ldK;
+  int ldK, nz, mslice;  // nz slices of mslice frames for the dW_u product (summed when merged)
   size_t o_dwu, o_gb, o_wu, o_hs, o_dbp, total;
 };
 UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   UnionCorrLayout L;
   L.ldK = (K_max + 7) / 8 * 8;
   const size_t k2 = static_cast<size_t>(2) * L.ldK;
+  const int tiles = static_cast<int>((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+  L.nz = 64 / tiles;  // a short, wide launch beside the dense part
+  if (L.nz > (M + 255) / 256) L.nz = (M + 255) / 256;
+  if (L.nz < 1) L.nz = 1;
+  L.mslice = ((M + L.nz - 1) / L.nz + 63) / 64 * 64;
+  L.nz = (M + L.mslice - 1) / L.mslice;  // every slice holds frames
+  if (L.nz < 1) L.nz = 1;
   L.o_dwu = align_up(static_cast<size_t>(M) * D * sizeof(float), 256);                   // after dH_u
-  L.o_gb = L.o_dwu + align_up(k2 * D * sizeof(float), 256);
+  L.o_gb = L.o_dwu + align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256);
   L.o_wu = L.o_gb + align_up(static_cast<size_t>(M) * k2 * sizeof(uint16_t), 256);
   L.o_hs = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
   L.o_dbp = L.o_hs + align_up(static_cast<size_t>(M) * D * sizeof(uint16_t), 256);
@@ -693,10 +714,10 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
     uint16_t* Hs2 = reinterpret_cast<uint16_t*>(sc + L.o_hs);
     hipError_t e = launch_hs_build_bf16(H, M, D, g, Hs2, stream);
     if (e != hipSuccess) return e;
-    const int grid = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dw", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,
-                       reinterpret_cast<float*>(sc + L.o_dwu));
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,
+                       reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice, static_cast<int64_t>(k2) * D);
   }
   if (want_db) {
     const int mper = (M + kColSlices - 1) / kColSlices;
@@ -714,7 +735,7 @@ hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t
   char* sc = static_cast<char*>(scratch);
   Prof pr("union_merge", stream);
   hipLaunchKernelGGL(union_merge_bf16, dim3((D + 255) / 256, K_max), dim3(256), 0, stream, Kdev, u_ids, D, L.ldK,
-                     K_max, kColSlices, reinterpret_cast<const float*>(sc + L.o_dwu),
+                     K_max, kColSlices, L.nz, reinterpret_cast<const float*>(sc + L.o_dwu),
                      reinterpret_cast<const float*>(sc + L.o_dbp), dW, db);
   return hipGetLastError();
 }
@@ -816,7 +837,8 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("dw_gemm", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW, 1, M,
+                       static_cast<int64_t>(0));
   }
   return hipGetLastError();
 }
