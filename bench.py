@@ -148,7 +148,10 @@ def aux_figures(wl, K: int, kernel_ms):
         # alpha and beta passes read each frame's U_n + 1 scores; tables written once per pass
         b = 2 * sum(int(t) * (int(u) + 1) * 4 + int(t) * (2 * int(u) + 1) * 4 for t, u in zip(T, U))
         out["dp_ms"] = round(dp_ms, 4)
+        # in the bf16 schedule the lattice runs on a second stream beside the dense backward,
+        # so this is a share of summed kernel time, not of the step
         out["dp_share_of_kernel_time"] = round(dp_ms / tot, 4)
+        out["dp_beside_backward"] = wl.dtype == "bf16"
         out["dp_alpha_beta_gbs"] = round(b / (kernel_ms.get("dp_alpha_beta", dp_ms) * 1e-3) / 1e9, 2)
     return out
 
