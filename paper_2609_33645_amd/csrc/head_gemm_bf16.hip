@@ -466,7 +466,10 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
       const int mm = m0 + 64 * half + 32 * j + row;
       const char* src = (half ? st1_ : st0_) + row * kPitch + vec * 16;
       const u32x4 v = *reinterpret_cast<const u32x4*>(src);
-      if (mm < M) *reinterpret_cast<u32x4*>(dZ + static_cast<int64_t>(mm) * chunk + vl0 + vec * 8) = v;
+      // streaming store: dZ is read back only by the next two products, and keeping its
+      // lines out of the caches leaves them to those products' operands
+      if (mm < M)
+        __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dZ + static_cast<int64_t>(mm) * chunk + vl0 + vec * 8));
     }
   }
   if (DB) dbpart[static_cast<int64_t>(mt) * chunk + vl0 + tid] = dbsum;
