@@ -383,7 +383,7 @@ def main():
         "dtype": wl.dtype,
         "data": "synthetic (seeded; shapes of the paper's workloads, no corpus data)",
         "config": {"workload": wl.name, "N": wl.N, "M": M, "D": D, "V": V, "K": K, "beam": wl.beam,
-                   "chunk": prunedctc.bwd_chunk(1 if wl.dtype == "bf16" else 0, M, D, a.chunk), "seed": a.seed, "dW": not a.frozen_head},
+                   "chunk": prunedctc.bwd_chunk(1 if wl.dtype == "bf16" else 0, M, D, V, a.chunk), "seed": a.seed, "dW": not a.frozen_head},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom)},
         "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),

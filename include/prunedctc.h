@@ -219,11 +219,12 @@ int32_t pctc_discarded_mass(const float* S, int32_t ldS, int32_t K_max, const in
  * int32 [V] from pctc_union_remap.  dH and/or dW may be NULL.
  * bwd_scratch: device scratch of pctc_bwd_scratch_bytes() bytes (ldG: the row pitch of G,
  * at least the union size K). */
-size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ldG, int32_t chunk);
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t ldG,
+                              int32_t chunk);
 /* Vocabulary columns per backward step that a call with this chunk argument uses (0 picks
- * the default: about 512 MiB of recomputed gradient, rounded to whole launch waves).
- * Returns 0 for invalid arguments. */
-int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk);
+ * the default: the fewest chunks that keep the recomputed gradient within about 512 MiB,
+ * made equal and rounded up to a multiple of 256).  Returns 0 for invalid arguments. */
+int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t chunk);
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
                       int32_t V, const double* lam, const float* G, int32_t ldG, const float* g,
                       const int32_t* remap, int32_t chunk, float* dH, float* dW, void* bwd_scratch,

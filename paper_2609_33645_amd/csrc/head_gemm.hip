@@ -620,28 +620,26 @@ __global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int
   dH[i] = s;
 }
 
-BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
+BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
   BwdPlan p{};
+  int cap;  // columns the gradient buffer holds (sizes the workspace; independent of V)
   if (chunk > 0) {
-    p.chunk = chunk;
+    p.chunk = cap = chunk;
   } else {
-    // default: the recomputed gradient chunk (M x chunk in the input dtype) takes about
-    // 512 MiB.  For bf16 the chunk is the nearest multiple of q columns when that is at
-    // least q, where q makes the dW launch (256 x 256 tiles) a whole number of
-    // 256-workgroup waves; otherwise a multiple of 256.
+    // default buffer: M x cap in the input dtype, about 512 MiB (at most 65536 columns);
+    // V is then cut into as few equal chunks (multiples of 256 columns) as fit in it, so
+    // that no launch works on a short remainder
     const size_t es0 = (dtype == 1) ? 2 : 4;
-    size_t c = (static_cast<size_t>(512) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
-    if (c > 65536) c = 65536;
-    size_t q = 4096;
-    if (dtype == 1) {
-      const int ndt = (D + 255) / 256;
-      q = static_cast<size_t>(256) * ((256 + ndt - 1) / ndt);
-    }
-    if (c >= q) c = (c + q / 2) / q * q;
-    else c = (c / 256) * 256;
-    if (c > 65536) c = 65536;
-    if (c < 256) c = 256;
+    size_t cmax = (static_cast<size_t>(512) << 20) / (es0 * static_cast<size_t>(M > 0 ? M : 1));
+    if (cmax > 65536) cmax = 65536;
+    cmax = cmax / 256 * 256;
+    if (cmax < 256) cmax = 256;
+    const size_t v = static_cast<size_t>(V > 0 ? V : 1);
+    const size_t n = (v + cmax - 1) / cmax;
+    size_t c = ((v + n - 1) / n + 255) / 256 * 256;
+    if (c > cmax) c = cmax;
     p.chunk = static_cast<int>(c);
+    cap = static_cast<int>(cmax);
   }
   const size_t es = (dtype == 1) ? 2 : 4;
   const int tr = (dtype == 1) ? 256 : kBwdB;  // dH tile rows of the kernel used
@@ -654,12 +652,12 @@ BwdPlan plan_bwd(int dtype, int M, int D, int chunk) {
   if (splits < 1) splits = 1;
   p.splits = splits;
   p.Mp = ((M + 63) / 64) * 64;
-  p.dz_bytes = align_up(static_cast<size_t>(M) * p.chunk * es, 256);
+  p.dz_bytes = align_up(static_cast<size_t>(M) * cap * es, 256);
   p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);  // >= M x D (bf16 masked copy of H)
   p.part_bytes = align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
   p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
   // bf16: per 128-frame tile column sums of dZ for db
-  p.dbpart_bytes = (dtype == 1) ? align_up(static_cast<size_t>((M + 127) / 128) * p.chunk * sizeof(float), 256) : 0;
+  p.dbpart_bytes = (dtype == 1) ? align_up(static_cast<size_t>((M + 127) / 128) * cap * sizeof(float), 256) : 0;
   p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes + p.dbpart_bytes;
   return p;
 }

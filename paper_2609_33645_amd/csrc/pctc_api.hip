@@ -134,7 +134,7 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.pruned = L.dp.pruned;
   L.K_max = (1 + L.Y < V) ? 1 + L.Y : V;
   L.ldS = static_cast<int>(align_up(static_cast<size_t>(L.K_max), 4));
-  L.bwd = plan_bwd(dtype == PCTC_BF16 ? 1 : 0, L.M, D, chunk);
+  L.bwd = plan_bwd(dtype == PCTC_BF16 ? 1 : 0, L.M, D, V, chunk);
   size_t o = 0;
   auto take = [&](size_t bytes) {
     size_t at = o;
@@ -512,9 +512,9 @@ struct BwdStageLayout {
   BwdPlan plan;
   size_t o_uids, o_K, o_S, total;
 };
-static BwdStageLayout bwd_stage_layout(int dt, int M, int D, int ldG, int chunk) {
+static BwdStageLayout bwd_stage_layout(int dt, int M, int D, int V, int ldG, int chunk) {
   BwdStageLayout b;
-  b.plan = plan_bwd(dt, M, D, chunk);
+  b.plan = plan_bwd(dt, M, D, V, chunk);
   b.o_uids = b.plan.total;
   b.o_K = b.o_uids + align_up(static_cast<size_t>(ldG) * 4, 256);
   b.o_S = b.o_K + 256;
@@ -522,17 +522,18 @@ static BwdStageLayout bwd_stage_layout(int dt, int M, int D, int ldG, int chunk)
   return b;
 }
 
-size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t ldG, int32_t chunk) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || ldG < 1 || chunk < 0 ||
+size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t ldG, int32_t chunk) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || V <= 1 || ldG < 1 || chunk < 0 ||
       (chunk > 0 && chunk % 256))
     return 0;
-  return bwd_stage_layout(dtype == PCTC_BF16 ? 1 : 0, M, D, ldG, chunk).total;
+  return bwd_stage_layout(dtype == PCTC_BF16 ? 1 : 0, M, D, V, ldG, chunk).total;
 }
 
-int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t chunk) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || chunk < 0 || (chunk > 0 && chunk % 256))
+int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t chunk) {
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || V <= 1 || chunk < 0 ||
+      (chunk > 0 && chunk % 256))
     return 0;
-  return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, chunk).chunk;
+  return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, V, chunk).chunk;
 }
 
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
@@ -544,7 +545,7 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
   if (M > 0 && (!H || !lam || !G || !g || !remap)) return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
-  const BwdStageLayout b = bwd_stage_layout(dt, M, D, ldG, chunk);
+  const BwdStageLayout b = bwd_stage_layout(dt, M, D, V, ldG, chunk);
   const BwdPlan& plan = b.plan;
   char* sc = static_cast<char*>(bwd_scratch);
   float2* lam2 = reinterpret_cast<float2*>(sc + plan.dz_bytes + plan.ht_bytes + plan.part_bytes);
@@ -574,7 +575,7 @@ struct GroupedLayout {
 static GroupedLayout grouped_layout(int dt, int M, int D, int V, int K, int chunk) {
   GroupedLayout L;
   const size_t m8 = align_up(static_cast<size_t>(M > 0 ? M : 1) * 8, 256);
-  L.plan = plan_bwd(dt, M, D, chunk);
+  L.plan = plan_bwd(dt, M, D, V, chunk);
   L.o_remap = 256;
   L.o_part = L.o_remap + align_up(static_cast<size_t>(V) * 4, 256);
   L.o_lamo = L.o_part + lse_partial_bytes(M);

@@ -56,7 +56,7 @@ struct BwdPlan {
   int Mp;          // padded frame count (pitch of the transposed head input)
   size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
 };
-BwdPlan plan_bwd(int dtype, int M, int D, int chunk);
+BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
 // S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
 // of each recomputed chunk from them).  remap == null (bf16 path): the dense part -g p only.
 // dH_extra (bf16 path, may be null): [M][D] added to dH by the final reduction, which

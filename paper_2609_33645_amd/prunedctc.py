@@ -78,9 +78,9 @@ def lib() -> ctypes.CDLL:
     L.pctc_discarded_mass.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, ctypes.POINTER(ctypes.c_float), c_i32,
                                       c_p, c_p, c_p]
     L.pctc_discarded_mass.restype = c_i32
-    L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32]
+    L.pctc_bwd_scratch_bytes.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_scratch_bytes.restype = c_sz
-    L.pctc_bwd_chunk.argtypes = [c_i32, c_i32, c_i32, c_i32]
+    L.pctc_bwd_chunk.argtypes = [c_i32, c_i32, c_i32, c_i32, c_i32]
     L.pctc_bwd_chunk.restype = c_i32
     L.pctc_head_bwd.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p,
                                 c_p, c_p]
@@ -156,9 +156,9 @@ def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, be
     return int(lib().pctc_workspace_size(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk))
 
 
-def bwd_chunk(dtype: int, M: int, D: int, chunk: int = 0) -> int:
+def bwd_chunk(dtype: int, M: int, D: int, V: int, chunk: int = 0) -> int:
     """Vocabulary columns per backward step used for this problem (0 chunk = the default)."""
-    return int(lib().pctc_bwd_chunk(int(dtype), int(M), int(D), int(chunk)))
+    return int(lib().pctc_bwd_chunk(int(dtype), int(M), int(D), int(V), int(chunk)))
 
 
 def _grad_buffer(t: Optional[torch.Tensor], shape, dev) -> torch.Tensor:
@@ -393,7 +393,7 @@ def head_bwd(H: torch.Tensor, W: torch.Tensor, lam: torch.Tensor, G: torch.Tenso
     ldG = int(G.shape[1])
     dH = torch.empty((M, D), dtype=torch.float32, device=dev) if want_dH else None
     dW = torch.empty((V, D), dtype=torch.float32, device=dev) if want_dW else None
-    scratch = _workspace(int(L.pctc_bwd_scratch_bytes(dt, M, D, ldG, int(chunk))), dev)
+    scratch = _workspace(int(L.pctc_bwd_scratch_bytes(dt, M, D, V, ldG, int(chunk))), dev)
     code = L.pctc_head_bwd(dt, _ptr(H), M, D, _ptr(W), V, _ptr(lam.to(torch.float64).contiguous()), _ptr(G), ldG,
                            _ptr(g.to(torch.float32).contiguous()), _ptr(remap.to(torch.int32).contiguous()),
                            int(chunk), _ptr(dH), _ptr(dW), ctypes.c_void_p(scratch.data_ptr()), _stream(stream))
