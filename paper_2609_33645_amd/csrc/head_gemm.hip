@@ -140,49 +140,57 @@ lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ 
   }
 }
 
-// lambda_m from the per-partition (max, sum) pairs: 64 frames per block, the partitions
-// split over 4 thread phases; the maximum is exact, the rescaled sum is accumulated in
-// double (each term's exponent taken in float on the exact difference to the maximum).
+// lambda_m from the per-partition (max, sum) pairs: 16 frames per block, 16 lanes per frame
+// splitting the partitions; the maximum is exact, the rescaled sum is accumulated in double
+// (each term's exponent taken in float on the exact difference to the maximum).  With Zd,
+// also S[m][j] = float(Zd[m][j] - lambda_m) for j < *K (one rounding).
+constexpr int kFinFrames = 16;
 __global__ void __launch_bounds__(256)
 lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
-                    float2* __restrict__ lam2) {
-  __shared__ float smax[4][64];
-  __shared__ double ssum[4][64];
-  __shared__ int snan[4][64];
-  const int t = threadIdx.x & 63, ph = threadIdx.x >> 6;
-  const int m = blockIdx.x * 64 + t;
+                    float2* __restrict__ lam2, const double* __restrict__ Zd, const int32_t* __restrict__ Kdev,
+                    float* __restrict__ S, int ldS) {
+  const int ph = threadIdx.x & 15;
+  const int m = blockIdx.x * kFinFrames + (threadIdx.x >> 4);
+  const bool live = m < M;
   float mx = -INFINITY;
   int nan = 0;
-  if (m < M)
-    for (int p = ph; p < P; p += 4) {
+  if (live)
+    for (int p = ph; p < P; p += 16) {
       const float2 q = partials[static_cast<int64_t>(p) * M + m];
       nan |= (q.x != q.x) | (q.y != q.y);
       mx = fmaxf(mx, q.x);
     }
-  smax[ph][t] = mx;
-  snan[ph][t] = nan;
-  __syncthreads();
-  mx = fmaxf(fmaxf(smax[0][t], smax[1][t]), fmaxf(smax[2][t], smax[3][t]));
-  nan = snan[0][t] | snan[1][t] | snan[2][t] | snan[3][t];
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) {
+    mx = fmaxf(mx, __shfl_xor(mx, o, 16));
+    nan |= __shfl_xor(nan, o, 16);
+  }
   double s = 0.0;
-  if (m < M && mx != -INFINITY)
-    for (int p = ph; p < P; p += 4) {
+  if (live && mx != -INFINITY)
+    for (int p = ph; p < P; p += 16) {
       const float2 q = partials[static_cast<int64_t>(p) * M + m];
       if (q.x != -INFINITY)
         s += static_cast<double>(q.y) *
              static_cast<double>(fast_exp2(static_cast<float>(static_cast<double>(q.x) - mx) * kLog2e));
     }
-  ssum[ph][t] = s;
-  __syncthreads();
-  if (ph != 0 || m >= M) return;
-  s = (ssum[0][t] + ssum[1][t]) + (ssum[2][t] + ssum[3][t]);
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o, 16);
+  if (!live) return;
   double l = static_cast<double>(mx) + log(s);
   if (mx == -INFINITY) l = -INFINITY;
   if (nan) l = __longlong_as_double(0x7ff8000000000000LL);
-  lam[m] = l;
-  const double l2 = l * kLog2eD;
-  const float hi = static_cast<float>(l2);
-  lam2[m] = make_float2(hi, static_cast<float>(l2 - static_cast<double>(hi)));
+  if (ph == 0) {
+    lam[m] = l;
+    const double l2 = l * kLog2eD;
+    const float hi = static_cast<float>(l2);
+    lam2[m] = make_float2(hi, static_cast<float>(l2 - static_cast<double>(hi)));
+  }
+  if (Zd) {
+    const int K = *Kdev;
+    const double* zr = Zd + static_cast<int64_t>(m) * ldS;
+    float* sr = S + static_cast<int64_t>(m) * ldS;
+    for (int j = ph; j < K; j += 16) sr[j] = static_cast<float>(zr[j] - l);
+  }
 }
 
 __global__ void lam2_kernel(const double* __restrict__ lam, int M, float2* __restrict__ lam2) {
@@ -234,8 +242,34 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, con
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
+  return launch_lse_finalize(partials, M, Pfin, lam, lam2, nullptr, nullptr, nullptr, 0, stream);
+}
+
+hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                               float2* partials, int* P_out, hipStream_t stream) {
+  *P_out = 0;
+  if (M <= 0) return hipSuccess;
+  if (dtype == 1)
+    return launch_lse_partial_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias, V,
+                                   partials, P_out, stream);
+  const int P = lse_partitions(M, V);
+  const int vtiles = (V + kFwdBR - 1) / kFwdBR;
+  const int vper = ((vtiles + P - 1) / P) * kFwdBR;
+  const int Peff = (V + vper - 1) / vper;
+  const int nMt = (M + kFwdBC - 1) / kFwdBC;
+  *P_out = Peff;
+  Prof pr("lse_partial", stream);
+  hipLaunchKernelGGL(lse_partial_kernel<float>, dim3(nMt * Peff), dim3(256), 0, stream, static_cast<const float*>(H), M,
+                     D, static_cast<const float*>(W), bias, V, Peff, vper, partials);
+  return hipGetLastError();
+}
+
+hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
+                               const int32_t* K, float* S, int ldS, hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
   Prof pr("lse_finalize", stream);
-  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + 63) / 64), dim3(256), 0, stream, partials, M, Pfin, lam, lam2);
+  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + kFinFrames - 1) / kFinFrames), dim3(256), 0, stream, partials, M,
+                     P, lam, lam2, Zd, K, S, ldS);
   return hipGetLastError();
 }
 

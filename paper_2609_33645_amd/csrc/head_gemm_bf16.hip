@@ -316,7 +316,7 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
 __global__ void __launch_bounds__(256, 2)
 gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
               const float* __restrict__ bias, const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev,
-              const double* __restrict__ lam, float* __restrict__ S, int ldS) {
+              const double* __restrict__ lam, float* __restrict__ S, int ldS, double* __restrict__ Zd) {
   using G = GFwd;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES(G)
@@ -336,7 +336,7 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
   for (int j = 0; j < FC; ++j) {
     const int m = m0 + GFwd::col_of(wave, lane, j);
     if (m >= M) continue;
-    const double l = lam[m];
+    const double l = Zd ? 0.0 : lam[m];
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
@@ -345,7 +345,10 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
         if (jj < K) {
           double z = static_cast<double>(acc[i][j][r]);
           if (bias) z += static_cast<double>(bias[u_ids[jj]]);
-          S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(z - l);
+          if (Zd)  // the logit itself; lambda is subtracted once it is known
+            Zd[static_cast<int64_t>(m) * ldS + jj] = z;
+          else
+            S[static_cast<int64_t>(m) * ldS + jj] = static_cast<float>(z - l);
         }
       }
   }
@@ -795,12 +798,12 @@ hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint1
 
 hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias,
                                 const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
-                                hipStream_t stream) {
+                                hipStream_t stream, double* Zd) {
   const int nMt = (M + kFC - 1) / kFC;
   const int nJt = (K_max + kFR - 1) / kFR;
   Prof pr("gather_s", stream);
   hipLaunchKernelGGL(gather_s_bf16, dim3(nMt * nJt), dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias, u_ids, K, lam,
-                     S, ldS);
+                     S, ldS, Zd);
   return hipGetLastError();
 }
 

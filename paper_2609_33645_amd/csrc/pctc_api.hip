@@ -101,7 +101,7 @@ struct Layout {
   DpPlan dp;
   BwdPlan bwd;
   size_t o_remap, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_gpred, o_pred,
-      o_corr, o_dp, o_bwd, total;
+      o_corr, o_dp, o_bwd, o_zd, total;
 };
 
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
@@ -160,6 +160,12 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   }
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
+  if (dtype == PCTC_BF16) {
+    // selected logits in double [M][ldS] until lambda is known: in the gradient buffer (not
+    // yet in use then) when it is large enough
+    const size_t need = static_cast<size_t>(L.M) * L.ldS * sizeof(double);
+    L.o_zd = (L.bwd.dz_bytes >= need) ? L.o_bwd : take(need);
+  }
   L.total = o;
   return L;
 }
@@ -292,36 +298,54 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   std::vector<int64_t> soff;
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
   PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
-  // Algorithm 1: union and relabel
-  PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
-  // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
-  PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
-  PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
   const bool want_bwd = (dH || dW || db);
   int32_t* fflag = Kdev + 2;  // forecast mismatch flag
   const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
   hipStream_t dps_stream = stream;
   struct Events {
-    hipEvent_t fork = nullptr, join = nullptr;
+    hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, join = nullptr;
     ~Events() {
-      if (fork) hipEventDestroy(fork);
-      if (join) hipEventDestroy(join);
+      for (hipEvent_t e : {start, sel, fork, join})
+        if (e) hipEventDestroy(e);
     }
   } ev;
   float* g_pred = nullptr;
   if (overlap) {
-    // Dense part -g p of the backward beside the lattice: g is forecast (-w_n on included
-    // utterances), the lattice runs on a second stream, and the union columns' part (from its
-    // G) is added once both are done.  A wrong forecast (rare: a -inf logit on a selected
-    // class) is caught and the backward is redone in the plain order.
+    // Two streams.  Second stream: union/relabel and the selected logits (beside the
+    // normaliser pass), later the lattice and the union columns' part of the backward.
+    // Caller's stream: the normaliser, S = logits - lambda, a forecast of g (-w_n on included
+    // utterances), and the dense part -g p of the backward beside the lattice.  A wrong
+    // forecast (rare: a -inf logit on a selected class) is caught and the backward is redone
+    // in the plain order.
+    PCTC_HIP(side_stream(&dps_stream));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.start, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.sel, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
+    PCTC_HIP(hipEventRecord(ev.start, stream));
+    PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
+    double* Zd = reinterpret_cast<double*>(ws + L.o_zd);
+    // Algorithm 1: union and relabel, then the selected logits X W_U^T (+ b_U)
+    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, dps_stream));
+    PCTC_HIP(launch_gather_s_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), bias,
+                                  u_ids, Kdev, L.K_max, nullptr, nullptr, L.ldS, dps_stream, Zd));
+    PCTC_HIP(hipEventRecord(ev.sel, dps_stream));
+    // online full-vocabulary log-sum-exp; S = logits - lambda once both are done
+    int P = 0;
+    PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    PCTC_HIP(hipStreamWaitEvent(stream, ev.sel, 0));
+    PCTC_HIP(launch_lse_finalize(partials, L.M, P, lam, lam2, Zd, Kdev, S, L.ldS, stream));
     g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
     int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
     PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, lam, utt_weight, g_pred, pred, stream));
-    PCTC_HIP(side_stream(&dps_stream));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
     PCTC_HIP(hipEventRecord(ev.fork, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
+  } else {
+    // Algorithm 1: union and relabel
+    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
+    // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
+    PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
+    PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
   }
   // lattice, total scores, zeroing of nonfinite losses, G = dL/dS
   PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status, G, g,

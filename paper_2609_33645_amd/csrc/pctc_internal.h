@@ -37,6 +37,13 @@ size_t lse_partial_bytes(int M);
 // bias: device float [V] or null (logits H W^T + b).
 hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                       float2* partials, double* lam, float2* lam2, hipStream_t stream);
+// The same in two halves: the partial (max, sum) pairs over the vocabulary partitions
+// (P_out: partitions written), then lambda and its hi/lo pair from them; with Zd the second
+// half also writes S[m * ldS + j] = float(Zd[m * ldS + j] - lambda_m) for j < *K.
+hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
+                               float2* partials, int* P_out, hipStream_t stream);
+hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
+                               const int32_t* K, float* S, int ldS, hipStream_t stream);
 hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const float* bias,
                            const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream);
@@ -71,9 +78,11 @@ hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t strea
 // ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
 hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                    float2* partials, int* P_out, hipStream_t stream);
+// Zd (may be null): write the selected logits in double (Zd[m * ldS + j]) instead of S; lam
+// is then not read (launch_lse_finalize subtracts it).
 hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias,
                                 const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
-                                hipStream_t stream);
+                                hipStream_t stream, double* Zd = nullptr);
 hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
