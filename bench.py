@@ -100,7 +100,8 @@ def make_workload(name: str, seed: int, beam):
     from paper_2609_33645_amd import workloads
     fn = workloads.NAMED[name]
     if beam is None:
-        beam = {"zipformer_m": 16.0, "qwen3_0p6b": 32.0, "qwen3_8b": 32.0, "qwen3_32b": 16.0}.get(name, math.inf)
+        beam = {"zipformer_m": 16.0, "qwen3_0p6b": 32.0, "qwen3_8b": 32.0, "qwen3_32b": 16.0,
+                "qwen3_8b_kstress": 32.0, "e3_qwen3_8b": 32.0}.get(name, math.inf)
     if name == "tiny_f32":
         wl = fn(seed)
         wl.beam = beam

@@ -183,12 +183,45 @@ def qwen3_32b(seed: int = 0, beam: float = 16.0) -> Workload:
                       p_repeat=0.1, h_law="rmsnorm", w_std=0.02, beam=beam)
 
 
+def qwen3_8b_kstress(seed: int = 0, beam: float = math.inf) -> Workload:
+    """The Qwen3-8B-style shape with uniform token draws instead of Zipf: nearly every
+    target id distinct, so the union is as large as the targets allow (K ~ 1 + sum U)."""
+    rng = np.random.default_rng(seed)
+    T = rng.integers(500, 751, size=4).astype(np.int32)
+    U = (T // 4).astype(np.int32)
+    return synthesize(name="qwen3_8b_kstress", dtype="bf16", T=T, U=U, D=4096, V=151_936, rng=rng,
+                      token_law="uniform", h_law="rmsnorm", w_std=0.02, beam=beam)
+
+
+def e1_zipformer_f32(seed: int = 0, beam: float = math.inf) -> Workload:
+    """The encoder benchmark's memory shape: 160 utterances x 100 frames (M = 16,000), D = 512,
+    V = 180,000, fp32 head; U = floor(T/6) Zipf(1.1)."""
+    rng = np.random.default_rng(seed)
+    T = np.full(160, 100, np.int32)
+    U = (T // 6).astype(np.int32)
+    return synthesize(name="e1_zipformer_f32", dtype="f32", T=T, U=U, D=512, V=180_000, rng=rng, beam=beam)
+
+
+def e3_qwen3_8b(seed: int = 0, beam: float = 32.0) -> Workload:
+    """The LLM benchmark's memory shape: N = 107 utterances of at most 111 frames (M = 11,458),
+    D = 4096, V = 151,936, bf16 (run with the head frozen: no dW); U = floor(T/4) Zipf(1.1)."""
+    rng = np.random.default_rng(seed)
+    T = np.full(107, 107, np.int32)
+    T[: 11458 - 107 * 107] += 1            # 11,458 frames, lengths 107..108 (<= 111)
+    U = (T // 4).astype(np.int32)
+    return synthesize(name="e3_qwen3_8b", dtype="bf16", T=T, U=U, D=4096, V=151_936, rng=rng,
+                      h_law="rmsnorm", w_std=0.02, beam=beam)
+
+
 NAMED = {
     "tiny_f32": tiny_f32,
     "zipformer_m": zipformer_m,
     "qwen3_0p6b": qwen3_0p6b,
     "qwen3_8b": qwen3_8b,
     "qwen3_32b": qwen3_32b,
+    "qwen3_8b_kstress": qwen3_8b_kstress,
+    "e1_zipformer_f32": e1_zipformer_f32,
+    "e3_qwen3_8b": e3_qwen3_8b,
 }
 
 

@@ -74,7 +74,7 @@ def _mask_check(res_utt, mk, T, Sp, band=1e-2):
 
 
 FULL = [("zipformer_m", 16.0), ("zipformer_m", math.inf), ("qwen3_0p6b", 32.0), ("qwen3_8b", 32.0),
-        ("qwen3_32b", 16.0)]
+        ("qwen3_32b", 16.0), ("qwen3_8b_kstress", 32.0), ("e1_zipformer_f32", math.inf)]
 
 
 @pytest.mark.timeout(900)
@@ -298,4 +298,40 @@ def test_full_size_grouped_export():
     say(f"  sampled gradients cos dH={cH:.7f} dW={cW:.7f}")
     assert cH >= 0.999 and cW >= 0.999
     del lp, pad, loss, Hg, Wg, H, W, y
+    torch.cuda.empty_cache()
+
+
+@pytest.mark.timeout(600)
+def test_e3_memory_shape_frozen_head():
+    """The LLM benchmark's memory shape (107 utterances, M = 11,458, D = 4096, V = 151,936,
+    head frozen: no dW).  Utterance losses and dH rows depend only on their own utterance, so
+    the first two utterances are checked against the oracle run on those two alone."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.NAMED["e3_qwen3_8b"](0)
+    say(f"e3 shape: N={wl.N} M={wl.M} D={wl.D} V={wl.V} U={int(wl.target_lengths.sum())}")
+    H, W, y = to_dev(wl)
+    torch.cuda.synchronize()
+    base = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
+                                       want_dW=False)
+    torch.cuda.synchronize()
+    peak = (torch.cuda.max_memory_allocated() - base) / 2**20
+    say(f"  peak above inputs {peak:.1f} MiB (workspace {out['workspace_bytes'] / 2**20:.1f} MiB)")
+    assert out["dW"] is None
+    assert (out["status"].cpu().numpy() == 0).all()
+    n2 = 2
+    T2, U2 = wl.input_lengths[:n2], wl.target_lengths[:n2]
+    M2, Y2 = int(T2.sum()), int(U2.sum())
+    ref = oracle.fwd_bwd(wl.H[:M2].astype(np.float64), wl.W.astype(np.float64), wl.targets[:Y2], T2, U2, wl.blank,
+                         wl.beam)
+    ln = out["loss_per_utt"].cpu().numpy()[:n2]
+    say(f"  losses gpu={ln.tolist()} oracle={ref['loss_n'].tolist()}")
+    np.testing.assert_allclose(ln, ref["loss_n"], rtol=1e-5)
+    dH = out["dH"][:M2].cpu().numpy()
+    c = cosine(dH, ref["dH"])
+    say(f"  dH rows of the two utterances: cos={c:.7f} rel={rel_err(dH, ref['dH']):.3g}")
+    assert c >= 0.99999
+    del out, H, W, y
     torch.cuda.empty_cache()
