@@ -396,6 +396,23 @@ def main():
         "workspace_mb": round(ws_mb, 1),
         "kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(kernel_ms.items(), key=lambda kv: -kv[1])},
     }
+    # the paper's protocol (App. C.1): 3 runs of 5 warm-up and 50 measured calls, each call timed
+    # with the device synchronised at both ends; the median of the run medians
+    meds = []
+    for _ in range(3):
+        for _ in range(5):
+            step()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(50):
+            t1 = time.perf_counter()
+            step()
+            torch.cuda.synchronize()
+            ts.append(time.perf_counter() - t1)
+        meds.append(float(np.median(ts)))
+    pm = float(np.median(meds))
+    line["paper_protocol"] = {"runs": 3, "warmup": 5, "steps": 50, "median_ms_per_call": round(pm * 1e3, 4),
+                              "frames_per_s": round(M / pm, 1)}
     if not a.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, a.cpu_utts)
     print(json.dumps(line), flush=True)

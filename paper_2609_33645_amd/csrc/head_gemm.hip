@@ -679,11 +679,25 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
   const int tr = (dtype == 1) ? 256 : kBwdB;  // dH tile rows of the kernel used
   const int tc = (dtype == 1) ? 256 : kBwdB;
   const int tiles = ((M + tr - 1) / tr) * ((D + tc - 1) / tc);
-  int splits = 256 / tiles;  // one wave of 256 workgroups
-  const int maxs = p.chunk / 256;
-  if (splits > maxs) splits = maxs;
-  if (splits > 8) splits = 8;
-  if (splits < 1) splits = 1;
+  // k-slices of the dH product (one workgroup per CU): when the tiles alone make less than
+  // two 256-workgroup waves, at most ~12,800 columns per slice (a launch of a few long
+  // workgroups is exposed to any CU that is held up); then the fewest slices whose launch
+  // fills its waves to at least 90%, else the fullest; at most 8
+  const int maxs = p.chunk / 256 < 8 ? (p.chunk / 256 > 0 ? p.chunk / 256 : 1) : 8;
+  int mins = (tiles < 512) ? (p.chunk + 12799) / 12800 : 1;
+  if (mins > maxs) mins = maxs;
+  if (mins < 1) mins = 1;
+  int splits = mins;
+  double best = -1.0;
+  for (int sp = mins; sp <= maxs; ++sp) {
+    const int wgs = tiles * sp;
+    const double fill = static_cast<double>(wgs) / (256.0 * ((wgs + 255) / 256));
+    if (fill > best + 1e-9) {
+      best = fill;
+      splits = sp;
+    }
+    if (fill >= 0.9) break;
+  }
   p.splits = splits;
   p.Mp = ((M + 63) / 64) * 64;
   p.dz_bytes = align_up(static_cast<size_t>(M) * cap * es, 256);

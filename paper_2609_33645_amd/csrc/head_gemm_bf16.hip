@@ -488,20 +488,59 @@ __global__ void db_reduce_bf16(const float* __restrict__ dbpart, int ntiles, int
   db[v] = s;
 }
 
+// Tile r of an nA x nB grid walked block by block: the grid is cut into ga x (8 / ga) blocks
+// (edge blocks smaller), blocks in row order, tiles within a block b fastest.
+__device__ __forceinline__ void block_tile(int r, int nA, int nB, int ga, int& a, int& b) {
+  const int gb = 8 / ga;
+  const int ba = (nA + ga - 1) / ga, bb = (nB + gb - 1) / gb;
+  for (int i = 0; i < ga; ++i) {
+    const int a0 = i * ba, ha = min(ba, nA - a0);
+    if (ha <= 0) break;
+    for (int j = 0; j < gb; ++j) {
+      const int b0 = j * bb, hb = min(bb, nB - b0);
+      if (hb <= 0) break;
+      if (r < ha * hb) {
+        a = a0 + r / hb;
+        b = b0 + r % hb;
+        return;
+      }
+      r -= ha * hb;
+    }
+  }
+  a = nA;  // not reached for r < nA nB
+  b = 0;
+}
+
+// gm for the dH product: the frame x d partition over 8 XCDs that reads the least (W columns
+// are read gm times, dZ rows 8 / gm times).
+static int dh_xcd_rows(int M, int D) {
+  int best = 8;
+  long long cost = -1;
+  for (int gm = 1; gm <= 8; gm *= 2) {
+    const long long c = static_cast<long long>(gm) * D + static_cast<long long>(8 / gm) * M;
+    if (cost < 0 || c < cost) {
+      cost = c;
+      best = gm;
+    }
+  }
+  return best;
+}
+
 __global__ void __launch_bounds__(512, 1)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
-             int slice, float* __restrict__ part) {
+             int slice, float* __restrict__ part, int gm) {
   const bool first = c0 == 0;
   using G = GDh;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES4(G)
   const int nMt = (M + kBR - 1) / kBR;
   const int nDt = (D + kBC - 1) / kBC;
-  // d-tiles fastest: the workgroups that read the same dZ rows run together on one XCD
+  // Each XCD (a contiguous run of work ids) takes one block of a gm x (8 / gm) partition of
+  // the frame x d tile grid: it reads dZ rows of its frame block and W columns of its d block
   const int work = xcd_swz(blockIdx.x, gridDim.x);
-  const int dt = work % nDt;
-  const int mt = (work / nDt) % nMt;
   const int s = work / (nMt * nDt);
+  int mt, dt;
+  block_tile(work % (nMt * nDt), nMt, nDt, gm, mt, dt);
   const int m0 = mt * kBR, d0 = dt * kBC;
   const int kb = s * slice;
   const int ke = min(cw, kb + slice);
@@ -714,7 +753,7 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dh", stream);
     hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles), dim3(GDh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2, k2,
-                       *dH_u);
+                       *dH_u, dh_xcd_rows(M, D));
   }
   if (want_dW) {
     uint16_t* Hs2 = reinterpret_cast<uint16_t*>(sc + L.o_hs);
@@ -838,7 +877,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
     hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D, c0, cw, slice,
-                       part);
+                       part, dh_xcd_rows(M, D));
   }
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
