@@ -31,6 +31,10 @@ constexpr int kBK = 32;
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 // 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
 using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4>;
+// normaliser for wide heads (D >= kWideD): the k loop is long enough that the epilogue is a
+// small share, so one 8-wave 256 x 256 workgroup per CU beats two 4-wave ones
+using GWide = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4>;
+constexpr int kWideD = 2048;
 using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4>;
 
 #define PCTC_STAGES2(G)                                                  \
@@ -86,13 +90,13 @@ __device__ __forceinline__ bool grouped_tile(int work, int nA, int nB, int& a, i
 }
 
 // Accumulators of a tile start at the bias of their row (bt: the tile's rows, in LDS).
-template <int FR, int FC>
+template <int FR, int FC, class G = GFwd>
 __device__ __forceinline__ void bias_init(f32x16 (&acc)[FR][FC], const float* bt, int wave, int lane) {
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-      const float4 b4 = *reinterpret_cast<const float4*>(bt + GFwd::row_of(wave, lane, i, 4 * q));
+      const float4 b4 = *reinterpret_cast<const float4*>(bt + G::row_of(wave, lane, i, 4 * q));
 #pragma unroll
       for (int j = 0; j < FC; ++j) {
         acc[i][j][4 * q + 0] = b4.x;
@@ -105,7 +109,7 @@ __device__ __forceinline__ void bias_init(f32x16 (&acc)[FR][FC], const float* bt
 
 // Online log-sum-exp update of the running (max, sum) of this lane's frames with one
 // tile of logits (bias included); rows at or past vend are skipped when MASK.
-template <bool MASK, int FR, int FC>
+template <bool MASK, int FR, int FC, class G = GFwd>
 __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], float (&run_max)[FC],
                                                 float (&run_sum)[FC], int v0, int vend, int wave, int lane) {
 #pragma unroll
@@ -115,7 +119,7 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
+        const int r0 = G::row_of(wave, lane, i, 4 * q);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float x = acc[i][j][4 * q + e];
@@ -135,7 +139,7 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
     for (int i = 0; i < FR; ++i)
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
-        const int r0 = GFwd::row_of(wave, lane, i, 4 * q);
+        const int r0 = G::row_of(wave, lane, i, 4 * q);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float ex = fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ms));
@@ -155,25 +159,32 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
 
 }  // namespace
 
-template <bool BIAS>
-__global__ void __launch_bounds__(256, 2)
+#define PCTC_STAGES_G(G)                                                                  \
+  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes];                      \
+  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes];                      \
+  __shared__ __attribute__((aligned(1024))) char st2_[G::kNS >= 3 ? G::kStageBytes : 16];   \
+  __shared__ __attribute__((aligned(1024))) char st3_[G::kNS >= 4 ? G::kStageBytes : 16];   \
+  char* const stx_[4] = {st0_, st1_, st2_, st3_};                                           \
+  char* const(&st)[G::kNS] = *reinterpret_cast<char* const(*)[G::kNS]>(&stx_);
+
+template <class G, bool BIAS, int OCC>
+__global__ void __launch_bounds__(G::kThreads, OCC)
 lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, const float* __restrict__ bias,
                  int V, int P, int vper, float2* __restrict__ partials) {
   extern __shared__ float bsh[];  // BIAS: b over this partition's rows (vper, padded to whole tiles)
-  using G = GFwd;
-  constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES(G)
-  const int nMt = (M + kFC - 1) / kFC;
+  constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
+  PCTC_STAGES_G(G)
+  const int nMt = (M + TC - 1) / TC;
   int mt, p;
   if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) return;
-  const int m0 = mt * kFC;
+  const int m0 = mt * TC;
   const int vbeg = p * vper;
   const int vend = min(V, vbeg + vper);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
+  const int ntiles = (vend - vbeg + TR - 1) / TR;
   if (BIAS) {
     // visible to every wave after the engine's first barrier
-    for (int r = tid; r < ntiles * kFR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
+    for (int r = tid; r < ntiles * TR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
     __syncthreads();
   }
   const GOp A{W, D, vend, D, nullptr};
@@ -186,22 +197,23 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
   }
   f32x16 acc[FR][FC];
   auto epi = [&](int i, const f32x16 (&a)[FR][FC]) {
-    const int v0 = vbeg + i * kFR;
-    if (v0 + kFR <= vend)
-      lse_tile_update<false, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+    const int v0 = vbeg + i * TR;
+    if (v0 + TR <= vend)
+      lse_tile_update<false, FR, FC, G>(a, run_max, run_sum, v0, vend, wave, lane);
     else
-      lse_tile_update<true, FR, FC>(a, run_max, run_sum, v0, vend, wave, lane);
+      lse_tile_update<true, FR, FC, G>(a, run_max, run_sum, v0, vend, wave, lane);
   };
   if (BIAS)
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int i, f32x16 (&a)[FR][FC]) {
-      bias_init<FR, FC>(a, bsh + i * kFR, wave, lane);
+      bias_init<FR, FC, G>(a, bsh + i * TR, wave, lane);
     });
   else
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
   __syncthreads();
   // the two wavefronts of each frame column (row halves) combine their partial sums
+  constexpr int WC = G::NW / 2;  // column groups (the wave grid is 2 x WC)
   float2* xch = reinterpret_cast<float2*>(st0_);
-  const int rowhalf = wave / 2, colq = wave % 2;
+  const int rowhalf = wave / WC, colq = wave % WC;
   if (rowhalf == 1 && lane < 32) {
 #pragma unroll
     for (int j = 0; j < FC; ++j) xch[colq * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
@@ -808,12 +820,22 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
   const int nMt = (M + kFC - 1) / kFC;
   *P_out = Peff;
   Prof pr("lse_partial", stream);
-  if (bias)
-    hipLaunchKernelGGL(lse_partial_bf16<true>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads),
-                       static_cast<size_t>(vper) * sizeof(float), stream, H, M, D, W, bias, V, Peff, vper, partials);
-  else
-    hipLaunchKernelGGL(lse_partial_bf16<false>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M,
-                       D, W, bias, V, Peff, vper, partials);
+  const size_t bsh = bias ? static_cast<size_t>(vper) * sizeof(float) : 0;
+  if (D >= kWideD) {
+    const int nMw = (M + GWide::kBC - 1) / GWide::kBC;
+    if (bias)
+      hipLaunchKernelGGL((lse_partial_bf16<GWide, true, 1>), dim3(grouped_grid(nMw, Peff)), dim3(GWide::kThreads), bsh,
+                         stream, H, M, D, W, bias, V, Peff, vper, partials);
+    else
+      hipLaunchKernelGGL((lse_partial_bf16<GWide, false, 1>), dim3(grouped_grid(nMw, Peff)), dim3(GWide::kThreads), 0,
+                         stream, H, M, D, W, bias, V, Peff, vper, partials);
+  } else if (bias) {
+    hipLaunchKernelGGL((lse_partial_bf16<GFwd, true, 2>), dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), bsh,
+                       stream, H, M, D, W, bias, V, Peff, vper, partials);
+  } else {
+    hipLaunchKernelGGL((lse_partial_bf16<GFwd, false, 2>), dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0,
+                       stream, H, M, D, W, bias, V, Peff, vper, partials);
+  }
   return hipGetLastError();
 }
 
