@@ -213,7 +213,7 @@ int lse_partitions(int M, int V) {
   return P;
 }
 
-size_t lse_partial_bytes(int M) { return align_up(static_cast<size_t>(256) * M * sizeof(float2), 256); }
+size_t lse_partial_bytes(int M) { return align_up(static_cast<size_t>(kMaxLseParts) * M * sizeof(float2), 256); }
 
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream) {
   if (M <= 0) return hipSuccess;

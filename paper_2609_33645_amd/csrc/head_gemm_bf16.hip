@@ -33,7 +33,7 @@ using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4>;
 // normaliser for wide heads (D >= kWideD): the k loop is long enough that the epilogue is a
 // small share, so one 8-wave 256 x 256 workgroup per CU beats two 4-wave ones
-using GWide = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4>;
+using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 constexpr int kWideD = 2048;
 using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4>;
 
@@ -247,24 +247,23 @@ __device__ __forceinline__ void amax_merge(float& bv, int& bi, float ov, int oi)
   }
 }
 
-template <bool BIAS>
-__global__ void __launch_bounds__(256, 2)
+template <class G, bool BIAS, int OCC>
+__global__ void __launch_bounds__(G::kThreads, OCC)
 amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
                   const float* __restrict__ bias, int V, int P, int vper, float2* __restrict__ partials) {
   extern __shared__ float bsh[];  // BIAS: b over this partition's rows
-  using G = GFwd;
-  constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES(G)
-  const int nMt = (M + kFC - 1) / kFC;
+  constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
+  PCTC_STAGES_G(G)
+  const int nMt = (M + TC - 1) / TC;
   int mt, p;
   if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) return;
-  const int m0 = mt * kFC;
+  const int m0 = mt * TC;
   const int vbeg = p * vper;
   const int vend = min(V, vbeg + vper);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int ntiles = (vend - vbeg + kFR - 1) / kFR;
+  const int ntiles = (vend - vbeg + TR - 1) / TR;
   if (BIAS) {
-    for (int r = tid; r < ntiles * kFR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
+    for (int r = tid; r < ntiles * TR; r += G::kThreads) bsh[r] = (vbeg + r < vend) ? bias[vbeg + r] : 0.f;
     __syncthreads();
   }
   const GOp A{W, D, vend, D, nullptr};
@@ -278,7 +277,7 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   }
   f32x16 acc[FR][FC];
   auto epi = [&](int it, const f32x16 (&a)[FR][FC]) {
-    const int v0 = vbeg + it * kFR;
+    const int v0 = vbeg + it * TR;
 #pragma unroll
     for (int j = 0; j < FC; ++j)
 #pragma unroll
@@ -294,7 +293,7 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   };
   if (BIAS)
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int it, f32x16 (&a)[FR][FC]) {
-      bias_init<FR, FC>(a, bsh + it * kFR, wave, lane);
+      bias_init<FR, FC, G>(a, bsh + it * TR, wave, lane);
     });
   else
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
@@ -307,7 +306,8 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
   }
   __syncthreads();
   float2* xch = reinterpret_cast<float2*>(st0_);
-  const int rowhalf = wave / 2, colq = wave % 2;
+  constexpr int WC = G::NW / 2;  // column groups (the wave grid is 2 x WC)
+  const int rowhalf = wave / WC, colq = wave % WC;
   if (rowhalf == 1 && lane < 32) {
 #pragma unroll
     for (int j = 0; j < FC; ++j)
@@ -801,59 +801,74 @@ hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t
 // launchers (bf16 path)
 // ---------------------------------------------------------------------------------------
 
-int lse_partitions_bf16(int M, int V) {
-  (void)M;
-  int P = 256;  // runs of a few vocabulary tiles per workgroup
-  const int vtiles = (V + kFR - 1) / kFR;
-  if (P > vtiles) P = vtiles;
-  if (P > 256) P = 256;
-  if (P < 1) P = 1;
-  return P;
+// Vocabulary split of a normaliser or argmax launch: each workgroup takes a run of vper / 256
+// vocabulary tiles for one frame tile (partition p covers rows [p vper, (p + 1) vper)), the
+// fewest runs that keep the partition count within the partial buffer.  (Runs chosen instead
+// to fill the last round of workgroups evenly measured slower: the run length also sets the
+// L2 reuse of the tile order.)
+struct LseSplit {
+  bool wide;  // one 8-wave 256 x 256 workgroup per CU; else two 4-wave 256 x 128
+  int vper, P, nM;
+};
+
+static LseSplit lse_split_bf16(int M, int D, int V) {
+  LseSplit s;
+  s.wide = D >= kWideD;
+  const int TR = s.wide ? GWide::kBR : GFwd::kBR, TC = s.wide ? GWide::kBC : GFwd::kBC;
+  const int vtiles = (V + TR - 1) / TR;
+  s.nM = (M + TC - 1) / TC;
+  s.vper = ((vtiles + kMaxLseParts - 1) / kMaxLseParts) * TR;
+  s.P = (V + s.vper - 1) / s.vper;
+  return s;
 }
 
 hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                    float2* partials, int* P_out, hipStream_t stream) {
-  const int P = lse_partitions_bf16(M, V);
-  const int vtiles = (V + kFR - 1) / kFR;
-  const int vper = ((vtiles + P - 1) / P) * kFR;
-  const int Peff = (V + vper - 1) / vper;
-  const int nMt = (M + kFC - 1) / kFC;
+  const LseSplit sp = lse_split_bf16(M, D, V);
+  const int vper = sp.vper, Peff = sp.P;
   *P_out = Peff;
   Prof pr("lse_partial", stream);
   const size_t bsh = bias ? static_cast<size_t>(vper) * sizeof(float) : 0;
-  if (D >= kWideD) {
-    const int nMw = (M + GWide::kBC - 1) / GWide::kBC;
+  const dim3 grid(grouped_grid(sp.nM, Peff));
+  if (sp.wide) {
     if (bias)
-      hipLaunchKernelGGL((lse_partial_bf16<GWide, true, 1>), dim3(grouped_grid(nMw, Peff)), dim3(GWide::kThreads), bsh,
-                         stream, H, M, D, W, bias, V, Peff, vper, partials);
+      hipLaunchKernelGGL((lse_partial_bf16<GWide, true, 1>), grid, dim3(GWide::kThreads), bsh, stream, H, M, D, W,
+                         bias, V, Peff, vper, partials);
     else
-      hipLaunchKernelGGL((lse_partial_bf16<GWide, false, 1>), dim3(grouped_grid(nMw, Peff)), dim3(GWide::kThreads), 0,
-                         stream, H, M, D, W, bias, V, Peff, vper, partials);
+      hipLaunchKernelGGL((lse_partial_bf16<GWide, false, 1>), grid, dim3(GWide::kThreads), 0, stream, H, M, D, W,
+                         bias, V, Peff, vper, partials);
   } else if (bias) {
-    hipLaunchKernelGGL((lse_partial_bf16<GFwd, true, 2>), dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), bsh,
-                       stream, H, M, D, W, bias, V, Peff, vper, partials);
+    hipLaunchKernelGGL((lse_partial_bf16<GFwd, true, 2>), grid, dim3(GFwd::kThreads), bsh, stream, H, M, D, W, bias,
+                       V, Peff, vper, partials);
   } else {
-    hipLaunchKernelGGL((lse_partial_bf16<GFwd, false, 2>), dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0,
-                       stream, H, M, D, W, bias, V, Peff, vper, partials);
+    hipLaunchKernelGGL((lse_partial_bf16<GFwd, false, 2>), grid, dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias,
+                       V, Peff, vper, partials);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                     float2* partials, int* P_out, hipStream_t stream) {
-  const int P = lse_partitions_bf16(M, V);
-  const int vtiles = (V + kFR - 1) / kFR;
-  const int vper = ((vtiles + P - 1) / P) * kFR;
-  const int Peff = (V + vper - 1) / vper;
-  const int nMt = (M + kFC - 1) / kFC;
+  const LseSplit sp = lse_split_bf16(M, D, V);
+  const int vper = sp.vper, Peff = sp.P;
   *P_out = Peff;
   Prof pr("amax_partial", stream);
-  if (bias)
-    hipLaunchKernelGGL(amax_partial_bf16<true>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads),
-                       static_cast<size_t>(vper) * sizeof(float), stream, H, M, D, W, bias, V, Peff, vper, partials);
-  else
-    hipLaunchKernelGGL(amax_partial_bf16<false>, dim3(grouped_grid(nMt, Peff)), dim3(GFwd::kThreads), 0, stream, H, M,
-                       D, W, bias, V, Peff, vper, partials);
+  const size_t bsh = bias ? static_cast<size_t>(vper) * sizeof(float) : 0;
+  const dim3 grid(grouped_grid(sp.nM, Peff));
+  if (sp.wide) {
+    if (bias)
+      hipLaunchKernelGGL((amax_partial_bf16<GWide, true, 1>), grid, dim3(GWide::kThreads), bsh, stream, H, M, D, W,
+                         bias, V, Peff, vper, partials);
+    else
+      hipLaunchKernelGGL((amax_partial_bf16<GWide, false, 1>), grid, dim3(GWide::kThreads), 0, stream, H, M, D, W,
+                         bias, V, Peff, vper, partials);
+  } else if (bias) {
+    hipLaunchKernelGGL((amax_partial_bf16<GFwd, true, 2>), grid, dim3(GFwd::kThreads), bsh, stream, H, M, D, W, bias,
+                       V, Peff, vper, partials);
+  } else {
+    hipLaunchKernelGGL((amax_partial_bf16<GFwd, false, 2>), grid, dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias,
+                       V, Peff, vper, partials);
+  }
   return hipGetLastError();
 }
 

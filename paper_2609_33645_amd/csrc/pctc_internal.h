@@ -33,6 +33,8 @@ hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t bla
 
 // ---- normaliser and selected log-probabilities ------------------------------------------
 int lse_partitions(int M, int V);
+// most vocabulary partitions of a normaliser or argmax launch (partial buffer rows)
+constexpr int kMaxLseParts = 256;
 size_t lse_partial_bytes(int M);
 // bias: device float [V] or null (logits H W^T + b).
 hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,

@@ -65,7 +65,7 @@ def test_union_remap_bad_label():
 # ---------------------------------------------------------------------------------------
 
 @pytest.mark.parametrize("dtype,M,D,V", [("f32", 92, 64, 1000), ("bf16", 300, 128, 3001), ("bf16", 129, 64, 70_000),
-                                         ("f32", 257, 136, 2050), ("bf16", 1, 8, 2)])
+                                         ("f32", 257, 136, 2050), ("bf16", 1, 8, 2), ("bf16", 300, 2056, 5001)])
 def test_lse_select(dtype, M, D, V):
     import torch
     from paper_2609_33645_amd import prunedctc
@@ -289,14 +289,15 @@ def test_error_codes():
 # head bias, blank offset, loss weights and the bias gradient (pruned_ctc_fwd_bwd_ex)
 # ---------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("seed,dtype,beam,blank,chunk,zero_w", [
-    (0, "f32", math.inf, 0, 256, False), (1, "bf16", 16.0, 0, 0, True), (2, "bf16", math.inf, 2999, 512, False),
-    (3, "f32", 4.0, 11, 0, True), (4, "bf16", 0.0, 0, 1024, False)])
-def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w):
+@pytest.mark.parametrize("seed,dtype,beam,blank,chunk,zero_w,D", [
+    (0, "f32", math.inf, 0, 256, False, 128), (1, "bf16", 16.0, 0, 0, True, 128),
+    (2, "bf16", math.inf, 2999, 512, False, 128), (3, "f32", 4.0, 11, 0, True, 128),
+    (4, "bf16", 0.0, 0, 1024, False, 128), (5, "bf16", 16.0, 3, 0, False, 2056)])
+def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w, D):
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(40 + seed, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
-                                blank=blank, beam=beam, w_std=0.5)
+    wl = workloads.random_small(40 + seed, N=5, T_range=(1, 140), D=D, V=3000, dtype=dtype, p_repeat=0.15,
+                                blank=blank, beam=beam, w_std=0.5 * math.sqrt(128 / D))
     rng = np.random.default_rng(seed)
     b = rng.standard_normal(wl.V).astype(np.float32)
     b[blank] += 2.0                                  # blank offset eta
@@ -394,12 +395,14 @@ def _check_greedy(wl, H64, W64, b64, got, ref, frames=None, eps=1e-3):
     return ids, sure
 
 
-@pytest.mark.parametrize("seed,dtype,blank,with_bias", [(0, "f32", 0, False), (1, "bf16", 0, True),
-                                                        (2, "bf16", 2999, False), (3, "f32", 5, True)])
-def test_greedy_decode(seed, dtype, blank, with_bias):
+@pytest.mark.parametrize("seed,dtype,blank,with_bias,D", [(0, "f32", 0, False, 128), (1, "bf16", 0, True, 128),
+                                                          (2, "bf16", 2999, False, 128), (3, "f32", 5, True, 128),
+                                                          (4, "bf16", 7, True, 2056), (5, "bf16", 0, False, 2048)])
+def test_greedy_decode(seed, dtype, blank, with_bias, D):
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(90 + seed, N=6, T_range=(1, 150), D=128, V=3000, dtype=dtype, blank=blank, w_std=0.5)
+    wl = workloads.random_small(90 + seed, N=6, T_range=(1, 150), D=D, V=3000, dtype=dtype, blank=blank,
+                                w_std=0.5 * math.sqrt(128 / D))
     H, W, _ = to_dev(wl)
     rng = np.random.default_rng(seed)
     b = rng.standard_normal(wl.V).astype(np.float32) if with_bias else np.zeros(wl.V, np.float32)
