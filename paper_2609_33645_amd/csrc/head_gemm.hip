@@ -152,27 +152,30 @@ lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* _
   const int ph = threadIdx.x & 15;
   const int m = blockIdx.x * kFinFrames + (threadIdx.x >> 4);
   const bool live = m < M;
+  // this lane's partitions ph, ph + 16, ... (at most kMaxLseParts / 16), read once
+  constexpr int kPer = kMaxLseParts / 16;
+  float2 q[kPer];
   float mx = -INFINITY;
   int nan = 0;
-  if (live)
-    for (int p = ph; p < P; p += 16) {
-      const float2 q = partials[static_cast<int64_t>(p) * M + m];
-      nan |= (q.x != q.x) | (q.y != q.y);
-      mx = fmaxf(mx, q.x);
-    }
+#pragma unroll
+  for (int i = 0; i < kPer; ++i) {
+    const int p = ph + 16 * i;
+    q[i] = (live && p < P) ? partials[static_cast<int64_t>(p) * M + m] : make_float2(-INFINITY, 0.f);
+    nan |= (q[i].x != q[i].x) | (q[i].y != q[i].y);
+    mx = fmaxf(mx, q[i].x);
+  }
 #pragma unroll
   for (int o = 8; o >= 1; o >>= 1) {
     mx = fmaxf(mx, __shfl_xor(mx, o, 16));
     nan |= __shfl_xor(nan, o, 16);
   }
   double s = 0.0;
-  if (live && mx != -INFINITY)
-    for (int p = ph; p < P; p += 16) {
-      const float2 q = partials[static_cast<int64_t>(p) * M + m];
-      if (q.x != -INFINITY)
-        s += static_cast<double>(q.y) *
-             static_cast<double>(fast_exp2(static_cast<float>(static_cast<double>(q.x) - mx) * kLog2e));
-    }
+  if (mx != -INFINITY)
+#pragma unroll
+    for (int i = 0; i < kPer; ++i)
+      if (q[i].x != -INFINITY)
+        s += static_cast<double>(q[i].y) *
+             static_cast<double>(fast_exp2(static_cast<float>(static_cast<double>(q[i].x) - mx) * kLog2e));
 #pragma unroll
   for (int o = 8; o >= 1; o >>= 1) s += __shfl_xor(s, o, 16);
   if (!live) return;
@@ -189,6 +192,7 @@ lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* _
     const int K = *Kdev;
     const double* zr = Zd + static_cast<int64_t>(m) * ldS;
     float* sr = S + static_cast<int64_t>(m) * ldS;
+#pragma unroll 4
     for (int j = ph; j < K; j += 16) sr[j] = static_cast<float>(zr[j] - l);
   }
 }
@@ -267,6 +271,7 @@ hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const voi
 hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
                                const int32_t* K, float* S, int ldS, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
+  if (P < 1 || P > kMaxLseParts) return hipErrorInvalidValue;  // the kernel holds at most kMaxLseParts
   Prof pr("lse_finalize", stream);
   hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + kFinFrames - 1) / kFinFrames), dim3(256), 0, stream, partials, M,
                      P, lam, lam2, Zd, K, S, ldS);
@@ -792,10 +797,8 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
   if (e != hipSuccess) return e;
   const int slice = ((chunk / plan.splits + 63) / 64) * 64;
-  if (dH) {
-    e = hipMemsetAsync(part, 0, static_cast<size_t>(plan.splits) * M * D * sizeof(float), stream);
-    if (e != hipSuccess) return e;
-  }
+  // split-K slices any chunk fills: the first chunk (the widest) starts them all from zero
+  const int nslices = (min(chunk, V) + slice - 1) / slice;
   for (int c0 = 0; c0 < V; c0 += chunk) {
     const int cw = min(chunk, V - c0);
     e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
@@ -810,7 +813,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
     const int64_t n = static_cast<int64_t>(M) * D;
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
-                       plan.splits, n, dH_extra, dH);
+                       nslices, n, dH_extra, dH);
   }
   return hipGetLastError();
 }

@@ -556,7 +556,7 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
   const int m0 = mt * kBR, d0 = dt * kBC;
   const int kb = s * slice;
   const int ke = min(cw, kb + slice);
-  if (kb >= ke) return;
+  if (kb >= ke && !first) return;  // the first chunk writes every slice (zeros when empty)
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // A: dZ rows (frames), k = vocabulary column; B: W_c viewed as rows d, k = vocabulary row
   const GOp A{dZ, chunk, M, cw, nullptr};

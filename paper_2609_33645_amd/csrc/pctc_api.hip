@@ -297,7 +297,6 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   std::vector<int32_t> toff, yoff;
   std::vector<int64_t> soff;
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
-  PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
   const bool want_bwd = (dH || dW || db);
   int32_t* fflag = Kdev + 2;  // forecast mismatch flag
   const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
@@ -325,14 +324,17 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     PCTC_HIP(hipEventRecord(ev.start, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     double* Zd = reinterpret_cast<double*>(ws + L.o_zd);
-    // Algorithm 1: union and relabel, then the selected logits X W_U^T (+ b_U)
+    // online full-vocabulary log-sum-exp, launched first: it is the longest step
+    int P = 0;
+    PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    // beside it: the lattice offsets, Algorithm 1 (union and relabel), then the selected
+    // logits X W_U^T (+ b_U)
+    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, dps_stream));
     PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, dps_stream));
     PCTC_HIP(launch_gather_s_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), bias,
                                   u_ids, Kdev, L.K_max, nullptr, nullptr, L.ldS, dps_stream, Zd));
     PCTC_HIP(hipEventRecord(ev.sel, dps_stream));
-    // online full-vocabulary log-sum-exp; S = logits - lambda once both are done
-    int P = 0;
-    PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    // S = logits - lambda once both are done
     PCTC_HIP(hipStreamWaitEvent(stream, ev.sel, 0));
     PCTC_HIP(launch_lse_finalize(partials, L.M, P, lam, lam2, Zd, Kdev, S, L.ldS, stream));
     g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
@@ -341,6 +343,7 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     PCTC_HIP(hipEventRecord(ev.fork, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
   } else {
+    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
     // Algorithm 1: union and relabel
     PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
     // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
