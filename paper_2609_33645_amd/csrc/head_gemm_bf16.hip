@@ -372,37 +372,40 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
 // are finite and, with g_m = 0, give zeros) plus the bias when there is one; the few union
 // columns of a tile are then rewritten in the staging buffer as G[m][j] - g_m exp(S[m][j])
 // from the forward's selected log-probabilities.  Columns past cw within the last tile
-// hold finite values that no consumer reads (their W rows read as zero).  Each 256 x 128
-// tile is staged through LDS so that every frame row is stored as contiguous 16-byte
-// vectors.  DB: the staged (rounded) values are also summed over the tile's frames, giving
+// hold finite values that no consumer reads (their W rows read as zero).  Each tile (256
+// vocabulary rows x 128 or 256 frames) is staged through LDS, 32 frames of each 64-frame
+// column group per pass, so that every frame row is stored as contiguous 16-byte vectors.  DB: the staged (rounded) values are also summed over the tile's frames, giving
 // this tile's share of db = dZ^T 1 in dbpart[frame tile][column].
-template <bool BIAS, bool DB>
-__global__ void __launch_bounds__(256, 2)
+template <class GG, bool BIAS, bool DB, int OCC>
+__global__ void __launch_bounds__(GG::kThreads, OCC)
 recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W,
                   const float* __restrict__ bias, int c0, int cw, const float2* __restrict__ lam2,
                   const float* __restrict__ g, const int32_t* __restrict__ remap, const float* __restrict__ S, int ldS,
                   const float* __restrict__ G, int ldG, uint16_t* __restrict__ dZ, int chunk,
                   float* __restrict__ dbpart) {
-  using GG = GFwd;
-  constexpr int FR = GG::FR, FC = GG::FC;
-  constexpr int kPitch = kFR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
-  static_assert(32 * kPitch <= GG::kStageBytes, "staging fits one stage");
-  PCTC_STAGES(GG)
-  const int nMt = (M + kFC - 1) / kFC;
-  const int nVt = (cw + kFR - 1) / kFR;
+  constexpr int FR = GG::FR, FC = GG::FC, TR = GG::kBR, TC = GG::kBC, NT = GG::kThreads;
+  static_assert(TR == 256 && NT % TR == 0, "each thread owns one tile column");
+  constexpr int WC = GG::NW / 2;        // column groups of 64 frames (the wave grid is 2 x WC)
+  constexpr int kPitch = TR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
+  // in each pass, column group q stages its 32 frames in stage q & 1, row block q >> 1
+  static_assert(((WC + 1) / 2) * 32 * kPitch <= GG::kStageBytes, "staging fits two stages");
+  PCTC_STAGES_G(GG)
+  const int nMt = (M + TC - 1) / TC;
+  const int nVt = (cw + TR - 1) / TR;
   int mt, vt;
   if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, nVt, mt, vt)) return;
-  const int m0 = mt * kFC;
-  const int vl0 = vt * kFR;
+  const int m0 = mt * TC;
+  const int vl0 = vt * TR;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // union columns of this tile: (union index << 8) | tile column; b per column
-  __shared__ int ulist[kFR];
+  __shared__ int ulist[TR];
   __shared__ int nu;
-  __shared__ __attribute__((aligned(16))) float bl[BIAS ? kFR : 4];
+  __shared__ __attribute__((aligned(16))) float bl[BIAS ? TR : 4];
+  __shared__ float dbx[(DB && NT > TR) ? NT - TR : 1];
   if (tid == 0) nu = 0;
-  const bool vin = vl0 + tid < cw;
+  const bool vin = tid < TR && vl0 + tid < cw;
   const int jsel = (vin && remap) ? remap[c0 + vl0 + tid] : -1;  // no remap: dense part only
-  if (BIAS) bl[tid] = vin ? bias[c0 + vl0 + tid] : 0.f;
+  if (BIAS && tid < TR) bl[tid] = vin ? bias[c0 + vl0 + tid] : 0.f;
   const int any_sel = __syncthreads_or(jsel >= 0);
   if (any_sel) {
     if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
@@ -422,15 +425,18 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   const GOp B{Hs, D, M, D, nullptr};
   f32x16 acc[FR][FC];
   if (BIAS) {  // the logits' accumulators start at b (visible after the barrier above)
-    bias_init<FR, FC>(acc, bl, wave, lane);
+    bias_init<FR, FC, GG>(acc, bl, wave, lane);
     GG::template run<false>(A, B, vl0, m0, 0, D, st, acc);
   } else {
     GG::run(A, B, vl0, m0, 0, D, st, acc);
   }
+  auto stage_of = [&](int q) -> char* { return ((q & 1) ? st1_ : st0_) + (q >> 1) * (32 * kPitch); };
   const int nunion = any_sel ? nu : 0;
-  const int ch = wave & 1;            // column half: frames [64 ch, 64 ch + 64) of the tile
-  char* stage = ch ? st1_ : st0_;     // 32 frames x 256 vocabulary columns per pass
-  float dbsum = 0.f;                  // DB: column tid of the tile, summed over the passes
+  char* stage = stage_of(wave % WC);  // this wave's frames [64 q, 64 q + 64) of the tile, 32 per pass
+  // DB: column tid % 256 of the tile over column groups [qb, qb + kQPer), summed over the passes
+  constexpr int kQPer = WC / (NT / TR);
+  const int qb = (tid / TR) * kQPer;
+  float dbsum = 0.f;
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     if (j > 0) __syncthreads();  // the previous pass's readers are done
@@ -447,39 +453,40 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
       }
     __syncthreads();
     if (nunion > 0) {
-      // the union columns of the 2 x 32 staged frames
-      for (int idx = tid; idx < nunion * 64; idx += 256) {
-        const int e = ulist[idx >> 6];
+      // the union columns of the WC x 32 staged frames
+      for (int idx = tid; idx < nunion * (WC * 32); idx += NT) {
+        const int e = ulist[idx / (WC * 32)];
         const int col = e & 255, ju = e >> 8;
-        const int half = (idx >> 5) & 1, row = idx & 31;
-        const int m = m0 + 64 * half + 32 * j + row;
+        const int grp = (idx >> 5) % WC, row = idx & 31;
+        const int m = m0 + 64 * grp + 32 * j + row;
         float val = 0.f;
         if (m < M) {
           const float gm = g[m];
           if (gm != 0.f)
             val = G[static_cast<int64_t>(m) * ldG + ju] - gm * fast_exp2(S[static_cast<int64_t>(m) * ldS + ju] * kLog2e);
         }
-        *reinterpret_cast<uint16_t*>((half ? st1_ : st0_) + row * kPitch + col * 2) = f32_to_bf16(val);
+        *reinterpret_cast<uint16_t*>(stage_of(grp) + row * kPitch + col * 2) = f32_to_bf16(val);
       }
       __syncthreads();
     }
     if (DB) {
-      // column tid over the 64 staged frames (frames past M hold zeros)
+      // column tid % 256 over this thread's staged frames (frames past M hold zeros)
+      const int col = tid % TR;
 #pragma unroll 4
-      for (int row = 0; row < 32; ++row) {
-        dbsum += bf16_to_f32(*reinterpret_cast<const uint16_t*>(st0_ + row * kPitch + tid * 2));
-        dbsum += bf16_to_f32(*reinterpret_cast<const uint16_t*>(st1_ + row * kPitch + tid * 2));
-      }
-    }
-    // 2 stages x 32 frames x 32 vectors of 16 bytes
+      for (int row = 0; row < 32; ++row)
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      const int idx = tid + 256 * k;
-      const int half = idx >> 10;
+        for (int q = 0; q < kQPer; ++q)
+          dbsum += bf16_to_f32(*reinterpret_cast<const uint16_t*>(stage_of(qb + q) + row * kPitch + col * 2));
+    }
+    // WC groups x 32 frames x 32 vectors of 16 bytes
+#pragma unroll
+    for (int k = 0; k < (WC * 1024) / NT; ++k) {
+      const int idx = tid + NT * k;
+      const int grp = idx >> 10;
       const int row = (idx >> 5) & 31;
       const int vec = idx & 31;
-      const int mm = m0 + 64 * half + 32 * j + row;
-      const char* src = (half ? st1_ : st0_) + row * kPitch + vec * 16;
+      const int mm = m0 + 64 * grp + 32 * j + row;
+      const char* src = stage_of(grp) + row * kPitch + vec * 16;
       const u32x4 v = *reinterpret_cast<const u32x4*>(src);
       // streaming store: dZ is read back only by the next two products, and keeping its
       // lines out of the caches leaves them to those products' operands
@@ -487,7 +494,17 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
         __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(dZ + static_cast<int64_t>(mm) * chunk + vl0 + vec * 8));
     }
   }
-  if (DB) dbpart[static_cast<int64_t>(mt) * chunk + vl0 + tid] = dbsum;
+  if (DB) {
+    if constexpr (NT > TR) {  // the other threads of each column hand over their share
+      if (tid >= TR) dbx[tid - TR] = dbsum;
+      __syncthreads();
+      if (tid < TR) {
+#pragma unroll
+        for (int p = 1; p < NT / TR; ++p) dbsum += dbx[(p - 1) * TR + tid];
+      }
+    }
+    if (tid < TR) dbpart[static_cast<int64_t>(mt) * chunk + vl0 + tid] = dbsum;
+  }
 }
 
 // db[c0 + v] = sum over frame tiles of dbpart[t][v], v < cw (fixed order).
@@ -888,21 +905,30 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
                                  hipStream_t stream) {
-  const int nMt = (M + kFC - 1) / kFC;
+  // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue)
+  const bool wide = D >= kWideD;
+  const int nMt = (M + (wide ? GWide::kBC : GFwd::kBC) - 1) / (wide ? GWide::kBC : GFwd::kBC);
   {
     const int nVt = (cw + kFR - 1) / kFR;
     const dim3 grid(grouped_grid(nMt, nVt));
     Prof pr("recompute_dz", stream);
-#define PCTC_RECOMPUTE(BI, DBI)                                                                                      \
-  hipLaunchKernelGGL((recompute_dz_bf16<BI, DBI>), grid, dim3(GFwd::kThreads), 0, stream, Hs, M, D, W, bias, c0, cw, \
-                     lam2, g, remap, S, ldS, G, ldG, dZ, chunk, dbpart)
-    if (bias) {
-      if (db) PCTC_RECOMPUTE(true, true);
-      else PCTC_RECOMPUTE(true, false);
+#define PCTC_RECOMPUTE(GC, OCC, BI, DBI)                                                                             \
+  hipLaunchKernelGGL((recompute_dz_bf16<GC, BI, DBI, OCC>), grid, dim3(GC::kThreads), 0, stream, Hs, M, D, W, bias, \
+                     c0, cw, lam2, g, remap, S, ldS, G, ldG, dZ, chunk, dbpart)
+#define PCTC_RECOMPUTE_CFG(GC, OCC)           \
+  if (bias) {                                 \
+    if (db) PCTC_RECOMPUTE(GC, OCC, true, true);  \
+    else PCTC_RECOMPUTE(GC, OCC, true, false);    \
+  } else {                                    \
+    if (db) PCTC_RECOMPUTE(GC, OCC, false, true); \
+    else PCTC_RECOMPUTE(GC, OCC, false, false);   \
+  }
+    if (wide) {
+      PCTC_RECOMPUTE_CFG(GWide, 1)
     } else {
-      if (db) PCTC_RECOMPUTE(false, true);
-      else PCTC_RECOMPUTE(false, false);
+      PCTC_RECOMPUTE_CFG(GFwd, 2)
     }
+#undef PCTC_RECOMPUTE_CFG
 #undef PCTC_RECOMPUTE
   }
   if (db) {

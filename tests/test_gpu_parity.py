@@ -163,12 +163,13 @@ def test_ctc_dp_parity(seed, N, Trange, K, beam, integer):
 # recomputed backward on identical inputs
 # ---------------------------------------------------------------------------------------
 
-@pytest.mark.parametrize("dtype,seed,chunk", [("f32", 0, 256), ("bf16", 1, 512), ("bf16", 2, 0), ("f32", 3, 0)])
-def test_head_bwd_parity(dtype, seed, chunk):
+@pytest.mark.parametrize("dtype,seed,chunk,D", [("f32", 0, 256, 136), ("bf16", 1, 512, 256), ("bf16", 2, 0, 256),
+                                               ("f32", 3, 0, 136), ("bf16", 4, 768, 2056), ("bf16", 5, 0, 2048)])
+def test_head_bwd_parity(dtype, seed, chunk, D):
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(seed, N=4, T_range=(20, 90), D=136 if dtype == "f32" else 256, V=3000,
-                                dtype=dtype, p_repeat=0.1, beam=5.0)
+    wl = workloads.random_small(seed, N=4, T_range=(20, 90) if D < 2048 else (60, 200), D=D, V=3000, dtype=dtype,
+                                p_repeat=0.1, beam=5.0, w_std=None if D < 2048 else 0.5 * math.sqrt(128 / D))
     say(f"head_bwd {dtype} seed={seed} M={wl.M} D={wl.D} V={wl.V} chunk={chunk}")
     full = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, 0, beam=wl.beam,
                           want_grads=False)
