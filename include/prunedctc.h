@@ -157,8 +157,10 @@ int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t 
  * lam[m] = log sum_v exp (H W^T)[m, v] in double; S[m, j] = float(Z[m, u_ids[j]] - lam[m])
  * with the subtraction in double and one rounding to float, for j < K (K read from the
  * device scalar), S row pitch ldS >= K_max.  K_max bounds K (1 + total targets).
- * partials: device scratch of pctc_lse_scratch_bytes(M) bytes. */
-size_t pctc_lse_scratch_bytes(int32_t M);
+ * partials: device scratch of pctc_lse_scratch_bytes(M, D) bytes (8 bytes per frame and
+ * vocabulary partition: 256 partitions, 1024 for D >= 2048; independent of V).  Returns 0
+ * for M < 0 or D <= 0. */
+size_t pctc_lse_scratch_bytes(int32_t M, int32_t D);
 int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W,
                         int32_t V, const int32_t* u_ids, const int32_t* K, int32_t K_max,
                         double* lam, float* S, int32_t ldS, void* partials, void* stream);
@@ -187,9 +189,9 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
  * ids: device int32 [M] or NULL: the per-frame argmax.  tokens: device int32 [M]: utterance
  * n's sequence occupies [o_n, o_n + token_lengths[n]) with o_n = sum of the earlier
  * input_lengths; the rest is unspecified.  token_lengths: device int32 [N].
- * workspace: pctc_greedy_workspace_size(N, M) bytes, 256-byte aligned.
+ * workspace: pctc_greedy_workspace_size(N, M, D) bytes, 256-byte aligned (independent of V).
  * NaN logits give an unspecified id for their frame.  Synchronises the stream. */
-size_t pctc_greedy_workspace_size(int32_t N, int32_t M);
+size_t pctc_greedy_workspace_size(int32_t N, int32_t M, int32_t D);
 int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const void* W,
                            const float* bias, int32_t V, const int32_t* input_lengths, int32_t N,
                            int32_t blank, int32_t* ids, int32_t* tokens, int32_t* token_lengths,

@@ -145,6 +145,7 @@ lse_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__ 
 // (each term's exponent taken in float on the exact difference to the maximum).  With Zd,
 // also S[m][j] = float(Zd[m][j] - lambda_m) for j < *K (one rounding).
 constexpr int kFinFrames = 16;
+template <int PER>  // partitions per lane held in registers: P <= 16 PER
 __global__ void __launch_bounds__(256)
 lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
                     float2* __restrict__ lam2, const double* __restrict__ Zd, const int32_t* __restrict__ Kdev,
@@ -152,8 +153,8 @@ lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* _
   const int ph = threadIdx.x & 15;
   const int m = blockIdx.x * kFinFrames + (threadIdx.x >> 4);
   const bool live = m < M;
-  // this lane's partitions ph, ph + 16, ... (at most kMaxLseParts / 16), read once
-  constexpr int kPer = kMaxLseParts / 16;
+  // this lane's partitions ph, ph + 16, ... (at most PER), read once
+  constexpr int kPer = PER;
   float2 q[kPer];
   float mx = -INFINITY;
   int nan = 0;
@@ -217,7 +218,9 @@ int lse_partitions(int M, int V) {
   return P;
 }
 
-size_t lse_partial_bytes(int M) { return align_up(static_cast<size_t>(kMaxLseParts) * M * sizeof(float2), 256); }
+size_t lse_partial_bytes(int M, int D) {
+  return align_up(static_cast<size_t>(lse_max_parts(D)) * M * sizeof(float2), 256);
+}
 
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
@@ -271,10 +274,14 @@ hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const voi
 hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
                                const int32_t* K, float* S, int ldS, hipStream_t stream) {
   if (M <= 0) return hipSuccess;
-  if (P < 1 || P > kMaxLseParts) return hipErrorInvalidValue;  // the kernel holds at most kMaxLseParts
+  if (P < 1 || P > kMaxLseParts) return hipErrorInvalidValue;
   Prof pr("lse_finalize", stream);
-  hipLaunchKernelGGL(lse_finalize_kernel, dim3((M + kFinFrames - 1) / kFinFrames), dim3(256), 0, stream, partials, M,
-                     P, lam, lam2, Zd, K, S, ldS);
+  const dim3 grid((M + kFinFrames - 1) / kFinFrames);
+  if (P <= 256)
+    hipLaunchKernelGGL(lse_finalize_kernel<16>, grid, dim3(256), 0, stream, partials, M, P, lam, lam2, Zd, K, S, ldS);
+  else
+    hipLaunchKernelGGL(lse_finalize_kernel<kMaxLseParts / 16>, grid, dim3(256), 0, stream, partials, M, P, lam, lam2,
+                       Zd, K, S, ldS);
   return hipGetLastError();
 }
 
@@ -355,31 +362,52 @@ amax_partial_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__
 }
 
 // ids[m]: the best of the partitions' (value, id) pairs, in partition order.
-__global__ void amax_finalize_kernel(const float2* __restrict__ partials, int M, int P, int32_t* __restrict__ ids) {
-  const int m = blockIdx.x * blockDim.x + threadIdx.x;
-  if (m >= M) return;
+// 16 frames per block, 16 lanes per frame splitting the partitions; the merge (larger value,
+// then smaller id) is order-independent, so the result does not depend on the split.
+__global__ void __launch_bounds__(256)
+amax_finalize_kernel(const float2* __restrict__ partials, int M, int P, int32_t* __restrict__ ids) {
+  const int ph = threadIdx.x & 15;
+  const int m = blockIdx.x * kFinFrames + (threadIdx.x >> 4);
+  const bool live = m < M;
   float bv = -INFINITY;
   int bi = 0x7fffffff;
-  for (int p = 0; p < P; ++p) {
-    const float2 q = partials[static_cast<int64_t>(p) * M + m];
-    amax_merge_g(bv, bi, q.x, __float_as_int(q.y));
+  if (live) {
+#pragma unroll 4
+    for (int p = ph; p < P; p += 16) {
+      const float2 q = partials[static_cast<int64_t>(p) * M + m];
+      amax_merge_g(bv, bi, q.x, __float_as_int(q.y));
+    }
   }
-  ids[m] = (bi == 0x7fffffff) ? 0 : bi;
+#pragma unroll
+  for (int o = 8; o >= 1; o >>= 1) {
+    const float ov = __shfl_xor(bv, o, 16);
+    const int oi = __shfl_xor(bi, o, 16);
+    amax_merge_g(bv, bi, ov, oi);
+  }
+  if (live && ph == 0) ids[m] = (bi == 0x7fffffff) ? 0 : bi;
 }
 
-// One thread per utterance walks its frames in order (lengths are at most a few thousand).
-__global__ void ctc_collapse_kernel(const int32_t* __restrict__ ids, const int32_t* __restrict__ toff, int N,
-                                    int blank, int32_t* __restrict__ tokens, int32_t* __restrict__ lengths) {
-  const int n = blockIdx.x * blockDim.x + threadIdx.x;
+// One wavefront per utterance: frame m keeps its id when it is not blank and differs from
+// the previous frame's (Sec. 3.1), and a ballot prefix count gives its output position.
+__global__ void __launch_bounds__(256)
+ctc_collapse_kernel(const int32_t* __restrict__ ids, const int32_t* __restrict__ toff, int N, int blank,
+                    int32_t* __restrict__ tokens, int32_t* __restrict__ lengths) {
+  const int lane = threadIdx.x & 63;
+  const int n = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (n >= N) return;
   const int t0 = toff[n], t1 = toff[n + 1];
-  int k = 0, prev = -1;
-  for (int m = t0; m < t1; ++m) {
-    const int c = ids[m];
-    if (c != prev && c != blank) tokens[t0 + k++] = c;
-    prev = c;
+  int k = 0;
+  for (int b = t0; b < t1; b += 64) {
+    const int m = b + lane;
+    const int c = (m < t1) ? ids[m] : blank;
+    const int prev = (m > t0 && m < t1) ? ids[m - 1] : -1;
+    const bool keep = c != blank && c != prev;
+    const uint64_t mask = __ballot(keep);
+    const int before = __popcll(mask & ((uint64_t{1} << lane) - 1));
+    if (keep) tokens[t0 + k + before] = c;
+    k += __popcll(mask);
   }
-  lengths[n] = k;
+  if (lane == 0) lengths[n] = k;
 }
 
 hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
@@ -403,11 +431,12 @@ hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, 
                          partials);
     }
     Prof pr("amax_finalize", stream);
-    hipLaunchKernelGGL(amax_finalize_kernel, dim3((M + 255) / 256), dim3(256), 0, stream, partials, M, Pfin, ids);
+    hipLaunchKernelGGL(amax_finalize_kernel, dim3((M + kFinFrames - 1) / kFinFrames), dim3(256), 0, stream, partials,
+                       M, Pfin, ids);
   }
   if (N > 0) {
     Prof pr("ctc_collapse", stream);
-    hipLaunchKernelGGL(ctc_collapse_kernel, dim3((N + 63) / 64), dim3(64), 0, stream, ids, toff, N, blank, tokens,
+    hipLaunchKernelGGL(ctc_collapse_kernel, dim3((N + 3) / 4), dim3(256), 0, stream, ids, toff, N, blank, tokens,
                        lengths);
   }
   return hipGetLastError();

@@ -31,10 +31,10 @@ constexpr int kBK = 32;
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 // 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
 using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4>;
-// normaliser for wide heads (D >= kWideD): the k loop is long enough that the epilogue is a
-// small share, so one 8-wave 256 x 256 workgroup per CU beats two 4-wave ones
+// logit products of wide heads (D >= kWideD: normaliser, argmax, recompute): the k loop is
+// long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
+// beats two 4-wave ones
 using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
-constexpr int kWideD = 2048;
 using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4>;
 
 #define PCTC_STAGES2(G)                                                  \
@@ -819,10 +819,13 @@ hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t
 // ---------------------------------------------------------------------------------------
 
 // Vocabulary split of a normaliser or argmax launch: each workgroup takes a run of vper / 256
-// vocabulary tiles for one frame tile (partition p covers rows [p vper, (p + 1) vper)), the
-// fewest runs that keep the partition count within the partial buffer.  (Runs chosen instead
-// to fill the last round of workgroups evenly measured slower: the run length also sets the
-// L2 reuse of the tile order.)
+// vocabulary tiles for one frame tile (partition p covers rows [p vper, (p + 1) vper)).  Wide
+// heads: one tile per workgroup while the partitions fit the partial buffer (the long k
+// loop makes a workgroup's start-up cost small; shorter runs also spread the last tiles
+// better).  Narrow heads: the fewest runs within 256 partitions, so that each workgroup's
+// copy pipeline runs through several tiles.  (Runs chosen to fill the last round of
+// workgroups evenly measured slower for narrow heads: the run length also sets the L2 reuse
+// of the tile order.)
 struct LseSplit {
   bool wide;  // one 8-wave 256 x 256 workgroup per CU; else two 4-wave 256 x 128
   int vper, P, nM;
@@ -834,7 +837,8 @@ static LseSplit lse_split_bf16(int M, int D, int V) {
   const int TR = s.wide ? GWide::kBR : GFwd::kBR, TC = s.wide ? GWide::kBC : GFwd::kBC;
   const int vtiles = (V + TR - 1) / TR;
   s.nM = (M + TC - 1) / TC;
-  s.vper = ((vtiles + kMaxLseParts - 1) / kMaxLseParts) * TR;
+  const int maxp = s.wide ? lse_max_parts(D) : 256;
+  s.vper = ((vtiles + maxp - 1) / maxp) * TR;
   s.P = (V + s.vper - 1) / s.vper;
   return s;
 }

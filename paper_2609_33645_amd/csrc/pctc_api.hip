@@ -147,7 +147,7 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.o_small = take(64);
   L.o_status = take(static_cast<size_t>(N) * 4);
   L.o_lossn = take(static_cast<size_t>(N) * 8);
-  L.o_part = take(lse_partial_bytes(L.M));
+  L.o_part = take(lse_partial_bytes(L.M, D));
   L.o_lam = take(static_cast<size_t>(L.M) * 8);
   L.o_lam2 = take(static_cast<size_t>(L.M) * 8);
   L.o_S = take(static_cast<size_t>(L.M) * L.ldS * 4);
@@ -403,8 +403,9 @@ int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t 
   return herr ? PCTC_ELABEL : PCTC_OK;
 }
 
-size_t pctc_lse_scratch_bytes(int32_t M) {
-  return M < 0 ? 0 : lse_partial_bytes(M) + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(float2), 256);
+size_t pctc_lse_scratch_bytes(int32_t M, int32_t D) {
+  return (M < 0 || D <= 0) ? 0
+                           : lse_partial_bytes(M, D) + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(float2), 256);
 }
 
 int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
@@ -416,7 +417,7 @@ int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, c
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
   // scratch = [partials][lam2]
-  float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(partials) + lse_partial_bytes(M));
+  float2* lam2 = reinterpret_cast<float2*>(static_cast<char*>(partials) + lse_partial_bytes(M, D));
   PCTC_HIP(launch_lse(dt, H, M, D, W, nullptr, V, static_cast<float2*>(partials), lam, lam2, stream));
   if (S && u_ids && K) PCTC_HIP(launch_gather_s(dt, H, M, D, W, nullptr, u_ids, K, K_max, lam, S, ldS, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
@@ -456,17 +457,17 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
 }
 
 // Greedy decode workspace: argmax partials, frame offsets, and the ids when not returned.
-static size_t greedy_layout(int32_t N, int32_t M, size_t* o_toff, size_t* o_ids) {
-  const size_t part = lse_partial_bytes(M > 0 ? M : 1);
+static size_t greedy_layout(int32_t N, int32_t M, int32_t D, size_t* o_toff, size_t* o_ids) {
+  const size_t part = lse_partial_bytes(M > 0 ? M : 1, D);
   *o_toff = part;
   *o_ids = part + align_up(static_cast<size_t>(N + 1) * sizeof(int32_t), 256);
   return *o_ids + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(int32_t), 256);
 }
 
-size_t pctc_greedy_workspace_size(int32_t N, int32_t M) {
-  if (N < 0 || M < 0) return 0;
+size_t pctc_greedy_workspace_size(int32_t N, int32_t M, int32_t D) {
+  if (N < 0 || M < 0 || D <= 0) return 0;
   size_t a, b;
-  return greedy_layout(N, M, &a, &b);
+  return greedy_layout(N, M, D, &a, &b);
 }
 
 int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
@@ -485,7 +486,7 @@ int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const voi
   const int M = static_cast<int>(M64);
   if (M > 0 && (!H || !tokens || !token_lengths)) return PCTC_EINVAL;
   size_t o_toff, o_ids;
-  const size_t need = greedy_layout(N, M, &o_toff, &o_ids);
+  const size_t need = greedy_layout(N, M, D, &o_toff, &o_ids);
   if (!workspace || workspace_bytes < need) return PCTC_EWORKSPACE;
   if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
   if (N == 0) return PCTC_OK;
@@ -605,7 +606,7 @@ static GroupedLayout grouped_layout(int dt, int M, int D, int V, int K, int chun
   L.plan = plan_bwd(dt, M, D, V, chunk);
   L.o_remap = 256;
   L.o_part = L.o_remap + align_up(static_cast<size_t>(V) * 4, 256);
-  L.o_lamo = L.o_part + lse_partial_bytes(M);
+  L.o_lamo = L.o_part + lse_partial_bytes(M, D);
   L.o_lam2f = L.o_lamo + m8;
   L.o_zero = L.o_lam2f + m8;
   L.o_bo = L.o_zero + m8;

@@ -33,9 +33,13 @@ hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t bla
 
 // ---- normaliser and selected log-probabilities ------------------------------------------
 int lse_partitions(int M, int V);
-// most vocabulary partitions of a normaliser or argmax launch (partial buffer rows)
-constexpr int kMaxLseParts = 256;
-size_t lse_partial_bytes(int M);
+// Heads with D >= kWideD run their bf16 products on 8-wave 256 x 256 tiles.
+constexpr int kWideD = 2048;
+// Most vocabulary partitions of a normaliser or argmax launch (partial buffer rows): 256,
+// or kMaxLseParts for wide heads (one vocabulary tile per workgroup there).
+constexpr int kMaxLseParts = 1024;
+inline int lse_max_parts(int D) { return D >= kWideD ? kMaxLseParts : 256; }
+size_t lse_partial_bytes(int M, int D);
 // bias: device float [V] or null (logits H W^T + b).
 hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                       float2* partials, double* lam, float2* lam2, hipStream_t stream);
@@ -51,7 +55,7 @@ hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W
                            hipStream_t stream);
 
 // ---- greedy emission head -----------------------------------------------------------------
-// partials: lse_partial_bytes(M); ids [M]; tokens [M] (utterance n at toff[n]); lengths [N].
+// partials: lse_partial_bytes(M, D); ids [M]; tokens [M] (utterance n at toff[n]); lengths [N].
 hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                          const int32_t* toff, int N, int blank, float2* partials, int32_t* ids, int32_t* tokens,
                          int32_t* lengths, hipStream_t stream);

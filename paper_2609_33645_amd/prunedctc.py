@@ -60,7 +60,7 @@ def lib() -> ctypes.CDLL:
     L.pctc_last_error.restype = ctypes.c_char_p
     L.pctc_union_remap.argtypes = [c_p, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_union_remap.restype = c_i32
-    L.pctc_lse_scratch_bytes.argtypes = [c_i32]
+    L.pctc_lse_scratch_bytes.argtypes = [c_i32, c_i32]
     L.pctc_lse_scratch_bytes.restype = c_sz
     L.pctc_lse_select.argtypes = [c_i32, c_p, c_i32, c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p, c_i32, c_p, c_p]
     L.pctc_lse_select.restype = c_i32
@@ -68,7 +68,7 @@ def lib() -> ctypes.CDLL:
     L.pctc_dp_scratch_bytes.restype = c_sz
     L.pctc_ctc_dp.argtypes = [c_p, c_i32, c_i32, c_p, i32p, i32p, c_i32, c_f, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_ctc_dp.restype = c_i32
-    L.pctc_greedy_workspace_size.argtypes = [c_i32, c_i32]
+    L.pctc_greedy_workspace_size.argtypes = [c_i32, c_i32, c_i32]
     L.pctc_greedy_workspace_size.restype = c_sz
     L.pctc_greedy_decode.argtypes = [c_i32, c_p, c_i32, c_p, c_p, c_i32, i32p, c_i32, c_i32, c_p, c_p, c_p, c_p, c_sz,
                                      c_p]
@@ -266,7 +266,7 @@ def lse_select(H: torch.Tensor, W: torch.Tensor, u_ids: Optional[torch.Tensor] =
     V = int(W.shape[0])
     dev = H.device
     lam = torch.empty(max(M, 1), dtype=torch.float64, device=dev)
-    scratch = _workspace(int(L.pctc_lse_scratch_bytes(M)), dev)
+    scratch = _workspace(int(L.pctc_lse_scratch_bytes(M, D)), dev)
     S = Kdev = None
     K = 1
     ldS = 1
@@ -337,7 +337,7 @@ def greedy_decode(H: torch.Tensor, W: torch.Tensor, input_lengths, blank: int = 
     ids = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
     tokens = torch.empty(max(M, 1), dtype=torch.int32, device=dev)
     lengths = torch.empty(max(N, 1), dtype=torch.int32, device=dev)
-    ws = _workspace(int(L.pctc_greedy_workspace_size(N, M)), dev)
+    ws = _workspace(int(L.pctc_greedy_workspace_size(N, M, D)), dev)
     code = L.pctc_greedy_decode(dt, _ptr(H), D, _ptr(W), _ptr(bias), V, _i32p(T), N, int(blank), _ptr(ids),
                                 _ptr(tokens), _ptr(lengths), ctypes.c_void_p(ws.data_ptr()), ctypes.c_size_t(ws.numel()),
                                 _stream(stream))
