@@ -760,21 +760,36 @@ dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restr
     fin[q] = valid[q] && s >= Sp - 2;
   }
   double af[Q], ap[Q];  // full and retained forward sums, scaled per frame
-  for (int t = 0; t < T; ++t) {
+  // emissions and arc flags of frame t + 1 are loaded while frame t is computed
+  float e_nx[Q];
+  int mk_nx[Q];
+  auto load_frame = [&](int t) {
     const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
-    float e[Q];
-    int mk[Q];
-    float em = -INFINITY;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-      e[q] = valid[q] ? row[col[q]] : -INFINITY;
-      mk[q] = valid[q] ? static_cast<int>(mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q]) : 0;
-      em = fmaxf(em, e[q]);
+      e_nx[q] = valid[q] ? row[col[q]] : -INFINITY;
+      mk_nx[q] = valid[q] ? static_cast<int>(mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q]) : 0;
     }
-    em = wave_max(em);
+  };
+  if (T > 0) load_frame(0);
+  for (int t = 0; t < T; ++t) {
+    float e[Q];
+    int mk[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      e[q] = e_nx[q];
+      mk[q] = mk_nx[q];
+    }
+    if (t + 1 < T) load_frame(t + 1);
+    // exp(e) in double over the whole range without a per-frame shift: 2^x = 2^i 2^(x - i),
+    // i = floor(x), the fraction's power in float and the integer one exact
     double pe[Q];
 #pragma unroll
-    for (int q = 0; q < Q; ++q) pe[q] = valid[q] ? static_cast<double>(fast_exp2((e[q] - em) * kLog2e)) : 0.0;
+    for (int q = 0; q < Q; ++q) {
+      const float x = e[q] * kLog2e;
+      const float fi = fminf(fmaxf(floorf(x), -2000.f), 2000.f);
+      pe[q] = (valid[q] && x > -INFINITY) ? ldexp(static_cast<double>(fast_exp2(x - fi)), static_cast<int>(fi)) : 0.0;
+    }
     double nf[Q], np[Q];
     if (t == 0) {
 #pragma unroll
@@ -804,7 +819,8 @@ dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restr
 #pragma unroll
     for (int q = 0; q < Q; ++q) c = fmax(c, nf[q]);
     c = wave_max_d(c);
-    const double inv = (c > 0.0) ? 1.0 / c : 0.0;
+    // any positive scale serves (both sums take the same one): an approximate reciprocal
+    const double inv = (c > 0.0) ? __builtin_amdgcn_rcp(c) : 0.0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       af[q] = nf[q] * inv;
