@@ -530,8 +530,9 @@ hipError_t launch_loss_reduce(int N, const double* loss_n, const int32_t* status
 // Inclusion forecast.  For an included utterance every frame's occupancies sum to one
 // (each retained alignment occupies exactly one state per frame), so g_m = -w_n there and
 // 0 on excluded utterances.  Before the lattice runs, an utterance is forecast included when
-// its targets fit its frames (T_n >= U_n + repeats), every frame has a finite normaliser,
-// and w_n != 0; the lattice's statuses are checked against the forecast afterwards.
+// its targets fit its frames (T_n >= U_n + repeats), w_n != 0 and, when lam is given, every
+// frame has a finite normaliser (else a nonfinite normaliser shows up in the lattice's
+// status); the lattice's statuses are checked against the forecast afterwards.
 // ---------------------------------------------------------------------------------------
 __global__ void __launch_bounds__(256)
 g_forecast_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ yoff, const int32_t* __restrict__ y_rel,
@@ -542,10 +543,11 @@ g_forecast_kernel(const int32_t* __restrict__ toff, const int32_t* __restrict__ 
   const int y0 = yoff[n], U = yoff[n + 1] - y0;
   int reps = 0, bad = 0;
   for (int i = 1 + threadIdx.x; i < U; i += blockDim.x) reps += (y_rel[y0 + i] == y_rel[y0 + i - 1]);
-  for (int t = threadIdx.x; t < T; t += blockDim.x) {
-    const double l = lam[t0 + t];
-    bad |= !(l > -INFINITY && l < INFINITY);  // NaN fails both
-  }
+  if (lam)
+    for (int t = threadIdx.x; t < T; t += blockDim.x) {
+      const double l = lam[t0 + t];
+      bad |= !(l > -INFINITY && l < INFINITY);  // NaN fails both
+    }
   __shared__ int sreps;
   if (threadIdx.x == 0) sreps = 0;
   __syncthreads();

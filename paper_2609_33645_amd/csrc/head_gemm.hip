@@ -811,35 +811,64 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* 
   return hipGetLastError();
 }
 
+uint16_t* bwd_hs(void* scratch, const BwdPlan& plan) {
+  return reinterpret_cast<uint16_t*>(static_cast<char*>(scratch) + plan.dz_bytes);
+}
+
 static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                 const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                                 const float* S, int ldS, float* dH, float* dW, float* db, char* scratch,
-                                const BwdPlan& plan, hipStream_t stream, const float* dH_extra,
-                                hipEvent_t before_reduce) {
+                                const BwdPlan& plan, hipStream_t stream, const BwdSide* side) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
-  uint16_t* Hs = reinterpret_cast<uint16_t*>(scratch + plan.dz_bytes);
+  uint16_t* Hs = bwd_hs(scratch, plan);
   float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
   float* dbpart = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes + plan.part_bytes + plan.lam2_bytes);
   const int chunk = plan.chunk;
+  const bool two = side && side->stream;
   hipError_t e;
   // Hs: H with the rows of excluded frames zeroed (read by the recompute and by dW)
-  e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
-  if (e != hipSuccess) return e;
+  if (!(side && side->hs_built)) {
+    e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
+    if (e != hipSuccess) return e;
+  }
   const int slice = ((chunk / plan.splits + 63) / 64) * 64;
   // split-K slices any chunk fills: the first chunk (the widest) starts them all from zero
   const int nslices = (min(chunk, V) + slice - 1) / slice;
+  const int64_t n = static_cast<int64_t>(M) * D;
+  const float* dH_extra = side ? side->dH_extra : nullptr;
   for (int c0 = 0; c0 < V; c0 += chunk) {
     const int cw = min(chunk, V - c0);
-    e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                              dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
-    if (e != hipSuccess) return e;
+    const bool last = c0 + chunk >= V;
+    if (last && two && dH) {
+      // the last chunk's dW product runs beside the final dH reduction (second stream)
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+                                true, true, false, dW, db, dbpart, stream);
+      if (e != hipSuccess) return e;
+      if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
+      if ((e = hipStreamWaitEvent(side->stream, side->dh_done, 0)) != hipSuccess) return e;
+      {
+        Prof pr("dh_reduce", side->stream);
+        hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, side->stream,
+                           part, nslices, n, dH_extra, dH);
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+      }
+      if (dW) {
+        e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+                                  false, false, true, dW, db, dbpart, stream);
+        if (e != hipSuccess) return e;
+      }
+    } else {
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+                                true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
+      if (e != hipSuccess) return e;
+    }
   }
-  if (before_reduce) {
-    e = hipStreamWaitEvent(stream, before_reduce, 0);
-    if (e != hipSuccess) return e;
-  }
-  if (dH) {
-    const int64_t n = static_cast<int64_t>(M) * D;
+  if (two) {
+    // the second stream's work (its union-column part and, with dH, the reduction) is done
+    // before this call's work on the caller's stream is
+    if ((e = hipEventRecord(side->reduced, side->stream)) != hipSuccess) return e;
+    if ((e = hipStreamWaitEvent(stream, side->reduced, 0)) != hipSuccess) return e;
+  } else if (dH) {
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
                        nslices, n, dH_extra, dH);
@@ -850,7 +879,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                            const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                            const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
-                           const BwdPlan& plan, hipStream_t stream, const float* dH_extra, hipEvent_t before_reduce) {
+                           const BwdPlan& plan, hipStream_t stream, const BwdSide* side) {
   if (M <= 0) {
     if (db) {
       hipError_t e = hipMemsetAsync(db, 0, static_cast<size_t>(V) * sizeof(float), stream);
@@ -862,7 +891,7 @@ hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W
   char* sc = static_cast<char*>(scratch);
   if (dtype == 1)
     return head_bwd_bf16(static_cast<const uint16_t*>(H), M, D, static_cast<const uint16_t*>(W), bias, V, lam2, G, ldG,
-                         g, remap, S, ldS, dH, dW, db, sc, plan, stream, dH_extra, before_reduce);
+                         g, remap, S, ldS, dH, dW, db, sc, plan, stream, side);
   return head_bwd_t<float>(static_cast<const float*>(H), M, D, static_cast<const float*>(W), bias, V, lam2, G, ldG, g,
                            remap, dH, dW, db, sc, plan, stream);
 }

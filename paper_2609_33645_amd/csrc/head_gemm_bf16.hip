@@ -760,9 +760,9 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
 size_t union_corr_bytes(int M, int D, int K_max) { return union_corr_layout(M, D, K_max).total; }
 
 hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, int M, int D,
-                                  bool want_dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
-                                  hipStream_t stream) {
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, const uint16_t* Hs,
+                                  int M, int D, bool want_dH, bool want_dW, bool want_db, void* scratch,
+                                  float** dH_u, hipStream_t stream) {
   *dH_u = nullptr;
   if (M <= 0 || K_max <= 0) return hipSuccess;
   const UnionCorrLayout L = union_corr_layout(M, D, K_max);
@@ -785,9 +785,13 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
                        *dH_u, dh_xcd_rows(M, D));
   }
   if (want_dW) {
-    uint16_t* Hs2 = reinterpret_cast<uint16_t*>(sc + L.o_hs);
-    hipError_t e = launch_hs_build_bf16(H, M, D, g, Hs2, stream);
-    if (e != hipSuccess) return e;
+    const uint16_t* Hs2 = Hs;
+    if (!Hs2) {
+      uint16_t* own = reinterpret_cast<uint16_t*>(sc + L.o_hs);
+      hipError_t e = launch_hs_build_bf16(H, M, D, g, own, stream);
+      if (e != hipSuccess) return e;
+      Hs2 = own;
+    }
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dw", stream);
     hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,
@@ -907,12 +911,12 @@ hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t*
 hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
-                                 int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
-                                 hipStream_t stream) {
+                                 int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
+                                 float* dbpart, hipStream_t stream) {
   // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue)
   const bool wide = D >= kWideD;
   const int nMt = (M + (wide ? GWide::kBC : GFwd::kBC) - 1) / (wide ? GWide::kBC : GFwd::kBC);
-  {
+  if (recompute) {
     const int nVt = (cw + kFR - 1) / kFR;
     const dim3 grid(grouped_grid(nMt, nVt));
     Prof pr("recompute_dz", stream);
@@ -935,7 +939,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
 #undef PCTC_RECOMPUTE_CFG
 #undef PCTC_RECOMPUTE
   }
-  if (db) {
+  if (db && recompute) {
     Prof pr("db_reduce", stream);
     hipLaunchKernelGGL(db_reduce_bf16, dim3((cw + 255) / 256), dim3(256), 0, stream, dbpart, nMt, chunk, cw, db + c0);
   }

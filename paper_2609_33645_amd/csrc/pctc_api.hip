@@ -302,24 +302,26 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
   hipStream_t dps_stream = stream;
   struct Events {
-    hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, join = nullptr;
+    hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, dh_done = nullptr, join = nullptr;
     ~Events() {
-      for (hipEvent_t e : {start, sel, fork, join})
+      for (hipEvent_t e : {start, sel, fork, dh_done, join})
         if (e) hipEventDestroy(e);
     }
   } ev;
   float* g_pred = nullptr;
   if (overlap) {
-    // Two streams.  Second stream: union/relabel and the selected logits (beside the
-    // normaliser pass), later the lattice and the union columns' part of the backward.
-    // Caller's stream: the normaliser, S = logits - lambda, a forecast of g (-w_n on included
-    // utterances), and the dense part -g p of the backward beside the lattice.  A wrong
-    // forecast (rare: a -inf logit on a selected class) is caught and the backward is redone
-    // in the plain order.
+    // Two streams.  Second stream: union/relabel, a forecast of g (-w_n on included
+    // utterances) and the masked copy of H it implies, the selected logits (all beside the
+    // normaliser pass), later the lattice, the union columns' part of the backward and the
+    // final dH reduction.  Caller's stream: the normaliser, S = logits - lambda, and the dense
+    // part -g p of the backward beside the lattice.  A wrong forecast (rare: a nonfinite
+    // normaliser or a -inf logit on a selected class) is caught and the backward is redone in
+    // the plain order.
     PCTC_HIP(side_stream(&dps_stream));
     PCTC_HIP(hipEventCreateWithFlags(&ev.start, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.sel, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.dh_done, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
     PCTC_HIP(hipEventRecord(ev.start, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
@@ -327,19 +329,21 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     // online full-vocabulary log-sum-exp, launched first: it is the longest step
     int P = 0;
     PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
-    // beside it: the lattice offsets, Algorithm 1 (union and relabel), then the selected
-    // logits X W_U^T (+ b_U)
+    // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
+    // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
     PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, dps_stream));
     PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, dps_stream));
+    g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
+    int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
+    PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, nullptr, utt_weight, g_pred, pred, dps_stream));
+    if (dH || dW)
+      PCTC_HIP(launch_hs_build_bf16(static_cast<const uint16_t*>(H), L.M, D, g_pred, bwd_hs(bws, L.bwd), dps_stream));
     PCTC_HIP(launch_gather_s_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), bias,
                                   u_ids, Kdev, L.K_max, nullptr, nullptr, L.ldS, dps_stream, Zd));
     PCTC_HIP(hipEventRecord(ev.sel, dps_stream));
     // S = logits - lambda once both are done
     PCTC_HIP(hipStreamWaitEvent(stream, ev.sel, 0));
     PCTC_HIP(launch_lse_finalize(partials, L.M, P, lam, lam2, Zd, Kdev, S, L.ldS, stream));
-    g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
-    int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
-    PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, lam, utt_weight, g_pred, pred, stream));
     PCTC_HIP(hipEventRecord(ev.fork, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
   } else {
@@ -361,16 +365,23 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   if (overlap) {
     PCTC_HIP(launch_forecast_check(N, status, utt_weight, reinterpret_cast<int32_t*>(ws + L.o_pred), fflag,
                                    dps_stream));
-    // the union columns' part of the backward, from the lattice's G, still beside the dense part
+    // the union columns' part of the backward, from the lattice's G, still beside the dense
+    // part (its frames with g == 0 are those of the forecast unless the check fails, and then
+    // the backward is redone)
     float* dH_u = nullptr;
     PCTC_HIP(launch_union_part_bf16(G, L.ldS, g, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
-                                    static_cast<const uint16_t*>(H), L.M, D, dH != nullptr, dW != nullptr,
-                                    db != nullptr, ws + L.o_corr, &dH_u, dps_stream));
-    PCTC_HIP(hipEventRecord(ev.join, dps_stream));
-    // dense part, chunk by chunk, on the caller's stream; its final dH reduction adds dH_u
+                                    static_cast<const uint16_t*>(H), bwd_hs(bws, L.bwd), L.M, D, dH != nullptr,
+                                    dW != nullptr, db != nullptr, ws + L.o_corr, &dH_u, dps_stream));
+    // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds
+    // dH_u, runs on the second stream beside the last dW product
+    BwdSide side;
+    side.stream = dps_stream;
+    side.dh_done = ev.dh_done;
+    side.reduced = ev.join;
+    side.dH_extra = dH_u;
+    side.hs_built = (dH || dW);
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, nullptr, L.ldS, g_pred, nullptr, nullptr, L.ldS, dH, dW,
-                             db, bws, L.bwd, stream, dH_u, ev.join));
-    PCTC_HIP(hipStreamWaitEvent(stream, ev.join, 0));
+                             db, bws, L.bwd, stream, &side));
     PCTC_HIP(launch_union_merge_bf16(Kdev, L.K_max, u_ids, L.M, D, dW, db, ws + L.o_corr, stream));
   } else if (want_bwd) {
     // backward: chunk by chunk recomputation

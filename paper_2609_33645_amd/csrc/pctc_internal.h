@@ -70,15 +70,26 @@ struct BwdPlan {
   size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
+// The bf16 fused schedule's side of the recomputed backward.  With a second stream, the last
+// chunk records dh_done after its dH product; the second stream then waits for it, runs the
+// final dH reduction (adding dH_extra, the union-column part, which that stream computed
+// earlier) beside the chunk's dW product, and records reduced, which the caller's stream
+// waits for before the call returns.  hs_built: the masked copy of H (bwd_hs) was already
+// written, from the same g, on a stream the caller's stream has waited for.
+struct BwdSide {
+  hipStream_t stream = nullptr;
+  hipEvent_t dh_done = nullptr, reduced = nullptr;
+  const float* dH_extra = nullptr;
+  bool hs_built = false;
+};
+// the masked copy of H (rows of frames with g == 0 zeroed) inside the backward's scratch
+uint16_t* bwd_hs(void* scratch, const BwdPlan& plan);
 // S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
 // of each recomputed chunk from them).  remap == null (bf16 path): the dense part -g p only.
-// dH_extra (bf16 path, may be null): [M][D] added to dH by the final reduction, which
-// first waits for before_reduce when that is not null.
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                            const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                            const float* S, int ldS, float* dH, float* dW, float* db, void* scratch,
-                           const BwdPlan& plan, hipStream_t stream, const float* dH_extra = nullptr,
-                           hipEvent_t before_reduce = nullptr);
+                           const BwdPlan& plan, hipStream_t stream, const BwdSide* side = nullptr);
 hipError_t launch_lam2(const double* lam, int M, float2* lam2, hipStream_t stream);
 
 // ---- bf16 kernels on the direct-to-LDS engine (head_gemm_bf16.hip) ---------------------
@@ -89,19 +100,23 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
 hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias,
                                 const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                                 hipStream_t stream, double* Zd = nullptr);
+// One chunk of the recomputed backward: the recompute of dZ (when `recompute`), then the dH
+// and dW products it feeds.
 hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
-                                 int slice, bool want_dH, bool want_dW, float* dW, float* db, float* dbpart,
-                                 hipStream_t stream);
+                                 int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
+                                 float* dbpart, hipStream_t stream);
 // Union-column part of the backward (bf16 path), into its own buffers: dH_u = G W_U [M][D],
 // dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left out;
 // then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch: union_corr_bytes().
+// Hs (may be null): H with the rows of frames with g == 0 zeroed, already built; else the
+// part builds its own copy from g.
 size_t union_corr_bytes(int M, int D, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, int M, int D,
-                                  bool want_dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
-                                  hipStream_t stream);
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, const uint16_t* Hs,
+                                  int M, int D, bool want_dH, bool want_dW, bool want_db, void* scratch,
+                                  float** dH_u, hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
