@@ -56,3 +56,40 @@ def test_host_side_validation_without_gpu():
     assert lib.pctc_workspace_size(1, 2, p(T), p(U2), 512, 1000, 16.0, 0) == 0   # target too long
     lib.pctc_status_string.restype = ctypes.c_char_p
     assert lib.pctc_status_string(-2).decode().startswith("target label")
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_host_side_sizing_rules():
+    """Scratch sizes of the stage entry points and the backward's chunk choice (host code)."""
+    import torch  # noqa: F401
+    lib = ctypes.CDLL(LIB)
+    sz, i32 = ctypes.c_size_t, ctypes.c_int32
+    lib.pctc_lse_scratch_bytes.restype = sz
+    lib.pctc_lse_scratch_bytes.argtypes = [i32, i32]
+    lib.pctc_greedy_workspace_size.restype = sz
+    lib.pctc_greedy_workspace_size.argtypes = [i32, i32, i32]
+    lib.pctc_bwd_chunk.restype = i32
+    lib.pctc_bwd_chunk.argtypes = [i32, i32, i32, i32, i32]
+    lib.pctc_bwd_scratch_bytes.restype = sz
+    lib.pctc_bwd_scratch_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    up = lambda x: (x + 255) // 256 * 256  # noqa: E731
+    # normaliser scratch: 8-byte (max, sum) pairs for 256 vocabulary partitions per frame, 1024
+    # for D >= 2048, then lambda's hi/lo pair per frame; no V argument at all
+    for M in (1, 4215, 11458):
+        assert lib.pctc_lse_scratch_bytes(M, 512) == up(256 * M * 8) + up(M * 8)
+        assert lib.pctc_lse_scratch_bytes(M, 2048) == up(1024 * M * 8) + up(M * 8)
+    assert lib.pctc_lse_scratch_bytes(-1, 512) == 0 and lib.pctc_lse_scratch_bytes(10, 0) == 0
+    assert lib.pctc_greedy_workspace_size(16, 4215, 4096) > lib.pctc_greedy_workspace_size(16, 4215, 512) > 0
+    assert lib.pctc_greedy_workspace_size(16, 4215, 0) == 0
+    # default chunk: the fewest equal chunks (multiples of 256) whose bf16 gradient fits ~512 MiB
+    for M, V in ((4215, 180_000), (2567, 151_936), (11458, 151_936), (16000, 180_000), (64, 1000)):
+        c = lib.pctc_bwd_chunk(1, M, 512, V, 0)
+        assert c > 0 and c % 256 == 0
+        n = -(-V // c)
+        assert c * 2 * M <= 512 * 2**20 + 256 * 2 * M or n == 1
+        assert c - -(-V // n) < 256          # equal chunks, rounded up to whole tiles
+    assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 0) == 60160
+    assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 1024) == 1024
+    # the backward's scratch does not grow with V
+    b = [lib.pctc_bwd_scratch_bytes(1, 4215, 512, V, 384, 0) for V in (100_000, 180_000, 400_000)]
+    assert b[0] > 0 and b[0] == b[1] == b[2]
