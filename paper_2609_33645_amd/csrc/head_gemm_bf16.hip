@@ -734,7 +734,7 @@ namespace {
 constexpr int kColSlices = 16;
 struct UnionCorrLayout {
   int ldK, nz, mslice;  // nz slices of mslice frames for the dW_u product (summed when merged)
-  size_t o_dwu, o_gb, o_wu, o_hs, o_dbp, total;
+  size_t o_dwu, o_gb, o_wu, o_dbp, total;
 };
 UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   UnionCorrLayout L;
@@ -750,8 +750,7 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   L.o_dwu = align_up(static_cast<size_t>(M) * D * sizeof(float), 256);                   // after dH_u
   L.o_gb = L.o_dwu + align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256);
   L.o_wu = L.o_gb + align_up(static_cast<size_t>(M) * k2 * sizeof(uint16_t), 256);
-  L.o_hs = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
-  L.o_dbp = L.o_hs + align_up(static_cast<size_t>(M) * D * sizeof(uint16_t), 256);
+  L.o_dbp = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
   L.total = L.o_dbp + align_up(static_cast<size_t>(kColSlices) * K_max * sizeof(float), 256);
   return L;
 }
@@ -786,12 +785,7 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
   }
   if (want_dW) {
     const uint16_t* Hs2 = Hs;
-    if (!Hs2) {
-      uint16_t* own = reinterpret_cast<uint16_t*>(sc + L.o_hs);
-      hipError_t e = launch_hs_build_bf16(H, M, D, g, own, stream);
-      if (e != hipSuccess) return e;
-      Hs2 = own;
-    }
+    if (!Hs2) return hipErrorInvalidValue;
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dw", stream);
     hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,

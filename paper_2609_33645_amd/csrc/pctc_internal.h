@@ -110,8 +110,8 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
 // Union-column part of the backward (bf16 path), into its own buffers: dH_u = G W_U [M][D],
 // dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left out;
 // then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch: union_corr_bytes().
-// Hs (may be null): H with the rows of frames with g == 0 zeroed, already built; else the
-// part builds its own copy from g.
+// Hs: H with the rows of frames with g == 0 zeroed (the dense part's copy, bwd_hs), needed
+// for dW_u.
 size_t union_corr_bytes(int M, int D, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
                                   const int32_t* u_ids, const uint16_t* W, const uint16_t* H, const uint16_t* Hs,
