@@ -678,8 +678,10 @@ __global__ void ht_build_kernel(const T* __restrict__ H, int M, int D, const flo
 }
 
 // dH = sum of the split-K partials (+ extra, the union-column part, when given), in order.
-__global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int64_t n, const float* __restrict__ extra,
-                                 float* __restrict__ dH) {
+// dH = sum of the split-K partials (+ extra, which may be dH itself: each element is read
+// before it is written by the same thread)
+__global__ void dh_reduce_kernel(const float* __restrict__ part, int splits, int64_t n, const float* extra,
+                                 float* dH) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
   if (i >= n) return;
   float s = 0.f;

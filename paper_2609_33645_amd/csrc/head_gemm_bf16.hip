@@ -747,7 +747,7 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   L.mslice = ((M + L.nz - 1) / L.nz + 63) / 64 * 64;
   L.nz = (M + L.mslice - 1) / L.mslice;  // every slice holds frames
   if (L.nz < 1) L.nz = 1;
-  L.o_dwu = align_up(static_cast<size_t>(M) * D * sizeof(float), 256);                   // after dH_u
+  L.o_dwu = 0;
   L.o_gb = L.o_dwu + align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256);
   L.o_wu = L.o_gb + align_up(static_cast<size_t>(M) * k2 * sizeof(uint16_t), 256);
   L.o_dbp = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
@@ -759,9 +759,10 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
 size_t union_corr_bytes(int M, int D, int K_max) { return union_corr_layout(M, D, K_max).total; }
 
 hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, const uint16_t* Hs,
-                                  int M, int D, bool want_dH, bool want_dW, bool want_db, void* scratch,
-                                  float** dH_u, hipStream_t stream) {
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* Hs, int M, int D,
+                                  float* dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
+                                  hipStream_t stream) {
+  const bool want_dH = dH != nullptr;
   *dH_u = nullptr;
   if (M <= 0 || K_max <= 0) return hipSuccess;
   const UnionCorrLayout L = union_corr_layout(M, D, K_max);
@@ -777,7 +778,7 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
   if (want_dH) {
     uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
     hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, L.ldK, WU2);
-    *dH_u = reinterpret_cast<float*>(sc);
+    *dH_u = dH;
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dh", stream);
     hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles), dim3(GDh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2, k2,

@@ -147,7 +147,6 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.o_small = take(64);
   L.o_status = take(static_cast<size_t>(N) * 4);
   L.o_lossn = take(static_cast<size_t>(N) * 8);
-  L.o_part = take(lse_partial_bytes(L.M, D));
   L.o_lam = take(static_cast<size_t>(L.M) * 8);
   L.o_lam2 = take(static_cast<size_t>(L.M) * 8);
   L.o_S = take(static_cast<size_t>(L.M) * L.ldS * 4);
@@ -160,12 +159,21 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   }
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
+  // The selected logits in double [M][ldS] (bf16 path) and the normaliser's partial pairs are
+  // dead once lambda and S are formed, before the first recompute writes the gradient buffer:
+  // they live in that buffer when it is large enough.
+  size_t lent = 0;
   if (dtype == PCTC_BF16) {
-    // selected logits in double [M][ldS] until lambda is known: in the gradient buffer (not
-    // yet in use then) when it is large enough
     const size_t need = static_cast<size_t>(L.M) * L.ldS * sizeof(double);
-    L.o_zd = (L.bwd.dz_bytes >= need) ? L.o_bwd : take(need);
+    if (L.bwd.dz_bytes >= need) {
+      L.o_zd = L.o_bwd;
+      lent = align_up(need, 256);
+    } else {
+      L.o_zd = take(need);
+    }
   }
+  const size_t part = lse_partial_bytes(L.M, D);
+  L.o_part = (L.bwd.dz_bytes >= lent + part) ? L.o_bwd + lent : take(part);
   L.total = o;
   return L;
 }
@@ -370,8 +378,8 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     // the backward is redone)
     float* dH_u = nullptr;
     PCTC_HIP(launch_union_part_bf16(G, L.ldS, g, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
-                                    static_cast<const uint16_t*>(H), bwd_hs(bws, L.bwd), L.M, D, dH != nullptr,
-                                    dW != nullptr, db != nullptr, ws + L.o_corr, &dH_u, dps_stream));
+                                    bwd_hs(bws, L.bwd), L.M, D, dH, dW != nullptr, db != nullptr, ws + L.o_corr,
+                                    &dH_u, dps_stream));
     // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds
     // dH_u, runs on the second stream beside the last dW product
     BwdSide side;

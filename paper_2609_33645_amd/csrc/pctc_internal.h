@@ -107,16 +107,17 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
                                  float* dbpart, hipStream_t stream);
-// Union-column part of the backward (bf16 path), into its own buffers: dH_u = G W_U [M][D],
-// dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left out;
-// then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch: union_corr_bytes().
-// Hs: H with the rows of frames with g == 0 zeroed (the dense part's copy, bwd_hs), needed
-// for dW_u.
+// Union-column part of the backward (bf16 path): dH_u = G W_U written into dH [M][D] (which
+// the final reduction then adds the dense part to; *dH_u = dH when written), and into its own
+// buffers dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left
+// out; then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch:
+// union_corr_bytes().  Hs: H with the rows of frames with g == 0 zeroed (the dense part's
+// copy, bwd_hs), needed for dW_u.
 size_t union_corr_bytes(int M, int D, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* H, const uint16_t* Hs,
-                                  int M, int D, bool want_dH, bool want_dW, bool want_db, void* scratch,
-                                  float** dH_u, hipStream_t stream);
+                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* Hs, int M, int D,
+                                  float* dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
+                                  hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
