@@ -556,3 +556,25 @@ def test_e2e_forecast_miss(dtype):
             assert rel_err(got, ref[name]) <= 1e-4, name
         else:
             assert cosine(got, ref[name]) >= 0.99999, name
+
+
+# ---------------------------------------------------------------------------------------
+# determinism: every reduction runs in a fixed order, also across the two streams
+# ---------------------------------------------------------------------------------------
+
+@pytest.mark.parametrize("dtype,D,chunk", [("bf16", 128, 1024), ("bf16", 2048, 768), ("f32", 136, 512)])
+def test_e2e_bitwise_repeatable(dtype, D, chunk):
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(81, N=5, T_range=(30, 160), D=D, V=3000, dtype=dtype, p_repeat=0.1, beam=16.0,
+                                w_std=0.5 * math.sqrt(128 / D))
+    rng = np.random.default_rng(5)
+    bias = torch.from_numpy(rng.standard_normal(wl.V).astype(np.float32)).cuda()
+    wts = torch.from_numpy(rng.uniform(0.5, 1.5, size=wl.N).astype(np.float32)).cuda()
+    H, W, y = to_dev(wl)
+    say(f"repeatable {dtype} M={wl.M} D={D} chunk={chunk}")
+    outs = [prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam, chunk=chunk,
+                                         bias=bias, utt_weight=wts, want_db=True) for _ in range(2)]
+    for k in ("loss", "loss_per_utt", "status", "dH", "dW", "db"):
+        a, b = outs[0][k].cpu().numpy(), outs[1][k].cpu().numpy()
+        assert np.array_equal(a.view(np.uint8), b.view(np.uint8)), k
