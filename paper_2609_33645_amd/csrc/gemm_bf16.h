@@ -175,8 +175,11 @@ __device__ __forceinline__ bf16x8 frag(const char* lds, int rr_base, int kk, int
 }
 
 // Tile engine.  Waves form a WR x WC grid; each owns (BR/WR) x (BC/WC) = FR x FC blocks of
-// 32x32.  BK must be a multiple of 32 (an even number of 16-deep k-steps per tile).
-template <int BR, int BC, int BK, LL LA, LL LB, int NS, int WR = 2, int WC = 2>
+// 32x32.  BK must be a multiple of 32 (an even number of 16-deep k-steps per tile).  PRE: in a
+// tile's last k-step, half of the products are issued before the barrier (they need only
+// registers), so the matrix pipe has work while the wave waits there; this pays where one
+// workgroup fills the CU (no other workgroup's products to fill the wait).
+template <int BR, int BC, int BK, LL LA, LL LB, int NS, int WR = 2, int WC = 2, bool PRE = false>
 struct Gemm {
   static constexpr int kNS = NS;
   static constexpr int kBR = BR, kBC = BC;
@@ -226,6 +229,14 @@ struct Gemm {
     for (int j = 0; j < FC; ++j) f.b[j] = frag<LB, BC, BK>(stage + kABytes, wc0 + 32 * j, kk * 16, lane);
   }
 
+  // products q in [B, E) of the FR x FC blocks (q = i FC + j)
+  template <int B, int E>
+  __device__ static __forceinline__ void mma_range(const Frags& f, f32x16 (&acc)[FR][FC]) {
+#pragma unroll
+    for (int q = B; q < E; ++q)
+      acc[q / FC][q % FC] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[q / FC], f.b[q % FC], acc[q / FC][q % FC], 0, 0, 0);
+  }
+
   __device__ static __forceinline__ void mma(const Frags& f, f32x16 (&acc)[FR][FC]) {
 #pragma unroll
     for (int i = 0; i < FR; ++i)
@@ -235,13 +246,13 @@ struct Gemm {
 
   // Instruction order of one k-step: each matrix product is followed by its share of the
   // ND reads of the next step and, in a tile's last step, of the NV copies.
-  template <int NV>
+  template <int NV, int NMM = NM>
   __device__ static __forceinline__ void interleave() {
 #pragma unroll
-    for (int q = 0; q < NM; ++q) {
+    for (int q = 0; q < NMM; ++q) {
       __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // one matrix product
       if (q < NV) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // one global load
-      const int d = (q + 1) * ND / NM - q * ND / NM;
+      const int d = (q + 1) * ND / NMM - q * ND / NMM;
       if (d == 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // LDS reads
       else if (d == 2) __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);
       else if (d == 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
@@ -266,13 +277,15 @@ struct Gemm {
         mma(cur, acc);
         interleave<0>();
       } else {
+        constexpr int NH = PRE ? NM / 2 : 0;
+        if constexpr (PRE) mma_range<0, NH>(cur, acc);
         wait_vmcnt<(NS - 2) * CPW>();
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of stage S are done
         __builtin_amdgcn_s_barrier();
         issue(st[S]);
         load(st[(S + 1) % NS], 0, wave, lane, nxt);
-        mma(cur, acc);
-        interleave<CPW>();
+        mma_range<NH, NM>(cur, acc);
+        interleave<CPW, NM - NH>();
       }
     }
   }

@@ -30,12 +30,12 @@ constexpr int kBK = 32;
 // other's products
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 // 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
-using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4>;
+using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
 // logit products of wide heads (D >= kWideD: normaliser, argmax, recompute): the k loop is
 // long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
 // beats two 4-wave ones
 using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
-using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4>;
+using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4, true>;
 
 #define PCTC_STAGES2(G)                                                  \
   __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
