@@ -585,7 +585,8 @@ recompute_dz_kernel(const T* __restrict__ H, int M, int D, const T* __restrict__
   }
 }
 
-// part[s][M][D] += dZ[:, slice s] . W[c0 + slice s, :]
+// part[s][M][D] += dZ[:, slice s] . W[c0 + slice s, :]; the first chunk (c0 == 0) writes
+// every slice instead (zeros when its k range is empty), so the partials need no clearing.
 template <typename T>
 __global__ void __launch_bounds__(256, 2)
 dh_gemm_kernel(const T* __restrict__ dZ, int M, int chunk, const T* __restrict__ W, int D, int c0, int cw,
@@ -608,7 +609,8 @@ dh_gemm_kernel(const T* __restrict__ dZ, int M, int chunk, const T* __restrict__
   Operand<T> B{W + static_cast<int64_t>(c0) * D, D, D, cw, nullptr, nullptr};
   f32x16 acc[FR][FC];
   tile_gemm<T, kBwdB, kBwdB, BK, Lay::KMajor, Lay::RowMajorT>(A, B, m0, d0, kb, ke, lds, acc);
-  if (kb >= ke) return;
+  const bool first = c0 == 0;
+  if (kb >= ke && !first) return;
   float* dst = part + static_cast<int64_t>(s) * M * D;
 #pragma unroll
   for (int i = 0; i < FR; ++i)
@@ -619,7 +621,10 @@ dh_gemm_kernel(const T* __restrict__ dZ, int M, int chunk, const T* __restrict__
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + acc_row<kBwdB>(wave, lane, i, r);
-        if (m < M) dst[static_cast<int64_t>(m) * D + d] += acc[i][j][r];
+        if (m < M) {
+          float* p = dst + static_cast<int64_t>(m) * D + d;
+          *p = first ? acc[i][j][r] : *p + acc[i][j][r];
+        }
       }
     }
 }
@@ -771,10 +776,8 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* 
                        Ht, plan.Mp);
   }
   int slice = ((chunk / plan.splits + 63) / 64) * 64;
-  if (dH) {
-    hipError_t e = hipMemsetAsync(part, 0, static_cast<size_t>(plan.splits) * M * D * sizeof(float), stream);
-    if (e != hipSuccess) return e;
-  }
+  // split-K slices any chunk fills: the first chunk (the widest) writes them all
+  const int nslices = (min(chunk, V) + slice - 1) / slice;
   for (int c0 = 0; c0 < V; c0 += chunk) {
     const int cw = min(chunk, V - c0);
     const int nVt = (cw + kFwdBR - 1) / kFwdBR;
@@ -808,7 +811,7 @@ static hipError_t head_bwd_t(const T* H, int M, int D, const T* W, const float* 
     const int64_t n = static_cast<int64_t>(M) * D;
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
-                       plan.splits, n, nullptr, dH);
+                       nslices, n, nullptr, dH);
   }
   return hipGetLastError();
 }

@@ -758,13 +758,13 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
 
 size_t union_corr_bytes(int M, int D, int K_max) { return union_corr_layout(M, D, K_max).total; }
 
-hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* Hs, int M, int D,
-                                  float* dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
-                                  hipStream_t stream) {
+hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
+                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool want_dW,
+                                  bool want_db, void* scratch, float** dH_u, hipStream_t stream) {
   const bool want_dH = dH != nullptr;
   *dH_u = nullptr;
   if (M <= 0 || K_max <= 0) return hipSuccess;
+  if (want_dW && !Hs) return hipErrorInvalidValue;
   const UnionCorrLayout L = union_corr_layout(M, D, K_max);
   char* sc = static_cast<char*>(scratch);
   const int k2 = 2 * L.ldK;
@@ -785,11 +785,9 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const
                        *dH_u, dh_xcd_rows(M, D));
   }
   if (want_dW) {
-    const uint16_t* Hs2 = Hs;
-    if (!Hs2) return hipErrorInvalidValue;
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dw", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs2, D, 0, k2,
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs, D, 0, k2,
                        reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice, static_cast<int64_t>(k2) * D);
   }
   if (want_db) {

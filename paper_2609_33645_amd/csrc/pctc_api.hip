@@ -377,7 +377,7 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     // part (its frames with g == 0 are those of the forecast unless the check fails, and then
     // the backward is redone)
     float* dH_u = nullptr;
-    PCTC_HIP(launch_union_part_bf16(G, L.ldS, g, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
+    PCTC_HIP(launch_union_part_bf16(G, L.ldS, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
                                     bwd_hs(bws, L.bwd), L.M, D, dH, dW != nullptr, db != nullptr, ws + L.o_corr,
                                     &dH_u, dps_stream));
     // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds

@@ -114,10 +114,9 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
 // union_corr_bytes().  Hs: H with the rows of frames with g == 0 zeroed (the dense part's
 // copy, bwd_hs), needed for dW_u.
 size_t union_corr_bytes(int M, int D, int K_max);
-hipError_t launch_union_part_bf16(const float* G, int ldG, const float* g, const int32_t* Kdev, int K_max,
-                                  const int32_t* u_ids, const uint16_t* W, const uint16_t* Hs, int M, int D,
-                                  float* dH, bool want_dW, bool want_db, void* scratch, float** dH_u,
-                                  hipStream_t stream);
+hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
+                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool want_dW,
+                                  bool want_db, void* scratch, float** dH_u, hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
