@@ -25,6 +25,9 @@
 namespace pctc {
 
 constexpr float kNeg = -1.0e30f;  // "impossible" score; absorbs finite additions
+constexpr int kMaxQ = 32;         // most states per lane of a lattice pass (2U+1 <= 64 kMaxQ)
+// arc flags of a pass without a mask: every arc kept
+__device__ const uint8_t kAllArcs[1] = {0x0f};
 
 DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
   DpPlan p{};
@@ -60,6 +63,7 @@ DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
   p.off_tab_fb = take(L * sizeof(float));
   p.off_sc_fa = take(M * sizeof(double));
   p.off_sc_fb = take(M * sizeof(double));
+  p.off_dummy = take(static_cast<size_t>(2 * N) * 64 * kMaxQ * sizeof(float));
   if (p.pruned) {
     p.off_tab_va = take(L * sizeof(float));
     p.off_tab_vb = take(L * sizeof(float));
@@ -199,7 +203,7 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
                const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
                int32_t* __restrict__ status, const uint8_t* __restrict__ mask, float* __restrict__ tab_f,
                float* __restrict__ tab_b, double* __restrict__ sc_f, double* __restrict__ sc_b,
-               double* __restrict__ total_out, double* __restrict__ loss_n, int N) {
+               double* __restrict__ total_out, double* __restrict__ loss_n, int N, float* __restrict__ dummy) {
   using Acc = typename std::conditional<VIT, float, double>::type;
   constexpr int PF = prefetch_depth<Q>();
   const int unit = blockIdx.x * kPassWaves + (threadIdx.x >> 6);  // (utterance, direction)
@@ -232,14 +236,20 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     skip_out[q] = (s2 < Sp) && (s2 & 1) && y[(s2 - 1) >> 1] != y[(s2 - 3) >> 1];
     fin[q] = valid[q] && s >= Sp - 2;
   }
-  // one frame of emissions and arc flags for this lane's states
+  // One frame of emissions and arc flags for this lane's states.  No load, store or prefetch
+  // of the frame loop sits under a branch (addresses are clamped in bounds, lanes past the
+  // last state store to this wave's dummy row): a branch around memory operations makes the
+  // compiler wait for every outstanding load at the join, which would serialise the ring.
+  float* const drow = dummy + static_cast<int64_t>(unit) * (64 * Q) + lane * Q;
   auto fetch = [&](int t, float (&e)[Q], int (&mk)[Q]) {
     const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
-    const uint8_t* mrow = mask ? mask + base + static_cast<int64_t>(t) * Sp + lane * Q : nullptr;
+    const uint8_t* mrow = mask ? mask + base + static_cast<int64_t>(t) * Sp : kAllArcs;
+    const int mstep = mask ? 1 : 0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       e[q] = row[col[q]];  // invalid states read the blank column (a valid address)
-      mk[q] = valid[q] ? (mrow ? static_cast<int>(mrow[q]) : 0x0f) : 0;
+      const int v = static_cast<int>(mrow[mstep * min(lane * Q + q, Sp - 1)]);
+      mk[q] = valid[q] ? v : 0;
     }
   };
   auto renorm_store = [&](Acc (&v)[Q], double& off, float* tab, double* sc, int t) {
@@ -253,9 +263,8 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     off += static_cast<double>(mx);
     float* trow = tab + base + static_cast<int64_t>(t) * Sp + lane * Q;
 #pragma unroll
-    for (int q = 0; q < Q; ++q)
-      if (valid[q]) trow[q] = static_cast<float>(v[q]);
-    if (lane == 0) sc[t0 + t] = off;
+    for (int q = 0; q < Q; ++q) *(valid[q] ? trow + q : drow + q) = static_cast<float>(v[q]);
+    sc[t0 + t] = off;  // wave-uniform: every lane stores the same value
   };
 
   float ring_e[PF][Q];
@@ -274,23 +283,19 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
       }
     }
 #pragma unroll
-    for (int k = 0; k < PF; ++k)
-      if (1 + k < T) fetch(1 + k, ring_e[k], ring_m[k]);
+    for (int k = 0; k < PF; ++k) fetch(min(1 + k, T - 1), ring_e[k], ring_m[k]);
     double off = 0.0;
     renorm_store(a, off, tab_f, sc_f, 0);
-    for (int tb = 1; tb < T; tb += PF) {
-#pragma unroll
-      for (int k = 0; k < PF; ++k) {
-        const int t = tb + k;
-        if (t < T) {
+    // frame t from ring slot k, which then prefetches frame t + PF (clamped to the last)
+    auto fstep = [&](int t, float (&re)[Q], int (&rm)[Q]) {
           float e[Q];
           int mk[Q];
 #pragma unroll
           for (int q = 0; q < Q; ++q) {
-            e[q] = ring_e[k][q];
-            mk[q] = ring_m[k][q];
+            e[q] = re[q];
+            mk[q] = rm[q];
           }
-          if (t + PF < T) fetch(t + PF, ring_e[k], ring_m[k]);
+          fetch(min(t + PF, T - 1), re, rm);
           const Acc up1 = lane_up(a[Q - 1]);
           const Acc up2 = (Q >= 2) ? lane_up(a[Q >= 2 ? Q - 2 : 0]) : lane_up(up1);
           Acc na[Q];
@@ -307,9 +312,15 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
 #pragma unroll
           for (int q = 0; q < Q; ++q) a[q] = na[q];
           renorm_store(a, off, tab_f, sc_f, t);
-        }
-      }
+    };
+    int tb = 1;
+    for (; tb + PF <= T; tb += PF) {
+#pragma unroll
+      for (int k = 0; k < PF; ++k) fstep(tb + k, ring_e[k], ring_m[k]);
     }
+#pragma unroll
+    for (int k = 0; k < PF; ++k)
+      if (tb + k < T) fstep(tb + k, ring_e[k], ring_m[k]);
     // total over final states (with final-arc flags)
     int fk[Q];
     {
@@ -354,23 +365,20 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
     }
     // ring slot k holds frame (T-1) - k - ... : frames T-1, T-2, ... are consumed as t+1
 #pragma unroll
-    for (int k = 0; k < PF; ++k)
-      if (T - 1 - k >= 1) fetch(T - 1 - k, ring_e[k], ring_m[k]);
+    for (int k = 0; k < PF; ++k) fetch(max(T - 1 - k, 0), ring_e[k], ring_m[k]);
     double off = 0.0;
     renorm_store(b, off, tab_b, sc_b, T - 1);
-    for (int tb = T - 2; tb >= 0; tb -= PF) {
-#pragma unroll
-      for (int k = 0; k < PF; ++k) {
-        const int t = tb - k;  // uses emissions and arcs of frame t + 1
-        if (t >= 0) {
+    // frame t uses the emissions and arcs of frame t + 1 from ring slot k, which then
+    // prefetches frame t + 1 - PF (clamped to the first)
+    auto bstep = [&](int t, float (&re)[Q], int (&rm)[Q]) {
           float e[Q];
           int mk[Q];
 #pragma unroll
           for (int q = 0; q < Q; ++q) {
-            e[q] = ring_e[k][q];
-            mk[q] = ring_m[k][q];
+            e[q] = re[q];
+            mk[q] = rm[q];
           }
-          if (t + 1 - PF >= 1) fetch(t + 1 - PF, ring_e[k], ring_m[k]);
+          fetch(max(t + 1 - PF, 0), re, rm);
           Acc nb[Q];
 #pragma unroll
           for (int q = 0; q < Q; ++q) nb[q] = valid[q] ? static_cast<Acc>(e[q]) + b[q] : neg;
@@ -395,9 +403,15 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
 #pragma unroll
           for (int q = 0; q < Q; ++q) b[q] = nbb[q];
           renorm_store(b, off, tab_b, sc_b, t);
-        }
-      }
+    };
+    int tb = T - 2;
+    for (; tb - (PF - 1) >= 0; tb -= PF) {
+#pragma unroll
+      for (int k = 0; k < PF; ++k) bstep(tb - k, ring_e[k], ring_m[k]);
     }
+#pragma unroll
+    for (int k = 0; k < PF; ++k)
+      if (tb - k >= 0) bstep(tb - k, ring_e[k], ring_m[k]);
   }
 }
 
@@ -595,11 +609,11 @@ template <bool VIT>
 static hipError_t launch_pass(int Q, int N, hipStream_t stream, const float* S, int ldS, const int32_t* toff,
                               const int32_t* yoff, const int64_t* soff, const int32_t* y_rel, int32_t* status,
                               const uint8_t* mask, float* tf, float* tb, double* sf, double* sb, double* total,
-                              double* loss_n) {
+                              double* loss_n, float* dummy) {
 #define PCTC_PASS(QQ)                                                                                       \
   case QQ:                                                                                                  \
     hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT>), grid, dim3(64 * kPassWaves), 0, stream, S, ldS, toff, yoff, \
-                       soff, y_rel, status, mask, tf, tb, sf, sb, total, loss_n, N);                        \
+                       soff, y_rel, status, mask, tf, tb, sf, sb, total, loss_n, N, dummy);                 \
     break;
   const dim3 grid((2 * N + kPassWaves - 1) / kPassWaves);
   switch (Q) {
@@ -623,7 +637,7 @@ static hipError_t launch_pass(int Q, int N, hipStream_t stream, const float* S, 
 }
 
 static int pick_q(int Smax) {
-  static const int qs[] = {1, 2, 3, 4, 6, 8, 10, 13, 16, 20, 24, 32};
+  static const int qs[] = {1, 2, 3, 4, 6, 8, 10, 13, 16, 20, 24, kMaxQ};
   const int need = (Smax + 63) / 64;
   for (int q : qs)
     if (q >= need) return q;
@@ -633,8 +647,9 @@ static int pick_q(int Smax) {
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
                          const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
-                         void*) {
+                         void*, int phase) {
   const int N = plan.N;
+  const bool front = phase != kDpBack, back = phase != kDpFront;
   char* sc = static_cast<char*>(scratch);
   int32_t* toff = reinterpret_cast<int32_t*>(sc + plan.off_toff);
   int32_t* yoff = reinterpret_cast<int32_t*>(sc + plan.off_yoff);
@@ -644,49 +659,52 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   int32_t* dfirst = reinterpret_cast<int32_t*>(sc + plan.off_dup_first);
   double* logp = reinterpret_cast<double*>(sc + plan.off_logp);
   float* tfa = reinterpret_cast<float*>(sc + plan.off_tab_fa);
+  float* dummy = reinterpret_cast<float*>(sc + plan.off_dummy);
   float* tfb = reinterpret_cast<float*>(sc + plan.off_tab_fb);
   double* sfa = reinterpret_cast<double*>(sc + plan.off_sc_fa);
   double* sfb = reinterpret_cast<double*>(sc + plan.off_sc_fb);
   hipError_t e;
-  // G and g start at zero: excluded utterances and unused columns stay zero.
-  if (plan.M > 0) {
-    e = hipMemsetAsync(G, 0, static_cast<size_t>(plan.M) * ldS * sizeof(float), stream);
-    if (e != hipSuccess) return e;
-    e = hipMemsetAsync(g, 0, static_cast<size_t>(plan.M) * sizeof(float), stream);
-    if (e != hipSuccess) return e;
-  }
-  if (N == 0) return hipSuccess;
-  {
-    Prof pr("dp_prep", stream);
-    hipLaunchKernelGGL(dp_prep_kernel, dim3(N), dim3(256), 0, stream, toff, yoff, y_rel, K_max, status, dnext,
-                       dfirst, frame_utt, loss_n);
-  }
   const int Q = pick_q(plan.Smax);
   if (Q < 0) return hipErrorInvalidValue;
-  uint8_t* mask = nullptr;
-  if (plan.pruned) {
-    float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
-    float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);
-    double* sva = reinterpret_cast<double*>(sc + plan.off_sc_va);
-    double* svb = reinterpret_cast<double*>(sc + plan.off_sc_vb);
-    double* vbest = reinterpret_cast<double*>(sc + plan.off_vbest);
-    mask = reinterpret_cast<uint8_t*>(sc + plan.off_mask);
-    {
-      Prof pr("dp_viterbi", stream);
-      e = launch_pass<true>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva,
-                            svb, vbest, loss_n);
+  uint8_t* mask = plan.pruned ? reinterpret_cast<uint8_t*>(sc + plan.off_mask) : nullptr;
+  if (front) {
+    // G and g start at zero: excluded utterances and unused columns stay zero.
+    if (plan.M > 0) {
+      e = hipMemsetAsync(G, 0, static_cast<size_t>(plan.M) * ldS * sizeof(float), stream);
+      if (e != hipSuccess) return e;
+      e = hipMemsetAsync(g, 0, static_cast<size_t>(plan.M) * sizeof(float), stream);
       if (e != hipSuccess) return e;
     }
-    if (plan.M > 0) {
-      Prof pr("dp_mask", stream);
-      hipLaunchKernelGGL(dp_mask_kernel, dim3(plan.M), dim3(256), 0, stream, S, ldS, toff, yoff, soff, y_rel,
-                         frame_utt, status, tva, tvb, sva, svb, vbest, beam, kKeepSlack, mask);
+    if (N == 0) return hipSuccess;
+    {
+      Prof pr("dp_prep", stream);
+      hipLaunchKernelGGL(dp_prep_kernel, dim3(N), dim3(256), 0, stream, toff, yoff, y_rel, K_max, status, dnext,
+                         dfirst, frame_utt, loss_n);
+    }
+    if (plan.pruned) {
+      float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
+      float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);
+      double* sva = reinterpret_cast<double*>(sc + plan.off_sc_va);
+      double* svb = reinterpret_cast<double*>(sc + plan.off_sc_vb);
+      double* vbest = reinterpret_cast<double*>(sc + plan.off_vbest);
+      {
+        Prof pr("dp_viterbi", stream);
+        e = launch_pass<true>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva,
+                              svb, vbest, loss_n, dummy);
+        if (e != hipSuccess) return e;
+      }
+      if (plan.M > 0) {
+        Prof pr("dp_mask", stream);
+        hipLaunchKernelGGL(dp_mask_kernel, dim3(plan.M), dim3(256), 0, stream, S, ldS, toff, yoff, soff, y_rel,
+                           frame_utt, status, tva, tvb, sva, svb, vbest, beam, kKeepSlack, mask);
+      }
     }
   }
+  if (!back || N == 0) return hipGetLastError();
   {
     Prof pr("dp_alpha_beta", stream);
     e = launch_pass<false>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, mask, tfa, tfb, sfa, sfb,
-                           logp, loss_n);
+                           logp, loss_n, dummy);
     if (e != hipSuccess) return e;
   }
   if (plan.M > 0) {
@@ -885,6 +903,7 @@ hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, co
   int32_t* status = reinterpret_cast<int32_t*>(sc + plan.off_status);
   double* loss_n = reinterpret_cast<double*>(sc + plan.off_logp);  // scratch use only
   float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
+  float* dummy = reinterpret_cast<float*>(sc + plan.off_dummy);
   float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);
   double* sva = reinterpret_cast<double*>(sc + plan.off_sc_va);
   double* svb = reinterpret_cast<double*>(sc + plan.off_sc_vb);
@@ -902,7 +921,7 @@ hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, co
     {
       Prof pr("dp_viterbi", stream);
       e = launch_pass<true>(Q, N, stream, S, ldS, toff, yoff, soff, y_rel, status, nullptr, tva, tvb, sva, svb,
-                            vbest, loss_n);
+                            vbest, loss_n, dummy);
       if (e != hipSuccess) return e;
     }
     if (plan.M > 0) {

@@ -841,7 +841,19 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   const int nslices = (min(chunk, V) + slice - 1) / slice;
   const int64_t n = static_cast<int64_t>(M) * D;
   const float* dH_extra = side ? side->dH_extra : nullptr;
-  for (int c0 = 0; c0 < V; c0 += chunk) {
+  int started = two ? 0 : 2;  // works of the second stream enqueued so far
+  const int nwork = two ? side->nwork : 0;
+  auto start_side = [&](int upto) -> hipError_t {  // enqueue works [started, upto)
+    for (; started < upto && started < nwork; ++started) {
+      hipError_t err;
+      if ((err = hipEventRecord(side->gate[started], stream)) != hipSuccess) return err;
+      if ((err = hipStreamWaitEvent(side->stream, side->gate[started], 0)) != hipSuccess) return err;
+      if ((err = side->work[started].fn(side->work[started].ctx)) != hipSuccess) return err;
+    }
+    return hipSuccess;
+  };
+  int ci = 0;  // chunk index
+  for (int c0 = 0; c0 < V; c0 += chunk, ++ci) {
     const int cw = min(chunk, V - c0);
     const bool last = c0 + chunk >= V;
     if (last && two && dH) {
@@ -849,6 +861,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
                                 true, true, false, dW, db, dbpart, stream);
       if (e != hipSuccess) return e;
+      if ((e = start_side(nwork)) != hipSuccess) return e;
       if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
       if ((e = hipStreamWaitEvent(side->stream, side->dh_done, 0)) != hipSuccess) return e;
       {
@@ -866,8 +879,10 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
                                 true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
       if (e != hipSuccess) return e;
+      if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
     }
   }
+  if ((e = start_side(nwork)) != hipSuccess) return e;
   if (two) {
     // the second stream's work (its union-column part and, with dH, the reduction) is done
     // before this call's work on the caller's stream is

@@ -310,9 +310,10 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
   hipStream_t dps_stream = stream;
   struct Events {
-    hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, dh_done = nullptr, join = nullptr;
+    hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, gate0 = nullptr, gate1 = nullptr, dh_done = nullptr,
+               join = nullptr;
     ~Events() {
-      for (hipEvent_t e : {start, sel, fork, dh_done, join})
+      for (hipEvent_t e : {start, sel, fork, gate0, gate1, dh_done, join})
         if (e) hipEventDestroy(e);
     }
   } ev;
@@ -329,6 +330,8 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     PCTC_HIP(hipEventCreateWithFlags(&ev.start, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.sel, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.gate0, hipEventDisableTiming));
+    PCTC_HIP(hipEventCreateWithFlags(&ev.gate1, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.dh_done, hipEventDisableTiming));
     PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
     PCTC_HIP(hipEventRecord(ev.start, stream));
@@ -362,39 +365,87 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
     PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
     PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
   }
-  // lattice, total scores, zeroing of nonfinite losses, G = dL/dS
-  PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status, G, g,
-                         nullptr, dps, L.K_max, dps_stream, nullptr));
-  PCTC_HIP(launch_loss_reduce(N, loss_n, status, utt_weight, loss, dps_stream));
-  if (loss_per_utt && N > 0)
-    PCTC_HIP(hipMemcpyAsync(loss_per_utt, loss_n, N * sizeof(double), hipMemcpyDeviceToDevice, dps_stream));
-  if (utt_status && N > 0)
-    PCTC_HIP(hipMemcpyAsync(utt_status, status, N * sizeof(int32_t), hipMemcpyDeviceToDevice, dps_stream));
+  // lattice, total scores, zeroing of nonfinite losses, G = dL/dS; then the loss and the
+  // per-utterance outputs
+  struct DpTail {
+    const DpPlan* dp;
+    const int32_t *T, *U, *y_rel;
+    const float* S;
+    int ldS, K_max, N;
+    float beam;
+    const float* weight;
+    double *loss_n, *loss, *loss_per_utt;
+    int32_t *status, *utt_status;
+    float *G, *g;
+    void* dps;
+    hipStream_t stream;
+    const int32_t* pred;  // forecast to check (two-stream schedule) or null
+    int32_t* fflag;
+    int phase;
+    static hipError_t run(void* p) {
+      const DpTail& d = *static_cast<const DpTail*>(p);
+      hipError_t e = launch_ctc_dp(*d.dp, d.T, d.U, d.S, d.ldS, d.y_rel, d.beam, d.weight, d.loss_n, d.status, d.G,
+                                   d.g, nullptr, d.dps, d.K_max, d.stream, nullptr, d.phase);
+      if (e == hipSuccess) e = launch_loss_reduce(d.N, d.loss_n, d.status, d.weight, d.loss, d.stream);
+      if (e == hipSuccess && d.loss_per_utt && d.N > 0)
+        e = hipMemcpyAsync(d.loss_per_utt, d.loss_n, d.N * sizeof(double), hipMemcpyDeviceToDevice, d.stream);
+      if (e == hipSuccess && d.utt_status && d.N > 0)
+        e = hipMemcpyAsync(d.utt_status, d.status, d.N * sizeof(int32_t), hipMemcpyDeviceToDevice, d.stream);
+      if (e == hipSuccess && d.pred) e = launch_forecast_check(d.N, d.status, d.weight, d.pred, d.fflag, d.stream);
+      return e;
+    }
+  } dpt{&L.dp, input_lengths, target_lengths, y_rel, S, L.ldS, L.K_max, N, beam, utt_weight, loss_n, loss,
+        loss_per_utt, status, utt_status, G, g, dps, dps_stream,
+        overlap ? reinterpret_cast<const int32_t*>(ws + L.o_pred) : nullptr, fflag, kDpAll};
   if (overlap) {
-    PCTC_HIP(launch_forecast_check(N, status, utt_weight, reinterpret_cast<int32_t*>(ws + L.o_pred), fflag,
-                                   dps_stream));
-    // the union columns' part of the backward, from the lattice's G, still beside the dense
-    // part (its frames with g == 0 are those of the forecast unless the check fails, and then
-    // the backward is redone)
-    float* dH_u = nullptr;
-    PCTC_HIP(launch_union_part_bf16(G, L.ldS, Kdev, L.K_max, u_ids, static_cast<const uint16_t*>(W),
-                                    bwd_hs(bws, L.bwd), L.M, D, dH, dW != nullptr, db != nullptr, ws + L.o_corr,
-                                    &dH_u, dps_stream));
+    // the lattice's front (Viterbi pass and arc mask) now, beside the first recompute; its
+    // log-sum passes, occupancies and the loss after the dense part's first chunk, and the
+    // union columns' part after its second (see BwdSide)
+    PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status,
+                           G, g, nullptr, dps, L.K_max, dps_stream, nullptr, kDpFront));
+    dpt.phase = kDpBack;
+    // the union columns' part of the backward, from the lattice's G (its frames with g == 0
+    // are those of the forecast unless the check fails, and then the backward is redone)
+    struct UnionWork {
+      const float* G;
+      int ldG;
+      const int32_t *Kdev, *u_ids;
+      int K_max, M, D;
+      const uint16_t *W, *Hs;
+      float* dH;
+      bool want_dW, want_db;
+      void* scratch;
+      hipStream_t stream;
+      static hipError_t run(void* p) {
+        const UnionWork& u = *static_cast<const UnionWork*>(p);
+        float* dH_u = nullptr;
+        return launch_union_part_bf16(u.G, u.ldG, u.Kdev, u.K_max, u.u_ids, u.W, u.Hs, u.M, u.D, u.dH, u.want_dW,
+                                      u.want_db, u.scratch, &dH_u, u.stream);
+      }
+    } uw{G, L.ldS, Kdev, u_ids, L.K_max, L.M, D, static_cast<const uint16_t*>(W), bwd_hs(bws, L.bwd), dH,
+         dW != nullptr, db != nullptr, ws + L.o_corr, dps_stream};
     // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds
-    // dH_u, runs on the second stream beside the last dW product
+    // the union part's dH_u (written into dH), runs on the second stream beside the last dW
     BwdSide side;
     side.stream = dps_stream;
+    side.gate[0] = ev.gate0;
+    side.gate[1] = ev.gate1;
     side.dh_done = ev.dh_done;
     side.reduced = ev.join;
-    side.dH_extra = dH_u;
+    side.work[0] = SideWork{&DpTail::run, &dpt};
+    side.work[1] = SideWork{&UnionWork::run, &uw};
+    side.nwork = 2;
+    side.dH_extra = (dH && L.K_max > 0) ? dH : nullptr;
     side.hs_built = (dH || dW);
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, nullptr, L.ldS, g_pred, nullptr, nullptr, L.ldS, dH, dW,
                              db, bws, L.bwd, stream, &side));
     PCTC_HIP(launch_union_merge_bf16(Kdev, L.K_max, u_ids, L.M, D, dW, db, ws + L.o_corr, stream));
-  } else if (want_bwd) {
+  } else {
+    PCTC_HIP(DpTail::run(&dpt));
     // backward: chunk by chunk recomputation
-    PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
-                             stream));
+    if (want_bwd)
+      PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
+                               stream));
   }
   int32_t hflags[2] = {0, 0};  // label error, forecast mismatch
   PCTC_HIP(hipMemcpyAsync(hflags, err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, stream));

@@ -70,15 +70,27 @@ struct BwdPlan {
   size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
-// The bf16 fused schedule's side of the recomputed backward.  With a second stream, the last
-// chunk records dh_done after its dH product; the second stream then waits for it, runs the
-// final dH reduction (adding dH_extra, the union-column part, which that stream computed
-// earlier) beside the chunk's dW product, and records reduced, which the caller's stream
-// waits for before the call returns.  hs_built: the masked copy of H (bwd_hs) was already
-// written, from the same g, on a stream the caller's stream has waited for.
+// The bf16 fused schedule's side of the recomputed backward.  With a second stream: work i
+// (i < nwork) is enqueued on that stream after chunk i + 1 of the dense part (the caller's
+// stream records gate[i], the second stream waits for it, then work[i].fn(work[i].ctx)
+// enqueues), or at the last chunk's dH product when there are fewer chunks, so that the
+// second stream's kernels run beside the next chunk's recompute, whose many short workgroups
+// leave room for them, rather than hold compute units while a dH or dW product launches.
+// The last chunk records dh_done after its dH product; the second stream waits for it and
+// runs the final dH reduction (adding dH_extra, written by its work) beside the chunk's dW
+// product, then records reduced, which the caller's stream waits for before the call returns.
+// hs_built: the masked copy of H (bwd_hs) was already written, from the same g, on a stream
+// the caller's stream has waited for.
+struct SideWork {
+  hipError_t (*fn)(void*) = nullptr;
+  void* ctx = nullptr;
+};
 struct BwdSide {
   hipStream_t stream = nullptr;
+  hipEvent_t gate[2] = {nullptr, nullptr};
   hipEvent_t dh_done = nullptr, reduced = nullptr;
+  SideWork work[2];
+  int nwork = 0;
   const float* dH_extra = nullptr;
   bool hs_built = false;
 };
@@ -139,16 +151,19 @@ struct DpPlan {
   int64_t lattice;  // sum_n T_n (2U_n+1)
   size_t off_toff, off_yoff, off_soff, off_frame_utt, off_dup_next, off_dup_first, off_logp, off_status,
       off_tab_fa, off_tab_fb, off_tab_va, off_tab_vb, off_sc_fa, off_sc_fb, off_sc_va, off_sc_vb,
-      off_vbest, off_mask, total;
+      off_vbest, off_mask, off_dummy, total;
 };
 DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam);
 // Uploads the host offsets into the scratch (async) and runs the whole lattice stage.
 // weight: device float [N] loss weights of the utterances, or null (all 1): G rows of
 // utterance n are -w_n gamma.
+// phase: kDpAll, or kDpFront (zeroing of G and g, prep, the Viterbi pass and the arc mask)
+// then kDpBack (the log-sum passes and the occupancies, G and g) on the same stream.
+constexpr int kDpAll = 0, kDpFront = 1, kDpBack = 2;
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
                          const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
-                         void* host_staging);
+                         void* host_staging, int phase = kDpAll);
 // delta [nbeams][N]: discarded posterior mass of each utterance at each beam (host beams).
 // Needs a plan made with a finite beam (the Viterbi tables and the arc mask).
 hipError_t launch_discarded_mass(const DpPlan& plan, const float* S, int ldS, const int32_t* y_rel, const float* beams,
