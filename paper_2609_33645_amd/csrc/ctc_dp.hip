@@ -780,73 +780,100 @@ dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restr
     fin[q] = valid[q] && s >= Sp - 2;
   }
   double af[Q], ap[Q];  // full and retained forward sums, scaled per frame
-  // emissions and arc flags of frame t + 1 are loaded while frame t is computed
-  float e_nx[Q];
-  int mk_nx[Q];
-  auto load_frame = [&](int t) {
+  // Emissions and arc flags of the next PF frames are held in a register ring; the loop has
+  // only loads and no branch around them (clamped addresses), so each frame waits only for
+  // its own ring slot.
+  constexpr int PF = prefetch_depth<Q>();
+  float ring_e[PF][Q];
+  int ring_m[PF][Q];
+  auto load_frame = [&](int t, float (&e)[Q], int (&mk)[Q]) {
     const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
+    const uint8_t* mrow = mask + base + static_cast<int64_t>(t) * Sp;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
-      e_nx[q] = valid[q] ? row[col[q]] : -INFINITY;
-      mk_nx[q] = valid[q] ? static_cast<int>(mask[base + static_cast<int64_t>(t) * Sp + lane * Q + q]) : 0;
+      const float v = row[col[q]];  // invalid states read the blank column (a valid address)
+      e[q] = valid[q] ? v : -INFINITY;
+      const int m = static_cast<int>(mrow[min(lane * Q + q, Sp - 1)]);
+      mk[q] = valid[q] ? m : 0;
     }
   };
-  if (T > 0) load_frame(0);
-  for (int t = 0; t < T; ++t) {
-    float e[Q];
-    int mk[Q];
-#pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      e[q] = e_nx[q];
-      mk[q] = mk_nx[q];
-    }
-    if (t + 1 < T) load_frame(t + 1);
-    // exp(e) in double over the whole range without a per-frame shift: 2^x = 2^i 2^(x - i),
-    // i = floor(x), the fraction's power in float and the integer one exact
-    double pe[Q];
+  // exp(e) in double over the whole range without a per-frame shift: 2^x = 2^i 2^(x - i),
+  // i = floor(x), the fraction's power in float and the integer one exact
+  auto emit = [&](const float (&e)[Q], double (&pe)[Q]) {
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       const float x = e[q] * kLog2e;
       const float fi = fminf(fmaxf(floorf(x), -2000.f), 2000.f);
       pe[q] = (valid[q] && x > -INFINITY) ? ldexp(static_cast<double>(fast_exp2(x - fi)), static_cast<int>(fi)) : 0.0;
     }
-    double nf[Q], np[Q];
-    if (t == 0) {
-#pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        const int s = lane * Q + q;
-        nf[q] = (valid[q] && s < 2) ? pe[q] : 0.0;
-        np[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? pe[q] : 0.0;
-      }
-    } else {
-      const double uf1 = lane_up_d(af[Q - 1]), up1 = lane_up_d(ap[Q - 1]);
-      const double uf2 = (Q >= 2) ? lane_up_d(af[Q >= 2 ? Q - 2 : 0]) : lane_up_d(uf1);
-      const double up2 = (Q >= 2) ? lane_up_d(ap[Q >= 2 ? Q - 2 : 0]) : lane_up_d(up1);
-#pragma unroll
-      for (int q = 0; q < Q; ++q) {
-        const double f0 = af[q], p0 = ap[q];
-        const double f1 = (q >= 1) ? af[q >= 1 ? q - 1 : 0] : uf1;
-        const double p1 = (q >= 1) ? ap[q >= 1 ? q - 1 : 0] : up1;
-        const double f2 = (q >= 2) ? af[q >= 2 ? q - 2 : 0] : (q == 1 ? uf1 : uf2);
-        const double p2 = (q >= 2) ? ap[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
-        nf[q] = valid[q] ? pe[q] * (f0 + f1 + (skip_in[q] ? f2 : 0.0)) : 0.0;
-        np[q] = valid[q] ? pe[q] * (((mk[q] & 1) ? p0 : 0.0) + ((mk[q] & 2) ? p1 : 0.0) +
-                                    ((skip_in[q] && (mk[q] & 4)) ? p2 : 0.0))
-                         : 0.0;
-      }
-    }
+  };
+  // any positive scale serves (both sums take the same one): an approximate reciprocal of
+  // the wave maximum
+  auto rescale = [&](double (&nf)[Q], double (&np)[Q]) {
     double c = 0.0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) c = fmax(c, nf[q]);
     c = wave_max_d(c);
-    // any positive scale serves (both sums take the same one): an approximate reciprocal
     const double inv = (c > 0.0) ? __builtin_amdgcn_rcp(c) : 0.0;
 #pragma unroll
     for (int q = 0; q < Q; ++q) {
       af[q] = nf[q] * inv;
       ap[q] = np[q] * inv;
     }
+  };
+  {  // frame 0: the start arcs
+    float e[Q];
+    int mk[Q];
+    load_frame(0, e, mk);
+#pragma unroll
+    for (int k = 0; k < PF; ++k) load_frame(min(1 + k, T - 1), ring_e[k], ring_m[k]);
+    double pe[Q], nf[Q], np[Q];
+    emit(e, pe);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const int s = lane * Q + q;
+      nf[q] = (valid[q] && s < 2) ? pe[q] : 0.0;
+      np[q] = (valid[q] && s < 2 && (mk[q] & 1)) ? pe[q] : 0.0;
+    }
+    rescale(nf, np);
   }
+  // frame t from ring slot k, which then prefetches frame t + PF (clamped to the last)
+  auto step = [&](int t, float (&re)[Q], int (&rm)[Q]) {
+    float e[Q];
+    int mk[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      e[q] = re[q];
+      mk[q] = rm[q];
+    }
+    load_frame(min(t + PF, T - 1), re, rm);
+    double pe[Q], nf[Q], np[Q];
+    emit(e, pe);
+    const double uf1 = lane_up_d(af[Q - 1]), up1 = lane_up_d(ap[Q - 1]);
+    const double uf2 = (Q >= 2) ? lane_up_d(af[Q >= 2 ? Q - 2 : 0]) : lane_up_d(uf1);
+    const double up2 = (Q >= 2) ? lane_up_d(ap[Q >= 2 ? Q - 2 : 0]) : lane_up_d(up1);
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+      const double f0 = af[q], p0 = ap[q];
+      const double f1 = (q >= 1) ? af[q >= 1 ? q - 1 : 0] : uf1;
+      const double p1 = (q >= 1) ? ap[q >= 1 ? q - 1 : 0] : up1;
+      const double f2 = (q >= 2) ? af[q >= 2 ? q - 2 : 0] : (q == 1 ? uf1 : uf2);
+      const double p2 = (q >= 2) ? ap[q >= 2 ? q - 2 : 0] : (q == 1 ? up1 : up2);
+      nf[q] = valid[q] ? pe[q] * (f0 + f1 + (skip_in[q] ? f2 : 0.0)) : 0.0;
+      np[q] = valid[q] ? pe[q] * (((mk[q] & 1) ? p0 : 0.0) + ((mk[q] & 2) ? p1 : 0.0) +
+                                  ((skip_in[q] && (mk[q] & 4)) ? p2 : 0.0))
+                       : 0.0;
+    }
+    rescale(nf, np);
+  };
+  int tb = 1;
+  for (; tb + PF <= T; tb += PF) {
+#pragma unroll
+    for (int k = 0; k < PF; ++k) step(tb + k, ring_e[k], ring_m[k]);
+  }
+#pragma unroll
+  for (int k = 0; k < PF; ++k)
+    if (tb + k < T) step(tb + k, ring_e[k], ring_m[k]);
   double sf = 0.0, sp = 0.0;
 #pragma unroll
   for (int q = 0; q < Q; ++q) {
