@@ -35,6 +35,9 @@ using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
 // long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
 // beats two 4-wave ones
 using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
+// the union-column part's dH product: 4-wave tiles (two workgroups per CU), so that its
+// workgroups find room beside a recompute's
+using GUh = bf::Gemm<256, 128, 32, LL::KC, LL::MC, 3, 2, 2>;
 using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4, true>;
 
 #define PCTC_STAGES2(G)                                                  \
@@ -555,22 +558,22 @@ static int dh_xcd_rows(int M, int D) {
   return best;
 }
 
-__global__ void __launch_bounds__(512, 1)
+template <class G, int OCC>
+__global__ void __launch_bounds__(G::kThreads, OCC)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
              int slice, float* __restrict__ part, int gm) {
   const bool first = c0 == 0;
-  using G = GDh;
-  constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES4(G)
-  const int nMt = (M + kBR - 1) / kBR;
-  const int nDt = (D + kBC - 1) / kBC;
+  constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
+  PCTC_STAGES_G(G)
+  const int nMt = (M + TR - 1) / TR;
+  const int nDt = (D + TC - 1) / TC;
   // Each XCD (a contiguous run of work ids) takes one block of a gm x (8 / gm) partition of
   // the frame x d tile grid: it reads dZ rows of its frame block and W columns of its d block
   const int work = xcd_swz(blockIdx.x, gridDim.x);
   const int s = work / (nMt * nDt);
   int mt, dt;
   block_tile(work % (nMt * nDt), nMt, nDt, gm, mt, dt);
-  const int m0 = mt * kBR, d0 = dt * kBC;
+  const int m0 = mt * TR, d0 = dt * TC;
   const int kb = s * slice;
   const int ke = min(cw, kb + slice);
   if (kb >= ke && !first) return;  // the first chunk writes every slice (zeros when empty)
@@ -779,10 +782,10 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
     uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
     hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, L.ldK, WU2);
     *dH_u = dH;
-    const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
     Prof pr("union_dh", stream);
-    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles), dim3(GDh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2, k2,
-                       *dH_u, dh_xcd_rows(M, D));
+    hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0,
+                       k2, k2, *dH_u, dh_xcd_rows(M, D));
   }
   if (want_dW) {
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
@@ -940,8 +943,8 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     const int tiles = ((M + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
-    hipLaunchKernelGGL(dh_gemm_bf16, dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D, c0, cw, slice,
-                       part, dh_xcd_rows(M, D));
+    hipLaunchKernelGGL((dh_gemm_bf16<GDh, 1>), dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D,
+                       c0, cw, slice, part, dh_xcd_rows(M, D));
   }
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
