@@ -144,7 +144,6 @@ __device__ __forceinline__ double lane_down(double x) {
   const int hi = dpp_dn_i(static_cast<int>(b >> 32), static_cast<int>(nb >> 32));
   return __longlong_as_double((static_cast<long long>(hi) << 32) | static_cast<unsigned int>(lo));
 }
-__device__ __forceinline__ int lane_up_i(int x) { return dpp_up_i(x, 0); }
 __device__ __forceinline__ int lane_down_i(int x) { return dpp_dn_i(x, 0); }
 
 // Maximum over the wavefront: DPP reductions within each row of 16 lanes, then the four

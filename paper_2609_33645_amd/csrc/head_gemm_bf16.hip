@@ -40,24 +40,6 @@ using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 using GUh = bf::Gemm<256, 128, 32, LL::KC, LL::MC, 3, 2, 2>;
 using GDw = bf::Gemm<kBR, kBC, kBK, LL::MC, LL::MC, 4, 2, 4, true>;
 
-#define PCTC_STAGES2(G)                                                  \
-  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
-  char* const st[2] = {st0_, st1_};
-
-#define PCTC_STAGES4(G)                                                  \
-  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st2_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st3_[G::kStageBytes]; \
-  char* const st[4] = {st0_, st1_, st2_, st3_};
-
-#define PCTC_STAGES(G)                                                   \
-  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes]; \
-  __shared__ __attribute__((aligned(1024))) char st2_[G::kStageBytes]; \
-  char* const st[3] = {st0_, st1_, st2_};
-
 __device__ __forceinline__ int xcd_swz(int bid, int nblocks) {
   const int full = (nblocks / 8) * 8;
   if (bid >= full) return bid;
@@ -334,7 +316,7 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
               const double* __restrict__ lam, float* __restrict__ S, int ldS, double* __restrict__ Zd) {
   using G = GFwd;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES(G)
+  PCTC_STAGES_G(G)
   const int nMt = (M + kFC - 1) / kFC;
   const int mt = blockIdx.x % nMt;
   const int jt = blockIdx.x / nMt;
@@ -618,7 +600,7 @@ dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
              float* __restrict__ dW, int nz, int mslice, int64_t zstride) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
-  PCTC_STAGES4(G)
+  PCTC_STAGES_G(G)
   const int nDt = (D + kBC - 1) / kBC;
   const int nVt = (cw + kBR - 1) / kBR;
   const int work = xcd_swz(blockIdx.x, gridDim.x);
