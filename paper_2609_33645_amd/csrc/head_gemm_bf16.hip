@@ -730,6 +730,7 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   if (L.nz > (M + 255) / 256) L.nz = (M + 255) / 256;
   if (L.nz < 1) L.nz = 1;
   L.mslice = ((M + L.nz - 1) / L.nz + 63) / 64 * 64;
+  if (L.mslice < 64) L.mslice = 64;       // M = 0 (no frames): one empty slice
   L.nz = (M + L.mslice - 1) / L.mslice;  // every slice holds frames
   if (L.nz < 1) L.nz = 1;
   L.o_dwu = 0;

@@ -93,3 +93,43 @@ def test_host_side_sizing_rules():
     # the backward's scratch does not grow with V
     b = [lib.pctc_bwd_scratch_bytes(1, 4215, 512, V, 384, 0) for V in (100_000, 180_000, 400_000)]
     assert b[0] > 0 and b[0] == b[1] == b[2]
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_zero_frame_sizing():
+    """Every size query accepts a batch without frames (N = 0 or M = 0) and returns a usable
+    size: the bf16 union part once divided by a zero frame-slice length there."""
+    import numpy as np
+    import torch  # noqa: F401
+    lib = ctypes.CDLL(LIB)
+    sz, i32, f32 = ctypes.c_size_t, ctypes.c_int32, ctypes.c_float
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.pctc_workspace_size.restype = sz
+    lib.pctc_workspace_size.argtypes = [i32, i32, i32p, i32p, i32, i32, f32, i32]
+    lib.pctc_dp_scratch_bytes.restype = sz
+    lib.pctc_dp_scratch_bytes.argtypes = [i32, i32p, i32p, f32]
+    lib.pctc_discarded_mass_scratch_bytes.restype = sz
+    lib.pctc_discarded_mass_scratch_bytes.argtypes = [i32, i32p, i32p]
+    lib.pctc_lse_scratch_bytes.restype = sz
+    lib.pctc_lse_scratch_bytes.argtypes = [i32, i32]
+    lib.pctc_greedy_workspace_size.restype = sz
+    lib.pctc_greedy_workspace_size.argtypes = [i32, i32, i32]
+    lib.pctc_bwd_scratch_bytes.restype = sz
+    lib.pctc_bwd_scratch_bytes.argtypes = [i32, i32, i32, i32, i32, i32]
+    lib.pctc_grouped_workspace_size.restype = sz
+    lib.pctc_grouped_workspace_size.argtypes = [i32, i32, i32, i32, i32, i32]
+    T = np.zeros(0, np.int32)
+    U = np.zeros(0, np.int32)
+    p = lambda a: a.ctypes.data_as(i32p)  # noqa: E731
+    for dt in (0, 1):
+        for D, V in ((8, 2), (64, 300), (512, 180_000), (4096, 151_936)):
+            for beam in (0.0, 16.0, float("inf")):
+                assert lib.pctc_workspace_size(dt, 0, p(T), p(U), D, V, beam, 0) > 0, (dt, D, V, beam)
+        assert lib.pctc_bwd_scratch_bytes(dt, 0, 512, 180_000, 8, 0) > 0
+        assert lib.pctc_grouped_workspace_size(dt, 0, 512, 180_000, 100, 0) > 0
+    for beam in (16.0, float("inf")):
+        assert lib.pctc_dp_scratch_bytes(0, p(T), p(U), beam) > 0
+    assert lib.pctc_discarded_mass_scratch_bytes(0, p(T), p(U)) > 0
+    for D in (512, 4096):
+        assert lib.pctc_lse_scratch_bytes(0, D) > 0
+        assert lib.pctc_greedy_workspace_size(0, 0, D) > 0

@@ -267,6 +267,31 @@ def test_e2e_edge_cases():
     del torch
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_e2e_empty_batch(dtype):
+    """No utterances (N = 0, M = 0): the loss is an empty sum (0), every head-gradient entry
+    is 0 (dW and db are written, not left as they were), and the call succeeds."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    say(f"empty batch {dtype}")
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    V, D = 300, 64
+    gen = torch.Generator(device="cpu").manual_seed(5)
+    H = torch.zeros((0, D), dtype=tdt, device="cuda")
+    W = torch.randn((V, D), generator=gen).to(tdt).cuda()
+    targets = torch.zeros(0, dtype=torch.int32, device="cuda")
+    bias = torch.randn(V, generator=gen).cuda()
+    for kw in ({}, {"bias": bias, "want_db": True}):
+        dW_out = torch.full((V, D), float("nan"), device="cuda")
+        res = prunedctc.pruned_ctc_fwd_bwd(H, W, targets, [], [], 0, 16.0, dW_out=dW_out, **kw)
+        torch.cuda.synchronize()
+        assert res["loss"].item() == 0.0
+        assert res["dH"].shape == (0, D) and res["loss_per_utt"].numel() == 0
+        assert torch.count_nonzero(torch.nan_to_num(res["dW"], nan=1.0)).item() == 0
+        if kw:
+            assert torch.count_nonzero(res["db"]).item() == 0
+
+
 def test_error_codes():
     import torch
     from paper_2609_33645_amd import prunedctc
