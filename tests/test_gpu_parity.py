@@ -292,6 +292,37 @@ def test_e2e_empty_batch(dtype):
             assert torch.count_nonzero(res["db"]).item() == 0
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_stage_entry_points_without_frames(dtype):
+    """Each stage entry point accepts a batch without frames: nothing to compute, no error,
+    and the head gradient of an empty sum is written as zeros."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    say(f"stages without frames {dtype}")
+    tdt = torch.bfloat16 if dtype == "bf16" else torch.float32
+    V, D, K = 300, 64, 3
+    gen = torch.Generator(device="cpu").manual_seed(6)
+    H = torch.zeros((0, D), dtype=tdt, device="cuda")
+    W = torch.randn((V, D), generator=gen).to(tdt).cuda()
+    u_ids = torch.tensor([0, 5, 9], dtype=torch.int32, device="cuda")
+    sel = prunedctc.lse_select(H, W, u_ids)
+    assert sel["lam"].numel() == 0
+    S = torch.zeros((0, K), dtype=torch.float32, device="cuda")
+    y_rel = torch.zeros(0, dtype=torch.int32, device="cuda")
+    dp = prunedctc.ctc_dp(S, y_rel, [], [], 16.0)
+    assert dp["loss_per_utt"].numel() == 0
+    dec = prunedctc.greedy_decode(H, W, [], 0)
+    assert dec["tokens"] == []
+    assert prunedctc.discarded_mass(S, y_rel, [], [], [1.0, 16.0]).numel() == 0
+    remap = torch.full((V,), -1, dtype=torch.int32, device="cuda")
+    bwd = prunedctc.head_bwd(H, W, torch.zeros(0, dtype=torch.float64, device="cuda"), S,
+                             torch.zeros(0, dtype=torch.float32, device="cuda"), remap)
+    torch.cuda.synchronize()
+    assert bwd["dH"].shape == (0, D) and torch.count_nonzero(bwd["dW"]).item() == 0
+    gl = prunedctc.grouped_logprobs(H, W, u_ids)
+    assert gl["logp"].shape == (0, K + 1) and gl["lam"].numel() == 0
+
+
 def test_error_codes():
     import torch
     from paper_2609_33645_amd import prunedctc
