@@ -125,11 +125,14 @@ def _mask_from_margins(res, T, Sp):
     (0, 3, (1, 40), 20, math.inf, False), (1, 5, (30, 120), 50, math.inf, False),
     (2, 2, (200, 400), 300, math.inf, False), (3, 4, (20, 90), 40, 6.5, True), (4, 3, (50, 150), 64, 12.5, True),
     (5, 2, (300, 500), 200, 16.5, True), (6, 6, (1, 8), 10, 0.5, True), (7, 2, (1500, 1500), 420, 8.5, True),
-    (8, 3, (100, 300), 100, math.inf, True), (9, 4, (10, 60), 30, 2.5, True)])
+    (8, 3, (100, 300), 100, math.inf, True), (9, 4, (10, 60), 30, 2.5, True),
+    (10, 1, (2100, 2100), 1100, 12.5, True)])  # U = 1023, the longest supported target
 def test_ctc_dp_parity(seed, N, Trange, K, beam, integer):
     import torch
     from paper_2609_33645_amd import prunedctc
-    S, y_rel, T, U = _dp_case(seed, N, Trange, K, U_frac=0.27 if seed == 7 else 0.3, integer=integer)
+    S, y_rel, T, U = _dp_case(seed, N, Trange, K, U_frac={7: 0.27, 10: 0.5}.get(seed, 0.3), integer=integer)
+    if seed == 10:
+        assert U.tolist() == [1023]
     say(f"ctc_dp seed={seed} N={N} T={T.tolist()} U={U.tolist()} K={K} beam={beam}")
     ref = oracle.ctc_from_scores(S.astype(np.float64), y_rel, T, U, beam=beam)
     out = prunedctc.ctc_dp(torch.from_numpy(S).cuda(), torch.from_numpy(y_rel).cuda(), T, U, beam=beam,
