@@ -270,6 +270,19 @@ def test_e2e_edge_cases():
     del torch
 
 
+def test_e2e_max_vocab():
+    """The largest supported vocabulary (524,288 classes: the limit of the union's on-chip
+    membership bitmap) with the blank at the last id, labels drawn over the whole range, and
+    several backward chunks."""
+    V = 524288
+    wl = workloads.random_small(12, N=3, T_range=(20, 60), D=64, V=V, dtype="bf16", token_law="uniform",
+                                p_repeat=0.1, blank=V - 1, beam=16.0, w_std=0.5)
+    say(f"e2e max vocabulary V={V} M={wl.M} T={wl.input_lengths.tolist()}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    res = run_gpu(wl, chunk=65536)
+    _check_e2e(wl, res, ref, fp32=False)
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_e2e_empty_batch(dtype):
     """No utterances (N = 0, M = 0): the loss is an empty sum (0), every head-gradient entry
