@@ -195,7 +195,7 @@ def test_head_bwd_parity(dtype, seed, chunk, D):
 # end to end
 # ---------------------------------------------------------------------------------------
 
-def _check_e2e(wl, res, ref, fp32: bool):
+def _check_e2e(wl, res, ref, fp32: bool, tight: bool = True):
     np.testing.assert_array_equal(res["status"], ref["status"])
     lr = loss_rel(res["loss"], ref["loss"])
     say(f"  loss gpu={res['loss']:.9g} oracle={ref['loss']:.9g} rel={lr:.3g}")
@@ -210,7 +210,8 @@ def _check_e2e(wl, res, ref, fp32: bool):
         assert cH >= 0.999 and cW >= 0.999
         # achieved accuracy is far tighter than the bar: bf16 inputs are exact and only dZ is rounded
         assert lr <= 1e-5
-        assert cH >= 0.99999 and cW >= 0.99999
+        if tight:
+            assert cH >= 0.99999 and cW >= 0.99999
 
 
 def test_e2e_tiny_f32():
@@ -219,6 +220,26 @@ def test_e2e_tiny_f32():
     ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl)
     _check_e2e(wl, res, ref, fp32=True)
+
+
+@pytest.mark.parametrize("dtype,D,V,blank", [
+    ("bf16", 8, 2, 0), ("f32", 8, 2, 1), ("bf16", 24, 3, 2), ("f32", 24, 1000, 0), ("bf16", 8, 1000, 999)])
+def test_e2e_smallest_shapes(dtype, D, V, blank):
+    """The narrowest heads (D = 8, the minimum; D = 24, not a whole k-tile of the products)
+    and the smallest vocabularies (V = 2: the blank and one label), with one-frame
+    utterances among the rest."""
+    wl = workloads.random_small(40 + D + V, N=5, T_range=(1, 5) if V <= 3 else (1, 30), D=D, V=V, dtype=dtype,
+                                token_law="uniform",
+                                p_repeat=0.2, blank=blank, beam=16.0 if V > 3 else math.inf, w_std=0.5)
+    say(f"e2e smallest {dtype} D={D} V={V} blank={blank} T={wl.input_lengths.tolist()} "
+        f"U={wl.target_lengths.tolist()}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    res = run_gpu(wl)
+    # With V <= 3 every class is in the union and dZ = p - gamma is a difference of two O(1)
+    # numbers whose dense part p is rounded to bf16: the cancellation amplifies that rounding
+    # past the tight check (which assumes p small beside the union columns); the stated bf16
+    # tolerance still applies.
+    _check_e2e(wl, res, ref, fp32=(dtype == "f32"), tight=V > 3)
 
 
 @pytest.mark.parametrize("seed,dtype,beam,blank,chunk", [
