@@ -291,6 +291,18 @@ def test_e2e_edge_cases():
     del torch
 
 
+@pytest.mark.parametrize("seed,N,Trange,V,u_frac", [
+    (61, 1000, (1, 12), 2000, 0.25),        # many short utterances (one lattice wavefront pair each)
+    (62, 1, (40000, 40000), 1000, 0.0025)])  # one very long utterance (40,000 sequential frames)
+def test_e2e_batch_extremes(seed, N, Trange, V, u_frac):
+    wl = workloads.random_small(seed, N=N, T_range=Trange, D=64, V=V, dtype="bf16", p_repeat=0.1, u_frac=u_frac,
+                                beam=16.0, w_std=0.5)
+    say(f"e2e batch extremes N={N} M={wl.M} U_total={int(wl.target_lengths.sum())}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    res = run_gpu(wl)
+    _check_e2e(wl, res, ref, fp32=False)
+
+
 def test_e2e_max_vocab():
     """The largest supported vocabulary (524,288 classes: the limit of the union's on-chip
     membership bitmap) with the blank at the last id, labels drawn over the whole range, and
