@@ -69,7 +69,8 @@ enum { PCTC_UTT_OK = 0, PCTC_UTT_NOT_ALIGNABLE = 1, PCTC_UTT_NONFINITE = 2 };
  * terms scale with M*K (selected log-probabilities and their gradient), the lattice
  * size sum_n T_n (2U_n+1), and M*chunk (one recomputed bf16 gradient chunk).
  * chunk: vocabulary columns recomputed per backward step; 0 selects the default (about
- * 512 MiB of recomputed gradient, see pctc_bwd_chunk).  Returns 0 if the arguments are
+ * 512 MiB of recomputed gradient, see pctc_bwd_chunk); a chunk wider than V rounded up to a
+ * multiple of 256 is taken as that width.  Returns 0 if the arguments are
  * invalid.  The same workspace serves pruned_ctc_fwd_bwd_ex. */
 size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
                            const int32_t* target_lengths, int32_t D, int32_t V, float beam,

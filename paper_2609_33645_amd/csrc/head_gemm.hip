@@ -699,7 +699,9 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
   BwdPlan p{};
   int cap;  // columns the gradient buffer holds (sizes the workspace; independent of V)
   if (chunk > 0) {
-    p.chunk = cap = chunk;
+    // a step never needs more columns than the vocabulary has (rounded up to whole tiles)
+    const int vr = (V > 0 ? V + 255 : 256) / 256 * 256;
+    p.chunk = cap = chunk < vr ? chunk : vr;
   } else {
     // default buffer: M x cap in the input dtype, about 512 MiB (at most 65536 columns);
     // V is then cut into as few equal chunks (multiples of 256 columns) as fit in it, so

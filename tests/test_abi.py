@@ -90,6 +90,10 @@ def test_host_side_sizing_rules():
         assert c - -(-V // n) < 256          # equal chunks, rounded up to whole tiles
     assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 0) == 60160
     assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 1024) == 1024
+    # an explicit chunk wider than the vocabulary is cut to V rounded up to whole tiles
+    assert lib.pctc_bwd_chunk(1, 4215, 512, 1000, 65536) == 1024
+    assert lib.pctc_bwd_chunk(0, 4215, 512, 3000, 1 << 20) == 3072
+    assert lib.pctc_bwd_chunk(1, 4215, 512, 3072, 3072) == 3072
     # the backward's scratch does not grow with V
     b = [lib.pctc_bwd_scratch_bytes(1, 4215, 512, V, 384, 0) for V in (100_000, 180_000, 400_000)]
     assert b[0] > 0 and b[0] == b[1] == b[2]

@@ -245,7 +245,8 @@ def test_e2e_smallest_shapes(dtype, D, V, blank):
 @pytest.mark.parametrize("seed,dtype,beam,blank,chunk", [
     (0, "bf16", math.inf, 0, 0), (1, "bf16", 8.0, 0, 512), (2, "f32", math.inf, 7, 256),
     (3, "bf16", 0.0, 0, 0), (4, "f32", 3.0, 2999, 0), (5, "bf16", 16.0, 1500, 1024),
-    (6, "bf16", 16.0, 0, 1536)])  # two chunks: the second stream's two gated works meet at the last dH
+    (6, "bf16", 16.0, 0, 1536),  # two chunks: the second stream's two gated works meet at the last dH
+    (7, "f32", 16.0, 0, 1 << 16), (8, "bf16", 16.0, 0, 1 << 16)])  # chunk wider than V: one step
 def test_e2e_small(seed, dtype, beam, blank, chunk):
     wl = workloads.random_small(seed, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
                                 blank=blank, beam=beam, w_std=0.5)
