@@ -373,6 +373,48 @@ def test_stage_entry_points_without_frames(dtype):
     assert gl["logp"].shape == (0, K + 1) and gl["lam"].numel() == 0
 
 
+def test_concurrent_calls_on_two_streams():
+    """Two host threads, each on its own stream with its own workspace and outputs, run the
+    fused call at the same time (their second-stream work shares one stream per device):
+    every result equals that of the same call made alone, bit for bit."""
+    import threading
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    say("concurrent calls on two streams")
+    wls = [workloads.random_small(90 + i, N=6, T_range=(40, 160), D=128, V=3000, dtype="bf16", p_repeat=0.1,
+                                  beam=16.0, w_std=0.5) for i in range(2)]
+
+    def call(wl):
+        H, W, y = to_dev(wl)
+        out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+        torch.cuda.current_stream().synchronize()
+        return [out["loss"].cpu(), out["status"].cpu(), out["dH"].cpu(), out["dW"].cpu()]
+
+    alone = [call(wl) for wl in wls]
+    results = [[None] * 3 for _ in wls]
+    errors = []
+
+    def worker(i):
+        try:
+            with torch.cuda.stream(torch.cuda.Stream()):
+                for r in range(3):
+                    results[i][r] = call(wls[i])
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join(timeout=100)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    for i in range(2):
+        for r in range(3):
+            for a, b in zip(results[i][r], alone[i]):
+                assert torch.equal(a, b), (i, r)
+
+
 def test_error_codes():
     import torch
     from paper_2609_33645_amd import prunedctc
