@@ -373,6 +373,41 @@ def test_stage_entry_points_without_frames(dtype):
     assert gl["logp"].shape == (0, K + 1) and gl["lam"].numel() == 0
 
 
+@pytest.mark.parametrize("beam", [math.inf, 0.0])
+def test_e2e_tight_alignment(beam):
+    """Utterances whose targets fill their frames exactly (T = U + repeats) have one alignment
+    (the labels, with a blank only between equal neighbours): the loss is minus the sum of its
+    log-probabilities (fp64 closed form here), pruned or not."""
+    rng = np.random.default_rng(77)
+    V, D = 500, 64
+    ys = [np.array([3, 3, 7], np.int32), np.array([9], np.int32), np.array([4, 5, 5, 5, 6], np.int32)]
+    paths = []
+    for y in ys:
+        pth, prev = [], None
+        for c in y.tolist():
+            if c == prev:
+                pth.append(0)  # the blank (id 0) between equal neighbours
+            pth.append(c)
+            prev = c
+        paths.append(pth)
+    T = np.array([len(q) for q in paths], np.int32)
+    U = np.array([len(y) for y in ys], np.int32)
+    H = workloads.round_to_bf16(rng.standard_normal((int(T.sum()), D)).astype(np.float32))
+    W = workloads.round_to_bf16(rng.standard_normal((V, D)).astype(np.float32) * 0.3)
+    wl = workloads.Workload("tight", "bf16", H, W, np.concatenate(ys), T, U, 0, beam)
+    say(f"e2e tight alignment beam={beam} T={T.tolist()} U={U.tolist()}")
+    z = H.astype(np.float64) @ W.astype(np.float64).T
+    zmax = z.max(axis=1, keepdims=True)
+    logp = z - (zmax + np.log(np.exp(z - zmax).sum(axis=1, keepdims=True)))
+    path = np.concatenate([np.asarray(q) for q in paths])
+    want = -logp[np.arange(path.size), path].sum()
+    res = run_gpu(wl)
+    assert res["status"].tolist() == [0, 0, 0]
+    assert abs(res["loss"] - want) <= 1e-5 * abs(want)
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    _check_e2e(wl, res, ref, fp32=False)
+
+
 def test_concurrent_calls_on_two_streams():
     """Two host threads, each on its own stream with its own workspace and outputs, run the
     fused call at the same time (their second-stream work shares one stream per device):

@@ -118,6 +118,36 @@ def test_uniform_logits_closed_form(T, U, r):
     assert abs(out["loss"] - expect) < 1e-9 * max(1.0, expect)
 
 
+@pytest.mark.parametrize("beam", [math.inf, 0.0])
+def test_tight_alignment_closed_form(beam):
+    # When T = U + r (r adjacent repeats) the only alignment is the labels with a blank
+    # inserted exactly between equal neighbours, so the loss is minus the sum of its
+    # log-softmax values and each frame's occupancy is a one-hot of that path's class; a
+    # zero beam keeps that path.
+    rng = np.random.default_rng(11)
+    V, D, blank = 40, 6, 2
+    y = [5, 5, 9, 9, 9, 1]
+    path = []
+    for i, c in enumerate(y):
+        if i > 0 and y[i - 1] == c:
+            path.append(blank)
+        path.append(c)
+    T = len(path)
+    H = rng.standard_normal((T, D))
+    W = rng.standard_normal((V, D))
+    z = H @ W.T
+    logp = z - (z.max(axis=1, keepdims=True) + np.log(np.exp(z - z.max(axis=1, keepdims=True)).sum(axis=1, keepdims=True)))
+    out = oracle.fwd_bwd(H, W, np.array(y), np.array([T]), np.array([len(y)]), blank=blank, beam=beam)
+    assert out["status"].tolist() == [0]
+    expect = -logp[np.arange(T), path].sum()
+    assert abs(out["loss"] - expect) < 1e-10 * expect
+    # dZ = p - onehot(path) on every frame, so dW = (p - onehot)^T H
+    p = np.exp(logp)
+    onehot = np.zeros_like(p)
+    onehot[np.arange(T), path] = 1.0
+    np.testing.assert_allclose(out["dW"], (p - onehot).T @ H, rtol=0, atol=1e-10)
+
+
 def test_empty_target_closed_form():
     rng = np.random.default_rng(3)
     H = rng.standard_normal((9, 4))
