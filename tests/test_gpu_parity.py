@@ -610,6 +610,27 @@ def test_greedy_decode(seed, dtype, blank, with_bias, D):
             assert got["tokens"][n] == ref["tokens"][n]
 
 
+@pytest.mark.parametrize("dtype,D,V,blank", [("f32", 8, 2, 0), ("bf16", 8, 2, 1), ("bf16", 24, 3, 2),
+                                               ("f32", 24, 300, 299)])
+def test_greedy_decode_smallest_shapes(dtype, D, V, blank):
+    """The greedy head at the narrowest widths and the smallest vocabularies, with one-frame
+    utterances."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(70 + D + V, N=5, T_range=(1, 9), D=D, V=V, dtype=dtype, blank=blank, w_std=0.5)
+    H, W, _ = to_dev(wl)
+    say(f"greedy smallest {dtype} D={D} V={V} T={wl.input_lengths.tolist()}")
+    got = prunedctc.greedy_decode(H, W, wl.input_lengths, blank)
+    H64, W64, b64 = wl.H.astype(np.float64), wl.W.astype(np.float64), np.zeros(V)
+    ref = oracle.greedy_decode(H64, W64, wl.input_lengths, blank, bias=b64)
+    ids, sure = _check_greedy(wl, H64, W64, b64, got, ref)
+    off = np.concatenate([[0], np.cumsum(wl.input_lengths)])
+    for n in range(wl.N):
+        assert got["tokens"][n] == oracle.ctc_collapse(ids[off[n]:off[n + 1]], blank)
+        if sure[off[n]:off[n + 1]].all():
+            assert got["tokens"][n] == ref["tokens"][n]
+
+
 # ---------------------------------------------------------------------------------------
 # grouped logits for a stock CTC (Eq. grouped, Prop. 1, Eq. offsupport)
 # ---------------------------------------------------------------------------------------
