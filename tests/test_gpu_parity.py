@@ -511,6 +511,34 @@ def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w, D):
     assert abs(db[blank] - ref["db"][blank]) <= 2e-3 * max(1.0, abs(ref["db"][blank]))
 
 
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_e2e_negative_weights(dtype):
+    """Loss weights of either sign (and a zero): g = -w_n changes sign with the weight, and only
+    a zero weight removes an utterance from the backward."""
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    wl = workloads.random_small(57, N=5, T_range=(20, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15, beam=16.0,
+                                w_std=0.5)
+    w = np.array([1.5, -0.4, 0.0, -0.6, 1.2], np.float32)
+    b = np.random.default_rng(57).standard_normal(wl.V).astype(np.float32)
+    say(f"e2e negative weights {dtype} M={wl.M} w={w.tolist()}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
+                         bias=b.astype(np.float64), weights=w.astype(np.float64))
+    H, W, y = to_dev(wl)
+    out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
+                                       bias=torch.from_numpy(b).cuda(), utt_weight=torch.from_numpy(w).cuda(),
+                                       want_db=True)
+    res = {"loss": float(out["loss"].item()), "status": out["status"].cpu().numpy(), "dH": out["dH"].cpu().numpy(),
+           "dW": out["dW"].cpu().numpy()}
+    np.testing.assert_allclose(out["loss_per_utt"].cpu().numpy(), ref["loss_n"], rtol=1e-5, atol=1e-6)
+    _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
+    db = out["db"].cpu().numpy()
+    if dtype == "f32":
+        assert rel_err(db, ref["db"]) <= 1e-4
+    else:
+        assert cosine(db, ref["db"]) >= 0.99999
+
+
 # ---------------------------------------------------------------------------------------
 # discarded posterior mass (App. B.3)
 # ---------------------------------------------------------------------------------------
