@@ -568,6 +568,18 @@ def test_e2e_masked_vocabulary(dtype):
     assert np.isfinite(db).all() and np.isfinite(res["dW"]).all() and np.isfinite(res["dH"]).all()
 
 
+@pytest.mark.parametrize("dtype,beam", [("bf16", 16.0), ("f32", math.inf)])
+def test_e2e_large_logits(dtype, beam):
+    """Logits with a spread of hundreds of nats (near one-hot probabilities: the exponentials
+    underflow for almost every class, the lattice's scores move by hundreds per frame)."""
+    wl = workloads.random_small(59, N=4, T_range=(20, 120), D=128, V=3000, dtype=dtype, p_repeat=0.15, beam=beam,
+                                w_std=5.0)
+    say(f"e2e large logits {dtype} beam={beam} M={wl.M}")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    res = run_gpu(wl)
+    _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
+
+
 # ---------------------------------------------------------------------------------------
 # discarded posterior mass (App. B.3)
 # ---------------------------------------------------------------------------------------
