@@ -10,7 +10,7 @@ from .prunedctc_oracle import (  # noqa: F401
     OracleError,
     PCTC_OK, PCTC_EINVAL, PCTC_ELABEL, PCTC_ELENGTH,
     STATUS_OK, STATUS_NOT_ALIGNABLE, STATUS_NONFINITE,
-    KEEP_SLACK,
+    beam_round_tol,
     validate,
     union_remap,
     log_normalizer,

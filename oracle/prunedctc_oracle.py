@@ -25,7 +25,9 @@ What it computes, with the passage each step follows:
   excluded or nonfinite utterances contribute zero loss and zero gradient.
 * Gradient dL/dZ_{m,v} = p_v(m) - gamma_v(m) (Eq. "grad-full"; for a pruned
   lattice held fixed, gamma is the occupancy over retained alignments, Sec. 3.3),
-  and the head gradients dX = dZ W, dW = dZ^T X (App. A, end of Step 3).
+  formed as written in fwd_bwd, and the head gradients dX = dZ W, dW = dZ^T X
+  (App. A, end of Step 3).  The recomputed form scatter_U(G) - g p of Eq. "vjp" is
+  the separate stage function head_backward.
 
 Everything is float64.  Inputs are taken exactly as the device sees them (bf16
 values are exact in float32, and float32 is exact in float64).
@@ -47,9 +49,20 @@ STATUS_OK = 0
 STATUS_NOT_ALIGNABLE = 1
 STATUS_NONFINITE = 2
 
-# Slack (nats) added to the beam threshold so that the best alignment is never lost
-# to rounding when beta is 0 (reading of App. B.3; the paper states no tie rule).
-KEEP_SLACK = 1e-3
+
+def beam_round_tol(E: np.ndarray) -> float:
+    """Rounding allowance of the beam rule for one utterance (E [T, S']: per-frame scores).
+
+    The rule of App. B.3 compares the best alignment through an arc with the best alignment
+    overall.  Both are sums of T per-frame scores, evaluated here in different orders (the
+    forward recursion up to the arc, the backward one after it).  Recursive summation of T
+    terms in float64 errs by at most (T - 1) u sum|x| (u = 2^-53), so two evaluations of the
+    same path score differ by at most 2 T u A with A = sum_t max_s |E_t(s)|.  Twice that
+    (4 T u A) is allowed: it keeps the best alignment's own arcs at beta = 0 and is far below
+    any margin the tests use; it is not a tolerance of the method."""
+    fin = np.where(np.isfinite(E), np.abs(E), 0.0)
+    A = float(fin.max(axis=1).sum()) if fin.size else 0.0
+    return 4.0 * E.shape[0] * 2.0 ** -53 * max(A, 1.0)
 
 
 class OracleError(ValueError):
@@ -237,13 +250,18 @@ def _all_arcs(T: int, S: int) -> Dict[str, np.ndarray]:
 
 
 def ctc_utterance(logp: np.ndarray, y: Sequence[int], blank_col: int, beam: float = math.inf,
-                  slack: float = KEEP_SLACK) -> Dict[str, object]:
+                  slack: float = 0.0) -> Dict[str, object]:
     """CTC (or beam-pruned CTC) for one utterance.
 
     logp: [T, C] log-probabilities over some column space; y: labels in that space;
     blank_col: the blank's column.  Returns log P (log of the retained alignment sum),
     per-state occupancies gamma [T, 2U+1], the extended labels, the arc keep flags and,
-    when pruning, the signed margin of every arc's decision.
+    when pruning, the signed margin of every arc's decision (through-score minus
+    (best - beta); the arc is kept iff its margin >= -(rounding allowance + slack)).
+
+    The paper's rule is slack = 0.  A non-zero slack moves the threshold by that many nats
+    (positive keeps more arcs); tests use it only to bracket a device result whose own
+    threshold carries a stated tolerance.
     """
     logp = np.asarray(logp, np.float64)
     T = logp.shape[0]
@@ -257,7 +275,8 @@ def ctc_utterance(logp: np.ndarray, y: Sequence[int], blank_col: int, beam: floa
     margins = None
     if beam_enabled(beam):
         va, vb, vbest = _recursions(E, skip_ok, keep, "max")
-        thr = vbest - beam - slack
+        thr = vbest - beam
+        allow = beam_round_tol(E) + slack
         margins = {}
         with np.errstate(invalid="ignore"):
             margins["start"] = np.where(keep["start"], E[0] + vb[0] - thr, -np.inf)
@@ -271,7 +290,7 @@ def ctc_utterance(logp: np.ndarray, y: Sequence[int], blank_col: int, beam: floa
                 margins["step"][1:] = _shift_right(va[:-1], 1) + through_in - thr
                 margins["skip"][1:] = np.where(skip_ok, _shift_right(va[:-1], 2) + through_in - thr,
                                                -np.inf)
-        keep = {k: keep[k] & (margins[k] >= 0.0) for k in keep}
+        keep = {k: keep[k] & (margins[k] >= -allow) for k in keep}
         out["viterbi_best"] = vbest
     alpha, beta, logP = _recursions(E, skip_ok, keep, "lse")
     with np.errstate(invalid="ignore", over="ignore"):
@@ -289,7 +308,7 @@ def _offsets(lengths) -> np.ndarray:
 
 
 def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: float = math.inf,
-                    slack: float = KEEP_SLACK, weights=None) -> Dict[str, object]:
+                    slack: float = 0.0, weights=None) -> Dict[str, object]:
     """The alignment stage alone: given per-frame scores S [M, K] over the selected classes
     (blank = column 0) and relabelled targets, return per-utterance losses, statuses, the
     occupancy-derived G = dL/dS (G[m, j] = -gamma over the states labelled j; zero for
@@ -327,7 +346,7 @@ def ctc_from_scores(S: np.ndarray, y_rel, input_lengths, target_lengths, beam: f
 
 
 def discarded_mass(S: np.ndarray, y_rel, input_lengths, target_lengths, beams,
-                   slack: float = KEEP_SLACK) -> np.ndarray:
+                   slack: float = 0.0) -> np.ndarray:
     """Discarded posterior mass (App. B.3): delta[b, n] = 1 - exp(-(L_beta,n - L_n)) for each
     beam, the posterior mass (given the transcript) of the alignments the beam drops, from
     the pruned and unpruned losses on the same scores (fp64), evaluated as
@@ -424,7 +443,7 @@ def head_backward_rows(H, W, lam, G, g, u_ids, frames, classes, chunk: int = 409
 # ---------------------------------------------------------------------------------------
 
 def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: float = math.inf,
-            chunk: int = 4096, want_grads: bool = True, slack: float = KEEP_SLACK, bias=None,
+            chunk: int = 4096, want_grads: bool = True, slack: float = 0.0, bias=None,
             weights=None) -> Dict[str, object]:
     """Loss and gradients of (beam-pruned) CTC on log-softmax(H W^T + 1 b^T) over the full
     vocabulary (Sec. 2 head (W, b); Eqs. lognorm, ctc, pruned-ctc).
@@ -453,8 +472,6 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
     loss_n = np.zeros(N)
     status = np.zeros(N, np.int64)
     included = np.zeros(M, bool)
-    gamma_cols: List[np.ndarray] = []   # per utterance: the full-vocabulary ids of its states
-    gamma_vals: List[np.ndarray] = []
     per_utt = []
     for n in range(N):
         rows = slice(int(toff[n]), int(toff[n + 1]))
@@ -489,21 +506,36 @@ def fwd_bwd(H, W, targets, input_lengths, target_lengths, blank: int, beam: floa
            "included": included}
     if not want_grads:
         return out
-    # dZ = p - gamma (Eq. grad-full), dense over V, one chunk at a time; zero on excluded frames.
+    # Eq. grad-full: dL/dZ[m, v] = w_n (p_v(m) - gamma_v(m)) for a frame m of an included
+    # utterance n (zero on the frames of excluded ones), with gamma_v(m) the occupancy of
+    # class v at frame m summed over the states labelled v; dense over V, one chunk at a time.
+    w_frame = np.zeros(M)
+    for n in range(N):
+        if status[n] == STATUS_OK:
+            w_frame[int(toff[n]):int(toff[n + 1])] = wv[n]
+    occ_cols = []   # per included utterance: first frame, its class ids, gamma_v per class
+    for n in range(N):
+        if status[n] != STATUS_OK:
+            continue
+        res = per_utt[n]
+        ext_ids = res["cols"][res["ext"]]
+        classes = np.unique(ext_ids)
+        occ = np.zeros((res["gamma"].shape[0], classes.size))
+        for s in range(ext_ids.size):
+            occ[:, int(np.searchsorted(classes, ext_ids[s]))] += res["gamma"][:, s]
+        occ_cols.append((int(toff[n]), classes, occ))
     dH = np.zeros((M, D))
     dW = np.zeros((V, D))
     db = np.zeros(V)
     inc = included
     for v0 in range(0, V, chunk):
         v1 = min(V, v0 + chunk)
-        Z = H[inc] @ W[v0:v1].T + b[v0:v1]
-        # dZ = -g p - (-G) scattered: -g_m = w_n for a frame of included utterance n
-        dZ = -G.sum(axis=1)[inc, None] * np.exp(Z - lam[inc, None])
-        # subtract the occupancies gamma_v(m) for v in this chunk
-        Ginc = G[inc]
-        for j, v in enumerate(un["u_ids"]):
-            if v0 <= v < v1:
-                dZ[:, v - v0] += Ginc[:, j]
+        p = np.exp(H[inc] @ W[v0:v1].T + b[v0:v1] - lam[inc, None])
+        gam = np.zeros((M, v1 - v0))
+        for t0, classes, occ in occ_cols:
+            sel = (classes >= v0) & (classes < v1)
+            gam[t0:t0 + occ.shape[0], classes[sel] - v0] = occ[:, sel]
+        dZ = w_frame[inc, None] * (p - gam[inc])
         dH[inc] += dZ @ W[v0:v1]
         dW[v0:v1] = dZ.T @ H[inc]
         db[v0:v1] = dZ.sum(axis=0)

@@ -20,7 +20,7 @@ import pytest
 
 import oracle
 from paper_2609_33645_amd import workloads
-from tests.gpu_util import cosine, loss_rel, rel_err, say, to_dev
+from tests.gpu_util import KERNEL_BAND, ambiguous_arcs, beam_bracket, cosine, loss_rel, rel_err, say, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -73,8 +73,11 @@ def _mask_check(res_utt, mk, T, Sp, band=1e-2):
     return compared, bad
 
 
+# Every workload at every beam it is specified with (Qwen3-32B: the beam sweep {8, 16, 64}),
+# plus the K-stress variant and the encoder memory shape in fp32.
 FULL = [("zipformer_m", 16.0), ("zipformer_m", math.inf), ("qwen3_0p6b", 32.0), ("qwen3_8b", 32.0),
-        ("qwen3_32b", 16.0), ("qwen3_8b_kstress", 32.0), ("e1_zipformer_f32", math.inf)]
+        ("qwen3_8b", math.inf), ("qwen3_32b", 8.0), ("qwen3_32b", 16.0), ("qwen3_32b", 64.0),
+        ("qwen3_8b_kstress", 32.0), ("e1_zipformer_f32", math.inf)]
 
 
 @pytest.mark.timeout(900)
@@ -114,7 +117,20 @@ def test_full_size_parity(name, beam):
     ln = out["loss_per_utt"].cpu().numpy()
     assert loss_rel(float(out["loss"].item()), dp["loss"]) <= 2e-3
     assert np.abs(ln - dp["loss_n"]).max() / np.abs(dp["loss_n"]).max() <= 2e-3
-    np.testing.assert_allclose(ln, dp["loss_n"], rtol=1e-5)          # achieved accuracy
+    if math.isfinite(beam):
+        # arcs within the kernel's tolerance band of the threshold may be decided either way
+        # by the device: its losses must lie between the oracle's with those arcs all kept and
+        # all dropped (the paper's rule lies between the two as well)
+        dp["S"], dp["y_rel"] = S, ref_un["y_rel"]
+        lo, hi = beam_bracket(dp, wl.input_lengths, wl.target_lengths, beam)
+        width = np.abs(lo["loss_n"] - hi["loss_n"]) / np.abs(dp["loss_n"]).clip(1.0)
+        say(f"  {ambiguous_arcs(dp)} arcs within {KERNEL_BAND} nats of the threshold; "
+            f"relative loss bracket {width.max():.3g}")
+        tol = 1e-5 * np.abs(dp["loss_n"])
+        assert np.all(ln >= np.minimum(lo["loss_n"], hi["loss_n"]) - tol)
+        assert np.all(ln <= np.maximum(lo["loss_n"], hi["loss_n"]) + tol)
+    if not math.isfinite(beam) or width.max() <= 1e-7:
+        np.testing.assert_allclose(ln, dp["loss_n"], rtol=1e-5)      # achieved accuracy
 
     rng = np.random.default_rng(7)
     frames, classes = _samples(wl, rng, ref_un["u_ids"])
@@ -301,11 +317,11 @@ def test_full_size_grouped_export():
     torch.cuda.empty_cache()
 
 
-@pytest.mark.timeout(600)
+@pytest.mark.timeout(900)
 def test_e3_memory_shape_frozen_head():
     """The LLM benchmark's memory shape (107 utterances, M = 11,458, D = 4096, V = 151,936,
     head frozen: no dW).  Utterance losses and dH rows depend only on their own utterance, so
-    the first two utterances are checked against the oracle run on those two alone."""
+    ten utterances spread over the batch are checked against the oracle run on those alone."""
     import torch
     from paper_2609_33645_amd import prunedctc
     wl = workloads.NAMED["e3_qwen3_8b"](0)
@@ -321,17 +337,22 @@ def test_e3_memory_shape_frozen_head():
     say(f"  peak above inputs {peak:.1f} MiB (workspace {out['workspace_bytes'] / 2**20:.1f} MiB)")
     assert out["dW"] is None
     assert (out["status"].cpu().numpy() == 0).all()
-    n2 = 2
-    T2, U2 = wl.input_lengths[:n2], wl.target_lengths[:n2]
-    M2, Y2 = int(T2.sum()), int(U2.sum())
-    ref = oracle.fwd_bwd(wl.H[:M2].astype(np.float64), wl.W.astype(np.float64), wl.targets[:Y2], T2, U2, wl.blank,
-                         wl.beam)
-    ln = out["loss_per_utt"].cpu().numpy()[:n2]
-    say(f"  losses gpu={ln.tolist()} oracle={ref['loss_n'].tolist()}")
+    pick = np.linspace(0, wl.N - 1, 10).round().astype(np.int64)
+    toff = np.concatenate([[0], np.cumsum(wl.input_lengths)])
+    yoff = np.concatenate([[0], np.cumsum(wl.target_lengths)])
+    fr = np.concatenate([np.arange(toff[n], toff[n + 1]) for n in pick])
+    T2, U2 = wl.input_lengths[pick], wl.target_lengths[pick]
+    y2 = np.concatenate([wl.targets[yoff[n]:yoff[n + 1]] for n in pick])
+    ref = oracle.fwd_bwd(wl.H[fr].astype(np.float64), wl.W.astype(np.float64), y2, T2, U2, wl.blank, wl.beam)
+    ln = out["loss_per_utt"].cpu().numpy()[pick]
+    say(f"  utterances {pick.tolist()}: losses gpu={ln.tolist()} oracle={ref['loss_n'].tolist()}")
     np.testing.assert_allclose(ln, ref["loss_n"], rtol=1e-5)
-    dH = out["dH"][:M2].cpu().numpy()
+    dH = out["dH"][torch.from_numpy(fr).cuda()].cpu().numpy()
     c = cosine(dH, ref["dH"])
-    say(f"  dH rows of the two utterances: cos={c:.7f} rel={rel_err(dH, ref['dH']):.3g}")
+    say(f"  dH rows of those utterances: cos={c:.7f} rel={rel_err(dH, ref['dH']):.3g}")
     assert c >= 0.99999
+    for i, n in enumerate(pick):       # utterance by utterance
+        rows = slice(int(np.sum(T2[:i])), int(np.sum(T2[:i + 1])))
+        assert cosine(dH[rows], ref["dH"][rows]) >= 0.99999, f"utterance {n}"
     del out, H, W, y
     torch.cuda.empty_cache()

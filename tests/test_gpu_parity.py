@@ -12,7 +12,7 @@ import pytest
 
 import oracle
 from paper_2609_33645_amd import workloads
-from tests.gpu_util import cosine, loss_rel, rel_err, run_gpu, say, to_dev
+from tests.gpu_util import cosine, loss_rel, rel_err, run_gpu, say, to_dev, unambiguous_case
 
 pytestmark = pytest.mark.gpu
 
@@ -228,12 +228,12 @@ def test_e2e_smallest_shapes(dtype, D, V, blank):
     """The narrowest heads (D = 8, the minimum; D = 24, not a whole k-tile of the products)
     and the smallest vocabularies (V = 2: the blank and one label), with one-frame
     utterances among the rest."""
-    wl = workloads.random_small(40 + D + V, N=5, T_range=(1, 5) if V <= 3 else (1, 30), D=D, V=V, dtype=dtype,
-                                token_law="uniform",
-                                p_repeat=0.2, blank=blank, beam=16.0 if V > 3 else math.inf, w_std=0.5)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=5, T_range=(1, 5) if V <= 3 else (1, 30), D=D, V=V, dtype=dtype,
+                                         token_law="uniform", p_repeat=0.2, blank=blank,
+                                         beam=16.0 if V > 3 else math.inf, w_std=0.5), 40 + D + V)
     say(f"e2e smallest {dtype} D={D} V={V} blank={blank} T={wl.input_lengths.tolist()} "
         f"U={wl.target_lengths.tolist()}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl)
     # With V <= 3 every class is in the union and dZ = p - gamma is a difference of two O(1)
     # numbers whose dense part p is rounded to bf16: the cancellation amplifies that rounding
@@ -248,10 +248,10 @@ def test_e2e_smallest_shapes(dtype, D, V, blank):
     (6, "bf16", 16.0, 0, 1536),  # two chunks: the second stream's two gated works meet at the last dH
     (7, "f32", 16.0, 0, 1 << 16), (8, "bf16", 16.0, 0, 1 << 16)])  # chunk wider than V: one step
 def test_e2e_small(seed, dtype, beam, blank, chunk):
-    wl = workloads.random_small(seed, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
-                                blank=blank, beam=beam, w_std=0.5)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
+                                         blank=blank, beam=beam, w_std=0.5), seed)
     say(f"e2e small seed={seed} {dtype} beam={beam} blank={blank} M={wl.M} T={wl.input_lengths.tolist()}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl, chunk=chunk)
     _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
 
@@ -296,10 +296,10 @@ def test_e2e_edge_cases():
     (61, 1000, (1, 12), 2000, 0.25),        # many short utterances (one lattice wavefront pair each)
     (62, 1, (40000, 40000), 1000, 0.0025)])  # one very long utterance (40,000 sequential frames)
 def test_e2e_batch_extremes(seed, N, Trange, V, u_frac):
-    wl = workloads.random_small(seed, N=N, T_range=Trange, D=64, V=V, dtype="bf16", p_repeat=0.1, u_frac=u_frac,
-                                beam=16.0, w_std=0.5)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=N, T_range=Trange, D=64, V=V, dtype="bf16", p_repeat=0.1,
+                                         u_frac=u_frac, beam=16.0, w_std=0.5), seed)
     say(f"e2e batch extremes N={N} M={wl.M} U_total={int(wl.target_lengths.sum())}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl)
     _check_e2e(wl, res, ref, fp32=False)
 
@@ -309,10 +309,10 @@ def test_e2e_max_vocab():
     membership bitmap) with the blank at the last id, labels drawn over the whole range, and
     several backward chunks."""
     V = 524288
-    wl = workloads.random_small(12, N=3, T_range=(20, 60), D=64, V=V, dtype="bf16", token_law="uniform",
-                                p_repeat=0.1, blank=V - 1, beam=16.0, w_std=0.5)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=3, T_range=(20, 60), D=64, V=V, dtype="bf16", token_law="uniform",
+                                         p_repeat=0.1, blank=V - 1, beam=16.0, w_std=0.5), 12)
     say(f"e2e max vocabulary V={V} M={wl.M} T={wl.input_lengths.tolist()}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl, chunk=65536)
     _check_e2e(wl, res, ref, fp32=False)
 
@@ -481,17 +481,17 @@ def test_error_codes():
 def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w, D):
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(40 + seed, N=5, T_range=(1, 140), D=D, V=3000, dtype=dtype, p_repeat=0.15,
-                                blank=blank, beam=beam, w_std=0.5 * math.sqrt(128 / D))
     rng = np.random.default_rng(seed)
-    b = rng.standard_normal(wl.V).astype(np.float32)
+    b = rng.standard_normal(3000).astype(np.float32)
     b[blank] += 2.0                                  # blank offset eta
-    w = rng.uniform(0.05, 2.0, size=wl.N).astype(np.float32)
+    w = rng.uniform(0.05, 2.0, size=5).astype(np.float32)
     if zero_w:
         w[1] = 0.0
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=5, T_range=(1, 140), D=D, V=3000, dtype=dtype, p_repeat=0.15,
+                                         blank=blank, beam=beam, w_std=0.5 * math.sqrt(128 / D)), 40 + seed,
+        bias=b.astype(np.float64), weights=w.astype(np.float64))
     say(f"e2e bias/weights seed={seed} {dtype} beam={beam} blank={blank} M={wl.M} w={np.round(w, 3).tolist()}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
-                         bias=b.astype(np.float64), weights=w.astype(np.float64))
     H, W, y = to_dev(wl)
     out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam, chunk=chunk,
                                        bias=torch.from_numpy(b).cuda(), utt_weight=torch.from_numpy(w).cuda(),
@@ -517,13 +517,13 @@ def test_e2e_negative_weights(dtype):
     a zero weight removes an utterance from the backward."""
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(57, N=5, T_range=(20, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15, beam=16.0,
-                                w_std=0.5)
     w = np.array([1.5, -0.4, 0.0, -0.6, 1.2], np.float32)
-    b = np.random.default_rng(57).standard_normal(wl.V).astype(np.float32)
+    b = np.random.default_rng(57).standard_normal(3000).astype(np.float32)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=5, T_range=(20, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
+                                         beam=16.0, w_std=0.5), 57,
+        bias=b.astype(np.float64), weights=w.astype(np.float64))
     say(f"e2e negative weights {dtype} M={wl.M} w={w.tolist()}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
-                         bias=b.astype(np.float64), weights=w.astype(np.float64))
     H, W, y = to_dev(wl)
     out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
                                        bias=torch.from_numpy(b).cuda(), utt_weight=torch.from_numpy(w).cuda(),
@@ -545,18 +545,22 @@ def test_e2e_masked_vocabulary(dtype):
     normaliser tiles): those classes get probability 0, so zero gradient rows in dW and db."""
     import torch
     from paper_2609_33645_amd import prunedctc
-    wl = workloads.random_small(58, N=4, T_range=(20, 120), D=128, V=5000, dtype=dtype, p_repeat=0.15, beam=16.0,
-                                w_std=0.5)
-    rng = np.random.default_rng(58)
-    b = rng.standard_normal(wl.V).astype(np.float32)
-    masked = rng.random(wl.V) < 0.3
-    masked[2048:3072] = True                      # whole tiles with no finite logit
-    masked[np.unique(wl.targets)] = False
-    masked[wl.blank] = False
-    b[masked] = -np.inf
+    def masked_bias(wl):
+        rng = np.random.default_rng(58)
+        b = rng.standard_normal(wl.V).astype(np.float32)
+        masked = rng.random(wl.V) < 0.3
+        masked[2048:3072] = True                      # whole tiles with no finite logit
+        masked[np.unique(wl.targets)] = False
+        masked[wl.blank] = False
+        b[masked] = -np.inf
+        return b, masked
+
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=4, T_range=(20, 120), D=128, V=5000, dtype=dtype, p_repeat=0.15,
+                                         beam=16.0, w_std=0.5), 58,
+        kw_of=lambda wl: {"bias": masked_bias(wl)[0].astype(np.float64)})
+    b, masked = masked_bias(wl)
     say(f"e2e masked vocabulary {dtype} M={wl.M} masked={int(masked.sum())}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
-                         bias=b.astype(np.float64))
     H, W, y = to_dev(wl)
     out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam,
                                        bias=torch.from_numpy(b).cuda(), want_db=True)
@@ -572,10 +576,10 @@ def test_e2e_masked_vocabulary(dtype):
 def test_e2e_large_logits(dtype, beam):
     """Logits with a spread of hundreds of nats (near one-hot probabilities: the exponentials
     underflow for almost every class, the lattice's scores move by hundreds per frame)."""
-    wl = workloads.random_small(59, N=4, T_range=(20, 120), D=128, V=3000, dtype=dtype, p_repeat=0.15, beam=beam,
-                                w_std=5.0)
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=4, T_range=(20, 120), D=128, V=3000, dtype=dtype, p_repeat=0.15,
+                                         beam=beam, w_std=5.0), 59)
     say(f"e2e large logits {dtype} beam={beam} M={wl.M}")
-    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
     res = run_gpu(wl)
     _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
 

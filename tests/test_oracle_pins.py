@@ -374,17 +374,22 @@ BEAM_CASES = [(6, 4, [1, 2, 1], 0), (6, 3, [1, 1], 0), (7, 3, [2, 1], 0), (5, 4,
 def test_beam_matches_enumeration(T, C, y, blank, beam):
     rng = np.random.default_rng(T * 7 + C + len(y) * 3)
     logp = _logsoftmax(rng.standard_normal((T, C)) * 2.5)
-    ref = brute.brute_ctc(logp, y, blank, beam=beam, slack=O.KEEP_SLACK)
+    ref = brute.brute_ctc(logp, y, blank, beam=beam)  # the paper's rule: no slack
     res = oracle.ctc_utterance(logp, y, blank, beam=beam)
     assert abs(res["logP"] - ref["logP"]) < 1e-12
     gam = np.zeros((T, C))
     for s, c in enumerate(res["ext"]):
         gam[:, c] += res["gamma"][:, s]
     np.testing.assert_allclose(gam, ref["gamma"], atol=1e-12)
-    # no arc decision sits on the threshold in these cases
+    # no arc decision sits on the threshold in these cases, except at beta = 0, where the
+    # best alignment's own arcs score exactly the best (margin 0 up to rounding) and are kept
     for k, m in res["margins"].items():
-        fm = np.asarray(m)[np.isfinite(m)]
-        assert (np.abs(fm) > 1e-9).all(), k
+        fin = np.isfinite(m)
+        near = np.abs(np.asarray(m)[fin]) <= 1e-9
+        if beam == 0.0:
+            assert np.asarray(res["keep"][k])[fin][near].all(), k
+        else:
+            assert not near.any(), k
 
 
 def test_beam_properties():
@@ -418,6 +423,24 @@ def test_beam_zero_keeps_only_best_path():
     assert abs(res["logP"] - max(ref["scores"])) < 1e-12
     gam = res["gamma"]
     assert set(np.round(gam, 12).ravel().tolist()) <= {0.0, 1.0}
+
+
+@pytest.mark.parametrize("gap", [5e-4, -5e-4, 1e-7, -1e-7])
+def test_beam_threshold_is_the_papers(gap):
+    """App. B.3 keeps an arc iff the best alignment through it is within beta of the best:
+    an alignment scoring best - beta - gap is dropped for any gap > 0, however small, and
+    kept for gap <= 0.  Two frames, target [1]: alignments (1,1) = 0, (1,-) = -beta - gap
+    and (-,1) = -beta + 0.25 written into the scores; the expected sum is enumerated."""
+    beta = 2.0
+    logp = np.array([[-beta + 0.25, 0.0, -30.0],
+                     [-beta - gap, 0.0, -30.0]])
+    res = oracle.ctc_utterance(logp, [1], 0, beam=beta)
+    ref = brute.brute_ctc(logp, [1], 0, beam=beta)
+    kept = [0.0, -beta + 0.25] + ([-beta - gap] if gap <= 0 else [])
+    want = math.log(sum(math.exp(x) for x in kept))
+    assert abs(ref["logP"] - want) < 1e-14
+    assert abs(res["logP"] - want) < 1e-14
+    assert ref["n_kept"] == len(kept)
 
 
 def test_scores_stage_matches_full_path():
@@ -586,7 +609,7 @@ def test_discarded_mass_by_enumeration(seed, beam):
     for pi, sc in zip(aligns, scores):
         for a in brute.arcs_of(pi, 0):
             best_through[a] = max(best_through.get(a, -math.inf), sc)
-    kept = {a for a, v in best_through.items() if v >= scores.max() - beam - oracle.KEEP_SLACK}
+    kept = {a for a, v in best_through.items() if v >= scores.max() - beam}
     keep = np.array([all(a in kept for a in brute.arcs_of(pi, 0)) for pi in aligns])
     want = 1.0 - np.exp(scores[keep]).sum() / np.exp(scores).sum()
     got = oracle.discarded_mass(logp, np.array(y), [T], [len(y)], [beam])
