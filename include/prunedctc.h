@@ -85,8 +85,10 @@ size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_len
  * blank    the blank class id, 0 <= blank < V.  It becomes column 0 of the union.
  * beam     alignment beam in natural-log units (Sec. 3.3, App. B.3).  A finite value
  *          >= 0 prunes every lattice arc whose best complete alignment scores more than
- *          beam (+1e-3 slack) below the best alignment; +INF or a negative value keeps
- *          all alignments (unpruned reduced CTC).  NaN is PCTC_EINVAL.
+ *          beam below the best alignment; +INF or a negative value keeps all alignments
+ *          (unpruned reduced CTC).  NaN is PCTC_EINVAL.  Tolerance: the rule is evaluated
+ *          in float32 and arcs up to 1e-3 nats beyond the beam are kept, so that rounding
+ *          never drops the best alignment (at beam 0 the best path is always kept).
  * chunk    vocabulary columns per backward recompute step (0 = the default of
  *          pctc_bwd_chunk; otherwise a positive multiple of 256).
  * loss     device double [1]: sum over utterances of the finite per-utterance losses.
@@ -131,6 +133,31 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
                               const float* utt_weight, double* loss, double* loss_per_utt,
                               int32_t* utt_status, float* dH, float* dW, float* db,
                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid allocation): pruned_ctc_fwd_bwd_ex without a
+ * workspace argument.  Its scratch is a file-scope device array of
+ * PCTC_NOALLOC_SCRATCH_MIB MiB inside the library, one copy per device, held from the
+ * first call on a device until the process ends; the call allocates nothing (no
+ * hipMalloc, no events, no second stream: every step runs on `stream` in Algorithm 1's
+ * order).  Inputs and outputs are the caller's, as for pruned_ctc_fwd_bwd_ex.
+ * chunk 0 selects the widest backward chunk whose layout fits the scratch (results then
+ * differ from pruned_ctc_fwd_bwd_ex's only by summation order); a batch that needs more
+ * scratch than the array holds even at the narrowest chunk, or an explicit chunk that does
+ * not fit, returns PCTC_EWORKSPACE before any work is queued (pctc_last_error() states
+ * both sizes).  Every call on a device shares that device's array and leaves its contents
+ * behind (nothing is assumed zero on entry): calls that overlap in time on one device,
+ * from any streams or threads, race and give unspecified results.  Synchronises `stream`
+ * once at the end, like pruned_ctc_fwd_bwd_ex. */
+#define PCTC_NOALLOC_SCRATCH_MIB 256
+size_t pctc_noalloc_scratch_bytes(void);
+int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, const void* W,
+                                   const float* bias, int32_t V, const int32_t* targets,
+                                   const int32_t* input_lengths, const int32_t* target_lengths,
+                                   int32_t N, int32_t blank, float beam, int32_t chunk,
+                                   const float* utt_weight, double* loss, double* loss_per_utt,
+                                   int32_t* utt_status, float* dH, float* dW, float* db,
+                                   void* stream);
 
 /* Human-readable text of a status code, and the text of the last HIP error seen by the
  * calling thread. */

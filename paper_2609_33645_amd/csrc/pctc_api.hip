@@ -270,22 +270,18 @@ int32_t pruned_ctc_fwd_bwd(pctc_dtype dtype, const void* H, int32_t D, const voi
                                workspace_bytes, stream_ptr);
 }
 
-int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
-                              const int32_t* targets, const int32_t* input_lengths, const int32_t* target_lengths,
-                              int32_t N, int32_t blank, float beam, int32_t chunk, const float* utt_weight,
-                              double* loss, double* loss_per_utt, int32_t* utt_status, float* dH, float* dW,
-                              float* db, void* workspace, size_t workspace_bytes, void* stream_ptr) {
-  int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
-  if (st != PCTC_OK) return st;
-  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
-  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
-  if (L.M > 0 && !H) return PCTC_EINVAL;
-  if (L.Y > 0 && !targets) return PCTC_EINVAL;
-  if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
-  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
-  hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
+}  // extern "C"
+
+// The whole path on a workspace laid out by L (arguments checked by the caller).
+// two_streams: the bf16 path may run the lattice and the union-column part on a second
+// stream beside the dense part of the backward (events are created per call); otherwise
+// every step runs on `stream` in Algorithm 1's order.
+static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
+                           const int32_t* targets, const int32_t* input_lengths, const int32_t* target_lengths,
+                           int32_t N, int32_t blank, float beam, const Layout& L, const float* utt_weight,
+                           double* loss, double* loss_per_utt, int32_t* utt_status, float* dH, float* dW, float* db,
+                           char* ws, hipStream_t stream, bool two_streams) {
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
-  char* ws = static_cast<char*>(workspace);
   int32_t* remap = reinterpret_cast<int32_t*>(ws + L.o_remap);
   int32_t* u_ids = reinterpret_cast<int32_t*>(ws + L.o_uids);
   int32_t* y_rel = reinterpret_cast<int32_t*>(ws + L.o_yrel);
@@ -307,7 +303,7 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
   const bool want_bwd = (dH || dW || db);
   int32_t* fflag = Kdev + 2;  // forecast mismatch flag
-  const bool overlap = (dt == 1) && want_bwd && L.M > 0 && N > 0;
+  const bool overlap = two_streams && (dt == 1) && want_bwd && L.M > 0 && N > 0;
   hipStream_t dps_stream = stream;
   struct Events {
     hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, gate0 = nullptr, gate1 = nullptr, dh_done = nullptr,
@@ -458,6 +454,88 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   prof_flush();
   if (hflags[0]) return PCTC_ELABEL;
   return PCTC_OK;
+}
+
+// Scratch of the allocation-free entry point: one copy per device, held from the library's
+// first use of a device until the process ends.  Host code reaches it only through the
+// address hipGetSymbolAddress returns for the current device (noalloc_scratch).
+constexpr size_t kNoAllocScratchBytes = static_cast<size_t>(PCTC_NOALLOC_SCRATCH_MIB) << 20;
+static __device__ __align__(256) char scratch[kNoAllocScratchBytes];
+
+static hipError_t noalloc_scratch(char** out) {
+  static std::mutex mu;
+  static std::map<int, char*> ptrs;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(mu);
+  auto it = ptrs.find(dev);
+  if (it == ptrs.end()) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || (reinterpret_cast<uintptr_t>(p) & 255) != 0) return hipErrorInvalidSymbol;
+    it = ptrs.emplace(dev, static_cast<char*>(p)).first;
+  }
+  *out = it->second;
+  return hipSuccess;
+}
+
+extern "C" {
+
+int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
+                              const int32_t* targets, const int32_t* input_lengths, const int32_t* target_lengths,
+                              int32_t N, int32_t blank, float beam, int32_t chunk, const float* utt_weight,
+                              double* loss, double* loss_per_utt, int32_t* utt_status, float* dH, float* dW,
+                              float* db, void* workspace, size_t workspace_bytes, void* stream_ptr) {
+  int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (st != PCTC_OK) return st;
+  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
+  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (L.M > 0 && !H) return PCTC_EINVAL;
+  if (L.Y > 0 && !targets) return PCTC_EINVAL;
+  if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
+  if ((reinterpret_cast<uintptr_t>(workspace) & 255) != 0) return PCTC_EINVAL;
+  return fwd_bwd_run(dtype, H, D, W, bias, V, targets, input_lengths, target_lengths, N, blank, beam, L, utt_weight,
+                     loss, loss_per_utt, utt_status, dH, dW, db, static_cast<char*>(workspace),
+                     static_cast<hipStream_t>(stream_ptr), true);
+}
+
+size_t pctc_noalloc_scratch_bytes(void) { return kNoAllocScratchBytes; }
+
+int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias,
+                                   int32_t V, const int32_t* targets, const int32_t* input_lengths,
+                                   const int32_t* target_lengths, int32_t N, int32_t blank, float beam, int32_t chunk,
+                                   const float* utt_weight, double* loss, double* loss_per_utt, int32_t* utt_status,
+                                   float* dH, float* dW, float* db, void* stream_ptr) {
+  int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (st != PCTC_OK) return st;
+  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
+  Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  if (chunk == 0 && L.total > kNoAllocScratchBytes) {
+    // the widest backward chunk (a multiple of 256 columns) whose layout fits the scratch;
+    // the layout is not monotone in the chunk (the dH product's split count changes with
+    // it), so every width is tried from the default down
+    for (int c = L.bwd.chunk / 256 * 256; c >= 256; c -= 256) {
+      const Layout Lc = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, c);
+      if (Lc.total <= kNoAllocScratchBytes) {
+        L = Lc;
+        break;
+      }
+    }
+  }
+  if (L.total > kNoAllocScratchBytes) {
+    snprintf(g_last_error, sizeof(g_last_error),
+             "the batch needs %zu bytes of scratch; the allocation-free entry point holds %zu", L.total,
+             kNoAllocScratchBytes);
+    return PCTC_EWORKSPACE;
+  }
+  if (L.M > 0 && !H) return PCTC_EINVAL;
+  if (L.Y > 0 && !targets) return PCTC_EINVAL;
+  char* ws = nullptr;
+  PCTC_HIP(noalloc_scratch(&ws));
+  return fwd_bwd_run(dtype, H, D, W, bias, V, targets, input_lengths, target_lengths, N, blank, beam, L, utt_weight,
+                     loss, loss_per_utt, utt_status, dH, dW, db, ws, static_cast<hipStream_t>(stream_ptr), false);
 }
 
 int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t blank, int32_t V, int32_t* remap,

@@ -54,6 +54,11 @@ def lib() -> ctypes.CDLL:
     L.pruned_ctc_fwd_bwd_ex.argtypes = [c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f, c_i32,
                                         c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]
     L.pruned_ctc_fwd_bwd_ex.restype = c_i32
+    L.pctc_noalloc_scratch_bytes.argtypes = []
+    L.pctc_noalloc_scratch_bytes.restype = c_sz
+    L.pruned_ctc_fwd_bwd_noalloc.argtypes = [c_i32, c_p, c_i32, c_p, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f,
+                                             c_i32, c_p, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
+    L.pruned_ctc_fwd_bwd_noalloc.restype = c_i32
     L.pctc_status_string.argtypes = [c_i32]
     L.pctc_status_string.restype = ctypes.c_char_p
     L.pctc_last_error.argtypes = []
@@ -234,6 +239,43 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
     _check(code, "pruned_ctc_fwd_bwd")
     return {"loss": loss, "loss_per_utt": loss_n[:N], "status": status[:N], "dH": dH, "dW": dW, "db": db,
             "workspace_bytes": nbytes}
+
+
+def noalloc_scratch_bytes() -> int:
+    """Size of the allocation-free entry point's per-device scratch array."""
+    return int(lib().pctc_noalloc_scratch_bytes())
+
+
+def pruned_ctc_fwd_bwd_noalloc(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor,
+                               input_lengths: Sequence[int], target_lengths: Sequence[int], out: Dict[str, torch.Tensor],
+                               blank: int = 0, beam: float = math.inf, chunk: int = 0,
+                               bias: Optional[torch.Tensor] = None, utt_weight: Optional[torch.Tensor] = None,
+                               stream=None) -> Dict[str, torch.Tensor]:
+    """The fused call through pruned_ctc_fwd_bwd_noalloc: the library uses its own static
+    scratch, and every output is a caller buffer passed in `out` (allocated beforehand):
+    loss (float64 [1]), loss_per_utt (float64 [N]) and status (int32 [N]) or absent, and
+    dH (float32 [M, D]), dW (float32 [V, D]), db (float32 [V]) or absent.  H, W, targets,
+    bias and utt_weight must already be contiguous device tensors of the right dtypes (no
+    conversion or copy is made here).  Returns `out`."""
+    L = lib()
+    dt = _dtype_code(H)
+    T = _host_i32(input_lengths)
+    U = _host_i32(target_lengths)
+    N = int(T.size)
+    for name, t in (("H", H), ("W", W), ("targets", targets), ("bias", bias), ("utt_weight", utt_weight)):
+        if t is not None and not (t.is_cuda and t.is_contiguous()):
+            raise PrunedCTCError(-1, f"{name} must be a contiguous device tensor")
+    if targets.dtype != torch.int32 or W.dtype != H.dtype:
+        raise PrunedCTCError(-1, "targets must be int32 and W of H's dtype")
+    if bias is not None and bias.dtype != torch.float32 or utt_weight is not None and utt_weight.dtype != torch.float32:
+        raise PrunedCTCError(-1, "bias and utt_weight must be float32")
+    code = L.pruned_ctc_fwd_bwd_noalloc(dt, _ptr(H), int(H.shape[1]), _ptr(W), _ptr(bias), int(W.shape[0]),
+                                        _ptr(targets), _i32p(T), _i32p(U), N, int(blank), float(beam), int(chunk),
+                                        _ptr(utt_weight), _ptr(out["loss"]), _ptr(out.get("loss_per_utt")),
+                                        _ptr(out.get("status")), _ptr(out.get("dH")), _ptr(out.get("dW")),
+                                        _ptr(out.get("db")), _stream(stream))
+    _check(code, "pruned_ctc_fwd_bwd_noalloc")
+    return out
 
 
 # ---- stage entry points ------------------------------------------------------------------
