@@ -9,6 +9,8 @@
 // Layouts in LDS follow global memory: W and H rows and dZ rows are K-contiguous for the
 // forward/recompute/dH-left operands; W (for dH) and dZ, H (for dW) are consumed
 // transposed through the LDS transpose read.
+#include <type_traits>
+
 #include "gemm_bf16.h"
 #include "pctc_internal.h"
 
@@ -35,6 +37,11 @@ using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
 // long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
 // beats two 4-wave ones
 using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
+// normaliser and argmax of narrow heads (D < kWideD): 8-wave 256 x 256 tiles, four 32-deep
+// stages, runs of kMidRun vocabulary tiles per workgroup (the copy pipeline runs through a
+// run, so one workgroup per CU still keeps the matrix pipe fed across tile boundaries)
+using GMid = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4, true>;
+constexpr int kMidRun = 8;
 // the union-column part's dH product: 4-wave tiles (two workgroups per CU), so that its
 // workgroups find room beside a recompute's
 using GUh = bf::Gemm<256, 128, 32, LL::KC, LL::MC, 3, 2, 2>;
@@ -92,29 +99,39 @@ __device__ __forceinline__ void bias_init(f32x16 (&acc)[FR][FC], const float* bt
     }
 }
 
+// Logits of rows at or past vend (a partition's ragged last tile, whose rows read as zeros)
+// become -inf in place, so that the update below treats every tile alike.  Each row test is
+// used at once for the FC columns it covers (a lane holds 4 consecutive rows per group):
+// keeping one test per accumulator live across both passes of the update would take a mask
+// register pair per element.
+template <int FR, int FC, class G = GFwd>
+__device__ __forceinline__ void mask_rows_inf(f32x16 (&acc)[FR][FC], int v0, int vend, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < FR; ++i)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int lim = vend - v0 - G::row_of(wave, lane, i, 4 * q);  // rows e < lim are in range
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const bool out = e >= lim;
+#pragma unroll
+        for (int j = 0; j < FC; ++j) acc[i][j][4 * q + e] = out ? -INFINITY : acc[i][j][4 * q + e];
+      }
+    }
+}
+
 // Online log-sum-exp update of the running (max, sum) of this lane's frames with one
-// tile of logits (bias included); rows at or past vend are skipped when MASK.
-template <bool MASK, int FR, int FC, class G = GFwd>
+// tile of logits (bias included; out-of-range rows already -inf).
+template <int FR, int FC, class G = GFwd>
 __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], float (&run_max)[FC],
-                                                float (&run_sum)[FC], int v0, int vend, int wave, int lane) {
+                                                float (&run_sum)[FC]) {
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     float tmax = -INFINITY;
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r0 = G::row_of(wave, lane, i, 4 * q);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float x = acc[i][j][4 * q + e];
-          if (MASK) {
-            if (v0 + r0 + e < vend) tmax = fmaxf(tmax, x);
-          } else {
-            tmax = fmaxf(tmax, x);
-          }
-        }
-      }
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[i][j][r]);
     tmax = fmaxf(tmax, swap_halves(tmax));
     const float nmax = fmaxf(run_max[j], tmax);
     // a column with no finite logit yet (rows masked by a -inf bias) adds nothing
@@ -123,18 +140,7 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
 #pragma unroll
     for (int i = 0; i < FR; ++i)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const int r0 = G::row_of(wave, lane, i, 4 * q);
-#pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float ex = fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ms));
-          if (MASK) {
-            if (v0 + r0 + e < vend) s += ex;
-          } else {
-            s += ex;
-          }
-        }
-      }
+      for (int r = 0; r < 16; ++r) s += fast_exp2(fmaf(acc[i][j][r], kLog2e, -ms));
     s += swap_halves(s);
     const float scale = (run_max[j] == -INFINITY) ? 0.f : fast_exp2((run_max[j] - nmax) * kLog2e);
     run_sum[j] = fmaf(run_sum[j], scale, s);
@@ -161,7 +167,16 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
   PCTC_STAGES_G(G)
   const int nMt = (M + TC - 1) / TC;
   int mt, p;
-  if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) return;
+  if constexpr (std::is_same<G, GMid>::value) {
+    // every frame tile of a vocabulary run on one XCD at about the same time: the run's W
+    // rows are fetched once and shared through that XCD's L2
+    const int w = xcd_swz(blockIdx.x, gridDim.x);
+    mt = w % nMt;
+    p = w / nMt;
+    if (p >= P) return;
+  } else if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) {
+    return;
+  }
   const int m0 = mt * TC;
   const int vbeg = p * vper;
   const int vend = min(V, vbeg + vper);
@@ -181,12 +196,10 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
     run_sum[j] = 0.f;
   }
   f32x16 acc[FR][FC];
-  auto epi = [&](int i, const f32x16 (&a)[FR][FC]) {
+  auto epi = [&](int i, f32x16 (&a)[FR][FC]) {
     const int v0 = vbeg + i * TR;
-    if (v0 + TR <= vend)
-      lse_tile_update<false, FR, FC, G>(a, run_max, run_sum, v0, vend, wave, lane);
-    else
-      lse_tile_update<true, FR, FC, G>(a, run_max, run_sum, v0, vend, wave, lane);
+    if (v0 + TR > vend) mask_rows_inf<FR, FC, G>(a, v0, vend, wave, lane);
+    lse_tile_update<FR, FC, G>(a, run_max, run_sum);
   };
   if (BIAS)
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int i, f32x16 (&a)[FR][FC]) {
@@ -261,20 +274,30 @@ amax_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* 
     bi[j] = 0x7fffffff;
   }
   f32x16 acc[FR][FC];
-  auto epi = [&](int it, const f32x16 (&a)[FR][FC]) {
+  auto epi = [&](int it, f32x16 (&a)[FR][FC]) {
     const int v0 = vbeg + it * TR;
+    if (v0 + TR > vend) mask_rows_inf<FR, FC, G>(a, v0, vend, wave, lane);  // -inf never replaces the best
+    // the lane's rows increase with (i, r): the tile's best is its largest logit at the first
+    // row holding it (found scanning backwards), and it replaces the running best only when
+    // strictly larger, so ties keep the smallest id; NaN never compares equal or larger
+    const int rbase = v0 + G::row_of(wave, lane, 0, 0);
 #pragma unroll
-    for (int j = 0; j < FC; ++j)
+    for (int j = 0; j < FC; ++j) {
+      float tmax = -INFINITY;
 #pragma unroll
       for (int i = 0; i < FR; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int rl = G::row_of(wave, lane, i, r);
-          if (v0 + rl < vend && a[i][j][r] > bv[j]) {
-            bv[j] = a[i][j][r];
-            bi[j] = v0 + rl;
-          }
-        }
+        for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, a[i][j][r]);
+      int off = 0;
+#pragma unroll
+      for (int i = FR - 1; i >= 0; --i)
+#pragma unroll
+        for (int r = 15; r >= 0; --r) off = (a[i][j][r] == tmax) ? 32 * i + 8 * (r >> 2) + (r & 3) : off;
+      if (tmax > bv[j]) {
+        bv[j] = tmax;
+        bi[j] = rbase + off;
+      }
+    }
   };
   if (BIAS)
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi, [&](int it, f32x16 (&a)[FR][FC]) {
@@ -810,18 +833,21 @@ hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t
 // workgroups evenly measured slower for narrow heads: the run length also sets the L2 reuse
 // of the tile order.)
 struct LseSplit {
-  bool wide;  // one 8-wave 256 x 256 workgroup per CU; else two 4-wave 256 x 128
+  bool wide;  // one 8-wave 256 x 256 workgroup per CU (GWide for wide heads, GMid otherwise)
   int vper, P, nM;
 };
 
 static LseSplit lse_split_bf16(int M, int D, int V) {
   LseSplit s;
   s.wide = D >= kWideD;
-  const int TR = s.wide ? GWide::kBR : GFwd::kBR, TC = s.wide ? GWide::kBC : GFwd::kBC;
+  constexpr int TR = 256, TC = 256;
+  static_assert(GWide::kBR == TR && GWide::kBC == TC && GMid::kBR == TR && GMid::kBC == TC, "tile shapes");
   const int vtiles = (V + TR - 1) / TR;
   s.nM = (M + TC - 1) / TC;
-  const int maxp = s.wide ? lse_max_parts(D) : 256;
-  s.vper = ((vtiles + maxp - 1) / maxp) * TR;
+  const int maxp = lse_max_parts(D);
+  int run = (vtiles + maxp - 1) / maxp;
+  if (!s.wide && run < kMidRun) run = kMidRun;
+  s.vper = run * TR;
   s.P = (V + s.vper - 1) / s.vper;
   return s;
 }
@@ -833,7 +859,7 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
   *P_out = Peff;
   Prof pr("lse_partial", stream);
   const size_t bsh = bias ? static_cast<size_t>(vper) * sizeof(float) : 0;
-  const dim3 grid(grouped_grid(sp.nM, Peff));
+  const dim3 grid(sp.wide ? grouped_grid(sp.nM, Peff) : sp.nM * Peff);
   if (sp.wide) {
     if (bias)
       hipLaunchKernelGGL((lse_partial_bf16<GWide, true, 1>), grid, dim3(GWide::kThreads), bsh, stream, H, M, D, W,
@@ -842,10 +868,10 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
       hipLaunchKernelGGL((lse_partial_bf16<GWide, false, 1>), grid, dim3(GWide::kThreads), 0, stream, H, M, D, W,
                          bias, V, Peff, vper, partials);
   } else if (bias) {
-    hipLaunchKernelGGL((lse_partial_bf16<GFwd, true, 2>), grid, dim3(GFwd::kThreads), bsh, stream, H, M, D, W, bias,
+    hipLaunchKernelGGL((lse_partial_bf16<GMid, true, 1>), grid, dim3(GMid::kThreads), bsh, stream, H, M, D, W, bias,
                        V, Peff, vper, partials);
   } else {
-    hipLaunchKernelGGL((lse_partial_bf16<GFwd, false, 2>), grid, dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias,
+    hipLaunchKernelGGL((lse_partial_bf16<GMid, false, 1>), grid, dim3(GMid::kThreads), 0, stream, H, M, D, W, bias,
                        V, Peff, vper, partials);
   }
   return hipGetLastError();
@@ -867,10 +893,10 @@ hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint1
       hipLaunchKernelGGL((amax_partial_bf16<GWide, false, 1>), grid, dim3(GWide::kThreads), 0, stream, H, M, D, W,
                          bias, V, Peff, vper, partials);
   } else if (bias) {
-    hipLaunchKernelGGL((amax_partial_bf16<GFwd, true, 2>), grid, dim3(GFwd::kThreads), bsh, stream, H, M, D, W, bias,
+    hipLaunchKernelGGL((amax_partial_bf16<GMid, true, 1>), grid, dim3(GMid::kThreads), bsh, stream, H, M, D, W, bias,
                        V, Peff, vper, partials);
   } else {
-    hipLaunchKernelGGL((amax_partial_bf16<GFwd, false, 2>), grid, dim3(GFwd::kThreads), 0, stream, H, M, D, W, bias,
+    hipLaunchKernelGGL((amax_partial_bf16<GMid, false, 1>), grid, dim3(GMid::kThreads), 0, stream, H, M, D, W, bias,
                        V, Peff, vper, partials);
   }
   return hipGetLastError();
