@@ -48,23 +48,28 @@ hipEvent_t take_event(ProfState& s) {
 thread_local char g_last_error[512] = "";
 }  // namespace
 
-Prof::Prof(const char* name, hipStream_t st) : slot(-1), stream(st) {
+Prof::Prof(const char* nm, hipStream_t st) : name(nm), stream(st) {
   ProfState& s = prof_state();
   if (!s.enabled) return;
   std::lock_guard<std::mutex> lk(s.mu);
-  if (!s.only.empty() && s.only != name) return;
-  ProfRec r{name, take_event(s), take_event(s)};
-  if (!r.start || !r.stop) return;
-  hipEventRecord(r.start, stream);
-  slot = static_cast<int>(s.pending.size());
-  s.pending.push_back(r);
+  if (!s.only.empty() && s.only != nm) return;
+  start = take_event(s);
+  stop = take_event(s);
+  if (!start || !stop) {
+    if (start) s.pool.push_back(start);
+    if (stop) s.pool.push_back(stop);
+    start = stop = nullptr;
+    return;
+  }
+  hipEventRecord(start, stream);
 }
 
 Prof::~Prof() {
-  if (slot < 0) return;
+  if (!start) return;
   ProfState& s = prof_state();
   std::lock_guard<std::mutex> lk(s.mu);
-  hipEventRecord(s.pending[slot].stop, stream);
+  hipEventRecord(stop, stream);
+  s.pending.push_back(ProfRec{name, start, stop});
 }
 
 void prof_flush() {

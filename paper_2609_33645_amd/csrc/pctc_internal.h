@@ -10,11 +10,14 @@
 namespace pctc {
 
 // Kernel timing: records a start event on construction and a stop event on destruction
-// when timing is enabled (pctc_prof_enable); resolved at pctc_prof_flush().
+// when timing is enabled (pctc_prof_enable); the scope owns its two events until it closes,
+// when the pair joins the shared list that prof_flush() resolves (a flush from another thread
+// meanwhile neither sees nor recycles them).
 struct Prof {
   Prof(const char* name, hipStream_t stream);
   ~Prof();
-  int slot;
+  const char* name;
+  hipEvent_t start = nullptr, stop = nullptr;
   hipStream_t stream;
 };
 void prof_flush();

@@ -836,7 +836,62 @@ def test_e2e_forecast_miss(dtype):
             assert cosine(got, ref[name]) >= 0.99999, name
 
 
+def test_concurrent_calls_with_kernel_timing():
+    """Kernel timing enabled while two host threads call the fused function at once: each timing
+    scope owns its events until it closes, so the flush at the end of one thread's call never
+    touches the other thread's open scopes.  Results equal those of the calls made alone, and
+    every launch is counted exactly once (one normaliser launch per call)."""
+    import threading
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    say("concurrent calls with kernel timing")
+    wls = [workloads.random_small(95 + i, N=5, T_range=(40, 160), D=128, V=3000, dtype="bf16", p_repeat=0.1,
+                                  beam=16.0, w_std=0.5) for i in range(2)]
+
+    def call(wl):
+        H, W, y = to_dev(wl)
+        out = prunedctc.pruned_ctc_fwd_bwd(H, W, y, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+        torch.cuda.current_stream().synchronize()
+        return [out["loss"].cpu(), out["dH"].cpu(), out["dW"].cpu()]
+
+    alone = [call(wl) for wl in wls]
+    calls = 4
+    results = [[None] * calls for _ in wls]
+    errors = []
+
+    def worker(i):
+        try:
+            with torch.cuda.stream(torch.cuda.Stream()):
+                for r in range(calls):
+                    results[i][r] = call(wls[i])
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    prunedctc.prof_reset()
+    prunedctc.prof_enable(True)
+    try:
+        threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+        for t in threads:
+            t.start()
+        for t in threads:
+            t.join(timeout=100)
+    finally:
+        prunedctc.prof_enable(False)
+    assert not any(t.is_alive() for t in threads)
+    assert not errors, errors
+    prof = prunedctc.prof_read()
+    prunedctc.prof_reset()
+    for i in range(2):
+        for r in range(calls):
+            for a, b in zip(results[i][r], alone[i]):
+                assert torch.equal(a, b), (i, r)
+    assert prof["lse_partial"]["launches"] == 2 * calls, prof["lse_partial"]
+    assert prof["recompute_dz"]["launches"] % (2 * calls) == 0
+    assert all(v["total_ms"] > 0 for v in prof.values())
+
+
 # ---------------------------------------------------------------------------------------
+# determinism: every reduction runs in a fixed order, also across the two streams# ---------------------------------------------------------------------------------------
 # determinism: every reduction runs in a fixed order, also across the two streams
 # ---------------------------------------------------------------------------------------
 
