@@ -28,7 +28,10 @@ PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix-core peak
 PEAK_F32_TFLOPS = 157.3     # MI355X fp32 matrix/vector peak
 PEAK_HBM_GBS = 8000.0
 
-GEMM_KERNELS = ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm", "gather_s")
+# every matrix-product kernel of the fused step: the dense products, the selected-logit product
+# and the union-column part's two products (their event times include any wait for free
+# compute units beside the dense part, so the fraction below is a lower bound)
+GEMM_KERNELS = ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm", "gather_s", "union_dh", "union_dw")
 
 
 def parse():
@@ -360,8 +363,12 @@ def main():
     fps = M * a.steps / dt
 
     # algorithmic work per step (bf16/fp32 matrix products)
+    # the union-column products run on G split into bf16 hi and lo halves, over the widest union
+    # the batch allows (1 + sum U_n, rounded up to 8; the union size is known on the device only)
+    ldk = (min(1 + int(U.sum()), V) + 7) // 8 * 8
     gemm_flops = {"lse_partial": 2.0 * M * V * D, "recompute_dz": 2.0 * M * V * D, "dh_gemm": 2.0 * M * V * D,
-                  "dw_gemm": 0.0 if a.frozen_head else 2.0 * M * V * D, "gather_s": 2.0 * M * K * D}
+                  "dw_gemm": 0.0 if a.frozen_head else 2.0 * M * V * D, "gather_s": 2.0 * M * K * D,
+                  "union_dh": 2.0 * M * 2 * ldk * D, "union_dw": 0.0 if a.frozen_head else 2.0 * M * 2 * ldk * D}
     kernel_ms = {k: v["total_ms"] / a.steps for k, v in prof.items()}
     launches = {k: v["launches"] / a.steps for k, v in prof.items()}
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS
@@ -369,7 +376,7 @@ def main():
     dom_flops_per_launch = gemm_flops[dom] / (dom_prof["launches"] / a.steps)
     achieved = dom_flops_per_launch / (dom_avg_ms * 1e-3) / 1e12
     gemm_ms = sum(kernel_ms.get(k, 0.0) for k in GEMM_KERNELS)
-    gemm_total = sum(gemm_flops[k] for k in gemm_flops if k != "gather_s")
+    gemm_total = sum(gemm_flops[k] for k in ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm"))  # 8 M V D
     line = {
         "metric": "frames/sec fused head+Pruned-CTC fwd+bwd at V=180K; % bf16 MFMA peak; peak MB",
         "value": round(fps, 1),
@@ -388,6 +395,7 @@ def main():
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
                      "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom)},
         "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),
+        "gemm_ms_per_step": round(gemm_ms, 4),
         "mfma_frac_step": round(gemm_total / (ms_step * 1e-3) / 1e12 / peak, 4),
         "mfma_frac_useful": round(6.0 * M * V * D / (ms_step * 1e-3) / 1e12 / peak, 4),
         "aux": aux_figures(wl, K, kernel_ms),

@@ -76,6 +76,14 @@ size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_len
                            const int32_t* target_lengths, int32_t D, int32_t V, float beam,
                            int32_t chunk);
 
+/* The same for a call of a stated kind: flags 0 is pctc_workspace_size; PCTC_WS_NO_DW sizes it
+ * for calls with dW == NULL (a frozen head, as in the paper's LLM-CTC runs), which need no room
+ * for the union classes' weight-gradient slices.  Returns 0 for unknown flags. */
+#define PCTC_WS_NO_DW 1
+size_t pctc_workspace_size_ex(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
+                              const int32_t* target_lengths, int32_t D, int32_t V, float beam,
+                              int32_t chunk, int32_t flags);
+
 /* Forward and backward pass of Pruned CTC (Algorithm 1).
  *
  * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8.

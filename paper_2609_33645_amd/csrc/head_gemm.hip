@@ -745,7 +745,8 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
   p.Mp = ((M + 63) / 64) * 64;
   p.dz_bytes = align_up(static_cast<size_t>(M) * cap * es, 256);
   p.ht_bytes = align_up(static_cast<size_t>(D) * p.Mp * es, 256);  // >= M x D (bf16 masked copy of H)
-  p.part_bytes = align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
+  // bf16 with a single slice: the dH product accumulates in the caller's dH (no partial buffer)
+  p.part_bytes = (dtype == 1 && splits == 1) ? 0 : align_up(static_cast<size_t>(splits) * M * D * sizeof(float), 256);
   p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
   // bf16: per 128-frame tile column sums of dZ for db
   p.dbpart_bytes = (dtype == 1) ? align_up(static_cast<size_t>((M + 127) / 128) * cap * sizeof(float), 256) : 0;
@@ -828,7 +829,9 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
                                 const BwdPlan& plan, hipStream_t stream, const BwdSide* side) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
   uint16_t* Hs = bwd_hs(scratch, plan);
-  float* part = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
+  // a single split-K slice accumulates straight into dH: no partials and no reduction
+  const bool in_place = plan.part_bytes == 0;
+  float* part = in_place ? dH : reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
   float* dbpart = reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes + plan.part_bytes + plan.lam2_bytes);
   const int chunk = plan.chunk;
   const bool two = side && side->stream;
@@ -866,7 +869,9 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
       if ((e = start_side(nwork)) != hipSuccess) return e;
       if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
       if ((e = hipStreamWaitEvent(side->stream, side->dh_done, 0)) != hipSuccess) return e;
-      {
+      if (in_place) {
+        if (side->after_dh.fn && (e = side->after_dh.fn(side->after_dh.ctx)) != hipSuccess) return e;
+      } else {
         Prof pr("dh_reduce", side->stream);
         hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, side->stream,
                            part, nslices, n, dH_extra, dH);
@@ -890,7 +895,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
     // before this call's work on the caller's stream is
     if ((e = hipEventRecord(side->reduced, side->stream)) != hipSuccess) return e;
     if ((e = hipStreamWaitEvent(stream, side->reduced, 0)) != hipSuccess) return e;
-  } else if (dH) {
+  } else if (dH && !in_place) {
     Prof pr("dh_reduce", stream);
     hipLaunchKernelGGL(dh_reduce_kernel, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, part,
                        nslices, n, dH_extra, dH);

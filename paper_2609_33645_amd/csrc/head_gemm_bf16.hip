@@ -566,8 +566,9 @@ static int dh_xcd_rows(int M, int D) {
 template <class G, int OCC>
 __global__ void __launch_bounds__(G::kThreads, OCC)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
-             int slice, float* __restrict__ part, int gm) {
-  const bool first = c0 == 0;
+             int slice, float* __restrict__ part, int gm, int accumulate) {
+  // the first chunk writes its slices; later chunks (and an accumulating call) add to them
+  const bool first = c0 == 0 && !accumulate;
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   PCTC_STAGES_G(G)
   const int nMt = (M + TR - 1) / TR;
@@ -742,9 +743,11 @@ namespace {
 constexpr int kColSlices = 16;
 struct UnionCorrLayout {
   int ldK, nz, mslice;  // nz slices of mslice frames for the dW_u product (summed when merged)
-  size_t o_dwu, o_gb, o_wu, o_dbp, total;
+  size_t o_dwu, o_wu, o_dbp, total;
 };
-UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
+// [dW_u slices (only when dW is wanted)][W_U rows twice][db_u slices]; the [hi | lo] copy of G
+// lives outside (gb_bytes, in the region of S, which is dead once the lattice is done)
+UnionCorrLayout union_corr_layout(int M, int D, int K_max, bool want_dW) {
   UnionCorrLayout L;
   L.ldK = (K_max + 7) / 8 * 8;
   const size_t k2 = static_cast<size_t>(2) * L.ldK;
@@ -757,27 +760,29 @@ UnionCorrLayout union_corr_layout(int M, int D, int K_max) {
   L.nz = (M + L.mslice - 1) / L.mslice;  // every slice holds frames
   if (L.nz < 1) L.nz = 1;
   L.o_dwu = 0;
-  L.o_gb = L.o_dwu + align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256);
-  L.o_wu = L.o_gb + align_up(static_cast<size_t>(M) * k2 * sizeof(uint16_t), 256);
+  L.o_wu = L.o_dwu + (want_dW ? align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256) : 0);
   L.o_dbp = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
   L.total = L.o_dbp + align_up(static_cast<size_t>(kColSlices) * K_max * sizeof(float), 256);
   return L;
 }
 }  // namespace
 
-size_t union_corr_bytes(int M, int D, int K_max) { return union_corr_layout(M, D, K_max).total; }
+size_t union_corr_bytes(int M, int D, int K_max, bool want_dW) {
+  return union_corr_layout(M, D, K_max, want_dW).total;
+}
+size_t union_gb_bytes(int M, int K_max) {
+  return static_cast<size_t>(M) * 2 * ((K_max + 7) / 8 * 8) * sizeof(uint16_t);
+}
 
 hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
-                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool want_dW,
-                                  bool want_db, void* scratch, float** dH_u, hipStream_t stream) {
-  const bool want_dH = dH != nullptr;
-  *dH_u = nullptr;
+                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool dh_later,
+                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream) {
+  const bool want_dH = dH != nullptr || dh_later;
   if (M <= 0 || K_max <= 0) return hipSuccess;
   if (want_dW && !Hs) return hipErrorInvalidValue;
-  const UnionCorrLayout L = union_corr_layout(M, D, K_max);
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max, want_dW);
   char* sc = static_cast<char*>(scratch);
   const int k2 = 2 * L.ldK;
-  uint16_t* Gb = reinterpret_cast<uint16_t*>(sc + L.o_gb);
   if (want_dH || want_dW) {
     Prof pr("union_prep", stream);
     const int64_t n = static_cast<int64_t>(M) * L.ldK;
@@ -787,11 +792,12 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
   if (want_dH) {
     uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
     hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, L.ldK, WU2);
-    *dH_u = dH;
-    const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
-    Prof pr("union_dh", stream);
-    hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0,
-                       k2, k2, *dH_u, dh_xcd_rows(M, D));
+    if (!dh_later) {
+      const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
+      Prof pr("union_dh", stream);
+      hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0,
+                         k2, k2, dH, dh_xcd_rows(M, D), 0);
+    }
   }
   if (want_dW) {
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
@@ -808,10 +814,23 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
   return hipGetLastError();
 }
 
+hipError_t launch_union_dh_bf16(const uint16_t* Gb, int K_max, int M, int D, float* dH, void* scratch, bool want_dW,
+                                hipStream_t stream) {
+  if (M <= 0 || K_max <= 0 || !dH) return hipSuccess;
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max, want_dW);
+  const int k2 = 2 * L.ldK;
+  const uint16_t* WU2 = reinterpret_cast<const uint16_t*>(static_cast<char*>(scratch) + L.o_wu);
+  const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
+  Prof pr("union_dh", stream);
+  hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2,
+                     k2, dH, dh_xcd_rows(M, D), 1);
+  return hipGetLastError();
+}
+
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream) {
   if (M <= 0 || K_max <= 0 || (!dW && !db)) return hipSuccess;
-  const UnionCorrLayout L = union_corr_layout(M, D, K_max);
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max, dW != nullptr);
   char* sc = static_cast<char*>(scratch);
   Prof pr("union_merge", stream);
   hipLaunchKernelGGL(union_merge_bf16, dim3((D + 255) / 256, K_max), dim3(256), 0, stream, Kdev, u_ids, D, L.ldK,
@@ -953,7 +972,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
     hipLaunchKernelGGL((dh_gemm_bf16<GDh, 1>), dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D,
-                       c0, cw, slice, part, dh_xcd_rows(M, D));
+                       c0, cw, slice, part, dh_xcd_rows(M, D), 0);
   }
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);

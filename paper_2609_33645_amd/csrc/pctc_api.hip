@@ -129,8 +129,9 @@ static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   return PCTC_OK;
 }
 
+// want_dW: the call asks for dW (the union columns' dW_u slices are only needed then).
 static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
-                          float beam, int32_t chunk) {
+                          float beam, int32_t chunk, bool want_dW = true) {
   Layout L{};
   L.N = N;
   L.dp = plan_dp(N, T, U, beam);
@@ -154,13 +155,16 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.o_lossn = take(static_cast<size_t>(N) * 8);
   L.o_lam = take(static_cast<size_t>(L.M) * 8);
   L.o_lam2 = take(static_cast<size_t>(L.M) * 8);
-  L.o_S = take(static_cast<size_t>(L.M) * L.ldS * 4);
+  // bf16: S is dead once the lattice is done; the union columns' [hi | lo] copy of G then uses its room
+  size_t s_bytes = static_cast<size_t>(L.M) * L.ldS * 4;
+  if (dtype == PCTC_BF16 && union_gb_bytes(L.M, L.K_max) > s_bytes) s_bytes = union_gb_bytes(L.M, L.K_max);
+  L.o_S = take(s_bytes);
   L.o_G = take(static_cast<size_t>(L.M) * L.ldS * 4);
   L.o_g = take(static_cast<size_t>(L.M) * 4);
   if (dtype == PCTC_BF16) {  // the overlapped schedule: forecast g and the union-column part
     L.o_gpred = take(static_cast<size_t>(L.M) * 4);
     L.o_pred = take(static_cast<size_t>(N) * 4);
-    L.o_corr = take(union_corr_bytes(L.M, D, L.K_max));
+    L.o_corr = take(union_corr_bytes(L.M, D, L.K_max, want_dW));
   }
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
@@ -239,6 +243,14 @@ size_t pctc_workspace_size(pctc_dtype dtype, int32_t N, const int32_t* input_len
                            int32_t D, int32_t V, float beam, int32_t chunk) {
   if (check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk) != PCTC_OK) return 0;
   return make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk).total;
+}
+
+size_t pctc_workspace_size_ex(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
+                              const int32_t* target_lengths, int32_t D, int32_t V, float beam, int32_t chunk,
+                              int32_t flags) {
+  if (check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk) != PCTC_OK) return 0;
+  if (flags & ~PCTC_WS_NO_DW) return 0;
+  return make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, !(flags & PCTC_WS_NO_DW)).total;
 }
 
 const char* pctc_status_string(int32_t status) {
@@ -407,6 +419,11 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     dpt.phase = kDpBack;
     // the union columns' part of the backward, from the lattice's G (its frames with g == 0
     // are those of the forecast unless the check fails, and then the backward is redone)
+    // With a single split-K slice the dense part accumulates dH in place; the union columns'
+    // dH_u is then added once the dense part's last dH product is done (after_dh), instead of
+    // being written first and summed in by the final reduction.
+    const bool dh_in_place = dH && L.bwd.part_bytes == 0;
+    uint16_t* Gb = reinterpret_cast<uint16_t*>(ws + L.o_S);  // S is dead once the lattice is done
     struct UnionWork {
       const float* G;
       int ldG;
@@ -414,17 +431,22 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
       int K_max, M, D;
       const uint16_t *W, *Hs;
       float* dH;
-      bool want_dW, want_db;
+      bool dh_later, want_dW, want_db;
       void* scratch;
+      uint16_t* Gb;
       hipStream_t stream;
       static hipError_t run(void* p) {
         const UnionWork& u = *static_cast<const UnionWork*>(p);
-        float* dH_u = nullptr;
-        return launch_union_part_bf16(u.G, u.ldG, u.Kdev, u.K_max, u.u_ids, u.W, u.Hs, u.M, u.D, u.dH, u.want_dW,
-                                      u.want_db, u.scratch, &dH_u, u.stream);
+        return launch_union_part_bf16(u.G, u.ldG, u.Kdev, u.K_max, u.u_ids, u.W, u.Hs, u.M, u.D,
+                                      u.dh_later ? nullptr : u.dH, u.dh_later, u.want_dW, u.want_db, u.scratch, u.Gb,
+                                      u.stream);
+      }
+      static hipError_t run_dh(void* p) {
+        const UnionWork& u = *static_cast<const UnionWork*>(p);
+        return launch_union_dh_bf16(u.Gb, u.K_max, u.M, u.D, u.dH, u.scratch, u.want_dW, u.stream);
       }
     } uw{G, L.ldS, Kdev, u_ids, L.K_max, L.M, D, static_cast<const uint16_t*>(W), bwd_hs(bws, L.bwd), dH,
-         dW != nullptr, db != nullptr, ws + L.o_corr, dps_stream};
+         dh_in_place, dW != nullptr, db != nullptr, ws + L.o_corr, Gb, dps_stream};
     // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds
     // the union part's dH_u (written into dH), runs on the second stream beside the last dW
     BwdSide side;
@@ -436,7 +458,8 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     side.work[0] = SideWork{&DpTail::run, &dpt};
     side.work[1] = SideWork{&UnionWork::run, &uw};
     side.nwork = 2;
-    side.dH_extra = (dH && L.K_max > 0) ? dH : nullptr;
+    if (dh_in_place) side.after_dh = SideWork{&UnionWork::run_dh, &uw};
+    side.dH_extra = (dH && !dh_in_place && L.K_max > 0) ? dH : nullptr;
     side.hs_built = (dH || dW);
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, nullptr, L.ldS, g_pred, nullptr, nullptr, L.ldS, dH, dW,
                              db, bws, L.bwd, stream, &side));
@@ -452,6 +475,8 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   PCTC_HIP(hipMemcpyAsync(hflags, err, 2 * sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
   if (overlap && hflags[1] && !hflags[0]) {
+    // the union columns' copy of G took the room of S: form S again for the plain-order backward
+    PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, G, L.ldS, g, remap, S, L.ldS, dH, dW, db, bws, L.bwd,
                              stream));
     PCTC_HIP(hipStreamSynchronize(stream));
@@ -496,7 +521,7 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
   if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
-  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr);
   if (L.M > 0 && !H) return PCTC_EINVAL;
   if (L.Y > 0 && !targets) return PCTC_EINVAL;
   if (!workspace || workspace_bytes < L.total) return PCTC_EWORKSPACE;
@@ -516,13 +541,13 @@ int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, c
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
   if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
-  Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
+  Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr);
   if (chunk == 0 && L.total > kNoAllocScratchBytes) {
     // the widest backward chunk (a multiple of 256 columns) whose layout fits the scratch;
     // the layout is not monotone in the chunk (the dH product's split count changes with
     // it), so every width is tried from the default down
     for (int c = L.bwd.chunk / 256 * 256; c >= 256; c -= 256) {
-      const Layout Lc = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, c);
+      const Layout Lc = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, c, dW != nullptr);
       if (Lc.total <= kNoAllocScratchBytes) {
         L = Lc;
         break;

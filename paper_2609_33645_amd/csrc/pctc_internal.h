@@ -82,6 +82,8 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
 // The last chunk records dh_done after its dH product; the second stream waits for it and
 // runs the final dH reduction (adding dH_extra, written by its work) beside the chunk's dW
 // product, then records reduced, which the caller's stream waits for before the call returns.
+// When the dense part accumulates dH in place (a single split-K slice: no partial buffer),
+// after_dh runs there instead of the reduction (it adds the union columns' part to dH).
 // hs_built: the masked copy of H (bwd_hs) was already written, from the same g, on a stream
 // the caller's stream has waited for.
 struct SideWork {
@@ -93,6 +95,7 @@ struct BwdSide {
   hipEvent_t gate[2] = {nullptr, nullptr};
   hipEvent_t dh_done = nullptr, reduced = nullptr;
   SideWork work[2];
+  SideWork after_dh;
   int nwork = 0;
   const float* dH_extra = nullptr;
   bool hs_built = false;
@@ -123,15 +126,20 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
                                  float* dbpart, hipStream_t stream);
 // Union-column part of the backward (bf16 path): dH_u = G W_U written into dH [M][D] (which
-// the final reduction then adds the dense part to; *dH_u = dH when written), and into its own
+// the final reduction then adds the dense part to), or later added to dH, and into its own
 // buffers dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left
 // out; then union_merge adds dW_u, db_u into the rows U of dW, db.  scratch:
 // union_corr_bytes().  Hs: H with the rows of frames with g == 0 zeroed (the dense part's
 // copy, bwd_hs), needed for dW_u.
-size_t union_corr_bytes(int M, int D, int K_max);
+// Gb [M][2 ldK] bf16 (union_gb_bytes): the [hi | lo] copy of G, caller-placed.  dh_later: dH_u is
+// not formed here but by launch_union_dh_bf16, which adds it to dH (after the dense part).
+size_t union_corr_bytes(int M, int D, int K_max, bool want_dW);
+size_t union_gb_bytes(int M, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
-                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool want_dW,
-                                  bool want_db, void* scratch, float** dH_u, hipStream_t stream);
+                                  const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool dh_later,
+                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream);
+hipError_t launch_union_dh_bf16(const uint16_t* Gb, int K_max, int M, int D, float* dH, void* scratch, bool want_dW,
+                                hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);

@@ -48,6 +48,8 @@ def lib() -> ctypes.CDLL:
     i32p = ctypes.POINTER(ctypes.c_int32)
     L.pctc_workspace_size.argtypes = [c_i32, c_i32, i32p, i32p, c_i32, c_i32, c_f, c_i32]
     L.pctc_workspace_size.restype = c_sz
+    L.pctc_workspace_size_ex.argtypes = [c_i32, c_i32, i32p, i32p, c_i32, c_i32, c_f, c_i32, c_i32]
+    L.pctc_workspace_size_ex.restype = c_sz
     L.pruned_ctc_fwd_bwd.argtypes = [c_i32, c_p, c_i32, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f, c_i32,
                                      c_p, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]
     L.pruned_ctc_fwd_bwd.restype = c_i32
@@ -155,10 +157,15 @@ def _bias_vector(bias: torch.Tensor, V: int, dev) -> torch.Tensor:
     return bias.reshape(V).to(device=dev, dtype=torch.float32).contiguous()
 
 
-def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, beam: float, chunk: int = 0) -> int:
+WS_NO_DW = 1  # workspace for calls without dW (frozen head)
+
+
+def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, beam: float, chunk: int = 0,
+                   want_dW: bool = True) -> int:
     T = _host_i32(input_lengths)
     U = _host_i32(target_lengths)
-    return int(lib().pctc_workspace_size(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk))
+    return int(lib().pctc_workspace_size_ex(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk,
+                                            0 if want_dW else WS_NO_DW))
 
 
 def bwd_chunk(dtype: int, M: int, D: int, V: int, chunk: int = 0) -> int:
@@ -209,7 +216,8 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
     if int(U.sum()) != int(targets.numel()):
         raise PrunedCTCError(-1, "sum of target lengths differs from the number of targets")
     dev = H.device
-    nbytes = int(L.pctc_workspace_size(dt, N, _i32p(T), _i32p(U), D, V, float(beam), chunk))
+    nbytes = int(L.pctc_workspace_size_ex(dt, N, _i32p(T), _i32p(U), D, V, float(beam), chunk,
+                                          0 if want_dW else WS_NO_DW))
     if nbytes == 0:
         code = -6 if (U > MAX_TARGET).any() else (-3 if ((T < 1).any() or (U < 0).any()) else -1)
         _check(code, "pruned_ctc_fwd_bwd")

@@ -246,7 +246,8 @@ def test_e2e_smallest_shapes(dtype, D, V, blank):
     (0, "bf16", math.inf, 0, 0), (1, "bf16", 8.0, 0, 512), (2, "f32", math.inf, 7, 256),
     (3, "bf16", 0.0, 0, 0), (4, "f32", 3.0, 2999, 0), (5, "bf16", 16.0, 1500, 1024),
     (6, "bf16", 16.0, 0, 1536),  # two chunks: the second stream's two gated works meet at the last dH
-    (7, "f32", 16.0, 0, 1 << 16), (8, "bf16", 16.0, 0, 1 << 16)])  # chunk wider than V: one step
+    (7, "f32", 16.0, 0, 1 << 16), (8, "bf16", 16.0, 0, 1 << 16),  # chunk wider than V: one step
+    (9, "bf16", 16.0, 0, 256), (10, "bf16", math.inf, 3, 256)])  # one split-K slice: dH accumulated in place
 def test_e2e_small(seed, dtype, beam, blank, chunk):
     wl, ref = unambiguous_case(
         lambda s: workloads.random_small(s, N=5, T_range=(1, 140), D=128, V=3000, dtype=dtype, p_repeat=0.15,
@@ -254,6 +255,26 @@ def test_e2e_small(seed, dtype, beam, blank, chunk):
     say(f"e2e small seed={seed} {dtype} beam={beam} blank={blank} M={wl.M} T={wl.input_lengths.tolist()}")
     res = run_gpu(wl, chunk=chunk)
     _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
+
+
+@pytest.mark.parametrize("chunk", [0, 256])
+def test_e2e_frozen_head(chunk):
+    """A frozen head (dW not requested, the LLM-CTC setting): loss and dH as with dW, from a
+    workspace sized for calls without dW; chunk 256 makes the dH product a single split-K slice
+    (dH accumulated in place, the union columns' part added after the dense part)."""
+    from paper_2609_33645_amd import prunedctc
+    wl, ref = unambiguous_case(
+        lambda s: workloads.random_small(s, N=5, T_range=(20, 140), D=256, V=4000, dtype="bf16", p_repeat=0.1,
+                                         beam=16.0, w_std=0.5 * math.sqrt(128 / 256)), 70 + chunk)
+    say(f"e2e frozen head chunk={chunk} M={wl.M}")
+    res = run_gpu(wl, chunk=chunk, want_dW=False)
+    assert res["workspace_bytes"] == prunedctc.workspace_size(1, wl.input_lengths, wl.target_lengths, wl.D, wl.V,
+                                                              wl.beam, chunk, want_dW=False)
+    assert res["workspace_bytes"] < prunedctc.workspace_size(1, wl.input_lengths, wl.target_lengths, wl.D, wl.V,
+                                                             wl.beam, chunk)
+    np.testing.assert_array_equal(res["status"], ref["status"])
+    assert loss_rel(res["loss"], ref["loss"]) <= 1e-5
+    assert cosine(res["dH"], ref["dH"]) >= 0.99999
 
 
 def test_e2e_edge_cases():
@@ -477,7 +498,8 @@ def test_error_codes():
 @pytest.mark.parametrize("seed,dtype,beam,blank,chunk,zero_w,D", [
     (0, "f32", math.inf, 0, 256, False, 128), (1, "bf16", 16.0, 0, 0, True, 128),
     (2, "bf16", math.inf, 2999, 512, False, 128), (3, "f32", 4.0, 11, 0, True, 128),
-    (4, "bf16", 0.0, 0, 1024, False, 128), (5, "bf16", 16.0, 3, 0, False, 2056)])
+    (4, "bf16", 0.0, 0, 1024, False, 128), (5, "bf16", 16.0, 3, 0, False, 2056),
+    (6, "bf16", 16.0, 0, 256, True, 128)])  # dH accumulated in place, union part added after it
 def test_e2e_bias_weights_db(seed, dtype, beam, blank, chunk, zero_w, D):
     import torch
     from paper_2609_33645_amd import prunedctc
