@@ -61,7 +61,7 @@ enum { PCTC_UTT_OK = 0, PCTC_UTT_NOT_ALIGNABLE = 1, PCTC_UTT_NONFINITE = 2 };
 
 /* Limits of this implementation. */
 #define PCTC_MAX_TARGET 1023    /* U_n (2U_n+1 lattice states per frame held in one wavefront) */
-#define PCTC_MAX_VOCAB 524288   /* V (membership bitmap of the union kept in on-chip memory) */
+#define PCTC_MAX_VOCAB 524288   /* V (the largest vocabulary the parity tests cover) */
 
 /* Bytes of workspace pruned_ctc_fwd_bwd needs for this batch.  Depends on N, the frame
  * and target lengths, D, the chunk width and (through the union bitmap, the vocabulary
@@ -184,10 +184,13 @@ const char* pctc_last_error(void);
  * y_rel    device int32 [sum target_lengths]: targets relabelled by their union index.
  * K        device int32 [1]: the union size.
  * err      device int32 [1]: set non-zero if a label is out of range or equals blank.
+ * scratch  device, pctc_union_scratch_bytes(V) bytes (a membership bitmap and a count per
+ *          block of 2048 classes; contents on entry ignored).
  * Synchronous (reads err back); returns PCTC_ELABEL on a bad label. */
+size_t pctc_union_scratch_bytes(int32_t V);
 int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t blank, int32_t V,
                          int32_t* remap, int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err,
-                         void* stream);
+                         void* scratch, void* stream);
 
 /* Normaliser and selected-class log-probabilities (Eq. lognorm; Algorithm 1):
  * lam[m] = log sum_v exp (H W^T)[m, v] in double; S[m, j] = float(Z[m, u_ids[j]] - lam[m])

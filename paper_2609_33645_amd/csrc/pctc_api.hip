@@ -105,7 +105,7 @@ struct Layout {
   bool pruned;
   DpPlan dp;
   BwdPlan bwd;
-  size_t o_remap, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_gpred, o_pred,
+  size_t o_remap, o_ubits, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_gpred, o_pred,
       o_corr, o_dp, o_bwd, o_zd, total;
 };
 
@@ -148,6 +148,7 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
     return at;
   };
   L.o_remap = take(static_cast<size_t>(V) * 4);
+  L.o_ubits = take(union_scratch_bytes(V));
   L.o_uids = take(static_cast<size_t>(1 + L.Y) * 4);
   L.o_yrel = take(static_cast<size_t>(L.Y) * 4);
   L.o_small = take(64);
@@ -356,7 +357,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
     // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
     PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, dps_stream));
-    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, dps_stream));
+    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, ws + L.o_ubits, dps_stream));
     g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
     int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
     PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, nullptr, utt_weight, g_pred, pred, dps_stream));
@@ -373,7 +374,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   } else {
     PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
     // Algorithm 1: union and relabel
-    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, stream));
+    PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, ws + L.o_ubits, stream));
     // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
     PCTC_HIP(launch_lse(dt, H, L.M, D, W, bias, V, partials, lam, lam2, stream));
     PCTC_HIP(launch_gather_s(dt, H, L.M, D, W, bias, u_ids, Kdev, L.K_max, lam, S, L.ldS, stream));
@@ -568,12 +569,14 @@ int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, c
                      loss, loss_per_utt, utt_status, dH, dW, db, ws, static_cast<hipStream_t>(stream_ptr), false);
 }
 
+size_t pctc_union_scratch_bytes(int32_t V) { return (V <= 1 || V > PCTC_MAX_VOCAB) ? 0 : union_scratch_bytes(V); }
+
 int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t blank, int32_t V, int32_t* remap,
-                         int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err, void* stream_ptr) {
+                         int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err, void* scratch, void* stream_ptr) {
   if (V <= 1 || V > PCTC_MAX_VOCAB || blank < 0 || blank >= V || total_targets < 0) return PCTC_EINVAL;
-  if (!remap || !u_ids || !K || !err || (total_targets > 0 && (!targets || !y_rel))) return PCTC_EINVAL;
+  if (!remap || !u_ids || !K || !err || !scratch || (total_targets > 0 && (!targets || !y_rel))) return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
-  PCTC_HIP(launch_union_remap(targets, total_targets, blank, V, remap, u_ids, y_rel, K, err, stream));
+  PCTC_HIP(launch_union_remap(targets, total_targets, blank, V, remap, u_ids, y_rel, K, err, scratch, stream));
   int32_t herr = 0;
   PCTC_HIP(hipMemcpyAsync(&herr, err, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
   PCTC_HIP(hipStreamSynchronize(stream));

@@ -30,9 +30,11 @@ inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
 // ---- union / relabel -------------------------------------------------------------------
 // u_ids[remap[v]] = v for remap[v] >= 0 and K = 1 + max remap (K zeroed here).
 hipError_t launch_remap_invert(const int32_t* remap, int32_t V, int32_t* u_ids, int32_t* K, hipStream_t stream);
+// scratch: union_scratch_bytes(V) (a membership bitmap and a count per block of classes).
+size_t union_scratch_bytes(int32_t V);
 hipError_t launch_union_remap(const int32_t* targets, int32_t total, int32_t blank, int32_t V,
                               int32_t* remap, int32_t* u_ids, int32_t* y_rel, int32_t* K, int32_t* err,
-                              hipStream_t stream);
+                              void* scratch, hipStream_t stream);
 
 // ---- normaliser and selected log-probabilities ------------------------------------------
 int lse_partitions(int M, int V);

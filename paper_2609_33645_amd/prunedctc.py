@@ -65,7 +65,9 @@ def lib() -> ctypes.CDLL:
     L.pctc_status_string.restype = ctypes.c_char_p
     L.pctc_last_error.argtypes = []
     L.pctc_last_error.restype = ctypes.c_char_p
-    L.pctc_union_remap.argtypes = [c_p, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p]
+    L.pctc_union_scratch_bytes.argtypes = [c_i32]
+    L.pctc_union_scratch_bytes.restype = c_sz
+    L.pctc_union_remap.argtypes = [c_p, c_i32, c_i32, c_i32, c_p, c_p, c_p, c_p, c_p, c_p, c_p]
     L.pctc_union_remap.restype = c_i32
     L.pctc_lse_scratch_bytes.argtypes = [c_i32, c_i32]
     L.pctc_lse_scratch_bytes.restype = c_sz
@@ -298,8 +300,9 @@ def union_remap(targets: torch.Tensor, blank: int, V: int, stream=None) -> Dict[
     y_rel = torch.empty(max(Y, 1), dtype=torch.int32, device=dev)
     K = torch.zeros(1, dtype=torch.int32, device=dev)
     err = torch.zeros(1, dtype=torch.int32, device=dev)
+    scratch = _workspace(int(L.pctc_union_scratch_bytes(int(V))), dev)
     code = L.pctc_union_remap(_ptr(targets), Y, int(blank), int(V), _ptr(remap), _ptr(u_ids), _ptr(y_rel), _ptr(K),
-                              _ptr(err), _stream(stream))
+                              _ptr(err), ctypes.c_void_p(scratch.data_ptr()), _stream(stream))
     _check(code, "pctc_union_remap")
     k = int(K.item())
     return {"remap": remap, "u_ids": u_ids[:k], "y_rel": y_rel[:Y], "K": k}

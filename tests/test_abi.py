@@ -48,8 +48,9 @@ def test_host_side_validation_without_gpu():
     p = lambda a: a.ctypes.data_as(i32p)  # noqa: E731
     ws = [lib.pctc_workspace_size(1, 2, p(T), p(U), 512, V, 16.0, 0) for V in (10_000, 100_000, 180_000)]
     assert all(w > 0 for w in ws)
-    # only the V-entry remap table grows with V (4 bytes per class, 256-byte aligned)
-    assert ws[2] - ws[0] <= 4 * (180_000 - 10_000) + 256
+    # only V-entry tables grow with V: the remap (4 bytes per class) and the union's
+    # membership bitmap and block counts (1/8 + 1/512 bytes per class), each 256-byte aligned
+    assert ws[2] - ws[0] <= (4 + 1 / 8 + 1 / 512) * (180_000 - 10_000) + 3 * 256
     assert lib.pctc_workspace_size(1, 2, p(T), p(U), 500, 1000, 16.0, 0) == 0      # D % 8 != 0
     assert lib.pctc_workspace_size(1, 2, p(T), p(U), 512, 1000, float("nan"), 0) == 0
     U2 = np.array([50, 2000], np.int32)
