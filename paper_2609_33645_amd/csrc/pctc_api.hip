@@ -201,16 +201,62 @@ static void host_offsets(int N, const int32_t* T, const int32_t* U, std::vector<
   }
 }
 
+// The three offset tables are consecutive in the lattice plan: one copy of a host image of
+// that region (img, which must outlive the copy: the callers synchronise before returning).
 static hipError_t upload_offsets(const DpPlan& dp, char* dpbase, const std::vector<int32_t>& toff,
                                  const std::vector<int32_t>& yoff, const std::vector<int64_t>& soff,
-                                 hipStream_t stream) {
-  hipError_t e;
-  e = hipMemcpyAsync(dpbase + dp.off_toff, toff.data(), toff.size() * 4, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return e;
-  e = hipMemcpyAsync(dpbase + dp.off_yoff, yoff.data(), yoff.size() * 4, hipMemcpyHostToDevice, stream);
-  if (e != hipSuccess) return e;
-  return hipMemcpyAsync(dpbase + dp.off_soff, soff.data(), soff.size() * 8, hipMemcpyHostToDevice, stream);
+                                 std::vector<char>& img, hipStream_t stream) {
+  img.assign(dp.off_soff + soff.size() * 8 - dp.off_toff, 0);
+  memcpy(img.data(), toff.data(), toff.size() * 4);
+  memcpy(img.data() + (dp.off_yoff - dp.off_toff), yoff.data(), yoff.size() * 4);
+  memcpy(img.data() + (dp.off_soff - dp.off_toff), soff.data(), soff.size() * 8);
+  return hipMemcpyAsync(dpbase + dp.off_toff, img.data(), img.size(), hipMemcpyHostToDevice, stream);
 }
+
+// Events of the two-stream schedule, reused across calls: a set is taken from a per-device
+// pool at the start of a call and returned at its end (after the call has synchronised, so
+// every record on it is complete).  Sets are created when the pool is empty and kept until
+// the process ends.
+constexpr int kCallEvents = 7;
+struct CallEvents {
+  hipEvent_t e[kCallEvents];
+};
+static std::mutex g_ev_mu;
+static std::map<int, std::vector<CallEvents*>> g_ev_pool;
+
+struct EventsLease {
+  int dev = -1;
+  CallEvents* set = nullptr;
+  hipError_t take() {
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    {
+      std::lock_guard<std::mutex> lk(g_ev_mu);
+      auto& pool = g_ev_pool[dev];
+      if (!pool.empty()) {
+        set = pool.back();
+        pool.pop_back();
+        return hipSuccess;
+      }
+    }
+    CallEvents* c = new CallEvents();
+    for (int i = 0; i < kCallEvents; ++i) {
+      e = hipEventCreateWithFlags(&c->e[i], hipEventDisableTiming);
+      if (e != hipSuccess) {
+        for (int j = 0; j < i; ++j) hipEventDestroy(c->e[j]);
+        delete c;
+        return e;
+      }
+    }
+    set = c;
+    return hipSuccess;
+  }
+  ~EventsLease() {
+    if (!set) return;
+    std::lock_guard<std::mutex> lk(g_ev_mu);
+    g_ev_pool[dev].push_back(set);
+  }
+};
 
 // A second stream per device for the lattice stage, which runs beside the dense part of the
 // backward.  Created once (default priority, non-blocking), kept until the process ends.
@@ -326,11 +372,9 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   struct Events {
     hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, gate0 = nullptr, gate1 = nullptr, dh_done = nullptr,
                join = nullptr;
-    ~Events() {
-      for (hipEvent_t e : {start, sel, fork, gate0, gate1, dh_done, join})
-        if (e) hipEventDestroy(e);
-    }
   } ev;
+  EventsLease lease;
+  std::vector<char> offsets_img;
   float* g_pred = nullptr;
   if (overlap) {
     // Two streams.  Second stream: union/relabel, a forecast of g (-w_n on included
@@ -341,13 +385,9 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // normaliser or a -inf logit on a selected class) is caught and the backward is redone in
     // the plain order.
     PCTC_HIP(side_stream(&dps_stream));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.start, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.sel, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.fork, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.gate0, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.gate1, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.dh_done, hipEventDisableTiming));
-    PCTC_HIP(hipEventCreateWithFlags(&ev.join, hipEventDisableTiming));
+    PCTC_HIP(lease.take());
+    ev = Events{lease.set->e[0], lease.set->e[1], lease.set->e[2], lease.set->e[3],
+                lease.set->e[4], lease.set->e[5], lease.set->e[6]};
     PCTC_HIP(hipEventRecord(ev.start, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     double* Zd = reinterpret_cast<double*>(ws + L.o_zd);
@@ -356,7 +396,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
     // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
-    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, dps_stream));
+    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, offsets_img, dps_stream));
     PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, ws + L.o_ubits, dps_stream));
     g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
     int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
@@ -372,7 +412,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     PCTC_HIP(hipEventRecord(ev.fork, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
   } else {
-    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, stream));
+    PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, offsets_img, stream));
     // Algorithm 1: union and relabel
     PCTC_HIP(launch_union_remap(targets, L.Y, blank, V, remap, u_ids, y_rel, Kdev, err, ws + L.o_ubits, stream));
     // online full-vocabulary log-sum-exp, then S = X W_U^T - lambda
@@ -629,7 +669,8 @@ int32_t pctc_ctc_dp(const float* S, int32_t ldS, int32_t K_max, const int32_t* y
   std::vector<int64_t> soff;
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
   char* dps = static_cast<char*>(dp_scratch);
-  PCTC_HIP(upload_offsets(dp, dps, toff, yoff, soff, stream));
+  std::vector<char> img;
+  PCTC_HIP(upload_offsets(dp, dps, toff, yoff, soff, img, stream));
   PCTC_HIP(launch_ctc_dp(dp, input_lengths, target_lengths, S, ldS, y_rel, beam, nullptr, loss_per_utt, utt_status, G, g,
                          keep_mask, dps, K_max, stream, nullptr));
   PCTC_HIP(hipStreamSynchronize(stream));
@@ -709,7 +750,8 @@ int32_t pctc_discarded_mass(const float* S, int32_t ldS, int32_t K_max, const in
   std::vector<int32_t> toff, yoff;
   std::vector<int64_t> soff;
   host_offsets(N, input_lengths, target_lengths, toff, yoff, soff);
-  PCTC_HIP(upload_offsets(dp, static_cast<char*>(dp_scratch), toff, yoff, soff, stream));
+  std::vector<char> img;
+  PCTC_HIP(upload_offsets(dp, static_cast<char*>(dp_scratch), toff, yoff, soff, img, stream));
   PCTC_HIP(launch_discarded_mass(dp, S, ldS, y_rel, beams, nbeams, delta, dp_scratch, K_max, stream));
   PCTC_HIP(hipStreamSynchronize(stream));
   prof_flush();

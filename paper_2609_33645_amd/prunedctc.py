@@ -224,9 +224,12 @@ def pruned_ctc_fwd_bwd(H: torch.Tensor, W: torch.Tensor, targets: torch.Tensor, 
         code = -6 if (U > MAX_TARGET).any() else (-3 if ((T < 1).any() or (U < 0).any()) else -1)
         _check(code, "pruned_ctc_fwd_bwd")
     ws = workspace if workspace is not None else _workspace(nbytes, dev)
-    loss = torch.zeros(1, dtype=torch.float64, device=dev)
-    loss_n = torch.zeros(max(N, 1), dtype=torch.float64, device=dev)
-    status = torch.zeros(max(N, 1), dtype=torch.int32, device=dev)
+    # the library writes all three on success: one uninitialised allocation, split in views
+    n1 = max(N, 1)
+    small = torch.empty(8 + 8 * n1 + 4 * n1, dtype=torch.uint8, device=dev)
+    loss = small[:8].view(torch.float64)
+    loss_n = small[8:8 + 8 * n1].view(torch.float64)
+    status = small[8 + 8 * n1:].view(torch.int32)
     dH = _grad_buffer(dH_out, (M, D), dev) if want_dH else None
     dW = _grad_buffer(dW_out, (V, D), dev) if want_dW else None
     db = torch.empty(V, dtype=torch.float32, device=dev) if want_db else None
