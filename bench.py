@@ -363,12 +363,10 @@ def main():
     fps = M * a.steps / dt
 
     # algorithmic work per step (bf16/fp32 matrix products)
-    # the union-column products run on G split into bf16 hi and lo halves, over the widest union
-    # the batch allows (1 + sum U_n, rounded up to 8; the union size is known on the device only)
-    ldk = (min(1 + int(U.sum()), V) + 7) // 8 * 8
+    # the union-column products run on G split into bf16 hi and lo halves (2 K columns)
     gemm_flops = {"lse_partial": 2.0 * M * V * D, "recompute_dz": 2.0 * M * V * D, "dh_gemm": 2.0 * M * V * D,
                   "dw_gemm": 0.0 if a.frozen_head else 2.0 * M * V * D, "gather_s": 2.0 * M * K * D,
-                  "union_dh": 2.0 * M * 2 * ldk * D, "union_dw": 0.0 if a.frozen_head else 2.0 * M * 2 * ldk * D}
+                  "union_dh": 2.0 * M * 2 * K * D, "union_dw": 0.0 if a.frozen_head else 2.0 * M * 2 * K * D}
     kernel_ms = {k: v["total_ms"] / a.steps for k, v in prof.items()}
     launches = {k: v["launches"] / a.steps for k, v in prof.items()}
     peak = PEAK_BF16_TFLOPS if wl.dtype == "bf16" else PEAK_F32_TFLOPS

@@ -566,9 +566,10 @@ static int dh_xcd_rows(int M, int D) {
 template <class G, int OCC>
 __global__ void __launch_bounds__(G::kThreads, OCC)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
-             int slice, float* __restrict__ part, int gm, int accumulate) {
+             int slice, float* __restrict__ part, int gm, int accumulate, const int32_t* __restrict__ kdev) {
   // the first chunk writes its slices; later chunks (and an accumulating call) add to them
   const bool first = c0 == 0 && !accumulate;
+  if (kdev) cw = min(cw, 2 * *kdev);  // union columns: [hi | lo] of the K classes the device found
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   PCTC_STAGES_G(G)
   const int nMt = (M + TR - 1) / TR;
@@ -621,7 +622,7 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
 // into nz slices of mslice frames and slice z writes its partial sums at dW + z * zstride.
 __global__ void __launch_bounds__(512, 1)
 dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ Hs, int D, int c0, int cw,
-             float* __restrict__ dW, int nz, int mslice, int64_t zstride) {
+             float* __restrict__ dW, int nz, int mslice, int64_t zstride, const int32_t* __restrict__ kdev) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES_G(G)
@@ -634,7 +635,8 @@ dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
   const int v0 = vt * kBR, d0 = dt * kBC;
   const int mb = z * mslice;
   const int mlen = min(M - mb, mslice);
-  if (z >= nz || mlen <= 0) return;
+  if (kdev) cw = min(cw, 2 * *kdev);  // union rows: [hi | lo] of the K classes the device found
+  if (z >= nz || mlen <= 0 || v0 >= cw) return;
   dW += static_cast<int64_t>(z) * zstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   // A: dZ viewed as rows v (columns of dZ), k = frame; B: Hs viewed as rows d, k = frame
@@ -675,31 +677,43 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
 // G to about 16 bits: dH_u is one product against [W_U; W_U], dW_u two row blocks that are
 // summed when merged into dW.
 // ---------------------------------------------------------------------------------------
+// Gb [M][2 ldK]: columns j and K + j hold the hi and lo halves of G[m][j] for j < K (K the
+// union size found on the device, <= ldK) and the columns from 2K on hold zeros (a product's
+// copy of a k-run may reach past 2K; those values meet zero rows of W_U, and must be finite).
 __global__ void __launch_bounds__(256)
-union_split_bf16(const float* __restrict__ G, int ldG, int K_max, int ldK, int M, uint16_t* __restrict__ Gb) {
+union_split_bf16(const float* __restrict__ G, int ldG, const int32_t* __restrict__ Kdev, int ldK, int M,
+                 uint16_t* __restrict__ Gb) {
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
   if (i >= static_cast<int64_t>(M) * ldK) return;
+  const int K = *Kdev;
   const int m = static_cast<int>(i / ldK), j = static_cast<int>(i % ldK);
-  const float x = (j < K_max) ? G[static_cast<int64_t>(m) * ldG + j] : 0.f;
-  const uint16_t hi = f32_to_bf16(x);
-  const uint16_t lo = f32_to_bf16(x - bf16_to_f32(hi));
+  const float* grow = G + static_cast<int64_t>(m) * ldG;
   uint16_t* row = Gb + static_cast<int64_t>(m) * (2 * ldK);
-  row[j] = hi;
-  row[ldK + j] = lo;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {  // columns j and ldK + j
+    const int c = j + h * ldK;
+    uint16_t out = 0;
+    if (c < K) {
+      out = f32_to_bf16(grow[c]);
+    } else if (c < 2 * K) {
+      const float x = grow[c - K];
+      out = f32_to_bf16(x - bf16_to_f32(f32_to_bf16(x)));
+    }
+    row[c] = out;
+  }
 }
 
-// WU2 [2 ldK][D]: rows j and ldK + j hold W[U_j] for j < K, zeros otherwise.
+// WU2 [2 ldK][D]: rows j and K + j hold W[U_j] for j < K; the rows past 2K are never read.
 __global__ void __launch_bounds__(256)
 union_rows_bf16(const uint16_t* __restrict__ W, int D, const int32_t* __restrict__ u_ids,
-                const int32_t* __restrict__ Kdev, int ldK, uint16_t* __restrict__ WU2) {
+                const int32_t* __restrict__ Kdev, uint16_t* __restrict__ WU2) {
   const int r = blockIdx.x;
-  const int j = r % ldK;
-  const bool live = j < *Kdev;
-  const uint16_t* src = live ? W + static_cast<int64_t>(u_ids[j]) * D : nullptr;
-  for (int d = threadIdx.x * 8; d < D; d += 256 * 8) {
-    const u32x4 v = live ? *reinterpret_cast<const u32x4*>(src + d) : u32x4{0u, 0u, 0u, 0u};
-    *reinterpret_cast<u32x4*>(WU2 + static_cast<int64_t>(r) * D + d) = v;
-  }
+  const int K = *Kdev;
+  if (r >= 2 * K) return;
+  const int j = r < K ? r : r - K;
+  const uint16_t* src = W + static_cast<int64_t>(u_ids[j]) * D;
+  for (int d = threadIdx.x * 8; d < D; d += 256 * 8)
+    *reinterpret_cast<u32x4*>(WU2 + static_cast<int64_t>(r) * D + d) = *reinterpret_cast<const u32x4*>(src + d);
 }
 
 // dbp[z][j] = sum of G[m][j] over the frames of slice z (fp32, in frame order)
@@ -714,7 +728,7 @@ union_colsum_bf16(const float* __restrict__ G, int ldG, int M, int K_max, int mp
   dbp[static_cast<int64_t>(z) * K_max + j] = acc;
 }
 
-// dW[U_j, :] += sum over the frame slices of dW_u2[j, :] + dW_u2[ldK + j, :];
+// dW[U_j, :] += sum over the frame slices of dW_u2[j, :] + dW_u2[K + j, :];
 // db[U_j] += sum_z dbp[z][j]
 __global__ void __launch_bounds__(256)
 union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u_ids, int D, int ldK, int K_max,
@@ -725,10 +739,11 @@ union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u
   const int v = u_ids[j];
   const int d = blockIdx.x * 256 + threadIdx.x;
   if (dW && d < D) {
+    const int K = *Kdev;
     float s = 0.f;
     for (int z = 0; z < nzw; ++z) {
       const float* p = dWu2 + static_cast<int64_t>(z) * 2 * ldK * D;
-      s += p[static_cast<int64_t>(j) * D + d] + p[static_cast<int64_t>(ldK + j) * D + d];
+      s += p[static_cast<int64_t>(j) * D + d] + p[static_cast<int64_t>(K + j) * D + d];
     }
     dW[static_cast<int64_t>(v) * D + d] += s;
   }
@@ -787,23 +802,23 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
     Prof pr("union_prep", stream);
     const int64_t n = static_cast<int64_t>(M) * L.ldK;
     hipLaunchKernelGGL(union_split_bf16, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, G, ldG,
-                       K_max, L.ldK, M, Gb);
+                       Kdev, L.ldK, M, Gb);
   }
   if (want_dH) {
     uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
-    hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, L.ldK, WU2);
+    hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, WU2);
     if (!dh_later) {
       const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
       Prof pr("union_dh", stream);
       hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0,
-                         k2, k2, dH, dh_xcd_rows(M, D), 0);
+                         k2, k2, dH, dh_xcd_rows(M, D), 0, Kdev);
     }
   }
   if (want_dW) {
     const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("union_dw", stream);
     hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs, D, 0, k2,
-                       reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice, static_cast<int64_t>(k2) * D);
+                       reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice, static_cast<int64_t>(k2) * D, Kdev);
   }
   if (want_db) {
     const int mper = (M + kColSlices - 1) / kColSlices;
@@ -814,8 +829,8 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
   return hipGetLastError();
 }
 
-hipError_t launch_union_dh_bf16(const uint16_t* Gb, int K_max, int M, int D, float* dH, void* scratch, bool want_dW,
-                                hipStream_t stream) {
+hipError_t launch_union_dh_bf16(const uint16_t* Gb, const int32_t* Kdev, int K_max, int M, int D, float* dH,
+                                void* scratch, bool want_dW, hipStream_t stream) {
   if (M <= 0 || K_max <= 0 || !dH) return hipSuccess;
   const UnionCorrLayout L = union_corr_layout(M, D, K_max, want_dW);
   const int k2 = 2 * L.ldK;
@@ -823,7 +838,7 @@ hipError_t launch_union_dh_bf16(const uint16_t* Gb, int K_max, int M, int D, flo
   const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
   Prof pr("union_dh", stream);
   hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2,
-                     k2, dH, dh_xcd_rows(M, D), 1);
+                     k2, dH, dh_xcd_rows(M, D), 1, Kdev);
   return hipGetLastError();
 }
 
@@ -972,13 +987,13 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
     hipLaunchKernelGGL((dh_gemm_bf16<GDh, 1>), dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D,
-                       c0, cw, slice, part, dh_xcd_rows(M, D), 0);
+                       c0, cw, slice, part, dh_xcd_rows(M, D), 0, nullptr);
   }
   if (want_dW) {
     const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
     Prof pr("dw_gemm", stream);
     hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW, 1, M,
-                       static_cast<int64_t>(0));
+                       static_cast<int64_t>(0), nullptr);
   }
   return hipGetLastError();
 }

@@ -484,7 +484,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
       }
       static hipError_t run_dh(void* p) {
         const UnionWork& u = *static_cast<const UnionWork*>(p);
-        return launch_union_dh_bf16(u.Gb, u.K_max, u.M, u.D, u.dH, u.scratch, u.want_dW, u.stream);
+        return launch_union_dh_bf16(u.Gb, u.Kdev, u.K_max, u.M, u.D, u.dH, u.scratch, u.want_dW, u.stream);
       }
     } uw{G, L.ldS, Kdev, u_ids, L.K_max, L.M, D, static_cast<const uint16_t*>(W), bwd_hs(bws, L.bwd), dH,
          dh_in_place, dW != nullptr, db != nullptr, ws + L.o_corr, Gb, dps_stream};

@@ -140,8 +140,8 @@ size_t union_gb_bytes(int M, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
                                   const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool dh_later,
                                   bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream);
-hipError_t launch_union_dh_bf16(const uint16_t* Gb, int K_max, int M, int D, float* dH, void* scratch, bool want_dW,
-                                hipStream_t stream);
+hipError_t launch_union_dh_bf16(const uint16_t* Gb, const int32_t* Kdev, int K_max, int M, int D, float* dH,
+                                void* scratch, bool want_dW, hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
