@@ -44,6 +44,8 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-paper-protocol", action="store_true",
+                    help="skip the paper's 3 x (5 + 50)-call timing protocol (profiling runs)")
     ap.add_argument("--cpu-utts", type=int, default=16, help="utterances in the CPU-baseline sample")
     ap.add_argument("--frozen-head", action="store_true", help="skip dW (frozen LLM head)")
     ap.add_argument("--path", default="fused", choices=("fused", "greedy", "grouped", "discarded"),
@@ -58,7 +60,8 @@ def parse():
 
 KERNEL_SOURCES = ("paper_2609_33645_amd/csrc/head_gemm_bf16.hip", "paper_2609_33645_amd/csrc/gemm_bf16.h",
                   "paper_2609_33645_amd/csrc/pctc_device.h", "paper_2609_33645_amd/csrc/head_gemm.hip",
-                  "paper_2609_33645_amd/csrc/ctc_dp.hip", "paper_2609_33645_amd/csrc/grouped_head.hip")
+                  "paper_2609_33645_amd/csrc/ctc_dp.hip", "paper_2609_33645_amd/csrc/grouped_head.hip",
+                  "paper_2609_33645_amd/csrc/union_remap.hip", "paper_2609_33645_amd/csrc/pctc_api.hip")
 
 
 def kernel_source_hash() -> str:
@@ -70,9 +73,9 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(kernel: str):
-    """HBM bytes per launch of `kernel` from the committed counter summary, or None when the
-    summary is missing or was taken on different kernel sources."""
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` on `workload` from the committed counter summary, or None
+    when the summary is missing or was taken on different kernel sources."""
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
@@ -81,7 +84,7 @@ def measured_traffic(kernel: str):
         return None
     if t.get("source_hash") != kernel_source_hash():
         return None
-    k = t.get("kernels", {}).get(kernel)
+    k = t.get("workloads", {}).get(workload, {}).get("kernels", {}).get(kernel)
     return None if k is None else k.get("traffic_bytes_per_launch")
 
 
@@ -391,7 +394,8 @@ def main():
         "config": {"workload": wl.name, "N": wl.N, "M": M, "D": D, "V": V, "K": K, "beam": wl.beam,
                    "chunk": prunedctc.bwd_chunk(1 if wl.dtype == "bf16" else 0, M, D, V, a.chunk), "seed": a.seed, "dW": not a.frozen_head},
         "roofline": {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2), "peak": peak,
-                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4), "traffic": measured_traffic(dom)},
+                     "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                     "traffic": measured_traffic(dom, wl.name)},
         "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),
         "gemm_ms_per_step": round(gemm_ms, 4),
         "mfma_frac_step": round(gemm_total / (ms_step * 1e-3) / 1e12 / peak, 4),
@@ -402,23 +406,24 @@ def main():
         "workspace_mb": round(ws_mb, 1),
         "kernel_ms_per_step": {k: round(v, 4) for k, v in sorted(kernel_ms.items(), key=lambda kv: -kv[1])},
     }
-    # the paper's protocol (App. C.1): 3 runs of 5 warm-up and 50 measured calls, each call timed
-    # with the device synchronised at both ends; the median of the run medians
-    meds = []
-    for _ in range(3):
-        for _ in range(5):
-            step()
-        torch.cuda.synchronize()
-        ts = []
-        for _ in range(50):
-            t1 = time.perf_counter()
-            step()
+    if not a.no_paper_protocol:
+        # the paper's protocol (App. C.1): 3 runs of 5 warm-up and 50 measured calls, each call timed
+        # with the device synchronised at both ends; the median of the run medians
+        meds = []
+        for _ in range(3):
+            for _ in range(5):
+                step()
             torch.cuda.synchronize()
-            ts.append(time.perf_counter() - t1)
-        meds.append(float(np.median(ts)))
-    pm = float(np.median(meds))
-    line["paper_protocol"] = {"runs": 3, "warmup": 5, "steps": 50, "median_ms_per_call": round(pm * 1e3, 4),
-                              "frames_per_s": round(M / pm, 1)}
+            ts = []
+            for _ in range(50):
+                t1 = time.perf_counter()
+                step()
+                torch.cuda.synchronize()
+                ts.append(time.perf_counter() - t1)
+            meds.append(float(np.median(ts)))
+        pm = float(np.median(meds))
+        line["paper_protocol"] = {"runs": 3, "warmup": 5, "steps": 50, "median_ms_per_call": round(pm * 1e3, 4),
+                                  "frames_per_s": round(M / pm, 1)}
     if not a.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, a.cpu_utts)
     print(json.dumps(line), flush=True)
