@@ -381,9 +381,11 @@ gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __re
 // columns of a tile are then rewritten in the staging buffer as G[m][j] - g_m exp(S[m][j])
 // from the forward's selected log-probabilities.  Columns past cw within the last tile
 // hold finite values that no consumer reads (their W rows read as zero).  Each tile (256
-// vocabulary rows x 128 or 256 frames) is staged through LDS, 32 frames of each 64-frame
-// column group per pass, so that every frame row is stored as contiguous 16-byte vectors.  DB: the staged (rounded) values are also summed over the tile's frames, giving
-// this tile's share of db = dZ^T 1 in dbpart[frame tile][column].
+// vocabulary rows x 128 or 256 frames) is staged through the drained LDS stages, 32 frames
+// of each 64-frame column group per pass, so that every frame row is stored as contiguous
+// 16-byte vectors.  DB: the staged (rounded) values are also summed
+// over the tile's frames, giving this tile's share of db = dZ^T 1 in
+// dbpart[frame tile][column].
 template <class GG, bool BIAS, bool DB, int OCC>
 __global__ void __launch_bounds__(GG::kThreads, OCC)
 recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W,
@@ -395,8 +397,10 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   static_assert(TR == 256 && NT % TR == 0, "each thread owns one tile column");
   constexpr int WC = GG::NW / 2;        // column groups of 64 frames (the wave grid is 2 x WC)
   constexpr int kPitch = TR * 2 + 16;  // staging row: 256 bf16 + 16 bytes
-  // in each pass, column group q stages its 32 frames in stage q & 1, row block q >> 1
-  static_assert(((WC + 1) / 2) * 32 * kPitch <= GG::kStageBytes, "staging fits two stages");
+  // in each pass, column group q stages its 32 frames in stage q / kGps, row block q % kGps
+  // (the k loop has drained, so every stage is free)
+  constexpr int kGps = GG::kStageBytes / (32 * kPitch);
+  static_assert(kGps >= 1 && (WC + kGps - 1) / kGps <= GG::kNS, "staging fits the stages");
   PCTC_STAGES_G(GG)
   const int nMt = (M + TC - 1) / TC;
   const int nVt = (cw + TR - 1) / TR;
@@ -419,15 +423,18 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
     if (jsel >= 0) ulist[atomicAdd(&nu, 1)] = (jsel << 8) | tid;
     __syncthreads();
   }
-  // this lane's frames: -g_m and lambda_m log2(e) (both zero on excluded frames)
-  float ng[FC], ll[FC];
+  // this lane's frames: -g_m p = -sign(g_m) 2^(z log2(e) - (lambda_m log2(e) - log2|g_m|)), so
+  // the exponent offset ll takes g_m's magnitude (+inf on excluded frames, whose products
+  // are finite: the values are zeros) and sg its sign, applied to a packed bf16 pair
+  float ll[FC];
+  uint32_t sg[FC];
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
     const int m = m0 + GG::col_of(wave, lane, j);
     const float gm = (m < M) ? g[m] : 0.f;
     const float2 l2 = (m < M) ? lam2[m] : make_float2(0.f, 0.f);
-    ng[j] = -gm;
-    ll[j] = (gm != 0.f) ? l2.x + l2.y : 0.f;
+    ll[j] = (gm != 0.f) ? (l2.x + l2.y) - fast_log2(fabsf(gm)) : INFINITY;
+    sg[j] = (gm > 0.f) ? 0x80008000u : 0u;
   }
   const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
   const GOp B{Hs, D, M, D, nullptr};
@@ -438,7 +445,11 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
   } else {
     GG::run(A, B, vl0, m0, 0, D, st, acc);
   }
-  auto stage_of = [&](int q) -> char* { return ((q & 1) ? st1_ : st0_) + (q >> 1) * (32 * kPitch); };
+  auto stage_of = [&](int q) -> char* {
+    const int sq = q / kGps;
+    char* const b = (sq == 0) ? st0_ : (sq == 1) ? st1_ : (sq == 2) ? st2_ : st3_;
+    return b + (q % kGps) * (32 * kPitch);
+  };
   const int nunion = any_sel ? nu : 0;
   char* stage = stage_of(wave % WC);  // this wave's frames [64 q, 64 q + 64) of the tile, 32 per pass
   // DB: column tid % 256 of the tile over column groups [qb, qb + kQPer), summed over the passes
@@ -455,9 +466,9 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
         const int rl0 = GG::row_of(wave, lane, i, 4 * q);
         float v[4];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) v[e] = ng[j] * fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ll[j]));
+        for (int e = 0; e < 4; ++e) v[e] = fast_exp2(fmaf(acc[i][j][4 * q + e], kLog2e, -ll[j]));
         *reinterpret_cast<u32x2*>(stage + (lane & 31) * kPitch + rl0 * 2) =
-            u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+            u32x2{pack_bf16x2(v[0], v[1]) ^ sg[j], pack_bf16x2(v[2], v[3]) ^ sg[j]};
       }
     __syncthreads();
     if (nunion > 0) {
@@ -952,7 +963,9 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
                                  float* dbpart, hipStream_t stream) {
-  // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue)
+  // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue);
+  // narrow heads: two 4-wave 256 x 128 workgroups per CU, so that one's epilogue (exp, pack,
+  // staged stores: VALU-bound) overlaps the other's products
   const bool wide = D >= kWideD;
   const int nMt = (M + (wide ? GWide::kBC : GFwd::kBC) - 1) / (wide ? GWide::kBC : GFwd::kBC);
   if (recompute) {
