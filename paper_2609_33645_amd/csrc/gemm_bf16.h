@@ -3,7 +3,7 @@
 // C[i][j] = sum_k A[i][k] B[j][k] over one BR x BC tile (4 wavefronts, 2 x 2; each owns
 // (BR/2) x (BC/2) = FR x FC blocks of 32x32 accumulated by v_mfma_f32_32x32x16_bf16).
 //
-// Operands are copied from global memory to LDS by global_load_lds_dwordx4 (16 bytes per
+// Operands are copied from global memory to LDS by buffer_load_dwordx4 ... lds (16 bytes per
 // lane, no register staging) in one of two LDS layouts, chosen to match global memory:
 //   KC: [row][k]  (k contiguous)   -- fragments read with ds_read_b128;
 //   MC: [k][row]  (rows contiguous) -- fragments read with two ds_read_b64_tr_b16, which
@@ -17,8 +17,13 @@
 // Fragments are double-buffered in registers across k-steps, and every k-step issues its
 // matrix products interleaved one by one with the next step's LDS reads (and copies), so
 // the matrix pipe is fed while the reads are in flight.
-// Out-of-range rows or k read from a 16-byte zero page, so ragged tiles need no masking;
-// the k loop runs a multiple of NS tiles (the extra tiles are zeros).
+// Out-of-range rows and k read zeros, so ragged tiles need no masking: each k-tile's copies
+// go through a buffer resource whose base and size (scalar registers) cover exactly the
+// tile's valid part, and the hardware returns zero for every lane whose offset falls past
+// the size (lanes of invalid columns or k carry bit 31 in their fixed offset).  A copy then
+// costs no vector arithmetic.  Row-gathered operands (GOp::rowidx) keep per-lane addresses
+// with a 16-byte zero page.  The k loop runs a multiple of NS tiles (the extra tiles are
+// zeros).
 #pragma once
 
 #include "pctc_device.h"
@@ -32,11 +37,15 @@ __device__ __attribute__((aligned(16))) static const uint32_t kZeroPage[4] = {0u
 
 struct GOp {
   const uint16_t* base;
-  int64_t pitch;        // elements between consecutive rows (KC) or k-lines (MC)
+  int64_t pitch;        // elements between consecutive rows (KC) or k-lines (MC); MC: rows <= pitch
   int rows;             // valid rows
-  int kmax;             // valid k
-  const int* rowidx;    // KC only: optional row gather table
+  int kmax;             // valid k (KC: kmax <= pitch)
+  const int* rowidx;    // KC only: optional row gather table (needs a Gemm with BUF false)
 };
+
+// Word 3 of a raw buffer resource on gfx9-family parts: 32-bit data format, no swizzle.
+constexpr int kBufWord3 = 0x00020000;
+constexpr uint32_t kOob = 0x80000000u;  // an offset past any size used here
 
 typedef __attribute__((address_space(3))) void lds_void;
 typedef __attribute__((ext_vector_type(4))) short s16x4;
@@ -76,8 +85,9 @@ struct MC {
 
 // Copies one operand tile (NR rows x BK k) into LDS as kCopies 1 KB copies; wave w of
 // NW issues copies w, w+NW, ...  Per-copy source offsets are fixed for the whole k loop
-// and are computed once (init); issue() adds the k-tile offset.
-template <LL L, int NR, int BK, int NW>
+// and are computed once (init); issue() adds the k-tile offset.  BUF: through buffer
+// resources (below); otherwise flat addresses with the zero page (row gathers).
+template <LL L, int NR, int BK, int NW, bool BUF>
 struct TileCopy {
   static constexpr int kBytes = NR * BK * 2;
   static constexpr int kCopies = kBytes / 1024;
@@ -147,6 +157,106 @@ struct TileCopy {
   }
 };
 
+// Buffer-resource copies.  Byte offsets of a lane's 16 bytes, relative to the k-tile base
+// (KC: row row0, element k0; MC: k-line k0, element row0):
+//   KC: r pitch 2 + 16 slot   valid while r < rows - row0 (the size stops there) and
+//                              k0 + 8 slot < klim (only the one partial k-tile can break
+//                              this: there, lanes past the limit add bit 31; a lane's slot
+//                              is the same in all its copies, so one flag covers them);
+//   MC: kr pitch 2 + 16 slot  valid while k0 + kr < klim (the size stops at that k-line)
+//                              and row0 + 8 slot < rows (otherwise bit 31 is set).
+// With 16-byte reads that either lie wholly below the size or start at or past it.
+template <LL L, int NR, int BK, int NW>
+struct TileCopy<L, NR, BK, NW, true> {
+  static constexpr int kBytes = NR * BK * 2;
+  static constexpr int kCopies = kBytes / 1024;
+  static constexpr int kPerWave = kCopies / NW;
+  static_assert(kBytes % 1024 == 0 && kCopies % NW == 0, "tile must be whole 1 KB copies per wave");
+  const uint16_t* tbase;  // KC: op.base + row0 pitch; MC: op.base + row0
+  int rows_left;          // KC: valid rows of the tile (0 .. NR); MC: row0
+  int kpart;              // KC: k0 of the partial k-tile (none: -1)
+  uint32_t poob;          // KC: bit 31 if this lane's slot is past the partial k-tile's limit
+  uint32_t off[kPerWave];
+
+  __device__ __forceinline__ void init(const GOp& op, int row0, int w, int lane, int kbeg, int klim) {
+    const int rem = (klim > kbeg) ? (klim - kbeg) % BK : 0;
+    kpart = rem ? klim - rem : -1;
+#pragma unroll
+    for (int i = 0; i < kPerWave; ++i) {
+      const int c = w + NW * i;
+      if constexpr (L == LL::KC) {
+        using G = KC<BK>;
+        const int r = c * G::kRowsPerCopy + lane / G::kSlots;
+        const int lc = (lane % G::kSlots) ^ G::swz(r);
+        off[i] = static_cast<uint32_t>(r * op.pitch * 2 + lc * 16);
+        poob = (lc * 8 < rem) ? 0u : kOob;  // the same for every i
+      } else {
+        using G = MC<NR>;
+        const int kr = c * G::kRowsPerCopy + lane / G::kSlots;
+        const int lc = (lane % G::kSlots) ^ G::swz(kr);
+        off[i] = static_cast<uint32_t>(kr * op.pitch * 2 + lc * 16) | ((row0 + lc * 8 < op.rows) ? 0u : kOob);
+      }
+    }
+    if constexpr (L == LL::MC) rows_left = row0;  // the offsets above are this tile's
+    retarget(op, row0, w, lane);
+  }
+
+  // The tile whose first row is row0 (same k range).
+  __device__ __forceinline__ void retarget(const GOp& op, int row0, int w, int lane) {
+    if constexpr (L == LL::KC) {
+      tbase = op.base + static_cast<int64_t>(row0) * op.pitch;
+      rows_left = min(max(op.rows - row0, 0), NR);
+    } else {
+      tbase = op.base + row0;
+      if (row0 != rows_left) {  // column validity moves with the tile
+#pragma unroll
+        for (int i = 0; i < kPerWave; ++i) {
+          const int c = w + NW * i;
+          using G = MC<NR>;
+          const int kr = c * G::kRowsPerCopy + lane / G::kSlots;
+          const int lc = (lane % G::kSlots) ^ G::swz(kr);
+          off[i] = static_cast<uint32_t>(kr * op.pitch * 2 + lc * 16) | ((row0 + lc * 8 < op.rows) ? 0u : kOob);
+        }
+      }
+      rows_left = row0;
+    }
+  }
+
+  __device__ __forceinline__ void issue(const GOp& op, int k0, int klim, char* lds, int w) const {
+#if defined(__HIP_DEVICE_COMPILE__)  // the buffer-resource type exists on the device side only
+    // 32-bit sizes (NR or BK pitch-long rows or k-lines) and a base made explicitly uniform, so
+    // that the resource sits in scalar registers (a per-lane resource would be looped over)
+    const int p2 = static_cast<int>(op.pitch) * 2;
+    int size;
+    const uint16_t* b;
+    if constexpr (L == LL::KC) {
+      b = tbase + k0;
+      size = (k0 < klim) ? rows_left * p2 - k0 * 2 : 0;
+    } else {
+      b = tbase + static_cast<int64_t>(k0) * op.pitch;
+      // (klim - k0 <= 0 leaves size <= 0: no k-line of this tile is valid)
+      size = min(klim - k0, BK) * p2 - rows_left * 2;
+    }
+    size = __builtin_amdgcn_readfirstlane(max(size, 0));
+    const uint64_t ba = reinterpret_cast<uint64_t>(b);
+    const uint64_t bu = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(ba >> 32))) << 32) |
+                        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(ba)));
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(bu),
+                                                                       static_cast<short>(0), size, kBufWord3);
+    uint32_t adj = 0u;
+    if constexpr (L == LL::KC) {
+      adj = (k0 == kpart) ? poob : 0u;
+      asm volatile("" : "+v"(adj));  // one register per issue, not a hoisted second offset set
+    }
+#pragma unroll
+    for (int i = 0; i < kPerWave; ++i) {
+      const int c = w + NW * i;
+      __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void*)(lds + c * 1024), 16, off[i] | adj, 0, 0, 0);
+    }
+#endif
+  }
+};
+
 // 8-element bf16 fragment of row (or column) `rr` for k in [kk + 8h, kk + 8h + 8).
 template <LL L, int NR, int BK>
 __device__ __forceinline__ bf16x8 frag(const char* lds, int rr_base, int kk, int lane) {
@@ -179,7 +289,7 @@ __device__ __forceinline__ bf16x8 frag(const char* lds, int rr_base, int kk, int
 // tile's last k-step, half of the products are issued before the barrier (they need only
 // registers), so the matrix pipe has work while the wave waits there; this pays where one
 // workgroup fills the CU (no other workgroup's products to fill the wait).
-template <int BR, int BC, int BK, LL LA, LL LB, int NS, int WR = 2, int WC = 2, bool PRE = false>
+template <int BR, int BC, int BK, LL LA, LL LB, int NS, int WR = 2, int WC = 2, bool PRE = false, bool BUF = true>
 struct Gemm {
   static constexpr int kNS = NS;
   static constexpr int kBR = BR, kBC = BC;
@@ -190,8 +300,8 @@ struct Gemm {
   static constexpr int kABytes = BR * BK * 2;
   static constexpr int kBBytes = BC * BK * 2;
   static constexpr int kStageBytes = kABytes + kBBytes;
-  using CA = TileCopy<LA, BR, BK, NW>;
-  using CB = TileCopy<LB, BC, BK, NW>;
+  using CA = TileCopy<LA, BR, BK, NW, BUF>;
+  using CB = TileCopy<LB, BC, BK, NW, BUF>;
   static constexpr int CPW = CA::kPerWave + CB::kPerWave;  // copies per wave per k-tile
   static_assert(NS >= 2 && NS <= 4, "stages");
   static_assert(KK % 2 == 0, "BK must be a multiple of 32");
@@ -297,15 +407,21 @@ struct Gemm {
   template <bool ZERO = true>
   __device__ static __forceinline__ void run(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
                                              char* const (&st)[NS], f32x16 (&acc)[FR][FC]) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: copy targets in scalar registers
     if constexpr (ZERO) zero(acc);
     const int nk = (kend - kbeg + BK - 1) / BK;
     if (nk <= 0) return;
     const int klimA = min(A.kmax, kend), klimB = min(B.kmax, kend);
     CA ca;
     CB cb;
-    ca.init(A, row0, wave, lane);
-    cb.init(B, col0, wave, lane);
+    if constexpr (BUF) {
+      ca.init(A, row0, wave, lane, kbeg, klimA);
+      cb.init(B, col0, wave, lane, kbeg, klimB);
+    } else {
+      ca.init(A, row0, wave, lane);
+      cb.init(B, col0, wave, lane);
+    }
     __builtin_amdgcn_s_barrier();  // previous users of the stages are done
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
@@ -348,7 +464,8 @@ struct Gemm {
   __device__ static __forceinline__ void run_seq(const GOp& A, const GOp& B, int row0, int col0, int ntiles, int K,
                                                  char* const (&st)[NS], f32x16 (&acc)[FR][FC], Epi&& epi,
                                                  Init&& init = Init{}) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: copy targets in scalar registers
     if (ntiles > 0) init(0, acc);
     else zero(acc);
     const int nk = (K + BK - 1) / BK;
@@ -356,8 +473,13 @@ struct Gemm {
     const int klimA = min(A.kmax, K), klimB = min(B.kmax, K);
     CA ca;
     CB cb;
-    ca.init(A, row0, wave, lane);
-    cb.init(B, col0, wave, lane);
+    if constexpr (BUF) {
+      ca.init(A, row0, wave, lane, 0, klimA);
+      cb.init(B, col0, wave, lane, 0, klimB);
+    } else {
+      ca.init(A, row0, wave, lane);
+      cb.init(B, col0, wave, lane);
+    }
     int ctile = 0, ck = 0;  // copy stream position
     auto issue = [&](char* stage) {
       if (ck == nk) {

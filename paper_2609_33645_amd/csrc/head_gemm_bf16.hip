@@ -31,6 +31,8 @@ constexpr int kBK = 32;
 // 4 wavefronts (2 x 2), two workgroups per CU so that one's epilogue overlaps the
 // other's products
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
+// the same tiles over gathered W rows (selected classes): flat per-lane addresses
+using GFwdGather = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3, 2, 2, false, false>;
 // 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
 using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
 // logit products of wide heads (D >= kWideD: normaliser, argmax, recompute): the k loop is
@@ -337,7 +339,7 @@ __global__ void __launch_bounds__(256, 2)
 gather_s_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W,
               const float* __restrict__ bias, const int32_t* __restrict__ u_ids, const int32_t* __restrict__ Kdev,
               const double* __restrict__ lam, float* __restrict__ S, int ldS, double* __restrict__ Zd) {
-  using G = GFwd;
+  using G = GFwdGather;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES_G(G)
   const int nMt = (M + kFC - 1) / kFC;
