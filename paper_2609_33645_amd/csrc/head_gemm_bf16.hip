@@ -168,17 +168,12 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   PCTC_STAGES_G(G)
   const int nMt = (M + TC - 1) / TC;
-  int mt, p;
-  if constexpr (std::is_same<G, GMid>::value) {
-    // every frame tile of a vocabulary run on one XCD at about the same time: the run's W
-    // rows are fetched once and shared through that XCD's L2
-    const int w = xcd_swz(blockIdx.x, gridDim.x);
-    mt = w % nMt;
-    p = w / nMt;
-    if (p >= P) return;
-  } else if (!grouped_tile(xcd_swz(blockIdx.x, gridDim.x), nMt, P, mt, p)) {
-    return;
-  }
+  // every frame tile of a vocabulary run on one XCD at about the same time: the run's W rows
+  // are fetched once and shared through that XCD's L2
+  const int w = xcd_swz(blockIdx.x, gridDim.x);
+  const int mt = w % nMt;
+  const int p = w / nMt;
+  if (p >= P) return;
   const int m0 = mt * TC;
   const int vbeg = p * vper;
   const int vend = min(V, vbeg + vper);
@@ -880,7 +875,7 @@ hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t
 // workgroups evenly measured slower for narrow heads: the run length also sets the L2 reuse
 // of the tile order.)
 struct LseSplit {
-  bool wide;  // one 8-wave 256 x 256 workgroup per CU (GWide for wide heads, GMid otherwise)
+  bool wide;  // D >= kWideD: one vocabulary tile per partition (argmax: GWide tiles)
   int vper, P, nM;
 };
 
@@ -906,15 +901,10 @@ hipError_t launch_lse_partial_bf16(const uint16_t* H, int M, int D, const uint16
   *P_out = Peff;
   Prof pr("lse_partial", stream);
   const size_t bsh = bias ? static_cast<size_t>(vper) * sizeof(float) : 0;
-  const dim3 grid(sp.wide ? grouped_grid(sp.nM, Peff) : sp.nM * Peff);
-  if (sp.wide) {
-    if (bias)
-      hipLaunchKernelGGL((lse_partial_bf16<GWide, true, 1>), grid, dim3(GWide::kThreads), bsh, stream, H, M, D, W,
-                         bias, V, Peff, vper, partials);
-    else
-      hipLaunchKernelGGL((lse_partial_bf16<GWide, false, 1>), grid, dim3(GWide::kThreads), 0, stream, H, M, D, W,
-                         bias, V, Peff, vper, partials);
-  } else if (bias) {
+  // every head on the 32-deep four-stage tiles (for wide heads each vocabulary tile is its own
+  // partition; the 64-deep two-stage tiles measured 4% slower there)
+  const dim3 grid(sp.nM * Peff);
+  if (bias) {
     hipLaunchKernelGGL((lse_partial_bf16<GMid, true, 1>), grid, dim3(GMid::kThreads), bsh, stream, H, M, D, W, bias,
                        V, Peff, vper, partials);
   } else {
