@@ -249,7 +249,7 @@ def bench_extra(a):
         per_launch = flops[dom] / (dom_prof["launches"] / a.steps)
         ach = per_launch / (dom_avg_ms * 1e-3) / 1e12
         roof = {"bound": "mfma", "kernel": dom, "achieved": round(ach, 2), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom)}
+                "frac": round(ach / peak, 4), "traffic": measured_traffic(dom, wl.name)}
     else:
         # lattice sums: each frame reads its U_n + 1 selected scores and 2U_n + 1 arc-mask bytes
         nbytes = float(sum(int(t) * ((int(u) + 1) * 4 + (2 * int(u) + 1)) for t, u in zip(T, U)))
