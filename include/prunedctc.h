@@ -307,8 +307,9 @@ int32_t pctc_grouped_backward(pctc_dtype dtype, const void* H, int32_t M, int32_
 
 /* ----------------------------------------------------------------------------------
  * Kernel timing for benchmarks.  When enabled, every kernel the library launches is
- * bracketed by HIP events on its stream; times are accumulated per kernel name at the
- * end of each pruned_ctc_fwd_bwd call (which synchronises anyway).
+ * bracketed by HIP events on its stream; the times are accumulated per kernel name when
+ * they are read (pctc_prof_count / pctc_prof_get, which wait for the recorded launches to
+ * finish) or reset, so that timing adds no per-call host work beyond the event records.
  * ---------------------------------------------------------------------------------- */
 void pctc_prof_enable(int32_t on);
 /* Restrict timing to the kernels of one name (as reported by pctc_prof_get); NULL or ""

@@ -72,9 +72,8 @@ Prof::~Prof() {
   s.pending.push_back(ProfRec{name, start, stop});
 }
 
-void prof_flush() {
-  ProfState& s = prof_state();
-  std::lock_guard<std::mutex> lk(s.mu);
+// Resolves the pending event pairs into the per-kernel totals (s.mu held).
+static void prof_resolve(ProfState& s) {
   for (auto& r : s.pending) {
     float ms = 0.f;
     if (hipEventSynchronize(r.stop) == hipSuccess && hipEventElapsedTime(&ms, r.start, r.stop) == hipSuccess) {
@@ -91,6 +90,16 @@ void prof_flush() {
     s.pool.push_back(r.stop);
   }
   s.pending.clear();
+}
+
+// Called at the end of every entry point.  The pairs are resolved when the totals are read
+// (or reset), so that timing costs a call only its event records; here only a long backlog
+// is resolved, which bounds the events held.
+void prof_flush() {
+  constexpr size_t kMaxPending = 4096;
+  ProfState& s = prof_state();
+  std::lock_guard<std::mutex> lk(s.mu);
+  if (s.pending.size() >= kMaxPending) prof_resolve(s);
 }
 
 static void set_error(const char* what, hipError_t e) {
@@ -389,11 +398,12 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     ev = Events{lease.set->e[0], lease.set->e[1], lease.set->e[2], lease.set->e[3],
                 lease.set->e[4], lease.set->e[5], lease.set->e[6]};
     PCTC_HIP(hipEventRecord(ev.start, stream));
-    PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     double* Zd = reinterpret_cast<double*>(ws + L.o_zd);
-    // online full-vocabulary log-sum-exp, launched first: it is the longest step
+    // online full-vocabulary log-sum-exp, launched first: it is the longest step (the
+    // second stream's wait on the work before it is enqueued after this launch)
     int P = 0;
     PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
     // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
     PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, offsets_img, dps_stream));
@@ -938,6 +948,7 @@ void pctc_prof_select(const char* name) {
 void pctc_prof_reset(void) {
   ProfState& s = prof_state();
   std::lock_guard<std::mutex> lk(s.mu);
+  prof_resolve(s);  // recycles the pending pairs; their times belong to the cleared totals
   s.totals.clear();
   s.names.clear();
 }
@@ -945,12 +956,14 @@ void pctc_prof_reset(void) {
 int32_t pctc_prof_count(void) {
   ProfState& s = prof_state();
   std::lock_guard<std::mutex> lk(s.mu);
+  prof_resolve(s);
   return static_cast<int32_t>(s.names.size());
 }
 
 int32_t pctc_prof_get(int32_t i, const char** name, double* total_ms, int64_t* launches) {
   ProfState& s = prof_state();
   std::lock_guard<std::mutex> lk(s.mu);
+  prof_resolve(s);
   if (i < 0 || i >= static_cast<int32_t>(s.names.size())) return 0;
   const auto& t = s.totals[s.names[i]];
   if (name) *name = s.names[i].c_str();

@@ -11,8 +11,9 @@ namespace pctc {
 
 // Kernel timing: records a start event on construction and a stop event on destruction
 // when timing is enabled (pctc_prof_enable); the scope owns its two events until it closes,
-// when the pair joins the shared list that prof_flush() resolves (a flush from another thread
-// meanwhile neither sees nor recycles them).
+// when the pair joins the shared list that is resolved when the totals are read (a reader in
+// another thread meanwhile neither sees nor recycles them).  prof_flush(), at the end of each
+// entry point, resolves that list only once it is long.
 struct Prof {
   Prof(const char* name, hipStream_t stream);
   ~Prof();
