@@ -21,11 +21,13 @@
 #include <type_traits>
 
 #include "pctc_internal.h"
+#include "prunedctc.h"
 
 namespace pctc {
 
 constexpr float kNeg = -1.0e30f;  // "impossible" score; absorbs finite additions
 constexpr int kMaxQ = 32;         // most states per lane of a lattice pass (2U+1 <= 64 kMaxQ)
+static_assert(2 * PCTC_MAX_TARGET + 1 <= 64 * kMaxQ, "the longest target fits a lattice pass");
 // arc flags of a pass without a mask: every arc kept
 __device__ const uint8_t kAllArcs[1] = {0x0f};
 
@@ -85,12 +87,15 @@ __global__ void dp_prep_kernel(const int32_t* __restrict__ toff, const int32_t* 
   const int n = blockIdx.x;
   const int t0 = toff[n], T = toff[n + 1] - t0;
   const int y0 = yoff[n], U = yoff[n + 1] - y0;
-  const int* y = y_rel + y0;
+  // the utterance's targets in LDS (every entry point rejects U > PCTC_MAX_TARGET before
+  // any launch): the duplicate search below compares every pair
+  __shared__ int y[PCTC_MAX_TARGET];
   __shared__ int reps, badlab;
   if (threadIdx.x == 0) {
     reps = 0;
     badlab = 0;
   }
+  for (int i = threadIdx.x; i < U; i += blockDim.x) y[i] = y_rel[y0 + i];
   __syncthreads();
   int myreps = 0;
   for (int i = threadIdx.x; i < U; i += blockDim.x) {

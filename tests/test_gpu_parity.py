@@ -223,11 +223,13 @@ def test_e2e_tiny_f32():
 
 
 @pytest.mark.parametrize("dtype,D,V,blank", [
-    ("bf16", 8, 2, 0), ("f32", 8, 2, 1), ("bf16", 24, 3, 2), ("f32", 24, 1000, 0), ("bf16", 8, 1000, 999)])
+    ("bf16", 8, 2, 0), ("f32", 8, 2, 1), ("bf16", 24, 3, 2), ("f32", 24, 1000, 0), ("bf16", 8, 1000, 999),
+    ("bf16", 40, 1000, 0), ("bf16", 104, 3001, 5)])
 def test_e2e_smallest_shapes(dtype, D, V, blank):
-    """The narrowest heads (D = 8, the minimum; D = 24, not a whole k-tile of the products)
-    and the smallest vocabularies (V = 2: the blank and one label), with one-frame
-    utterances among the rest."""
+    """The narrowest heads (D = 8, the minimum; D = 24, not a whole k-tile of the products;
+    D = 40 and 104, whole k-tiles followed by a partial one, with V = 3001 leaving a partial
+    8-column group in the last chunk) and the smallest vocabularies (V = 2: the blank and one
+    label), with one-frame utterances among the rest."""
     wl, ref = unambiguous_case(
         lambda s: workloads.random_small(s, N=5, T_range=(1, 5) if V <= 3 else (1, 30), D=D, V=V, dtype=dtype,
                                          token_law="uniform", p_repeat=0.2, blank=blank,
