@@ -878,8 +878,11 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
         if ((e = hipGetLastError()) != hipSuccess) return e;
       }
       if (dW) {
+        // the union columns' dW_u rides in this launch's last round once their bf16 G is written
+        const DwExtra* udw = side->udw.Z ? &side->udw : nullptr;
+        if (udw && (e = hipStreamWaitEvent(stream, udw->ready, 0)) != hipSuccess) return e;
         e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                  false, false, true, dW, db, dbpart, stream);
+                                  false, false, true, dW, db, dbpart, stream, udw);
         if (e != hipSuccess) return e;
       }
     } else {

@@ -626,29 +626,45 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
     }
 }
 
-// dW[c0 + v][:] = sum over frames of dZ[m][v] Hs[m][:].  With nz > 1 the frames are split
-// into nz slices of mslice frames and slice z writes its partial sums at dW + z * zstride.
+// One operand set of a dW product: out[(c0 + v) * D + d] = sum over frames of Z[m][v] Hs[m][d]
+// for v < cw (cut to 2 *kdev when kdev is set: the union columns' [hi | lo] of the K classes
+// the device found).  With nz > 1 the frames are split into nz slices of mslice frames and
+// slice z writes its partial sums at out + z * zstride.
+struct DwOp {
+  const uint16_t* Z;
+  int ld, c0, cw;
+  float* out;
+  int nz, mslice;
+  int64_t zstride;
+  const int32_t* kdev;
+};
+
+// dW products of up to two operand sets in one launch: work ids below tiles0 take P0's output
+// tiles, the rest P1's (the union columns' dW_u in the last chunk's launch).
 __global__ void __launch_bounds__(512, 1)
-dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ Hs, int D, int c0, int cw,
-             float* __restrict__ dW, int nz, int mslice, int64_t zstride, const int32_t* __restrict__ kdev) {
+dw_gemm_bf16(DwOp P0, DwOp P1, int tiles0, const uint16_t* __restrict__ Hs, int M, int D) {
   using G = GDw;
   constexpr int FR = G::FR, FC = G::FC;
   PCTC_STAGES_G(G)
-  const int nDt = (D + kBC - 1) / kBC;
-  const int nVt = (cw + kBR - 1) / kBR;
   const int work = xcd_swz(blockIdx.x, gridDim.x);
-  const int dt = work % nDt;
-  const int vt = (work / nDt) % nVt;
-  const int z = work / (nDt * nVt);
+  const bool second = work >= tiles0;
+  const DwOp P = second ? P1 : P0;
+  const int w = second ? work - tiles0 : work;
+  const int nDt = (D + kBC - 1) / kBC;
+  int cw = P.cw;
+  const int nVt = (cw + kBR - 1) / kBR;
+  const int dt = w % nDt;
+  const int vt = (w / nDt) % nVt;
+  const int z = w / (nDt * nVt);
   const int v0 = vt * kBR, d0 = dt * kBC;
-  const int mb = z * mslice;
-  const int mlen = min(M - mb, mslice);
-  if (kdev) cw = min(cw, 2 * *kdev);  // union rows: [hi | lo] of the K classes the device found
-  if (z >= nz || mlen <= 0 || v0 >= cw) return;
-  dW += static_cast<int64_t>(z) * zstride;
+  const int mb = z * P.mslice;
+  const int mlen = min(M - mb, P.mslice);
+  if (P.kdev) cw = min(cw, 2 * *P.kdev);
+  if (z >= P.nz || mlen <= 0 || v0 >= cw) return;
+  float* const dW = P.out + static_cast<int64_t>(z) * P.zstride;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  // A: dZ viewed as rows v (columns of dZ), k = frame; B: Hs viewed as rows d, k = frame
-  const GOp A{dZ + static_cast<int64_t>(mb) * chunk, chunk, cw, mlen, nullptr};
+  // A: Z viewed as rows v (columns of Z), k = frame; B: Hs viewed as rows d, k = frame
+  const GOp A{P.Z + static_cast<int64_t>(mb) * P.ld, P.ld, cw, mlen, nullptr};
   const GOp B{Hs + static_cast<int64_t>(mb) * D, D, D, mlen, nullptr};
   f32x16 acc[FR][FC];
   G::run(A, B, v0, d0, 0, mlen, st, acc);
@@ -661,7 +677,7 @@ dw_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int v = v0 + G::row_of(wave, lane, i, r);
-        if (v < cw) dW[static_cast<int64_t>(c0 + v) * D + d] = acc[i][j][r];
+        if (v < cw) dW[static_cast<int64_t>(P.c0 + v) * D + d] = acc[i][j][r];
       }
     }
 }
@@ -691,23 +707,27 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
 __global__ void __launch_bounds__(256)
 union_split_bf16(const float* __restrict__ G, int ldG, const int32_t* __restrict__ Kdev, int ldK, int M,
                  uint16_t* __restrict__ Gb) {
-  const int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x;
-  if (i >= static_cast<int64_t>(M) * ldK) return;
   const int K = *Kdev;
-  const int m = static_cast<int>(i / ldK), j = static_cast<int>(i % ldK);
-  const float* grow = G + static_cast<int64_t>(m) * ldG;
-  uint16_t* row = Gb + static_cast<int64_t>(m) * (2 * ldK);
+  const int64_t n = static_cast<int64_t>(M) * ldK;
+  // a few hundred workgroups stride over the elements: the launch runs beside a recompute,
+  // whose compute units it should not churn with thousands of tiny workgroups
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * 256 + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * 256) {
+    const int m = static_cast<int>(i / ldK), j = static_cast<int>(i % ldK);
+    const float* grow = G + static_cast<int64_t>(m) * ldG;
+    uint16_t* row = Gb + static_cast<int64_t>(m) * (2 * ldK);
 #pragma unroll
-  for (int h = 0; h < 2; ++h) {  // columns j and ldK + j
-    const int c = j + h * ldK;
-    uint16_t out = 0;
-    if (c < K) {
-      out = f32_to_bf16(grow[c]);
-    } else if (c < 2 * K) {
-      const float x = grow[c - K];
-      out = f32_to_bf16(x - bf16_to_f32(f32_to_bf16(x)));
+    for (int h = 0; h < 2; ++h) {  // columns j and ldK + j
+      const int c = j + h * ldK;
+      uint16_t out = 0;
+      if (c < K) {
+        out = f32_to_bf16(grow[c]);
+      } else if (c < 2 * K) {
+        const float x = grow[c - K];
+        out = f32_to_bf16(x - bf16_to_f32(f32_to_bf16(x)));
+      }
+      row[c] = out;
     }
-    row[c] = out;
   }
 }
 
@@ -715,13 +735,13 @@ union_split_bf16(const float* __restrict__ G, int ldG, const int32_t* __restrict
 __global__ void __launch_bounds__(256)
 union_rows_bf16(const uint16_t* __restrict__ W, int D, const int32_t* __restrict__ u_ids,
                 const int32_t* __restrict__ Kdev, uint16_t* __restrict__ WU2) {
-  const int r = blockIdx.x;
   const int K = *Kdev;
-  if (r >= 2 * K) return;
-  const int j = r < K ? r : r - K;
-  const uint16_t* src = W + static_cast<int64_t>(u_ids[j]) * D;
-  for (int d = threadIdx.x * 8; d < D; d += 256 * 8)
-    *reinterpret_cast<u32x4*>(WU2 + static_cast<int64_t>(r) * D + d) = *reinterpret_cast<const u32x4*>(src + d);
+  for (int r = blockIdx.x; r < 2 * K; r += gridDim.x) {
+    const int j = r < K ? r : r - K;
+    const uint16_t* src = W + static_cast<int64_t>(u_ids[j]) * D;
+    for (int d = threadIdx.x * 8; d < D; d += 256 * 8)
+      *reinterpret_cast<u32x4*>(WU2 + static_cast<int64_t>(r) * D + d) = *reinterpret_cast<const u32x4*>(src + d);
+  }
 }
 
 // dbp[z][j] = sum of G[m][j] over the frames of slice z (fp32, in frame order)
@@ -765,23 +785,19 @@ union_merge_bf16(const int32_t* __restrict__ Kdev, const int32_t* __restrict__ u
 namespace {
 constexpr int kColSlices = 16;
 struct UnionCorrLayout {
-  int ldK, nz, mslice;  // nz slices of mslice frames for the dW_u product (summed when merged)
+  int ldK, nz, mslice;  // dW_u over nz slices of mslice frames (one: every frame)
   size_t o_dwu, o_wu, o_dbp, total;
 };
-// [dW_u slices (only when dW is wanted)][W_U rows twice][db_u slices]; the [hi | lo] copy of G
-// lives outside (gb_bytes, in the region of S, which is dead once the lattice is done)
+// [dW_u (only when dW is wanted)][W_U rows twice][db_u slices]; the [hi | lo] copy of G lives
+// outside (gb_bytes, in the region of S, which is dead once the lattice is done).  dW_u is one
+// launch's worth of 256 x 256 tiles over all frames, like a dense dW tile, so that it can ride
+// in the last round of the last chunk's dense dW launch.
 UnionCorrLayout union_corr_layout(int M, int D, int K_max, bool want_dW) {
   UnionCorrLayout L;
   L.ldK = (K_max + 7) / 8 * 8;
   const size_t k2 = static_cast<size_t>(2) * L.ldK;
-  const int tiles = static_cast<int>((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
-  L.nz = 64 / tiles;  // a short, wide launch beside the dense part
-  if (L.nz > (M + 255) / 256) L.nz = (M + 255) / 256;
-  if (L.nz < 1) L.nz = 1;
-  L.mslice = ((M + L.nz - 1) / L.nz + 63) / 64 * 64;
-  if (L.mslice < 64) L.mslice = 64;       // M = 0 (no frames): one empty slice
-  L.nz = (M + L.mslice - 1) / L.mslice;  // every slice holds frames
-  if (L.nz < 1) L.nz = 1;
+  L.nz = 1;
+  L.mslice = M > 0 ? M : 1;
   L.o_dwu = 0;
   L.o_wu = L.o_dwu + (want_dW ? align_up(static_cast<size_t>(L.nz) * k2 * D * sizeof(float), 256) : 0);
   L.o_dbp = L.o_wu + align_up(k2 * D * sizeof(uint16_t), 256);
@@ -797,9 +813,22 @@ size_t union_gb_bytes(int M, int K_max) {
   return static_cast<size_t>(M) * 2 * ((K_max + 7) / 8 * 8) * sizeof(uint16_t);
 }
 
+DwExtra union_dw_extra(int M, int D, int K_max, const int32_t* Kdev, void* scratch, const uint16_t* Gb) {
+  DwExtra x;
+  if (M <= 0 || K_max <= 0) return x;
+  const UnionCorrLayout L = union_corr_layout(M, D, K_max, true);
+  x.Z = Gb;
+  x.ld = 2 * L.ldK;
+  x.cols = 2 * L.ldK;
+  x.kdev = Kdev;
+  x.out = reinterpret_cast<float*>(static_cast<char*>(scratch) + L.o_dwu);
+  return x;
+}
+
 hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
                                   const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool dh_later,
-                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream) {
+                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream,
+                                  bool dw_elsewhere) {
   const bool want_dH = dH != nullptr || dh_later;
   if (M <= 0 || K_max <= 0) return hipSuccess;
   if (want_dW && !Hs) return hipErrorInvalidValue;
@@ -809,12 +838,13 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
   if (want_dH || want_dW) {
     Prof pr("union_prep", stream);
     const int64_t n = static_cast<int64_t>(M) * L.ldK;
-    hipLaunchKernelGGL(union_split_bf16, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream, G, ldG,
-                       Kdev, L.ldK, M, Gb);
+    const int64_t blocks = (n + 255) / 256;
+    hipLaunchKernelGGL(union_split_bf16, dim3(static_cast<unsigned>(blocks < 512 ? blocks : 512)), dim3(256), 0,
+                       stream, G, ldG, Kdev, L.ldK, M, Gb);
   }
   if (want_dH) {
     uint16_t* WU2 = reinterpret_cast<uint16_t*>(sc + L.o_wu);
-    hipLaunchKernelGGL(union_rows_bf16, dim3(k2), dim3(256), 0, stream, W, D, u_ids, Kdev, WU2);
+    hipLaunchKernelGGL(union_rows_bf16, dim3(k2 < 256 ? k2 : 256), dim3(256), 0, stream, W, D, u_ids, Kdev, WU2);
     if (!dh_later) {
       const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
       Prof pr("union_dh", stream);
@@ -822,11 +852,12 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
                          k2, k2, dH, dh_xcd_rows(M, D), 0, Kdev);
     }
   }
-  if (want_dW) {
-    const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+  if (want_dW && !dw_elsewhere) {
+    const int tiles = ((k2 + kBR - 1) / kBR) * ((D + kBC - 1) / kBC) * L.nz;
+    const DwOp p{Gb, k2, 0, k2, reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice,
+                 static_cast<int64_t>(k2) * D, Kdev};
     Prof pr("union_dw", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles * L.nz), dim3(GDw::kThreads), 0, stream, Gb, M, k2, Hs, D, 0, k2,
-                       reinterpret_cast<float*>(sc + L.o_dwu), L.nz, L.mslice, static_cast<int64_t>(k2) * D, Kdev);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles), dim3(GDw::kThreads), 0, stream, p, p, tiles, Hs, M, D);
   }
   if (want_db) {
     const int mper = (M + kColSlices - 1) / kColSlices;
@@ -954,7 +985,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
-                                 float* dbpart, hipStream_t stream) {
+                                 float* dbpart, hipStream_t stream, const DwExtra* extra) {
   // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue);
   // narrow heads: two 4-wave 256 x 128 workgroups per CU, so that one's epilogue (exp, pack,
   // staged stores: VALU-bound) overlaps the other's products
@@ -995,10 +1026,17 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                        c0, cw, slice, part, dh_xcd_rows(M, D), 0, nullptr);
   }
   if (want_dW) {
-    const int grid = ((cw + kBR - 1) / kBR) * ((D + kBC - 1) / kBC);
+    const int nDt = (D + kBC - 1) / kBC;
+    const int tiles0 = ((cw + kBR - 1) / kBR) * nDt;
+    const DwOp p0{dZ, chunk, c0, cw, dW, 1, M, 0, nullptr};
+    DwOp p1 = p0;
+    int tiles1 = 0;
+    if (extra && extra->Z) {  // the union columns' dW_u, in this launch's last round
+      p1 = DwOp{extra->Z, extra->ld, 0, extra->cols, extra->out, 1, M, 0, extra->kdev};
+      tiles1 = ((extra->cols + kBR - 1) / kBR) * nDt;
+    }
     Prof pr("dw_gemm", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(grid), dim3(GDw::kThreads), 0, stream, dZ, M, chunk, Hs, D, c0, cw, dW, 1, M,
-                       static_cast<int64_t>(0), nullptr);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles0 + tiles1), dim3(GDw::kThreads), 0, stream, p0, p1, tiles0, Hs, M, D);
   }
   return hipGetLastError();
 }

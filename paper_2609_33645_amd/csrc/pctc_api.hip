@@ -226,7 +226,7 @@ static hipError_t upload_offsets(const DpPlan& dp, char* dpbase, const std::vect
 // pool at the start of a call and returned at its end (after the call has synchronised, so
 // every record on it is complete).  Sets are created when the pool is empty and kept until
 // the process ends.
-constexpr int kCallEvents = 7;
+constexpr int kCallEvents = 8;
 struct CallEvents {
   hipEvent_t e[kCallEvents];
 };
@@ -380,7 +380,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   hipStream_t dps_stream = stream;
   struct Events {
     hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, gate0 = nullptr, gate1 = nullptr, dh_done = nullptr,
-               join = nullptr;
+               join = nullptr, udw = nullptr;
   } ev;
   EventsLease lease;
   std::vector<char> offsets_img;
@@ -396,7 +396,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     PCTC_HIP(side_stream(&dps_stream));
     PCTC_HIP(lease.take());
     ev = Events{lease.set->e[0], lease.set->e[1], lease.set->e[2], lease.set->e[3],
-                lease.set->e[4], lease.set->e[5], lease.set->e[6]};
+                lease.set->e[4], lease.set->e[5], lease.set->e[6], lease.set->e[7]};
     PCTC_HIP(hipEventRecord(ev.start, stream));
     double* Zd = reinterpret_cast<double*>(ws + L.o_zd);
     // online full-vocabulary log-sum-exp, launched first: it is the longest step (the
@@ -486,18 +486,25 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
       void* scratch;
       uint16_t* Gb;
       hipStream_t stream;
+      hipEvent_t dw_ready;  // non-null: dW_u is left to the last dense dW launch, which waits for it
       static hipError_t run(void* p) {
         const UnionWork& u = *static_cast<const UnionWork*>(p);
-        return launch_union_part_bf16(u.G, u.ldG, u.Kdev, u.K_max, u.u_ids, u.W, u.Hs, u.M, u.D,
-                                      u.dh_later ? nullptr : u.dH, u.dh_later, u.want_dW, u.want_db, u.scratch, u.Gb,
-                                      u.stream);
+        hipError_t e = launch_union_part_bf16(u.G, u.ldG, u.Kdev, u.K_max, u.u_ids, u.W, u.Hs, u.M, u.D,
+                                              u.dh_later ? nullptr : u.dH, u.dh_later, u.want_dW, u.want_db,
+                                              u.scratch, u.Gb, u.stream, u.dw_ready != nullptr);
+        if (e == hipSuccess && u.dw_ready) e = hipEventRecord(u.dw_ready, u.stream);
+        return e;
       }
       static hipError_t run_dh(void* p) {
         const UnionWork& u = *static_cast<const UnionWork*>(p);
         return launch_union_dh_bf16(u.Gb, u.Kdev, u.K_max, u.M, u.D, u.dH, u.scratch, u.want_dW, u.stream);
       }
     } uw{G, L.ldS, Kdev, u_ids, L.K_max, L.M, D, static_cast<const uint16_t*>(W), bwd_hs(bws, L.bwd), dH,
-         dh_in_place, dW != nullptr, db != nullptr, ws + L.o_corr, Gb, dps_stream};
+         dh_in_place, dW != nullptr, db != nullptr, ws + L.o_corr, Gb, dps_stream,
+         // with dH wanted and at least three chunks the union part is enqueued after the second
+         // chunk, well before the last chunk's dW launch, which then also computes dW_u in its
+         // last round (with fewer chunks that launch would wait for the whole lattice)
+         (dH && dW && L.K_max > 0 && (V + L.bwd.chunk - 1) / L.bwd.chunk >= 3) ? ev.udw : nullptr};
     // dense part, chunk by chunk, on the caller's stream; the final dH reduction, which adds
     // the union part's dH_u (written into dH), runs on the second stream beside the last dW
     BwdSide side;
@@ -512,6 +519,10 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     if (dh_in_place) side.after_dh = SideWork{&UnionWork::run_dh, &uw};
     side.dH_extra = (dH && !dh_in_place && L.K_max > 0) ? dH : nullptr;
     side.hs_built = (dH || dW);
+    if (uw.dw_ready) {
+      side.udw = union_dw_extra(L.M, D, L.K_max, Kdev, ws + L.o_corr, Gb);
+      side.udw.ready = uw.dw_ready;
+    }
     PCTC_HIP(launch_head_bwd(dt, H, L.M, D, W, bias, V, lam2, nullptr, L.ldS, g_pred, nullptr, nullptr, L.ldS, dH, dW,
                              db, bws, L.bwd, stream, &side));
     PCTC_HIP(launch_union_merge_bf16(Kdev, L.K_max, u_ids, L.M, D, dW, db, ws + L.o_corr, stream));

@@ -68,6 +68,17 @@ hipError_t launch_greedy(int dtype, const void* H, int M, int D, const void* W, 
 hipError_t launch_amax_partial_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                     float2* partials, int* P_out, hipStream_t stream);
 
+// A second operand set for a dW product's launch: out[v][:] = sum over frames of Z[m][v] Hs[m][:]
+// for v < cols (cut to 2 *kdev when kdev is set), Z [M][ld] bf16.  The union columns' dW_u
+// rides this way in the last chunk's dense dW launch (its work fits the launch's last round).
+struct DwExtra {
+  const uint16_t* Z = nullptr;  // null: none
+  int ld = 0, cols = 0;
+  const int32_t* kdev = nullptr;
+  float* out = nullptr;
+  hipEvent_t ready = nullptr;   // recorded once Z is written (second stream); waited on first
+};
+
 // ---- backward ---------------------------------------------------------------------------
 struct BwdPlan {
   int chunk;       // vocabulary columns per step
@@ -88,7 +99,8 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
 // When the dense part accumulates dH in place (a single split-K slice: no partial buffer),
 // after_dh runs there instead of the reduction (it adds the union columns' part to dH).
 // hs_built: the masked copy of H (bwd_hs) was already written, from the same g, on a stream
-// the caller's stream has waited for.
+// the caller's stream has waited for.  udw (when udw.Z is set): with dH wanted, the last
+// chunk's dW launch waits for udw.ready and also computes the union columns' dW_u.
 struct SideWork {
   hipError_t (*fn)(void*) = nullptr;
   void* ctx = nullptr;
@@ -102,6 +114,7 @@ struct BwdSide {
   int nwork = 0;
   const float* dH_extra = nullptr;
   bool hs_built = false;
+  DwExtra udw;  // the union columns' dW_u, folded into the last chunk's dW launch (dH wanted)
 };
 // the masked copy of H (rows of frames with g == 0 zeroed) inside the backward's scratch
 uint16_t* bwd_hs(void* scratch, const BwdPlan& plan);
@@ -127,7 +140,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
-                                 float* dbpart, hipStream_t stream);
+                                 float* dbpart, hipStream_t stream, const DwExtra* extra = nullptr);
 // Union-column part of the backward (bf16 path): dH_u = G W_U written into dH [M][D] (which
 // the final reduction then adds the dense part to), or later added to dH, and into its own
 // buffers dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left
@@ -136,11 +149,15 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
 // copy, bwd_hs), needed for dW_u.
 // Gb [M][2 ldK] bf16 (union_gb_bytes): the [hi | lo] copy of G, caller-placed.  dh_later: dH_u is
 // not formed here but by launch_union_dh_bf16, which adds it to dH (after the dense part).
+// dw_elsewhere: dW_u's buffer is sized and merged as usual, but its product is left to a dense
+// dW launch (union_dw_extra gives that launch's second operand set).
 size_t union_corr_bytes(int M, int D, int K_max, bool want_dW);
 size_t union_gb_bytes(int M, int K_max);
 hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, int K_max, const int32_t* u_ids,
                                   const uint16_t* W, const uint16_t* Hs, int M, int D, float* dH, bool dh_later,
-                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream);
+                                  bool want_dW, bool want_db, void* scratch, uint16_t* Gb, hipStream_t stream,
+                                  bool dw_elsewhere = false);
+DwExtra union_dw_extra(int M, int D, int K_max, const int32_t* Kdev, void* scratch, const uint16_t* Gb);
 hipError_t launch_union_dh_bf16(const uint16_t* Gb, const int32_t* Kdev, int K_max, int M, int D, float* dH,
                                 void* scratch, bool want_dW, hipStream_t stream);
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
