@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <functional>
 #include <map>
 #include <mutex>
 #include <string>
@@ -267,24 +268,37 @@ struct EventsLease {
   }
 };
 
-// A second stream per device for the lattice stage, which runs beside the dense part of the
-// backward.  Created once (default priority, non-blocking), kept until the process ends.
-static hipError_t side_stream(hipStream_t* out) {
+// Second streams for the lattice stage, which runs beside the dense part of the backward: one
+// per caller stream (so that calls on different streams do not queue each other's lattice and
+// union work), up to kSideStreams per device, after which caller streams share them by hash.
+// Created on first use (default priority, non-blocking) and kept until the process ends.
+constexpr int kSideStreams = 4;
+static hipError_t side_stream(hipStream_t caller, hipStream_t* out) {
+  struct DevSide {
+    std::vector<hipStream_t> streams;
+    std::map<hipStream_t, hipStream_t> of;
+  };
   static std::mutex mu;
-  static std::map<int, hipStream_t> streams;
+  static std::map<int, DevSide> sides;
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return e;
   std::lock_guard<std::mutex> lk(mu);
-  auto it = streams.find(dev);
-  if (it != streams.end()) {
+  DevSide& d = sides[dev];
+  auto it = d.of.find(caller);
+  if (it != d.of.end()) {
     *out = it->second;
     return hipSuccess;
   }
   hipStream_t st = nullptr;
-  e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
-  if (e != hipSuccess) return e;
-  streams[dev] = st;
+  if (static_cast<int>(d.streams.size()) < kSideStreams) {
+    e = hipStreamCreateWithFlags(&st, hipStreamNonBlocking);
+    if (e != hipSuccess) return e;
+    d.streams.push_back(st);
+  } else {
+    st = d.streams[std::hash<hipStream_t>{}(caller) % d.streams.size()];
+  }
+  d.of[caller] = st;
   *out = st;
   return hipSuccess;
 }
@@ -393,7 +407,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // part -g p of the backward beside the lattice.  A wrong forecast (rare: a nonfinite
     // normaliser or a -inf logit on a selected class) is caught and the backward is redone in
     // the plain order.
-    PCTC_HIP(side_stream(&dps_stream));
+    PCTC_HIP(side_stream(stream, &dps_stream));
     PCTC_HIP(lease.take());
     ev = Events{lease.set->e[0], lease.set->e[1], lease.set->e[2], lease.set->e[3],
                 lease.set->e[4], lease.set->e[5], lease.set->e[6], lease.set->e[7]};

@@ -431,16 +431,18 @@ def test_e2e_tight_alignment(beam):
     _check_e2e(wl, res, ref, fp32=False)
 
 
-def test_concurrent_calls_on_two_streams():
-    """Two host threads, each on its own stream with its own workspace and outputs, run the
-    fused call at the same time (their second-stream work shares one stream per device):
-    every result equals that of the same call made alone, bit for bit."""
+@pytest.mark.parametrize("nthreads", [2, 6])
+def test_concurrent_calls_on_streams(nthreads):
+    """Host threads, each on its own stream with its own workspace and outputs, run the fused
+    call at the same time (each caller stream has its own second stream, up to four per
+    device; with six, some share one): every result equals that of the same call made
+    alone, bit for bit."""
     import threading
     import torch
     from paper_2609_33645_amd import prunedctc
-    say("concurrent calls on two streams")
+    say(f"concurrent calls on {nthreads} streams")
     wls = [workloads.random_small(90 + i, N=6, T_range=(40, 160), D=128, V=3000, dtype="bf16", p_repeat=0.1,
-                                  beam=16.0, w_std=0.5) for i in range(2)]
+                                  beam=16.0, w_std=0.5) for i in range(nthreads)]
 
     def call(wl):
         H, W, y = to_dev(wl)
@@ -460,14 +462,14 @@ def test_concurrent_calls_on_two_streams():
         except Exception as e:  # reported below
             errors.append(repr(e))
 
-    threads = [threading.Thread(target=worker, args=(i,)) for i in range(2)]
+    threads = [threading.Thread(target=worker, args=(i,)) for i in range(nthreads)]
     for t in threads:
         t.start()
     for t in threads:
         t.join(timeout=100)
     assert not any(t.is_alive() for t in threads)
     assert not errors, errors
-    for i in range(2):
+    for i in range(nthreads):
         for r in range(3):
             for a, b in zip(results[i][r], alone[i]):
                 assert torch.equal(a, b), (i, r)
