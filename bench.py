@@ -44,6 +44,9 @@ def parse():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--chunk", type=int, default=0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--streams", type=int, default=0,
+                    help="also time S host threads calling concurrently, each on its own stream with its own "
+                         "workspace and gradients (aggregate frames/s in the 'concurrent' field)")
     ap.add_argument("--no-paper-protocol", action="store_true",
                     help="skip the paper's 3 x (5 + 50)-call timing protocol (profiling runs)")
     ap.add_argument("--cpu-utts", type=int, default=16, help="utterances in the CPU-baseline sample")
@@ -424,10 +427,59 @@ def main():
         pm = float(np.median(meds))
         line["paper_protocol"] = {"runs": 3, "warmup": 5, "steps": 50, "median_ms_per_call": round(pm * 1e3, 4),
                                   "frames_per_s": round(M / pm, 1)}
+    if a.streams >= 2:
+        line["concurrent"] = concurrent_calls(a, wl, H, W, y, ws.numel(), dev)
     if not a.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, a.cpu_utts)
     print(json.dumps(line), flush=True)
     return 0
+
+
+def concurrent_calls(a, wl, H, W, y, ws_bytes: int, dev) -> dict:
+    """S host threads, each on its own stream with its own workspace and gradient buffers,
+    call the fused step `steps` times at once (inputs shared, read-only).  Aggregate frames/s
+    over the wall time of all of them, so one call's host work can hide behind another's
+    kernels."""
+    import threading
+    import torch
+    from paper_2609_33645_amd import prunedctc
+    S = a.streams
+    T, U = wl.input_lengths, wl.target_lengths
+    bufs = []
+    for _ in range(S):
+        bufs.append((prunedctc._workspace(ws_bytes, dev), torch.empty((wl.M, wl.D), dtype=torch.float32, device=dev),
+                     None if a.frozen_head else torch.empty((wl.V, wl.D), dtype=torch.float32, device=dev),
+                     torch.cuda.Stream()))
+    errors = []
+
+    def run(i, n):
+        ws, dh, dw, st = bufs[i]
+        try:
+            with torch.cuda.stream(st):
+                for _ in range(n):
+                    prunedctc.pruned_ctc_fwd_bwd(H, W, y, T, U, wl.blank, wl.beam, chunk=a.chunk,
+                                                 want_dW=not a.frozen_head, workspace=ws, dH_out=dh, dW_out=dw)
+                st.synchronize()
+        except Exception as e:  # reported below
+            errors.append(repr(e))
+
+    def together(n):
+        ts = [threading.Thread(target=run, args=(i, n)) for i in range(S)]
+        for t in ts:
+            t.start()
+        for t in ts:
+            t.join()
+
+    together(max(1, a.warmup))
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    together(a.steps)
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    if errors:
+        raise RuntimeError(f"concurrent calls failed: {errors}")
+    return {"streams": S, "calls": S * a.steps, "frames_per_s": round(S * a.steps * wl.M / dt, 1),
+            "ms_per_call": round(dt * 1e3 / a.steps, 4)}
 
 
 if __name__ == "__main__":
