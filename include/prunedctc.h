@@ -62,6 +62,7 @@ enum { PCTC_UTT_OK = 0, PCTC_UTT_NOT_ALIGNABLE = 1, PCTC_UTT_NONFINITE = 2 };
 /* Limits of this implementation. */
 #define PCTC_MAX_TARGET 1023    /* U_n (2U_n+1 lattice states per frame held in one wavefront) */
 #define PCTC_MAX_VOCAB 524288   /* V (the largest vocabulary the parity tests cover) */
+#define PCTC_MAX_DIM 1048576    /* D (the products address 256-row tiles with 32-bit byte offsets) */
 
 /* Bytes of workspace pruned_ctc_fwd_bwd needs for this batch.  Depends on N, the frame
  * and target lengths, D, the chunk width and (through the union bitmap, the vocabulary
@@ -86,7 +87,8 @@ size_t pctc_workspace_size_ex(pctc_dtype dtype, int32_t N, const int32_t* input_
 
 /* Forward and backward pass of Pruned CTC (Algorithm 1).
  *
- * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8.
+ * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8 and at
+ *          most PCTC_MAX_DIM.
  * W        [V, D] row-major, dtype (the head weight; a bias: pruned_ctc_fwd_bwd_ex).
  * targets  device int32 [sum target_lengths]: concatenated blank-free labels.
  * input_lengths, target_lengths: HOST int32 [N].

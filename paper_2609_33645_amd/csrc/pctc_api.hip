@@ -122,7 +122,7 @@ struct Layout {
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
                           float beam, int32_t chunk) {
   if (dtype != PCTC_F32 && dtype != PCTC_BF16) return PCTC_EINVAL;
-  if (N < 0 || D <= 0 || (D % 8) != 0 || V <= 1 || V > PCTC_MAX_VOCAB) return PCTC_EINVAL;
+  if (N < 0 || D <= 0 || (D % 8) != 0 || D > PCTC_MAX_DIM || V <= 1 || V > PCTC_MAX_VOCAB) return PCTC_EINVAL;
   if (beam != beam) return PCTC_EINVAL;
   if (chunk < 0 || (chunk > 0 && (chunk % 256) != 0)) return PCTC_EINVAL;
   if (N > 0 && (!T || !U)) return PCTC_EINVAL;
@@ -660,14 +660,14 @@ int32_t pctc_union_remap(const int32_t* targets, int32_t total_targets, int32_t 
 }
 
 size_t pctc_lse_scratch_bytes(int32_t M, int32_t D) {
-  return (M < 0 || D <= 0) ? 0
+  return (M < 0 || D <= 0 || D > PCTC_MAX_DIM) ? 0
                            : lse_partial_bytes(M, D) + align_up(static_cast<size_t>(M > 0 ? M : 1) * sizeof(float2), 256);
 }
 
 int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
                         const int32_t* u_ids, const int32_t* K, int32_t K_max, double* lam, float* S, int32_t ldS,
                         void* partials, void* stream_ptr) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || V <= 1 || K_max < 1 ||
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || K_max < 1 ||
       ldS < K_max || !W || !lam || !partials || (M > 0 && !H))
     return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
@@ -722,7 +722,7 @@ static size_t greedy_layout(int32_t N, int32_t M, int32_t D, size_t* o_toff, siz
 }
 
 size_t pctc_greedy_workspace_size(int32_t N, int32_t M, int32_t D) {
-  if (N < 0 || M < 0 || D <= 0) return 0;
+  if (N < 0 || M < 0 || D <= 0 || D > PCTC_MAX_DIM) return 0;
   size_t a, b;
   return greedy_layout(N, M, D, &a, &b);
 }
@@ -730,7 +730,7 @@ size_t pctc_greedy_workspace_size(int32_t N, int32_t M, int32_t D) {
 int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const void* W, const float* bias, int32_t V,
                            const int32_t* input_lengths, int32_t N, int32_t blank, int32_t* ids, int32_t* tokens,
                            int32_t* token_lengths, void* workspace, size_t workspace_bytes, void* stream_ptr) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || N < 0 || D <= 0 || D % 8 || V <= 1 || V > PCTC_MAX_VOCAB ||
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || N < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || V > PCTC_MAX_VOCAB ||
       blank < 0 || blank >= V || !W)
     return PCTC_EINVAL;
   if (N > 0 && !input_lengths) return PCTC_EINVAL;
@@ -809,14 +809,14 @@ static BwdStageLayout bwd_stage_layout(int dt, int M, int D, int V, int ldG, int
 }
 
 size_t pctc_bwd_scratch_bytes(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t ldG, int32_t chunk) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || V <= 1 || ldG < 1 || chunk < 0 ||
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D > PCTC_MAX_DIM || V <= 1 || ldG < 1 || chunk < 0 ||
       (chunk > 0 && chunk % 256))
     return 0;
   return bwd_stage_layout(dtype == PCTC_BF16 ? 1 : 0, M, D, V, ldG, chunk).total;
 }
 
 int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t chunk) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || V <= 1 || chunk < 0 ||
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D > PCTC_MAX_DIM || V <= 1 || chunk < 0 ||
       (chunk > 0 && chunk % 256))
     return 0;
   return plan_bwd(dtype == PCTC_BF16 ? 1 : 0, M, D, V, chunk).chunk;
@@ -825,7 +825,7 @@ int32_t pctc_bwd_chunk(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_
 int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, int32_t V,
                       const double* lam, const float* G, int32_t ldG, const float* g, const int32_t* remap,
                       int32_t chunk, float* dH, float* dW, void* bwd_scratch, void* stream_ptr) {
-  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || V <= 1 || chunk < 0 ||
+  if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || chunk < 0 ||
       (chunk > 0 && chunk % 256) || !W || !bwd_scratch || ldG < 1)
     return PCTC_EINVAL;
   if (M > 0 && (!H || !lam || !G || !g || !remap)) return PCTC_EINVAL;
@@ -879,7 +879,7 @@ static GroupedLayout grouped_layout(int dt, int M, int D, int V, int K, int chun
 }
 
 static bool grouped_args_ok(pctc_dtype dtype, int32_t M, int32_t D, int32_t V, int32_t K, int32_t chunk) {
-  return (dtype == PCTC_F32 || dtype == PCTC_BF16) && M >= 0 && D > 0 && D % 8 == 0 && V > 1 && K >= 1 && K <= V &&
+  return (dtype == PCTC_F32 || dtype == PCTC_BF16) && M >= 0 && D > 0 && D % 8 == 0 && D <= PCTC_MAX_DIM && V > 1 && K >= 1 && K <= V &&
          chunk >= 0 && (chunk == 0 || chunk % 256 == 0) && static_cast<int64_t>(M) * (K + 1) <= INT32_MAX;
 }
 

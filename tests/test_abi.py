@@ -52,6 +52,8 @@ def test_host_side_validation_without_gpu():
     # membership bitmap and block counts (1/8 + 1/512 bytes per class), each 256-byte aligned
     assert ws[2] - ws[0] <= (4 + 1 / 8 + 1 / 512) * (180_000 - 10_000) + 3 * 256
     assert lib.pctc_workspace_size(1, 2, p(T), p(U), 500, 1000, 16.0, 0) == 0      # D % 8 != 0
+    assert lib.pctc_workspace_size(1, 2, p(T), p(U), 1 << 20, 1000, 16.0, 0) > 0   # D = PCTC_MAX_DIM
+    assert lib.pctc_workspace_size(1, 2, p(T), p(U), (1 << 20) + 8, 1000, 16.0, 0) == 0  # D too wide
     assert lib.pctc_workspace_size(1, 2, p(T), p(U), 512, 1000, float("nan"), 0) == 0
     U2 = np.array([50, 2000], np.int32)
     assert lib.pctc_workspace_size(1, 2, p(T), p(U2), 512, 1000, 16.0, 0) == 0   # target too long
