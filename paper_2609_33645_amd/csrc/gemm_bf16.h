@@ -375,7 +375,12 @@ struct Gemm {
   // k-step: wait for this wave's copies of the next tile, barrier (the next tile is
   // visible and every wave is done reading stage S), then `issue` refills stage S and
   // the next tile's first fragments are read into f0 (stage S+1).
-  template <int S, class Issue>
+  //
+  // XTRA > 0 (run_seq_aligned): at least XTRA vector memory instructions (an epilogue's
+  // stores) were issued after the copies this wait is for, so the wait leaves that many more
+  // outstanding (the counter completes in issue order) and the stores drain under the
+  // products.
+  template <int S, int XTRA = 0, class Issue>
   __device__ static __forceinline__ void ktile(char* const (&st)[NS], int wave, int lane, f32x16 (&acc)[FR][FC],
                                                Frags& f0, Frags& f1, Issue&& issue) {
 #pragma unroll
@@ -389,7 +394,8 @@ struct Gemm {
       } else {
         constexpr int NH = PRE ? NM / 2 : 0;
         if constexpr (PRE) mma_range<0, NH>(cur, acc);
-        wait_vmcnt<(NS - 2) * CPW>();
+        static_assert((NS - 2) * CPW + XTRA < 64, "vmcnt range");
+        wait_vmcnt<(NS - 2) * CPW + XTRA>();
         __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of stage S are done
         __builtin_amdgcn_s_barrier();
         issue(st[S]);
@@ -524,6 +530,83 @@ struct Gemm {
         ktile<3 % NS>(st, wave, lane, acc, f0, f1, issue);
         after();
       }
+    }
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+  }
+
+  // run_seq for K a multiple of NS BK (every tile starts at stage 0, no padded k-tiles) with
+  // zero-initialised tiles and an epilogue that issues exactly EXTRA vector memory
+  // instructions per wave (stores; epi may use LDS outside the stages).  The first NS - 1
+  // k-tiles of the next tile wait with EXTRA more outstanding (the stores were issued after
+  // the copies those waits are for), so the stores drain under that tile's first products.
+  // The tile loop is nested with each tile's first k-tile group written out, so that the
+  // compiler, which waits on its own before reading a stage whose copy it cannot prove has
+  // landed, sees the issue order these waits rely on.
+  template <int EXTRA, class Epi>
+  __device__ static __forceinline__ void run_seq_aligned(const GOp& A, const GOp& B, int row0, int col0, int ntiles,
+                                                         int K, char* const (&st)[NS], f32x16 (&acc)[FR][FC],
+                                                         Epi&& epi) {
+    static_assert(BUF, "buffer-resource copies");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    zero(acc);
+    const int nk = K / BK;  // the caller guarantees K % (NS BK) == 0
+    if (nk <= 0 || ntiles <= 0) return;
+    const int klimA = min(A.kmax, K), klimB = min(B.kmax, K);
+    CA ca;
+    CB cb;
+    ca.init(A, row0, wave, lane, 0, klimA);
+    cb.init(B, col0, wave, lane, 0, klimB);
+    int ctile = 0, ck = 0;  // copy stream position
+    auto issue = [&](char* stage) {
+      if (ck == nk) {
+        ck = 0;
+        ++ctile;
+        ca.retarget(A, row0 + ctile * BR, wave, lane);
+      }
+      const bool live = ctile < ntiles;
+      ca.issue(A, ck * BK, live ? klimA : 0, stage, wave);
+      cb.issue(B, ck * BK, live ? klimB : 0, stage + kABytes, wave);
+      ++ck;
+    };
+    __builtin_amdgcn_s_barrier();
+#pragma unroll
+    for (int s = 0; s < NS; ++s) issue(st[s]);
+    wait_vmcnt<(NS - 1) * CPW>();
+    __builtin_amdgcn_s_barrier();
+    Frags f0, f1;
+    load(st[0], 0, wave, lane, f0);
+    const int ng = nk / NS;
+    auto group = [&]() {
+      ktile<0>(st, wave, lane, acc, f0, f1, issue);
+      ktile<1 % NS>(st, wave, lane, acc, f0, f1, issue);
+      if constexpr (NS >= 3) ktile<2 % NS>(st, wave, lane, acc, f0, f1, issue);
+      if constexpr (NS >= 4) ktile<3 % NS>(st, wave, lane, acc, f0, f1, issue);
+    };
+    auto relaxed_group = [&]() {
+      ktile<0, EXTRA>(st, wave, lane, acc, f0, f1, issue);
+      if constexpr (NS == 2) {
+        ktile<1>(st, wave, lane, acc, f0, f1, issue);
+      } else {
+        ktile<1, EXTRA>(st, wave, lane, acc, f0, f1, issue);
+        if constexpr (NS == 3) ktile<2>(st, wave, lane, acc, f0, f1, issue);
+        if constexpr (NS >= 4) {
+          ktile<2, EXTRA>(st, wave, lane, acc, f0, f1, issue);
+          ktile<3>(st, wave, lane, acc, f0, f1, issue);
+        }
+      }
+    };
+    group();
+    for (int gi = 1; gi < ng; ++gi) group();
+    epi(0, acc);
+    zero(acc);
+    for (int t = 1; t < ntiles; ++t) {
+      relaxed_group();
+      for (int gi = 1; gi < ng; ++gi) group();
+      epi(t, acc);
+      zero(acc);
     }
     wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt(0xC07F);

@@ -44,6 +44,7 @@ using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 // run, so one workgroup per CU still keeps the matrix pipe fed across tile boundaries)
 using GMid = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4, true>;
 constexpr int kMidRun = 8;
+constexpr int kRcCus = 224;  // workgroups of the dense recompute (one round)
 // the union-column part's dH product: 4-wave tiles (two workgroups per CU), so that its
 // workgroups find room beside a recompute's
 using GUh = bf::Gemm<256, 128, 32, LL::KC, LL::MC, 3, 2, 2>;
@@ -521,6 +522,89 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
     }
     if (tid < TR) dbpart[static_cast<int64_t>(mt) * chunk + vl0 + tid] = dbsum;
   }
+}
+
+// The dense part -g p of one chunk (no bias, no db, no union columns) on the normaliser's
+// 8-wave 256 x 256 tiles, `run` vocabulary tiles per workgroup: the copy pipeline runs
+// through the run, so the next tile's copies land while this tile's epilogue runs.  The
+// epilogue needs no barrier: each wave stages its own 64-vocabulary x 32-frame blocks (four
+// per tile) through a private 4 KB LDS buffer (16-byte slots XOR-swizzled by frame) and
+// writes 128 contiguous bytes per frame row with buffer stores.  The stores always issue
+// (frames past M fall outside the resource, which drops them), so the copy pipeline can
+// count them and leave them in flight under the next tile's first products.
+constexpr int kRcStores = 16;  // buffer stores per wave per tile
+
+__global__ void __launch_bounds__(512, 1)
+recompute_run_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
+                   int run, const float2* __restrict__ lam2, const float* __restrict__ g, uint16_t* __restrict__ dZ,
+                   int chunk) {
+  using G = GMid;
+  constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
+  static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
+  PCTC_STAGES_G(G)
+  __shared__ __attribute__((aligned(1024))) char stg_[G::NW * 4096];
+  const int nMt = (M + TC - 1) / TC;
+  const int nVt = (cw + TR - 1) / TR;
+  // all frame tiles of a vocabulary run consecutive on one XCD (it fetches the run's W rows once)
+  const int w = xcd_swz(blockIdx.x, gridDim.x);
+  const int mt = w % nMt;
+  const int vt0 = (w / nMt) * run;
+  if (vt0 >= nVt) return;
+  const int ntiles = min(run, nVt - vt0);
+  const int m0 = mt * TC;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wr = wave / (G::NW / 2), wc = wave % (G::NW / 2);
+  // -g_m p = -sign(g_m) 2^(z log2(e) - (lambda_m log2(e) - log2|g_m|)), as in recompute_dz_bf16
+  float ll[FC];
+  uint32_t sg[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    const int m = m0 + G::col_of(wave, lane, j);
+    const float gm = (m < M) ? g[m] : 0.f;
+    const float2 l2 = (m < M) ? lam2[m] : make_float2(0.f, 0.f);
+    ll[j] = (gm != 0.f) ? (l2.x + l2.y) - fast_log2(fabsf(gm)) : INFINITY;
+    sg[j] = (gm > 0.f) ? 0x80008000u : 0u;
+  }
+  const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
+  const GOp B{Hs, D, M, D, nullptr};
+  // store resource: this frame tile's rows of dZ (byte offsets < 256 rows x 2 chunk)
+  const uint64_t zb = reinterpret_cast<uint64_t>(dZ + static_cast<int64_t>(m0) * chunk);
+  const uint64_t zbu = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(zb >> 32))) << 32) |
+                       static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(zb)));
+  const int zsize = __builtin_amdgcn_readfirstlane(min(M - m0, TC) * chunk * 2);
+  const __amdgpu_buffer_rsrc_t zr =
+      __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(zbu), static_cast<short>(0), zsize, bf::kBufWord3);
+  char* const stg = stg_ + wave * 4096;
+  const int rf = lane & 31, hl = lane >> 5;
+  f32x16 acc[FR][FC];
+  auto epi = [&](int it, f32x16 (&a)[FR][FC]) {
+    const int vb = (vt0 + it) * TR + (TR / 2) * wr;  // this wave's first vocabulary column in the chunk
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {  // frames 32 j.. of the wave, vocabulary blocks ib, ib + 1
+      const int j = h >> 1, ib = 2 * (h & 1);
+#pragma unroll
+      for (int il = 0; il < 2; ++il)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          float v[4];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] = fast_exp2(fmaf(a[ib + il][j][4 * q + e], kLog2e, -ll[j]));
+          const int c = 32 * il + 8 * q + 4 * hl;  // 4 consecutive vocabulary columns of frame rf
+          const int off = rf * 128 + (((c >> 3) ^ (rf & 7)) << 4) + (((c >> 2) & 1) << 3);
+          *reinterpret_cast<u32x2*>(stg + off) = u32x2{pack_bf16x2(v[0], v[1]) ^ sg[j], pack_bf16x2(v[2], v[3]) ^ sg[j]};
+        }
+#pragma unroll
+      for (int t = 0; t < 4; ++t) {  // lanes 8 f.. 8 f + 7 take frame row f + 8 t
+        const int f = (lane >> 3) + 8 * t, slot = lane & 7;
+        const u32x4 val = *reinterpret_cast<const u32x4*>(stg + f * 128 + ((slot ^ (f & 7)) << 4));
+        const int row = 64 * wc + 32 * j + f;  // frame within the tile
+        const uint32_t off = static_cast<uint32_t>(row * chunk + vb + 64 * (h & 1) + 8 * slot) * 2u;
+        __builtin_amdgcn_raw_buffer_store_b128(val, zr, off, 0, 2 /* nt: read back only by dH and dW */);
+      }
+    }
+  };
+  G::template run_seq_aligned<kRcStores>(A, B, vt0 * TR, m0, ntiles, D, st, acc, epi);
 }
 
 // db[c0 + v] = sum over frame tiles of dbpart[t][v], v < cw (fixed order).
@@ -1008,6 +1092,16 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
   }
     if (wide) {
       PCTC_RECOMPUTE_CFG(GWide, 1)
+    } else if (!bias && !db && !remap && D % (GMid::kNS * GMid::KK * 16) == 0) {
+      // one round of workgroups (one per CU, 256 x 256 tiles), each taking a run of vocabulary
+      // tiles for one frame tile; kRcCus workgroups at most, so that the second stream's
+      // lattice and union work keeps a few CUs of every XCD beside them
+      const int nMt2 = (M + GMid::kBC - 1) / GMid::kBC;
+      const int runs = max(1, min(nVt, kRcCus / nMt2));
+      const int run = (nVt + runs - 1) / runs;
+      const int nruns = (nVt + run - 1) / run;
+      hipLaunchKernelGGL(recompute_run_bf16, dim3(nMt2 * nruns), dim3(GMid::kThreads), 0, stream, Hs, M, D, W, c0,
+                         cw, run, lam2, g, dZ, chunk);
     } else {
       PCTC_RECOMPUTE_CFG(GFwd, 2)
     }
