@@ -149,7 +149,8 @@ template <int PER>  // partitions per lane held in registers: P <= 16 PER
 __global__ void __launch_bounds__(256)
 lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* __restrict__ lam,
                     float2* __restrict__ lam2, const double* __restrict__ Zd, const int32_t* __restrict__ Kdev,
-                    float* __restrict__ S, int ldS) {
+                    float* __restrict__ S, int ldS, const float* __restrict__ g, float* __restrict__ rowscale,
+                    int32_t* __restrict__ einv) {
   const int ph = threadIdx.x & 15;
   const int m = blockIdx.x * kFinFrames + (threadIdx.x >> 4);
   const bool live = m < M;
@@ -188,6 +189,10 @@ lse_finalize_kernel(const float2* __restrict__ partials, int M, int P, double* _
     const double l2 = l * kLog2eD;
     const float hi = static_cast<float>(l2);
     lam2[m] = make_float2(hi, static_cast<float>(l2 - static_cast<double>(hi)));
+    if (g) {
+      if (!(l >= kEMin && l <= kEMax)) atomicOr(einv, 1);
+      rowscale[m] = static_cast<float>(-static_cast<double>(g[m]) * exp(-l));
+    }
   }
   if (Zd) {
     const int K = *Kdev;
@@ -272,16 +277,18 @@ hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const voi
 }
 
 hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
-                               const int32_t* K, float* S, int ldS, hipStream_t stream) {
+                               const int32_t* K, float* S, int ldS, hipStream_t stream, const float* g,
+                               float* rowscale, int32_t* einv) {
   if (M <= 0) return hipSuccess;
   if (P < 1 || P > kMaxLseParts) return hipErrorInvalidValue;
   Prof pr("lse_finalize", stream);
   const dim3 grid((M + kFinFrames - 1) / kFinFrames);
   if (P <= 256)
-    hipLaunchKernelGGL(lse_finalize_kernel<16>, grid, dim3(256), 0, stream, partials, M, P, lam, lam2, Zd, K, S, ldS);
+    hipLaunchKernelGGL(lse_finalize_kernel<16>, grid, dim3(256), 0, stream, partials, M, P, lam, lam2, Zd, K, S, ldS,
+                       g, rowscale, einv);
   else
     hipLaunchKernelGGL(lse_finalize_kernel<kMaxLseParts / 16>, grid, dim3(256), 0, stream, partials, M, P, lam, lam2,
-                       Zd, K, S, ldS);
+                       Zd, K, S, ldS, g, rowscale, einv);
   return hipGetLastError();
 }
 
@@ -715,6 +722,16 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
     const size_t n = (v + cmax - 1) / cmax;
     size_t c = ((v + n - 1) / n + 255) / 256 * 256;
     if (c > cmax) c = cmax;
+    if (dtype == 1 && D < kWideD) {
+      // narrow bf16 heads: whole normaliser partitions (kEAlign columns), so that the first
+      // chunk's dZ rows can come from the normaliser (lse_partial_e_bf16)
+      size_t n2 = n, c2 = ((v + n2 - 1) / n2 + kEAlign - 1) / kEAlign * kEAlign;
+      while (c2 > cmax && c2 > static_cast<size_t>(kEAlign)) {
+        ++n2;
+        c2 = ((v + n2 - 1) / n2 + kEAlign - 1) / kEAlign * kEAlign;
+      }
+      if (c2 <= cmax) c = c2;
+    }
     p.chunk = static_cast<int>(c);
     cap = static_cast<int>(cmax);
   }
@@ -861,10 +878,11 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   for (int c0 = 0; c0 < V; c0 += chunk, ++ci) {
     const int cw = min(chunk, V - c0);
     const bool last = c0 + chunk >= V;
+    const ChunkE* ce = (c0 == 0 && side) ? side->ce : nullptr;
     if (last && two && dH) {
       // the last chunk's dW product runs beside the final dH reduction (second stream)
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                true, true, false, dW, db, dbpart, stream);
+                                true, true, false, dW, db, dbpart, stream, nullptr, ce);
       if (e != hipSuccess) return e;
       if ((e = start_side(nwork)) != hipSuccess) return e;
       if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
@@ -882,12 +900,12 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
         const DwExtra* udw = side->udw.Z ? &side->udw : nullptr;
         if (udw && (e = hipStreamWaitEvent(stream, udw->ready, 0)) != hipSuccess) return e;
         e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                  false, false, true, dW, db, dbpart, stream, udw);
+                                  false, false, true, dW, db, dbpart, stream, udw, ce);
         if (e != hipSuccess) return e;
       }
     } else {
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream);
+                                true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream, nullptr, ce);
       if (e != hipSuccess) return e;
       if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
     }

@@ -45,6 +45,7 @@ using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 using GMid = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4, true>;
 constexpr int kMidRun = 8;
 constexpr int kRcCus = 224;  // workgroups of the dense recompute (one round)
+constexpr int kRcStores = 16;  // buffer stores per wave per 256 x 256 tile (recompute, E)
 // the union-column part's dH product: 4-wave tiles (two workgroups per CU), so that its
 // workgroups find room beside a recompute's
 using GUh = bf::Gemm<256, 128, 32, LL::KC, LL::MC, 3, 2, 2>;
@@ -161,6 +162,37 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
   char* const stx_[4] = {st0_, st1_, st2_, st3_};                                           \
   char* const(&st)[G::kNS] = *reinterpret_cast<char* const(*)[G::kNS]>(&stx_);
 
+// The two wavefronts of each frame column (row halves) combine their running (max, sum)
+// pairs through LDS (xch: any drained stage) and write the partition's pair of every frame.
+template <class G>
+__device__ __forceinline__ void lse_store_partials(const float (&run_max)[G::FC], const float (&run_sum)[G::FC],
+                                                   char* xchb, int wave, int lane, int m0, int M,
+                                                   float2* __restrict__ out) {
+  constexpr int FC = G::FC;
+  __syncthreads();
+  constexpr int WC = G::NW / 2;  // column groups (the wave grid is 2 x WC)
+  float2* xch = reinterpret_cast<float2*>(xchb);
+  const int rowhalf = wave / WC, colq = wave % WC;
+  if (rowhalf == 1 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) xch[colq * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
+  }
+  __syncthreads();
+  if (rowhalf == 0 && lane < 32) {
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const float2 o = xch[colq * (FC * 32) + j * 32 + lane];
+      const float nmax = fmaxf(run_max[j], o.x);
+      float s = 0.f;
+      if (run_max[j] != -INFINITY) s += run_sum[j] * fast_exp2((run_max[j] - nmax) * kLog2e);
+      if (o.x != -INFINITY) s += o.y * fast_exp2((o.x - nmax) * kLog2e);
+      if (nmax != nmax) s = nmax;
+      const int m = m0 + G::col_of(wave, lane, j);
+      if (m < M) out[m] = make_float2(nmax, s);
+    }
+  }
+}
+
 template <class G, bool BIAS, int OCC>
 __global__ void __launch_bounds__(G::kThreads, OCC)
 lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, const float* __restrict__ bias,
@@ -205,29 +237,137 @@ lse_partial_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* _
     });
   else
     G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
-  __syncthreads();
-  // the two wavefronts of each frame column (row halves) combine their partial sums
-  constexpr int WC = G::NW / 2;  // column groups (the wave grid is 2 x WC)
-  float2* xch = reinterpret_cast<float2*>(st0_);
-  const int rowhalf = wave / WC, colq = wave % WC;
-  if (rowhalf == 1 && lane < 32) {
+  lse_store_partials<G>(run_max, run_sum, st0_, wave, lane, m0, M, partials + static_cast<int64_t>(p) * M);
+}
+
+// Log-sum-exp update of one frame column of an E tile (lse_partial_e_bf16) with the pair
+// (0, s): s is this lane's sum of exp(z) over its rows, the other lane half's rows are added
+// here; when the tile's sum leaves [2^-100, 2^100] the maximum-based update is taken on the
+// same logits instead (the decision is the same on both lane halves).
+template <int FR, int FC>
+__device__ __forceinline__ void lse_e_update(const f32x16 (&a)[FR][FC], int j, float s, float& run_max,
+                                             float& run_sum) {
+  float sj = s + swap_halves(s);
+  float mj = 0.f;
+  if (!(sj >= 0x1p-100f && sj <= 0x1p100f)) {
+    float tmax = -INFINITY;
 #pragma unroll
-    for (int j = 0; j < FC; ++j) xch[colq * (FC * 32) + j * 32 + lane] = make_float2(run_max[j], run_sum[j]);
-  }
-  __syncthreads();
-  if (rowhalf == 0 && lane < 32) {
+    for (int i = 0; i < FR; ++i)
 #pragma unroll
-    for (int j = 0; j < FC; ++j) {
-      const float2 o = xch[colq * (FC * 32) + j * 32 + lane];
-      const float nmax = fmaxf(run_max[j], o.x);
-      float s = 0.f;
-      if (run_max[j] != -INFINITY) s += run_sum[j] * fast_exp2((run_max[j] - nmax) * kLog2e);
-      if (o.x != -INFINITY) s += o.y * fast_exp2((o.x - nmax) * kLog2e);
-      if (nmax != nmax) s = nmax;
-      const int m = m0 + G::col_of(wave, lane, j);
-      if (m < M) partials[static_cast<int64_t>(p) * M + m] = make_float2(nmax, s);
-    }
+      for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, a[i][j][r]);
+    tmax = fmaxf(tmax, swap_halves(tmax));
+    const float ms = (tmax == -INFINITY) ? 0.f : tmax * kLog2e;
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < FR; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) t += fast_exp2(fmaf(a[i][j][r], kLog2e, -ms));
+    sj = t + swap_halves(t);
+    mj = tmax;
   }
+  const float nmax = fmaxf(run_max, mj);
+  float acc_s = 0.f;
+  if (run_max != -INFINITY) acc_s += run_sum * fast_exp2((run_max - nmax) * kLog2e);
+  if (mj != -INFINITY) acc_s += sj * fast_exp2((mj - nmax) * kLog2e);
+  run_sum = acc_s;
+  run_max = nmax;
+}
+
+// The normaliser of a narrow head (8-wave 256 x 256 tiles, no bias) that also writes, for the
+// vocabulary rows of the first eparts partitions (the backward's first chunk), E = exp(z) in
+// bf16 into the gradient buffer, laid out like dZ (E[m * epitch + v]); the backward then needs
+// no recompute for that chunk: its dense part -g_m p_v(m) = s_m E[m][v] with the per-frame
+// scale s_m = -g_m exp(-lambda_m) (hs_scale_bf16).  On those partitions the log-sum-exp is
+// taken on the same exponentials with 0 as the reference instead of the running maximum
+// (the pair (0, sum exp z) is exact as long as the sum stays in range; a column whose tile
+// sum leaves [2^-100, 2^100] takes the maximum-based update instead).  E itself is usable
+// when every lambda_m lies in [kEMin, kEMax] (no bf16 overflow, no significant underflow); the
+// finalize checks that and the backward recomputes the chunk otherwise.  E partitions run the
+// aligned tile sequence (the stores drain under the next tile's products); the others run
+// exactly like lse_partial_bf16.  einv (the check flag) is cleared here, before the finalize
+// sets it.
+__global__ void __launch_bounds__(512, 1)
+lse_partial_e_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int V, int P,
+                   int vper, float2* __restrict__ partials, uint16_t* __restrict__ E, int epitch, int eparts,
+                   int32_t* __restrict__ einv) {
+  using G = GMid;
+  constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
+  static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
+  PCTC_STAGES_G(G)
+  __shared__ __attribute__((aligned(1024))) char stg_[G::NW * 4096];
+  const int nMt = (M + TC - 1) / TC;
+  const int w = xcd_swz(blockIdx.x, gridDim.x);
+  const int mt = w % nMt;
+  const int p = w / nMt;
+  if (blockIdx.x == 0 && threadIdx.x == 0) *einv = 0;
+  if (p >= P) return;
+  const int m0 = mt * TC;
+  const int vbeg = p * vper;
+  const int vend = min(V, vbeg + vper);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int ntiles = (vend - vbeg + TR - 1) / TR;
+  const GOp A{W, D, vend, D, nullptr};
+  const GOp B{H, D, M, D, nullptr};
+  float run_max[FC], run_sum[FC];
+#pragma unroll
+  for (int j = 0; j < FC; ++j) {
+    run_max[j] = -INFINITY;
+    run_sum[j] = 0.f;
+  }
+  f32x16 acc[FR][FC];
+  if (p >= eparts) {
+    auto epi = [&](int i, f32x16 (&a)[FR][FC]) {
+      const int v0 = vbeg + i * TR;
+      if (v0 + TR > vend) mask_rows_inf<FR, FC, G>(a, v0, vend, wave, lane);
+      lse_tile_update<FR, FC, G>(a, run_max, run_sum);
+    };
+    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
+  } else {
+    const int wr = wave / (G::NW / 2), wc = wave % (G::NW / 2);
+    const uint64_t zb = reinterpret_cast<uint64_t>(E + static_cast<int64_t>(m0) * epitch);
+    const uint64_t zbu =
+        (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(zb >> 32))) << 32) |
+        static_cast<uint32_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(zb)));
+    const int zsize = __builtin_amdgcn_readfirstlane(min(M - m0, TC) * epitch * 2);
+    const __amdgpu_buffer_rsrc_t zr = __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(zbu),
+                                                                       static_cast<short>(0), zsize, bf::kBufWord3);
+    char* const stg = stg_ + wave * 4096;
+    const int rf = lane & 31, hl = lane >> 5;
+    auto epi = [&](int it, f32x16 (&a)[FR][FC]) {
+      const int v0 = vbeg + it * TR;
+      if (v0 + TR > vend) mask_rows_inf<FR, FC, G>(a, v0, vend, wave, lane);
+      const int vb = v0 + (TR / 2) * wr;  // this wave's first vocabulary row
+      float s[FC] = {0.f, 0.f};
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {  // frames 32 j.. of the wave, vocabulary blocks ib, ib + 1
+        const int j = h >> 1, ib = 2 * (h & 1);
+#pragma unroll
+        for (int il = 0; il < 2; ++il)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            float v[4];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) v[e] = fast_exp2(a[ib + il][j][4 * q + e] * kLog2e);
+            s[j] += (v[0] + v[1]) + (v[2] + v[3]);
+            const int c = 32 * il + 8 * q + 4 * hl;
+            const int off = rf * 128 + (((c >> 3) ^ (rf & 7)) << 4) + (((c >> 2) & 1) << 3);
+            *reinterpret_cast<u32x2*>(stg + off) = u32x2{pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3])};
+          }
+#pragma unroll
+        for (int t = 0; t < 4; ++t) {
+          const int f = (lane >> 3) + 8 * t, slot = lane & 7;
+          const u32x4 val = *reinterpret_cast<const u32x4*>(stg + f * 128 + ((slot ^ (f & 7)) << 4));
+          const int row = 64 * wc + 32 * j + f;
+          const uint32_t off = static_cast<uint32_t>(row * epitch + vb + 64 * (h & 1) + 8 * slot) * 2u;
+          __builtin_amdgcn_raw_buffer_store_b128(val, zr, off, 0, 2 /* nt: read back only by dH and dW */);
+        }
+        if (h & 1) lse_e_update(a, j, s[j], run_max[j], run_sum[j]);  // column j's logits are done with
+      }
+    };
+    G::template run_seq_aligned<kRcStores>(A, B, vbeg, m0, ntiles, D, st, acc, epi);
+  }
+  lse_store_partials<G>(run_max, run_sum, st0_, wave, lane, m0, M, partials + static_cast<int64_t>(p) * M);
 }
 
 // ---------------------------------------------------------------------------------------
@@ -532,12 +672,13 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
 // writes 128 contiguous bytes per frame row with buffer stores.  The stores always issue
 // (frames past M fall outside the resource, which drops them), so the copy pipeline can
 // count them and leave them in flight under the next tile's first products.
-constexpr int kRcStores = 16;  // buffer stores per wave per tile
 
 __global__ void __launch_bounds__(512, 1)
 recompute_run_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
                    int run, const float2* __restrict__ lam2, const float* __restrict__ g, uint16_t* __restrict__ dZ,
-                   int chunk) {
+                   int chunk, const int32_t* __restrict__ only_if) {
+  // only_if (the normaliser's E check flag): recompute only when its E cannot be used
+  if (only_if && *only_if == 0) return;
   using G = GMid;
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
@@ -658,7 +799,8 @@ static int dh_xcd_rows(int M, int D) {
 template <class G, int OCC>
 __global__ void __launch_bounds__(G::kThreads, OCC)
 dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* __restrict__ W, int D, int c0, int cw,
-             int slice, float* __restrict__ part, int gm, int accumulate, const int32_t* __restrict__ kdev) {
+             int slice, float* __restrict__ part, int gm, int accumulate, const int32_t* __restrict__ kdev,
+             const float* __restrict__ rowscale) {
   // the first chunk writes its slices; later chunks (and an accumulating call) add to them
   const bool first = c0 == 0 && !accumulate;
   if (kdev) cw = min(cw, 2 * *kdev);  // union columns: [hi | lo] of the K classes the device found
@@ -705,7 +847,9 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int m = m0 + G::row_of(wave, lane, i, r);
-        if (m < M) dst[static_cast<int64_t>(m) * D + d] = acc[i][j][r];
+        // rowscale (a first chunk only, whose partial sums start at zero): dZ rows were
+        // written without their per-frame factor
+        if (m < M) dst[static_cast<int64_t>(m) * D + d] = rowscale ? acc[i][j][r] * rowscale[m] : acc[i][j][r];
       }
     }
 }
@@ -775,6 +919,30 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
   u32x4 v = *reinterpret_cast<const u32x4*>(H + i);
   if (g[m] == 0.f) v = u32x4{0u, 0u, 0u, 0u};
   *reinterpret_cast<u32x4*>(Hs + i) = v;
+}
+
+// Hp = s_m Hs (bf16) for the dW product of the chunk whose dZ rows hold the normaliser's
+// E = exp(z): its dense part is s_m E[m][v] with s_m = -g_m exp(-lambda_m) (rowscale, written
+// by the finalize).  When the finalize's check failed (*einv: E unusable, the chunk is
+// recomputed with its factor), Hp = Hs and rowscale = 1.
+__global__ void hs_scale_bf16(const uint16_t* __restrict__ Hs, int64_t n, int D, const int32_t* __restrict__ einv,
+                              float* __restrict__ rowscale, uint16_t* __restrict__ Hp) {
+  const int64_t i = (static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x) * 8;
+  if (i >= n) return;
+  const int m = static_cast<int>(i / D);
+  const u32x4 v = *reinterpret_cast<const u32x4*>(Hs + i);
+  if (*einv != 0) {
+    if (i % D == 0) rowscale[m] = 1.f;  // no other thread reads it on this branch
+    *reinterpret_cast<u32x4*>(Hp + i) = v;
+    return;
+  }
+  const float sm = rowscale[m];
+  u32x4 o;
+#pragma unroll
+  for (int k = 0; k < 4; ++k)
+    o[k] = pack_bf16x2(bf16_to_f32(static_cast<uint16_t>(v[k] & 0xffffu)) * sm,
+                       bf16_to_f32(static_cast<uint16_t>(v[k] >> 16)) * sm);
+  *reinterpret_cast<u32x4*>(Hp + i) = o;
 }
 
 // ---------------------------------------------------------------------------------------
@@ -933,7 +1101,7 @@ hipError_t launch_union_part_bf16(const float* G, int ldG, const int32_t* Kdev, 
       const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
       Prof pr("union_dh", stream);
       hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0,
-                         k2, k2, dH, dh_xcd_rows(M, D), 0, Kdev);
+                         k2, k2, dH, dh_xcd_rows(M, D), 0, Kdev, nullptr);
     }
   }
   if (want_dW && !dw_elsewhere) {
@@ -961,7 +1129,7 @@ hipError_t launch_union_dh_bf16(const uint16_t* Gb, const int32_t* Kdev, int K_m
   const int tiles = ((M + GUh::kBR - 1) / GUh::kBR) * ((D + GUh::kBC - 1) / GUh::kBC);
   Prof pr("union_dh", stream);
   hipLaunchKernelGGL((dh_gemm_bf16<GUh, 2>), dim3(tiles), dim3(GUh::kThreads), 0, stream, Gb, M, k2, WU2, D, 0, k2,
-                     k2, dH, dh_xcd_rows(M, D), 1, Kdev);
+                     k2, dH, dh_xcd_rows(M, D), 1, Kdev, nullptr);
   return hipGetLastError();
 }
 
@@ -1069,7 +1237,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
-                                 float* dbpart, hipStream_t stream, const DwExtra* extra) {
+                                 float* dbpart, hipStream_t stream, const DwExtra* extra, const ChunkE* ce) {
   // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue);
   // narrow heads: two 4-wave 256 x 128 workgroups per CU, so that one's epilogue (exp, pack,
   // staged stores: VALU-bound) overlaps the other's products
@@ -1092,7 +1260,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
   }
     if (wide) {
       PCTC_RECOMPUTE_CFG(GWide, 1)
-    } else if (!bias && !db && !remap && D % (GMid::kNS * GMid::KK * 16) == 0) {
+    } else if (ce || (!bias && !db && !remap && D % (GMid::kNS * GMid::KK * 16) == 0)) {
       // one round of workgroups (one per CU, 256 x 256 tiles), each taking a run of vocabulary
       // tiles for one frame tile; kRcCus workgroups at most, so that the second stream's
       // lattice and union work keeps a few CUs of every XCD beside them
@@ -1101,7 +1269,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
       const int run = (nVt + runs - 1) / runs;
       const int nruns = (nVt + run - 1) / run;
       hipLaunchKernelGGL(recompute_run_bf16, dim3(nMt2 * nruns), dim3(GMid::kThreads), 0, stream, Hs, M, D, W, c0,
-                         cw, run, lam2, g, dZ, chunk);
+                         cw, run, lam2, g, dZ, chunk, ce ? ce->einv : nullptr);
     } else {
       PCTC_RECOMPUTE_CFG(GFwd, 2)
     }
@@ -1117,7 +1285,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     const int ns = (cw + slice - 1) / slice;
     Prof pr("dh_gemm", stream);
     hipLaunchKernelGGL((dh_gemm_bf16<GDh, 1>), dim3(tiles * ns), dim3(GDh::kThreads), 0, stream, dZ, M, chunk, W, D,
-                       c0, cw, slice, part, dh_xcd_rows(M, D), 0, nullptr);
+                       c0, cw, slice, part, dh_xcd_rows(M, D), 0, nullptr, ce ? ce->rowscale : nullptr);
   }
   if (want_dW) {
     const int nDt = (D + kBC - 1) / kBC;
@@ -1130,8 +1298,39 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
       tiles1 = ((extra->cols + kBR - 1) / kBR) * nDt;
     }
     Prof pr("dw_gemm", stream);
-    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles0 + tiles1), dim3(GDw::kThreads), 0, stream, p0, p1, tiles0, Hs, M, D);
+    hipLaunchKernelGGL(dw_gemm_bf16, dim3(tiles0 + tiles1), dim3(GDw::kThreads), 0, stream, p0, p1, tiles0,
+                       ce ? ce->Hp : Hs, M, D);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_hs_scale_bf16(const uint16_t* Hs, int M, int D, const int32_t* einv, float* rowscale, uint16_t* Hp,
+                                hipStream_t stream) {
+  const int64_t n = static_cast<int64_t>(M) * D;
+  const int64_t threads = (n + 7) / 8;
+  if (threads <= 0) return hipSuccess;
+  Prof pr("hs_scale", stream);
+  hipLaunchKernelGGL(hs_scale_bf16, dim3(static_cast<unsigned>((threads + 255) / 256)), dim3(256), 0, stream, Hs, n, D,
+                     einv, rowscale, Hp);
+  return hipGetLastError();
+}
+
+int lse_e_parts_bf16(int M, int D, int V, int chunk) {
+  if (M <= 0 || D >= kWideD || D % (GMid::kNS * GMid::KK * 16) != 0 || chunk <= 0) return 0;
+  const LseSplit sp = lse_split_bf16(M, D, V);
+  if (chunk % sp.vper != 0) return 0;
+  const int ep = chunk / sp.vper;
+  return ep < sp.P ? ep : sp.P;
+}
+
+hipError_t launch_lse_partial_e_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
+                                     int* P_out, uint16_t* E, int epitch, int eparts, int32_t* einv,
+                                     hipStream_t stream) {
+  const LseSplit sp = lse_split_bf16(M, D, V);
+  *P_out = sp.P;
+  Prof pr("lse_partial", stream);
+  hipLaunchKernelGGL(lse_partial_e_bf16, dim3(sp.nM * sp.P), dim3(GMid::kThreads), 0, stream, H, M, D, W, V, sp.P,
+                     sp.vper, partials, E, epitch, eparts, einv);
   return hipGetLastError();
 }
 

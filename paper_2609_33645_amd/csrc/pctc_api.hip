@@ -117,6 +117,10 @@ struct Layout {
   BwdPlan bwd;
   size_t o_remap, o_ubits, o_uids, o_yrel, o_small, o_status, o_lossn, o_part, o_lam, o_lam2, o_S, o_G, o_g, o_gpred, o_pred,
       o_corr, o_dp, o_bwd, o_zd, total;
+  // narrow bf16 heads: partitions of the normaliser that write the first chunk's E (0: none),
+  // the per-frame factors and the scaled H of that chunk's dW product
+  int eparts;
+  size_t o_escale, o_hp;
 };
 
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
@@ -140,8 +144,9 @@ static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const i
 }
 
 // want_dW: the call asks for dW (the union columns' dW_u slices are only needed then).
+// allow_e: the layout may serve the two-stream schedule (room for the normaliser's E chunk).
 static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
-                          float beam, int32_t chunk, bool want_dW = true) {
+                          float beam, int32_t chunk, bool want_dW = true, bool allow_e = true) {
   Layout L{};
   L.N = N;
   L.dp = plan_dp(N, T, U, beam);
@@ -179,15 +184,22 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   }
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
+  L.eparts = (dtype == PCTC_BF16 && allow_e) ? lse_e_parts_bf16(L.M, D, V, L.bwd.chunk) : 0;
+  size_t e_bytes = 0;  // the first chunk's E rows, written by the normaliser
+  if (L.eparts > 0) {
+    e_bytes = align_up(static_cast<size_t>(L.M) * L.bwd.chunk * 2, 256);
+    L.o_escale = take(static_cast<size_t>(L.M) * 4);
+    L.o_hp = take(static_cast<size_t>(L.M) * D * 2);
+  }
   // The selected logits in double [M][ldS] (bf16 path) and the normaliser's partial pairs are
   // dead once lambda and S are formed, before the first recompute writes the gradient buffer:
-  // they live in that buffer when it is large enough.
-  size_t lent = 0;
+  // they live in that buffer (past the E rows) when it is large enough.
+  size_t lent = e_bytes;
   if (dtype == PCTC_BF16) {
     const size_t need = static_cast<size_t>(L.M) * L.ldS * sizeof(double);
-    if (L.bwd.dz_bytes >= need) {
-      L.o_zd = L.o_bwd;
-      lent = align_up(need, 256);
+    if (L.bwd.dz_bytes >= lent + need) {
+      L.o_zd = L.o_bwd + lent;
+      lent += align_up(need, 256);
     } else {
       L.o_zd = take(need);
     }
@@ -391,6 +403,13 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   const bool want_bwd = (dH || dW || db);
   int32_t* fflag = Kdev + 2;  // forecast mismatch flag
   const bool overlap = two_streams && (dt == 1) && want_bwd && L.M > 0 && N > 0;
+  // the normaliser writes the first chunk's dZ rows as E = exp(z) (dense part only: no bias,
+  // no db); einv: its range check, rowscale (escale) and Hp: that chunk's factors
+  const bool use_e = overlap && L.eparts > 0 && !bias && !db && (dH || dW);
+  int32_t* einv = Kdev + 3;
+  float* escale = use_e ? reinterpret_cast<float*>(ws + L.o_escale) : nullptr;
+  ChunkE chunk_e;
+  if (use_e) chunk_e = ChunkE{escale, reinterpret_cast<const uint16_t*>(ws + L.o_hp), einv};
   hipStream_t dps_stream = stream;
   struct Events {
     hipEvent_t start = nullptr, sel = nullptr, fork = nullptr, gate0 = nullptr, gate1 = nullptr, dh_done = nullptr,
@@ -416,7 +435,12 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // online full-vocabulary log-sum-exp, launched first: it is the longest step (the
     // second stream's wait on the work before it is enqueued after this launch)
     int P = 0;
-    PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    if (use_e)  // also E = exp(z) for the backward's first chunk, into the gradient buffer
+      PCTC_HIP(launch_lse_partial_e_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), V,
+                                         partials, &P, reinterpret_cast<uint16_t*>(bws), L.bwd.chunk, L.eparts, einv,
+                                         stream));
+    else
+      PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
     // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
@@ -432,7 +456,11 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     PCTC_HIP(hipEventRecord(ev.sel, dps_stream));
     // S = logits - lambda once both are done
     PCTC_HIP(hipStreamWaitEvent(stream, ev.sel, 0));
-    PCTC_HIP(launch_lse_finalize(partials, L.M, P, lam, lam2, Zd, Kdev, S, L.ldS, stream));
+    PCTC_HIP(launch_lse_finalize(partials, L.M, P, lam, lam2, Zd, Kdev, S, L.ldS, stream, use_e ? g_pred : nullptr,
+                                 escale, einv));
+    if (use_e)
+      PCTC_HIP(launch_hs_scale_bf16(bwd_hs(bws, L.bwd), L.M, D, einv, escale, reinterpret_cast<uint16_t*>(ws + L.o_hp),
+                                    stream));
     PCTC_HIP(hipEventRecord(ev.fork, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
   } else {
@@ -533,6 +561,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     if (dh_in_place) side.after_dh = SideWork{&UnionWork::run_dh, &uw};
     side.dH_extra = (dH && !dh_in_place && L.K_max > 0) ? dH : nullptr;
     side.hs_built = (dH || dW);
+    if (use_e) side.ce = &chunk_e;
     if (uw.dw_ready) {
       side.udw = union_dw_extra(L.M, D, L.K_max, Kdev, ws + L.o_corr, Gb);
       side.udw.ready = uw.dw_ready;
@@ -617,13 +646,13 @@ int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, c
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
   if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
-  Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr);
+  Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr, false);
   if (chunk == 0 && L.total > kNoAllocScratchBytes) {
     // the widest backward chunk (a multiple of 256 columns) whose layout fits the scratch;
     // the layout is not monotone in the chunk (the dH product's split count changes with
     // it), so every width is tried from the default down
     for (int c = L.bwd.chunk / 256 * 256; c >= 256; c -= 256) {
-      const Layout Lc = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, c, dW != nullptr);
+      const Layout Lc = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, c, dW != nullptr, false);
       if (Lc.total <= kNoAllocScratchBytes) {
         L = Lc;
         break;

@@ -54,8 +54,13 @@ hipError_t launch_lse(int dtype, const void* H, int M, int D, const void* W, con
 // half also writes S[m * ldS + j] = float(Zd[m * ldS + j] - lambda_m) for j < *K.
 hipError_t launch_lse_partials(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
                                float2* partials, int* P_out, hipStream_t stream);
+// With g (forecast dense-part factors), also rowscale[m] = -g_m exp(-lambda_m) and *einv = 1
+// if any lambda_m lies outside [kEMin, kEMax] (the normaliser's E = exp(z) is then unusable:
+// bf16 overflow or significant underflow).
+constexpr double kEMin = -40.0, kEMax = 60.0;
 hipError_t launch_lse_finalize(const float2* partials, int M, int P, double* lam, float2* lam2, const double* Zd,
-                               const int32_t* K, float* S, int ldS, hipStream_t stream);
+                               const int32_t* K, float* S, int ldS, hipStream_t stream, const float* g = nullptr,
+                               float* rowscale = nullptr, int32_t* einv = nullptr);
 hipError_t launch_gather_s(int dtype, const void* H, int M, int D, const void* W, const float* bias,
                            const int32_t* u_ids, const int32_t* K, int K_max, const double* lam, float* S, int ldS,
                            hipStream_t stream);
@@ -87,6 +92,9 @@ struct BwdPlan {
   size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
+// Column multiple of the default chunk of narrow bf16 heads: the normaliser's partition width
+// (eight 256-row tiles; any V up to PCTC_MAX_VOCAB keeps it within 256 partitions).
+constexpr int kEAlign = 2048;
 // The bf16 fused schedule's side of the recomputed backward.  With a second stream: work i
 // (i < nwork) is enqueued on that stream after chunk i + 1 of the dense part (the caller's
 // stream records gate[i], the second stream waits for it, then work[i].fn(work[i].ctx)
@@ -115,6 +123,7 @@ struct BwdSide {
   const float* dH_extra = nullptr;
   bool hs_built = false;
   DwExtra udw;  // the union columns' dW_u, folded into the last chunk's dW launch (dH wanted)
+  const struct ChunkE* ce = nullptr;  // the first chunk's dZ rows come from the normaliser
 };
 // the masked copy of H (rows of frames with g == 0 zeroed) inside the backward's scratch
 uint16_t* bwd_hs(void* scratch, const BwdPlan& plan);
@@ -136,11 +145,33 @@ hipError_t launch_gather_s_bf16(const uint16_t* H, int M, int D, const uint16_t*
                                 hipStream_t stream, double* Zd = nullptr);
 // One chunk of the recomputed backward: the recompute of dZ (when `recompute`), then the dH
 // and dW products it feeds.
+// The backward's first chunk when the normaliser wrote its dZ rows as E = exp(z) without the
+// per-frame factor s_m = -g_m exp(-lambda_m) (bf16 fused schedule, narrow heads): the dH
+// product scales its rows by rowscale and the dW product reads Hp = s Hs instead of Hs; the
+// recompute runs only when *einv is set (E unusable; rowscale then holds ones and Hp a copy
+// of Hs).
+struct ChunkE {
+  const float* rowscale = nullptr;
+  const uint16_t* Hp = nullptr;
+  const int32_t* einv = nullptr;
+};
 hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_t* W, const float* bias, int c0,
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
-                                 float* dbpart, hipStream_t stream, const DwExtra* extra = nullptr);
+                                 float* dbpart, hipStream_t stream, const DwExtra* extra = nullptr,
+                                 const ChunkE* ce = nullptr);
+// Partitions of the normaliser that can write E for a first chunk of `chunk` columns (0: none;
+// narrow heads with D a multiple of 128, chunk a multiple of the partition width).
+int lse_e_parts_bf16(int M, int D, int V, int chunk);
+// The normaliser (no bias) that also writes E = exp(z) in bf16 at E[m * epitch + v] for the
+// rows of its first eparts partitions, and clears *einv (see launch_lse_finalize).
+hipError_t launch_lse_partial_e_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
+                                     int* P_out, uint16_t* E, int epitch, int eparts, int32_t* einv,
+                                     hipStream_t stream);
+// rowscale/Hp of ChunkE from the finalize's s_m (in rowscale) and its check flag.
+hipError_t launch_hs_scale_bf16(const uint16_t* Hs, int M, int D, const int32_t* einv, float* rowscale, uint16_t* Hp,
+                                hipStream_t stream);
 // Union-column part of the backward (bf16 path): dH_u = G W_U written into dH [M][D] (which
 // the final reduction then adds the dense part to), or later added to dH, and into its own
 // buffers dW_u = G^T H [K_max][D] and db_u = column sums of G [K_max], frames with g == 0 left

@@ -84,14 +84,21 @@ def test_host_side_sizing_rules():
     assert lib.pctc_lse_scratch_bytes(-1, 512) == 0 and lib.pctc_lse_scratch_bytes(10, 0) == 0
     assert lib.pctc_greedy_workspace_size(16, 4215, 4096) > lib.pctc_greedy_workspace_size(16, 4215, 512) > 0
     assert lib.pctc_greedy_workspace_size(16, 4215, 0) == 0
-    # default chunk: the fewest equal chunks (multiples of 256) whose bf16 gradient fits ~512 MiB
+    # default chunk: the fewest equal chunks (multiples of 256) whose bf16 gradient fits ~512 MiB;
+    # narrow bf16 heads (D < 2048) round to whole normaliser partitions (2048 columns), so that
+    # the normaliser can write the first chunk's gradient rows
     for M, V in ((4215, 180_000), (2567, 151_936), (11458, 151_936), (16000, 180_000), (64, 1000)):
-        c = lib.pctc_bwd_chunk(1, M, 512, V, 0)
-        assert c > 0 and c % 256 == 0
-        n = -(-V // c)
-        assert c * 2 * M <= 512 * 2**20 + 256 * 2 * M or n == 1
-        assert c - -(-V // n) < 256          # equal chunks, rounded up to whole tiles
-    assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 0) == 60160
+        for D, align in ((512, 2048), (4096, 256)):
+            c = lib.pctc_bwd_chunk(1, M, D, V, 0)
+            assert c > 0 and c % align == 0
+            cap = min(65536, (512 * 2**20 // (2 * M)) // 256 * 256)
+            assert c <= cap
+            n = -(-V // c)
+            assert c - -(-V // n) < align or n == 1   # equal chunks, rounded up to whole tiles/partitions
+        c = lib.pctc_bwd_chunk(0, M, 512, V, 0)     # fp32: whole tiles
+        assert c % 256 == 0 and c - -(-V // -(-V // c)) < 256
+    assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 0) == 61440
+    assert lib.pctc_bwd_chunk(1, 2567, 4096, 151_936, 0) == 50688
     assert lib.pctc_bwd_chunk(1, 4215, 512, 180_000, 1024) == 1024
     # an explicit chunk wider than the vocabulary is cut to V rounded up to whole tiles
     assert lib.pctc_bwd_chunk(1, 4215, 512, 1000, 65536) == 1024

@@ -5,6 +5,7 @@ path loss relative error <= 1e-5 and gradient max-abs relative error <= 1e-4; bf
 loss relative error <= 2e-3 and gradient cosine >= 0.999 (plus tighter checks that
 document the achieved accuracy).
 """
+import dataclasses
 import math
 
 import numpy as np
@@ -608,6 +609,38 @@ def test_e2e_large_logits(dtype, beam):
     say(f"e2e large logits {dtype} beam={beam} M={wl.M}")
     res = run_gpu(wl)
     _check_e2e(wl, res, ref, fp32=(dtype == "f32"))
+
+
+@pytest.mark.parametrize("case", ["in_range", "high", "low"])
+def test_e2e_first_chunk_from_normaliser(case):
+    """Narrow bf16 heads: the normaliser writes the first backward chunk's rows as exp(z) and
+    the backward applies each frame's factor -g exp(-lambda) afterwards (Eq. vjp; no recompute
+    of that chunk).  That is usable while every lambda lies in [-40, 60]; frames whose lambda
+    leaves that range (high: logits scaled up; low: every logit far below zero) make the
+    call recompute the chunk instead.  Each case is checked against the oracle with the
+    default chunk (two chunks, the first from the normaliser when usable) and with an explicit
+    chunk that is not a whole number of normaliser partitions (every chunk recomputed)."""
+    wl = workloads.random_small(7, N=4, T_range=(40, 90), D=128, V=70_000, dtype="bf16")
+    if case != "in_range":
+        H, W = wl.H.copy(), wl.W.copy()
+        if case == "high":
+            H[:10] *= 20.0  # logits of those frames scaled by 20: lambda up to about 100
+        else:
+            u = np.full(wl.D, 1.0 / np.sqrt(wl.D), np.float32)
+            W = W + u  # a common direction in every class row
+            H[:10] = -100.0 * u  # those frames: every logit near -100, lambda about -60
+        wl = dataclasses.replace(wl, H=workloads.round_to_bf16(H), W=workloads.round_to_bf16(W))
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    lam = ref["lam"]
+    say(f"e2e first chunk from the normaliser: {case} M={wl.M} lambda in [{lam.min():.1f}, {lam.max():.1f}]")
+    if case == "in_range":
+        assert lam.min() >= -40 and lam.max() <= 60
+    else:
+        assert lam.min() < -40 or lam.max() > 60
+    for chunk in (0, 36608):
+        res = run_gpu(wl, chunk=chunk)
+        say(f"  chunk {chunk}")
+        _check_e2e(wl, res, ref, fp32=False)
 
 
 # ---------------------------------------------------------------------------------------
