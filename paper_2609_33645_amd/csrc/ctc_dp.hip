@@ -653,7 +653,9 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
                          void*, int phase) {
   const int N = plan.N;
-  const bool front = phase != kDpBack, back = phase != kDpFront;
+  const bool prep = phase == kDpAll || phase == kDpFront || phase == kDpPrep;
+  const bool vit = phase == kDpAll || phase == kDpFront || phase == kDpVit;
+  const bool back = phase == kDpAll || phase == kDpBack;
   char* sc = static_cast<char*>(scratch);
   int32_t* toff = reinterpret_cast<int32_t*>(sc + plan.off_toff);
   int32_t* yoff = reinterpret_cast<int32_t*>(sc + plan.off_yoff);
@@ -671,7 +673,7 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
   const int Q = pick_q(plan.Smax);
   if (Q < 0) return hipErrorInvalidValue;
   uint8_t* mask = plan.pruned ? reinterpret_cast<uint8_t*>(sc + plan.off_mask) : nullptr;
-  if (front) {
+  if (prep) {
     // G and g start at zero: excluded utterances and unused columns stay zero.
     if (plan.M > 0) {
       e = hipMemsetAsync(G, 0, static_cast<size_t>(plan.M) * ldS * sizeof(float), stream);
@@ -685,6 +687,9 @@ hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U,
       hipLaunchKernelGGL(dp_prep_kernel, dim3(N), dim3(256), 0, stream, toff, yoff, y_rel, K_max, status, dnext,
                          dfirst, frame_utt, loss_n);
     }
+  }
+  if (N == 0) return hipGetLastError();
+  if (vit) {
     if (plan.pruned) {
       float* tva = reinterpret_cast<float*>(sc + plan.off_tab_va);
       float* tvb = reinterpret_cast<float*>(sc + plan.off_tab_vb);

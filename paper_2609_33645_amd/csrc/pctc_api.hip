@@ -145,6 +145,7 @@ static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const i
 
 // want_dW: the call asks for dW (the union columns' dW_u slices are only needed then).
 // allow_e: the layout may serve the two-stream schedule (room for the normaliser's E chunk).
+constexpr size_t kEMaxExtra = static_cast<size_t>(64) << 20;
 static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
                           float beam, int32_t chunk, bool want_dW = true, bool allow_e = true) {
   Layout L{};
@@ -185,7 +186,21 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   L.o_dp = take(L.dp.total);
   L.o_bwd = take(L.bwd.total);
   L.eparts = (dtype == PCTC_BF16 && allow_e) ? lse_e_parts_bf16(L.M, D, V, L.bwd.chunk) : 0;
+  const size_t zd_need = static_cast<size_t>(L.M) * L.ldS * sizeof(double);
+  const size_t part = lse_partial_bytes(L.M, D);
   size_t e_bytes = 0;  // the first chunk's E rows, written by the normaliser
+  if (L.eparts > 0) {
+    // the selected logits and the partial pairs then live past the E rows of the gradient
+    // buffer; where that tail is too short by more than kEMaxExtra bytes (many frames at a
+    // wide head), the first chunk is recomputed instead
+    e_bytes = align_up(static_cast<size_t>(L.M) * L.bwd.chunk * 2, 256);
+    const size_t tail = L.bwd.dz_bytes > e_bytes ? L.bwd.dz_bytes - e_bytes : 0;
+    const size_t lodge = align_up(zd_need, 256) + part;
+    if (lodge > tail + kEMaxExtra) {
+      L.eparts = 0;
+      e_bytes = 0;
+    }
+  }
   if (L.eparts > 0) {
     e_bytes = align_up(static_cast<size_t>(L.M) * L.bwd.chunk * 2, 256);
     L.o_escale = take(static_cast<size_t>(L.M) * 4);
@@ -196,15 +211,13 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
   // they live in that buffer (past the E rows) when it is large enough.
   size_t lent = e_bytes;
   if (dtype == PCTC_BF16) {
-    const size_t need = static_cast<size_t>(L.M) * L.ldS * sizeof(double);
-    if (L.bwd.dz_bytes >= lent + need) {
+    if (L.bwd.dz_bytes >= lent + zd_need) {
       L.o_zd = L.o_bwd + lent;
-      lent += align_up(need, 256);
+      lent += align_up(zd_need, 256);
     } else {
-      L.o_zd = take(need);
+      L.o_zd = take(zd_need);
     }
   }
-  const size_t part = lse_partial_bytes(L.M, D);
   L.o_part = (L.bwd.dz_bytes >= lent + part) ? L.o_bwd + lent : take(part);
   L.total = o;
   return L;
@@ -453,6 +466,9 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
       PCTC_HIP(launch_hs_build_bf16(static_cast<const uint16_t*>(H), L.M, D, g_pred, bwd_hs(bws, L.bwd), dps_stream));
     PCTC_HIP(launch_gather_s_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), bias,
                                   u_ids, Kdev, L.K_max, nullptr, nullptr, L.ldS, dps_stream, Zd));
+    // the lattice's set-up (zeroing of G and g, per-utterance prep), which does not read S
+    PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status,
+                           G, g, nullptr, dps, L.K_max, dps_stream, nullptr, kDpPrep));
     PCTC_HIP(hipEventRecord(ev.sel, dps_stream));
     // S = logits - lambda once both are done
     PCTC_HIP(hipStreamWaitEvent(stream, ev.sel, 0));
@@ -508,7 +524,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // log-sum passes, occupancies and the loss after the dense part's first chunk, and the
     // union columns' part after its second (see BwdSide)
     PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status,
-                           G, g, nullptr, dps, L.K_max, dps_stream, nullptr, kDpFront));
+                           G, g, nullptr, dps, L.K_max, dps_stream, nullptr, kDpVit));
     dpt.phase = kDpBack;
     // the union columns' part of the backward, from the lattice's G (its frames with g == 0
     // are those of the forecast unless the check fails, and then the backward is redone)

@@ -220,8 +220,9 @@ DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam);
 // weight: device float [N] loss weights of the utterances, or null (all 1): G rows of
 // utterance n are -w_n gamma.
 // phase: kDpAll, or kDpFront (zeroing of G and g, prep, the Viterbi pass and the arc mask)
-// then kDpBack (the log-sum passes and the occupancies, G and g) on the same stream.
-constexpr int kDpAll = 0, kDpFront = 1, kDpBack = 2;
+// then kDpBack (the log-sum passes and the occupancies, G and g) on the same stream; kDpFront
+// may itself be split into kDpPrep (the zeroing and prep, which do not read S) and kDpVit.
+constexpr int kDpAll = 0, kDpFront = 1, kDpBack = 2, kDpPrep = 3, kDpVit = 4;
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
                          const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
