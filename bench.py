@@ -31,7 +31,8 @@ PEAK_HBM_GBS = 8000.0
 # every matrix-product kernel of the fused step: the dense products, the selected-logit product
 # and the union-column part's two products (their event times include any wait for free
 # compute units beside the dense part, so the fraction below is a lower bound)
-GEMM_KERNELS = ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm", "gather_s", "union_dh", "union_dw")
+GEMM_KERNELS = ("lse_partial", "recompute_dz", "recompute_check", "dh_gemm", "dw_gemm", "gather_s", "union_dh",
+                "union_dw")
 
 
 def parse():
@@ -368,9 +369,15 @@ def main():
     M, D, V = wl.M, wl.D, wl.V
     fps = M * a.steps / dt
 
-    # algorithmic work per step (bf16/fp32 matrix products)
-    # the union-column products run on G split into bf16 hi and lo halves (2 K columns)
-    gemm_flops = {"lse_partial": 2.0 * M * V * D, "recompute_dz": 2.0 * M * V * D, "dh_gemm": 2.0 * M * V * D,
+    # matrix-product work executed per step (bf16/fp32).  The normaliser writes the first
+    # backward chunk's gradient rows itself where pctc_normaliser_chunk_columns says so (the
+    # recompute then covers V - ecols columns; its guard launch, "recompute_check", only
+    # recomputes when some lambda leaves the range that allows it, which no workload here does).
+    # The union-column products run on G split into bf16 hi and lo halves (2 K columns).
+    ecols = prunedctc.normaliser_chunk_columns(1 if wl.dtype == "bf16" else 0, T, U, D, V, wl.beam, a.chunk,
+                                               not a.frozen_head)
+    gemm_flops = {"lse_partial": 2.0 * M * V * D, "recompute_dz": 2.0 * M * (V - ecols) * D,
+                  "recompute_check": 0.0, "dh_gemm": 2.0 * M * V * D,
                   "dw_gemm": 0.0 if a.frozen_head else 2.0 * M * V * D, "gather_s": 2.0 * M * K * D,
                   "union_dh": 2.0 * M * 2 * K * D, "union_dw": 0.0 if a.frozen_head else 2.0 * M * 2 * K * D}
     kernel_ms = {k: v["total_ms"] / a.steps for k, v in prof.items()}
@@ -380,7 +387,8 @@ def main():
     dom_flops_per_launch = gemm_flops[dom] / (dom_prof["launches"] / a.steps)
     achieved = dom_flops_per_launch / (dom_avg_ms * 1e-3) / 1e12
     gemm_ms = sum(kernel_ms.get(k, 0.0) for k in GEMM_KERNELS)
-    gemm_total = sum(gemm_flops[k] for k in ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm"))  # 8 M V D
+    gemm_total = sum(gemm_flops[k] for k in ("lse_partial", "recompute_dz", "dh_gemm", "dw_gemm"))  # executed
+    method_total = (8.0 if not a.frozen_head else 6.0) * M * V * D  # the recomputed method's products
     line = {
         "metric": "frames/sec fused head+Pruned-CTC fwd+bwd at V=180K; % bf16 MFMA peak; peak MB",
         "value": round(fps, 1),
@@ -402,6 +410,8 @@ def main():
         "mfma_frac_gemms": round(gemm_total / (gemm_ms * 1e-3) / 1e12 / peak, 4),
         "gemm_ms_per_step": round(gemm_ms, 4),
         "mfma_frac_step": round(gemm_total / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "mfma_frac_step_8mvd": round(method_total / (ms_step * 1e-3) / 1e12 / peak, 4),
+        "normaliser_chunk_columns": ecols,
         "mfma_frac_useful": round(6.0 * M * V * D / (ms_step * 1e-3) / 1e12 / peak, 4),
         "aux": aux_figures(wl, K, kernel_ms),
         "peak_mb": round(peak_mb, 1),

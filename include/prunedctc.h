@@ -85,6 +85,18 @@ size_t pctc_workspace_size_ex(pctc_dtype dtype, int32_t N, const int32_t* input_
                               const int32_t* target_lengths, int32_t D, int32_t V, float beam,
                               int32_t chunk, int32_t flags);
 
+/* Vocabulary columns of the first backward chunk whose gradient rows the normaliser pass of a
+ * fused call of this shape writes itself (Eq. vjp: the dense part -g_m p_v(m) of that chunk is
+ * exp(z) times a per-frame factor formed once lambda is known, so the chunk needs no recomputed
+ * logits), or 0 when every chunk is recomputed.  Applies to bf16 calls with a second stream
+ * (pruned_ctc_fwd_bwd, pruned_ctc_fwd_bwd_ex without bias and db) asking for dH or dW; at run
+ * time the call still recomputes the chunk when some frame's lambda lies outside [-40, 60]
+ * (where exp(z) in bf16 would overflow or lose mass).  Arguments as pctc_workspace_size_ex; 0
+ * on invalid arguments.  Host only; no device work. */
+int32_t pctc_normaliser_chunk_columns(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
+                                      const int32_t* target_lengths, int32_t D, int32_t V, float beam,
+                                      int32_t chunk, int32_t flags);
+
 /* Forward and backward pass of Pruned CTC (Algorithm 1).
  *
  * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8 and at

@@ -1246,7 +1246,8 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
   if (recompute) {
     const int nVt = (cw + kFR - 1) / kFR;
     const dim3 grid(grouped_grid(nMt, nVt));
-    Prof pr("recompute_dz", stream);
+    // with ce the launch only recomputes when the normaliser's rows are unusable
+    Prof pr(ce ? "recompute_check" : "recompute_dz", stream);
 #define PCTC_RECOMPUTE(GC, OCC, BI, DBI)                                                                             \
   hipLaunchKernelGGL((recompute_dz_bf16<GC, BI, DBI, OCC>), grid, dim3(GC::kThreads), 0, stream, Hs, M, D, W, bias, \
                      c0, cw, lam2, g, remap, S, ldS, G, ldG, dZ, chunk, dbpart)
@@ -1258,7 +1259,7 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
     if (db) PCTC_RECOMPUTE(GC, OCC, false, true); \
     else PCTC_RECOMPUTE(GC, OCC, false, false);   \
   }
-    if (wide) {
+    if (!ce && wide) {
       PCTC_RECOMPUTE_CFG(GWide, 1)
     } else if (ce || (!bias && !db && !remap && D % (GMid::kNS * GMid::KK * 16) == 0)) {
       // one round of workgroups (one per CU, 256 x 256 tiles), each taking a run of vocabulary
@@ -1316,7 +1317,7 @@ hipError_t launch_hs_scale_bf16(const uint16_t* Hs, int M, int D, const int32_t*
 }
 
 int lse_e_parts_bf16(int M, int D, int V, int chunk) {
-  if (M <= 0 || D >= kWideD || D % (GMid::kNS * GMid::KK * 16) != 0 || chunk <= 0) return 0;
+  if (M <= 0 || D % (GMid::kNS * GMid::KK * 16) != 0 || chunk <= 0) return 0;
   const LseSplit sp = lse_split_bf16(M, D, V);
   if (chunk % sp.vper != 0) return 0;
   const int ep = chunk / sp.vper;

@@ -4,6 +4,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <functional>
 #include <map>
 #include <mutex>
@@ -346,6 +347,15 @@ size_t pctc_workspace_size_ex(pctc_dtype dtype, int32_t N, const int32_t* input_
   if (check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk) != PCTC_OK) return 0;
   if (flags & ~PCTC_WS_NO_DW) return 0;
   return make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, !(flags & PCTC_WS_NO_DW)).total;
+}
+
+int32_t pctc_normaliser_chunk_columns(pctc_dtype dtype, int32_t N, const int32_t* input_lengths,
+                                      const int32_t* target_lengths, int32_t D, int32_t V, float beam,
+                                      int32_t chunk, int32_t flags) {
+  if (check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk) != PCTC_OK) return 0;
+  if (flags & ~PCTC_WS_NO_DW) return 0;
+  const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, !(flags & PCTC_WS_NO_DW));
+  return L.eparts > 0 ? std::min(L.bwd.chunk, V) : 0;
 }
 
 const char* pctc_status_string(int32_t status) {

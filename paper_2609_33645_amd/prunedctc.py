@@ -50,6 +50,8 @@ def lib() -> ctypes.CDLL:
     L.pctc_workspace_size.restype = c_sz
     L.pctc_workspace_size_ex.argtypes = [c_i32, c_i32, i32p, i32p, c_i32, c_i32, c_f, c_i32, c_i32]
     L.pctc_workspace_size_ex.restype = c_sz
+    L.pctc_normaliser_chunk_columns.argtypes = [c_i32, c_i32, i32p, i32p, c_i32, c_i32, c_f, c_i32, c_i32]
+    L.pctc_normaliser_chunk_columns.restype = c_i32
     L.pruned_ctc_fwd_bwd.argtypes = [c_i32, c_p, c_i32, c_p, c_i32, c_p, i32p, i32p, c_i32, c_i32, c_f, c_i32,
                                      c_p, c_p, c_p, c_p, c_p, c_p, c_sz, c_p]
     L.pruned_ctc_fwd_bwd.restype = c_i32
@@ -168,6 +170,16 @@ def workspace_size(dtype: int, input_lengths, target_lengths, D: int, V: int, be
     U = _host_i32(target_lengths)
     return int(lib().pctc_workspace_size_ex(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk,
                                             0 if want_dW else WS_NO_DW))
+
+
+def normaliser_chunk_columns(dtype: int, input_lengths, target_lengths, D: int, V: int, beam: float, chunk: int = 0,
+                             want_dW: bool = True) -> int:
+    """Vocabulary columns of the first backward chunk that the normaliser of a fused call writes
+    itself (0: every chunk is recomputed); see pctc_normaliser_chunk_columns."""
+    T = _host_i32(input_lengths)
+    U = _host_i32(target_lengths)
+    return int(lib().pctc_normaliser_chunk_columns(dtype, T.size, _i32p(T), _i32p(U), D, V, float(beam), chunk,
+                                                   0 if want_dW else WS_NO_DW))
 
 
 def bwd_chunk(dtype: int, M: int, D: int, V: int, chunk: int = 0) -> int:

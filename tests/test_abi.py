@@ -110,6 +110,33 @@ def test_host_side_sizing_rules():
 
 
 @pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_normaliser_chunk_columns():
+    """Host rule for the first backward chunk that the normaliser writes itself (bf16, D a
+    multiple of 128, chunk a whole number of normaliser partitions: 2048 columns for D < 2048,
+    256 for wider heads, and the selected logits and partial pairs lodged past those rows
+    within 64 MiB of extra memory)."""
+    import numpy as np
+    from paper_2609_33645_amd import prunedctc as pc
+
+    rng = np.random.default_rng(0)
+    Tz = rng.integers(150, 376, size=16).astype(np.int32)       # Zipformer-M-like batch
+    Tq = rng.integers(500, 751, size=4).astype(np.int32)        # Qwen3-8B-like batch
+    Te = np.full(107, 107, np.int32)                            # 107 utterances (LLM memory shape)
+
+    def cols(dtype, T, D, V, chunk=0, want_dW=True, u=6):
+        return pc.normaliser_chunk_columns(dtype, T, T // u, D, V, float("inf"), chunk, want_dW)
+    assert cols(1, Tz, 512, 180_000) == pc.bwd_chunk(1, int(Tz.sum()), 512, 180_000) == 61440
+    assert cols(0, Tz, 512, 180_000) == 0                       # fp32: every chunk recomputed
+    assert cols(1, Tz, 512, 180_000, chunk=4096) == 4096 and cols(1, Tz, 512, 180_000, chunk=4352) == 0
+    assert cols(1, Tq, 4096, 151_936, u=4) == pc.bwd_chunk(1, int(Tq.sum()), 4096, 151_936) == 50688
+    assert cols(1, Te, 4096, 151_936, want_dW=False, u=4) == 0  # off: lodging would add > 64 MiB
+    assert cols(1, Tz[:3], 136, 5000) == 0                      # D not a multiple of 128
+    assert cols(1, Tz[:3], 128, 5000) == 5000                   # one chunk: the whole vocabulary
+    bad = np.array([0], np.int32)
+    assert pc.normaliser_chunk_columns(1, bad, bad, 128, 5000, 0.0) == 0   # invalid lengths
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
 def test_zero_frame_sizing():
     """Every size query accepts a batch without frames (N = 0 or M = 0) and returns a usable
     size: the bf16 union part once divided by a zero frame-slice length there."""

@@ -945,12 +945,13 @@ def test_concurrent_calls_with_kernel_timing():
             for a, b in zip(results[i][r], alone[i]):
                 assert torch.equal(a, b), (i, r)
     assert prof["lse_partial"]["launches"] == 2 * calls, prof["lse_partial"]
-    assert prof["recompute_dz"]["launches"] % (2 * calls) == 0
+    # recompute launches (or, where the normaliser wrote a chunk's rows, its guard launch)
+    nrc = sum(prof[k]["launches"] for k in ("recompute_dz", "recompute_check") if k in prof)
+    assert nrc > 0 and nrc % (2 * calls) == 0, prof
     assert all(v["total_ms"] > 0 for v in prof.values())
 
 
 # ---------------------------------------------------------------------------------------
-# determinism: every reduction runs in a fixed order, also across the two streams# ---------------------------------------------------------------------------------------
 # determinism: every reduction runs in a fixed order, also across the two streams
 # ---------------------------------------------------------------------------------------
 
