@@ -29,7 +29,7 @@ constexpr float kNeg = -1.0e30f;  // "impossible" score; absorbs finite addition
 constexpr int kMaxQ = 32;         // most states per lane of a lattice pass (2U+1 <= 64 kMaxQ)
 static_assert(2 * PCTC_MAX_TARGET + 1 <= 64 * kMaxQ, "the longest target fits a lattice pass");
 // arc flags of a pass without a mask: every arc kept
-__device__ const uint8_t kAllArcs[1] = {0x0f};
+constexpr int kAllArcs = 0x0f;
 
 DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
   DpPlan p{};
@@ -185,10 +185,14 @@ __device__ __forceinline__ Acc comb3(Acc a, Acc b, Acc c) {
   }
 }
 
-// Frames of emissions (and arc flags) loaded ahead of the recursion.
-template <int Q>
+// Frames of emissions (and arc flags) loaded ahead of the recursion.  A pass without a mask
+// issues a third fewer memory instructions per frame (no flag loads) and holds no flags, so it
+// prefetches deeper: the frames in flight are bounded by the wave's memory counter (63
+// instructions) and by registers.
+template <int Q, bool MASK>
 constexpr int prefetch_depth() {
-  return Q <= 3 ? 8 : (Q <= 4 ? 6 : (Q <= 6 ? 4 : (Q <= 8 ? 3 : 2)));
+  if (MASK) return Q <= 3 ? 8 : (Q <= 4 ? 6 : (Q <= 6 ? 4 : (Q <= 8 ? 3 : 2)));
+  return Q <= 4 ? 8 : (Q <= 8 ? 5 : (Q <= 13 ? 3 : 2));
 }
 
 // One wavefront per (utterance, direction), natural-log units.  VIT: Viterbi (max-plus)
@@ -201,7 +205,7 @@ constexpr int prefetch_depth() {
 // wavefronts of this latency-bound stage occupy few compute units.
 constexpr int kPassWaves = 4;
 
-template <int Q, bool VIT>
+template <int Q, bool VIT, bool MASK>
 __global__ void __launch_bounds__(64 * kPassWaves)
 dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__ toff,
                const int32_t* __restrict__ yoff, const int64_t* __restrict__ soff, const int32_t* __restrict__ y_rel,
@@ -209,7 +213,7 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
                float* __restrict__ tab_b, double* __restrict__ sc_f, double* __restrict__ sc_b,
                double* __restrict__ total_out, double* __restrict__ loss_n, int N, float* __restrict__ dummy) {
   using Acc = typename std::conditional<VIT, float, double>::type;
-  constexpr int PF = prefetch_depth<Q>();
+  constexpr int PF = prefetch_depth<Q, MASK>();
   const int unit = blockIdx.x * kPassWaves + (threadIdx.x >> 6);  // (utterance, direction)
   if (unit >= 2 * N) return;
   const int n = unit >> 1;
@@ -247,13 +251,18 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
   float* const drow = dummy + static_cast<int64_t>(unit) * (64 * Q) + lane * Q;
   auto fetch = [&](int t, float (&e)[Q], int (&mk)[Q]) {
     const float* row = S + static_cast<int64_t>(t0 + t) * ldS;
-    const uint8_t* mrow = mask ? mask + base + static_cast<int64_t>(t) * Sp : kAllArcs;
-    const int mstep = mask ? 1 : 0;
 #pragma unroll
-    for (int q = 0; q < Q; ++q) {
-      e[q] = row[col[q]];  // invalid states read the blank column (a valid address)
-      const int v = static_cast<int>(mrow[mstep * min(lane * Q + q, Sp - 1)]);
-      mk[q] = valid[q] ? v : 0;
+    for (int q = 0; q < Q; ++q) e[q] = row[col[q]];  // invalid states read the blank column (a valid address)
+    if constexpr (MASK) {
+      const uint8_t* mrow = mask + base + static_cast<int64_t>(t) * Sp;
+#pragma unroll
+      for (int q = 0; q < Q; ++q) {
+        const int v = static_cast<int>(mrow[min(lane * Q + q, Sp - 1)]);
+        mk[q] = valid[q] ? v : 0;
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < Q; ++q) mk[q] = valid[q] ? kAllArcs : 0;
     }
   };
   auto renorm_store = [&](Acc (&v)[Q], double& off, float* tab, double* sc, int t) {
@@ -614,10 +623,14 @@ static hipError_t launch_pass(int Q, int N, hipStream_t stream, const float* S, 
                               const int32_t* yoff, const int64_t* soff, const int32_t* y_rel, int32_t* status,
                               const uint8_t* mask, float* tf, float* tb, double* sf, double* sb, double* total,
                               double* loss_n, float* dummy) {
-#define PCTC_PASS(QQ)                                                                                       \
-  case QQ:                                                                                                  \
-    hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT>), grid, dim3(64 * kPassWaves), 0, stream, S, ldS, toff, yoff, \
-                       soff, y_rel, status, mask, tf, tb, sf, sb, total, loss_n, N, dummy);                 \
+#define PCTC_PASS(QQ)                                                                                         \
+  case QQ:                                                                                                    \
+    if (mask)                                                                                                 \
+      hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT, !VIT>), grid, dim3(64 * kPassWaves), 0, stream, S, ldS, toff, \
+                         yoff, soff, y_rel, status, mask, tf, tb, sf, sb, total, loss_n, N, dummy);           \
+    else                                                                                                      \
+      hipLaunchKernelGGL((dp_pass_kernel<QQ, VIT, false>), grid, dim3(64 * kPassWaves), 0, stream, S, ldS,   \
+                         toff, yoff, soff, y_rel, status, nullptr, tf, tb, sf, sb, total, loss_n, N, dummy);  \
     break;
   const dim3 grid((2 * N + kPassWaves - 1) / kPassWaves);
   switch (Q) {
@@ -792,7 +805,7 @@ dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restr
   // Emissions and arc flags of the next PF frames are held in a register ring; the loop has
   // only loads and no branch around them (clamped addresses), so each frame waits only for
   // its own ring slot.
-  constexpr int PF = prefetch_depth<Q>();
+  constexpr int PF = prefetch_depth<Q, true>();
   float ring_e[PF][Q];
   int ring_m[PF][Q];
   auto load_frame = [&](int t, float (&e)[Q], int (&mk)[Q]) {
