@@ -30,6 +30,10 @@ constexpr int kMaxQ = 32;         // most states per lane of a lattice pass (2U+
 static_assert(2 * PCTC_MAX_TARGET + 1 <= 64 * kMaxQ, "the longest target fits a lattice pass");
 // arc flags of a pass without a mask: every arc kept
 constexpr int kAllArcs = 0x0f;
+// bytes the mask region extends past its last cell: a pass reads each lane's flags as whole
+// aligned words, up to (kMaxQ + 3) / 4 + 1 words from the lane's first cell
+constexpr int kMaskPad = 64;
+static_assert(4 * ((kMaxQ + 3) / 4 + 1) <= kMaskPad, "mask padding covers a lane's word reads");
 
 DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
   DpPlan p{};
@@ -72,7 +76,7 @@ DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam) {
     p.off_sc_va = take(M * sizeof(double));
     p.off_sc_vb = take(M * sizeof(double));
     p.off_vbest = take(N * sizeof(double));
-    p.off_mask = take(L * sizeof(uint8_t));
+    p.off_mask = take(L * sizeof(uint8_t) + kMaskPad);  // the passes read whole words past a row's end
   }
   p.total = o;
   return p;
@@ -185,14 +189,18 @@ __device__ __forceinline__ Acc comb3(Acc a, Acc b, Acc c) {
   }
 }
 
-// Frames of emissions (and arc flags) loaded ahead of the recursion.  A pass without a mask
-// issues a third fewer memory instructions per frame (no flag loads) and holds no flags, so it
-// prefetches deeper: the frames in flight are bounded by the wave's memory counter (63
-// instructions) and by registers.
+// Frames of emissions (and arc flags) loaded ahead of the recursion: the frames in flight are
+// bounded by the wave's memory counter (63 instructions: per frame Q emission loads, Q table
+// stores and the offset store, and with a mask (Q + 3) / 4 + 1 flag-word loads) and by
+// registers.
 template <int Q, bool MASK>
 constexpr int prefetch_depth() {
-  if (MASK) return Q <= 3 ? 8 : (Q <= 4 ? 6 : (Q <= 6 ? 4 : (Q <= 8 ? 3 : 2)));
   return Q <= 4 ? 8 : (Q <= 8 ? 5 : (Q <= 13 ? 3 : 2));
+}
+// The discarded-mass pass loads one flag byte per state.
+template <int Q>
+constexpr int prefetch_depth_bytes() {
+  return Q <= 3 ? 8 : (Q <= 4 ? 6 : (Q <= 6 ? 4 : (Q <= 8 ? 3 : 2)));
 }
 
 // One wavefront per (utterance, direction), natural-log units.  VIT: Viterbi (max-plus)
@@ -254,11 +262,21 @@ dp_pass_kernel(const float* __restrict__ S, int ldS, const int32_t* __restrict__
 #pragma unroll
     for (int q = 0; q < Q; ++q) e[q] = row[col[q]];  // invalid states read the blank column (a valid address)
     if constexpr (MASK) {
-      const uint8_t* mrow = mask + base + static_cast<int64_t>(t) * Sp;
+      // this lane's Q flag bytes (from its first cell, clamped into the row) as the NWD aligned
+      // words that cover them, shifted into place: a few loads instead of Q byte loads (the
+      // bytes past the row's end, read only for cells past the last state, are not used)
+      constexpr int NWD = (Q + 3) / 4 + 1;
+      // (the region starts 256-byte aligned, so the offset's low bits are the address's)
+      const int64_t a = base + static_cast<int64_t>(t) * Sp + min(lane * Q, Sp - 1);
+      const uint32_t* wp = reinterpret_cast<const uint32_t*>(mask + (a & ~static_cast<int64_t>(3)));
+      const uint32_t sh = static_cast<uint32_t>(a & 3);
+      uint32_t w[NWD];
+#pragma unroll
+      for (int j = 0; j < NWD; ++j) w[j] = wp[j];
 #pragma unroll
       for (int q = 0; q < Q; ++q) {
-        const int v = static_cast<int>(mrow[min(lane * Q + q, Sp - 1)]);
-        mk[q] = valid[q] ? v : 0;
+        const uint32_t d = __builtin_amdgcn_alignbyte(w[(q >> 2) + 1], w[q >> 2], sh);
+        mk[q] = valid[q] ? static_cast<int>((d >> (8 * (q & 3))) & 0xffu) : 0;
       }
     } else {
 #pragma unroll
@@ -805,7 +823,7 @@ dp_discarded_kernel(const float* __restrict__ S, int ldS, const int32_t* __restr
   // Emissions and arc flags of the next PF frames are held in a register ring; the loop has
   // only loads and no branch around them (clamped addresses), so each frame waits only for
   // its own ring slot.
-  constexpr int PF = prefetch_depth<Q, true>();
+  constexpr int PF = prefetch_depth_bytes<Q>();
   float ring_e[PF][Q];
   int ring_m[PF][Q];
   auto load_frame = [&](int t, float (&e)[Q], int (&mk)[Q]) {
