@@ -456,6 +456,82 @@ struct Gemm {
     __builtin_amdgcn_s_barrier();         // before anyone reuses the stages
   }
 
+  // ---- ping-pong schedule (8 waves) ----
+  // Waves 0-3 and 4-7 form two groups; waves w and w + 4 share a SIMD.  Every k-tile is one
+  // memory phase (this group's copies of the tile NS - 1 ahead, then all of the tile's
+  // fragments read into registers) and one compute phase (the tile's products, registers
+  // only).  Group 1 runs one phase behind group 0, so that on every SIMD one wave issues
+  // products while the other moves data; a barrier ends every phase.  The stage refilled in
+  // a memory phase is the one both groups read in the two phases before it.
+  __device__ static __forceinline__ void phase_barrier() {
+    __builtin_amdgcn_sched_barrier(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  template <int S, class Issue>
+  __device__ static __forceinline__ void pp_tile(char* const (&st)[NS], int wave, int lane, f32x16 (&acc)[FR][FC],
+                                                 Frags (&f)[KK], Issue&& issue) {
+    issue(st[(S + NS - 1) % NS]);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) load(st[S], kk, wave, lane, f[kk]);
+    // this group's copies up to the next tile have landed (NS - 2 newer tiles may still be in
+    // flight); its reads of stage S are done before anyone refills it
+    wait_vmcnt<(NS - 2) * CPW>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    phase_barrier();
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) mma(f[kk], acc);
+    phase_barrier();
+  }
+
+  // Same contract as run (all kThreads threads call; barriers inside), ping-pong schedule.
+  template <bool ZERO = true>
+  __device__ static __forceinline__ void run_pp(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
+                                                char* const (&st)[NS], f32x16 (&acc)[FR][FC]) {
+    static_assert(NW == 8 && NS >= 3, "two groups of four waves, at least three stages");
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if constexpr (ZERO) zero(acc);
+    const int nk = (kend - kbeg + BK - 1) / BK;
+    if (nk <= 0) return;
+    const int klimA = min(A.kmax, kend), klimB = min(B.kmax, kend);
+    CA ca;
+    CB cb;
+    if constexpr (BUF) {
+      ca.init(A, row0, wave, lane, kbeg, klimA);
+      cb.init(B, col0, wave, lane, kbeg, klimB);
+    } else {
+      ca.init(A, row0, wave, lane);
+      cb.init(B, col0, wave, lane);
+    }
+    int knext = kbeg;  // k of the next tile to copy
+    auto issue = [&](char* stage) {
+      ca.issue(A, knext, klimA, stage, wave);
+      cb.issue(B, knext, klimB, stage + kABytes, wave);
+      knext += BK;
+    };
+    __builtin_amdgcn_s_barrier();  // previous users of the stages are done
+#pragma unroll
+    for (int s = 0; s < NS - 1; ++s) issue(st[s]);
+    wait_vmcnt<(NS - 2) * CPW>();  // tile 0
+    __builtin_amdgcn_s_barrier();
+    const bool lag = wave >= 4;
+    if (lag) phase_barrier();  // group 1 starts one phase behind
+    Frags f[KK];
+    const int nkp = (nk + NS - 1) / NS * NS;
+    for (int t = 0; t < nkp; t += NS) {
+      pp_tile<0>(st, wave, lane, acc, f, issue);
+      pp_tile<1>(st, wave, lane, acc, f, issue);
+      pp_tile<2 % NS>(st, wave, lane, acc, f, issue);
+      if constexpr (NS >= 4) pp_tile<3 % NS>(st, wave, lane, acc, f, issue);
+    }
+    if (!lag) phase_barrier();  // the barrier group 1 took at the start
+    wait_vmcnt<0>();                      // the copies past the end (zeros) have landed
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();         // before anyone reuses the stages
+  }
+
   struct ZeroInit {
     __device__ __forceinline__ void operator()(int, f32x16 (&acc)[FR][FC]) const { zero(acc); }
   };

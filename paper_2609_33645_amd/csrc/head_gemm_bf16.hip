@@ -33,7 +33,7 @@ constexpr int kBK = 32;
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 // the same tiles over gathered W rows (selected classes): flat per-lane addresses
 using GFwdGather = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3, 2, 2, false, false>;
-// 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32
+// 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32 (run on the ping-pong schedule)
 using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
 // logit products of wide heads (D >= kWideD: normaliser, argmax, recompute): the k loop is
 // long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
@@ -837,7 +837,9 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
         acc[i][j][r] = (first || d >= D || m >= M) ? 0.f : dst[static_cast<int64_t>(m) * D + d];
       }
     }
-  G::template run<false>(A, B, m0, d0, kb, ke, st, acc);
+  // 8-wave tiles on the ping-pong schedule (each SIMD's two waves alternate products and copies)
+  if constexpr (G::NW == 8) G::template run_pp<false>(A, B, m0, d0, kb, ke, st, acc);
+  else G::template run<false>(A, B, m0, d0, kb, ke, st, acc);
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
@@ -895,7 +897,7 @@ dw_gemm_bf16(DwOp P0, DwOp P1, int tiles0, const uint16_t* __restrict__ Hs, int 
   const GOp A{P.Z + static_cast<int64_t>(mb) * P.ld, P.ld, cw, mlen, nullptr};
   const GOp B{Hs + static_cast<int64_t>(mb) * D, D, D, mlen, nullptr};
   f32x16 acc[FR][FC];
-  G::run(A, B, v0, d0, 0, mlen, st, acc);
+  G::run_pp(A, B, v0, d0, 0, mlen, st, acc);
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
