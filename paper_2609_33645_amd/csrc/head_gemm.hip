@@ -767,7 +767,9 @@ BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk) {
   p.lam2_bytes = align_up(static_cast<size_t>(M) * sizeof(float2), 256);
   // bf16: per 128-frame tile column sums of dZ for db
   p.dbpart_bytes = (dtype == 1) ? align_up(static_cast<size_t>((M + 127) / 128) * cap * sizeof(float), 256) : 0;
-  p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes + p.dbpart_bytes;
+  // narrow bf16 heads: the dense recompute reads its frames from Hs transposed (whole k-lines)
+  p.hst_bytes = (dtype == 1 && D < kWideD && D % 128 == 0) ? align_up(static_cast<size_t>(D) * p.Mp * 2, 256) : 0;
+  p.total = p.dz_bytes + p.ht_bytes + p.part_bytes + p.lam2_bytes + p.dbpart_bytes + p.hst_bytes;
   return p;
 }
 
@@ -840,12 +842,19 @@ uint16_t* bwd_hs(void* scratch, const BwdPlan& plan) {
   return reinterpret_cast<uint16_t*>(static_cast<char*>(scratch) + plan.dz_bytes);
 }
 
+uint16_t* bwd_hst(void* scratch, const BwdPlan& plan) {
+  if (plan.hst_bytes == 0) return nullptr;
+  return reinterpret_cast<uint16_t*>(static_cast<char*>(scratch) + plan.dz_bytes + plan.ht_bytes + plan.part_bytes +
+                                     plan.lam2_bytes + plan.dbpart_bytes);
+}
+
 static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t* W, const float* bias, int V,
                                 const float2* lam2, const float* G, int ldG, const float* g, const int32_t* remap,
                                 const float* S, int ldS, float* dH, float* dW, float* db, char* scratch,
                                 const BwdPlan& plan, hipStream_t stream, const BwdSide* side) {
   uint16_t* dZ = reinterpret_cast<uint16_t*>(scratch);
   uint16_t* Hs = bwd_hs(scratch, plan);
+  uint16_t* Hst = bwd_hst(scratch, plan);
   // a single split-K slice accumulates straight into dH: no partials and no reduction
   const bool in_place = plan.part_bytes == 0;
   float* part = in_place ? dH : reinterpret_cast<float*>(scratch + plan.dz_bytes + plan.ht_bytes);
@@ -853,9 +862,10 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
   const int chunk = plan.chunk;
   const bool two = side && side->stream;
   hipError_t e;
-  // Hs: H with the rows of excluded frames zeroed (read by the recompute and by dW)
+  // Hs: H with the rows of excluded frames zeroed (read by the recompute and by dW), and its
+  // transpose where the recompute reads that
   if (!(side && side->hs_built)) {
-    e = launch_hs_build_bf16(H, M, D, g, Hs, stream);
+    e = Hst ? launch_ht_build_bf16(H, M, D, g, Hs, Hst, plan.Mp, stream) : launch_hs_build_bf16(H, M, D, g, Hs, stream);
     if (e != hipSuccess) return e;
   }
   const int slice = ((chunk / plan.splits + 63) / 64) * 64;
@@ -882,7 +892,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
     if (last && two && dH) {
       // the last chunk's dW product runs beside the final dH reduction (second stream)
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                true, true, false, dW, db, dbpart, stream, nullptr, ce);
+                                true, true, false, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
       if (e != hipSuccess) return e;
       if ((e = start_side(nwork)) != hipSuccess) return e;
       if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
@@ -900,12 +910,12 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
         const DwExtra* udw = side->udw.Z ? &side->udw : nullptr;
         if (udw && (e = hipStreamWaitEvent(stream, udw->ready, 0)) != hipSuccess) return e;
         e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                  false, false, true, dW, db, dbpart, stream, udw, ce);
+                                  false, false, true, dW, db, dbpart, stream, udw, ce, Hst, plan.Mp);
         if (e != hipSuccess) return e;
       }
     } else {
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
-                                true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream, nullptr, ce);
+                                true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
       if (e != hipSuccess) return e;
       if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
     }

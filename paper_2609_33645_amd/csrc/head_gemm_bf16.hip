@@ -43,6 +43,10 @@ using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 // stages, runs of kMidRun vocabulary tiles per workgroup (the copy pipeline runs through a
 // run, so one workgroup per CU still keeps the matrix pipe fed across tile boundaries)
 using GMid = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4, true>;
+// the same tiles with the frame operand read from the transposed head input Ht [D][Mp]: its
+// copies then take whole 512-byte k-lines instead of 64-byte row pieces (half cache lines),
+// a quarter fewer cache-line requests per k-tile
+using GMidT = bf::Gemm<256, 256, 32, LL::KC, LL::MC, 4, 2, 4, true>;
 constexpr int kMidRun = 8;
 constexpr int kRcCus = 224;  // workgroups of the dense recompute (one round)
 constexpr int kRcStores = 16;  // buffer stores per wave per 256 x 256 tile (recompute, E)
@@ -286,11 +290,13 @@ __device__ __forceinline__ void lse_e_update(const f32x16 (&a)[FR][FC], int j, f
 // aligned tile sequence (the stores drain under the next tile's products); the others run
 // exactly like lse_partial_bf16.  einv (the check flag) is cleared here, before the finalize
 // sets it.
+// HT: the frames come from Ht [D][Mp] (the transposed head input) instead of H [M][D].
+template <bool HT>
 __global__ void __launch_bounds__(512, 1)
-lse_partial_e_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t* __restrict__ W, int V, int P,
-                   int vper, float2* __restrict__ partials, uint16_t* __restrict__ E, int epitch, int eparts,
-                   int32_t* __restrict__ einv) {
-  using G = GMid;
+lse_partial_e_bf16(const uint16_t* __restrict__ H, const uint16_t* __restrict__ Ht, int Mp, int M, int D,
+                   const uint16_t* __restrict__ W, int V, int P, int vper, float2* __restrict__ partials,
+                   uint16_t* __restrict__ E, int epitch, int eparts, int32_t* __restrict__ einv) {
+  using G = std::conditional_t<HT, GMidT, GMid>;
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
   PCTC_STAGES_G(G)
@@ -308,7 +314,7 @@ lse_partial_e_bf16(const uint16_t* __restrict__ H, int M, int D, const uint16_t*
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int ntiles = (vend - vbeg + TR - 1) / TR;
   const GOp A{W, D, vend, D, nullptr};
-  const GOp B{H, D, M, D, nullptr};
+  const GOp B = HT ? GOp{Ht, Mp, M, D, nullptr} : GOp{H, D, M, D, nullptr};
   float run_max[FC], run_sum[FC];
 #pragma unroll
   for (int j = 0; j < FC; ++j) {
@@ -673,13 +679,16 @@ recompute_dz_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t*
 // (frames past M fall outside the resource, which drops them), so the copy pipeline can
 // count them and leave them in flight under the next tile's first products.
 
+// HT: the frames come from Hst [D][Mp] (Hs transposed) instead of Hs [M][D].
+template <bool HT>
 __global__ void __launch_bounds__(512, 1)
-recompute_run_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t* __restrict__ W, int c0, int cw,
-                   int run, const float2* __restrict__ lam2, const float* __restrict__ g, uint16_t* __restrict__ dZ,
-                   int chunk, const int32_t* __restrict__ only_if) {
+recompute_run_bf16(const uint16_t* __restrict__ Hs, const uint16_t* __restrict__ Hst, int Mp, int M, int D,
+                   const uint16_t* __restrict__ W, int c0, int cw, int run, const float2* __restrict__ lam2,
+                   const float* __restrict__ g, uint16_t* __restrict__ dZ, int chunk,
+                   const int32_t* __restrict__ only_if) {
   // only_if (the normaliser's E check flag): recompute only when its E cannot be used
   if (only_if && *only_if == 0) return;
-  using G = GMid;
+  using G = std::conditional_t<HT, GMidT, GMid>;
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
   PCTC_STAGES_G(G)
@@ -708,7 +717,7 @@ recompute_run_bf16(const uint16_t* __restrict__ Hs, int M, int D, const uint16_t
     sg[j] = (gm > 0.f) ? 0x80008000u : 0u;
   }
   const GOp A{W + static_cast<int64_t>(c0) * D, D, cw, D, nullptr};
-  const GOp B{Hs, D, M, D, nullptr};
+  const GOp B = HT ? GOp{Hst, Mp, M, D, nullptr} : GOp{Hs, D, M, D, nullptr};
   // store resource: this frame tile's rows of dZ (byte offsets < 256 rows x 2 chunk)
   const uint64_t zb = reinterpret_cast<uint64_t>(dZ + static_cast<int64_t>(m0) * chunk);
   const uint64_t zbu = (static_cast<uint64_t>(__builtin_amdgcn_readfirstlane(static_cast<uint32_t>(zb >> 32))) << 32) |
@@ -921,6 +930,41 @@ __global__ void hs_build_bf16(const uint16_t* __restrict__ H, int64_t n, int D, 
   u32x4 v = *reinterpret_cast<const u32x4*>(H + i);
   if (g[m] == 0.f) v = u32x4{0u, 0u, 0u, 0u};
   *reinterpret_cast<u32x4*>(Hs + i) = v;
+}
+
+// Ht[d][m] = H[m][d] for m < M (zero where g is given and g[m] == 0), zero for m in [M, Mp); with
+// Hs given, the same masked rows are also written there in H's layout (the hs_build_bf16 copy).
+// 64 frames x 64 columns per workgroup through LDS, 16 bytes per access both ways (D is a
+// multiple of 8, Mp of 64).
+__global__ void __launch_bounds__(256) ht_build_bf16(const uint16_t* __restrict__ H, int M, int D,
+                                                     const float* __restrict__ g, uint16_t* __restrict__ Hs,
+                                                     uint16_t* __restrict__ Ht, int Mp) {
+  __shared__ __attribute__((aligned(16))) uint16_t tile[64][72];  // rows 144 bytes apart
+  const int m0 = blockIdx.x * 64, d0 = blockIdx.y * 64;
+#pragma unroll
+  for (int q = threadIdx.x; q < 512; q += 256) {  // 64 frames x 8 runs of 8 columns
+    const int r = q >> 3, c = (q & 7) * 8;
+    const int m = m0 + r, d = d0 + c;
+    u32x4 v = u32x4{0u, 0u, 0u, 0u};
+    if (m < M && d < D) {
+      const int64_t i = static_cast<int64_t>(m) * D + d;
+      if (!(g && g[m] == 0.f)) v = *reinterpret_cast<const u32x4*>(H + i);
+      if (Hs) *reinterpret_cast<u32x4*>(Hs + i) = v;
+    }
+    *reinterpret_cast<u32x4*>(&tile[r][c]) = v;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int q = threadIdx.x; q < 512; q += 256) {  // 64 columns x 8 runs of 8 frames
+    const int r = q >> 3, c = (q & 7) * 8;
+    const int d = d0 + r;
+    if (d >= D) continue;
+    u32x4 o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      o[k] = static_cast<uint32_t>(tile[c + 2 * k][r]) | (static_cast<uint32_t>(tile[c + 2 * k + 1][r]) << 16);
+    *reinterpret_cast<u32x4*>(Ht + static_cast<int64_t>(d) * Mp + m0 + c) = o;
+  }
 }
 
 // Hp = s_m Hs (bf16) for the dW product of the chunk whose dZ rows hold the normaliser's
@@ -1239,7 +1283,8 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  int cw, const float2* lam2, const float* G, int ldG, const float* g,
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
-                                 float* dbpart, hipStream_t stream, const DwExtra* extra, const ChunkE* ce) {
+                                 float* dbpart, hipStream_t stream, const DwExtra* extra, const ChunkE* ce,
+                                 const uint16_t* Hst, int Mp) {
   // wide heads: one 8-wave 256 x 256 workgroup per CU (the long k loop hides the epilogue);
   // narrow heads: two 4-wave 256 x 128 workgroups per CU, so that one's epilogue (exp, pack,
   // staged stores: VALU-bound) overlaps the other's products
@@ -1271,8 +1316,12 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
       const int runs = max(1, min(nVt, kRcCus / nMt2));
       const int run = (nVt + runs - 1) / runs;
       const int nruns = (nVt + run - 1) / run;
-      hipLaunchKernelGGL(recompute_run_bf16, dim3(nMt2 * nruns), dim3(GMid::kThreads), 0, stream, Hs, M, D, W, c0,
-                         cw, run, lam2, g, dZ, chunk, ce ? ce->einv : nullptr);
+      if (Hst)
+        hipLaunchKernelGGL(recompute_run_bf16<true>, dim3(nMt2 * nruns), dim3(GMid::kThreads), 0, stream, Hs, Hst,
+                           Mp, M, D, W, c0, cw, run, lam2, g, dZ, chunk, ce ? ce->einv : nullptr);
+      else
+        hipLaunchKernelGGL(recompute_run_bf16<false>, dim3(nMt2 * nruns), dim3(GMid::kThreads), 0, stream, Hs, Hst,
+                           Mp, M, D, W, c0, cw, run, lam2, g, dZ, chunk, ce ? ce->einv : nullptr);
     } else {
       PCTC_RECOMPUTE_CFG(GFwd, 2)
     }
@@ -1328,12 +1377,25 @@ int lse_e_parts_bf16(int M, int D, int V, int chunk) {
 
 hipError_t launch_lse_partial_e_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
                                      int* P_out, uint16_t* E, int epitch, int eparts, int32_t* einv,
-                                     hipStream_t stream) {
+                                     hipStream_t stream, const uint16_t* Ht, int Mp) {
   const LseSplit sp = lse_split_bf16(M, D, V);
   *P_out = sp.P;
   Prof pr("lse_partial", stream);
-  hipLaunchKernelGGL(lse_partial_e_bf16, dim3(sp.nM * sp.P), dim3(GMid::kThreads), 0, stream, H, M, D, W, V, sp.P,
-                     sp.vper, partials, E, epitch, eparts, einv);
+  if (Ht)
+    hipLaunchKernelGGL(lse_partial_e_bf16<true>, dim3(sp.nM * sp.P), dim3(GMid::kThreads), 0, stream, H, Ht, Mp, M, D,
+                       W, V, sp.P, sp.vper, partials, E, epitch, eparts, einv);
+  else
+    hipLaunchKernelGGL(lse_partial_e_bf16<false>, dim3(sp.nM * sp.P), dim3(GMid::kThreads), 0, stream, H, Ht, Mp, M,
+                       D, W, V, sp.P, sp.vper, partials, E, epitch, eparts, einv);
+  return hipGetLastError();
+}
+
+hipError_t launch_ht_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, uint16_t* Ht, int Mp,
+                                hipStream_t stream) {
+  if (M <= 0) return hipSuccess;
+  Prof pr(Hs ? "hs_build" : "ht_build", stream);
+  hipLaunchKernelGGL(ht_build_bf16, dim3(static_cast<unsigned>(Mp / 64), static_cast<unsigned>((D + 63) / 64)),
+                     dim3(256), 0, stream, H, M, D, g, Hs, Ht, Mp);
   return hipGetLastError();
 }
 

@@ -122,6 +122,8 @@ struct Layout {
   // the per-frame factors and the scaled H of that chunk's dW product
   int eparts;
   size_t o_escale, o_hp;
+  // with E at a narrow head: H transposed [D][Mp] for the normaliser (0: none)
+  size_t o_ht = 0;
 };
 
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
@@ -206,6 +208,7 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
     e_bytes = align_up(static_cast<size_t>(L.M) * L.bwd.chunk * 2, 256);
     L.o_escale = take(static_cast<size_t>(L.M) * 4);
     L.o_hp = take(static_cast<size_t>(L.M) * D * 2);
+    if (L.bwd.hst_bytes > 0) L.o_ht = take(L.bwd.hst_bytes);  // same shape as the recompute's Hst
   }
   // The selected logits in double [M][ldS] (bf16 path) and the normaliser's partial pairs are
   // dead once lambda and S are formed, before the first recompute writes the gradient buffer:
@@ -458,11 +461,15 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // online full-vocabulary log-sum-exp, launched first: it is the longest step (the
     // second stream's wait on the work before it is enqueued after this launch)
     int P = 0;
-    if (use_e)  // also E = exp(z) for the backward's first chunk, into the gradient buffer
+    if (use_e) {  // also E = exp(z) for the backward's first chunk, into the gradient buffer
+      // narrow heads: the frames as H transposed (whole k-lines per copy)
+      uint16_t* Ht = L.o_ht ? reinterpret_cast<uint16_t*>(ws + L.o_ht) : nullptr;
+      if (Ht)
+        PCTC_HIP(launch_ht_build_bf16(static_cast<const uint16_t*>(H), L.M, D, nullptr, nullptr, Ht, L.bwd.Mp, stream));
       PCTC_HIP(launch_lse_partial_e_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), V,
                                          partials, &P, reinterpret_cast<uint16_t*>(bws), L.bwd.chunk, L.eparts, einv,
-                                         stream));
-    else
+                                         stream, Ht, L.bwd.Mp));
+    } else
       PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
@@ -472,8 +479,14 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     g_pred = reinterpret_cast<float*>(ws + L.o_gpred);
     int32_t* pred = reinterpret_cast<int32_t*>(ws + L.o_pred);
     PCTC_HIP(launch_g_forecast(L.dp, dps, y_rel, nullptr, utt_weight, g_pred, pred, dps_stream));
-    if (dH || dW)
-      PCTC_HIP(launch_hs_build_bf16(static_cast<const uint16_t*>(H), L.M, D, g_pred, bwd_hs(bws, L.bwd), dps_stream));
+    if (dH || dW) {
+      uint16_t* Hst = bwd_hst(bws, L.bwd);
+      if (Hst)
+        PCTC_HIP(launch_ht_build_bf16(static_cast<const uint16_t*>(H), L.M, D, g_pred, bwd_hs(bws, L.bwd), Hst,
+                                      L.bwd.Mp, dps_stream));
+      else
+        PCTC_HIP(launch_hs_build_bf16(static_cast<const uint16_t*>(H), L.M, D, g_pred, bwd_hs(bws, L.bwd), dps_stream));
+    }
     PCTC_HIP(launch_gather_s_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), bias,
                                   u_ids, Kdev, L.K_max, nullptr, nullptr, L.ldS, dps_stream, Zd));
     // the lattice's set-up (zeroing of G and g, per-utterance prep), which does not read S

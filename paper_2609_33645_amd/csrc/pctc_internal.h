@@ -89,7 +89,8 @@ struct BwdPlan {
   int chunk;       // vocabulary columns per step
   int splits;      // k-slices of the dH product per chunk
   int Mp;          // padded frame count (pitch of the transposed head input)
-  size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, total;
+  // hst_bytes: Hs transposed, [D][Mp] bf16, read by the dense recompute of narrow bf16 heads
+  size_t dz_bytes, ht_bytes, part_bytes, lam2_bytes, dbpart_bytes, hst_bytes, total;
 };
 BwdPlan plan_bwd(int dtype, int M, int D, int V, int chunk);
 // Column multiple of the default chunk of narrow bf16 heads: the normaliser's partition width
@@ -125,8 +126,10 @@ struct BwdSide {
   DwExtra udw;  // the union columns' dW_u, folded into the last chunk's dW launch (dH wanted)
   const struct ChunkE* ce = nullptr;  // the first chunk's dZ rows come from the normaliser
 };
-// the masked copy of H (rows of frames with g == 0 zeroed) inside the backward's scratch
+// the masked copy of H (rows of frames with g == 0 zeroed) inside the backward's scratch, and
+// its transpose [D][Mp] (null where the plan has none)
 uint16_t* bwd_hs(void* scratch, const BwdPlan& plan);
+uint16_t* bwd_hst(void* scratch, const BwdPlan& plan);
 // S/ldS: the forward's selected log-probabilities (the bf16 path writes the union columns
 // of each recomputed chunk from them).  remap == null (bf16 path): the dense part -g p only.
 hipError_t launch_head_bwd(int dtype, const void* H, int M, int D, const void* W, const float* bias, int V,
@@ -160,15 +163,16 @@ hipError_t launch_bwd_chunk_bf16(const uint16_t* Hs, int M, int D, const uint16_
                                  const int32_t* remap, const float* S, int ldS, uint16_t* dZ, int chunk, float* part,
                                  int slice, bool recompute, bool want_dH, bool want_dW, float* dW, float* db,
                                  float* dbpart, hipStream_t stream, const DwExtra* extra = nullptr,
-                                 const ChunkE* ce = nullptr);
+                                 const ChunkE* ce = nullptr, const uint16_t* Hst = nullptr, int Mp = 0);
 // Partitions of the normaliser that can write E for a first chunk of `chunk` columns (0: none;
 // narrow heads with D a multiple of 128, chunk a multiple of the partition width).
 int lse_e_parts_bf16(int M, int D, int V, int chunk);
 // The normaliser (no bias) that also writes E = exp(z) in bf16 at E[m * epitch + v] for the
-// rows of its first eparts partitions, and clears *einv (see launch_lse_finalize).
+// rows of its first eparts partitions, and clears *einv (see launch_lse_finalize).  With Ht
+// (H transposed, [D][Mp], from launch_ht_build_bf16) the frames are read from there.
 hipError_t launch_lse_partial_e_bf16(const uint16_t* H, int M, int D, const uint16_t* W, int V, float2* partials,
                                      int* P_out, uint16_t* E, int epitch, int eparts, int32_t* einv,
-                                     hipStream_t stream);
+                                     hipStream_t stream, const uint16_t* Ht = nullptr, int Mp = 0);
 // rowscale/Hp of ChunkE from the finalize's s_m (in rowscale) and its check flag.
 hipError_t launch_hs_scale_bf16(const uint16_t* Hs, int M, int D, const int32_t* einv, float* rowscale, uint16_t* Hp,
                                 hipStream_t stream);
@@ -194,6 +198,10 @@ hipError_t launch_union_dh_bf16(const uint16_t* Gb, const int32_t* Kdev, int K_m
 hipError_t launch_union_merge_bf16(const int32_t* Kdev, int K_max, const int32_t* u_ids, int M, int D, float* dW,
                                    float* db, void* scratch, hipStream_t stream);
 hipError_t launch_hs_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, hipStream_t stream);
+// Ht[d][m] = H[m][d] ([D][Mp], Mp a multiple of 64; frames with g[m] == 0 zeroed when g is
+// given; columns m >= M zero), and with Hs given the masked rows in H's layout as well.
+hipError_t launch_ht_build_bf16(const uint16_t* H, int M, int D, const float* g, uint16_t* Hs, uint16_t* Ht, int Mp,
+                                hipStream_t stream);
 
 // ---- grouped logits for a stock CTC (grouped_head.hip) ----------------------------------
 // small: device int32 [2] = {K, error flag}; remap[v] = j for v = u_ids[j], else -1.
