@@ -690,5 +690,106 @@ struct Gemm {
   }
 };
 
+// 8-wave 256 x 256 tile of C = A B^T for a k-contiguous A whose rows lie far apart (the dH
+// product's dZ rows) and a row-contiguous B, on the ping-pong schedule.  A is copied 64 deep, so
+// that every row piece is a whole 128-byte line (a 32-deep copy takes half lines, which cost
+// the cache about as much as whole ones): two 32 KB A super-stages (k-tiles 2j, 2j + 1); B 32
+// deep in four 16 KB stages.  Each super-stage is refilled in the memory phase of an even
+// k-tile, two k-tiles before it is read; B is copied three k-tiles ahead.  Every stage is an
+// LDS array of its own, so that the compiler can tell the stage being read from the ones being
+// filled (it waits for every copy in flight before a read it cannot tell apart from them).
+template <int WR, int WC>
+struct GemmA64 : Gemm<256, 256, 32, LL::KC, LL::MC, 4, WR, WC, true> {
+  using Base = Gemm<256, 256, 32, LL::KC, LL::MC, 4, WR, WC, true>;
+  using Frags = typename Base::Frags;
+  using CA = TileCopy<LL::KC, 256, 64, 8, true>;
+  using CB = typename Base::CB;
+  static constexpr int FR = Base::FR, FC = Base::FC, KK = Base::KK;
+  static constexpr int CPA = CA::kPerWave, CPB = CB::kPerWave;
+  static_assert(Base::NW == 8 && CA::kBytes == 32768 && CB::kBytes == 16384, "stage sizes");
+  static_assert(2 * CPB + CPA < 64, "vmcnt range");
+
+  // sl[0], sl[1]: A super-stages; sl[2..5]: B stages
+  template <int S>
+  __device__ static __forceinline__ void load_tile(char* const (&sl)[6], int wave, int lane, Frags (&f)[KK]) {
+    const int wr0 = (wave / WC) * (256 / WR), wc0 = (wave % WC) * (256 / WC);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+#pragma unroll
+      for (int i = 0; i < FR; ++i)
+        f[kk].a[i] = frag<LL::KC, 256, 64>(sl[S / 2], wr0 + 32 * i, (S % 2) * 32 + kk * 16, lane);
+#pragma unroll
+      for (int j = 0; j < FC; ++j) f[kk].b[j] = frag<LL::MC, 256, 32>(sl[2 + S], wc0 + 32 * j, kk * 16, lane);
+    }
+  }
+
+  template <int S, class IssueA, class IssueB>
+  __device__ static __forceinline__ void pp_tile(char* const (&sl)[6], int wave, int lane, f32x16 (&acc)[FR][FC],
+                                                 Frags (&f)[KK], IssueA&& issue_a, IssueB&& issue_b) {
+    // even k-tile t: the A super-stage of k-tiles t - 2, t - 1 takes k-tiles t + 2, t + 3
+    if constexpr (S % 2 == 0) issue_a(sl[(S / 2 + 1) % 2]);
+    issue_b(sl[2 + (S + 3) % 4]);  // k-tile t + 3 into the stage of t - 1
+    load_tile<S>(sl, wave, lane, f);
+    // the next k-tile's copies from this wave have landed: B's (issued three k-tiles back) and,
+    // after an odd k-tile, the A super-stage issued in the previous (even) k-tile, before that
+    // k-tile's B copy; what may still be in flight was issued after them
+    if constexpr (S % 2 == 0) wait_vmcnt<2 * CPB + CPA>();
+    else wait_vmcnt<2 * CPB>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    Base::phase_barrier();
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) Base::mma(f[kk], acc);
+    Base::phase_barrier();
+  }
+
+  // Same contract as Gemm::run (all 512 threads call; barriers inside), stages declared here.
+  template <bool ZERO = true>
+  __device__ static __forceinline__ void product(const GOp& A, const GOp& B, int row0, int col0, int kbeg, int kend,
+                                                 f32x16 (&acc)[FR][FC]) {
+    __shared__ __attribute__((aligned(1024))) char a0[32768], a1[32768];
+    __shared__ __attribute__((aligned(1024))) char b0[16384], b1[16384], b2[16384], b3[16384];
+    char* const sl[6] = {a0, a1, b0, b1, b2, b3};
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    if constexpr (ZERO) Base::zero(acc);
+    const int nk = (kend - kbeg + 31) / 32;
+    if (nk <= 0) return;
+    const int klimA = min(A.kmax, kend), klimB = min(B.kmax, kend);
+    CA ca;
+    CB cb;
+    ca.init(A, row0, wave, lane, kbeg, klimA);
+    cb.init(B, col0, wave, lane, kbeg, klimB);
+    int kna = kbeg, knb = kbeg;  // k of the next A super-tile and B tile to copy
+    auto issue_a = [&](char* stage) {
+      ca.issue(A, kna, klimA, stage, wave);
+      kna += 64;
+    };
+    auto issue_b = [&](char* stage) {
+      cb.issue(B, knb, klimB, stage, wave);
+      knb += 32;
+    };
+    __builtin_amdgcn_s_barrier();  // previous users of the stages are done
+    issue_a(sl[0]);
+#pragma unroll
+    for (int b = 0; b < 3; ++b) issue_b(sl[2 + b]);
+    wait_vmcnt<2 * CPB>();  // A super-tile 0 and B tile 0
+    __builtin_amdgcn_s_barrier();
+    const bool lag = wave >= 4;
+    if (lag) Base::phase_barrier();  // group 1 starts one phase behind
+    Frags f[KK];
+    const int nkp = (nk + 3) / 4 * 4;
+    for (int t = 0; t < nkp; t += 4) {
+      pp_tile<0>(sl, wave, lane, acc, f, issue_a, issue_b);
+      pp_tile<1>(sl, wave, lane, acc, f, issue_a, issue_b);
+      pp_tile<2>(sl, wave, lane, acc, f, issue_a, issue_b);
+      pp_tile<3>(sl, wave, lane, acc, f, issue_a, issue_b);
+    }
+    if (!lag) Base::phase_barrier();
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+  }
+};
+
 }  // namespace bf
 }  // namespace pctc

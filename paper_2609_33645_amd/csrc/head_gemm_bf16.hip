@@ -33,8 +33,9 @@ constexpr int kBK = 32;
 using GFwd = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3>;
 // the same tiles over gathered W rows (selected classes): flat per-lane addresses
 using GFwdGather = bf::Gemm<kFR, kFC, kFK, LL::KC, LL::KC, 3, 2, 2, false, false>;
-// 8 wavefronts (2 x 4), four stages of 256 x 32 + 256 x 32 (run on the ping-pong schedule)
-using GDh = bf::Gemm<kBR, kBC, kBK, LL::KC, LL::MC, 4, 2, 4, true>;
+// 8 wavefronts (2 x 4) on the ping-pong schedule; dZ copied 64 deep (whole 128-byte lines per
+// frame row), W 32 deep
+using GDh = bf::GemmA64<2, 4>;
 // logit products of wide heads (D >= kWideD: normaliser, argmax, recompute): the k loop is
 // long enough that the epilogue is a small share, so one 8-wave 256 x 256 workgroup per CU
 // beats two 4-wave ones
@@ -814,7 +815,6 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
   const bool first = c0 == 0 && !accumulate;
   if (kdev) cw = min(cw, 2 * *kdev);  // union columns: [hi | lo] of the K classes the device found
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
-  PCTC_STAGES_G(G)
   const int nMt = (M + TR - 1) / TR;
   const int nDt = (D + TC - 1) / TC;
   // Each XCD (a contiguous run of work ids) takes one block of a gm x (8 / gm) partition of
@@ -847,8 +847,12 @@ dh_gemm_bf16(const uint16_t* __restrict__ dZ, int M, int chunk, const uint16_t* 
       }
     }
   // 8-wave tiles on the ping-pong schedule (each SIMD's two waves alternate products and copies)
-  if constexpr (G::NW == 8) G::template run_pp<false>(A, B, m0, d0, kb, ke, st, acc);
-  else G::template run<false>(A, B, m0, d0, kb, ke, st, acc);
+  if constexpr (G::NW == 8) {
+    G::template product<false>(A, B, m0, d0, kb, ke, acc);
+  } else {
+    PCTC_STAGES_G(G)
+    G::template run<false>(A, B, m0, d0, kb, ke, st, acc);
+  }
 #pragma unroll
   for (int i = 0; i < FR; ++i)
 #pragma unroll
