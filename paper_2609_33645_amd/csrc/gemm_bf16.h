@@ -66,8 +66,12 @@ struct KC {
   static constexpr int kSlots = BK / 8;          // 16-byte slots per row
   static constexpr int kRowBytes = BK * 2;
   static constexpr int kRowsPerCopy = 64 / kSlots;
+  // A ds_read_b128 phase serves 16 lanes (16 rows) from 64 banks of 4 bytes: rows of 128 bytes
+  // (BK = 64) put even and odd rows in different halves of the banks, so the slot is XORed with
+  // (r >> 1) mod 8 (eight different slots among the even rows of a phase, eight among the odd);
+  // rows of 64 bytes (BK = 32) fill a 256-byte bank line four at a time.
   __device__ static __forceinline__ int swz(int r) {
-    if constexpr (BK == 64) return r & 7;
+    if constexpr (BK == 64) return (r >> 1) & 7;
     else return (r >> 2) & 3;
   }
 };
