@@ -304,6 +304,9 @@ struct Gemm {
   static constexpr int kABytes = BR * BK * 2;
   static constexpr int kBBytes = BC * BK * 2;
   static constexpr int kStageBytes = kABytes + kBBytes;
+  // bytes of each stage array a kernel declares for this engine (engines that declare their
+  // own stages set it to a stub)
+  static constexpr int kKernelStageBytes = kStageBytes;
   using CA = TileCopy<LA, BR, BK, NW, BUF>;
   using CB = TileCopy<LB, BC, BK, NW, BUF>;
   static constexpr int CPW = CA::kPerWave + CB::kPerWave;  // copies per wave per k-tile
@@ -789,6 +792,146 @@ struct GemmA64 : Gemm<256, 256, 32, LL::KC, LL::MC, 4, WR, WC, true> {
       pp_tile<3>(sl, wave, lane, acc, f, issue_a, issue_b);
     }
     if (!lag) Base::phase_barrier();
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+  }
+};
+
+// 8-wave 256 x 256 tile runs of C = A B^T with epilogues (the contract of
+// Gemm::run_seq_aligned, K a multiple of 128) for a k-contiguous A whose 64-byte row pieces
+// would be half cache lines (W rows of 1 KB and more) and a row-contiguous B, on the interleaved
+// schedule.  A is copied 64 deep, so that every row piece is a whole 128-byte line: two 32 KB A
+// super-stages (k-tiles 2j, 2j + 1) and four 16 KB B stages, each an LDS array of its own
+// (declared here; the compiler waits for every copy in flight before a read of an array it
+// cannot tell apart from one being filled).  After the barrier that ends k-tile t, B's stage of
+// t takes t + 4 and, for odd t, the A super-stage of t - 1, t takes t + 3, t + 4 (read two
+// k-tiles later); the copies of A (odd t) are issued before B's, and the prologue issues in the
+// same order (A0 B0 B1 B2 A1 B3), so every k-tile waits by the same count.
+template <int WR, int WC>
+struct GemmMidA64 : Gemm<256, 256, 32, LL::KC, LL::MC, 4, WR, WC, true> {
+  using Base = Gemm<256, 256, 32, LL::KC, LL::MC, 4, WR, WC, true>;
+  using Frags = typename Base::Frags;
+  using CA = TileCopy<LL::KC, 256, 64, 8, true>;
+  using CB = typename Base::CB;
+  static constexpr int FR = Base::FR, FC = Base::FC, KK = Base::KK, NM = Base::NM;
+  static constexpr int CPA = CA::kPerWave, CPB = CB::kPerWave;
+  static constexpr int kKernelStageBytes = 16;
+  static_assert(Base::NW == 8 && CA::kBytes == 32768 && CB::kBytes == 16384 && KK == 2, "layout");
+  static_assert(3 * CPB + CPA + 16 < 64, "vmcnt range");
+
+  // fragments of k-step kk of k-tile t (S = t mod 4)
+  template <int S>
+  __device__ static __forceinline__ void load(char* const (&sl)[6], int kk, int wave, int lane, Frags& f) {
+    const int wr0 = (wave / WC) * (256 / WR), wc0 = (wave % WC) * (256 / WC);
+#pragma unroll
+    for (int i = 0; i < FR; ++i) f.a[i] = frag<LL::KC, 256, 64>(sl[S / 2], wr0 + 32 * i, (S % 2) * 32 + kk * 16, lane);
+#pragma unroll
+    for (int j = 0; j < FC; ++j) f.b[j] = frag<LL::MC, 256, 32>(sl[2 + S], wc0 + 32 * j, kk * 16, lane);
+  }
+
+  // k-tile t (S = t mod 4); the fragments of its first k-step are in f0.  XTRA: as in
+  // Gemm::ktile (an epilogue's stores were issued after the copies this wait is for).
+  template <int S, int XTRA = 0, class IssueA, class IssueB>
+  __device__ static __forceinline__ void ktile(char* const (&sl)[6], int wave, int lane, f32x16 (&acc)[FR][FC],
+                                               Frags& f0, Frags& f1, IssueA&& issue_a, IssueB&& issue_b) {
+    constexpr int NH = NM / 2;
+    load<S>(sl, 1, wave, lane, f1);
+    Base::mma(f0, acc);
+    Base::template interleave<0>();
+    Base::template mma_range<0, NH>(f1, acc);
+    // k-tile t + 1 has landed: B's copy (issued after k-tile t - 3) and, for odd t, the A
+    // super-stage (issued after k-tile t - 2, before that k-tile's B copy)
+    if constexpr (S % 2 == 0) wait_vmcnt<2 * CPB + CPA + XTRA>();
+    else wait_vmcnt<2 * CPB + XTRA>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's reads of k-tile t are done
+    __builtin_amdgcn_s_barrier();
+    if constexpr (S % 2 == 1) issue_a(sl[S / 2]);  // the super-stage of t - 1, t
+    issue_b(sl[2 + S]);
+    load<(S + 1) % 4>(sl, 0, wave, lane, f0);
+    Base::template mma_range<NH, NM>(f1, acc);
+    Base::template interleave<(S % 2 == 1) ? CPA + CPB : CPB, NM - NH>();
+  }
+
+  // The stage arrays, one set per kernel (not per seq_aligned instantiation).
+  __device__ static __forceinline__ void stages(char* (&sl)[6]) {
+    __shared__ __attribute__((aligned(1024))) char a0[32768], a1[32768];
+    __shared__ __attribute__((aligned(1024))) char b0[16384], b1[16384], b2[16384], b3[16384];
+    sl[0] = a0;
+    sl[1] = a1;
+    sl[2] = b0;
+    sl[3] = b1;
+    sl[4] = b2;
+    sl[5] = b3;
+  }
+
+  template <int EXTRA, class Epi>
+  __device__ static __forceinline__ void seq_aligned(const GOp& A, const GOp& B, int row0, int col0, int ntiles,
+                                                     int K, f32x16 (&acc)[FR][FC], Epi&& epi) {
+    char* sl[6];
+    stages(sl);
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    Base::zero(acc);
+    const int nk = K / 32;  // the caller guarantees K % 128 == 0
+    if (nk <= 0 || ntiles <= 0) return;
+    const int klimA = min(A.kmax, K), klimB = min(B.kmax, K);
+    CA ca;
+    CB cb;
+    ca.init(A, row0, wave, lane, 0, klimA);
+    cb.init(B, col0, wave, lane, 0, klimB);
+    int atile = 0, ak = 0, btile = 0, bk = 0;  // copy stream positions (output tile, k)
+    auto issue_a = [&](char* stage) {
+      if (ak == K) {
+        ak = 0;
+        ++atile;
+        ca.retarget(A, row0 + atile * 256, wave, lane);
+      }
+      ca.issue(A, ak, atile < ntiles ? klimA : 0, stage, wave);
+      ak += 64;
+    };
+    auto issue_b = [&](char* stage) {
+      if (bk == K) {
+        bk = 0;
+        ++btile;
+      }
+      cb.issue(B, bk, btile < ntiles ? klimB : 0, stage, wave);
+      bk += 32;
+    };
+    __builtin_amdgcn_s_barrier();
+    issue_a(sl[0]);
+    issue_b(sl[2]);
+    issue_b(sl[3]);
+    issue_b(sl[4]);
+    issue_a(sl[1]);
+    issue_b(sl[5]);
+    wait_vmcnt<3 * CPB + CPA>();  // A super-tile 0 and B tile 0
+    __builtin_amdgcn_s_barrier();
+    Frags f0, f1;
+    load<0>(sl, 0, wave, lane, f0);
+    const int ng = nk / 4;
+    auto group = [&]() {
+      ktile<0>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<1>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<2>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<3>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+    };
+    auto relaxed_group = [&]() {
+      ktile<0, EXTRA>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<1, EXTRA>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<2, EXTRA>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+      ktile<3>(sl, wave, lane, acc, f0, f1, issue_a, issue_b);
+    };
+    group();
+    for (int gi = 1; gi < ng; ++gi) group();
+    epi(0, acc);
+    Base::zero(acc);
+    for (int t = 1; t < ntiles; ++t) {
+      relaxed_group();
+      for (int gi = 1; gi < ng; ++gi) group();
+      epi(t, acc);
+      Base::zero(acc);
+    }
     wait_vmcnt<0>();
     __builtin_amdgcn_s_waitcnt(0xC07F);
     __builtin_amdgcn_s_barrier();

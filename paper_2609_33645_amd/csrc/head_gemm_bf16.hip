@@ -44,10 +44,13 @@ using GWide = bf::Gemm<256, 256, 64, LL::KC, LL::KC, 2, 2, 4>;
 // stages, runs of kMidRun vocabulary tiles per workgroup (the copy pipeline runs through a
 // run, so one workgroup per CU still keeps the matrix pipe fed across tile boundaries)
 using GMid = bf::Gemm<256, 256, 32, LL::KC, LL::KC, 4, 2, 4, true>;
-// the same tiles with the frame operand read from the transposed head input Ht [D][Mp]: its
-// copies then take whole 512-byte k-lines instead of 64-byte row pieces (half cache lines),
-// a quarter fewer cache-line requests per k-tile
+// the same tiles with the frame operand read from the transposed head input Ht [D][Mp] (whole
+// 512-byte k-lines per copy instead of 64-byte row pieces, i.e. half cache lines): the
+// narrow-head dense recompute; the narrow-head normaliser also copies its W rows 64 deep (whole
+// 128-byte lines; 3-4% faster there, but 3-5% slower in the recompute, whose W rows come two
+// k-tiles ahead instead of three)
 using GMidT = bf::Gemm<256, 256, 32, LL::KC, LL::MC, 4, 2, 4, true>;
+using GMidTW = bf::GemmMidA64<2, 4>;
 constexpr int kMidRun = 8;
 constexpr int kRcCus = 224;  // workgroups of the dense recompute (one round)
 constexpr int kRcStores = 16;  // buffer stores per wave per 256 x 256 tile (recompute, E)
@@ -160,10 +163,10 @@ __device__ __forceinline__ void lse_tile_update(const f32x16 (&acc)[FR][FC], flo
 }  // namespace
 
 #define PCTC_STAGES_G(G)                                                                  \
-  __shared__ __attribute__((aligned(1024))) char st0_[G::kStageBytes];                      \
-  __shared__ __attribute__((aligned(1024))) char st1_[G::kStageBytes];                      \
-  __shared__ __attribute__((aligned(1024))) char st2_[G::kNS >= 3 ? G::kStageBytes : 16];   \
-  __shared__ __attribute__((aligned(1024))) char st3_[G::kNS >= 4 ? G::kStageBytes : 16];   \
+  __shared__ __attribute__((aligned(1024))) char st0_[G::kKernelStageBytes];                      \
+  __shared__ __attribute__((aligned(1024))) char st1_[G::kKernelStageBytes];                      \
+  __shared__ __attribute__((aligned(1024))) char st2_[G::kNS >= 3 ? G::kKernelStageBytes : 16];   \
+  __shared__ __attribute__((aligned(1024))) char st3_[G::kNS >= 4 ? G::kKernelStageBytes : 16];   \
   char* const stx_[4] = {st0_, st1_, st2_, st3_};                                           \
   char* const(&st)[G::kNS] = *reinterpret_cast<char* const(*)[G::kNS]>(&stx_);
 
@@ -297,7 +300,7 @@ __global__ void __launch_bounds__(512, 1)
 lse_partial_e_bf16(const uint16_t* __restrict__ H, const uint16_t* __restrict__ Ht, int Mp, int M, int D,
                    const uint16_t* __restrict__ W, int V, int P, int vper, float2* __restrict__ partials,
                    uint16_t* __restrict__ E, int epitch, int eparts, int32_t* __restrict__ einv) {
-  using G = std::conditional_t<HT, GMidT, GMid>;
+  using G = std::conditional_t<HT, GMidTW, GMid>;
   constexpr int FR = G::FR, FC = G::FC, TR = G::kBR, TC = G::kBC;
   static_assert(FR == 4 && FC == 2 && G::NW == 8 && TR == 256, "waves of 128 vocabulary rows x 64 frames");
   PCTC_STAGES_G(G)
@@ -329,7 +332,8 @@ lse_partial_e_bf16(const uint16_t* __restrict__ H, const uint16_t* __restrict__ 
       if (v0 + TR > vend) mask_rows_inf<FR, FC, G>(a, v0, vend, wave, lane);
       lse_tile_update<FR, FC, G>(a, run_max, run_sum);
     };
-    G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
+    if constexpr (HT) G::template seq_aligned<0>(A, B, vbeg, m0, ntiles, D, acc, epi);
+    else G::run_seq(A, B, vbeg, m0, ntiles, D, st, acc, epi);
   } else {
     const int wr = wave / (G::NW / 2), wc = wave % (G::NW / 2);
     const uint64_t zb = reinterpret_cast<uint64_t>(E + static_cast<int64_t>(m0) * epitch);
@@ -372,9 +376,10 @@ lse_partial_e_bf16(const uint16_t* __restrict__ H, const uint16_t* __restrict__ 
         if (h & 1) lse_e_update(a, j, s[j], run_max[j], run_sum[j]);  // column j's logits are done with
       }
     };
-    G::template run_seq_aligned<kRcStores>(A, B, vbeg, m0, ntiles, D, st, acc, epi);
+    if constexpr (HT) G::template seq_aligned<kRcStores>(A, B, vbeg, m0, ntiles, D, acc, epi);
+    else G::template run_seq_aligned<kRcStores>(A, B, vbeg, m0, ntiles, D, st, acc, epi);
   }
-  lse_store_partials<G>(run_max, run_sum, st0_, wave, lane, m0, M, partials + static_cast<int64_t>(p) * M);
+  lse_store_partials<G>(run_max, run_sum, stg_, wave, lane, m0, M, partials + static_cast<int64_t>(p) * M);
 }
 
 // ---------------------------------------------------------------------------------------
