@@ -122,7 +122,7 @@ struct Layout {
   // the per-frame factors and the scaled H of that chunk's dW product
   int eparts;
   size_t o_escale, o_hp;
-  // with E at a narrow head: H transposed [D][Mp] for the normaliser (0: none)
+  // with E: H transposed [D][Mp] for the normaliser (0: none)
   size_t o_ht = 0;
 };
 
@@ -208,7 +208,7 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
     e_bytes = align_up(static_cast<size_t>(L.M) * L.bwd.chunk * 2, 256);
     L.o_escale = take(static_cast<size_t>(L.M) * 4);
     L.o_hp = take(static_cast<size_t>(L.M) * D * 2);
-    if (L.bwd.hst_bytes > 0) L.o_ht = take(L.bwd.hst_bytes);  // same shape as the recompute's Hst
+    L.o_ht = take(align_up(static_cast<size_t>(D) * L.bwd.Mp * 2, 256));  // H^T [D][Mp] for the normaliser
   }
   // The selected logits in double [M][ldS] (bf16 path) and the normaliser's partial pairs are
   // dead once lambda and S are formed, before the first recompute writes the gradient buffer:
@@ -462,7 +462,7 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     // second stream's wait on the work before it is enqueued after this launch)
     int P = 0;
     if (use_e) {  // also E = exp(z) for the backward's first chunk, into the gradient buffer
-      // narrow heads: the frames as H transposed (whole k-lines per copy)
+      // the frames as H transposed (whole k-lines per copy)
       uint16_t* Ht = L.o_ht ? reinterpret_cast<uint16_t*>(ws + L.o_ht) : nullptr;
       if (Ht)
         PCTC_HIP(launch_ht_build_bf16(static_cast<const uint16_t*>(H), L.M, D, nullptr, nullptr, Ht, L.bwd.Mp, stream));
