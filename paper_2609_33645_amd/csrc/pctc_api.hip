@@ -223,6 +223,13 @@ static Layout make_layout(pctc_dtype dtype, int32_t N, const int32_t* T, const i
     }
   }
   L.o_part = (L.bwd.dz_bytes >= lent + part) ? L.o_bwd + lent : take(part);
+  if (part <= L.bwd.dz_bytes - std::min(L.bwd.dz_bytes, lent)) lent += align_up(part, 256);
+  // without E rows the normaliser's H^T also lives in the gradient buffer when it fits there
+  // (it is dead before the first recompute), so it costs no memory; otherwise it is not made
+  if (dtype == PCTC_BF16 && L.eparts == 0 && L.M > 0 && D % 128 == 0) {
+    const size_t ht = align_up(static_cast<size_t>(D) * L.bwd.Mp * 2, 256);
+    if (L.bwd.dz_bytes >= lent + ht) L.o_ht = L.o_bwd + lent;
+  }
   L.total = o;
   return L;
 }
@@ -469,8 +476,16 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
       PCTC_HIP(launch_lse_partial_e_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), V,
                                          partials, &P, reinterpret_cast<uint16_t*>(bws), L.bwd.chunk, L.eparts, einv,
                                          stream, Ht, L.bwd.Mp));
-    } else
+    } else if (dt == 1 && !bias && L.o_ht) {
+      // no E rows: the same kernel with none of its partitions writing them, frames from H^T
+      uint16_t* Ht = reinterpret_cast<uint16_t*>(ws + L.o_ht);
+      PCTC_HIP(launch_ht_build_bf16(static_cast<const uint16_t*>(H), L.M, D, nullptr, nullptr, Ht, L.bwd.Mp, stream));
+      PCTC_HIP(launch_lse_partial_e_bf16(static_cast<const uint16_t*>(H), L.M, D, static_cast<const uint16_t*>(W), V,
+                                         partials, &P, reinterpret_cast<uint16_t*>(bws), L.bwd.chunk, 0, einv, stream,
+                                         Ht, L.bwd.Mp));
+    } else {
       PCTC_HIP(launch_lse_partials(dt, H, L.M, D, W, bias, V, partials, &P, stream));
+    }
     PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.start, 0));
     // beside it: the lattice offsets, Algorithm 1 (union and relabel), the forecast of g and
     // the masked H of the dense part, then the selected logits X W_U^T (+ b_U)
