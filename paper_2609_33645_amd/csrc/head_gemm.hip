@@ -12,6 +12,8 @@
 //  * dh_gemm / dw_gemm: dH += dZ W_c and dW_c = dZ^T H (App. A, Step 3).
 //
 // Every product C[i][j] = sum_k A[i][k] B[j][k] goes through tile_gemm (pctc_device.h).
+#include <algorithm>
+
 #include "pctc_internal.h"
 
 namespace pctc {
@@ -889,9 +891,12 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
     const int cw = min(chunk, V - c0);
     const bool last = c0 + chunk >= V;
     const ChunkE* ce = (c0 == 0 && side) ? side->ce : nullptr;
+    // the first chunk (the widest) sets the slices; a narrower later chunk spreads its columns
+    // over as many slices (shorter ones), so that its dH launch keeps its workgroups
+    const int sl = (c0 == 0) ? slice : std::max(64, ((cw + nslices - 1) / nslices + 63) / 64 * 64);
     if (last && two && dH) {
       // the last chunk's dW product runs beside the final dH reduction (second stream)
-      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
                                 true, true, false, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
       if (e != hipSuccess) return e;
       if ((e = start_side(nwork)) != hipSuccess) return e;
@@ -909,12 +914,12 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
         // the union columns' dW_u rides in this launch's last round once their bf16 G is written
         const DwExtra* udw = side->udw.Z ? &side->udw : nullptr;
         if (udw && (e = hipStreamWaitEvent(stream, udw->ready, 0)) != hipSuccess) return e;
-        e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+        e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
                                   false, false, true, dW, db, dbpart, stream, udw, ce, Hst, plan.Mp);
         if (e != hipSuccess) return e;
       }
     } else {
-      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, slice,
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
                                 true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
       if (e != hipSuccess) return e;
       if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
