@@ -102,6 +102,8 @@ int32_t pctc_normaliser_chunk_columns(pctc_dtype dtype, int32_t N, const int32_t
  * H        [M, D] row-major, dtype; M = sum input_lengths.  D must be a multiple of 8 and at
  *          most PCTC_MAX_DIM.
  * W        [V, D] row-major, dtype (the head weight; a bias: pruned_ctc_fwd_bwd_ex).
+ *          H and W are read in 16-byte pieces: both pointers must be 16-byte aligned
+ *          (PCTC_EINVAL otherwise; every entry point below that takes H or W checks this).
  * targets  device int32 [sum target_lengths]: concatenated blank-free labels.
  * input_lengths, target_lengths: HOST int32 [N].
  * blank    the blank class id, 0 <= blank < V.  It becomes column 0 of the union.

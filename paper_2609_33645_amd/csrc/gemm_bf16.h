@@ -1,7 +1,7 @@
 // bf16 matrix-core tile engine for gfx950 with direct global->LDS staging.
 //
-// C[i][j] = sum_k A[i][k] B[j][k] over one BR x BC tile (4 wavefronts, 2 x 2; each owns
-// (BR/2) x (BC/2) = FR x FC blocks of 32x32 accumulated by v_mfma_f32_32x32x16_bf16).
+// C[i][j] = sum_k A[i][k] B[j][k] over one BR x BC tile (WR x WC wavefronts, 4 or 8; each owns
+// (BR/WR) x (BC/WC) = FR x FC blocks of 32x32 accumulated by v_mfma_f32_32x32x16_bf16).
 //
 // Operands are copied from global memory to LDS by buffer_load_dwordx4 ... lds (16 bytes per
 // lane, no register staging) in one of two LDS layouts, chosen to match global memory:
@@ -24,6 +24,11 @@
 // costs no vector arithmetic.  Row-gathered operands (GOp::rowidx) keep per-lane addresses
 // with a 16-byte zero page.  The k loop runs a multiple of NS tiles (the extra tiles are
 // zeros).
+// Schedules: Gemm::run / run_seq / run_seq_aligned interleave products and reads in every
+// wave (one barrier per k-tile); Gemm::run_pp (8 waves) alternates two groups of four waves
+// between a memory phase and a products-only phase.  GemmA64 (ping-pong) and GemmMidA64 (tile
+// runs with epilogues) copy a k-contiguous operand 64 deep, so that each of its row pieces is
+// a whole 128-byte line: a 64-byte piece costs the cache about as much as a whole line.
 #pragma once
 
 #include "pctc_device.h"

@@ -126,6 +126,10 @@ struct Layout {
   size_t o_ht = 0;
 };
 
+// The head input and weight are read in 16-byte pieces (their rows then are too: D is a
+// multiple of 8).
+static bool misaligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) != 0; }
+
 static int32_t check_args(pctc_dtype dtype, int32_t N, const int32_t* T, const int32_t* U, int32_t D, int32_t V,
                           float beam, int32_t chunk) {
   if (dtype != PCTC_F32 && dtype != PCTC_BF16) return PCTC_EINVAL;
@@ -679,7 +683,7 @@ int32_t pruned_ctc_fwd_bwd_ex(pctc_dtype dtype, const void* H, int32_t D, const 
                               float* db, void* workspace, size_t workspace_bytes, void* stream_ptr) {
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
-  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
+  if (blank < 0 || blank >= V || !loss || !W || misaligned16(W) || misaligned16(H)) return PCTC_EINVAL;
   const Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr);
   if (L.M > 0 && !H) return PCTC_EINVAL;
   if (L.Y > 0 && !targets) return PCTC_EINVAL;
@@ -699,7 +703,7 @@ int32_t pruned_ctc_fwd_bwd_noalloc(pctc_dtype dtype, const void* H, int32_t D, c
                                    float* dH, float* dW, float* db, void* stream_ptr) {
   int32_t st = check_args(dtype, N, input_lengths, target_lengths, D, V, beam, chunk);
   if (st != PCTC_OK) return st;
-  if (blank < 0 || blank >= V || !loss || !W) return PCTC_EINVAL;
+  if (blank < 0 || blank >= V || !loss || !W || misaligned16(W) || misaligned16(H)) return PCTC_EINVAL;
   Layout L = make_layout(dtype, N, input_lengths, target_lengths, D, V, beam, chunk, dW != nullptr, false);
   if (chunk == 0 && L.total > kNoAllocScratchBytes) {
     // the widest backward chunk (a multiple of 256 columns) whose layout fits the scratch;
@@ -751,7 +755,7 @@ int32_t pctc_lse_select(pctc_dtype dtype, const void* H, int32_t M, int32_t D, c
                         const int32_t* u_ids, const int32_t* K, int32_t K_max, double* lam, float* S, int32_t ldS,
                         void* partials, void* stream_ptr) {
   if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || K_max < 1 ||
-      ldS < K_max || !W || !lam || !partials || (M > 0 && !H))
+      ldS < K_max || !W || !lam || !partials || (M > 0 && !H) || misaligned16(W) || misaligned16(H))
     return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
@@ -814,7 +818,7 @@ int32_t pctc_greedy_decode(pctc_dtype dtype, const void* H, int32_t D, const voi
                            const int32_t* input_lengths, int32_t N, int32_t blank, int32_t* ids, int32_t* tokens,
                            int32_t* token_lengths, void* workspace, size_t workspace_bytes, void* stream_ptr) {
   if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || N < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || V > PCTC_MAX_VOCAB ||
-      blank < 0 || blank >= V || !W)
+      blank < 0 || blank >= V || !W || misaligned16(W) || misaligned16(H))
     return PCTC_EINVAL;
   if (N > 0 && !input_lengths) return PCTC_EINVAL;
   int64_t M64 = 0;
@@ -909,7 +913,7 @@ int32_t pctc_head_bwd(pctc_dtype dtype, const void* H, int32_t M, int32_t D, con
                       const double* lam, const float* G, int32_t ldG, const float* g, const int32_t* remap,
                       int32_t chunk, float* dH, float* dW, void* bwd_scratch, void* stream_ptr) {
   if ((dtype != PCTC_F32 && dtype != PCTC_BF16) || M < 0 || D <= 0 || D % 8 || D > PCTC_MAX_DIM || V <= 1 || chunk < 0 ||
-      (chunk > 0 && chunk % 256) || !W || !bwd_scratch || ldG < 1)
+      (chunk > 0 && chunk % 256) || !W || !bwd_scratch || ldG < 1 || misaligned16(W) || misaligned16(H))
     return PCTC_EINVAL;
   if (M > 0 && (!H || !lam || !G || !g || !remap)) return PCTC_EINVAL;
   hipStream_t stream = static_cast<hipStream_t>(stream_ptr);
@@ -985,7 +989,7 @@ size_t pctc_grouped_workspace_size(pctc_dtype dtype, int32_t M, int32_t D, int32
 int32_t pctc_grouped_logprobs(pctc_dtype dtype, const void* H, int32_t M, int32_t D, const void* W, const float* bias,
                               int32_t V, const int32_t* u_ids, int32_t K, float* logp, double* lam, void* workspace,
                               size_t workspace_bytes, void* stream_ptr) {
-  if (!grouped_args_ok(dtype, M, D, V, K, 0) || !W || !u_ids) return PCTC_EINVAL;
+  if (!grouped_args_ok(dtype, M, D, V, K, 0) || !W || !u_ids || misaligned16(W) || misaligned16(H)) return PCTC_EINVAL;
   if (M > 0 && (!H || !logp || !lam)) return PCTC_EINVAL;
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
   const GroupedLayout L = grouped_layout(dt, M, D, V, K, 0);
@@ -1021,7 +1025,8 @@ int32_t pctc_grouped_backward(pctc_dtype dtype, const void* H, int32_t M, int32_
                               int32_t V, const int32_t* u_ids, int32_t K, const float* logp, const double* lam,
                               const float* dlogp, int32_t chunk, float* dH, float* dW, float* db, void* workspace,
                               size_t workspace_bytes, void* stream_ptr) {
-  if (!grouped_args_ok(dtype, M, D, V, K, chunk) || !W || !u_ids) return PCTC_EINVAL;
+  if (!grouped_args_ok(dtype, M, D, V, K, chunk) || !W || !u_ids || misaligned16(W) || misaligned16(H))
+    return PCTC_EINVAL;
   if (M > 0 && (!H || !logp || !lam || !dlogp)) return PCTC_EINVAL;
   const int dt = (dtype == PCTC_BF16) ? 1 : 0;
   const GroupedLayout L = grouped_layout(dt, M, D, V, K, chunk);

@@ -174,3 +174,25 @@ def test_zero_frame_sizing():
     for D in (512, 4096):
         assert lib.pctc_lse_scratch_bytes(0, D) > 0
         assert lib.pctc_greedy_workspace_size(0, 0, D) > 0
+
+
+@pytest.mark.skipif(not os.path.exists(LIB), reason="library not built")
+def test_misaligned_head_pointers_rejected_on_host():
+    """H and W are read in 16-byte pieces: a pointer off that alignment is PCTC_EINVAL, returned
+    before any device work (the pointers here are never dereferenced)."""
+    import numpy as np
+    import torch  # noqa: F401
+    lib = ctypes.CDLL(LIB)
+    i32, f32, vp, sz = ctypes.c_int32, ctypes.c_float, ctypes.c_void_p, ctypes.c_size_t
+    i32p = ctypes.POINTER(ctypes.c_int32)
+    lib.pruned_ctc_fwd_bwd.restype = i32
+    lib.pruned_ctc_fwd_bwd.argtypes = [i32, vp, i32, vp, i32, vp, i32p, i32p, i32, i32, f32, i32, vp, vp, vp, vp, vp,
+                                       vp, sz, vp]
+    T = np.array([30, 20], np.int32)
+    U = np.array([5, 4], np.int32)
+    p = lambda a: a.ctypes.data_as(i32p)  # noqa: E731
+    ok, off = 0x7f0000000000, 0x7f0000000008  # aligned and 8-byte-offset stand-ins
+    for H, W in ((off, ok), (ok, off)):
+        rc = lib.pruned_ctc_fwd_bwd(1, H, 64, W, 100, ok, p(T), p(U), 2, 0, 16.0, 0, ok, None, None, None, None,
+                                    ok, 1 << 30, None)
+        assert rc == -1, (hex(H), hex(W), rc)
