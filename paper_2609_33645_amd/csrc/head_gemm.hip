@@ -886,6 +886,15 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
     }
     return hipSuccess;
   };
+  bool front_pending = two && side->front.fn;
+  auto start_front = [&]() -> hipError_t {
+    if (!front_pending) return hipSuccess;
+    front_pending = false;
+    hipError_t err;
+    if ((err = hipEventRecord(side->front_gate, stream)) != hipSuccess) return err;
+    if ((err = hipStreamWaitEvent(side->stream, side->front_gate, 0)) != hipSuccess) return err;
+    return side->front.fn(side->front.ctx);
+  };
   int ci = 0;  // chunk index
   for (int c0 = 0; c0 < V; c0 += chunk, ++ci) {
     const int cw = min(chunk, V - c0);
@@ -899,6 +908,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
                                 true, true, false, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
       if (e != hipSuccess) return e;
+      if ((e = start_front()) != hipSuccess) return e;
       if ((e = start_side(nwork)) != hipSuccess) return e;
       if ((e = hipEventRecord(side->dh_done, stream)) != hipSuccess) return e;
       if ((e = hipStreamWaitEvent(side->stream, side->dh_done, 0)) != hipSuccess) return e;
@@ -918,6 +928,16 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
                                   false, false, true, dW, db, dbpart, stream, udw, ce, Hst, plan.Mp);
         if (e != hipSuccess) return e;
       }
+    } else if (front_pending) {
+      // the first chunk: the second stream's front starts beside its dW product, not its dH
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
+                                true, dH != nullptr, false, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
+      if (e != hipSuccess) return e;
+      if ((e = start_front()) != hipSuccess) return e;
+      e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
+                                false, false, dW != nullptr, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
+      if (e != hipSuccess) return e;
+      if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
     } else {
       e = launch_bwd_chunk_bf16(Hs, M, D, W, bias, c0, cw, lam2, G, ldG, g, remap, S, ldS, dZ, chunk, part, sl,
                                 true, dH != nullptr, dW != nullptr, dW, db, dbpart, stream, nullptr, ce, Hst, plan.Mp);
@@ -925,6 +945,7 @@ static hipError_t head_bwd_bf16(const uint16_t* H, int M, int D, const uint16_t*
       if ((e = start_side(last ? nwork : ci + 1)) != hipSuccess) return e;
     }
   }
+  if ((e = start_front()) != hipSuccess) return e;
   if ((e = start_side(nwork)) != hipSuccess) return e;
   if (two) {
     // the second stream's work (its union-column part and, with dH, the reduction) is done

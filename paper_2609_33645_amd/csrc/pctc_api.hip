@@ -443,6 +443,12 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
   // the normaliser writes the first chunk's dZ rows as E = exp(z) (dense part only: no bias,
   // no db); einv: its range check, rowscale (escale) and Hp: that chunk's factors
   const bool use_e = overlap && L.eparts > 0 && !bias && !db && (dH || dW);
+  // a short lattice (every utterance at most kFrontDeferT frames) starts its front beside the
+  // first chunk's dW product, which it slows less than that chunk's dH; a longer one is on the
+  // critical path and starts as soon as S is formed
+  int t_max = 0;
+  for (int n = 0; n < N; ++n) t_max = std::max(t_max, input_lengths[n]);
+  const bool defer_front = overlap && t_max <= kFrontDeferT;
   int32_t* einv = Kdev + 3;
   float* escale = use_e ? reinterpret_cast<float*>(ws + L.o_escale) : nullptr;
   ChunkE chunk_e;
@@ -519,8 +525,10 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     if (use_e)
       PCTC_HIP(launch_hs_scale_bf16(bwd_hs(bws, L.bwd), L.M, D, einv, escale, reinterpret_cast<uint16_t*>(ws + L.o_hp),
                                     stream));
-    PCTC_HIP(hipEventRecord(ev.fork, stream));
-    PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
+    if (!defer_front) {
+      PCTC_HIP(hipEventRecord(ev.fork, stream));
+      PCTC_HIP(hipStreamWaitEvent(dps_stream, ev.fork, 0));
+    }
   } else {
     PCTC_HIP(upload_offsets(L.dp, dps, toff, yoff, soff, offsets_img, stream));
     // Algorithm 1: union and relabel
@@ -562,11 +570,19 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
         loss_per_utt, status, utt_status, G, g, dps, dps_stream,
         overlap ? reinterpret_cast<const int32_t*>(ws + L.o_pred) : nullptr, fflag, kDpAll};
   if (overlap) {
-    // the lattice's front (Viterbi pass and arc mask) now, beside the first recompute; its
-    // log-sum passes, occupancies and the loss after the dense part's first chunk, and the
-    // union columns' part after its second (see BwdSide)
-    PCTC_HIP(launch_ctc_dp(L.dp, input_lengths, target_lengths, S, L.ldS, y_rel, beam, utt_weight, loss_n, status,
-                           G, g, nullptr, dps, L.K_max, dps_stream, nullptr, kDpVit));
+    // the lattice's front (Viterbi passes and arc mask) now or, deferred, beside the first
+    // chunk's dW product; its log-sum passes, occupancies and the loss after the dense part's
+    // first chunk, and the union columns' part after its second (see BwdSide)
+    DpTail front = dpt;
+    front.phase = kDpVit;
+    struct FrontWork {
+      static hipError_t run(void* p) {
+        const DpTail& d = *static_cast<const DpTail*>(p);
+        return launch_ctc_dp(*d.dp, d.T, d.U, d.S, d.ldS, d.y_rel, d.beam, d.weight, d.loss_n, d.status, d.G, d.g,
+                             nullptr, d.dps, d.K_max, d.stream, nullptr, d.phase);
+      }
+    };
+    if (!defer_front) PCTC_HIP(FrontWork::run(&front));
     dpt.phase = kDpBack;
     // the union columns' part of the backward, from the lattice's G (its frames with g == 0
     // are those of the forecast unless the check fails, and then the backward is redone)
@@ -613,6 +629,10 @@ static int32_t fwd_bwd_run(pctc_dtype dtype, const void* H, int32_t D, const voi
     side.gate[1] = ev.gate1;
     side.dh_done = ev.dh_done;
     side.reduced = ev.join;
+    if (defer_front) {
+      side.front = SideWork{&FrontWork::run, &front};
+      side.front_gate = ev.fork;
+    }
     side.work[0] = SideWork{&DpTail::run, &dpt};
     side.work[1] = SideWork{&UnionWork::run, &uw};
     side.nwork = 2;

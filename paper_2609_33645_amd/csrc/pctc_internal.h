@@ -120,6 +120,10 @@ struct BwdSide {
   hipEvent_t dh_done = nullptr, reduced = nullptr;
   SideWork work[2];
   SideWork after_dh;
+  // enqueued on the second stream once the first chunk's dH product is (beside that chunk's dW),
+  // before the works; front_gate orders it after everything enqueued on the caller's stream
+  SideWork front;
+  hipEvent_t front_gate = nullptr;
   int nwork = 0;
   const float* dH_extra = nullptr;
   bool hs_built = false;
@@ -231,6 +235,9 @@ DpPlan plan_dp(int N, const int32_t* T, const int32_t* U, float beam);
 // then kDpBack (the log-sum passes and the occupancies, G and g) on the same stream; kDpFront
 // may itself be split into kDpPrep (the zeroing and prep, which do not read S) and kDpVit.
 constexpr int kDpAll = 0, kDpFront = 1, kDpBack = 2, kDpPrep = 3, kDpVit = 4;
+// Longest utterance (frames) whose lattice front the two-stream schedule starts beside the first
+// chunk's dW product rather than at once.
+constexpr int kFrontDeferT = 512;
 hipError_t launch_ctc_dp(const DpPlan& plan, const int32_t* T, const int32_t* U, const float* S, int ldS,
                          const int32_t* y_rel, float beam, const float* weight, double* loss_n, int32_t* status,
                          float* G, float* g, uint8_t* keep_mask_out, void* scratch, int K_max, hipStream_t stream,
