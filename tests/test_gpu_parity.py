@@ -432,6 +432,22 @@ def test_e2e_tight_alignment(beam):
     _check_e2e(wl, res, ref, fp32=False)
 
 
+@pytest.mark.parametrize("t_max", [512, 513])
+def test_e2e_lattice_front_schedules(t_max):
+    """The two-stream schedule starts the lattice's Viterbi front beside the first chunk's dW
+    product when no utterance is longer than 512 frames, and as soon as S is formed otherwise;
+    both orders give the oracle's loss and gradients (three backward chunks, so the gated
+    log-sum passes, the union part and the final reduction all run on the second stream)."""
+    rng = np.random.default_rng(512)
+    T = np.array([t_max, 301, 447], np.int32)
+    U = (T // 4).astype(np.int32)
+    wl = workloads.synthesize(name=f"front{t_max}", dtype="bf16", T=T, U=U, D=128, V=3001, rng=rng, beam=16.0)
+    say(f"e2e lattice front schedule T={T.tolist()} U={U.tolist()} V={wl.V} chunk=1024")
+    ref = oracle.fwd_bwd(wl.H, wl.W, wl.targets, wl.input_lengths, wl.target_lengths, wl.blank, wl.beam)
+    res = run_gpu(wl, chunk=1024)
+    _check_e2e(wl, res, ref, fp32=False)
+
+
 @pytest.mark.parametrize("nthreads", [2, 6])
 def test_concurrent_calls_on_streams(nthreads):
     """Host threads, each on its own stream with its own workspace and outputs, run the fused
